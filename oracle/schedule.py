@@ -1,0 +1,271 @@
+"""Checkpointing schedules: Revolve and asynchronous two-level (float-free).
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+Vocabulary (one action per line in the canonical text):
+  A t0 t1    advance the live state from x_t0 to x_t1 (t1 - t0 forward steps)
+  S k t      take a snapshot: copy the live state x_t into fast slot k
+  R k t      restore: the live state becomes x_t from fast slot k
+  F t        first turn: forward step t = n-1 (x_n, loss, seed), then its adjoint
+  Y t        adjoint of step t (needs the live state x_t and xbar_{t+1})
+  W k h t    store fast slot k (holding x_t) to slow slot h, asynchronously
+  P h k t    prefetch slow slot h (holding x_t) into fast slot k, asynchronously
+
+Counting (Revolve, Griewank and Walther; the paper's R(n, s), Section 3):
+  beta(s, r) = C(s + r, s).  With s slots (the one holding the interval's
+  first state included) and l >= 1 steps, let r be the integer with
+  beta(s, r-1) < l <= beta(s, r).  The least number of advanced steps needed
+  to run the l adjoint steps is  F(l, s) = r*l - beta(s+1, r-1).
+  Forward evaluations of a schedule = advanced steps + 1 (the first turn's
+  forward step); the recompute factor is forward evaluations / n, so storing
+  every state gives 1 (Section 1.1).
+
+Split rule (one optimal choice among many; the paper does not fix it):
+  reversing [a, a+l) with s >= 2 slots advances m steps, snapshots x_{a+m}
+  into the lowest free slot, reverses [a+m, a+l) with s-1 slots, releases the
+  slot, restores x_a and reverses [a, a+m) with s slots.  The optimal m form
+  the range [lo, hi] with
+      lo = max(1, l - beta(s-1, r), beta(s, r-2)),
+      hi = min(l-1, beta(s, r-1), l - beta(s-1, r-1));
+  this oracle takes m = hi.  With one slot the interval is reversed as a
+  chain (restore x_a and advance i steps, for i = l-1 .. 0).  A restore is
+  emitted only when the live state is not already x_a.
+
+Asynchronous two-level policy (Section 2, with the interval of Section 3):
+  interval I = max(I_min, 1, ceil(n / (H+1))) so that the K-1 stored states,
+  K = ceil(n / I), fit in H slow slots.  Fast slots 0 and 1 alternately hold
+  the interval starts (one being stored or prefetched while the other is in
+  use); Revolve inside an interval gets the other s-1 slots (the start's slot
+  included), i.e. working slots 2 .. s-1.
+    forward sweep, k = 0 .. K-2:   S (k%2) kI ; W (k%2) k kI ; A kI (k+1)I
+    reverse, k = K-1 .. 0, a = kI, l = n-a (last) or I, base = k%2:
+       k = K-1: S base a
+       k >= 1 : P (k-1) ((k-1)%2) (k-1)I        (prefetch one interval ahead)
+       reverse [a, a+l) with s-1 slots
+  Forward evaluations = (K-1) I + F(I_last, s-1) + 1 + (K-1) F(I, s-1).
+  When H = 0, s < 2, I >= n, or this is not strictly fewer than plain
+  Revolve needs with s slots, plain Revolve is used (the paper's fallback
+  when not even one store fits, Section 3, generalised), so the policy never
+  recomputes more than Revolve at the same fast-slot budget.
+
+Canonical text: a header line
+  ambptt-schedule v1 n=<n> s=<s> H=<H> I=<I or 0> mode=<revolve|async>
+then the actions, single spaces, decimal integers, newline-terminated.
+"""
+from __future__ import annotations
+
+from math import comb
+
+import numpy as np
+
+
+def beta(s: int, r: int) -> int:
+    if r < 0 or s < 0:
+        return 0
+    return comb(s + r, s)
+
+
+def revolve_r(l: int, s: int) -> int:
+    """Smallest r >= 0 with beta(s, r) >= l."""
+    r = 0
+    while beta(s, r) < l:
+        r += 1
+    return r
+
+
+def advances(l: int, s: int) -> int:
+    """F(l, s): least number of advanced steps to reverse l steps with s slots."""
+    if l < 1 or s < 1:
+        raise ValueError("need l >= 1 and s >= 1")
+    r = revolve_r(l, s)
+    return r * l - beta(s + 1, r - 1)
+
+
+def split_range(l: int, s: int) -> tuple[int, int]:
+    r = revolve_r(l, s)
+    lo = max(1, l - beta(s - 1, r), beta(s, r - 2))
+    hi = min(l - 1, beta(s, r - 1), l - beta(s - 1, r - 1))
+    return lo, hi
+
+
+def revolve_evals(n: int, s: int) -> int:
+    return advances(n, s) + 1
+
+
+def choose(n: int, s: int, H: int, I_min: int) -> tuple[str, int, int]:
+    """(mode, I, forward evaluations) under the policy above."""
+    plain = revolve_evals(n, s)
+    if H <= 0 or s < 2:
+        return "revolve", 0, plain
+    I = max(I_min, 1, -(-n // (H + 1)))
+    if I >= n:
+        return "revolve", 0, plain
+    K = -(-n // I)
+    last = n - (K - 1) * I
+    ev = (K - 1) * I + advances(last, s - 1) + 1 + (K - 1) * advances(I, s - 1)
+    if ev >= plain:
+        return "revolve", 0, plain
+    return "async", I, ev
+
+
+class _Gen:
+    def __init__(self, n: int):
+        self.n = n
+        self.out: list[tuple] = []
+        self.live = None
+
+    def emit(self, *a):
+        self.out.append(a)
+
+    def leaf(self, t):
+        self.emit("F" if t == self.n - 1 else "Y", t)
+
+    def restore(self, k, a):
+        if self.live != a:
+            self.emit("R", k, a)
+            self.live = a
+
+    def advance(self, t0, t1):
+        self.emit("A", t0, t1)
+        self.live = t1
+
+    def reverse(self, a: int, l: int, s: int, base: int, free: list[int]):
+        """Reverse [a, a+l) with s slots; x_a sits in slot `base`; `free` = free slot ids."""
+        while True:
+            if l == 1:
+                self.restore(base, a)
+                self.leaf(a)
+                return
+            if s == 1:
+                for i in range(l - 1, -1, -1):
+                    self.restore(base, a)
+                    if i > 0:
+                        self.advance(a, a + i)
+                    self.leaf(a + i)
+                return
+            m = split_range(l, s)[1]
+            self.restore(base, a)
+            self.advance(a, a + m)
+            k = min(free)
+            free.remove(k)
+            self.emit("S", k, a + m)
+            self.reverse(a + m, l - m, s - 1, k, free)
+            free.append(k)
+            l = m
+
+
+def schedule(n: int, s: int, H: int = 0, I_min: int = 0) -> tuple[dict, list[tuple]]:
+    """(header dict, action list) for n steps, s fast slots, H slow slots."""
+    if n < 1 or s < 1 or H < 0 or I_min < 0:
+        raise ValueError("need n >= 1, s >= 1, H >= 0, I_min >= 0")
+    mode, I, ev = choose(n, s, H, I_min)
+    g = _Gen(n)
+    if mode == "revolve":
+        g.emit("S", 0, 0)
+        g.live = 0
+        g.reverse(0, n, s, 0, list(range(1, s)))
+    else:
+        K = -(-n // I)
+        g.live = 0
+        for k in range(K - 1):
+            g.emit("S", k % 2, k * I)
+            g.emit("W", k % 2, k, k * I)
+            g.advance(k * I, (k + 1) * I)
+        for k in range(K - 1, -1, -1):
+            a = k * I
+            l = n - a if k == K - 1 else I
+            base = k % 2
+            if k == K - 1:
+                g.emit("S", base, a)
+            if k >= 1:
+                g.emit("P", k - 1, (k - 1) % 2, (k - 1) * I)
+            g.reverse(a, l, s - 1, base, list(range(2, s)))
+    head = {"n": n, "s": s, "H": H, "I": I, "mode": mode, "evals": ev}
+    return head, g.out
+
+
+def text(n: int, s: int, H: int = 0, I_min: int = 0) -> str:
+    head, acts = schedule(n, s, H, I_min)
+    lines = [f"ambptt-schedule v1 n={n} s={s} H={H} I={head['I']} mode={head['mode']}"]
+    lines += [" ".join(str(v) for v in a) for a in acts]
+    return "\n".join(lines) + "\n"
+
+
+# ---------------------------------------------------------------------------
+
+def check(n: int, s: int, H: int, acts: list[tuple]) -> dict:
+    """Symbolic execution: every action reads what it claims, adjoints run n-1..0 once.
+
+    Returns counters (forward evaluations, snapshots, ...) or raises AssertionError.
+    """
+    slot: dict[int, int] = {}
+    host: dict[int, int] = {}
+    live = 0
+    nxt = n - 1
+    c = dict(evals=0, advances=0, takeshots=0, restores=0, stores=0, prefetches=0, adjoints=0)
+    for a in acts:
+        op = a[0]
+        if op == "A":
+            t0, t1 = a[1], a[2]
+            assert live == t0 and t0 < t1 <= nxt, a
+            live = t1
+            c["advances"] += t1 - t0
+            c["evals"] += t1 - t0
+        elif op == "S":
+            k, t = a[1], a[2]
+            assert 0 <= k < s and live == t, a
+            slot[k] = t
+            c["takeshots"] += 1
+        elif op == "R":
+            k, t = a[1], a[2]
+            assert slot.get(k) == t, a
+            live = t
+            c["restores"] += 1
+        elif op in ("F", "Y"):
+            t = a[1]
+            assert t == nxt and live == t, a
+            assert (op == "F") == (t == n - 1), a
+            if op == "F":
+                c["evals"] += 1
+            nxt -= 1
+            c["adjoints"] += 1
+        elif op == "W":
+            k, h, t = a[1:]
+            assert 0 <= h < H and slot.get(k) == t, a
+            host[h] = t
+            c["stores"] += 1
+        elif op == "P":
+            h, k, t = a[1:]
+            assert 0 <= k < s and host.get(h) == t, a
+            slot[k] = t
+            c["prefetches"] += 1
+        else:
+            raise AssertionError(f"unknown action {a}")
+    assert nxt == -1, "not every adjoint step ran"
+    return c
+
+
+def replay(cell, n: int, u_of, x0: tuple, acts: list[tuple]) -> dict:
+    """Execute a schedule on the CPU with copies applied at once; returns like store_all."""
+    from .bptt import Reverse
+
+    slot: dict[int, tuple] = {}
+    host: dict[int, tuple] = {}
+    live = tuple(np.asarray(v, np.float64) for v in x0)
+    rev = Reverse(cell, n, u_of)
+    for a in acts:
+        op = a[0]
+        if op == "A":
+            for t in range(a[1], a[2]):
+                live = cell.step(t, live, u_of(t))
+        elif op == "S":
+            slot[a[1]] = tuple(v.copy() for v in live)
+        elif op == "R":
+            live = tuple(v.copy() for v in slot[a[1]])
+        elif op in ("F", "Y"):
+            rev.adjoint(a[1], live)
+        elif op == "W":
+            host[a[2]] = tuple(v.copy() for v in slot[a[1]])
+        elif op == "P":
+            slot[a[2]] = tuple(v.copy() for v in host[a[1]])
+    return rev.result()

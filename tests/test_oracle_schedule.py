@@ -1,0 +1,177 @@
+"""Pins for the oracle's checkpointing schedules (CPU only).
+
+The schedule oracle is pinned against things other than itself:
+  * a brute-force dynamic program over every split point (the recursive
+    structure of binomial checkpointing) for the least advanced-step count
+    and for the set of optimal splits;
+  * the textbook special cases: one slot costs l(l-1)/2 advanced steps, and
+    l <= s+1 steps cost l-1 (no recomputation, memory ratio 1, Section 1.1);
+  * hand-derived small schedules (tests/golden/schedules_small.txt);
+  * a symbolic execution of every generated schedule;
+  * the policy invariants of Sections 2-3: stream-all when I = 1, fallback
+    to Revolve when no store fits, never more recomputation than Revolve.
+"""
+import functools
+import os
+import random
+
+import pytest
+
+from oracle import schedule as S
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "schedules_small.txt")
+
+
+@functools.lru_cache(maxsize=None)
+def dp(l: int, s: int) -> int:
+    """Least advanced steps over every split point (brute force)."""
+    if l == 1:
+        return 0
+    if s == 1:
+        # chain: advance i steps from x_a for i = l-1 .. 1
+        return sum(range(1, l))
+    return min(m + dp(l - m, s - 1) + dp(m, s) for m in range(1, l))
+
+
+def dp_argmins(l: int, s: int) -> list[int]:
+    vals = [(m + dp(l - m, s - 1) + dp(m, s), m) for m in range(1, l)]
+    best = min(v for v, _ in vals)
+    return [m for v, m in vals if v == best]
+
+
+def test_closed_form_equals_dp():
+    for s in range(1, 11):
+        for l in range(1, 181):
+            assert S.advances(l, s) == dp(l, s), (l, s)
+
+
+def test_split_range_is_exactly_the_optimal_set():
+    for s in range(2, 8):
+        for l in range(2, 120):
+            lo, hi = S.split_range(l, s)
+            ms = dp_argmins(l, s)
+            assert ms == list(range(lo, hi + 1)), (l, s, lo, hi, ms)
+
+
+def test_textbook_special_cases():
+    for l in range(1, 60):
+        assert S.advances(l, 1) == l * (l - 1) // 2
+        for s in range(l - 1 if l > 1 else 1, l + 4):
+            if s >= 1:
+                assert S.advances(l, s) == l - 1, (l, s)
+
+
+def test_recompute_grows_with_n_and_shrinks_with_s():
+    # Section 3: the recompute factor increases with n and decreases with s.
+    for s in (2, 5, 20):
+        prev = 0.0
+        for n in (10, 100, 1000, 10000):
+            R = S.revolve_evals(n, s) / n
+            assert R >= prev and R >= 1.0
+            prev = R
+    for n in (100, 1000):
+        Rs = [S.revolve_evals(n, s) / n for s in range(1, 40)]
+        assert all(a >= b for a, b in zip(Rs, Rs[1:]))
+
+
+def _golden_cases():
+    cases, cur = [], None
+    for line in open(GOLDEN):
+        if line.startswith("#") or not line.strip():
+            continue
+        if line.startswith("case "):
+            cur = [tuple(int(v) for v in line.split()[1:]), ""]
+            cases.append(cur)
+        else:
+            cur[1] += line
+    return cases
+
+
+@pytest.mark.parametrize("case", _golden_cases(), ids=lambda c: "-".join(map(str, c[0])))
+def test_hand_derived_golden(case):
+    (n, s, H, I), want = case
+    assert S.text(n, s, H, I) == want
+
+
+def _grid():
+    rng = random.Random(1806)
+    out = []
+    for n in list(range(1, 40)) + [57, 100, 128, 257]:
+        for s in (1, 2, 3, 4, 7, 10):
+            for H in (0, 1, 3, 1000):
+                for I in (0, 1, 2, 3, 5, 8):
+                    out.append((n, s, H, I))
+    rng.shuffle(out)
+    return out[:2500]
+
+
+def test_generated_schedules_are_valid_and_counted():
+    for n, s, H, I in _grid():
+        head, acts = S.schedule(n, s, H, I)
+        c = S.check(n, s, H, acts)
+        assert c["evals"] == head["evals"], (n, s, H, I)
+        plain = S.revolve_evals(n, s)
+        if head["mode"] == "revolve":
+            assert c["evals"] == plain
+            assert c["stores"] == 0 and c["prefetches"] == 0
+        else:
+            assert c["evals"] < plain                # never worse than Revolve
+            K = -(-n // head["I"])
+            assert c["stores"] == K - 1 and c["prefetches"] == K - 1 <= H
+
+
+def test_stream_all_and_memory_ratio_one():
+    for n in (4, 5, 17, 100):
+        # T_T <= T_A: every state streamed out, no recomputation (Section 3)
+        # (from n = 4 on, two slots alone would need recomputation)
+        head, acts = S.schedule(n, 2, n, 1)
+        assert head["mode"] == "async" and head["I"] == 1
+        assert S.check(n, 2, n, acts)["evals"] == n
+        # enough fast slots for every state: recompute factor 1
+        for s in (n - 1, n, n + 3):
+            if s >= 1:
+                head, acts = S.schedule(n, s)
+                assert S.check(n, s, 0, acts)["evals"] == n
+
+
+def test_fallback_to_revolve():
+    # Section 3: if not even one store fits in the forward pass, plain Revolve.
+    assert S.schedule(10, 3, 100, 10)[0]["mode"] == "revolve"
+    assert S.schedule(10, 3, 100, 50)[0]["mode"] == "revolve"
+    assert S.schedule(10, 3, 0, 1)[0]["mode"] == "revolve"
+    assert S.schedule(10, 1, 100, 1)[0]["mode"] == "revolve"
+
+
+def test_bounded_slow_tier_sets_the_interval():
+    # K-1 stored states must fit in H slow slots
+    head, acts = S.schedule(1000, 10, 99, 1)
+    assert head["I"] == 10
+    assert S.check(1000, 10, 99, acts)["stores"] <= 99
+
+
+def test_interval_count_is_constant_in_n():
+    # Section 3: with a fixed interval the recompute factor stops growing with n.
+    Rs = [S.schedule(n, 8, n, 16)[0]["evals"] / n for n in (1000, 4000, 16000)]
+    assert max(Rs) - min(Rs) < 0.02          # ~2.43 at I = 16, s = 8
+    assert Rs[-1] < S.revolve_evals(16000, 8) / 16000
+
+
+def dp_table(N: int, smax: int):
+    """F[s][l] for l <= N, s <= smax by the same brute force, vectorised over m."""
+    import numpy as np
+    F = np.zeros((smax + 1, N + 1), np.int64)
+    l = np.arange(N + 1)
+    F[1] = l * (l - 1) // 2
+    for s in range(2, smax + 1):
+        for L in range(2, N + 1):
+            m = np.arange(1, L)
+            F[s, L] = np.min(m + F[s - 1, L - m] + F[s, m])
+    return F
+
+
+def test_workload_schedule_counts():
+    # Revolve counts at the workloads' (n, s): closed form vs brute force
+    F = dp_table(2000, 16)
+    for n, s in ((128, 4), (1000, 10), (2000, 16), (1777, 7)):
+        assert S.advances(n, s) == F[s, n]
+    assert S.revolve_evals(128, 4) == 517
