@@ -1,0 +1,174 @@
+#!/usr/bin/env python3
+"""Throughput of checkpointed BPTT on one MI355X.
+
+A step is one whole forward + reverse pass (ambptt_run) over the 1000-step
+LSTM workload (hidden 512, input 256, batch 64, fp32) with 10 HBM checkpoint
+slots and a pinned host tier, under the asynchronous two-level schedule whose
+interval comes from measured T_A and T_T.  Inputs are seeded, synthetic and
+resident in HBM before the timed region starts.
+
+Prints one JSON line: timesteps/s over the timed steps, the recompute factor,
+the same pass under plain Revolve at the same 10 slots, the roofline of the
+dominant kernel (sampled HIP-event durations on the compute stream), and the
+CPU oracle's rate on a bounded sample.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "BPTT timesteps/sec at fixed HBM slot budget; recompute factor; MFMA % of peak"
+WORKLOAD = "lstm_h512_t1000"
+FP32_MFMA_PEAK_TFLOPS = 157.3
+
+
+def step_flops(spec, window: int) -> dict:
+    """Algorithmic flops of one launch of each kernel."""
+    B, D, H, G = spec.batch, spec.input, spec.hidden, spec.gates
+    gate = 2.0 * B * G * H * (D + H)            # z = [x|h] W^T
+    hbar = 2.0 * B * H * G * H                  # hbar = zbar W_h
+    dw = 2.0 * G * H * (D + H + 1) * window * B  # dW (+ db) over one window
+    return {"fwd": gate, "adj": gate + hbar, "dw": dw}
+
+
+def cpu_baseline(wl, budget_s: float = 12.0) -> dict:
+    import numpy as np
+    import synth
+    from oracle import bptt
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    W, b = synth.params(wl)
+    cell = bptt.cell_for(wl, (W.astype(np.float64), b.astype(np.float64)))
+    x0 = synth.initial_state(wl)
+    st = (x0["h"].astype(np.float64), x0["c"].astype(np.float64))
+
+    def one(n):
+        w = wl.with_(n_steps=n)
+        xs = synth.x_slice(w, 0, n).astype(np.float64)
+        t = time.perf_counter()
+        bptt.store_all(cell, n, lambda i: xs[i], st)
+        return time.perf_counter() - t
+
+    probe = 16
+    dt = one(probe)
+    n = int(max(probe, min(wl.n_steps, budget_s * probe / max(dt, 1e-6))))
+    dt = one(n)
+    return {"value": n / dt, "unit": "timesteps/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"float64 store-all BPTT (numpy) over the first {n} of {wl.n_steps} steps "
+                      f"at the full shapes, {dt:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--timing-sample", type=int, default=8)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(--gpus must be 1)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_1806_01117_amd as amb
+    import synth
+
+    wl = synth.get(WORKLOAD)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    x = synth.x_slice(wl, 0, wl.n_steps)
+    W, b = synth.params(wl)
+    x0 = synth.initial_state(wl)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    dx, dW, db, dh, dc = t(x), t(W), t(b), t(x0["h"]), t(x0["c"])
+
+    spec = amb.ProblemSpec.from_workload(wl)
+    r = amb.Runner(spec, device=dev)
+    I_min, t_a, t_t = r.calibrate(dx, dW, db, dh, dc)
+    r.set("timing_sample", args.timing_sample)
+    for _ in range(args.warmup):
+        r.run(dx, dW, db, dh, dc)
+    torch.cuda.synchronize()
+    stats = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        out = r.run(dx, dW, db, dh, dc)
+        stats.append(out["stats"])
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    value = wl.n_steps * args.steps / el
+    st = stats[-1]
+
+    # plain Revolve at the same HBM slot budget (no host tier), for comparison
+    rv = amb.Runner(amb.ProblemSpec.from_workload(wl, slow_slots=0), device=dev)
+    rv.run(dx, dW, db, dh, dc)
+    torch.cuda.synchronize()
+    tr = time.perf_counter()
+    reps = max(1, min(3, args.steps))
+    for _ in range(reps):
+        rvo = rv.run(dx, dW, db, dh, dc)
+    torch.cuda.synchronize()
+    rv_value = wl.n_steps * reps / (time.perf_counter() - tr)
+    rv.close()
+
+    # roofline of the dominant kernel (largest device time in one pass)
+    fl = step_flops(spec, st["window"])
+    nwin = -(-wl.n_steps // st["window"])
+    avg = lambda k: float(np.mean([s[k] for s in stats if s[k] > 0])) if any(s[k] > 0 for s in stats) else 0.0
+    kern = {"fwd": (avg("fwd_kernel_us"), st["forward_evals"] - 1),
+            "adj": (avg("adj_kernel_us"), st["adjoints"]),
+            "dw": (avg("dw_kernel_us"), nwin)}
+    tot = {k: us * cnt for k, (us, cnt) in kern.items()}
+    dom = max(tot, key=tot.get)
+    dom_us = kern[dom][0]
+    achieved = fl[dom] / (dom_us * 1e-6) / 1e12 if dom_us > 0 else 0.0
+    names = {"fwd": "step_f32 forward (gate GEMM + LSTM cell)",
+             "adj": "step_f32 adjoint (gate recompute + h-adjoint GEMM + gate derivatives)",
+             "dw": "dw_f32 weight-gradient window"}
+    r.close()
+
+    line = {
+        "metric": METRIC, "value": round(value, 2), "unit": "timesteps/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(1000 * el / args.steps, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded normal inputs, uniform weights)",
+        "config": {"workload": WORKLOAD, "cell": "lstm", "batch": wl.batch, "input": wl.input,
+                   "hidden": wl.hidden, "n_steps": wl.n_steps, "fast_slots": wl.fast_slots,
+                   "slow_slots": spec.slow_slots, "mode": "async" if st["mode"] else "revolve",
+                   "interval": st["interval"], "interval_min": I_min, "t_a_us": round(t_a, 3),
+                   "t_t_us": round(t_t, 3), "window": st["window"]},
+        "recompute_factor": round(st["recompute_factor"], 4),
+        "plain_revolve": {"value": round(rv_value, 2), "unit": "timesteps/s",
+                          "recompute_factor": round(rvo["stats"]["recompute_factor"], 4)},
+        "kernel_us": {k: round(v[0], 3) for k, v in kern.items()},
+        "host_link": {"bytes_d2h": st["bytes_d2h"], "bytes_h2d": st["bytes_h2d"],
+                      "stores": st["stores"], "prefetches": st["prefetches"],
+                      "prefetches_elided": st["prefetches_elided"], "compute_waits": st["compute_waits"]},
+        "roofline": {"bound": "mfma", "kernel": names[dom], "achieved": round(achieved, 3),
+                     "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": None,
+                     "avg_launch_us": round(dom_us, 3), "flops_per_launch": fl[dom]},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,189 @@
+/*
+ * ambptt — backpropagation through time under asynchronous multistage
+ * checkpointing, on one AMD Instinct MI355X (gfx950).
+ *
+ * Kukreja, Hückelheim, Gorman, "Backpropagation for long sequences: beyond
+ * memory constraints with constant overheads" (arXiv 1806.01117).
+ *
+ * The library drives one whole forward + reverse pass over n recurrent steps
+ * (Section 4: the driver calls the forward and backward operators as the
+ * schedule directs).  Level 1 is a pool of s fast checkpoint slots in HBM;
+ * Level 2 is pinned host DRAM (Section 2: only the relative speed and size of
+ * the two levels matter).  Every I-th state is copied to Level 2 on a
+ * dedicated copy stream while the forward sweep continues, and is prefetched
+ * back one interval before the reverse sweep needs it; Revolve schedules the
+ * recomputation inside each interval (Section 2, Fig. 2).  The interval is
+ * I = ceil(T_T / T_A) (Section 3), raised if needed so the stored states fit
+ * the Level-2 budget; with no Level 2, or when the two-level schedule would
+ * not recompute strictly less, plain Revolve is used (Section 3, fallback).
+ *
+ * Conventions for every call below
+ *   - Device pointers are HIP device addresses; the caller owns all device
+ *     memory (inputs, parameters, gradients, the slot pool and the
+ *     workspace).  The library never allocates device memory.
+ *   - The library owns the pinned host tier (allocated with hipHostMalloc
+ *     when a schedule first needs it), one copy stream and its events.
+ *   - Every call returns a status; nothing throws across this boundary.  On
+ *     failure ambptt_last_error() returns a message for the calling thread.
+ *     After AMBPTT_EHIP the context must be destroyed.
+ *   - Row-major layouts.  Batch rows first: a state h is [B][H].
+ *   - Operand dtype (AMBPTT_F32 or AMBPTT_BF16) applies to x, W and the
+ *     stored hidden state h; biases, the LSTM cell state c, every gradient
+ *     and all accumulation are fp32.
+ */
+#ifndef AMBPTT_H
+#define AMBPTT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  AMBPTT_OK = 0,
+  AMBPTT_EINVAL = -1,       /* bad argument or size; nothing was enqueued */
+  AMBPTT_ENOMEM = -2,       /* pinned host allocation failed; nothing leaked */
+  AMBPTT_EHIP = -3,         /* a HIP runtime call failed; context unusable */
+  AMBPTT_EUNSUPPORTED = -4, /* valid but not implemented (e.g. a shape constraint) */
+  AMBPTT_EINTERNAL = -5     /* schedule / executor invariant broken */
+} ambptt_status;
+
+/* Recurrent cells: the per-step forward operator and its adjoint. */
+enum {
+  AMBPTT_CELL_TANH_RNN = 1, /* h' = tanh(W [x|h] + b), W[H][D+H] */
+  AMBPTT_CELL_LSTM = 2,     /* z = W [x|h] + b, W[4H][D+H], gate blocks i,f,g,o;
+                               c' = s(f) c + s(i) tanh(g); h' = s(o) tanh(c') */
+  AMBPTT_CELL_RESMLP = 3    /* depth as sequence: y' = y + relu(W_l y + b_l),
+                               W[L][w][w] (output x input), b[L][w]; D = 0 */
+};
+
+enum { AMBPTT_F32 = 0, AMBPTT_BF16 = 1 };
+
+enum {
+  AMBPTT_LOSS_HALF_SQ_LAST = 0, /* L = 1/2 sum(h_n^2) */
+  AMBPTT_LOSS_MEAN_SQ_ALL = 1,  /* L = sum_{t=1..n} mean(h_t^2) */
+  AMBPTT_LOSS_MEAN_LAST = 2     /* L = mean(h_n) */
+};
+
+/* The problem as the paper states it (Sections 3-4): n steps, the state
+ * described by the cell and its sizes, s fast slots, a slow-storage budget. */
+typedef struct {
+  int32_t cell;          /* AMBPTT_CELL_* */
+  int32_t dtype;         /* AMBPTT_F32 | AMBPTT_BF16 */
+  int32_t loss;          /* AMBPTT_LOSS_* */
+  int32_t batch;         /* B >= 1 */
+  int32_t input;         /* D >= 0, multiple of 16 (0 for RESMLP) */
+  int32_t hidden;        /* H (or MLP width) >= 16, multiple of 16 */
+  int64_t n_steps;       /* n >= 1 (layers L for RESMLP) */
+  int32_t fast_slots;    /* s >= 1 HBM checkpoint slots (the first state's included) */
+  int32_t interval_min;  /* I_min >= 1, or 0 to measure it (ambptt_calibrate) */
+  int64_t slow_slots;    /* host slots H >= 0; 0 = single-stage Revolve */
+} ambptt_problem;
+
+/* Counters of one ambptt_run.  recompute_factor = forward_evals / n, where a
+ * forward evaluation is one forward step (advances plus the first turn's). */
+typedef struct {
+  int32_t mode;            /* 0 = Revolve, 1 = asynchronous two-level */
+  int32_t interval;        /* I (0 in Revolve mode) */
+  int32_t window;          /* steps per dW accumulation window */
+  int32_t reserved0;
+  int64_t n_steps;
+  int64_t actions;
+  int64_t forward_evals;
+  int64_t adjoints;
+  int64_t takeshots, takeshot_copies, restores;
+  int64_t stores, prefetches, prefetches_elided;
+  int64_t bytes_d2h, bytes_h2d;
+  int64_t compute_waits;   /* compute-stream waits on the copy stream */
+  int64_t kernel_launches;
+  double recompute_factor;
+  double schedule_us;      /* host time to build the schedule */
+  double run_us;           /* host wall time of the forward + reverse pass */
+  /* average device time of sampled launches (0 if sampling is off) */
+  double fwd_kernel_us, adj_kernel_us, dw_kernel_us;
+  int64_t fwd_samples, adj_samples, dw_samples;
+} ambptt_stats;
+
+typedef struct ambptt_ctx ambptt_ctx;
+
+/* ---- pure host calls (no GPU needed) ------------------------------------ */
+
+const char* ambptt_version(void);
+
+/* Least number of advanced steps that reverses n steps with s slots
+ * (binomial checkpointing of Griewank and Walther, behind the paper's
+ * R(n, s) in Section 3): F(n, s) = r n - C(s + r, s + 1), where r is the
+ * integer with C(s + r - 1, s) < n <= C(s + r, s).  Plain Revolve then runs
+ * F(n, s) + 1 forward steps.  Returns < 0 on bad arguments. */
+int64_t ambptt_revolve_advances(int64_t n, int32_t s);
+
+/* Forward evaluations of the schedule the library would run for (n, s, H,
+ * I_min); writes the chosen interval (0 = Revolve) and mode (0/1) when the
+ * pointers are non-NULL.  Returns < 0 on bad arguments. */
+int64_t ambptt_schedule_evals(int64_t n, int32_t s, int64_t H, int32_t interval_min,
+                              int32_t* interval_out, int32_t* mode_out);
+
+/* Canonical text of that schedule: a header line
+ *   "ambptt-schedule v1 n=<n> s=<s> H=<H> I=<I|0> mode=<revolve|async>"
+ * then one action per line: "A t0 t1" advance, "S k t" snapshot to slot k,
+ * "R k t" restore from slot k, "F t" first turn, "Y t" adjoint step,
+ * "W k h t" store slot k to host slot h, "P h k t" prefetch host h to slot k.
+ * Writes at most cap bytes (NUL-terminated when it fits) and sets *needed to
+ * the full length + 1.  EINVAL if cap is too small (buf untouched). */
+ambptt_status ambptt_schedule_text(int64_t n, int32_t s, int64_t H, int32_t interval_min,
+                                   char* buf, size_t cap, size_t* needed);
+
+/* Sizes the caller allocates: bytes of one state (padded slot stride), of the
+ * slot pool (fast_slots * stride) and of the workspace. */
+ambptt_status ambptt_query(const ambptt_problem* p, size_t* state_bytes,
+                           size_t* slot_pool_bytes, size_t* workspace_bytes);
+
+const char* ambptt_last_error(void);
+
+/* ---- GPU calls ----------------------------------------------------------- */
+
+/* Validates p, creates the copy stream and events on the current device.
+ * stream is the compute stream (hipStream_t; NULL = the null stream). */
+ambptt_status ambptt_create(const ambptt_problem* p, void* stream, ambptt_ctx** out);
+
+/* Binds caller-owned device memory: the slot pool and the workspace, at
+ * least the sizes ambptt_query reports, 256-byte aligned. */
+ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
+                          void* workspace, size_t workspace_bytes);
+
+/* Sets a tuning / debug knob.  Keys: "timing_sample" (time every k-th
+ * kernel launch with events, 0 = off), "elide_prefetch" (0/1, default 1),
+ * "window" (dW window steps, 0 = automatic).  EINVAL for unknown keys. */
+ambptt_status ambptt_set_int(ambptt_ctx* ctx, const char* key, int64_t value);
+
+/* Measures T_A (one forward step) and T_T (one state over the host link,
+ * the slower direction) and sets the context's I_min = ceil(T_T / T_A)
+ * (Section 3).  Uses the same inputs as ambptt_run; writes nothing the
+ * caller owns.  Any out pointer may be NULL. */
+ambptt_status ambptt_calibrate(ambptt_ctx* ctx, const void* x_seq, const void* W,
+                               const float* b, const void* h0, const float* c0,
+                               int32_t* interval_min_out, double* t_a_us, double* t_t_us);
+
+/* One forward + reverse pass (blocks until the compute stream is done).
+ *   x_seq  [n][B][D] operand dtype (NULL for RESMLP)
+ *   W      TANH_RNN/LSTM: [G*H][D+H]; RESMLP: [L][w][w]; operand dtype
+ *   b      fp32 [G*H] (RESMLP: [L][w])
+ *   h0     [B][H] operand dtype; c0 fp32 [B][H] for LSTM, else NULL
+ *   dW, db fp32, same layouts as W, b (overwritten)
+ *   dh0    fp32 [B][H]; dc0 fp32 [B][H] for LSTM, else NULL
+ *   loss   host double (may be NULL); stats host (may be NULL)
+ * The inputs must not be written while the call runs. */
+ambptt_status ambptt_run(ambptt_ctx* ctx, const void* x_seq, const void* W, const float* b,
+                         const void* h0, const float* c0, float* dW, float* db,
+                         float* dh0, float* dc0, double* loss, ambptt_stats* stats);
+
+/* Frees the host tier, the copy stream and events.  NULL-safe. */
+void ambptt_destroy(ambptt_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AMBPTT_H */

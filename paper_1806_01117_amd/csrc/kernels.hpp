@@ -1,0 +1,64 @@
+// Device kernels of one recurrent step and of the weight-gradient windows,
+// with their host launchers.  Host code includes this header; the kernels
+// live in the .hip files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace ambptt {
+
+// Arguments of one step kernel (fp32 operands).  G = 1 (tanh RNN) or 4
+// (LSTM, gate blocks i, f, g, o).  Layouts are row-major with batch rows.
+struct StepArgs {
+  const float* x;        // x_t [B][D]
+  const float* h;        // h_t [B][H]
+  const float* c;        // c_t [B][H] (LSTM)
+  float* h_out;          // forward: h_{t+1} [B][H]
+  float* c_out;          // forward: c_{t+1} [B][H] (LSTM)
+  const float* W;        // [G*H][D+H]
+  const float* bias;     // [G*H]
+  const float* WhT;      // [H][G*H]: WhT[j][k] = W[k][D+j]
+  const float* zbar_in;  // adjoint: zbar_{t+1} [B][G*H] (unused when first)
+  const float* cbar_in;  // adjoint: cbar_{t+1} [B][H] (LSTM; unused when first)
+  float* zbar_out;       // adjoint: zbar_t [B][G*H]
+  float* cbar_out;       // adjoint: cbar_t [B][H] (LSTM)
+  float* hwin_out;       // adjoint: copy of h_t for the weight-gradient window
+  double* loss_acc;      // adjoint: one accumulator per workgroup
+  float* dh0;            // final: dL/dh_0 [B][H]
+  float* dc0;            // final: dL/dc_0 [B][H] (LSTM)
+  int B, D, H;
+  int loss;              // AMBPTT_LOSS_*
+  int first;             // adjoint of step n-1: no incoming adjoint
+  int last;              // the step's output is x_n
+  float inv_bh;          // 1 / (B H)
+};
+
+// Weight-gradient window: dW[k][c] += sum_r Z[r][k] X[r][c], db[k] += sum_r Z[r][k],
+// where X[r] = [x row | h row] for the R = w*B rows of w consecutive steps.
+struct DwArgs {
+  const float* zbar;  // [R][G*H]
+  const float* x;     // [R][D]
+  const float* hwin;  // [R][H]
+  float* dW;          // [G*H][D+H]
+  float* db;          // [G*H]
+  int R, D, H, GH;
+};
+
+enum StepMode { kForward = 0, kAdjoint = 1, kFinal = 2 };
+
+struct StepCfg {
+  int rm, rj, ks;  // 16x16 tiles per wave in m and j; waves splitting K
+};
+
+StepCfg pick_step_cfg(int G, int B, int D, int H);
+void step_grid(const StepCfg& cfg, int B, int H, dim3* grid, dim3* block);
+hipError_t launch_step(int G, int mode, const StepCfg& cfg, const StepArgs& a, hipStream_t s);
+hipError_t launch_dw(const DwArgs& a, hipStream_t s);
+hipError_t launch_transpose_wh(const float* W, float* WhT, int GH, int D, int H, hipStream_t s);
+hipError_t launch_fill32(void* p, size_t words, uint32_t value, hipStream_t s);
+hipError_t launch_loss_sum(const double* acc, int n, double scale, double* out, hipStream_t s);
+
+}  // namespace ambptt

@@ -1,0 +1,701 @@
+// C-ABI runtime: context, checkpoint tiers, executor and calibration.
+//
+// Level 1 is the caller's HBM slot pool (s slots); Level 2 is pinned host
+// memory owned here (Section 2).  The executor walks the action list on the
+// host and enqueues:
+//   - step kernels and state copies on the caller's compute stream,
+//   - stores (slot -> host) and prefetches (host -> slot) on one copy stream,
+// with event edges that keep the two streams race-free:
+//   1. a store of slot k waits for the compute work that wrote slot k;
+//   2. a later write of slot k by compute waits for that store to finish;
+//   3. a prefetch into slot k waits for compute's earlier readers of slot k;
+//   4. compute reads slot k only after the prefetch into it finished;
+//   5. a prefetch of host slot h follows the store that filled it because one
+//      in-order copy stream carries both directions.
+// The copy stream never blocks the compute stream except through edges 2 and
+// 4, which the interval rule I = ceil(T_T / T_A) (Section 3) is meant to keep
+// already satisfied by the time they are reached.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <stdexcept>
+#include <string>
+#include <vector>
+
+#include "ambptt.h"
+#include "kernels.hpp"
+#include "schedule.hpp"
+
+using namespace ambptt;
+
+namespace {
+
+thread_local std::string g_err;
+
+ambptt_status fail(ambptt_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+#define HIPCK(expr)                                                                      \
+  do {                                                                                   \
+    hipError_t e_ = (expr);                                                              \
+    if (e_ != hipSuccess) return fail(AMBPTT_EHIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+double now_us() {
+  using namespace std::chrono;
+  return duration<double, std::micro>(steady_clock::now().time_since_epoch()).count();
+}
+
+struct Layout {
+  int G = 1, dsize = 4, window = 1;
+  size_t h_bytes = 0, c_bytes = 0, state_bytes = 0, stride = 0;
+  size_t off_live[2] = {0, 0}, off_wht = 0, off_zbar = 0, off_hwin = 0, off_cbar[2] = {0, 0};
+  size_t off_loss = 0, off_lossout = 0, total = 0;
+  int loss_slots = 0;
+  StepCfg cfg{1, 1, 1};
+};
+
+ambptt_status validate(const ambptt_problem* p) {
+  if (!p) return fail(AMBPTT_EINVAL, "problem is NULL");
+  if (p->cell != AMBPTT_CELL_TANH_RNN && p->cell != AMBPTT_CELL_LSTM && p->cell != AMBPTT_CELL_RESMLP)
+    return fail(AMBPTT_EINVAL, "unknown cell");
+  if (p->dtype != AMBPTT_F32 && p->dtype != AMBPTT_BF16) return fail(AMBPTT_EINVAL, "unknown dtype");
+  if (p->loss < AMBPTT_LOSS_HALF_SQ_LAST || p->loss > AMBPTT_LOSS_MEAN_LAST) return fail(AMBPTT_EINVAL, "unknown loss");
+  if (p->batch < 1 || p->hidden < 1 || p->input < 0) return fail(AMBPTT_EINVAL, "sizes must be positive");
+  if (p->n_steps < 1) return fail(AMBPTT_EINVAL, "n_steps must be >= 1");
+  if (p->fast_slots < 1) return fail(AMBPTT_EINVAL, "fast_slots must be >= 1");
+  if (p->slow_slots < 0) return fail(AMBPTT_EINVAL, "slow_slots must be >= 0");
+  if (p->interval_min < 0) return fail(AMBPTT_EINVAL, "interval_min must be >= 0");
+  if (p->hidden % 16 || p->input % 16)
+    return fail(AMBPTT_EUNSUPPORTED, "hidden and input sizes must be multiples of 16");
+  if (p->cell == AMBPTT_CELL_RESMLP) return fail(AMBPTT_EUNSUPPORTED, "residual MLP cell not built yet");
+  if (p->dtype == AMBPTT_BF16) return fail(AMBPTT_EUNSUPPORTED, "bf16 operands not built yet");
+  if ((int64_t)p->batch * p->hidden > (int64_t(1) << 31)) return fail(AMBPTT_EUNSUPPORTED, "state too large");
+  return AMBPTT_OK;
+}
+
+int auto_window(int B) {
+  int w = (1024 + B - 1) / B;
+  return std::max(1, std::min(64, w));
+}
+
+Layout make_layout(const ambptt_problem* p, int window) {
+  Layout L;
+  L.G = p->cell == AMBPTT_CELL_LSTM ? 4 : 1;
+  L.dsize = p->dtype == AMBPTT_BF16 ? 2 : 4;
+  L.window = window > 0 ? window : auto_window(p->batch);
+  const size_t BH = (size_t)p->batch * p->hidden;
+  const size_t GH = (size_t)L.G * p->hidden;
+  L.h_bytes = BH * L.dsize;
+  L.c_bytes = p->cell == AMBPTT_CELL_LSTM ? BH * 4 : 0;
+  L.state_bytes = align_up(L.h_bytes) + L.c_bytes;
+  L.stride = align_up(L.state_bytes);
+  L.cfg = pick_step_cfg(L.G, p->batch, p->input, p->hidden);
+  dim3 grid, block;
+  step_grid(L.cfg, p->batch, p->hidden, &grid, &block);
+  L.loss_slots = int(grid.x * grid.y);
+  size_t o = 0;
+  L.off_live[0] = o; o += L.stride;
+  L.off_live[1] = o; o += L.stride;
+  L.off_wht = o; o += align_up((size_t)p->hidden * GH * L.dsize);
+  L.off_zbar = o; o += align_up(2 * (size_t)L.window * p->batch * GH * 4);
+  L.off_hwin = o; o += align_up(2 * (size_t)L.window * BH * 4);
+  L.off_cbar[0] = o; o += align_up(BH * 4);
+  L.off_cbar[1] = o; o += align_up(BH * 4);
+  L.off_loss = o; o += align_up((size_t)L.loss_slots * 8);
+  L.off_lossout = o; o += kAlign;
+  L.total = o;
+  return L;
+}
+
+}  // namespace
+
+struct ambptt_ctx {
+  ambptt_problem p{};
+  Layout L;
+  int device = 0;
+  hipStream_t cs = nullptr;  // compute (caller's)
+  hipStream_t xs = nullptr;  // copy stream (owned)
+  char* pool = nullptr;
+  char* ws = nullptr;
+  char* host = nullptr;
+  size_t host_bytes = 0;
+  double* host_loss = nullptr;  // pinned scalar
+  std::vector<hipEvent_t> ev_slot;
+  std::vector<int> pend;  // 0 none, 1 store in flight, 2 prefetch in flight
+  hipEvent_t ev_c = nullptr;
+  int64_t interval_min = 0;
+  int64_t timing_sample = 0;
+  bool elide_prefetch = true;
+  int window_opt = 0;
+};
+
+namespace {
+
+enum { kNone = 0, kStorePending = 1, kPrefetchPending = 2 };
+
+struct Sample {
+  int cls;
+  hipEvent_t a, b;
+};
+
+struct Exec {
+  ambptt_ctx* C;
+  const Layout& L;
+  const ambptt_problem& p;
+  const float* x;
+  const float* W;
+  const float* b;
+  float* WhT;
+  ambptt_stats st{};
+  char* cur = nullptr;
+  int cur_slot = -1;  // slot index the live state aliases, or -1
+  int cur_live = -1;  // live buffer index, or -1
+  std::vector<int64_t> slot_t;
+  int64_t launches[3] = {0, 0, 0};
+  std::vector<Sample> samples;
+
+  Exec(ambptt_ctx* c, const float* x_, const float* W_, const float* b_)
+      : C(c), L(c->L), p(c->p), x(x_), W(W_), b(b_), slot_t(size_t(c->p.fast_slots), -1) {
+    WhT = (float*)(C->ws + L.off_wht);
+  }
+
+  char* slot(int64_t k) const { return C->pool + (size_t)k * L.stride; }
+  char* live(int i) const { return C->ws + L.off_live[i]; }
+  float* hpart(char* s) const { return (float*)s; }
+  float* cpart(char* s) const { return (float*)(s + align_up(L.h_bytes)); }
+
+  ambptt_status wait_slot(int64_t k, bool for_write) {
+    int& pd = C->pend[size_t(k)];
+    if (pd == kPrefetchPending || (for_write && pd == kStorePending)) {
+      HIPCK(hipStreamWaitEvent(C->cs, C->ev_slot[size_t(k)], 0));
+      pd = kNone;
+      st.compute_waits++;
+    }
+    return AMBPTT_OK;
+  }
+
+  ambptt_status timed_launch(int cls, int G, int mode, const StepArgs& a) {
+    const bool sample = C->timing_sample > 0 && (launches[cls] % C->timing_sample) == 0 && samples.size() < 4096;
+    Sample smp{cls, nullptr, nullptr};
+    if (sample) {
+      HIPCK(hipEventCreate(&smp.a));
+      HIPCK(hipEventCreate(&smp.b));
+      HIPCK(hipEventRecord(smp.a, C->cs));
+    }
+    HIPCK(launch_step(G, mode, L.cfg, a, C->cs));
+    if (sample) {
+      HIPCK(hipEventRecord(smp.b, C->cs));
+      samples.push_back(smp);
+    }
+    launches[cls]++;
+    st.kernel_launches++;
+    return AMBPTT_OK;
+  }
+
+  StepArgs base_args() const {
+    StepArgs a{};
+    a.B = p.batch;
+    a.D = p.input;
+    a.H = p.hidden;
+    a.W = W;
+    a.bias = b;
+    a.WhT = WhT;
+    a.loss = p.loss;
+    a.inv_bh = 1.0f / float((double)p.batch * p.hidden);
+    return a;
+  }
+
+  // one forward step: state at `src` -> `dst`
+  ambptt_status fwd_step(int64_t t, char* src, char* dst) {
+    StepArgs a = base_args();
+    a.x = x + (size_t)t * p.batch * p.input;
+    a.h = hpart(src);
+    a.c = L.G == 4 ? cpart(src) : nullptr;
+    a.h_out = hpart(dst);
+    a.c_out = L.G == 4 ? cpart(dst) : nullptr;
+    st.forward_evals++;
+    return timed_launch(0, L.G, kForward, a);
+  }
+
+  int64_t ring(int64_t t) const { return t % (2 * (int64_t)L.window); }
+  float* zbar_at(int64_t t) const {
+    return (float*)(C->ws + L.off_zbar) + (size_t)ring(t) * p.batch * L.G * p.hidden;
+  }
+  float* hwin_at(int64_t t) const { return (float*)(C->ws + L.off_hwin) + (size_t)ring(t) * p.batch * p.hidden; }
+  float* cbar(int64_t t) const { return (float*)(C->ws + L.off_cbar[t & 1]); }
+
+  ambptt_status adjoint(int64_t t, float* dW, float* db) {
+    const int64_t n = p.n_steps;
+    StepArgs a = base_args();
+    a.x = x + (size_t)t * p.batch * p.input;
+    a.h = hpart(cur);
+    a.c = L.G == 4 ? cpart(cur) : nullptr;
+    a.first = (t == n - 1);
+    a.last = (t == n - 1);
+    a.zbar_in = a.first ? nullptr : zbar_at(t + 1);
+    a.cbar_in = a.first ? nullptr : cbar(t + 1);
+    a.zbar_out = zbar_at(t);
+    a.cbar_out = cbar(t);
+    a.hwin_out = hwin_at(t);
+    a.loss_acc = (double*)(C->ws + L.off_loss);
+    if (a.first) st.forward_evals++;  // the first turn's forward step
+    st.adjoints++;
+    ambptt_status s = timed_launch(1, L.G, kAdjoint, a);
+    if (s != AMBPTT_OK) return s;
+    const int64_t w = L.window;
+    if (t % w == 0) {  // window [t, min(t + w, n)) complete
+      const int64_t cnt = std::min(w, n - t);
+      DwArgs d{};
+      d.zbar = zbar_at(t);
+      d.x = x + (size_t)t * p.batch * p.input;
+      d.hwin = hwin_at(t);
+      d.dW = dW;
+      d.db = db;
+      d.R = int(cnt * p.batch);
+      d.D = p.input;
+      d.H = p.hidden;
+      d.GH = L.G * p.hidden;
+      const bool sample = C->timing_sample > 0 && (launches[2] % std::max<int64_t>(1, C->timing_sample / 8)) == 0 &&
+                          samples.size() < 4096;
+      Sample smp{2, nullptr, nullptr};
+      if (sample) {
+        HIPCK(hipEventCreate(&smp.a));
+        HIPCK(hipEventCreate(&smp.b));
+        HIPCK(hipEventRecord(smp.a, C->cs));
+      }
+      HIPCK(launch_dw(d, C->cs));
+      if (sample) {
+        HIPCK(hipEventRecord(smp.b, C->cs));
+        samples.push_back(smp);
+      }
+      launches[2]++;
+      st.kernel_launches++;
+    }
+    return AMBPTT_OK;
+  }
+
+  ambptt_status copy_state(char* dst, char* src) {
+    HIPCK(hipMemcpyAsync(dst, src, L.state_bytes, hipMemcpyDeviceToDevice, C->cs));
+    return AMBPTT_OK;
+  }
+
+  char* other_live() {
+    const int i = (cur_live == 0) ? 1 : 0;
+    return live(i);
+  }
+  void set_cur_live(char* ptr) {
+    cur = ptr;
+    cur_slot = -1;
+    cur_live = (ptr == live(0)) ? 0 : 1;
+  }
+  void set_cur_slot(int64_t k) {
+    cur = slot(k);
+    cur_slot = int(k);
+    cur_live = -1;
+  }
+
+  ambptt_status run(const Plan& plan, float* dW, float* db) {
+    const auto& acts = plan.acts;
+    ambptt_status s;
+    for (size_t i = 0; i < acts.size(); ++i) {
+      const Action& A = acts[i];
+      switch (A.op) {
+        case Op::Advance: {
+          int64_t fuse_k = -1;
+          if (i + 1 < acts.size() && acts[i + 1].op == Op::Snap && acts[i + 1].b == A.b &&
+              acts[i + 1].a != cur_slot)
+            fuse_k = acts[i + 1].a;
+          for (int64_t t = A.a; t < A.b; ++t) {
+            const bool last = (t + 1 == A.b);
+            if (last && fuse_k >= 0) {
+              if ((s = wait_slot(fuse_k, true)) != AMBPTT_OK) return s;
+              if ((s = fwd_step(t, cur, slot(fuse_k))) != AMBPTT_OK) return s;
+              set_cur_slot(fuse_k);
+            } else {
+              char* dst = other_live();
+              if ((s = fwd_step(t, cur, dst)) != AMBPTT_OK) return s;
+              set_cur_live(dst);
+            }
+          }
+          if (fuse_k >= 0) {
+            slot_t[size_t(fuse_k)] = A.b;
+            st.takeshots++;
+            ++i;
+          }
+          break;
+        }
+        case Op::Snap: {
+          st.takeshots++;
+          if (cur_slot == A.a) {  // already there
+            slot_t[size_t(A.a)] = A.b;
+            break;
+          }
+          if ((s = wait_slot(A.a, true)) != AMBPTT_OK) return s;
+          if ((s = copy_state(slot(A.a), cur)) != AMBPTT_OK) return s;
+          st.takeshot_copies++;
+          slot_t[size_t(A.a)] = A.b;
+          break;
+        }
+        case Op::Restore: {
+          st.restores++;
+          if ((s = wait_slot(A.a, false)) != AMBPTT_OK) return s;
+          set_cur_slot(A.a);
+          break;
+        }
+        case Op::First:
+        case Op::Youturn:
+          if ((s = adjoint(A.a, dW, db)) != AMBPTT_OK) return s;
+          break;
+        case Op::Store: {
+          const int64_t k = A.a, h = A.b;
+          HIPCK(hipEventRecord(C->ev_c, C->cs));
+          HIPCK(hipStreamWaitEvent(C->xs, C->ev_c, 0));
+          HIPCK(hipMemcpyAsync(C->host + (size_t)h * L.stride, slot(k), L.state_bytes, hipMemcpyDeviceToHost, C->xs));
+          HIPCK(hipEventRecord(C->ev_slot[size_t(k)], C->xs));
+          if (C->pend[size_t(k)] != kPrefetchPending) C->pend[size_t(k)] = kStorePending;
+          st.stores++;
+          st.bytes_d2h += (int64_t)L.state_bytes;
+          break;
+        }
+        case Op::Prefetch: {
+          const int64_t h = A.a, k = A.b, t = A.c;
+          st.prefetches++;
+          if (C->elide_prefetch && slot_t[size_t(k)] == t) {
+            st.prefetches_elided++;
+            break;
+          }
+          if (cur_slot == k) {  // the live state aliases the target: keep it
+            char* dst = live(0);
+            if ((s = copy_state(dst, cur)) != AMBPTT_OK) return s;
+            set_cur_live(dst);
+          }
+          HIPCK(hipEventRecord(C->ev_c, C->cs));
+          HIPCK(hipStreamWaitEvent(C->xs, C->ev_c, 0));
+          HIPCK(hipMemcpyAsync(slot(k), C->host + (size_t)h * L.stride, L.state_bytes, hipMemcpyHostToDevice, C->xs));
+          HIPCK(hipEventRecord(C->ev_slot[size_t(k)], C->xs));
+          C->pend[size_t(k)] = kPrefetchPending;
+          slot_t[size_t(k)] = t;
+          st.bytes_h2d += (int64_t)L.state_bytes;
+          break;
+        }
+      }
+    }
+    return AMBPTT_OK;
+  }
+};
+
+ambptt_status ensure_host(ambptt_ctx* C, size_t bytes) {
+  if (bytes <= C->host_bytes) return AMBPTT_OK;
+  if (C->host) {
+    HIPCK(hipStreamSynchronize(C->xs));
+    HIPCK(hipHostFree(C->host));
+    C->host = nullptr;
+    C->host_bytes = 0;
+  }
+  void* ptr = nullptr;
+  if (hipHostMalloc(&ptr, bytes, hipHostMallocDefault) != hipSuccess || !ptr) {
+    (void)hipGetLastError();
+    return fail(AMBPTT_ENOMEM, "hipHostMalloc of " + std::to_string(bytes) + " bytes for the host tier failed");
+  }
+  C->host = (char*)ptr;
+  C->host_bytes = bytes;
+  return AMBPTT_OK;
+}
+
+ambptt_status prepare_inputs(ambptt_ctx* C, const float* W, const void* h0, const float* c0, Exec& E) {
+  const Layout& L = C->L;
+  const ambptt_problem& p = C->p;
+  HIPCK(launch_transpose_wh(W, E.WhT, L.G * p.hidden, p.input, p.hidden, C->cs));
+  // live state <- x_0
+  char* l0 = E.live(0);
+  HIPCK(hipMemcpyAsync(l0, h0, L.h_bytes, hipMemcpyDeviceToDevice, C->cs));
+  if (L.G == 4) HIPCK(hipMemcpyAsync(E.cpart(l0), c0, L.c_bytes, hipMemcpyDeviceToDevice, C->cs));
+  E.set_cur_live(l0);
+  return AMBPTT_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+
+extern "C" {
+
+const char* ambptt_version(void) { return "ambptt 0.1 (gfx950)"; }
+
+const char* ambptt_last_error(void) { return g_err.c_str(); }
+
+int64_t ambptt_revolve_advances(int64_t n, int32_t s) {
+  if (n < 1 || s < 1) return -1;
+  return revolve_advances(n, s);
+}
+
+int64_t ambptt_schedule_evals(int64_t n, int32_t s, int64_t H, int32_t interval_min, int32_t* interval_out,
+                              int32_t* mode_out) {
+  if (n < 1 || s < 1 || H < 0 || interval_min < 0) return -1;
+  bool async = false;
+  int64_t I = 0, ev = 0;
+  plan_counts(n, s, H, interval_min, &async, &I, &ev);
+  if (interval_out) *interval_out = int32_t(I);
+  if (mode_out) *mode_out = async ? 1 : 0;
+  return ev;
+}
+
+ambptt_status ambptt_schedule_text(int64_t n, int32_t s, int64_t H, int32_t interval_min, char* buf, size_t cap,
+                                   size_t* needed) {
+  if (n < 1 || s < 1 || H < 0 || interval_min < 0) return fail(AMBPTT_EINVAL, "schedule: bad arguments");
+  try {
+    const std::string t = plan_text(make_plan(n, s, H, interval_min));
+    if (needed) *needed = t.size() + 1;
+    if (!buf || cap < t.size() + 1) return fail(AMBPTT_EINVAL, "schedule: buffer too small");
+    std::memcpy(buf, t.c_str(), t.size() + 1);
+    return AMBPTT_OK;
+  } catch (const std::exception& e) {
+    return fail(AMBPTT_EINTERNAL, e.what());
+  }
+}
+
+ambptt_status ambptt_query(const ambptt_problem* p, size_t* state_bytes, size_t* slot_pool_bytes,
+                           size_t* workspace_bytes) {
+  ambptt_status s = validate(p);
+  if (s != AMBPTT_OK) return s;
+  const Layout L = make_layout(p, 0);
+  if (state_bytes) *state_bytes = L.stride;
+  if (slot_pool_bytes) *slot_pool_bytes = L.stride * (size_t)p->fast_slots;
+  if (workspace_bytes) *workspace_bytes = L.total;
+  return AMBPTT_OK;
+}
+
+ambptt_status ambptt_create(const ambptt_problem* p, void* stream, ambptt_ctx** out) {
+  if (!out) return fail(AMBPTT_EINVAL, "out is NULL");
+  *out = nullptr;
+  ambptt_status s = validate(p);
+  if (s != AMBPTT_OK) return s;
+  ambptt_ctx* C = new ambptt_ctx();
+  C->p = *p;
+  C->L = make_layout(p, 0);
+  C->interval_min = p->interval_min;
+  C->cs = (hipStream_t)stream;
+  auto bail = [&](const char* what, hipError_t e) {
+    std::string m = std::string(what) + ": " + hipGetErrorString(e);
+    ambptt_destroy(C);
+    return fail(AMBPTT_EHIP, m);
+  };
+  hipError_t e;
+  if ((e = hipGetDevice(&C->device)) != hipSuccess) return bail("hipGetDevice", e);
+  if ((e = hipStreamCreateWithFlags(&C->xs, hipStreamNonBlocking)) != hipSuccess) return bail("hipStreamCreate", e);
+  if ((e = hipEventCreateWithFlags(&C->ev_c, hipEventDisableTiming)) != hipSuccess) return bail("hipEventCreate", e);
+  C->ev_slot.resize(size_t(p->fast_slots), nullptr);
+  C->pend.assign(size_t(p->fast_slots), kNone);
+  for (auto& ev : C->ev_slot)
+    if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess) return bail("hipEventCreate", e);
+  void* hl = nullptr;
+  if ((e = hipHostMalloc(&hl, 64, hipHostMallocDefault)) != hipSuccess) return bail("hipHostMalloc", e);
+  C->host_loss = (double*)hl;
+  *out = C;
+  return AMBPTT_OK;
+}
+
+ambptt_status ambptt_bind(ambptt_ctx* C, void* slot_pool, size_t pool_bytes, void* workspace, size_t ws_bytes) {
+  if (!C) return fail(AMBPTT_EINVAL, "ctx is NULL");
+  if (!slot_pool || !workspace) return fail(AMBPTT_EINVAL, "slot pool and workspace are required");
+  if (((uintptr_t)slot_pool % kAlign) || ((uintptr_t)workspace % kAlign))
+    return fail(AMBPTT_EINVAL, "slot pool and workspace must be 256-byte aligned");
+  if (pool_bytes < C->L.stride * (size_t)C->p.fast_slots) return fail(AMBPTT_EINVAL, "slot pool too small");
+  if (ws_bytes < C->L.total) return fail(AMBPTT_EINVAL, "workspace too small");
+  C->pool = (char*)slot_pool;
+  C->ws = (char*)workspace;
+  return AMBPTT_OK;
+}
+
+ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
+  if (!C || !key) return fail(AMBPTT_EINVAL, "ctx/key is NULL");
+  const std::string k(key);
+  if (k == "timing_sample") {
+    if (v < 0) return fail(AMBPTT_EINVAL, "timing_sample must be >= 0");
+    C->timing_sample = v;
+  } else if (k == "elide_prefetch") {
+    C->elide_prefetch = v != 0;
+  } else if (k == "window") {
+    const int wmax = auto_window(C->p.batch);
+    if (v < 0 || v > wmax) return fail(AMBPTT_EINVAL, "window must be in [0, " + std::to_string(wmax) + "]");
+    C->window_opt = int(v);
+    const Layout L2 = make_layout(&C->p, int(v == 0 ? wmax : v));
+    // same offsets except the rings, which only shrink
+    C->L.window = L2.window;
+  } else if (k == "interval_min") {
+    if (v < 0) return fail(AMBPTT_EINVAL, "interval_min must be >= 0");
+    C->interval_min = v;
+  } else {
+    return fail(AMBPTT_EINVAL, "unknown key " + k);
+  }
+  return AMBPTT_OK;
+}
+
+static ambptt_status check_run_args(ambptt_ctx* C, const void* x_seq, const void* W, const float* b, const void* h0,
+                                    const float* c0) {
+  if (!C) return fail(AMBPTT_EINVAL, "ctx is NULL");
+  if (!C->pool || !C->ws) return fail(AMBPTT_EINVAL, "ambptt_bind has not been called");
+  if ((!x_seq && C->p.input > 0) || !W || !b || !h0) return fail(AMBPTT_EINVAL, "missing input pointer");
+  if (C->L.G == 4 && !c0) return fail(AMBPTT_EINVAL, "LSTM needs c0");
+  return AMBPTT_OK;
+}
+
+ambptt_status ambptt_calibrate(ambptt_ctx* C, const void* x_seq, const void* W, const float* b, const void* h0,
+                               const float* c0, int32_t* interval_min_out, double* t_a_us, double* t_t_us) {
+  ambptt_status s = check_run_args(C, x_seq, W, b, h0, c0);
+  if (s != AMBPTT_OK) return s;
+  Exec E(C, (const float*)x_seq, (const float*)W, b);
+  if ((s = prepare_inputs(C, (const float*)W, h0, c0, E)) != AMBPTT_OK) return s;
+  if ((s = ensure_host(C, C->L.stride)) != AMBPTT_OK) return s;
+  hipEvent_t e0, e1;
+  HIPCK(hipEventCreate(&e0));
+  HIPCK(hipEventCreate(&e1));
+  const int64_t n = C->p.n_steps;
+  const int reps = 16;
+  float ms = 0.f;
+  for (int warm = 0; warm < 2; ++warm) {
+    HIPCK(hipEventRecord(e0, C->cs));
+    for (int i = 0; i < reps; ++i) {
+      char* dst = E.other_live();
+      if ((s = E.fwd_step(i % n, E.cur, dst)) != AMBPTT_OK) return s;
+      E.set_cur_live(dst);
+    }
+    HIPCK(hipEventRecord(e1, C->cs));
+    HIPCK(hipEventSynchronize(e1));
+    HIPCK(hipEventElapsedTime(&ms, e0, e1));
+  }
+  const double ta = 1000.0 * ms / reps;
+  double tt = 0.0;
+  for (int dir = 0; dir < 2; ++dir) {
+    double best = 1e30;
+    for (int rep = 0; rep < 3; ++rep) {
+      HIPCK(hipEventRecord(e0, C->xs));
+      if (dir == 0)
+        HIPCK(hipMemcpyAsync(C->host, E.live(0), C->L.state_bytes, hipMemcpyDeviceToHost, C->xs));
+      else
+        HIPCK(hipMemcpyAsync(E.live(1), C->host, C->L.state_bytes, hipMemcpyHostToDevice, C->xs));
+      HIPCK(hipEventRecord(e1, C->xs));
+      HIPCK(hipEventSynchronize(e1));
+      HIPCK(hipEventElapsedTime(&ms, e0, e1));
+      best = std::min(best, 1000.0 * ms);
+    }
+    tt = std::max(tt, best);
+  }
+  HIPCK(hipEventDestroy(e0));
+  HIPCK(hipEventDestroy(e1));
+  const int64_t I = std::max<int64_t>(1, (int64_t)std::ceil(tt / std::max(ta, 1e-3)));
+  C->interval_min = I;
+  if (interval_min_out) *interval_min_out = int32_t(std::min<int64_t>(I, INT32_MAX));
+  if (t_a_us) *t_a_us = ta;
+  if (t_t_us) *t_t_us = tt;
+  return AMBPTT_OK;
+}
+
+ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const float* b, const void* h0,
+                         const float* c0, float* dW, float* db, float* dh0, float* dc0, double* loss,
+                         ambptt_stats* stats) {
+  ambptt_status s = check_run_args(C, x_seq, W, b, h0, c0);
+  if (s != AMBPTT_OK) return s;
+  if (!dW || !db || !dh0 || (C->L.G == 4 && !dc0)) return fail(AMBPTT_EINVAL, "missing gradient pointer");
+  const ambptt_problem& p = C->p;
+  const Layout& L = C->L;
+  if (p.slow_slots > 0 && C->interval_min == 0) {
+    if ((s = ambptt_calibrate(C, x_seq, W, b, h0, c0, nullptr, nullptr, nullptr)) != AMBPTT_OK) return s;
+  }
+  const double t0 = now_us();
+  Plan plan;
+  try {
+    plan = make_plan(p.n_steps, p.fast_slots, p.slow_slots, std::max<int64_t>(C->interval_min, 1));
+  } catch (const std::exception& e) {
+    return fail(AMBPTT_EINTERNAL, e.what());
+  }
+  const double t1 = now_us();
+  if (plan.async) {
+    if ((s = ensure_host(C, (size_t)plan.host_slots_used * L.stride)) != AMBPTT_OK) return s;
+  }
+  Exec E(C, (const float*)x_seq, (const float*)W, b);
+  std::fill(C->pend.begin(), C->pend.end(), kNone);
+  const size_t GH = (size_t)L.G * p.hidden;
+  HIPCK(launch_fill32(dW, GH * (p.input + p.hidden), 0u, C->cs));
+  HIPCK(launch_fill32(db, GH, 0u, C->cs));
+  HIPCK(launch_fill32(C->ws + L.off_loss, (size_t)L.loss_slots * 2, 0u, C->cs));
+  if ((s = prepare_inputs(C, (const float*)W, h0, c0, E)) != AMBPTT_OK) return s;
+  if ((s = E.run(plan, dW, db)) != AMBPTT_OK) return s;
+  // dL/dx_0 = (zbar_0 W_h, cbar_0)
+  {
+    StepArgs a = E.base_args();
+    a.zbar_in = E.zbar_at(0);
+    a.cbar_in = E.cbar(0);
+    a.dh0 = dh0;
+    a.dc0 = dc0;
+    HIPCK(launch_step(L.G, kFinal, L.cfg, a, C->cs));
+    E.st.kernel_launches++;
+  }
+  double scale = 1.0;
+  if (p.loss == AMBPTT_LOSS_HALF_SQ_LAST) scale = 0.5;
+  else scale = 1.0 / ((double)p.batch * p.hidden);
+  double* dloss = (double*)(C->ws + L.off_lossout);
+  HIPCK(launch_loss_sum((const double*)(C->ws + L.off_loss), L.loss_slots, scale, dloss, C->cs));
+  HIPCK(hipMemcpyAsync(C->host_loss, dloss, sizeof(double), hipMemcpyDeviceToHost, C->cs));
+  HIPCK(hipStreamSynchronize(C->cs));
+  HIPCK(hipStreamSynchronize(C->xs));
+  const double t2 = now_us();
+  if (loss) *loss = *C->host_loss;
+  ambptt_stats& st = E.st;
+  double sum[3] = {0, 0, 0};
+  int64_t cnt[3] = {0, 0, 0};
+  for (auto& smp : E.samples) {
+    float ms = 0.f;
+    HIPCK(hipEventElapsedTime(&ms, smp.a, smp.b));
+    sum[smp.cls] += 1000.0 * ms;
+    cnt[smp.cls]++;
+    (void)hipEventDestroy(smp.a);
+    (void)hipEventDestroy(smp.b);
+  }
+  if (stats) {
+    st.mode = plan.async ? 1 : 0;
+    st.interval = int32_t(plan.interval);
+    st.window = L.window;
+    st.n_steps = p.n_steps;
+    st.actions = (int64_t)plan.acts.size();
+    st.recompute_factor = double(st.forward_evals) / double(p.n_steps);
+    st.schedule_us = t1 - t0;
+    st.run_us = t2 - t1;
+    st.fwd_kernel_us = cnt[0] ? sum[0] / cnt[0] : 0.0;
+    st.adj_kernel_us = cnt[1] ? sum[1] / cnt[1] : 0.0;
+    st.dw_kernel_us = cnt[2] ? sum[2] / cnt[2] : 0.0;
+    st.fwd_samples = cnt[0];
+    st.adj_samples = cnt[1];
+    st.dw_samples = cnt[2];
+    *stats = st;
+  }
+  if (st.forward_evals != plan.evals)
+    return fail(AMBPTT_EINTERNAL, "executor forward count " + std::to_string(st.forward_evals) +
+                                      " != schedule count " + std::to_string(plan.evals));
+  return AMBPTT_OK;
+}
+
+void ambptt_destroy(ambptt_ctx* C) {
+  if (!C) return;
+  if (C->xs) (void)hipStreamSynchronize(C->xs);
+  for (auto& ev : C->ev_slot)
+    if (ev) (void)hipEventDestroy(ev);
+  if (C->ev_c) (void)hipEventDestroy(C->ev_c);
+  if (C->xs) (void)hipStreamDestroy(C->xs);
+  if (C->host) (void)hipHostFree(C->host);
+  if (C->host_loss) (void)hipHostFree(C->host_loss);
+  delete C;
+}
+
+}  // extern "C"

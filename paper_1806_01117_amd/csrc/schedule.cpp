@@ -1,0 +1,203 @@
+// Checkpointing schedules (host only).
+//
+// Counting follows binomial checkpointing (Griewank and Walther), which the
+// paper uses as R(n, s) in Section 3: with s slots, the one that holds the
+// interval's first state included, reversing l steps needs at least
+//   F(l, s) = r l - beta(s + 1, r - 1)   advanced steps,
+// beta(s, r) = C(s + r, s), r the integer with beta(s, r-1) < l <= beta(s, r).
+// Schedules are built recursively: advance m steps, snapshot, reverse the
+// right part with one slot fewer, restore, reverse the left part.  Every m in
+// [max(1, l - beta(s-1, r), beta(s, r-2)), min(l-1, beta(s, r-1),
+// l - beta(s-1, r-1))] is optimal; the largest is taken.
+//
+// The two-level policy (Section 2) stores every I-th state of the forward
+// sweep to the slow level, prefetches interval starts one interval ahead in
+// the reverse sweep, and reverses each interval with the remaining fast slots;
+// I = ceil(T_T / T_A) (Section 3), raised to ceil(n / (H+1)) so the stored
+// states fit H slow slots.  Fast slots 0 and 1 alternate as interval bases.
+// If the result would not need strictly fewer forward evaluations than plain
+// Revolve at the same s, plain Revolve is used (generalising the fallback at
+// the end of Section 3).
+#include "schedule.hpp"
+
+#include <algorithm>
+#include <cstdio>
+#include <stdexcept>
+
+namespace ambptt {
+
+int64_t binom_beta(int64_t s, int64_t r) {
+  if (s < 0 || r < 0) return 0;
+  const int64_t N = s + r;
+  const int64_t k = std::min(s, r);
+  int64_t c = 1;
+  for (int64_t i = 1; i <= k; ++i) {
+    const int64_t f = N - k + i;
+    if (c > kBig / f) return kBig;
+    c = c * f / i;  // c == C(N - k + i, i), exact
+  }
+  return c;
+}
+
+static int64_t revolve_r(int64_t l, int64_t s) {
+  int64_t r = 0;
+  while (binom_beta(s, r) < l) ++r;
+  return r;
+}
+
+int64_t revolve_advances(int64_t l, int64_t s) {
+  if (l < 1 || s < 1) return -1;
+  const int64_t r = revolve_r(l, s);
+  return r * l - binom_beta(s + 1, r - 1);
+}
+
+int64_t revolve_split(int64_t l, int64_t s) {
+  const int64_t r = revolve_r(l, s);
+  int64_t hi = l - 1;
+  hi = std::min(hi, binom_beta(s, r - 1));
+  hi = std::min(hi, l - binom_beta(s - 1, r - 1));
+  return hi;
+}
+
+void plan_counts(int64_t n, int32_t s, int64_t H, int64_t interval_min, bool* async,
+                 int64_t* interval, int64_t* evals) {
+  if (n < 1 || s < 1 || H < 0 || interval_min < 0)
+    throw std::invalid_argument("schedule: need n >= 1, s >= 1, H >= 0, I_min >= 0");
+  const int64_t plain = revolve_advances(n, s) + 1;
+  *async = false;
+  *interval = 0;
+  *evals = plain;
+  if (H <= 0 || s < 2) return;
+  int64_t I = std::max<int64_t>(interval_min, 1);
+  I = std::max<int64_t>(I, (n + H) / (H + 1));  // ceil(n / (H + 1))
+  if (I >= n) return;
+  const int64_t K = (n + I - 1) / I;
+  const int64_t last = n - (K - 1) * I;
+  const int64_t ev = (K - 1) * I + revolve_advances(last, s - 1) + 1 +
+                     (K - 1) * revolve_advances(I, s - 1);
+  if (ev >= plain) return;
+  *async = true;
+  *interval = I;
+  *evals = ev;
+}
+
+namespace {
+
+struct Builder {
+  int64_t n;
+  std::vector<Action>* out;
+  int64_t live = 0;
+  std::vector<char> busy;  // fast slot occupied by an active snapshot
+
+  void push(Op op, int64_t a, int64_t b = 0, int64_t c = 0) { out->push_back({op, a, b, c}); }
+  void turn(int64_t t) { push(t == n - 1 ? Op::First : Op::Youturn, t); }
+  void restore(int64_t k, int64_t a) {
+    if (live != a) {
+      push(Op::Restore, k, a);
+      live = a;
+    }
+  }
+  void advance(int64_t t0, int64_t t1) {
+    push(Op::Advance, t0, t1);
+    live = t1;
+  }
+  int64_t take_slot() {
+    for (size_t k = 0; k < busy.size(); ++k)
+      if (!busy[k]) {
+        busy[k] = 1;
+        return int64_t(k);
+      }
+    throw std::logic_error("schedule: no free slot");
+  }
+
+  // Reverse [a, a + l) with s slots; x_a sits in slot `base`.
+  void reverse(int64_t a, int64_t l, int64_t s, int64_t base) {
+    for (;;) {
+      if (l == 1) {
+        restore(base, a);
+        turn(a);
+        return;
+      }
+      if (s == 1) {
+        for (int64_t i = l - 1; i >= 0; --i) {
+          restore(base, a);
+          if (i > 0) advance(a, a + i);
+          turn(a + i);
+        }
+        return;
+      }
+      const int64_t m = revolve_split(l, s);
+      restore(base, a);
+      advance(a, a + m);
+      const int64_t k = take_slot();
+      push(Op::Snap, k, a + m);
+      reverse(a + m, l - m, s - 1, k);
+      busy[size_t(k)] = 0;
+      l = m;  // the left part, same slots and base
+    }
+  }
+};
+
+}  // namespace
+
+Plan make_plan(int64_t n, int32_t s, int64_t H, int64_t interval_min) {
+  Plan p;
+  p.n = n;
+  p.s = s;
+  p.H = H;
+  plan_counts(n, s, H, interval_min, &p.async, &p.interval, &p.evals);
+  Builder b{n, &p.acts, 0, std::vector<char>(size_t(s), 0)};
+  if (!p.async) {
+    b.push(Op::Snap, 0, 0);
+    b.busy[0] = 1;
+    b.reverse(0, n, s, 0);
+    return p;
+  }
+  const int64_t I = p.interval;
+  const int64_t K = (n + I - 1) / I;
+  p.host_slots_used = K - 1;
+  b.busy[0] = b.busy[1] = 1;  // interval bases; Revolve works in slots 2 .. s-1
+  for (int64_t k = 0; k + 1 < K; ++k) {
+    b.push(Op::Snap, k % 2, k * I);
+    b.push(Op::Store, k % 2, k, k * I);
+    b.advance(k * I, (k + 1) * I);
+  }
+  for (int64_t k = K - 1; k >= 0; --k) {
+    const int64_t a = k * I;
+    const int64_t l = (k == K - 1) ? n - a : I;
+    const int64_t base = k % 2;
+    if (k == K - 1) b.push(Op::Snap, base, a);
+    if (k >= 1) b.push(Op::Prefetch, k - 1, (k - 1) % 2, (k - 1) * I);
+    b.reverse(a, l, s - 1, base);
+  }
+  return p;
+}
+
+std::string plan_text(const Plan& p) {
+  std::string t;
+  t.reserve(p.acts.size() * 12 + 96);
+  t += "ambptt-schedule v1 n=" + std::to_string(p.n) + " s=" + std::to_string(p.s) +
+       " H=" + std::to_string(p.H) + " I=" + std::to_string(p.interval) +
+       " mode=" + (p.async ? "async" : "revolve") + "\n";
+  char line[96];
+  for (const Action& x : p.acts) {
+    int len = 0;
+    switch (x.op) {
+      case Op::Advance: len = snprintf(line, sizeof line, "A %lld %lld\n", (long long)x.a, (long long)x.b); break;
+      case Op::Snap: len = snprintf(line, sizeof line, "S %lld %lld\n", (long long)x.a, (long long)x.b); break;
+      case Op::Restore: len = snprintf(line, sizeof line, "R %lld %lld\n", (long long)x.a, (long long)x.b); break;
+      case Op::First: len = snprintf(line, sizeof line, "F %lld\n", (long long)x.a); break;
+      case Op::Youturn: len = snprintf(line, sizeof line, "Y %lld\n", (long long)x.a); break;
+      case Op::Store:
+        len = snprintf(line, sizeof line, "W %lld %lld %lld\n", (long long)x.a, (long long)x.b, (long long)x.c);
+        break;
+      case Op::Prefetch:
+        len = snprintf(line, sizeof line, "P %lld %lld %lld\n", (long long)x.a, (long long)x.b, (long long)x.c);
+        break;
+    }
+    t.append(line, size_t(len));
+  }
+  return t;
+}
+
+}  // namespace ambptt

@@ -1,0 +1,96 @@
+"""The C-ABI library on the CPU: it loads, exports what the header declares,
+and its host-only calls agree with the oracle (no GPU calls here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle import schedule as S
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def amb():
+    import paper_1806_01117_amd as amb
+    amb.load()
+    return amb
+
+
+def _declared():
+    names = []
+    for f in os.listdir(os.path.join(ROOT, "include")):
+        if f.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", f)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names += re.findall(r"\b(ambptt_[a-z_0-9]+)\s*\(", src)
+    return sorted(set(names))
+
+
+def test_every_declared_symbol_is_exported(amb):
+    lib = ctypes.CDLL(amb.LIB_PATH)
+    names = _declared()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(lib, n), n
+    from paper_1806_01117_amd import _lib
+    assert sorted(_lib.EXPORTS) == names
+
+
+def test_version(amb):
+    assert "gfx950" in amb.version()
+
+
+def test_revolve_counts_match_oracle(amb):
+    for n in list(range(1, 80)) + [128, 1000, 2000, 10000, 20000, 123457]:
+        for s in (1, 2, 3, 4, 10, 16, 32, 64):
+            if s == 1 and n > 5000:
+                continue
+            assert amb.revolve_advances(n, s) == S.advances(n, s), (n, s)
+    with pytest.raises(ValueError):
+        amb.revolve_advances(0, 3)
+
+
+def test_schedule_text_matches_oracle_bytewise(amb):
+    for n in list(range(1, 34)) + [57, 100, 128, 257, 1000]:
+        for s in (1, 2, 3, 4, 7, 10):
+            for H in (0, 1, 3, 2000):
+                for I in (0, 1, 2, 3, 5):
+                    assert amb.schedule_text(n, s, H, I) == S.text(n, s, H, I), (n, s, H, I)
+
+
+@pytest.mark.parametrize("n,s,H,I", [(128, 4, 0, 0), (1000, 10, 1000, 1), (1000, 10, 1000, 2),
+                                     (2000, 16, 2000, 10), (10000, 32, 10000, 5)])
+def test_workload_schedules_match_oracle(amb, n, s, H, I):
+    assert amb.schedule_text(n, s, H, I) == S.text(n, s, H, I)
+    ev, interval, mode = amb.schedule_evals(n, s, H, I)
+    head, _ = S.schedule(n, s, H, I)
+    assert (ev, interval, mode) == (head["evals"], head["I"], head["mode"])
+
+
+def test_schedule_text_small_buffer(amb):
+    from paper_1806_01117_amd import _lib
+    L = amb.load()
+    need = ctypes.c_size_t(0)
+    buf = ctypes.create_string_buffer(8)
+    st = L.ambptt_schedule_text(10, 3, 0, 0, buf, 8, ctypes.byref(need))
+    assert st == _lib.EINVAL and need.value == len(S.text(10, 3)) + 1
+    assert buf.value == b""
+
+
+def test_query_sizes_and_validation(amb):
+    from paper_1806_01117_amd import ProblemSpec, AmbpttError, query
+    spec = ProblemSpec("lstm", "f32", "mean_sq_all", 64, 256, 512, 1000, 10, 1000)
+    stride, pool, ws = query(spec)
+    assert stride == 2 * 64 * 512 * 4 and pool == 10 * stride and ws > 4 * 512 * 2048
+    spec_rnn = ProblemSpec("rnn", "f32", "half_sq_last", 4, 32, 64, 128, 4)
+    stride, pool, ws = query(spec_rnn)
+    assert stride == 1024 and pool == 4 * 1024
+    for bad in (dict(n_steps=0), dict(fast_slots=0), dict(batch=0), dict(slow_slots=-1)):
+        with pytest.raises(AmbpttError) as e:
+            query(ProblemSpec(**{**spec.__dict__, **bad}))
+        assert e.value.status == -1
+    with pytest.raises(AmbpttError) as e:
+        query(ProblemSpec(**{**spec.__dict__, "hidden": 500}))
+    assert e.value.status == -4
