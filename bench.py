@@ -167,6 +167,10 @@ def main() -> int:
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl)
     print(json.dumps(line), flush=True)
+    # release device memory before interpreter teardown
+    del dx, dW, db, dh, dc, r, rv
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
     return 0
 
 

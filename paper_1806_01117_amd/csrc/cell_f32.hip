@@ -46,8 +46,64 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// acc[i][nb] += sum over 16-wide chunks [c0, c1) of A_i(ch) . B_nb(ch).
+// la(ch, i) / lb(ch, nb) return the lane's float4 of chunk ch.  Loads run one
+// group of U chunks ahead of the MFMAs (register double buffering), so a wave
+// keeps up to 2U chunks of loads in flight instead of waiting on each one.
+template <int RM, int NB, int U, class LA, class LB>
+__device__ __forceinline__ void nt_chunks(int c0, int c1, f4 (&acc)[RM][NB], LA la, LB lb) {
+  if (c0 >= c1) return;
+  f4 a[U][RM], b[U][NB];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int ch = min(c0 + u, c1 - 1);
+#pragma unroll
+    for (int i = 0; i < RM; ++i) a[u][i] = la(ch, i);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) b[u][nb] = lb(ch, nb);
+  }
+  for (int g = c0; g < c1; g += U) {
+    f4 an[U][RM], bn[U][NB];
+    const bool more = g + U < c1;
+    if (more) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int ch = min(g + U + u, c1 - 1);
+#pragma unroll
+        for (int i = 0; i < RM; ++i) an[u][i] = la(ch, i);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) bn[u][nb] = lb(ch, nb);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (g + u < c1) {
+#pragma unroll
+        for (int i = 0; i < RM; ++i)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            acc[i][nb] = mfma4(a[u][i].x, b[u][nb].x, acc[i][nb]);
+            acc[i][nb] = mfma4(a[u][i].y, b[u][nb].y, acc[i][nb]);
+            acc[i][nb] = mfma4(a[u][i].z, b[u][nb].z, acc[i][nb]);
+            acc[i][nb] = mfma4(a[u][i].w, b[u][nb].w, acc[i][nb]);
+          }
+      }
+    }
+    if (more) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+#pragma unroll
+        for (int i = 0; i < RM; ++i) a[u][i] = an[u][i];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) b[u][nb] = bn[u][nb];
+      }
+    }
+  }
+}
+
 template <int G, int RM, int RJ, int KS, int MODE>
 __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
+  constexpr int U = (RM * RJ >= 4) ? 2 : 4;   // chunks per prefetch group
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int r = lane & 15, q = lane >> 4;
@@ -56,16 +112,15 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
   const int m0 = blockIdx.x * (16 * RM);
   const int j0 = blockIdx.y * (16 * RJ);
 
-  f4 acc[RM][RJ][G];
-  f4 acch[RM][RJ];
+  f4 acc[RM][RJ * G];  // gate GEMM, column block nb = jj * G + g
+  f4 acch[RM][RJ];     // h-adjoint GEMM
 #pragma unroll
-  for (int i = 0; i < RM; ++i)
+  for (int i = 0; i < RM; ++i) {
 #pragma unroll
-    for (int jj = 0; jj < RJ; ++jj) {
+    for (int nb = 0; nb < RJ * G; ++nb) acc[i][nb] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int g = 0; g < G; ++g) acc[i][jj][g] = f4{0.f, 0.f, 0.f, 0.f};
-      acch[i][jj] = f4{0.f, 0.f, 0.f, 0.f};
-    }
+    for (int jj = 0; jj < RJ; ++jj) acch[i][jj] = f4{0.f, 0.f, 0.f, 0.f};
+  }
 
   int rows[RM];
 #pragma unroll
@@ -75,34 +130,19 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
   if (MODE != kFinal) {
     const int nch = K1 / 16;
     const int c0 = (nch * wave) / KS, c1 = (nch * (wave + 1)) / KS;
-    for (int ch = c0; ch < c1; ++ch) {
+    const float* x = a.x;
+    const float* h = a.h;
+    const float* W = a.W;
+    auto la = [&](int ch, int i) -> f4 {
       const int k = ch * 16 + 4 * q;
-      f4 av[RM];
-      if (ch * 16 < D) {
-#pragma unroll
-        for (int i = 0; i < RM; ++i) av[i] = *(const f4*)(a.x + (size_t)rows[i] * D + k);
-      } else {
-#pragma unroll
-        for (int i = 0; i < RM; ++i) av[i] = *(const f4*)(a.h + (size_t)rows[i] * H + (k - D));
-      }
-      f4 bv[RJ][G];
-#pragma unroll
-      for (int jj = 0; jj < RJ; ++jj)
-#pragma unroll
-        for (int g = 0; g < G; ++g)
-          bv[jj][g] = *(const f4*)(a.W + (size_t)(g * H + j0 + 16 * jj + r) * K1 + k);
-#pragma unroll
-      for (int i = 0; i < RM; ++i)
-#pragma unroll
-        for (int jj = 0; jj < RJ; ++jj)
-#pragma unroll
-          for (int g = 0; g < G; ++g) {
-            acc[i][jj][g] = mfma4(av[i].x, bv[jj][g].x, acc[i][jj][g]);
-            acc[i][jj][g] = mfma4(av[i].y, bv[jj][g].y, acc[i][jj][g]);
-            acc[i][jj][g] = mfma4(av[i].z, bv[jj][g].z, acc[i][jj][g]);
-            acc[i][jj][g] = mfma4(av[i].w, bv[jj][g].w, acc[i][jj][g]);
-          }
-    }
+      const float* p = (ch * 16 < D) ? x + (size_t)rows[i] * D + k : h + (size_t)rows[i] * H + (k - D);
+      return *(const f4*)p;
+    };
+    auto lb = [&](int ch, int nb) -> f4 {
+      const int jj = nb / G, g = nb % G;
+      return *(const f4*)(W + (size_t)(g * H + j0 + 16 * jj + r) * K1 + ch * 16 + 4 * q);
+    };
+    nt_chunks<RM, RJ * G, U>(c0, c1, acc, la, lb);
   }
 
   // ---- h-adjoint GEMM of the following step: hbar_{t+1} = zbar_{t+1} W_h --
@@ -110,41 +150,31 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
   if (do_hbar) {
     const int nch = GH / 16;
     const int c0 = (nch * wave) / KS, c1 = (nch * (wave + 1)) / KS;
-    for (int ch = c0; ch < c1; ++ch) {
-      const int k = ch * 16 + 4 * q;
-      f4 av[RM], bv[RJ];
-#pragma unroll
-      for (int i = 0; i < RM; ++i) av[i] = *(const f4*)(a.zbar_in + (size_t)rows[i] * GH + k);
-#pragma unroll
-      for (int jj = 0; jj < RJ; ++jj) bv[jj] = *(const f4*)(a.WhT + (size_t)(j0 + 16 * jj + r) * GH + k);
-#pragma unroll
-      for (int i = 0; i < RM; ++i)
-#pragma unroll
-        for (int jj = 0; jj < RJ; ++jj) {
-          acch[i][jj] = mfma4(av[i].x, bv[jj].x, acch[i][jj]);
-          acch[i][jj] = mfma4(av[i].y, bv[jj].y, acch[i][jj]);
-          acch[i][jj] = mfma4(av[i].z, bv[jj].z, acch[i][jj]);
-          acch[i][jj] = mfma4(av[i].w, bv[jj].w, acch[i][jj]);
-        }
-    }
+    const float* zb = a.zbar_in;
+    const float* wt = a.WhT;
+    auto la = [&](int ch, int i) -> f4 { return *(const f4*)(zb + (size_t)rows[i] * GH + ch * 16 + 4 * q); };
+    auto lb = [&](int ch, int jj) -> f4 {
+      return *(const f4*)(wt + (size_t)(j0 + 16 * jj + r) * GH + ch * 16 + 4 * q);
+    };
+    nt_chunks<RM, RJ, U>(c0, c1, acch, la, lb);
   }
 
   // ---- fixed-order reduction of the K-split partials ----------------------
   if constexpr (KS > 1) {
-    constexpr int NG = (MODE == kFinal) ? 0 : G;
-    constexpr int NA = RM * RJ * (NG + (MODE == kForward ? 0 : 1));
+    constexpr int NG = (MODE == kFinal) ? 0 : RJ * G;
+    constexpr int NH = (MODE == kForward) ? 0 : RJ;
+    constexpr int NA = RM * (NG + NH);
     __shared__ f4 red[(KS - 1) * NA * 64];
     if (wave > 0) {
       f4* dst = red + (size_t)(wave - 1) * NA * 64 + lane;
       int idx = 0;
 #pragma unroll
-      for (int i = 0; i < RM; ++i)
+      for (int i = 0; i < RM; ++i) {
 #pragma unroll
-        for (int jj = 0; jj < RJ; ++jj) {
+        for (int nb = 0; nb < NG; ++nb) dst[(idx++) * 64] = acc[i][nb];
 #pragma unroll
-          for (int g = 0; g < NG; ++g) dst[(idx++) * 64] = acc[i][jj][g];
-          if (MODE != kForward) dst[(idx++) * 64] = acch[i][jj];
-        }
+        for (int jj = 0; jj < NH; ++jj) dst[(idx++) * 64] = acch[i][jj];
+      }
     }
     __syncthreads();
     if (wave != 0) return;
@@ -152,13 +182,12 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
       const f4* src = red + (size_t)(w - 1) * NA * 64 + lane;
       int idx = 0;
 #pragma unroll
-      for (int i = 0; i < RM; ++i)
+      for (int i = 0; i < RM; ++i) {
 #pragma unroll
-        for (int jj = 0; jj < RJ; ++jj) {
+        for (int nb = 0; nb < NG; ++nb) acc[i][nb] += src[(idx++) * 64];
 #pragma unroll
-          for (int g = 0; g < NG; ++g) acc[i][jj][g] += src[(idx++) * 64];
-          if (MODE != kForward) acch[i][jj] += src[(idx++) * 64];
-        }
+        for (int jj = 0; jj < NH; ++jj) acch[i][jj] += src[(idx++) * 64];
+      }
     }
   }
 
@@ -180,18 +209,19 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
           if (G == 4) a.dc0[o] = a.cbar_in[o];
           continue;
         }
+        const int nb = jj * G;
         float h1, c1 = 0.f, tc = 0.f, ig = 0.f, fg = 0.f, gg = 0.f, og = 0.f, cold = 0.f;
         if (G == 4) {
-          ig = sigm(acc[i][jj][0][v] + a.bias[j]);
-          fg = sigm(acc[i][jj][1 % G][v] + a.bias[H + j]);
-          gg = tanhf(acc[i][jj][2 % G][v] + a.bias[2 * H + j]);
-          og = sigm(acc[i][jj][3 % G][v] + a.bias[3 * H + j]);
+          ig = sigm(acc[i][nb][v] + a.bias[j]);
+          fg = sigm(acc[i][nb + 1 % G][v] + a.bias[H + j]);
+          gg = tanhf(acc[i][nb + 2 % G][v] + a.bias[2 * H + j]);
+          og = sigm(acc[i][nb + 3 % G][v] + a.bias[3 * H + j]);
           cold = a.c[o];
           c1 = fg * cold + ig * gg;
           tc = tanhf(c1);
           h1 = og * tc;
         } else {
-          h1 = tanhf(acc[i][jj][0][v] + a.bias[j]);
+          h1 = tanhf(acc[i][nb][v] + a.bias[j]);
         }
         if (MODE == kForward) {
           a.h_out[o] = h1;
@@ -234,49 +264,112 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
   }
 }
 
-// dW[k][c] += sum_r Z[r][k] X[r][c]: a "TN" product, both operands row-major in
-// the reduction index r.  Lane l feeds Z[r][k0 + (l & 15)] and X[r][c0 + (l & 15)]
-// for r = r0 + 4 q + (l >> 4); column D+H of X is the constant 1 (bias gradient).
-template <int RK, int RC>
-__global__ __launch_bounds__(64) void dw_f32(DwArgs a) {
-  const int lane = threadIdx.x;
+// dW[k][c] += sum_r Z[r][k] X[r][c] and db[k] += sum_r Z[r][k] over the R rows
+// of one window: a "TN" product, both operands row-major in the reduction index
+// r.  Lane l feeds Z[r][k0 + (l & 15)] and X[r][c0 + (l & 15)] for
+// r = r0 + 4 qq + (l >> 4).  A workgroup owns a (16 RK) x (16 RC) tile of dW;
+// its KSR waves split the rows and their partials are summed through LDS in a
+// fixed order.  The bias gradient is a plain column sum of Z, done with vector
+// adds by the workgroups of the first column tile.
+template <int RK, int RC, int KSR, int U>
+__global__ __launch_bounds__(64 * KSR) void dw_f32(DwArgs a) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int li = lane & 15, lk = lane >> 4;
   const int k0 = blockIdx.x * (16 * RK);
   const int c0 = blockIdx.y * (16 * RC);
   const int D = a.D, H = a.H, GH = a.GH, R = a.R, N = D + H;
+  const bool do_bias = blockIdx.y == 0;
 
   f4 acc[RK][RC];
+  float bsum[RK];
 #pragma unroll
-  for (int ik = 0; ik < RK; ++ik)
+  for (int ik = 0; ik < RK; ++ik) {
+    bsum[ik] = 0.f;
 #pragma unroll
     for (int ic = 0; ic < RC; ++ic) acc[ik][ic] = f4{0.f, 0.f, 0.f, 0.f};
-
-  for (int r0 = 0; r0 < R; r0 += 16) {
-    float za[RK][4], xb[RC][4];
+  }
+  const float* zcol = a.zbar + k0 + li;
+  const float* xcol[RC];
+  int xld[RC];
+  bool cok[RC];
+#pragma unroll
+  for (int ic = 0; ic < RC; ++ic) {
+    const int c = c0 + 16 * ic + li;
+    cok[ic] = c < N;
+    xcol[ic] = c < D ? a.x + c : a.hwin + (min(c, N - 1) - D);
+    xld[ic] = c < D ? D : H;
+  }
+  auto load = [&](int ch, float (&za)[4][RK], float (&xb)[4][RC]) {
 #pragma unroll
     for (int qq = 0; qq < 4; ++qq) {
-      const int rr = r0 + 4 * qq + lk;
+      const int rr = ch * 16 + 4 * qq + lk;
       const bool ok = rr < R;
 #pragma unroll
-      for (int ik = 0; ik < RK; ++ik) za[ik][qq] = ok ? a.zbar[(size_t)rr * GH + k0 + 16 * ik + li] : 0.f;
+      for (int ik = 0; ik < RK; ++ik) za[qq][ik] = ok ? zcol[(size_t)rr * GH + 16 * ik] : 0.f;
 #pragma unroll
-      for (int ic = 0; ic < RC; ++ic) {
-        const int c = c0 + 16 * ic + li;
-        float v = 0.f;
-        if (ok) {
-          if (c < D) v = a.x[(size_t)rr * D + c];
-          else if (c < N) v = a.hwin[(size_t)rr * H + (c - D)];
-          else if (c == N) v = 1.f;
+      for (int ic = 0; ic < RC; ++ic) xb[qq][ic] = (ok && cok[ic]) ? xcol[ic][(size_t)rr * xld[ic]] : 0.f;
+    }
+  };
+  const int nch = (R + 15) / 16;
+  const int ch0 = (nch * wave) / KSR, ch1 = (nch * (wave + 1)) / KSR;
+  if (ch0 < ch1) {
+    float za[U][4][RK], xb[U][4][RC];
+#pragma unroll
+    for (int u = 0; u < U; ++u) load(min(ch0 + u, ch1 - 1), za[u], xb[u]);
+    for (int g = ch0; g < ch1; g += U) {
+      float zn[U][4][RK], xn[U][4][RC];
+      const bool more = g + U < ch1;
+      if (more) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) load(min(g + U + u, ch1 - 1), zn[u], xn[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (g + u < ch1) {
+#pragma unroll
+          for (int qq = 0; qq < 4; ++qq)
+#pragma unroll
+            for (int ik = 0; ik < RK; ++ik) {
+#pragma unroll
+              for (int ic = 0; ic < RC; ++ic) acc[ik][ic] = mfma4(za[u][qq][ik], xb[u][qq][ic], acc[ik][ic]);
+              if (do_bias) bsum[ik] += za[u][qq][ik];
+            }
         }
-        xb[ic][qq] = v;
+      }
+      if (more) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+          for (int qq = 0; qq < 4; ++qq) {
+#pragma unroll
+            for (int ik = 0; ik < RK; ++ik) za[u][qq][ik] = zn[u][qq][ik];
+#pragma unroll
+            for (int ic = 0; ic < RC; ++ic) xb[u][qq][ic] = xn[u][qq][ic];
+          }
       }
     }
+  }
+  if constexpr (KSR > 1) {
+    __shared__ f4 red[(KSR - 1) * RK * RC * 64];
+    __shared__ float bred[(KSR - 1) * RK * 64];
+    if (wave > 0) {
 #pragma unroll
-    for (int qq = 0; qq < 4; ++qq)
+      for (int ik = 0; ik < RK; ++ik) {
 #pragma unroll
-      for (int ik = 0; ik < RK; ++ik)
+        for (int ic = 0; ic < RC; ++ic) red[((wave - 1) * RK * RC + ik * RC + ic) * 64 + lane] = acc[ik][ic];
+        bred[((wave - 1) * RK + ik) * 64 + lane] = bsum[ik];
+      }
+    }
+    __syncthreads();
+    if (wave != 0) return;
+    for (int w = 1; w < KSR; ++w) {
 #pragma unroll
-        for (int ic = 0; ic < RC; ++ic) acc[ik][ic] = mfma4(za[ik][qq], xb[ic][qq], acc[ik][ic]);
+      for (int ik = 0; ik < RK; ++ik) {
+#pragma unroll
+        for (int ic = 0; ic < RC; ++ic) acc[ik][ic] += red[((w - 1) * RK * RC + ik * RC + ic) * 64 + lane];
+        bsum[ik] += bred[((w - 1) * RK + ik) * 64 + lane];
+      }
+    }
   }
 #pragma unroll
   for (int ik = 0; ik < RK; ++ik)
@@ -287,8 +380,16 @@ __global__ __launch_bounds__(64) void dw_f32(DwArgs a) {
         const int k = k0 + 16 * ik + 4 * lk + v;
         const int c = c0 + 16 * ic + li;
         if (c < N) a.dW[(size_t)k * N + c] += acc[ik][ic][v];
-        else if (c == N) a.db[k] += acc[ik][ic][v];
       }
+  if (do_bias) {
+#pragma unroll
+    for (int ik = 0; ik < RK; ++ik) {
+      float v = bsum[ik];
+      v += __shfl_xor(v, 16, 64);
+      v += __shfl_xor(v, 32, 64);
+      if (lk == 0) a.db[k0 + 16 * ik + li] += v;
+    }
+  }
 }
 
 __global__ void transpose_wh_f32(const float* __restrict__ W, float* __restrict__ WhT, int GH, int D, int H) {
@@ -375,13 +476,13 @@ hipError_t launch_step(int G, int mode, const StepCfg& c, const StepArgs& a, hip
 }
 
 hipError_t launch_dw(const DwArgs& a, hipStream_t s) {
-  const int N1 = a.D + a.H + 1;
-  if (a.GH % 32 == 0) {
-    dim3 grid(a.GH / 32, (N1 + 31) / 32);
-    hipLaunchKernelGGL((dw_f32<2, 2>), grid, dim3(64), 0, s, a);
+  const int N = a.D + a.H;
+  if (a.GH % 64 == 0) {
+    dim3 grid(a.GH / 64, (N + 63) / 64);
+    hipLaunchKernelGGL((dw_f32<4, 4, 4, 2>), grid, dim3(256), 0, s, a);
   } else {
-    dim3 grid(a.GH / 16, (N1 + 15) / 16);
-    hipLaunchKernelGGL((dw_f32<1, 1>), grid, dim3(64), 0, s, a);
+    dim3 grid(a.GH / 16, (N + 63) / 64);
+    hipLaunchKernelGGL((dw_f32<1, 4, 4, 2>), grid, dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

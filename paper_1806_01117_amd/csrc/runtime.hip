@@ -178,9 +178,15 @@ struct Exec {
   ambptt_status wait_slot(int64_t k, bool for_write) {
     int& pd = C->pend[size_t(k)];
     if (pd == kPrefetchPending || (for_write && pd == kStorePending)) {
-      HIPCK(hipStreamWaitEvent(C->cs, C->ev_slot[size_t(k)], 0));
+      // only a copy still in flight costs the compute stream a wait
+      const hipError_t q = hipEventQuery(C->ev_slot[size_t(k)]);
+      if (q == hipErrorNotReady) {
+        HIPCK(hipStreamWaitEvent(C->cs, C->ev_slot[size_t(k)], 0));
+        st.compute_waits++;
+      } else if (q != hipSuccess) {
+        HIPCK(q);
+      }
       pd = kNone;
-      st.compute_waits++;
     }
     return AMBPTT_OK;
   }
