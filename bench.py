@@ -127,19 +127,22 @@ def main() -> int:
     rv.close()
 
     # roofline of the dominant kernel (largest device time in one pass)
+    from paper_1806_01117_amd._lib import KERNEL_CLASSES
     fl = step_flops(spec, st["window"])
-    nwin = -(-wl.n_steps // st["window"])
-    avg = lambda k: float(np.mean([s[k] for s in stats if s[k] > 0])) if any(s[k] > 0 for s in stats) else 0.0
-    kern = {"fwd": (avg("fwd_kernel_us"), st["forward_evals"] - 1),
-            "adj": (avg("adj_kernel_us"), st["adjoints"]),
-            "dw": (avg("dw_kernel_us"), nwin)}
+    flops = {"fwd": fl["fwd"], "adj": fl["adj"], "dw": fl["dw"]}
+    kern = {}
+    for i, name in enumerate(KERNEL_CLASSES):
+        us = [s_["kernel_us"][i] for s_ in stats if s_["kernel_samples"][i] > 0]
+        if us:
+            kern[name] = (float(np.mean(us)), st["kernel_calls"][i])
     tot = {k: us * cnt for k, (us, cnt) in kern.items()}
-    dom = max(tot, key=tot.get)
-    dom_us = kern[dom][0]
-    achieved = fl[dom] / (dom_us * 1e-6) / 1e12 if dom_us > 0 else 0.0
-    names = {"fwd": "step_f32 forward (gate GEMM + LSTM cell)",
-             "adj": "step_f32 adjoint (gate recompute + h-adjoint GEMM + gate derivatives)",
-             "dw": "dw_f32 weight-gradient window"}
+    cand = [k for k in tot if k in flops]
+    dom = max(cand, key=tot.get) if cand else "adj"
+    dom_us = kern[dom][0] if dom in kern else 0.0
+    achieved = flops[dom] / (dom_us * 1e-6) / 1e12 if dom_us > 0 else 0.0
+    names = {"fwd": "forward step gate GEMM (part_gemm_f32, split-K)",
+             "adj": "adjoint step GEMMs: gate recompute + h-adjoint (part_gemm_f32, split-K)",
+             "dw": "weight-gradient window (dw_lds_f32)"}
     r.close()
 
     line = {
@@ -156,6 +159,10 @@ def main() -> int:
         "plain_revolve": {"value": round(rv_value, 2), "unit": "timesteps/s",
                           "recompute_factor": round(rvo["stats"]["recompute_factor"], 4)},
         "kernel_us": {k: round(v[0], 3) for k, v in kern.items()},
+        "kernel_calls_per_pass": {k: int(v[1]) for k, v in kern.items()},
+        "device_ms_per_pass": round(sum(tot.values()) / 1000.0, 3),
+        "host_enqueue_ms_per_pass": round(st["enqueue_us"] / 1000.0, 3),
+        "host_run_ms_per_pass": round(st["run_us"] / 1000.0, 3),
         "host_link": {"bytes_d2h": st["bytes_d2h"], "bytes_h2d": st["bytes_h2d"],
                       "stores": st["stores"], "prefetches": st["prefetches"],
                       "prefetches_elided": st["prefetches_elided"], "compute_waits": st["compute_waits"]},

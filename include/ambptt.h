@@ -101,10 +101,20 @@ typedef struct {
   double recompute_factor;
   double schedule_us;      /* host time to build the schedule */
   double run_us;           /* host wall time of the forward + reverse pass */
-  /* average device time of sampled launches (0 if sampling is off) */
-  double fwd_kernel_us, adj_kernel_us, dw_kernel_us;
-  int64_t fwd_samples, adj_samples, dw_samples;
+  double enqueue_us;       /* host time spent enqueueing it (run_us minus the final wait) */
+  /* average device time of sampled launches per kernel class (0 if sampling
+   * is off): AMBPTT_K_* below */
+  double kernel_us[6];
+  int64_t kernel_samples[6];
+  int64_t kernel_calls[6];
 } ambptt_stats;
+
+/* Kernel classes of ambptt_stats.kernel_*: forward step GEMM (the whole
+ * forward step on the single-launch path), its cell epilogue, adjoint step
+ * GEMM (the whole adjoint step on the single-launch path), its epilogue, the
+ * weight-gradient window, and everything else. */
+enum { AMBPTT_K_FWD = 0, AMBPTT_K_FWD_EPI = 1, AMBPTT_K_ADJ = 2, AMBPTT_K_ADJ_EPI = 3,
+       AMBPTT_K_DW = 4, AMBPTT_K_OTHER = 5 };
 
 typedef struct ambptt_ctx ambptt_ctx;
 

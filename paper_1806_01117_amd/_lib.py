@@ -31,12 +31,21 @@ class Stats(C.Structure):
                 ("restores", C.c_int64), ("stores", C.c_int64), ("prefetches", C.c_int64),
                 ("prefetches_elided", C.c_int64), ("bytes_d2h", C.c_int64), ("bytes_h2d", C.c_int64),
                 ("compute_waits", C.c_int64), ("kernel_launches", C.c_int64),
-                ("recompute_factor", C.c_double), ("schedule_us", C.c_double), ("run_us", C.c_double),
-                ("fwd_kernel_us", C.c_double), ("adj_kernel_us", C.c_double), ("dw_kernel_us", C.c_double),
-                ("fwd_samples", C.c_int64), ("adj_samples", C.c_int64), ("dw_samples", C.c_int64)]
+                ("recompute_factor", C.c_double), ("schedule_us", C.c_double), ("run_us", C.c_double), ("enqueue_us", C.c_double),
+                ("kernel_us", C.c_double * 6), ("kernel_samples", C.c_int64 * 6),
+                ("kernel_calls", C.c_int64 * 6)]
 
     def as_dict(self) -> dict:
-        return {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved0"}
+        d = {}
+        for k, _ in self._fields_:
+            if k == "reserved0":
+                continue
+            v = getattr(self, k)
+            d[k] = list(v) if isinstance(v, C.Array) else v
+        return d
+
+
+KERNEL_CLASSES = ["fwd", "fwd_epi", "adj", "adj_epi", "dw", "other"]
 
 
 _lib = None

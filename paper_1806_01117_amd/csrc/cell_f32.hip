@@ -265,131 +265,96 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
 }
 
 // dW[k][c] += sum_r Z[r][k] X[r][c] and db[k] += sum_r Z[r][k] over the R rows
-// of one window: a "TN" product, both operands row-major in the reduction index
-// r.  Lane l feeds Z[r][k0 + (l & 15)] and X[r][c0 + (l & 15)] for
-// r = r0 + 4 qq + (l >> 4).  A workgroup owns a (16 RK) x (16 RC) tile of dW;
-// its KSR waves split the rows and their partials are summed through LDS in a
-// fixed order.  The bias gradient is a plain column sum of Z, done with vector
-// adds by the workgroups of the first column tile.
-template <int RK, int RC, int KSR, int U>
-__global__ __launch_bounds__(64 * KSR) void dw_f32(DwArgs a) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// of one window (a "TN" product: both operands are row-major in r).
+// Workgroup = 4 waves on a 64 (k) x 64 (c) tile of dW, each wave a 32 x 32
+// quarter (2 x 2 MFMA blocks).  Rows stream through LDS in stages of 64:
+// every thread loads 4 float4 of Z and 4 of X per stage with coalesced
+// row-contiguous reads, the next stage's loads are in flight while the
+// current stage's MFMAs run, and LDS rows are padded to 80 floats so the MFMA
+// operand reads (16 consecutive floats from each of 4 rows) hit distinct banks.
+// Lane l feeds Z[r][k0 + (l & 15)] and X[r][c0 + (l & 15)] for
+// r = 4 g + (l >> 4).  The bias gradient is the column sum of Z, taken from
+// LDS by the first wave of the workgroups of column tile 0.
+constexpr int kDwT = 64, kDwS = 64, kDwLd = 80;
+
+__global__ __launch_bounds__(256) void dw_lds_f32(DwArgs a) {
+  __shared__ float Zs[2][kDwS][kDwLd];
+  __shared__ float Xs[2][kDwS][kDwLd];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
   const int li = lane & 15, lk = lane >> 4;
-  const int k0 = blockIdx.x * (16 * RK);
-  const int c0 = blockIdx.y * (16 * RC);
+  const int k0 = blockIdx.x * kDwT, c0 = blockIdx.y * kDwT;
   const int D = a.D, H = a.H, GH = a.GH, R = a.R, N = D + H;
   const bool do_bias = blockIdx.y == 0;
 
-  f4 acc[RK][RC];
-  float bsum[RK];
+  // loader: thread t moves rows (t >> 4) + 16 p, columns 4 (t & 15) .. +3
+  const int lrow = tid >> 4, lcol = 4 * (tid & 15);
+  const int c = c0 + lcol;
+  const bool cok = c < N;
+  const float* xsrc = c < D ? a.x + c : a.hwin + (min(c, N - 1) - D);
+  const int xld = c < D ? D : H;
+  const bool kok = k0 + lcol < GH;  // GH % 16 == 0: a float4 is wholly in or out
+  const float* zsrc = a.zbar + min(k0 + lcol, GH - 4);
+  f4 zr[4], xr[4];
+  auto load = [&](int st) {
 #pragma unroll
-  for (int ik = 0; ik < RK; ++ik) {
-    bsum[ik] = 0.f;
-#pragma unroll
-    for (int ic = 0; ic < RC; ++ic) acc[ik][ic] = f4{0.f, 0.f, 0.f, 0.f};
-  }
-  const float* zcol = a.zbar + k0 + li;
-  const float* xcol[RC];
-  int xld[RC];
-  bool cok[RC];
-#pragma unroll
-  for (int ic = 0; ic < RC; ++ic) {
-    const int c = c0 + 16 * ic + li;
-    cok[ic] = c < N;
-    xcol[ic] = c < D ? a.x + c : a.hwin + (min(c, N - 1) - D);
-    xld[ic] = c < D ? D : H;
-  }
-  auto load = [&](int ch, float (&za)[4][RK], float (&xb)[4][RC]) {
-#pragma unroll
-    for (int qq = 0; qq < 4; ++qq) {
-      const int rr = ch * 16 + 4 * qq + lk;
-      const bool ok = rr < R;
-#pragma unroll
-      for (int ik = 0; ik < RK; ++ik) za[qq][ik] = ok ? zcol[(size_t)rr * GH + 16 * ik] : 0.f;
-#pragma unroll
-      for (int ic = 0; ic < RC; ++ic) xb[qq][ic] = (ok && cok[ic]) ? xcol[ic][(size_t)rr * xld[ic]] : 0.f;
+    for (int p = 0; p < 4; ++p) {
+      const int row = st * kDwS + lrow + 16 * p;
+      const bool ok = row < R;
+      zr[p] = (ok && kok) ? *(const f4*)(zsrc + (size_t)row * GH) : f4{0.f, 0.f, 0.f, 0.f};
+      xr[p] = (ok && cok) ? *(const f4*)(xsrc + (size_t)row * xld) : f4{0.f, 0.f, 0.f, 0.f};
     }
   };
-  const int nch = (R + 15) / 16;
-  const int ch0 = (nch * wave) / KSR, ch1 = (nch * (wave + 1)) / KSR;
-  if (ch0 < ch1) {
-    float za[U][4][RK], xb[U][4][RC];
+  auto store = [&](int buf) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) load(min(ch0 + u, ch1 - 1), za[u], xb[u]);
-    for (int g = ch0; g < ch1; g += U) {
-      float zn[U][4][RK], xn[U][4][RC];
-      const bool more = g + U < ch1;
-      if (more) {
-#pragma unroll
-        for (int u = 0; u < U; ++u) load(min(g + U + u, ch1 - 1), zn[u], xn[u]);
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        if (g + u < ch1) {
-#pragma unroll
-          for (int qq = 0; qq < 4; ++qq)
-#pragma unroll
-            for (int ik = 0; ik < RK; ++ik) {
-#pragma unroll
-              for (int ic = 0; ic < RC; ++ic) acc[ik][ic] = mfma4(za[u][qq][ik], xb[u][qq][ic], acc[ik][ic]);
-              if (do_bias) bsum[ik] += za[u][qq][ik];
-            }
-        }
-      }
-      if (more) {
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-          for (int qq = 0; qq < 4; ++qq) {
-#pragma unroll
-            for (int ik = 0; ik < RK; ++ik) za[u][qq][ik] = zn[u][qq][ik];
-#pragma unroll
-            for (int ic = 0; ic < RC; ++ic) xb[u][qq][ic] = xn[u][qq][ic];
-          }
-      }
+    for (int p = 0; p < 4; ++p) {
+      *(f4*)&Zs[buf][lrow + 16 * p][lcol] = zr[p];
+      *(f4*)&Xs[buf][lrow + 16 * p][lcol] = xr[p];
     }
-  }
-  if constexpr (KSR > 1) {
-    __shared__ f4 red[(KSR - 1) * RK * RC * 64];
-    __shared__ float bred[(KSR - 1) * RK * 64];
-    if (wave > 0) {
+  };
+
+  f4 acc[2][2];
 #pragma unroll
-      for (int ik = 0; ik < RK; ++ik) {
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int ic = 0; ic < RC; ++ic) red[((wave - 1) * RK * RC + ik * RC + ic) * 64 + lane] = acc[ik][ic];
-        bred[((wave - 1) * RK + ik) * 64 + lane] = bsum[ik];
-      }
+    for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+  float bsum = 0.f;
+
+  const int nst = (R + kDwS - 1) / kDwS;
+  load(0);
+  store(0);
+  __syncthreads();
+  for (int st = 0; st < nst; ++st) {
+    const int buf = st & 1;
+    const bool more = st + 1 < nst;
+    if (more) load(st + 1);
+#pragma unroll 4
+    for (int g = 0; g < kDwS / 4; ++g) {
+      const int rr = 4 * g + lk;
+      const float a0 = Zs[buf][rr][wm * 32 + li], a1 = Zs[buf][rr][wm * 32 + 16 + li];
+      const float b0 = Xs[buf][rr][wn * 32 + li], b1 = Xs[buf][rr][wn * 32 + 16 + li];
+      acc[0][0] = mfma4(a0, b0, acc[0][0]);
+      acc[0][1] = mfma4(a0, b1, acc[0][1]);
+      acc[1][0] = mfma4(a1, b0, acc[1][0]);
+      acc[1][1] = mfma4(a1, b1, acc[1][1]);
     }
+    if (do_bias && wave == 0) {
+      for (int rr = 0; rr < kDwS; ++rr) bsum += Zs[buf][rr][lane];
+    }
+    if (more) store(buf ^ 1);
     __syncthreads();
-    if (wave != 0) return;
-    for (int w = 1; w < KSR; ++w) {
-#pragma unroll
-      for (int ik = 0; ik < RK; ++ik) {
-#pragma unroll
-        for (int ic = 0; ic < RC; ++ic) acc[ik][ic] += red[((w - 1) * RK * RC + ik * RC + ic) * 64 + lane];
-        bsum[ik] += bred[((w - 1) * RK + ik) * 64 + lane];
-      }
-    }
   }
 #pragma unroll
-  for (int ik = 0; ik < RK; ++ik)
+  for (int ik = 0; ik < 2; ++ik)
 #pragma unroll
-    for (int ic = 0; ic < RC; ++ic)
+    for (int ic = 0; ic < 2; ++ic)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int k = k0 + 16 * ik + 4 * lk + v;
-        const int c = c0 + 16 * ic + li;
-        if (c < N) a.dW[(size_t)k * N + c] += acc[ik][ic][v];
+        const int k = k0 + wm * 32 + 16 * ik + 4 * lk + v;
+        const int cc = c0 + wn * 32 + 16 * ic + li;
+        if (cc < N && k < GH) a.dW[(size_t)k * N + cc] += acc[ik][ic][v];
       }
-  if (do_bias) {
-#pragma unroll
-    for (int ik = 0; ik < RK; ++ik) {
-      float v = bsum[ik];
-      v += __shfl_xor(v, 16, 64);
-      v += __shfl_xor(v, 32, 64);
-      if (lk == 0) a.db[k0 + 16 * ik + li] += v;
-    }
-  }
+  if (do_bias && wave == 0 && k0 + lane < GH) a.db[k0 + lane] += bsum;
 }
 
 __global__ void transpose_wh_f32(const float* __restrict__ W, float* __restrict__ WhT, int GH, int D, int H) {
@@ -476,17 +441,12 @@ hipError_t launch_step(int G, int mode, const StepCfg& c, const StepArgs& a, hip
 }
 
 hipError_t launch_dw(const DwArgs& a, hipStream_t s) {
+  if (a.GH % 16 != 0) return hipErrorInvalidValue;
   const int N = a.D + a.H;
-  if (a.GH % 64 == 0) {
-    dim3 grid(a.GH / 64, (N + 63) / 64);
-    hipLaunchKernelGGL((dw_f32<4, 4, 4, 2>), grid, dim3(256), 0, s, a);
-  } else {
-    dim3 grid(a.GH / 16, (N + 63) / 64);
-    hipLaunchKernelGGL((dw_f32<1, 4, 4, 2>), grid, dim3(256), 0, s, a);
-  }
+  dim3 grid((a.GH + kDwT - 1) / kDwT, (N + kDwT - 1) / kDwT);
+  hipLaunchKernelGGL(dw_lds_f32, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
-
 hipError_t launch_transpose_wh(const float* W, float* WhT, int GH, int D, int H, hipStream_t s) {
   dim3 grid((GH + 31) / 32, (H + 31) / 32);
   hipLaunchKernelGGL(transpose_wh_f32, grid, dim3(32, 8), 0, s, W, WhT, GH, D, H);

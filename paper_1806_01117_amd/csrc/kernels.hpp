@@ -57,6 +57,9 @@ StepCfg pick_step_cfg(int G, int B, int D, int H);
 void step_grid(const StepCfg& cfg, int B, int H, dim3* grid, dim3* block);
 hipError_t launch_step(int G, int mode, const StepCfg& cfg, const StepArgs& a, hipStream_t s);
 hipError_t launch_dw(const DwArgs& a, hipStream_t s);
+// Small-batch path: one launch per step, 16 rows x (8 LSTM | 16 RNN) units per workgroup.
+void step_small_grid(int G, int B, int H, dim3* grid, dim3* block);
+hipError_t launch_step_small(int G, int mode, const StepArgs& a, hipStream_t s);
 hipError_t launch_transpose_wh(const float* W, float* WhT, int GH, int D, int H, hipStream_t s);
 hipError_t launch_fill32(void* p, size_t words, uint32_t value, hipStream_t s);
 hipError_t launch_loss_sum(const double* acc, int n, double scale, double* out, hipStream_t s);

@@ -62,7 +62,8 @@ struct Layout {
   size_t off_live[2] = {0, 0}, off_wht = 0, off_zbar = 0, off_hwin = 0, off_cbar[2] = {0, 0};
   size_t off_loss = 0, off_lossout = 0, total = 0;
   int loss_slots = 0;
-  StepCfg cfg{1, 1, 1};
+  StepCfg cfg{1, 1, 1};  // single-launch path
+  bool small = false;    // one-launch small-batch path (step_small_f32)
 };
 
 ambptt_status validate(const ambptt_problem* p) {
@@ -104,6 +105,14 @@ Layout make_layout(const ambptt_problem* p, int window) {
   dim3 grid, block;
   step_grid(L.cfg, p->batch, p->hidden, &grid, &block);
   L.loss_slots = int(grid.x * grid.y);
+  // Problems with fewer than 1024 tiles of 16 rows x 16 units run the
+  // small-batch kernels, which spread even a 64-row batch over all CUs.
+  const long tiles = (long)((p->batch + 15) / 16) * (p->hidden / 16);
+  L.small = tiles < 1024;
+  if (L.small) {
+    step_small_grid(L.G, p->batch, p->hidden, &grid, &block);
+    L.loss_slots = int(grid.x * grid.y);
+  }
   size_t o = 0;
   L.off_live[0] = o; o += L.stride;
   L.off_live[1] = o; o += L.stride;
@@ -126,6 +135,10 @@ struct ambptt_ctx {
   int device = 0;
   hipStream_t cs = nullptr;  // compute (caller's)
   hipStream_t xs = nullptr;  // copy stream (owned)
+  hipStream_t ds = nullptr;  // weight-gradient stream (owned)
+  hipEvent_t ev_dw[2] = {nullptr, nullptr};  // last dW launch per ring half
+  hipEvent_t ev_c2 = nullptr;
+  std::vector<hipEvent_t> tpool;  // timing events, reused across runs
   char* pool = nullptr;
   char* ws = nullptr;
   char* host = nullptr;
@@ -162,8 +175,9 @@ struct Exec {
   int cur_slot = -1;  // slot index the live state aliases, or -1
   int cur_live = -1;  // live buffer index, or -1
   std::vector<int64_t> slot_t;
-  int64_t launches[3] = {0, 0, 0};
+  int64_t calls[6] = {0, 0, 0, 0, 0, 0};
   std::vector<Sample> samples;
+  bool live_dead = false;  // the live state was consumed by an adjoint step
 
   Exec(ambptt_ctx* c, const float* x_, const float* W_, const float* b_)
       : C(c), L(c->L), p(c->p), x(x_), W(W_), b(b_), slot_t(size_t(c->p.fast_slots), -1) {
@@ -191,20 +205,30 @@ struct Exec {
     return AMBPTT_OK;
   }
 
-  ambptt_status timed_launch(int cls, int G, int mode, const StepArgs& a) {
-    const bool sample = C->timing_sample > 0 && (launches[cls] % C->timing_sample) == 0 && samples.size() < 4096;
+  // Runs one launch; every timing_sample-th launch of a class is bracketed by
+  // events on the compute stream (the stream the kernel runs on).
+  template <class F>
+  ambptt_status timed(int cls, F launch, hipStream_t strm = nullptr) {
+    if (!strm) strm = C->cs;
+    const bool sample = C->timing_sample > 0 && (calls[cls] % C->timing_sample) == 0 && samples.size() < 4096;
     Sample smp{cls, nullptr, nullptr};
     if (sample) {
-      HIPCK(hipEventCreate(&smp.a));
-      HIPCK(hipEventCreate(&smp.b));
-      HIPCK(hipEventRecord(smp.a, C->cs));
+      const size_t need = 2 * (samples.size() + 1);
+      while (C->tpool.size() < need) {
+        hipEvent_t e;
+        HIPCK(hipEventCreate(&e));
+        C->tpool.push_back(e);
+      }
+      smp.a = C->tpool[need - 2];
+      smp.b = C->tpool[need - 1];
+      HIPCK(hipEventRecord(smp.a, strm));
     }
-    HIPCK(launch_step(G, mode, L.cfg, a, C->cs));
+    HIPCK(launch());
     if (sample) {
-      HIPCK(hipEventRecord(smp.b, C->cs));
+      HIPCK(hipEventRecord(smp.b, strm));
       samples.push_back(smp);
     }
-    launches[cls]++;
+    calls[cls]++;
     st.kernel_launches++;
     return AMBPTT_OK;
   }
@@ -222,16 +246,20 @@ struct Exec {
     return a;
   }
 
+  hipError_t launch(int mode, const StepArgs& a) const {
+    return L.small ? launch_step_small(L.G, mode, a, C->cs) : launch_step(L.G, mode, L.cfg, a, C->cs);
+  }
+
   // one forward step: state at `src` -> `dst`
   ambptt_status fwd_step(int64_t t, char* src, char* dst) {
+    st.forward_evals++;
     StepArgs a = base_args();
     a.x = x + (size_t)t * p.batch * p.input;
     a.h = hpart(src);
     a.c = L.G == 4 ? cpart(src) : nullptr;
     a.h_out = hpart(dst);
     a.c_out = L.G == 4 ? cpart(dst) : nullptr;
-    st.forward_evals++;
-    return timed_launch(0, L.G, kForward, a);
+    return timed(AMBPTT_K_FWD, [&] { return launch(kForward, a); });
   }
 
   int64_t ring(int64_t t) const { return t % (2 * (int64_t)L.window); }
@@ -241,26 +269,45 @@ struct Exec {
   float* hwin_at(int64_t t) const { return (float*)(C->ws + L.off_hwin) + (size_t)ring(t) * p.batch * p.hidden; }
   float* cbar(int64_t t) const { return (float*)(C->ws + L.off_cbar[t & 1]); }
 
+  // ring half of the z-bar / h window that step t writes
+  int half_of(int64_t t) const { return int((t / L.window) & 1); }
+  bool dw_pending[2] = {false, false};
+
   ambptt_status adjoint(int64_t t, float* dW, float* db) {
     const int64_t n = p.n_steps;
+    const bool first = (t == n - 1);
+    if (first) st.forward_evals++;  // the first turn's forward step
+    st.adjoints++;
+    const int64_t w = L.window;
+    // the window half this step writes was last read by the dW launch two
+    // windows later in t; wait for it if it is still running
+    const int hf = half_of(t);
+    if (dw_pending[hf]) {
+      const hipError_t q = hipEventQuery(C->ev_dw[hf]);
+      if (q == hipErrorNotReady) {
+        HIPCK(hipStreamWaitEvent(C->cs, C->ev_dw[hf], 0));
+        st.compute_waits++;
+      } else if (q != hipSuccess) {
+        HIPCK(q);
+      }
+      dw_pending[hf] = false;
+    }
     StepArgs a = base_args();
     a.x = x + (size_t)t * p.batch * p.input;
     a.h = hpart(cur);
     a.c = L.G == 4 ? cpart(cur) : nullptr;
-    a.first = (t == n - 1);
-    a.last = (t == n - 1);
-    a.zbar_in = a.first ? nullptr : zbar_at(t + 1);
-    a.cbar_in = a.first ? nullptr : cbar(t + 1);
+    a.first = first;
+    a.last = first;
+    a.zbar_in = first ? nullptr : zbar_at(t + 1);
+    a.cbar_in = first ? nullptr : cbar(t + 1);
     a.zbar_out = zbar_at(t);
     a.cbar_out = cbar(t);
     a.hwin_out = hwin_at(t);
     a.loss_acc = (double*)(C->ws + L.off_loss);
-    if (a.first) st.forward_evals++;  // the first turn's forward step
-    st.adjoints++;
-    ambptt_status s = timed_launch(1, L.G, kAdjoint, a);
+    ambptt_status s = timed(AMBPTT_K_ADJ, [&] { return launch(kAdjoint, a); });
     if (s != AMBPTT_OK) return s;
-    const int64_t w = L.window;
-    if (t % w == 0) {  // window [t, min(t + w, n)) complete
+    live_dead = true;
+    if (t % w == 0) {  // window [t, min(t + w, n)) complete: accumulate it on the dW stream
       const int64_t cnt = std::min(w, n - t);
       DwArgs d{};
       d.zbar = zbar_at(t);
@@ -272,23 +319,24 @@ struct Exec {
       d.D = p.input;
       d.H = p.hidden;
       d.GH = L.G * p.hidden;
-      const bool sample = C->timing_sample > 0 && (launches[2] % std::max<int64_t>(1, C->timing_sample / 8)) == 0 &&
-                          samples.size() < 4096;
-      Sample smp{2, nullptr, nullptr};
-      if (sample) {
-        HIPCK(hipEventCreate(&smp.a));
-        HIPCK(hipEventCreate(&smp.b));
-        HIPCK(hipEventRecord(smp.a, C->cs));
-      }
-      HIPCK(launch_dw(d, C->cs));
-      if (sample) {
-        HIPCK(hipEventRecord(smp.b, C->cs));
-        samples.push_back(smp);
-      }
-      launches[2]++;
-      st.kernel_launches++;
+      HIPCK(hipEventRecord(C->ev_c2, C->cs));
+      HIPCK(hipStreamWaitEvent(C->ds, C->ev_c2, 0));
+      s = timed(AMBPTT_K_DW, [&] { return launch_dw(d, C->ds); }, C->ds);
+      if (s != AMBPTT_OK) return s;
+      HIPCK(hipEventRecord(C->ev_dw[hf], C->ds));
+      dw_pending[hf] = true;
     }
     return AMBPTT_OK;
+  }
+
+  // dL/dx_0 = (zbar_0 W_h, cbar_0)
+  ambptt_status final_step(float* dh0, float* dc0) {
+    StepArgs a = base_args();
+    a.zbar_in = zbar_at(0);
+    a.cbar_in = cbar(0);
+    a.dh0 = dh0;
+    a.dc0 = dc0;
+    return timed(AMBPTT_K_OTHER, [&] { return launch(kFinal, a); });
   }
 
   ambptt_status copy_state(char* dst, char* src) {
@@ -339,6 +387,7 @@ struct Exec {
             st.takeshots++;
             ++i;
           }
+          live_dead = false;
           break;
         }
         case Op::Snap: {
@@ -357,6 +406,7 @@ struct Exec {
           st.restores++;
           if ((s = wait_slot(A.a, false)) != AMBPTT_OK) return s;
           set_cur_slot(A.a);
+          live_dead = false;
           break;
         }
         case Op::First:
@@ -381,7 +431,7 @@ struct Exec {
             st.prefetches_elided++;
             break;
           }
-          if (cur_slot == k) {  // the live state aliases the target: keep it
+          if (cur_slot == k && !live_dead) {  // the live state aliases the target: keep it
             char* dst = live(0);
             if ((s = copy_state(dst, cur)) != AMBPTT_OK) return s;
             set_cur_live(dst);
@@ -501,6 +551,10 @@ ambptt_status ambptt_create(const ambptt_problem* p, void* stream, ambptt_ctx** 
   if ((e = hipGetDevice(&C->device)) != hipSuccess) return bail("hipGetDevice", e);
   if ((e = hipStreamCreateWithFlags(&C->xs, hipStreamNonBlocking)) != hipSuccess) return bail("hipStreamCreate", e);
   if ((e = hipEventCreateWithFlags(&C->ev_c, hipEventDisableTiming)) != hipSuccess) return bail("hipEventCreate", e);
+  if ((e = hipStreamCreateWithFlags(&C->ds, hipStreamNonBlocking)) != hipSuccess) return bail("hipStreamCreate", e);
+  if ((e = hipEventCreateWithFlags(&C->ev_c2, hipEventDisableTiming)) != hipSuccess) return bail("hipEventCreate", e);
+  for (auto& ev : C->ev_dw)
+    if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess) return bail("hipEventCreate", e);
   C->ev_slot.resize(size_t(p->fast_slots), nullptr);
   C->pend.assign(size_t(p->fast_slots), kNone);
   for (auto& ev : C->ev_slot)
@@ -638,16 +692,8 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   HIPCK(launch_fill32(C->ws + L.off_loss, (size_t)L.loss_slots * 2, 0u, C->cs));
   if ((s = prepare_inputs(C, (const float*)W, h0, c0, E)) != AMBPTT_OK) return s;
   if ((s = E.run(plan, dW, db)) != AMBPTT_OK) return s;
-  // dL/dx_0 = (zbar_0 W_h, cbar_0)
-  {
-    StepArgs a = E.base_args();
-    a.zbar_in = E.zbar_at(0);
-    a.cbar_in = E.cbar(0);
-    a.dh0 = dh0;
-    a.dc0 = dc0;
-    HIPCK(launch_step(L.G, kFinal, L.cfg, a, C->cs));
-    E.st.kernel_launches++;
-  }
+  if ((s = E.final_step(dh0, dc0)) != AMBPTT_OK) return s;
+  const double t_enq = now_us();
   double scale = 1.0;
   if (p.loss == AMBPTT_LOSS_HALF_SQ_LAST) scale = 0.5;
   else scale = 1.0 / ((double)p.batch * p.hidden);
@@ -655,19 +701,18 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   HIPCK(launch_loss_sum((const double*)(C->ws + L.off_loss), L.loss_slots, scale, dloss, C->cs));
   HIPCK(hipMemcpyAsync(C->host_loss, dloss, sizeof(double), hipMemcpyDeviceToHost, C->cs));
   HIPCK(hipStreamSynchronize(C->cs));
+  HIPCK(hipStreamSynchronize(C->ds));
   HIPCK(hipStreamSynchronize(C->xs));
   const double t2 = now_us();
   if (loss) *loss = *C->host_loss;
   ambptt_stats& st = E.st;
-  double sum[3] = {0, 0, 0};
-  int64_t cnt[3] = {0, 0, 0};
+  double sum[6] = {0, 0, 0, 0, 0, 0};
+  int64_t cnt[6] = {0, 0, 0, 0, 0, 0};
   for (auto& smp : E.samples) {
     float ms = 0.f;
     HIPCK(hipEventElapsedTime(&ms, smp.a, smp.b));
     sum[smp.cls] += 1000.0 * ms;
     cnt[smp.cls]++;
-    (void)hipEventDestroy(smp.a);
-    (void)hipEventDestroy(smp.b);
   }
   if (stats) {
     st.mode = plan.async ? 1 : 0;
@@ -678,12 +723,12 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
     st.recompute_factor = double(st.forward_evals) / double(p.n_steps);
     st.schedule_us = t1 - t0;
     st.run_us = t2 - t1;
-    st.fwd_kernel_us = cnt[0] ? sum[0] / cnt[0] : 0.0;
-    st.adj_kernel_us = cnt[1] ? sum[1] / cnt[1] : 0.0;
-    st.dw_kernel_us = cnt[2] ? sum[2] / cnt[2] : 0.0;
-    st.fwd_samples = cnt[0];
-    st.adj_samples = cnt[1];
-    st.dw_samples = cnt[2];
+    st.enqueue_us = t_enq - t1;
+    for (int k = 0; k < 6; ++k) {
+      st.kernel_us[k] = cnt[k] ? sum[k] / cnt[k] : 0.0;
+      st.kernel_samples[k] = cnt[k];
+      st.kernel_calls[k] = E.calls[k];
+    }
     *stats = st;
   }
   if (st.forward_evals != plan.evals)
@@ -698,6 +743,12 @@ void ambptt_destroy(ambptt_ctx* C) {
   for (auto& ev : C->ev_slot)
     if (ev) (void)hipEventDestroy(ev);
   if (C->ev_c) (void)hipEventDestroy(C->ev_c);
+  for (auto& ev : C->tpool) (void)hipEventDestroy(ev);
+  if (C->ds) (void)hipStreamSynchronize(C->ds);
+  for (auto& ev : C->ev_dw)
+    if (ev) (void)hipEventDestroy(ev);
+  if (C->ev_c2) (void)hipEventDestroy(C->ev_c2);
+  if (C->ds) (void)hipStreamDestroy(C->ds);
   if (C->xs) (void)hipStreamDestroy(C->xs);
   if (C->host) (void)hipHostFree(C->host);
   if (C->host_loss) (void)hipHostFree(C->host_loss);

@@ -94,3 +94,15 @@ def test_query_sizes_and_validation(amb):
     with pytest.raises(AmbpttError) as e:
         query(ProblemSpec(**{**spec.__dict__, "hidden": 500}))
     assert e.value.status == -4
+
+
+def test_stats_struct_layout(amb):
+    from paper_1806_01117_amd import _lib
+    st = _lib.Stats()
+    st.kernel_launches = 7
+    st.kernel_us[2] = 1.5
+    d = st.as_dict()
+    assert d["kernel_launches"] == 7 and d["kernel_us"][2] == 1.5 and len(d["kernel_calls"]) == 6
+    # int32 x4, int64 x14, double x4, double x6, int64 x12
+    assert ctypes.sizeof(_lib.Stats) == 16 + 14 * 8 + 4 * 8 + 6 * 8 + 12 * 8
+    assert ctypes.sizeof(_lib.Problem) == 48
