@@ -130,9 +130,9 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
   if (MODE != kFinal) {
     const int nch = K1 / 16;
     const int c0 = (nch * wave) / KS, c1 = (nch * (wave + 1)) / KS;
-    const float* x = a.x;
-    const float* h = a.h;
-    const float* W = a.W;
+    const float* x = (const float*)a.x;
+    const float* h = (const float*)a.h;
+    const float* W = (const float*)a.W;
     auto la = [&](int ch, int i) -> f4 {
       const int k = ch * 16 + 4 * q;
       const float* p = (ch * 16 < D) ? x + (size_t)rows[i] * D + k : h + (size_t)rows[i] * H + (k - D);
@@ -150,8 +150,8 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
   if (do_hbar) {
     const int nch = GH / 16;
     const int c0 = (nch * wave) / KS, c1 = (nch * (wave + 1)) / KS;
-    const float* zb = a.zbar_in;
-    const float* wt = a.WhT;
+    const float* zb = (const float*)a.zbar_in;
+    const float* wt = (const float*)a.WhT;
     auto la = [&](int ch, int i) -> f4 { return *(const f4*)(zb + (size_t)rows[i] * GH + ch * 16 + 4 * q); };
     auto lb = [&](int ch, int jj) -> f4 {
       return *(const f4*)(wt + (size_t)(j0 + 16 * jj + r) * GH + ch * 16 + 4 * q);
@@ -224,7 +224,7 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
           h1 = tanhf(acc[i][nb][v] + a.bias[j]);
         }
         if (MODE == kForward) {
-          a.h_out[o] = h1;
+          ((float*)a.h_out)[o] = h1;
           if (G == 4) a.c_out[o] = c1;
           continue;
         }
@@ -243,7 +243,7 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
           }
         }
         const float hb = (a.first ? 0.f : acch[i][jj][v]) + sd;
-        float* zo = a.zbar_out + (size_t)m * GH + j;
+        float* zo = (float*)a.zbar_out + (size_t)m * GH + j;
         if (G == 4) {
           const float cb = a.first ? 0.f : a.cbar_in[o];
           const float ob = hb * tc;
@@ -256,7 +256,7 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
         } else {
           zo[0] = hb * (1.f - h1 * h1);
         }
-        a.hwin_out[o] = a.h[o];
+        ((float*)a.hwin_out)[o] = ((const float*)a.h)[o];
       }
   if (MODE == kAdjoint) {
     const float s = wave_sum(lterm);
@@ -291,10 +291,10 @@ __global__ __launch_bounds__(256) void dw_lds_f32(DwArgs a) {
   const int lrow = tid >> 4, lcol = 4 * (tid & 15);
   const int c = c0 + lcol;
   const bool cok = c < N;
-  const float* xsrc = c < D ? a.x + c : a.hwin + (min(c, N - 1) - D);
+  const float* xsrc = c < D ? (const float*)a.x + c : (const float*)a.hwin + (min(c, N - 1) - D);
   const int xld = c < D ? D : H;
   const bool kok = k0 + lcol < GH;  // GH % 16 == 0: a float4 is wholly in or out
-  const float* zsrc = a.zbar + min(k0 + lcol, GH - 4);
+  const float* zsrc = (const float*)a.zbar + min(k0 + lcol, GH - 4);
   f4 zr[4], xr[4];
   auto load = [&](int st) {
 #pragma unroll
@@ -385,13 +385,13 @@ __global__ void loss_sum(const double* acc, int n, double scale, double* out) {
 }
 
 template <int G, int MODE>
-hipError_t launch_g(const StepCfg& c, const StepArgs& a, hipStream_t s) {
+hipError_t launch_g(const StepCfg& c, const StepArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   dim3 grid, block;
   step_grid(c, a.B, a.H, &grid, &block);
-#define AMB_CASE(RM_, RJ_, KS_)                                                     \
-  if (c.rm == RM_ && c.rj == RJ_ && c.ks == KS_) {                                  \
-    hipLaunchKernelGGL((step_f32<G, RM_, RJ_, KS_, MODE>), grid, block, 0, s, a); \
-    return hipGetLastError();                                                       \
+#define AMB_CASE(RM_, RJ_, KS_)                                                                   \
+  if (c.rm == RM_ && c.rj == RJ_ && c.ks == KS_) {                                                \
+    hipExtLaunchKernelGGL((step_f32<G, RM_, RJ_, KS_, MODE>), grid, block, 0, s, e0, e1, 0, a); \
+    return hipGetLastError();                                                                     \
   }
   AMB_CASE(1, 1, 1)
   AMB_CASE(1, 1, 2)
@@ -429,22 +429,23 @@ void step_grid(const StepCfg& c, int B, int H, dim3* grid, dim3* block) {
   *block = dim3(64 * c.ks, 1, 1);
 }
 
-hipError_t launch_step(int G, int mode, const StepCfg& c, const StepArgs& a, hipStream_t s) {
+hipError_t launch_step(int G, int mode, const StepCfg& c, const StepArgs& a, hipStream_t s, hipEvent_t e0,
+                       hipEvent_t e1) {
   if (G == 4) {
-    if (mode == kForward) return launch_g<4, kForward>(c, a, s);
-    if (mode == kAdjoint) return launch_g<4, kAdjoint>(c, a, s);
-    return launch_g<4, kFinal>(c, a, s);
+    if (mode == kForward) return launch_g<4, kForward>(c, a, s, e0, e1);
+    if (mode == kAdjoint) return launch_g<4, kAdjoint>(c, a, s, e0, e1);
+    return launch_g<4, kFinal>(c, a, s, e0, e1);
   }
-  if (mode == kForward) return launch_g<1, kForward>(c, a, s);
-  if (mode == kAdjoint) return launch_g<1, kAdjoint>(c, a, s);
-  return launch_g<1, kFinal>(c, a, s);
+  if (mode == kForward) return launch_g<1, kForward>(c, a, s, e0, e1);
+  if (mode == kAdjoint) return launch_g<1, kAdjoint>(c, a, s, e0, e1);
+  return launch_g<1, kFinal>(c, a, s, e0, e1);
 }
 
-hipError_t launch_dw(const DwArgs& a, hipStream_t s) {
+hipError_t launch_dw(const DwArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (a.GH % 16 != 0) return hipErrorInvalidValue;
   const int N = a.D + a.H;
   dim3 grid((a.GH + kDwT - 1) / kDwT, (N + kDwT - 1) / kDwT);
-  hipLaunchKernelGGL(dw_lds_f32, grid, dim3(256), 0, s, a);
+  hipExtLaunchKernelGGL(dw_lds_f32, grid, dim3(256), 0, s, e0, e1, 0, a);
   return hipGetLastError();
 }
 hipError_t launch_transpose_wh(const float* W, float* WhT, int GH, int D, int H, hipStream_t s) {

@@ -3,6 +3,7 @@
 // live in the .hip files.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstddef>
@@ -10,22 +11,24 @@
 
 namespace ambptt {
 
-// Arguments of one step kernel (fp32 operands).  G = 1 (tanh RNN) or 4
-// (LSTM, gate blocks i, f, g, o).  Layouts are row-major with batch rows.
+// Arguments of one step kernel.  G = 1 (tanh RNN) or 4 (LSTM, gate blocks
+// i, f, g, o).  Layouts are row-major with batch rows.  "op" pointers hold the
+// operand dtype (fp32 or bf16); the cell state, its adjoint, biases and
+// gradients are fp32.
 struct StepArgs {
-  const float* x;        // x_t [B][D]
-  const float* h;        // h_t [B][H]
+  const void* x;         // op: x_t [B][D]
+  const void* h;         // op: h_t [B][H]
   const float* c;        // c_t [B][H] (LSTM)
-  float* h_out;          // forward: h_{t+1} [B][H]
+  void* h_out;           // op: forward: h_{t+1} [B][H]
   float* c_out;          // forward: c_{t+1} [B][H] (LSTM)
-  const float* W;        // [G*H][D+H]
+  const void* W;         // op: [G*H][D+H]
   const float* bias;     // [G*H]
-  const float* WhT;      // [H][G*H]: WhT[j][k] = W[k][D+j]
-  const float* zbar_in;  // adjoint: zbar_{t+1} [B][G*H] (unused when first)
+  const void* WhT;       // op: [H][G*H]: WhT[j][k] = W[k][D+j]
+  const void* zbar_in;   // op: adjoint: zbar_{t+1} [B][G*H] (unused when first)
   const float* cbar_in;  // adjoint: cbar_{t+1} [B][H] (LSTM; unused when first)
-  float* zbar_out;       // adjoint: zbar_t [B][G*H]
+  void* zbar_out;        // op: adjoint: zbar_t [B][G*H]
   float* cbar_out;       // adjoint: cbar_t [B][H] (LSTM)
-  float* hwin_out;       // adjoint: copy of h_t for the weight-gradient window
+  void* hwin_out;        // op: adjoint: copy of h_t for the weight-gradient window
   double* loss_acc;      // adjoint: one accumulator per workgroup
   float* dh0;            // final: dL/dh_0 [B][H]
   float* dc0;            // final: dL/dc_0 [B][H] (LSTM)
@@ -39,11 +42,11 @@ struct StepArgs {
 // Weight-gradient window: dW[k][c] += sum_r Z[r][k] X[r][c], db[k] += sum_r Z[r][k],
 // where X[r] = [x row | h row] for the R = w*B rows of w consecutive steps.
 struct DwArgs {
-  const float* zbar;  // [R][G*H]
-  const float* x;     // [R][D]
-  const float* hwin;  // [R][H]
-  float* dW;          // [G*H][D+H]
-  float* db;          // [G*H]
+  const void* zbar;  // op: [R][G*H]
+  const void* x;     // op: [R][D]
+  const void* hwin;  // op: [R][H]
+  float* dW;         // [G*H][D+H]
+  float* db;         // [G*H]
   int R, D, H, GH;
 };
 
@@ -55,11 +58,17 @@ struct StepCfg {
 
 StepCfg pick_step_cfg(int G, int B, int D, int H);
 void step_grid(const StepCfg& cfg, int B, int H, dim3* grid, dim3* block);
-hipError_t launch_step(int G, int mode, const StepCfg& cfg, const StepArgs& a, hipStream_t s);
-hipError_t launch_dw(const DwArgs& a, hipStream_t s);
+// Launchers take an optional pair of events that the dispatch itself records
+// at kernel start and end (hipExtLaunchKernel); pass nullptr for none.
+hipError_t launch_step(int G, int mode, const StepCfg& cfg, const StepArgs& a, hipStream_t s,
+                       hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+hipError_t launch_dw(const DwArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 // Small-batch path: one launch per step, 16 rows x (8 LSTM | 16 RNN) units per workgroup.
 void step_small_grid(int G, int B, int H, dim3* grid, dim3* block);
-hipError_t launch_step_small(int G, int mode, const StepArgs& a, hipStream_t s);
+hipError_t launch_step_small(int G, int bf16, int mode, const StepArgs& a, hipStream_t s,
+                             hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+hipError_t launch_dw_bf16(const DwArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+hipError_t launch_transpose_wh_bf16(const void* W, void* WhT, int GH, int D, int H, hipStream_t s);
 hipError_t launch_transpose_wh(const float* W, float* WhT, int GH, int D, int H, hipStream_t s);
 hipError_t launch_fill32(void* p, size_t words, uint32_t value, hipStream_t s);
 hipError_t launch_loss_sum(const double* acc, int n, double scale, double* out, hipStream_t s);

@@ -79,8 +79,9 @@ ambptt_status validate(const ambptt_problem* p) {
   if (p->interval_min < 0) return fail(AMBPTT_EINVAL, "interval_min must be >= 0");
   if (p->hidden % 16 || p->input % 16)
     return fail(AMBPTT_EUNSUPPORTED, "hidden and input sizes must be multiples of 16");
+  if (p->dtype == AMBPTT_BF16 && (p->hidden % 32 || p->input % 32))
+    return fail(AMBPTT_EUNSUPPORTED, "bf16 operands need hidden and input sizes that are multiples of 32");
   if (p->cell == AMBPTT_CELL_RESMLP) return fail(AMBPTT_EUNSUPPORTED, "residual MLP cell not built yet");
-  if (p->dtype == AMBPTT_BF16) return fail(AMBPTT_EUNSUPPORTED, "bf16 operands not built yet");
   if ((int64_t)p->batch * p->hidden > (int64_t(1) << 31)) return fail(AMBPTT_EUNSUPPORTED, "state too large");
   return AMBPTT_OK;
 }
@@ -108,7 +109,7 @@ Layout make_layout(const ambptt_problem* p, int window) {
   // Problems with fewer than 1024 tiles of 16 rows x 16 units run the
   // small-batch kernels, which spread even a 64-row batch over all CUs.
   const long tiles = (long)((p->batch + 15) / 16) * (p->hidden / 16);
-  L.small = tiles < 1024;
+  L.small = tiles < 1024 || p->dtype == AMBPTT_BF16;
   if (L.small) {
     step_small_grid(L.G, p->batch, p->hidden, &grid, &block);
     L.loss_slots = int(grid.x * grid.y);
@@ -117,8 +118,8 @@ Layout make_layout(const ambptt_problem* p, int window) {
   L.off_live[0] = o; o += L.stride;
   L.off_live[1] = o; o += L.stride;
   L.off_wht = o; o += align_up((size_t)p->hidden * GH * L.dsize);
-  L.off_zbar = o; o += align_up(2 * (size_t)L.window * p->batch * GH * 4);
-  L.off_hwin = o; o += align_up(2 * (size_t)L.window * BH * 4);
+  L.off_zbar = o; o += align_up(2 * (size_t)L.window * p->batch * GH * L.dsize);
+  L.off_hwin = o; o += align_up(2 * (size_t)L.window * BH * L.dsize);
   L.off_cbar[0] = o; o += align_up(BH * 4);
   L.off_cbar[1] = o; o += align_up(BH * 4);
   L.off_loss = o; o += align_up((size_t)L.loss_slots * 8);
@@ -166,10 +167,10 @@ struct Exec {
   ambptt_ctx* C;
   const Layout& L;
   const ambptt_problem& p;
-  const float* x;
-  const float* W;
+  const char* x;   // operand dtype, [n][B][D]
+  const void* W;
   const float* b;
-  float* WhT;
+  void* WhT;
   ambptt_stats st{};
   char* cur = nullptr;
   int cur_slot = -1;  // slot index the live state aliases, or -1
@@ -179,14 +180,15 @@ struct Exec {
   std::vector<Sample> samples;
   bool live_dead = false;  // the live state was consumed by an adjoint step
 
-  Exec(ambptt_ctx* c, const float* x_, const float* W_, const float* b_)
-      : C(c), L(c->L), p(c->p), x(x_), W(W_), b(b_), slot_t(size_t(c->p.fast_slots), -1) {
-    WhT = (float*)(C->ws + L.off_wht);
+  Exec(ambptt_ctx* c, const void* x_, const void* W_, const float* b_)
+      : C(c), L(c->L), p(c->p), x((const char*)x_), W(W_), b(b_), slot_t(size_t(c->p.fast_slots), -1) {
+    WhT = C->ws + L.off_wht;
   }
+  const void* x_at(int64_t t) const { return x + (size_t)t * p.batch * p.input * L.dsize; }
 
   char* slot(int64_t k) const { return C->pool + (size_t)k * L.stride; }
   char* live(int i) const { return C->ws + L.off_live[i]; }
-  float* hpart(char* s) const { return (float*)s; }
+  void* hpart(char* s) const { return s; }
   float* cpart(char* s) const { return (float*)(s + align_up(L.h_bytes)); }
 
   ambptt_status wait_slot(int64_t k, bool for_write) {
@@ -207,6 +209,10 @@ struct Exec {
 
   // Runs one launch; every timing_sample-th launch of a class is bracketed by
   // events on the compute stream (the stream the kernel runs on).
+  // Runs one launch; every timing_sample-th launch of a class is bracketed by a
+  // pair of events recorded on the stream the kernel runs on.  The interval
+  // includes the kernel's dispatch latency (a few microseconds on top of the
+  // execution time a kernel trace reports).
   template <class F>
   ambptt_status timed(int cls, F launch, hipStream_t strm = nullptr) {
     if (!strm) strm = C->cs;
@@ -223,7 +229,7 @@ struct Exec {
       smp.b = C->tpool[need - 1];
       HIPCK(hipEventRecord(smp.a, strm));
     }
-    HIPCK(launch());
+    HIPCK(launch(nullptr, nullptr));
     if (sample) {
       HIPCK(hipEventRecord(smp.b, strm));
       samples.push_back(smp);
@@ -246,27 +252,28 @@ struct Exec {
     return a;
   }
 
-  hipError_t launch(int mode, const StepArgs& a) const {
-    return L.small ? launch_step_small(L.G, mode, a, C->cs) : launch_step(L.G, mode, L.cfg, a, C->cs);
+  hipError_t launch(int mode, const StepArgs& a, hipEvent_t e0, hipEvent_t e1) const {
+    return L.small ? launch_step_small(L.G, p.dtype == AMBPTT_BF16, mode, a, C->cs, e0, e1)
+                   : launch_step(L.G, mode, L.cfg, a, C->cs, e0, e1);
   }
 
   // one forward step: state at `src` -> `dst`
   ambptt_status fwd_step(int64_t t, char* src, char* dst) {
     st.forward_evals++;
     StepArgs a = base_args();
-    a.x = x + (size_t)t * p.batch * p.input;
+    a.x = x_at(t);
     a.h = hpart(src);
     a.c = L.G == 4 ? cpart(src) : nullptr;
     a.h_out = hpart(dst);
     a.c_out = L.G == 4 ? cpart(dst) : nullptr;
-    return timed(AMBPTT_K_FWD, [&] { return launch(kForward, a); });
+    return timed(AMBPTT_K_FWD, [&](hipEvent_t e0, hipEvent_t e1) { return launch(kForward, a, e0, e1); });
   }
 
   int64_t ring(int64_t t) const { return t % (2 * (int64_t)L.window); }
-  float* zbar_at(int64_t t) const {
-    return (float*)(C->ws + L.off_zbar) + (size_t)ring(t) * p.batch * L.G * p.hidden;
+  void* zbar_at(int64_t t) const {
+    return C->ws + L.off_zbar + (size_t)ring(t) * p.batch * L.G * p.hidden * L.dsize;
   }
-  float* hwin_at(int64_t t) const { return (float*)(C->ws + L.off_hwin) + (size_t)ring(t) * p.batch * p.hidden; }
+  void* hwin_at(int64_t t) const { return C->ws + L.off_hwin + (size_t)ring(t) * p.batch * p.hidden * L.dsize; }
   float* cbar(int64_t t) const { return (float*)(C->ws + L.off_cbar[t & 1]); }
 
   // ring half of the z-bar / h window that step t writes
@@ -293,7 +300,7 @@ struct Exec {
       dw_pending[hf] = false;
     }
     StepArgs a = base_args();
-    a.x = x + (size_t)t * p.batch * p.input;
+    a.x = x_at(t);
     a.h = hpart(cur);
     a.c = L.G == 4 ? cpart(cur) : nullptr;
     a.first = first;
@@ -304,14 +311,15 @@ struct Exec {
     a.cbar_out = cbar(t);
     a.hwin_out = hwin_at(t);
     a.loss_acc = (double*)(C->ws + L.off_loss);
-    ambptt_status s = timed(AMBPTT_K_ADJ, [&] { return launch(kAdjoint, a); });
+    ambptt_status s =
+        timed(AMBPTT_K_ADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch(kAdjoint, a, e0, e1); });
     if (s != AMBPTT_OK) return s;
     live_dead = true;
     if (t % w == 0) {  // window [t, min(t + w, n)) complete: accumulate it on the dW stream
       const int64_t cnt = std::min(w, n - t);
       DwArgs d{};
       d.zbar = zbar_at(t);
-      d.x = x + (size_t)t * p.batch * p.input;
+      d.x = x_at(t);
       d.hwin = hwin_at(t);
       d.dW = dW;
       d.db = db;
@@ -321,7 +329,12 @@ struct Exec {
       d.GH = L.G * p.hidden;
       HIPCK(hipEventRecord(C->ev_c2, C->cs));
       HIPCK(hipStreamWaitEvent(C->ds, C->ev_c2, 0));
-      s = timed(AMBPTT_K_DW, [&] { return launch_dw(d, C->ds); }, C->ds);
+      s = timed(
+          AMBPTT_K_DW,
+          [&](hipEvent_t e0, hipEvent_t e1) {
+            return p.dtype == AMBPTT_BF16 ? launch_dw_bf16(d, C->ds, e0, e1) : launch_dw(d, C->ds, e0, e1);
+          },
+          C->ds);
       if (s != AMBPTT_OK) return s;
       HIPCK(hipEventRecord(C->ev_dw[hf], C->ds));
       dw_pending[hf] = true;
@@ -336,7 +349,7 @@ struct Exec {
     a.cbar_in = cbar(0);
     a.dh0 = dh0;
     a.dc0 = dc0;
-    return timed(AMBPTT_K_OTHER, [&] { return launch(kFinal, a); });
+    return timed(AMBPTT_K_OTHER, [&](hipEvent_t e0, hipEvent_t e1) { return launch(kFinal, a, e0, e1); });
   }
 
   ambptt_status copy_state(char* dst, char* src) {
@@ -469,10 +482,13 @@ ambptt_status ensure_host(ambptt_ctx* C, size_t bytes) {
   return AMBPTT_OK;
 }
 
-ambptt_status prepare_inputs(ambptt_ctx* C, const float* W, const void* h0, const float* c0, Exec& E) {
+ambptt_status prepare_inputs(ambptt_ctx* C, const void* W, const void* h0, const float* c0, Exec& E) {
   const Layout& L = C->L;
   const ambptt_problem& p = C->p;
-  HIPCK(launch_transpose_wh(W, E.WhT, L.G * p.hidden, p.input, p.hidden, C->cs));
+  if (p.dtype == AMBPTT_BF16)
+    HIPCK(launch_transpose_wh_bf16(W, E.WhT, L.G * p.hidden, p.input, p.hidden, C->cs));
+  else
+    HIPCK(launch_transpose_wh((const float*)W, (float*)E.WhT, L.G * p.hidden, p.input, p.hidden, C->cs));
   // live state <- x_0
   char* l0 = E.live(0);
   HIPCK(hipMemcpyAsync(l0, h0, L.h_bytes, hipMemcpyDeviceToDevice, C->cs));
@@ -615,8 +631,8 @@ ambptt_status ambptt_calibrate(ambptt_ctx* C, const void* x_seq, const void* W, 
                                const float* c0, int32_t* interval_min_out, double* t_a_us, double* t_t_us) {
   ambptt_status s = check_run_args(C, x_seq, W, b, h0, c0);
   if (s != AMBPTT_OK) return s;
-  Exec E(C, (const float*)x_seq, (const float*)W, b);
-  if ((s = prepare_inputs(C, (const float*)W, h0, c0, E)) != AMBPTT_OK) return s;
+  Exec E(C, x_seq, W, b);
+  if ((s = prepare_inputs(C, W, h0, c0, E)) != AMBPTT_OK) return s;
   if ((s = ensure_host(C, C->L.stride)) != AMBPTT_OK) return s;
   hipEvent_t e0, e1;
   HIPCK(hipEventCreate(&e0));
@@ -684,13 +700,13 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   if (plan.async) {
     if ((s = ensure_host(C, (size_t)plan.host_slots_used * L.stride)) != AMBPTT_OK) return s;
   }
-  Exec E(C, (const float*)x_seq, (const float*)W, b);
+  Exec E(C, x_seq, W, b);
   std::fill(C->pend.begin(), C->pend.end(), kNone);
   const size_t GH = (size_t)L.G * p.hidden;
   HIPCK(launch_fill32(dW, GH * (p.input + p.hidden), 0u, C->cs));
   HIPCK(launch_fill32(db, GH, 0u, C->cs));
   HIPCK(launch_fill32(C->ws + L.off_loss, (size_t)L.loss_slots * 2, 0u, C->cs));
-  if ((s = prepare_inputs(C, (const float*)W, h0, c0, E)) != AMBPTT_OK) return s;
+  if ((s = prepare_inputs(C, W, h0, c0, E)) != AMBPTT_OK) return s;
   if ((s = E.run(plan, dW, db)) != AMBPTT_OK) return s;
   if ((s = E.final_step(dh0, dc0)) != AMBPTT_OK) return s;
   const double t_enq = now_us();

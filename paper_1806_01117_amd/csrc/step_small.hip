@@ -18,19 +18,23 @@
 // its (rows, units) tile, the one product that needs the previous launch's
 // output; W_h is read through its transpose WhT[j][k] = W[k][D+j] so both
 // products are row-contiguous in the reduction index.
+//
+// Operands are fp32 (v_mfma_f32_16x16x4_f32, chunks of 16 reduction indices,
+// 4 per lane) or bf16 (v_mfma_f32_16x16x32_bf16, chunks of 32, 8 per lane):
+// either way a lane loads 16 bytes per operand row per chunk.  With bf16 the
+// stored h, the copy of h_t for the weight gradient and zbar (the adjoint
+// GEMMs' operand) are rounded to bf16 (nearest even); accumulation, the cell
+// state and its adjoint stay fp32.
 #include <hip/hip_runtime.h>
 
 #include "ambptt.h"
 #include "kernels.hpp"
+#include "mfma.hpp"
 
 namespace ambptt {
 namespace {
 
-typedef float f4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-}
+__device__ __forceinline__ f4 mfma4(float a, float b, f4 c) { return mfma_f32_16x16x4(a, b, c); }
 
 __device__ __forceinline__ float sigm(float z) { return 1.0f / (1.0f + __expf(-z)); }
 
@@ -40,15 +44,42 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+template <class T>
+struct Op;
+template <>
+struct Op<float> {
+  using V = f4;
+  static constexpr int CW = 16;  // reduction indices per chunk
+  static __device__ __forceinline__ f4 mma(const V& a, const V& b, f4 c) {
+    c = mfma4(a.x, b.x, c);
+    c = mfma4(a.y, b.y, c);
+    c = mfma4(a.z, b.z, c);
+    return mfma4(a.w, b.w, c);
+  }
+  static __device__ __forceinline__ float store(float v) { return v; }
+  static __device__ __forceinline__ float load(float v) { return v; }
+};
+template <>
+struct Op<__bf16> {
+  using V = bf16x8;
+  static constexpr int CW = 32;
+  static __device__ __forceinline__ f4 mma(const V& a, const V& b, f4 c) {
+    return mfma_bf16_16x16x32(a, b, c);
+  }
+  static __device__ __forceinline__ __bf16 store(float v) { return (__bf16)v; }  // nearest even
+  static __device__ __forceinline__ float load(__bf16 v) { return (float)v; }
+};
+
 constexpr int kWaves = 8;
 constexpr int kU = 4;  // chunks per prefetch group
 
 // acc[nb] += sum over chunks [c0, c1) of a(ch) . b(ch, nb); loads run one group
 // of kU chunks ahead of the MFMAs.
-template <int NB, class LA, class LB>
+template <class T, int NB, class LA, class LB>
 __device__ __forceinline__ void chunks(int c0, int c1, f4 (&acc)[NB], LA la, LB lb) {
+  using V = typename Op<T>::V;
   if (c0 >= c1) return;
-  f4 a[kU], b[kU][NB];
+  V a[kU], b[kU][NB];
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
     const int ch = min(c0 + u, c1 - 1);
@@ -57,7 +88,7 @@ __device__ __forceinline__ void chunks(int c0, int c1, f4 (&acc)[NB], LA la, LB 
     for (int nb = 0; nb < NB; ++nb) b[u][nb] = lb(ch, nb);
   }
   for (int g = c0; g < c1; g += kU) {
-    f4 an[kU], bn[kU][NB];
+    V an[kU], bn[kU][NB];
     const bool more = g + kU < c1;
     if (more) {
 #pragma unroll
@@ -72,12 +103,7 @@ __device__ __forceinline__ void chunks(int c0, int c1, f4 (&acc)[NB], LA la, LB 
     for (int u = 0; u < kU; ++u) {
       if (g + u < c1) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          acc[nb] = mfma4(a[u].x, b[u][nb].x, acc[nb]);
-          acc[nb] = mfma4(a[u].y, b[u][nb].y, acc[nb]);
-          acc[nb] = mfma4(a[u].z, b[u][nb].z, acc[nb]);
-          acc[nb] = mfma4(a[u].w, b[u][nb].w, acc[nb]);
-        }
+        for (int nb = 0; nb < NB; ++nb) acc[nb] = Op<T>::mma(a[u], b[u][nb], acc[nb]);
       }
     }
     if (more) {
@@ -91,8 +117,11 @@ __device__ __forceinline__ void chunks(int c0, int c1, f4 (&acc)[NB], LA la, LB 
   }
 }
 
-template <int G, int MODE>
-__global__ __launch_bounds__(64 * kWaves) void step_small_f32(StepArgs a) {
+template <class T, int G, int MODE>
+__global__ __launch_bounds__(64 * kWaves) void step_small(StepArgs a) {
+  using V = typename Op<T>::V;
+  constexpr int CW = Op<T>::CW;
+  constexpr int LE = CW / 4;  // elements per lane per chunk (16 bytes)
   constexpr int U = (G == 4) ? 8 : 16;  // units per workgroup
   constexpr int NC = G * U;             // gate columns (32 or 16)
   constexpr int NB = NC / 16;           // MFMA column blocks
@@ -119,22 +148,22 @@ __global__ __launch_bounds__(64 * kWaves) void step_small_f32(StepArgs a) {
     f4 acc[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[nb] = f4{0.f, 0.f, 0.f, 0.f};
-    const int nch = K1 / 16;
+    const int nch = K1 / CW;
     const int c0 = (nch * wave) / kWaves, c1 = (nch * (wave + 1)) / kWaves;
-    const float* xr = a.x + (size_t)row * D;
-    const float* hr = a.h + (size_t)row * H;
-    const float* wr[NB];
+    const T* xr = (const T*)a.x + (size_t)row * D;
+    const T* hr = (const T*)a.h + (size_t)row * H;
+    const T* wr[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const int n = nb * 16 + r;  // column of this lane in block nb
-      wr[nb] = a.W + (size_t)((n / U) * H + j0 + (n % U)) * K1;
+      wr[nb] = (const T*)a.W + (size_t)((n / U) * H + j0 + (n % U)) * K1;
     }
-    chunks<NB>(c0, c1, acc,
-               [&](int ch) -> f4 {
-                 const int k = ch * 16 + 4 * q;
-                 return *(const f4*)(ch * 16 < D ? xr + k : hr + (k - D));
-               },
-               [&](int ch, int nb) -> f4 { return *(const f4*)(wr[nb] + ch * 16 + 4 * q); });
+    chunks<T, NB>(c0, c1, acc,
+                  [&](int ch) -> V {
+                    const int k = ch * CW + LE * q;
+                    return *(const V*)(ch * CW < D ? xr + k : hr + (k - D));
+                  },
+                  [&](int ch, int nb) -> V { return *(const V*)(wr[nb] + ch * CW + LE * q); });
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
@@ -143,13 +172,13 @@ __global__ __launch_bounds__(64 * kWaves) void step_small_f32(StepArgs a) {
   const bool do_hbar = (MODE == kFinal) || (MODE == kAdjoint && !a.first);
   if (do_hbar) {
     f4 acc[1] = {f4{0.f, 0.f, 0.f, 0.f}};
-    const int nch = GH / 16;
+    const int nch = GH / CW;
     const int c0 = (nch * wave) / kWaves, c1 = (nch * (wave + 1)) / kWaves;
-    const float* zr = a.zbar_in + (size_t)row * GH;
+    const T* zr = (const T*)a.zbar_in + (size_t)row * GH;
     // U units; lanes r >= U (LSTM) repeat units so no extra rows are fetched
-    const float* wt = a.WhT + (size_t)(j0 + (r % U)) * GH;
-    chunks<1>(c0, c1, acc, [&](int ch) -> f4 { return *(const f4*)(zr + ch * 16 + 4 * q); },
-              [&](int ch, int) -> f4 { return *(const f4*)(wt + ch * 16 + 4 * q); });
+    const T* wt = (const T*)a.WhT + (size_t)(j0 + (r % U)) * GH;
+    chunks<T, 1>(c0, c1, acc, [&](int ch) -> V { return *(const V*)(zr + ch * CW + LE * q); },
+                 [&](int ch, int) -> V { return *(const V*)(wt + ch * CW + LE * q); });
 #pragma unroll
     for (int v = 0; v < 4; ++v) hs[wave][4 * q + v][r] = acc[0][v];
   }
@@ -192,38 +221,40 @@ __global__ __launch_bounds__(64 * kWaves) void step_small_f32(StepArgs a) {
         } else {
           h1 = tanhf(z[0]);
         }
+        const T h1s = Op<T>::store(h1);  // the stored state
         if (MODE == kForward) {
-          a.h_out[o] = h1;
+          ((T*)a.h_out)[o] = h1s;
           if (G == 4) a.c_out[o] = c1;
         } else {
+          const float hl = Op<T>::load(h1s);  // loss and seed read the stored h_{t+1}
           float sd = 0.f;
           if (a.loss == AMBPTT_LOSS_MEAN_SQ_ALL) {
-            sd = 2.f * h1 * a.inv_bh;
-            lterm = h1 * h1;
+            sd = 2.f * hl * a.inv_bh;
+            lterm = hl * hl;
           } else if (a.last) {
             if (a.loss == AMBPTT_LOSS_HALF_SQ_LAST) {
-              sd = h1;
-              lterm = h1 * h1;
+              sd = hl;
+              lterm = hl * hl;
             } else {
               sd = a.inv_bh;
-              lterm = h1;
+              lterm = hl;
             }
           }
           const float hb = hbar + sd;
-          float* zo = a.zbar_out + (size_t)m * GH + j;
+          T* zo = (T*)a.zbar_out + (size_t)m * GH + j;
           if (G == 4) {
             const float cb = a.first ? 0.f : a.cbar_in[o];
             const float ob = hb * tc;
             const float ch = cb + hb * og * (1.f - tc * tc);
-            zo[0] = ch * gg * ig * (1.f - ig);
-            zo[H] = ch * cold * fg * (1.f - fg);
-            zo[2 * H] = ch * ig * (1.f - gg * gg);
-            zo[3 * H] = ob * og * (1.f - og);
+            zo[0] = Op<T>::store(ch * gg * ig * (1.f - ig));
+            zo[H] = Op<T>::store(ch * cold * fg * (1.f - fg));
+            zo[2 * H] = Op<T>::store(ch * ig * (1.f - gg * gg));
+            zo[3 * H] = Op<T>::store(ob * og * (1.f - og));
             a.cbar_out[o] = ch * fg;
           } else {
-            zo[0] = hb * (1.f - h1 * h1);
+            zo[0] = Op<T>::store(hb * (1.f - h1 * h1));
           }
-          a.hwin_out[o] = a.h[o];
+          ((T*)a.hwin_out)[o] = ((const T*)a.h)[o];
         }
       }
     }
@@ -252,19 +283,27 @@ void step_small_grid(int G, int B, int H, dim3* grid, dim3* block) {
   *block = dim3(64 * kWaves, 1, 1);
 }
 
-hipError_t launch_step_small(int G, int mode, const StepArgs& a, hipStream_t s) {
+hipError_t launch_step_small(int G, int bf16, int mode, const StepArgs& a, hipStream_t s, hipEvent_t e0,
+                             hipEvent_t e1) {
   dim3 grid, block;
   step_small_grid(G, a.B, a.H, &grid, &block);
-#define AMB_L(G_, M_) hipLaunchKernelGGL((step_small_f32<G_, M_>), grid, block, 0, s, a)
-  if (G == 4) {
-    if (mode == kForward) AMB_L(4, kForward);
-    else if (mode == kAdjoint) AMB_L(4, kAdjoint);
-    else AMB_L(4, kFinal);
-  } else {
-    if (mode == kForward) AMB_L(1, kForward);
-    else if (mode == kAdjoint) AMB_L(1, kAdjoint);
-    else AMB_L(1, kFinal);
+#define AMB_L(T_, G_, M_) hipExtLaunchKernelGGL((step_small<T_, G_, M_>), grid, block, 0, s, e0, e1, 0, a)
+#define AMB_T(T_)                                   \
+  if (G == 4) {                                     \
+    if (mode == kForward) AMB_L(T_, 4, kForward);   \
+    else if (mode == kAdjoint) AMB_L(T_, 4, kAdjoint); \
+    else AMB_L(T_, 4, kFinal);                      \
+  } else {                                          \
+    if (mode == kForward) AMB_L(T_, 1, kForward);   \
+    else if (mode == kAdjoint) AMB_L(T_, 1, kAdjoint); \
+    else AMB_L(T_, 1, kFinal);                      \
   }
+  if (bf16) {
+    AMB_T(__bf16)
+  } else {
+    AMB_T(float)
+  }
+#undef AMB_T
 #undef AMB_L
   return hipGetLastError();
 }

@@ -94,6 +94,13 @@ def test_query_sizes_and_validation(amb):
     with pytest.raises(AmbpttError) as e:
         query(ProblemSpec(**{**spec.__dict__, "hidden": 500}))
     assert e.value.status == -4
+    # bf16 operands: sizes must be multiples of 32; state = bf16 h + fp32 c
+    bf = ProblemSpec("lstm", "bf16", "mean_last", 128, 1024, 2048, 10000, 32, 10000)
+    stride, pool, ws = query(bf)
+    assert stride == 128 * 2048 * 2 + 128 * 2048 * 4 and pool == 32 * stride
+    with pytest.raises(AmbpttError) as e:
+        query(ProblemSpec(**{**bf.__dict__, "hidden": 48}))
+    assert e.value.status == -4
 
 
 def test_stats_struct_layout(amb):

@@ -7,7 +7,7 @@ import pytest
 import synth
 from oracle import schedule as S
 
-from gpu_util import (TOL_F32, assert_bitwise, assert_close, device_inputs, inputs, run_gpu,
+from gpu_util import (TOL_BF16, TOL_F32, assert_bitwise, assert_close, device_inputs, inputs, run_gpu,
                       run_oracle, say)
 
 pytestmark = pytest.mark.gpu
@@ -101,4 +101,31 @@ def test_lstm4096_shapes_short():
     assert a["stats"]["mode"] == 1
     assert_close(a, want, TOL_F32)
     b = run_gpu(wl, dev, fast_slots=1, slow_slots=0)
+    assert_bitwise(a, b)
+
+
+def test_lstm_bf16_small_schedules():
+    """bf16 operands and stored h, fp32 cell state: oracle within 2e-2, schedules bit for bit."""
+    wl = synth.get("lstm_h2048_bf16_t10000").with_(batch=20, input=64, hidden=96, n_steps=30,
+                                                   name="lstm_bf16_small")
+    host, dev = _case(wl)
+    want = run_oracle(wl, *host)
+    ref = run_gpu(wl, dev, fast_slots=30, slow_slots=0)
+    assert ref["stats"]["forward_evals"] == 30
+    assert_close(ref, want, TOL_BF16)
+    for kw in (dict(fast_slots=3, slow_slots=0), dict(fast_slots=3, slow_slots=30, interval_min=2),
+               dict(fast_slots=2, slow_slots=30, interval_min=1)):
+        got = run_gpu(wl, dev, **kw)
+        assert_bitwise(got, ref)
+
+
+def test_lstm2048_bf16_shapes_short():
+    """The 2048-wide bf16 LSTM at its full per-step shapes (B=128, D=1024, H=2048), 6 steps."""
+    wl = synth.get("lstm_h2048_bf16_t10000").with_(n_steps=6)
+    host, dev = _case(wl)
+    want = run_oracle(wl, *host)
+    a = run_gpu(wl, dev, fast_slots=2, slow_slots=6, interval_min=2)   # async: 8 evaluations vs Revolve's 9
+    assert a["stats"]["mode"] == 1 and a["stats"]["forward_evals"] == 8
+    assert_close(a, want, TOL_BF16)
+    b = run_gpu(wl, dev, fast_slots=6, slow_slots=0)
     assert_bitwise(a, b)
