@@ -352,9 +352,12 @@ __global__ __launch_bounds__(256) void dw_lds_f32(DwArgs a) {
       for (int v = 0; v < 4; ++v) {
         const int k = k0 + wm * 32 + 16 * ik + 4 * lk + v;
         const int cc = c0 + wn * 32 + 16 * ic + li;
-        if (cc < N && k < GH) a.dW[(size_t)k * N + cc] += acc[ik][ic][v];
+        if (cc < N && k < GH) {
+          float* d = a.dW + (size_t)k * N + cc;
+          *d = a.accumulate ? *d + acc[ik][ic][v] : acc[ik][ic][v];
+        }
       }
-  if (do_bias && wave == 0 && k0 + lane < GH) a.db[k0 + lane] += bsum;
+  if (do_bias && wave == 0 && k0 + lane < GH) a.db[k0 + lane] = a.accumulate ? a.db[k0 + lane] + bsum : bsum;
 }
 
 __global__ void transpose_wh_f32(const float* __restrict__ W, float* __restrict__ WhT, int GH, int D, int H) {

@@ -103,9 +103,12 @@ __global__ __launch_bounds__(256) void dw_bf16(DwArgs a) {
       for (int v = 0; v < 4; ++v) {
         const int k = k0 + wm * 32 + 16 * ik + 4 * lq + v;
         const int c = c0 + wn * 32 + 16 * ic + li;
-        if (c < N && k < GH) a.dW[(size_t)k * N + c] += acc[ik][ic][v];
+        if (c < N && k < GH) {
+          float* d = a.dW + (size_t)k * N + c;
+          *d = a.accumulate ? *d + acc[ik][ic][v] : acc[ik][ic][v];
+        }
       }
-  if (do_bias && wave == 0 && k0 + lane < GH) a.db[k0 + lane] += bsum;
+  if (do_bias && wave == 0 && k0 + lane < GH) a.db[k0 + lane] = a.accumulate ? a.db[k0 + lane] + bsum : bsum;
 }
 
 __global__ void transpose_wh_u16(const uint16_t* __restrict__ W, uint16_t* __restrict__ WhT, int GH, int D,

@@ -48,6 +48,25 @@ struct DwArgs {
   float* dW;         // [G*H][D+H]
   float* db;         // [G*H]
   int R, D, H, GH;
+  int accumulate;    // 1: dW += ..., 0: dW = ... (one window per weight set)
+};
+
+// Arguments of one residual-MLP step kernel (layer l).
+struct MlpArgs {
+  const void* y;          // op: y_l [B][w]
+  void* y_out;            // op: forward: y_{l+1}
+  const void* W;          // op: W_l [w][w]
+  const float* bias;      // b_l [w]
+  const void* Wn;         // op: adjoint: W_{l+1}; final: W_0
+  const void* zbar_in;    // op: adjoint: zbar_{l+1}; final: zbar_0
+  const float* ybar_in;   // adjoint: ybar_{l+2}; final: ybar_1
+  void* zbar_out;         // op: zbar_l
+  float* ybar_out;        // ybar_{l+1}
+  void* ywin_out;         // op: copy of y_l for the weight gradient
+  double* loss_acc;
+  float* dy0;
+  int B, w, loss, first;
+  float inv_bw;
 };
 
 enum StepMode { kForward = 0, kAdjoint = 1, kFinal = 2 };
@@ -67,6 +86,8 @@ hipError_t launch_dw(const DwArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hi
 void step_small_grid(int G, int B, int H, dim3* grid, dim3* block);
 hipError_t launch_step_small(int G, int bf16, int mode, const StepArgs& a, hipStream_t s,
                              hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+void resmlp_grid(int B, int w, dim3* grid, dim3* block);
+hipError_t launch_resmlp(int bf16, int mode, const MlpArgs& a, hipStream_t s);
 hipError_t launch_dw_bf16(const DwArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_transpose_wh_bf16(const void* W, void* WhT, int GH, int D, int H, hipStream_t s);
 hipError_t launch_transpose_wh(const float* W, float* WhT, int GH, int D, int H, hipStream_t s);

@@ -63,7 +63,8 @@ struct Layout {
   size_t off_loss = 0, off_lossout = 0, total = 0;
   int loss_slots = 0;
   StepCfg cfg{1, 1, 1};  // single-launch path
-  bool small = false;    // one-launch small-batch path (step_small_f32)
+  bool small = false;    // one-launch small-batch path (step_small)
+  bool mlp = false;      // residual MLP (per-layer weights, one-step dW windows)
 };
 
 ambptt_status validate(const ambptt_problem* p) {
@@ -81,13 +82,14 @@ ambptt_status validate(const ambptt_problem* p) {
     return fail(AMBPTT_EUNSUPPORTED, "hidden and input sizes must be multiples of 16");
   if (p->dtype == AMBPTT_BF16 && (p->hidden % 32 || p->input % 32))
     return fail(AMBPTT_EUNSUPPORTED, "bf16 operands need hidden and input sizes that are multiples of 32");
-  if (p->cell == AMBPTT_CELL_RESMLP) return fail(AMBPTT_EUNSUPPORTED, "residual MLP cell not built yet");
+  if (p->cell == AMBPTT_CELL_RESMLP && p->input != 0) return fail(AMBPTT_EINVAL, "the residual MLP has no step input");
   if ((int64_t)p->batch * p->hidden > (int64_t(1) << 31)) return fail(AMBPTT_EUNSUPPORTED, "state too large");
   return AMBPTT_OK;
 }
 
-int auto_window(int B) {
-  int w = (1024 + B - 1) / B;
+int auto_window(const ambptt_problem* p) {
+  if (p->cell == AMBPTT_CELL_RESMLP) return 1;  // every layer has its own dW
+  int w = (1024 + p->batch - 1) / p->batch;
   return std::max(1, std::min(64, w));
 }
 
@@ -95,7 +97,8 @@ Layout make_layout(const ambptt_problem* p, int window) {
   Layout L;
   L.G = p->cell == AMBPTT_CELL_LSTM ? 4 : 1;
   L.dsize = p->dtype == AMBPTT_BF16 ? 2 : 4;
-  L.window = window > 0 ? window : auto_window(p->batch);
+  L.window = window > 0 ? window : auto_window(p);
+  L.mlp = p->cell == AMBPTT_CELL_RESMLP;
   const size_t BH = (size_t)p->batch * p->hidden;
   const size_t GH = (size_t)L.G * p->hidden;
   L.h_bytes = BH * L.dsize;
@@ -114,10 +117,15 @@ Layout make_layout(const ambptt_problem* p, int window) {
     step_small_grid(L.G, p->batch, p->hidden, &grid, &block);
     L.loss_slots = int(grid.x * grid.y);
   }
+  if (L.mlp) {
+    L.small = false;
+    resmlp_grid(p->batch, p->hidden, &grid, &block);
+    L.loss_slots = int(grid.x * grid.y);
+  }
   size_t o = 0;
   L.off_live[0] = o; o += L.stride;
   L.off_live[1] = o; o += L.stride;
-  L.off_wht = o; o += align_up((size_t)p->hidden * GH * L.dsize);
+  L.off_wht = o; o += L.mlp ? 0 : align_up((size_t)p->hidden * GH * L.dsize);
   L.off_zbar = o; o += align_up(2 * (size_t)L.window * p->batch * GH * L.dsize);
   L.off_hwin = o; o += align_up(2 * (size_t)L.window * BH * L.dsize);
   L.off_cbar[0] = o; o += align_up(BH * 4);
@@ -258,8 +266,31 @@ struct Exec {
   }
 
   // one forward step: state at `src` -> `dst`
+  // residual MLP: layer t's weights and bias
+  const void* W_of(int64_t t) const {
+    return (const char*)W + (size_t)t * p.hidden * p.hidden * L.dsize;
+  }
+  MlpArgs mlp_args(int64_t t) const {
+    MlpArgs a{};
+    a.W = W_of(t);
+    a.bias = b + (size_t)t * p.hidden;
+    a.B = p.batch;
+    a.w = p.hidden;
+    a.loss = p.loss;
+    a.inv_bw = 1.0f / float((double)p.batch * p.hidden);
+    return a;
+  }
+
   ambptt_status fwd_step(int64_t t, char* src, char* dst) {
     st.forward_evals++;
+    if (L.mlp) {
+      MlpArgs a = mlp_args(t);
+      a.y = src;
+      a.y_out = dst;
+      return timed(AMBPTT_K_FWD, [&](hipEvent_t, hipEvent_t) {
+        return launch_resmlp(p.dtype == AMBPTT_BF16, kForward, a, C->cs);
+      });
+    }
     StepArgs a = base_args();
     a.x = x_at(t);
     a.h = hpart(src);
@@ -299,27 +330,43 @@ struct Exec {
       }
       dw_pending[hf] = false;
     }
-    StepArgs a = base_args();
-    a.x = x_at(t);
-    a.h = hpart(cur);
-    a.c = L.G == 4 ? cpart(cur) : nullptr;
-    a.first = first;
-    a.last = first;
-    a.zbar_in = first ? nullptr : zbar_at(t + 1);
-    a.cbar_in = first ? nullptr : cbar(t + 1);
-    a.zbar_out = zbar_at(t);
-    a.cbar_out = cbar(t);
-    a.hwin_out = hwin_at(t);
-    a.loss_acc = (double*)(C->ws + L.off_loss);
-    ambptt_status s =
-        timed(AMBPTT_K_ADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch(kAdjoint, a, e0, e1); });
+    ambptt_status s;
+    if (L.mlp) {
+      MlpArgs a = mlp_args(t);
+      a.y = cur;
+      a.first = first;
+      a.Wn = first ? nullptr : W_of(t + 1);
+      a.zbar_in = first ? nullptr : zbar_at(t + 1);
+      a.ybar_in = first ? nullptr : cbar(t + 1);
+      a.zbar_out = zbar_at(t);
+      a.ybar_out = cbar(t);
+      a.ywin_out = hwin_at(t);
+      a.loss_acc = (double*)(C->ws + L.off_loss);
+      s = timed(AMBPTT_K_ADJ, [&](hipEvent_t, hipEvent_t) {
+        return launch_resmlp(p.dtype == AMBPTT_BF16, kAdjoint, a, C->cs);
+      });
+    } else {
+      StepArgs a = base_args();
+      a.x = x_at(t);
+      a.h = hpart(cur);
+      a.c = L.G == 4 ? cpart(cur) : nullptr;
+      a.first = first;
+      a.last = first;
+      a.zbar_in = first ? nullptr : zbar_at(t + 1);
+      a.cbar_in = first ? nullptr : cbar(t + 1);
+      a.zbar_out = zbar_at(t);
+      a.cbar_out = cbar(t);
+      a.hwin_out = hwin_at(t);
+      a.loss_acc = (double*)(C->ws + L.off_loss);
+      s = timed(AMBPTT_K_ADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch(kAdjoint, a, e0, e1); });
+    }
     if (s != AMBPTT_OK) return s;
     live_dead = true;
     if (t % w == 0) {  // window [t, min(t + w, n)) complete: accumulate it on the dW stream
       const int64_t cnt = std::min(w, n - t);
       DwArgs d{};
       d.zbar = zbar_at(t);
-      d.x = x_at(t);
+      d.x = p.input > 0 ? x_at(t) : nullptr;
       d.hwin = hwin_at(t);
       d.dW = dW;
       d.db = db;
@@ -327,6 +374,12 @@ struct Exec {
       d.D = p.input;
       d.H = p.hidden;
       d.GH = L.G * p.hidden;
+      d.accumulate = 1;
+      if (L.mlp) {  // layer t's own gradient, written once
+        d.dW = dW + (size_t)t * p.hidden * p.hidden;
+        d.db = db + (size_t)t * p.hidden;
+        d.accumulate = 0;
+      }
       HIPCK(hipEventRecord(C->ev_c2, C->cs));
       HIPCK(hipStreamWaitEvent(C->ds, C->ev_c2, 0));
       s = timed(
@@ -344,6 +397,16 @@ struct Exec {
 
   // dL/dx_0 = (zbar_0 W_h, cbar_0)
   ambptt_status final_step(float* dh0, float* dc0) {
+    if (L.mlp) {
+      MlpArgs a = mlp_args(0);
+      a.Wn = W_of(0);
+      a.zbar_in = zbar_at(0);
+      a.ybar_in = cbar(0);
+      a.dy0 = dh0;
+      return timed(AMBPTT_K_OTHER, [&](hipEvent_t, hipEvent_t) {
+        return launch_resmlp(p.dtype == AMBPTT_BF16, kFinal, a, C->cs);
+      });
+    }
     StepArgs a = base_args();
     a.zbar_in = zbar_at(0);
     a.cbar_in = cbar(0);
@@ -485,10 +548,13 @@ ambptt_status ensure_host(ambptt_ctx* C, size_t bytes) {
 ambptt_status prepare_inputs(ambptt_ctx* C, const void* W, const void* h0, const float* c0, Exec& E) {
   const Layout& L = C->L;
   const ambptt_problem& p = C->p;
-  if (p.dtype == AMBPTT_BF16)
+  if (L.mlp) {
+    // no transposed weights: the residual MLP kernels transpose W tiles in LDS
+  } else if (p.dtype == AMBPTT_BF16) {
     HIPCK(launch_transpose_wh_bf16(W, E.WhT, L.G * p.hidden, p.input, p.hidden, C->cs));
-  else
+  } else {
     HIPCK(launch_transpose_wh((const float*)W, (float*)E.WhT, L.G * p.hidden, p.input, p.hidden, C->cs));
+  }
   // live state <- x_0
   char* l0 = E.live(0);
   HIPCK(hipMemcpyAsync(l0, h0, L.h_bytes, hipMemcpyDeviceToDevice, C->cs));
@@ -603,7 +669,7 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
   } else if (k == "elide_prefetch") {
     C->elide_prefetch = v != 0;
   } else if (k == "window") {
-    const int wmax = auto_window(C->p.batch);
+    const int wmax = auto_window(&C->p);
     if (v < 0 || v > wmax) return fail(AMBPTT_EINVAL, "window must be in [0, " + std::to_string(wmax) + "]");
     C->window_opt = int(v);
     const Layout L2 = make_layout(&C->p, int(v == 0 ? wmax : v));
@@ -703,8 +769,10 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   Exec E(C, x_seq, W, b);
   std::fill(C->pend.begin(), C->pend.end(), kNone);
   const size_t GH = (size_t)L.G * p.hidden;
-  HIPCK(launch_fill32(dW, GH * (p.input + p.hidden), 0u, C->cs));
-  HIPCK(launch_fill32(db, GH, 0u, C->cs));
+  if (!L.mlp) {  // windows accumulate into dW; the MLP writes each layer once
+    HIPCK(launch_fill32(dW, GH * (p.input + p.hidden), 0u, C->cs));
+    HIPCK(launch_fill32(db, GH, 0u, C->cs));
+  }
   HIPCK(launch_fill32(C->ws + L.off_loss, (size_t)L.loss_slots * 2, 0u, C->cs));
   if ((s = prepare_inputs(C, W, h0, c0, E)) != AMBPTT_OK) return s;
   if ((s = E.run(plan, dW, db)) != AMBPTT_OK) return s;

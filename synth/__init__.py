@@ -15,8 +15,8 @@ Every array is drawn from numpy's PCG64 stream seeded by a SeedSequence of
 layer's weights can be regenerated on its own, in any order, with the same
 values.
 """
-from .workloads import (Workload, WORKLOADS, get, x_slice, params, initial_state,
+from .workloads import (Workload, WORKLOADS, get, x_slice, params, layer_params, initial_state,
                         f32_to_bf16_bits, bf16_bits_to_f32)
 
-__all__ = ["Workload", "WORKLOADS", "get", "x_slice", "params", "initial_state",
+__all__ = ["Workload", "WORKLOADS", "get", "x_slice", "params", "layer_params", "initial_state",
            "f32_to_bf16_bits", "bf16_bits_to_f32"]

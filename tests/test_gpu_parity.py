@@ -7,8 +7,8 @@ import pytest
 import synth
 from oracle import schedule as S
 
-from gpu_util import (TOL_BF16, TOL_F32, assert_bitwise, assert_close, device_inputs, inputs, run_gpu,
-                      run_oracle, say)
+from gpu_util import (TOL_BF16, TOL_F32, assert_bitwise, assert_close, assert_close_relu, device_inputs,
+                      inputs, run_gpu, run_oracle, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -128,4 +128,33 @@ def test_lstm2048_bf16_shapes_short():
     assert a["stats"]["mode"] == 1 and a["stats"]["forward_evals"] == 8
     assert_close(a, want, TOL_BF16)
     b = run_gpu(wl, dev, fast_slots=6, slow_slots=0)
+    assert_bitwise(a, b)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_resmlp_small_schedules(dtype):
+    """Residual MLP, depth as the sequence: oracle parity and bit-exact schedules."""
+    wl = synth.get("resmlp_w4096_l2000_bf16").with_(dtype=dtype, batch=20, hidden=64, n_steps=13,
+                                                    w_scale=0.1, name="resmlp_small")
+    host, dev = _case(wl)
+    want = run_oracle(wl, *host)
+    tol = TOL_F32 if dtype == "f32" else TOL_BF16
+    ref = run_gpu(wl, dev, fast_slots=13, slow_slots=0)
+    assert ref["stats"]["forward_evals"] == 13
+    assert_close(ref, want, tol)
+    for kw in (dict(fast_slots=3, slow_slots=0), dict(fast_slots=3, slow_slots=13, interval_min=2),
+               dict(fast_slots=2, slow_slots=13, interval_min=1)):
+        got = run_gpu(wl, dev, **kw)
+        assert_bitwise(got, ref)
+
+
+def test_resmlp4096_shapes_short():
+    """The 4096-wide bf16 residual MLP at its full layer shape (B=256), 5 layers."""
+    wl = synth.get("resmlp_w4096_l2000_bf16").with_(n_steps=5)
+    host, dev = _case(wl)
+    want = run_oracle(wl, *host)
+    a = run_gpu(wl, dev, fast_slots=2, slow_slots=5, interval_min=1)
+    assert a["stats"]["mode"] == 1
+    assert_close_relu(a, want, TOL_BF16)
+    b = run_gpu(wl, dev, fast_slots=5, slow_slots=0)
     assert_bitwise(a, b)
