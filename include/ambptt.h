@@ -87,8 +87,8 @@ typedef struct {
 typedef struct {
   int32_t mode;            /* 0 = Revolve, 1 = asynchronous two-level */
   int32_t interval;        /* I (0 in Revolve mode) */
-  int32_t window;          /* steps per dW accumulation window */
-  int32_t reserved0;
+  int32_t window;          /* steps per dW accumulation window (0: resident kernel) */
+  int32_t path;            /* 0 = one launch per step, 1 = resident whole-pass kernel */
   int64_t n_steps;
   int64_t actions;
   int64_t forward_evals;
@@ -109,11 +109,10 @@ typedef struct {
   int64_t kernel_calls[6];
 } ambptt_stats;
 
-/* Kernel classes of ambptt_stats.kernel_*: forward step GEMM (the whole
- * forward step on the single-launch path), its cell epilogue, adjoint step
- * GEMM (the whole adjoint step on the single-launch path), its epilogue, the
- * weight-gradient window, and everything else. */
-enum { AMBPTT_K_FWD = 0, AMBPTT_K_FWD_EPI = 1, AMBPTT_K_ADJ = 2, AMBPTT_K_ADJ_EPI = 3,
+/* Kernel classes of ambptt_stats.kernel_*: forward step, the resident
+ * whole-pass kernel, adjoint step, (unused), weight-gradient window, and
+ * everything else. */
+enum { AMBPTT_K_FWD = 0, AMBPTT_K_PASS = 1, AMBPTT_K_ADJ = 2, AMBPTT_K_UNUSED = 3,
        AMBPTT_K_DW = 4, AMBPTT_K_OTHER = 5 };
 
 typedef struct ambptt_ctx ambptt_ctx;
@@ -145,6 +144,21 @@ int64_t ambptt_schedule_evals(int64_t n, int32_t s, int64_t H, int32_t interval_
 ambptt_status ambptt_schedule_text(int64_t n, int32_t s, int64_t H, int32_t interval_min,
                                    char* buf, size_t cap, size_t* needed);
 
+/* The program the resident whole-pass kernel would run for the schedule of
+ * (n, s, H, I_min), 4 int32 per entry {op, y, z, w}:
+ *   0 end (dL/dx_0, dW, loss)      1 forward step y, buffer z -> buffer w
+ *   2 adjoint step y from buffer z (w = 1: first turn)
+ *   3 copy buffer z -> w, first waiting until every workgroup has read the
+ *     inputs of barrier y (y = 0: no wait)
+ *   4 store slot z to host slot w  5 prefetch host slot z to slot w
+ *   6 barrier only
+ * Buffers 0..s-1 are the HBM slots, s and s+1 the two live buffers.  Ops 0,
+ * 1, 2 and 6 are the barriers of the workgroups that share batch rows.
+ * Writes at most cap entries and sets *entries to the full count.  EINVAL if
+ * cap is too small (buf untouched) or on bad arguments.  Pure host. */
+ambptt_status ambptt_resident_program(int64_t n, int32_t s, int64_t H, int32_t interval_min,
+                                      int32_t elide_prefetch, int32_t* buf, size_t cap, size_t* entries);
+
 /* Sizes the caller allocates: bytes of one state (padded slot stride), of the
  * slot pool (fast_slots * stride) and of the workspace. */
 ambptt_status ambptt_query(const ambptt_problem* p, size_t* state_bytes,
@@ -165,7 +179,17 @@ ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
 
 /* Sets a tuning / debug knob.  Keys: "timing_sample" (time every k-th
  * kernel launch with events, 0 = off), "elide_prefetch" (0/1, default 1),
- * "window" (dW window steps, 0 = automatic).  EINVAL for unknown keys. */
+ * "window" (dW window steps, 0 = automatic), "path" (0 = the resident
+ * whole-pass kernel when the problem and device allow it, else one launch
+ * per step; 1 = one launch per step; 2 = resident, EUNSUPPORTED at run time
+ * if it does not fit), "resident_timeout_ms" (how long one barrier wait of the
+ * resident kernel may take before the pass aborts with EINTERNAL; default
+ * 2000), "resident_cooperative" (0, default: a plain launch of the resident
+ * grid, which the device holds at once when nothing else occupies it, else
+ * the pass ends in the barrier timeout; 1: hipLaunchCooperativeKernel, whose
+ * runtime guarantees residency), "resident_test_stall" (1: the resident program starts with a wait
+ * that is never satisfied, so the pass ends in that timeout; for tests of the
+ * abort path).  EINVAL for unknown keys or values out of range. */
 ambptt_status ambptt_set_int(ambptt_ctx* ctx, const char* key, int64_t value);
 
 /* Measures T_A (one forward step) and T_T (one state over the host link,

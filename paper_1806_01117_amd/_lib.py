@@ -13,7 +13,7 @@ DTYPE = {"f32": 0, "bf16": 1}
 LOSS = {"half_sq_last": 0, "mean_sq_all": 1, "mean_last": 2}
 
 EXPORTS = ["ambptt_version", "ambptt_revolve_advances", "ambptt_schedule_evals", "ambptt_schedule_text",
-           "ambptt_query", "ambptt_last_error", "ambptt_create", "ambptt_bind", "ambptt_set_int",
+           "ambptt_resident_program", "ambptt_query", "ambptt_last_error", "ambptt_create", "ambptt_bind", "ambptt_set_int",
            "ambptt_calibrate", "ambptt_run", "ambptt_destroy"]
 
 
@@ -25,7 +25,7 @@ class Problem(C.Structure):
 
 
 class Stats(C.Structure):
-    _fields_ = [("mode", C.c_int32), ("interval", C.c_int32), ("window", C.c_int32), ("reserved0", C.c_int32),
+    _fields_ = [("mode", C.c_int32), ("interval", C.c_int32), ("window", C.c_int32), ("path", C.c_int32),
                 ("n_steps", C.c_int64), ("actions", C.c_int64), ("forward_evals", C.c_int64),
                 ("adjoints", C.c_int64), ("takeshots", C.c_int64), ("takeshot_copies", C.c_int64),
                 ("restores", C.c_int64), ("stores", C.c_int64), ("prefetches", C.c_int64),
@@ -38,14 +38,12 @@ class Stats(C.Structure):
     def as_dict(self) -> dict:
         d = {}
         for k, _ in self._fields_:
-            if k == "reserved0":
-                continue
             v = getattr(self, k)
             d[k] = list(v) if isinstance(v, C.Array) else v
         return d
 
 
-KERNEL_CLASSES = ["fwd", "fwd_epi", "adj", "adj_epi", "dw", "other"]
+KERNEL_CLASSES = ["fwd", "pass", "adj", "unused", "dw", "other"]
 
 
 _lib = None
@@ -74,6 +72,8 @@ def load():
     L.ambptt_schedule_evals.restype = i64
     L.ambptt_schedule_text.argtypes = [i64, i32, i64, i32, C.c_char_p, sz, C.POINTER(sz)]
     L.ambptt_schedule_text.restype = C.c_int
+    L.ambptt_resident_program.argtypes = [i64, i32, i64, i32, i32, C.POINTER(i32), sz, C.POINTER(sz)]
+    L.ambptt_resident_program.restype = C.c_int
     L.ambptt_query.argtypes = [C.POINTER(Problem), C.POINTER(sz), C.POINTER(sz), C.POINTER(sz)]
     L.ambptt_query.restype = C.c_int
     L.ambptt_create.argtypes = [C.POINTER(Problem), vp, C.POINTER(vp)]

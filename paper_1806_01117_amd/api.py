@@ -44,6 +44,19 @@ def schedule_text(n: int, s: int, H: int = 0, interval_min: int = 0) -> str:
     return buf.value.decode()
 
 
+def resident_program(n: int, s: int, H: int = 0, interval_min: int = 0, elide_prefetch: bool = True):
+    """The resident whole-pass kernel's program for a schedule, as a list of
+    (op, y, z, w) tuples (see ambptt_resident_program in include/ambptt.h)."""
+    L = load()
+    need = C.c_size_t(0)
+    L.ambptt_resident_program(n, s, H, interval_min, int(elide_prefetch), None, 0, C.byref(need))
+    if need.value == 0:
+        check(L.ambptt_resident_program(n, s, H, interval_min, int(elide_prefetch), None, 0, C.byref(need)))
+    buf = (C.c_int32 * (4 * need.value))()
+    check(L.ambptt_resident_program(n, s, H, interval_min, int(elide_prefetch), buf, need.value, C.byref(need)))
+    return [tuple(buf[4 * i:4 * i + 4]) for i in range(need.value)]
+
+
 @dataclasses.dataclass
 class ProblemSpec:
     cell: str             # "rnn" | "lstm" | "resmlp"

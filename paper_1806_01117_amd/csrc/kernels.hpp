@@ -9,6 +9,8 @@
 #include <cstddef>
 #include <cstdint>
 
+#include "resident_prog.hpp"
+
 namespace ambptt {
 
 // Arguments of one step kernel.  G = 1 (tanh RNN) or 4 (LSTM, gate blocks
@@ -70,6 +72,51 @@ struct MlpArgs {
 };
 
 enum StepMode { kForward = 0, kAdjoint = 1, kFinal = 2 };
+
+// Resident whole-pass kernel (fp32 tanh RNN / LSTM with small states): one
+// launch runs a program compiled from the schedule (resident_prog.hpp).
+struct ResidentArgs {
+  const int* prog;      // [nprog][4]
+  int nprog;
+  const float* x;       // [n][B][D]
+  const float* W;       // [G*H][D+H]
+  const float* bias;    // [G*H]
+  char* pool;           // slot k at pool + k * stride
+  char* live0;
+  char* live1;
+  size_t stride;        // bytes between slots
+  size_t c_off;         // byte offset of c within a state (LSTM)
+  int nslots;
+  char* host;           // host tier (device-visible): [host slot][workgroup][1 KiB]
+  float* P;             // partial h-adjoints [2][mtiles][ng][ng][16 U]
+  float* dWp;           // per row tile dW partials [mtiles][G*H][D+H]
+  float* dbp;           // [mtiles][G*H]
+  float* dh0;           // [B][H]
+  float* dc0;           // [B][H] (LSTM)
+  double* loss_acc;     // [mtiles * ng]
+  unsigned* ready;      // [mtiles * ng] syncs entered (zero before launch)
+  unsigned* consumed;   // [mtiles * ng] syncs whose inputs are read (zero before launch)
+  unsigned* status;     // [0]: abort flag, [1]: op index of the abort + 1
+  long long timeout;    // s_memrealtime ticks (100 MHz) a wait may take
+  int B, D, H, loss;
+  int mtiles, ng;       // row tiles (16 rows); unit groups per row tile
+  int xcd_map;          // 1: place each row tile's workgroups on 8 / mtiles XCDs
+  float inv_bh;
+};
+
+// units per workgroup of the resident kernel (8 LSTM, 16 RNN)
+int resident_units(int G);
+// largest D + H and H the resident kernel holds in registers
+int resident_max_k(int G);
+int resident_max_h(int G);
+// workgroups of the resident kernel that can be resident at once on device dev
+hipError_t resident_capacity(int G, int* blocks);
+// cooperative: hipLaunchCooperativeKernel (the runtime guarantees that the
+// whole grid is resident); otherwise a plain launch of a grid that fits
+hipError_t launch_resident(int G, const ResidentArgs& a, hipStream_t s, bool cooperative);
+// dW = sum over row tiles of dWp (fixed order), db likewise
+hipError_t launch_resident_reduce(const float* dWp, const float* dbp, int mtiles, int GH, int K1, float* dW,
+                                  float* db, hipStream_t s);
 
 struct StepCfg {
   int rm, rj, ks;  // 16x16 tiles per wave in m and j; waves splitting K

@@ -29,6 +29,7 @@
 
 #include "ambptt.h"
 #include "kernels.hpp"
+#include "resident_prog.hpp"
 #include "schedule.hpp"
 
 using namespace ambptt;
@@ -65,7 +66,16 @@ struct Layout {
   StepCfg cfg{1, 1, 1};  // single-launch path
   bool small = false;    // one-launch small-batch path (step_small)
   bool mlp = false;      // residual MLP (per-layer weights, one-step dW windows)
+  // resident whole-pass kernel (fp32 RNN / LSTM whose weights fit in registers)
+  bool res = false;
+  int r_mtiles = 0, r_ng = 0, r_nwg = 0;
+  size_t r_prog_cap = 0;  // program entries
+  size_t off_prog = 0, off_ready = 0, off_consumed = 0, off_status = 0, off_P = 0, off_dWp = 0, off_dbp = 0;
 };
+
+// Largest grid of the resident kernel the layout provisions for; the device's
+// own limit is checked when a context is created.
+constexpr int kResidentMaxWg = 1024;
 
 ambptt_status validate(const ambptt_problem* p) {
   if (!p) return fail(AMBPTT_EINVAL, "problem is NULL");
@@ -122,6 +132,23 @@ Layout make_layout(const ambptt_problem* p, int window) {
     resmlp_grid(p->batch, p->hidden, &grid, &block);
     L.loss_slots = int(grid.x * grid.y);
   }
+  if (!L.mlp && p->dtype == AMBPTT_F32) {
+    const int U = resident_units(L.G);
+    const int K1 = p->input + p->hidden;
+    const int mtiles = (p->batch + 15) / 16, ng = p->hidden / U;
+    const long nwg = (long)mtiles * ng;
+    const double evr = double(revolve_advances(p->n_steps, p->fast_slots)) + 1.0;
+    const double cap = 2.0 * (evr + 3.0 * double(p->n_steps)) + 256.0;
+    if (K1 <= resident_max_k(L.G) && p->hidden <= resident_max_h(L.G) && p->hidden % U == 0 &&
+        nwg <= kResidentMaxWg && cap < 8.0e6) {
+      L.res = true;
+      L.r_mtiles = mtiles;
+      L.r_ng = ng;
+      L.r_nwg = int(nwg);
+      L.r_prog_cap = size_t(cap);
+      L.loss_slots = std::max(L.loss_slots, L.r_nwg);
+    }
+  }
   size_t o = 0;
   L.off_live[0] = o; o += L.stride;
   L.off_live[1] = o; o += L.stride;
@@ -132,6 +159,17 @@ Layout make_layout(const ambptt_problem* p, int window) {
   L.off_cbar[1] = o; o += align_up(BH * 4);
   L.off_loss = o; o += align_up((size_t)L.loss_slots * 8);
   L.off_lossout = o; o += kAlign;
+  if (L.res) {
+    const size_t U = size_t(resident_units(L.G)), K1 = size_t(p->input + p->hidden);
+    const size_t mt = size_t(L.r_mtiles), ng = size_t(L.r_ng), nwg = size_t(L.r_nwg);
+    L.off_prog = o; o += align_up(L.r_prog_cap * 16);
+    L.off_ready = o; o += align_up(nwg * 4);
+    L.off_consumed = o; o += align_up(nwg * 4);
+    L.off_status = o; o += kAlign;
+    L.off_P = o; o += align_up(2 * mt * ng * ng * 16 * U * 4);
+    L.off_dWp = o; o += align_up(mt * GH * K1 * 4);
+    L.off_dbp = o; o += align_up(mt * GH * 4);
+  }
   L.total = o;
   return L;
 }
@@ -160,6 +198,15 @@ struct ambptt_ctx {
   int64_t timing_sample = 0;
   bool elide_prefetch = true;
   int window_opt = 0;
+  int path_opt = 0;            // 0: resident kernel when it fits, 1: per-step launches, 2: resident kernel
+  int res_cap = -1;            // resident workgroups the device holds at once (-1: not queried)
+  int64_t res_timeout_ms = 2000;
+  bool res_test_stall = false;
+  bool res_coop = false;         // cooperative launch of the resident kernel   // tests of the abort path: the first entry waits for a barrier that never comes
+  int32_t* prog_host = nullptr;  // pinned staging of the resident program
+  size_t prog_host_cap = 0;
+  unsigned* status_host = nullptr;  // pinned copy of the resident kernel's status words
+  hipEvent_t ev_r[2] = {nullptr, nullptr};
 };
 
 namespace {
@@ -563,6 +610,237 @@ ambptt_status prepare_inputs(ambptt_ctx* C, const void* W, const void* h0, const
   return AMBPTT_OK;
 }
 
+// ---- resident whole-pass kernel ----------------------------------------------
+
+bool resident_possible(ambptt_ctx* C) {
+  if (!C->L.res || C->path_opt == 1) return false;
+  if (C->res_cap < 0) {
+    int cap = 0;
+    if (resident_capacity(C->L.G, &cap) != hipSuccess) {
+      (void)hipGetLastError();
+      cap = 0;
+    }
+    C->res_cap = cap;
+  }
+  return C->L.r_nwg <= C->res_cap;
+}
+
+ambptt_status ensure_prog_host(ambptt_ctx* C, size_t ints) {
+  if (ints <= C->prog_host_cap) return AMBPTT_OK;
+  if (C->prog_host) {
+    HIPCK(hipStreamSynchronize(C->cs));
+    HIPCK(hipHostFree(C->prog_host));
+    C->prog_host = nullptr;
+    C->prog_host_cap = 0;
+  }
+  void* ptr = nullptr;
+  HIPCK(hipHostMalloc(&ptr, ints * sizeof(int32_t), hipHostMallocDefault));
+  C->prog_host = (int32_t*)ptr;
+  C->prog_host_cap = ints;
+  return AMBPTT_OK;
+}
+
+ambptt_status resident_args(ambptt_ctx* C, const void* x, const void* W, const float* b, ResidentArgs* out) {
+  const Layout& L = C->L;
+  const ambptt_problem& p = C->p;
+  ResidentArgs a{};
+  a.prog = (const int*)(C->ws + L.off_prog);
+  a.x = (const float*)x;
+  a.W = (const float*)W;
+  a.bias = b;
+  a.pool = C->pool;
+  a.live0 = C->ws + L.off_live[0];
+  a.live1 = C->ws + L.off_live[1];
+  a.stride = L.stride;
+  a.c_off = align_up(L.h_bytes);
+  a.nslots = p.fast_slots;
+  a.host = nullptr;
+  if (C->host) HIPCK(hipHostGetDevicePointer((void**)&a.host, C->host, 0));
+  a.P = (float*)(C->ws + L.off_P);
+  a.dWp = (float*)(C->ws + L.off_dWp);
+  a.dbp = (float*)(C->ws + L.off_dbp);
+  a.loss_acc = (double*)(C->ws + L.off_loss);
+  a.ready = (unsigned*)(C->ws + L.off_ready);
+  a.consumed = (unsigned*)(C->ws + L.off_consumed);
+  a.status = (unsigned*)(C->ws + L.off_status);
+  a.timeout = (long long)C->res_timeout_ms * 100000LL;  // s_memrealtime runs at 100 MHz
+  a.B = p.batch;
+  a.D = p.input;
+  a.H = p.hidden;
+  a.loss = p.loss;
+  a.mtiles = L.r_mtiles;
+  a.ng = L.r_ng;
+  a.xcd_map = (L.r_nwg % 8 == 0 && 8 % L.r_mtiles == 0 && L.r_ng % (8 / L.r_mtiles) == 0) ? 1 : 0;
+  a.inv_bh = 1.0f / float((double)p.batch * p.hidden);
+  *out = a;
+  return AMBPTT_OK;
+}
+
+// live state <- x_0 (the resident kernel reads no transposed weights)
+ambptt_status resident_inputs(ambptt_ctx* C, const void* h0, const float* c0) {
+  const Layout& L = C->L;
+  char* l0 = C->ws + L.off_live[0];
+  HIPCK(hipMemcpyAsync(l0, h0, L.h_bytes, hipMemcpyDeviceToDevice, C->cs));
+  if (L.G == 4) HIPCK(hipMemcpyAsync(l0 + align_up(L.h_bytes), c0, L.c_bytes, hipMemcpyDeviceToDevice, C->cs));
+  return AMBPTT_OK;
+}
+
+// Uploads the program, clears the barrier flags and launches the kernel.  The
+// pinned staging buffer is rewritten only after the caller synchronised.
+ambptt_status resident_launch(ambptt_ctx* C, ResidentArgs a, const std::vector<int32_t>& prog, bool timed) {
+  const Layout& L = C->L;
+  const size_t n = prog.size();
+  if (n / 4 > L.r_prog_cap) return fail(AMBPTT_EINTERNAL, "resident program exceeds its workspace");
+  ambptt_status s = ensure_prog_host(C, n);
+  if (s != AMBPTT_OK) return s;
+  std::memcpy(C->prog_host, prog.data(), n * sizeof(int32_t));
+  HIPCK(hipMemcpyAsync(C->ws + L.off_prog, C->prog_host, n * sizeof(int32_t), hipMemcpyHostToDevice, C->cs));
+  a.nprog = int(n / 4);
+  HIPCK(launch_fill32(C->ws + L.off_ready, size_t(L.r_nwg), 0u, C->cs));
+  HIPCK(launch_fill32(C->ws + L.off_consumed, size_t(L.r_nwg), 0u, C->cs));
+  HIPCK(launch_fill32(C->ws + L.off_status, 4, 0u, C->cs));
+  if (timed) HIPCK(hipEventRecord(C->ev_r[0], C->cs));
+  HIPCK(launch_resident(L.G, a, C->cs, C->res_coop));
+  if (timed) HIPCK(hipEventRecord(C->ev_r[1], C->cs));
+  return AMBPTT_OK;
+}
+
+// after the stream finished: did every wait end in time?
+ambptt_status resident_status(ambptt_ctx* C) {
+  HIPCK(hipMemcpy(C->status_host, C->ws + C->L.off_status, 2 * sizeof(unsigned), hipMemcpyDeviceToHost));
+  if (C->status_host[0] == 0u) return AMBPTT_OK;
+  const unsigned w = C->status_host[1];
+  const unsigned code = w >> 24, entry = (w & 0xffffffu);
+  const char* why = code == 0 ? "a barrier wait exceeded the timeout"
+                  : code == 3 ? "two prefetches without a barrier between them"
+                  : code == 4 ? "unknown program entry" : "abort";
+  return fail(AMBPTT_EINTERNAL, std::string("resident pass aborted: ") + why +
+                                    (entry ? " (program entry " + std::to_string(entry - 1) + ")" : std::string()));
+}
+
+// T_A: one forward step (barrier included); T_T: one forward step when every
+// step also moves a state over the host link (stores, then prefetches).  Each
+// from the difference of a long and a short program, so that the launch and
+// the weight load cancel.
+ambptt_status resident_calibrate(ambptt_ctx* C, const void* x, const void* W, const float* b, const void* h0,
+                                 const float* c0, double* ta_us, double* tt_us) {
+  const Layout& L = C->L;
+  const ambptt_problem& p = C->p;
+  ambptt_status s = ensure_host(C, 2 * size_t(L.r_nwg) * 1024);
+  if (s != AMBPTT_OK) return s;
+  if ((s = resident_inputs(C, h0, c0)) != AMBPTT_OK) return s;
+  ResidentArgs a;
+  if ((s = resident_args(C, x, W, b, &a)) != AMBPTT_OK) return s;
+  const int L0 = p.fast_slots, L1 = p.fast_slots + 1;
+  auto program = [&](int steps, int kind) {
+    std::vector<int32_t> v;
+    int cur = L0;
+    for (int i = 0; i < steps; ++i) {
+      const int dst = cur == L0 ? L1 : L0;
+      v.insert(v.end(), {kPFwd, int32_t(i % p.n_steps), cur, dst});
+      cur = dst;
+      if (kind == 1) v.insert(v.end(), {kPStore, 0, 0, i % 2});
+      if (kind == 2) v.insert(v.end(), {kPPref, 0, i % 2, 0});
+    }
+    return v;
+  };
+  double per[3] = {0, 0, 0};
+  for (int kind = 0; kind < 3; ++kind) {
+    float ms[2] = {0.f, 0.f};
+    const int steps[2] = {16, 80};
+    for (int rep = 0; rep < 2; ++rep) {  // the first round warms up
+      for (int k = 0; k < 2; ++k) {
+        if ((s = resident_launch(C, a, program(steps[k], kind), true)) != AMBPTT_OK) return s;
+        HIPCK(hipEventSynchronize(C->ev_r[1]));
+        HIPCK(hipEventElapsedTime(&ms[k], C->ev_r[0], C->ev_r[1]));
+        if ((s = resident_status(C)) != AMBPTT_OK) return s;
+      }
+    }
+    per[kind] = 1000.0 * double(ms[1] - ms[0]) / double(steps[1] - steps[0]);
+  }
+  *ta_us = std::max(per[0], 1e-3);
+  *tt_us = std::max(per[1], per[2]);
+  return AMBPTT_OK;
+}
+
+ambptt_status resident_run(ambptt_ctx* C, const void* x_seq, const void* W, const float* b, const void* h0,
+                           const float* c0, float* dW, float* db, float* dh0, float* dc0, double* loss,
+                           ambptt_stats* stats) {
+  const ambptt_problem& p = C->p;
+  const Layout& L = C->L;
+  const double t0 = now_us();
+  Plan plan;
+  ResidentCounts rc;
+  std::vector<int32_t> prog;
+  try {
+    plan = make_plan(p.n_steps, p.fast_slots, p.slow_slots, std::max<int64_t>(C->interval_min, 1));
+    prog = compile_resident(plan, p.fast_slots, C->elide_prefetch, &rc);
+    if (C->res_test_stall) prog.insert(prog.begin(), {kPCopy, INT32_MAX, p.fast_slots, p.fast_slots + 1});
+  } catch (const std::exception& e) {
+    return fail(AMBPTT_EINTERNAL, e.what());
+  }
+  const double t1 = now_us();
+  ambptt_status s;
+  if (plan.async && (s = ensure_host(C, size_t(plan.host_slots_used) * size_t(L.r_nwg) * 1024)) != AMBPTT_OK)
+    return s;
+  ResidentArgs a;
+  if ((s = resident_args(C, x_seq, W, b, &a)) != AMBPTT_OK) return s;
+  a.dh0 = dh0;
+  a.dc0 = dc0;
+  HIPCK(launch_fill32(C->ws + L.off_loss, (size_t)L.loss_slots * 2, 0u, C->cs));
+  if ((s = resident_inputs(C, h0, c0)) != AMBPTT_OK) return s;
+  const bool timed = C->timing_sample > 0;
+  if ((s = resident_launch(C, a, prog, timed)) != AMBPTT_OK) return s;
+  const int GH = L.G * p.hidden, K1 = p.input + p.hidden;
+  HIPCK(launch_resident_reduce(a.dWp, a.dbp, L.r_mtiles, GH, K1, dW, db, C->cs));
+  const double scale = p.loss == AMBPTT_LOSS_HALF_SQ_LAST ? 0.5 : 1.0 / ((double)p.batch * p.hidden);
+  double* dloss = (double*)(C->ws + L.off_lossout);
+  HIPCK(launch_loss_sum((const double*)(C->ws + L.off_loss), L.loss_slots, scale, dloss, C->cs));
+  HIPCK(hipMemcpyAsync(C->host_loss, dloss, sizeof(double), hipMemcpyDeviceToHost, C->cs));
+  const double t_enq = now_us();
+  HIPCK(hipStreamSynchronize(C->cs));
+  const double t2 = now_us();
+  if ((s = resident_status(C)) != AMBPTT_OK) return s;
+  if (loss) *loss = *C->host_loss;
+  if (stats) {
+    ambptt_stats st{};
+    st.mode = plan.async ? 1 : 0;
+    st.interval = int32_t(plan.interval);
+    st.window = 0;
+    st.path = 1;
+    st.n_steps = p.n_steps;
+    st.actions = (int64_t)plan.acts.size();
+    st.forward_evals = rc.forward_evals;
+    st.adjoints = rc.adjoints;
+    st.takeshots = rc.takeshots;
+    st.takeshot_copies = rc.takeshot_copies;
+    st.restores = rc.restores;
+    st.stores = rc.stores;
+    st.prefetches = rc.prefetches;
+    st.prefetches_elided = rc.prefetches_elided;
+    st.bytes_d2h = rc.stores * (int64_t)L.state_bytes;
+    st.bytes_h2d = (rc.prefetches - rc.prefetches_elided) * (int64_t)L.state_bytes;
+    st.compute_waits = 0;
+    st.kernel_launches = 6;
+    st.recompute_factor = double(rc.forward_evals) / double(p.n_steps);
+    st.schedule_us = t1 - t0;
+    st.run_us = t2 - t1;
+    st.enqueue_us = t_enq - t1;
+    if (timed) {
+      float ms = 0.f;
+      HIPCK(hipEventElapsedTime(&ms, C->ev_r[0], C->ev_r[1]));
+      st.kernel_us[AMBPTT_K_PASS] = 1000.0 * ms;
+      st.kernel_samples[AMBPTT_K_PASS] = 1;
+    }
+    st.kernel_calls[AMBPTT_K_PASS] = 1;
+    st.kernel_calls[AMBPTT_K_OTHER] = 1;
+    *stats = st;
+  }
+  if (rc.forward_evals != plan.evals)
+    return fail(AMBPTT_EINTERNAL, "resident forward count differs from the schedule");
+  return AMBPTT_OK;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -597,6 +875,22 @@ ambptt_status ambptt_schedule_text(int64_t n, int32_t s, int64_t H, int32_t inte
     if (needed) *needed = t.size() + 1;
     if (!buf || cap < t.size() + 1) return fail(AMBPTT_EINVAL, "schedule: buffer too small");
     std::memcpy(buf, t.c_str(), t.size() + 1);
+    return AMBPTT_OK;
+  } catch (const std::exception& e) {
+    return fail(AMBPTT_EINTERNAL, e.what());
+  }
+}
+
+ambptt_status ambptt_resident_program(int64_t n, int32_t s, int64_t H, int32_t interval_min, int32_t elide_prefetch,
+                                      int32_t* buf, size_t cap, size_t* entries) {
+  if (n < 1 || s < 1 || H < 0 || interval_min < 0) return fail(AMBPTT_EINVAL, "resident program: bad arguments");
+  try {
+    const std::vector<int32_t> prog =
+        compile_resident(make_plan(n, s, H, std::max<int32_t>(interval_min, 1)), s, elide_prefetch != 0, nullptr);
+    const size_t m = prog.size() / 4;
+    if (entries) *entries = m;
+    if (!buf || cap < m) return fail(AMBPTT_EINVAL, "resident program: buffer too small");
+    std::memcpy(buf, prog.data(), prog.size() * sizeof(int32_t));
     return AMBPTT_OK;
   } catch (const std::exception& e) {
     return fail(AMBPTT_EINTERNAL, e.what());
@@ -644,6 +938,11 @@ ambptt_status ambptt_create(const ambptt_problem* p, void* stream, ambptt_ctx** 
   void* hl = nullptr;
   if ((e = hipHostMalloc(&hl, 64, hipHostMallocDefault)) != hipSuccess) return bail("hipHostMalloc", e);
   C->host_loss = (double*)hl;
+  void* sh = nullptr;
+  if ((e = hipHostMalloc(&sh, 64, hipHostMallocDefault)) != hipSuccess) return bail("hipHostMalloc", e);
+  C->status_host = (unsigned*)sh;
+  for (auto& ev : C->ev_r)
+    if ((e = hipEventCreate(&ev)) != hipSuccess) return bail("hipEventCreate", e);
   *out = C;
   return AMBPTT_OK;
 }
@@ -675,6 +974,16 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
     const Layout L2 = make_layout(&C->p, int(v == 0 ? wmax : v));
     // same offsets except the rings, which only shrink
     C->L.window = L2.window;
+  } else if (k == "path") {
+    if (v < 0 || v > 2) return fail(AMBPTT_EINVAL, "path must be 0 (auto), 1 (per-step launches) or 2 (resident)");
+    C->path_opt = int(v);
+  } else if (k == "resident_cooperative") {
+    C->res_coop = v != 0;
+  } else if (k == "resident_test_stall") {
+    C->res_test_stall = v != 0;
+  } else if (k == "resident_timeout_ms") {
+    if (v < 0 || v > 600000) return fail(AMBPTT_EINVAL, "resident_timeout_ms must be in [0, 600000]");
+    C->res_timeout_ms = v;
   } else if (k == "interval_min") {
     if (v < 0) return fail(AMBPTT_EINVAL, "interval_min must be >= 0");
     C->interval_min = v;
@@ -697,6 +1006,19 @@ ambptt_status ambptt_calibrate(ambptt_ctx* C, const void* x_seq, const void* W, 
                                const float* c0, int32_t* interval_min_out, double* t_a_us, double* t_t_us) {
   ambptt_status s = check_run_args(C, x_seq, W, b, h0, c0);
   if (s != AMBPTT_OK) return s;
+  if (C->path_opt == 2 && !resident_possible(C))
+    return fail(AMBPTT_EUNSUPPORTED, "the resident kernel does not fit this problem on this device");
+  if (resident_possible(C)) {
+    double ta = 0.0, tt = 0.0;
+    if ((s = resident_calibrate(C, x_seq, W, b, h0, c0, &ta, &tt)) != AMBPTT_OK) return s;
+    // transfers that lengthen a step by less than 5% count as hidden
+    const int64_t I = std::max<int64_t>(1, (int64_t)std::ceil(tt / ta - 0.05));
+    C->interval_min = I;
+    if (interval_min_out) *interval_min_out = int32_t(std::min<int64_t>(I, INT32_MAX));
+    if (t_a_us) *t_a_us = ta;
+    if (t_t_us) *t_t_us = tt;
+    return AMBPTT_OK;
+  }
   Exec E(C, x_seq, W, b);
   if ((s = prepare_inputs(C, W, h0, c0, E)) != AMBPTT_OK) return s;
   if ((s = ensure_host(C, C->L.stride)) != AMBPTT_OK) return s;
@@ -755,6 +1077,9 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   if (p.slow_slots > 0 && C->interval_min == 0) {
     if ((s = ambptt_calibrate(C, x_seq, W, b, h0, c0, nullptr, nullptr, nullptr)) != AMBPTT_OK) return s;
   }
+  if (C->path_opt == 2 && !resident_possible(C))
+    return fail(AMBPTT_EUNSUPPORTED, "the resident kernel does not fit this problem on this device");
+  if (resident_possible(C)) return resident_run(C, x_seq, W, b, h0, c0, dW, db, dh0, dc0, loss, stats);
   const double t0 = now_us();
   Plan plan;
   try {
@@ -836,6 +1161,13 @@ void ambptt_destroy(ambptt_ctx* C) {
   if (C->xs) (void)hipStreamDestroy(C->xs);
   if (C->host) (void)hipHostFree(C->host);
   if (C->host_loss) (void)hipHostFree(C->host_loss);
+  if (C->prog_host) {
+    (void)hipStreamSynchronize(C->cs);
+    (void)hipHostFree(C->prog_host);
+  }
+  if (C->status_host) (void)hipHostFree(C->status_host);
+  for (auto& ev : C->ev_r)
+    if (ev) (void)hipEventDestroy(ev);
   delete C;
 }
 

@@ -41,13 +41,18 @@ def device_inputs(wl, x, W, b, x0):
             t(x0["c"], torch.float32) if "c" in x0 else None)
 
 
-def run_gpu(wl, dev_in, window: int | None = None, timing_sample: int = 0, elide: bool = True, **spec_kw):
-    """One forward + reverse pass on the GPU; returns numpy results and stats."""
+def run_gpu(wl, dev_in, window: int | None = None, timing_sample: int = 0, elide: bool = True,
+            path: int | None = None, **spec_kw):
+    """One forward + reverse pass on the GPU; returns numpy results and stats.
+
+    path: None (library default), 1 (one launch per step), 2 (resident kernel)."""
     import paper_1806_01117_amd as amb
     spec = amb.ProblemSpec.from_workload(wl, **spec_kw)
-    say(wl.name, spec)
+    say(wl.name, spec, "path", path)
     r = amb.Runner(spec)
     try:
+        if path is not None:
+            r.set("path", path)
         if window is not None:
             r.set("window", window)
         if timing_sample:
@@ -57,6 +62,8 @@ def run_gpu(wl, dev_in, window: int | None = None, timing_sample: int = 0, elide
     finally:
         r.close()
     res = {k: (v.float().cpu().numpy() if hasattr(v, "cpu") else v) for k, v in out.items() if v is not None}
+    if path is not None:
+        assert res["stats"]["path"] == path - 1, "the requested path did not run"
     return res
 
 

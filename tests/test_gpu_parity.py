@@ -12,84 +12,117 @@ from gpu_util import (TOL_BF16, TOL_F32, assert_bitwise, assert_close, assert_cl
 
 pytestmark = pytest.mark.gpu
 
+# 1: one launch per step; 2: the resident whole-pass kernel
+PATHS = [pytest.param(1, id="steps"), pytest.param(2, id="resident")]
+
 
 def _case(wl):
     x, W, b, x0 = inputs(wl)
     return (x, W, b, x0), device_inputs(wl, x, W, b, x0)
 
 
-def test_rnn_workload_full():
+@pytest.mark.parametrize("path", PATHS)
+def test_rnn_workload_full(path):
     """64-wide tanh RNN, 128 steps, 4 slots, no host tier: Revolve, R = 517/128."""
     wl = synth.get("rnn_h64_t128")
     host, dev = _case(wl)
     want = run_oracle(wl, *host)
-    got = run_gpu(wl, dev)
+    got = run_gpu(wl, dev, path=path)
     st = got["stats"]
     assert st["mode"] == 0 and st["forward_evals"] == 517 == S.revolve_evals(128, 4)
     assert st["recompute_factor"] == pytest.approx(517 / 128)
     assert_close(got, want, TOL_F32)
-    allst = run_gpu(wl, dev, fast_slots=128)           # store-all: memory ratio 1
+    allst = run_gpu(wl, dev, fast_slots=128, path=path)  # store-all: memory ratio 1
     assert allst["stats"]["forward_evals"] == 128
     assert_bitwise(got, allst)
 
 
-def test_lstm_small_schedules_bitwise():
+@pytest.mark.parametrize("path", PATHS)
+def test_lstm_small_schedules_bitwise(path):
     """A reduced 512-LSTM: Revolve, async I=1, async I=3 and store-all agree bit for bit."""
     wl = synth.get("lstm_h512_t1000").with_(n_steps=48)
     host, dev = _case(wl)
     want = run_oracle(wl, *host)
-    ref = run_gpu(wl, dev, fast_slots=48, slow_slots=0)
+    ref = run_gpu(wl, dev, fast_slots=48, slow_slots=0, path=path)
     assert ref["stats"]["forward_evals"] == 48
     assert_close(ref, want, TOL_F32)
     for kw in (dict(fast_slots=3, slow_slots=0), dict(fast_slots=3, slow_slots=48, interval_min=1),
                dict(fast_slots=4, slow_slots=48, interval_min=3), dict(fast_slots=2, slow_slots=5, interval_min=1)):
-        got = run_gpu(wl, dev, **kw)
+        got = run_gpu(wl, dev, path=path, **kw)
         ev = S.schedule(48, kw["fast_slots"], kw["slow_slots"], kw.get("interval_min", 0))[0]["evals"]
         assert got["stats"]["forward_evals"] == ev
         assert_bitwise(got, ref)
 
 
-def test_lstm_ragged_shapes_and_window():
+@pytest.mark.parametrize("path", PATHS)
+def test_lstm_ragged_shapes_and_window(path):
     """Batch not a multiple of 16, a dW window that does not divide n, no prefetch elision."""
     wl = synth.get("lstm_h512_t1000").with_(batch=5, input=16, hidden=32, n_steps=37, name="lstm_ragged")
     host, dev = _case(wl)
     want = run_oracle(wl, *host)
-    a = run_gpu(wl, dev, fast_slots=37, slow_slots=0)
+    a = run_gpu(wl, dev, fast_slots=37, slow_slots=0, path=path)
     assert_close(a, want, TOL_F32)
-    b = run_gpu(wl, dev, fast_slots=3, slow_slots=37, interval_min=2, window=3, elide=False)
-    assert b["stats"]["mode"] == 1 and b["stats"]["window"] == 3
+    b = run_gpu(wl, dev, fast_slots=3, slow_slots=37, interval_min=2, window=3, elide=False, path=path)
+    assert b["stats"]["mode"] == 1 and b["stats"]["window"] == (3 if path == 1 else 0)
     assert b["stats"]["prefetches_elided"] == 0
     assert_close(b, want, TOL_F32)
-    c = run_gpu(wl, dev, fast_slots=3, slow_slots=37, interval_min=2)
-    assert_bitwise(b, c, keys=("loss", "dh0", "dc0"))
+    c = run_gpu(wl, dev, fast_slots=3, slow_slots=37, interval_min=2, path=path)
+    assert_bitwise(b, c, keys=("loss", "dh0", "dc0") if path == 1 else ("loss", "dW", "db", "dh0", "dc0"))
 
 
-@pytest.mark.parametrize("loss", ["half_sq_last", "mean_last"])
-def test_rnn_losses(loss):
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("loss", ["half_sq_last", "mean_last", "mean_sq_all"])
+def test_rnn_losses(loss, path):
     wl = synth.get("rnn_h64_t128").with_(loss=loss, n_steps=40, batch=20)
     host, dev = _case(wl)
     want = run_oracle(wl, *host)
-    got = run_gpu(wl, dev, fast_slots=3, slow_slots=40, interval_min=2)
+    got = run_gpu(wl, dev, fast_slots=3, slow_slots=40, interval_min=2, path=path)
     assert_close(got, want, TOL_F32)
 
 
-def test_lstm512_workload_full():
+@pytest.mark.parametrize("path", PATHS)
+def test_lstm512_workload_full(path):
     """512-LSTM, 1000 steps, 10 slots + host tier: async at I=1 and I=2, plain
     Revolve at the same 10 slots, all against the oracle and bit-exact."""
     wl = synth.get("lstm_h512_t1000")
     host, dev = _case(wl)
     want = run_oracle(wl, *host)
-    a1 = run_gpu(wl, dev, interval_min=1)
+    a1 = run_gpu(wl, dev, interval_min=1, path=path)
     assert a1["stats"]["mode"] == 1 and a1["stats"]["forward_evals"] == 1000   # R = 1
     assert_close(a1, want, TOL_F32)
-    a2 = run_gpu(wl, dev, interval_min=2)
+    a2 = run_gpu(wl, dev, interval_min=2, path=path)
     assert a2["stats"]["forward_evals"] == 1499
     assert_bitwise(a1, a2)
-    rv = run_gpu(wl, dev, slow_slots=0)
+    rv = run_gpu(wl, dev, slow_slots=0, path=path)
     assert rv["stats"]["forward_evals"] == 3637
     assert_bitwise(a1, rv)
     say("R async I=1/2, revolve:", a1["stats"]["recompute_factor"], a2["stats"]["recompute_factor"],
         rv["stats"]["recompute_factor"])
+
+
+def test_resident_abort_path():
+    """A resident pass whose first wait can never be satisfied ends in the
+    kernel's own timeout: the call fails with EINTERNAL, every workgroup
+    exits, and the next pass on the same context is correct."""
+    import paper_1806_01117_amd as amb
+    wl = synth.get("lstm_h512_t1000").with_(n_steps=24)
+    host, dev = _case(wl)
+    want = run_oracle(wl, *host)
+    spec = amb.ProblemSpec.from_workload(wl, fast_slots=3, slow_slots=24, interval_min=2)
+    r = amb.Runner(spec)
+    try:
+        r.set("path", 2)
+        r.set("resident_timeout_ms", 50)
+        r.set("resident_test_stall", 1)
+        with pytest.raises(amb.AmbpttError, match="timeout"):
+            r.run(*dev)
+        r.set("resident_test_stall", 0)
+        out = r.run(*dev)
+    finally:
+        r.close()
+    got = {k: (v.float().cpu().numpy() if hasattr(v, "cpu") else v) for k, v in out.items() if v is not None}
+    assert got["stats"]["path"] == 1
+    assert_close(got, want, TOL_F32)
 
 
 def test_lstm4096_shapes_short():
