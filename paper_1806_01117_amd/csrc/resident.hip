@@ -63,9 +63,9 @@ constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kCopyWave = kWaves - 1;        // issues the host-tier transfers
 constexpr int kStageThreads = 64 * kCopyWave;  // waves that stage step inputs
-constexpr int kKch = 6;                      // 16-wide reduction chunks per wave: D + H <= 768
-constexpr int kNbw = 5;                      // 16-column blocks of the partial product per wave: H <= 560
-constexpr int kHmax = 16 * (kWaves - 1) * kNbw;
+constexpr int kKch = 6;                      // most 16-wide reduction chunks per wave: D + H <= 768
+constexpr int kNbw = 5;                      // 16-column blocks of the partial product per wave
+constexpr int kHmax = 512;                   // H <= 512 (and <= 16 * 7 * kNbw)
 constexpr int kKmax = 16 * kWaves * kKch;
 constexpr int kXld = kKmax + 4;              // LDS row stride of the staged [x | h] rows
 constexpr int kDev = 16;                     // sc1: coherent across the device
@@ -73,8 +73,14 @@ constexpr int kSys = 17;                     // sc0 sc1: system scope (host memo
 
 typedef unsigned int u4v __attribute__((ext_vector_type(4)));
 
+// Every buffer this kernel addresses is the same for all lanes of a wave;
+// readfirstlane states that, so the descriptor lives in scalar registers even
+// where the compiler cannot prove it (otherwise it emits a loop over lanes).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, unsigned bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+  const unsigned long long p = (unsigned long long)base;
+  const unsigned lo = __builtin_amdgcn_readfirstlane(unsigned(p)), hi = __builtin_amdgcn_readfirstlane(unsigned(p >> 32));
+  void* ub = (void*)(((unsigned long long)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(ub, 0, __builtin_amdgcn_readfirstlane(bytes), 0x00020000);
 }
 template <int AUX>
 __device__ __forceinline__ f4 ld4(__amdgpu_buffer_rsrc_t r, unsigned off) {
@@ -106,7 +112,11 @@ __device__ __forceinline__ f4 mma4(const f4& a, const f4& b, f4 c) {
   return mfma_f32_16x16x4(a.w, b.w, c);
 }
 
-__device__ __forceinline__ float sigm(float z) { return 1.0f / (1.0f + __expf(-z)); }
+// Gate nonlinearities on the hardware exp2 and reciprocal (about 1 ulp each):
+// sigma(z) = 1 / (1 + e^-z), tanh(z) = 2 sigma(2z) - 1.  Both saturate
+// correctly for |z| -> inf (e^-z -> inf gives 0, -> 0 gives 1).
+__device__ __forceinline__ float sigm(float z) { return __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
+__device__ __forceinline__ float tanh_f(float z) { return 2.0f * sigm(2.0f * z) - 1.0f; }
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -114,7 +124,9 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-template <int G>
+// KCH: 16-wide reduction chunks per wave (the reduction is zero-padded to
+// 8 KCH chunks, so no loop over chunks has a bound that varies by wave)
+template <int G, int KCH>
 __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
   constexpr int U = (G == 4) ? 8 : 16;
   constexpr int NC = G * U;            // gate columns of the workgroup (32 | 16)
@@ -142,7 +154,7 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
   const int me = mt * ng + ug;
   const int m0 = 16 * mt, j0 = U * ug;
   const int nch = K1 / 16;
-  const int c0 = (nch * wave) / kWaves, c1 = (nch * (wave + 1)) / kWaves;
+  const int c0 = KCH * wave;  // chunks c0 .. c0 + KCH - 1; those >= nch are zero
   const int hb16 = H / 16;
   const unsigned hbytes = unsigned(B) * unsigned(H) * 4u;
   const unsigned sbytes = G == 4 ? unsigned(a.c_off) + hbytes : hbytes;
@@ -156,35 +168,41 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
   __shared__ __attribute__((aligned(16))) float zb[16][NC + 4];  // zbar_t of the workgroup
   __shared__ float hp[NGRP][NS];                               // partial h-adjoint sums
   __shared__ float cbs[NS];                                    // cbar carried between adjoints
-  __shared__ __attribute__((aligned(16))) float whs[NC * (kHmax + 4)];  // W_h rows of the gate columns
-  __shared__ float wsum[kWaves];
+  __shared__ __attribute__((aligned(16))) float whs[kHmax * (NC + 4)];  // W_h^T of the gate columns
+  __shared__ __attribute__((aligned(16))) float stg[2 * NS];  // the last forward step's output slice (h, c)
+  __shared__ double wsum[kWaves];
   __shared__ int stop;
 
   // ---- weights into registers ---------------------------------------------
-  f4 Wr[kKch][NB];  // B operands of the gate GEMM: W[col][16 ch + 4 q + e]
+  f4 Wr[KCH][NB];  // B operands of the gate GEMM: W[col][16 ch + 4 q + e]
 #pragma unroll
-  for (int i = 0; i < kKch; ++i) {
+  for (int i = 0; i < KCH; ++i) {
     const int ch = c0 + i;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
-      Wr[i][nb] = ch < c1 ? *(const f4*)(a.W + (size_t)wrow(nb * 16 + r) * K1 + ch * 16 + 4 * q)
-                          : f4{0.f, 0.f, 0.f, 0.f};
+      Wr[i][nb] = ch < nch ? *(const f4*)(a.W + (size_t)wrow(nb * 16 + r) * K1 + ch * 16 + 4 * q)
+                           : f4{0.f, 0.f, 0.f, 0.f};
   }
-  // rows of W_h for the workgroup's gate columns (the partial product's B
-  // operand), whs[n][j] = W[wrow(n)][D + j]; the row stride H + 4 keeps the
-  // four row groups of a wave's read on different banks
-  const int whld = H + 4;
-  for (int idx = tid; idx < NC * (H / 4); idx += kThreads) {
-    const int n = idx / (H / 4), col = 4 * (idx % (H / 4));
-    *(f4*)&whs[n * whld + col] = *(const f4*)(a.W + (size_t)wrow(n) * K1 + D + col);
+  // W_h^T for the workgroup's gate columns (the partial product's B
+  // operand): whs[j][n] = W[wrow(n)][D + j], so that a lane's four reduction
+  // indices n = 16 ch + 4 q .. + 3 are one 16-byte read
+  constexpr int WLD = NC + 4;
+  for (int idx = tid; idx < NC * H; idx += kThreads) {
+    const int n = idx / H, j = idx % H;
+    whs[j * WLD + n] = a.W[(size_t)wrow(n) * K1 + D + j];
   }
-  f4 dacc[kKch][NB];  // dW blocks (gate block nb, reduction chunk c0 + i)
+  // reduction columns K1 .. 16 * 8 KCH of the staged rows stay zero
+  for (int idx = tid; idx < 16 * (16 * kWaves * KCH - K1); idx += kThreads) {
+    const int w = 16 * kWaves * KCH - K1;
+    xs[idx / w][K1 + idx % w] = 0.f;
+  }
+  f4 dacc[KCH][NB];  // dW blocks (gate block nb, reduction chunk c0 + i)
 #pragma unroll
-  for (int i = 0; i < kKch; ++i)
+  for (int i = 0; i < KCH; ++i)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) dacc[i][nb] = f4{0.f, 0.f, 0.f, 0.f};
   float dbacc = 0.f;
-  double lacc = 0.0;
+  double lacc = 0.0;  // loss terms of this thread's (row, unit), summed over the adjoint steps in order
 
   // epilogue thread (ml, u) of the slice
   const bool epi = tid < NS;
@@ -212,16 +230,44 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
   unsigned sc = 0;     // group barriers passed
   int na = 0;          // adjoint steps done
   int pend_pref = -1;  // slot of the prefetch whose data the copy wave holds
+  int pref_next = -1;  // program entry of the next prefetch (its host read may start early)
+  int early_pc = -1;   // entry whose host read was started at the last prefetch's landing
+  bool pcie_st = false;  // host-tier stores issued since the copy wave last waited
+  bool early_after_st = false;  // an early host read was issued after the slot store being drained
   int pend_store = -1; // host slot of the store whose data the copy wave holds
   bool dirty = false;  // the copy wave wrote a slot since its last drain
   f4 pv = f4{0.f, 0.f, 0.f, 0.f}, sv = f4{0.f, 0.f, 0.f, 0.f};
   int pc = 0;
+  // the program is read-only for the whole launch: reading it through the
+  // constant address space makes every entry a scalar load, which no wave
+  // waits for behind its own vector memory traffic (host-link reads and
+  // writes of the copy wave in particular)
+  const __attribute__((address_space(4))) int* prog = (const __attribute__((address_space(4))) int*)a.prog;
 
   // all stores of this workgroup that others may read are complete
   auto drain = [&]() {
-    if (wave != kCopyWave || dirty) __builtin_amdgcn_s_waitcnt(0);
+    if (wave != kCopyWave) {
+      __builtin_amdgcn_s_waitcnt(0);
+    } else if (dirty) {
+      // the slot store issued by the last flush must land; an early host read
+      // issued after it may stay in flight (vector memory counts retire in order)
+      if (early_after_st) __builtin_amdgcn_s_waitcnt(0x0F71);  // vmcnt(1)
+      else __builtin_amdgcn_s_waitcnt(0x0F70);                 // vmcnt(0)
+      pcie_st = pcie_st && early_after_st;
+    }
     dirty = false;
+    early_after_st = false;
     __syncthreads();
+  };
+  // copy wave: host read of the slice of host slot h into pv.  The data are
+  // first used by the slot store at the next flush, so the read stays in
+  // flight across everything the wave does until then.
+  auto host_read = [&](int h) {
+    if (pcie_st) {  // a store to the host tier may target the same slot: let it land first
+      __builtin_amdgcn_s_waitcnt(0x0F70);
+      pcie_st = false;
+    }
+    if (cl_ok) pv = ld4<kSys>(host_rsrc(h), unsigned(lane) * 16u);
   };
   // wave 0 waits until every member's flag reaches target
   auto wait_group = [&](const unsigned* flags, unsigned target) -> bool {
@@ -255,8 +301,43 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
     __syncthreads();
     return stop == 0;
   };
-  auto enter = [&]() -> bool {  // group barrier number sc + 1 (caller drained)
+  // weight gradient of the workgroup's gate rows for the last adjoint step,
+  // dW += zbar^T [x | h], on the wave's own reduction chunks (block (nb,
+  // chunk c0 + i) of 16 x 16).  It feeds nothing the other workgroups wait
+  // for, so it runs after this workgroup has raised its flag for the next
+  // barrier, while the flags of the others are on their way.
+  bool pend_dw = false;
+  auto deferred_dw = [&]() {
+#pragma unroll 2
+    for (int c4 = 0; c4 < 4; ++c4) {
+      float av[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) av[nb] = zb[4 * c4 + q][nb * 16 + r];
+      float bv[KCH];
+#pragma unroll
+      for (int i = 0; i < KCH; ++i) bv[i] = xs[4 * c4 + q][(c0 + i) * 16 + r];
+#pragma unroll
+      for (int i = 0; i < KCH; ++i)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) dacc[i][nb] = mfma_f32_16x16x4(av[nb], bv[i], dacc[i][nb]);
+    }
+    if (tid < NC) {
+      float s = 0.f;
+#pragma unroll
+      for (int row = 0; row < 16; ++row) s += zb[row][tid];
+      dbacc += s;
+    }
+    pend_dw = false;
+  };
+  // group barrier number sc + 1, in two halves (the caller drained first)
+  auto raise = [&]() {
     if (tid == 0) st_flag(a.ready + me, sc + 1);
+    if (pend_dw) {
+      deferred_dw();
+      __syncthreads();  // its reads of the staged rows come before new rows are staged
+    }
+  };
+  auto enter = [&]() -> bool {
     if (!wait_group(a.ready, sc + 1)) return false;
     ++sc;
     return true;
@@ -266,9 +347,16 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
       if (cl_ok) st4<kDev>(rsrc(buf(pend_pref), sbytes), cl_off, pv);
       dirty = true;
       pend_pref = -1;
+      if (pref_next >= 0) {  // start the next prefetch's host read now (pv is free again)
+        if (wave == kCopyWave) host_read(prog[4 * pref_next + 2]);
+        early_pc = pref_next;
+        early_after_st = true;
+        pref_next = -1;
+      }
     }
     if (pend_store >= 0) {
       if (cl_ok) st4<kSys>(host_rsrc(pend_store), unsigned(lane) * 16u, sv);
+      pcie_st = true;
       pend_store = -1;
     }
   };
@@ -282,6 +370,7 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
   // one forward (adj = false) or adjoint step t from buffer src
   auto step = [&](int t, int src, int dst, bool adj, bool first) -> bool {
     drain();
+    raise();
     const char* sb = buf(src);
     const __amdgpu_buffer_rsrc_t srs = rsrc(sb, sbytes);
     // inputs that do not depend on the other members, staged while wave 0
@@ -326,13 +415,10 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) acc[nb] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < kKch; ++i) {
-        const int ch = c0 + i;
-        if (ch < c1) {
-          const f4 av = *(const f4*)&xs[r][ch * 16 + 4 * q];
+      for (int i = 0; i < KCH; ++i) {
+        const f4 av = *(const f4*)&xs[r][(c0 + i) * 16 + 4 * q];
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) acc[nb] = mma4(av, Wr[i][nb], acc[nb]);
-        }
+        for (int nb = 0; nb < NB; ++nb) acc[nb] = mma4(av, Wr[i][nb], acc[nb]);
       }
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
@@ -355,13 +441,13 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
       if (G == 4) {
         ig = sigm(z[0]);
         fg = sigm(z[1 % G]);
-        gg = tanhf(z[2 % G]);
+        gg = tanh_f(z[2 % G]);
         og = sigm(z[3 % G]);
         c1 = fg * cold + ig * gg;
-        tc = tanhf(c1);
+        tc = tanh_f(c1);
         h1 = og * tc;
       } else {
-        h1 = tanhf(z[0]);
+        h1 = tanh_f(z[0]);
       }
       if (!adj) {
         if (erow) {
@@ -369,6 +455,8 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
           st1<kDev>(drs, eoff, h1);
           if (G == 4) st1<kDev>(drs, unsigned(a.c_off) + eoff, c1);
         }
+        stg[tid] = h1;  // host-slice order: h [16][U], then c [16][U]
+        if (G == 4) stg[NS + tid] = c1;
       } else {
         float hbar = 0.f;
         if (!first) {
@@ -402,70 +490,41 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
           zb[ml][u] = erow ? hb * (1.f - h1 * h1) : 0.f;
         }
         if (!erow) lterm = 0.f;
+        lacc += (double)lterm;
       }
     }
     if (!adj) return true;
-
-    const float ls = wave_sum(lterm);
-    if (lane == 0) wsum[wave] = ls;
     __syncthreads();
-    if (tid == 0) {
-      float s = 0.f;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) s += wsum[w];
-      lacc += (double)s;
-    }
     // partial h-adjoint of the workgroup's gate columns, to the owners of the units
     if (wave < kCopyWave) {
       float* pbase = a.P + (((size_t)(na & 1) * a.mtiles + mt) * ng) * ng * NS;
       const __amdgpu_buffer_rsrc_t prs = rsrc(pbase, unsigned(ng * ng * NS * 4));
+      f4 av[KW];
+#pragma unroll
+      for (int ch = 0; ch < KW; ++ch) av[ch] = *(const f4*)&zb[r][16 * ch + 4 * q];
 #pragma unroll
       for (int i = 0; i < kNbw; ++i) {
         const int jb = wave + kCopyWave * i;
         if (jb < hb16) {
+          f4 bv[KW];
+#pragma unroll
+          for (int ch = 0; ch < KW; ++ch) bv[ch] = *(const f4*)&whs[(jb * 16 + r) * WLD + 16 * ch + 4 * q];
           f4 acc = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int ch = 0; ch < KW; ++ch) {
-            const f4 av = *(const f4*)&zb[r][16 * ch + 4 * q];
-            const float* wb = &whs[(16 * ch + 4 * q) * whld + jb * 16 + r];
-            const f4 bv = f4{wb[0], wb[whld], wb[2 * whld], wb[3 * whld]};
-            acc = mma4(av, bv, acc);
-          }
+          for (int ch = 0; ch < KW; ++ch) acc = mma4(av[ch], bv[ch], acc);
           const int col = jb * 16 + r, dsw = col / U, du = col % U;
           st4<kDev>(prs, unsigned(((dsw * ng + ug) * NS + du * 16 + 4 * q) * 4), acc);
         }
       }
     }
-    // weight gradient of the workgroup's gate rows, dW += zbar^T [x | h], on
-    // the wave's own reduction chunks (block (nb, chunk) of 16 x 16)
-#pragma unroll
-    for (int c4 = 0; c4 < 4; ++c4) {
-      float av[NB];
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) av[nb] = zb[4 * c4 + q][nb * 16 + r];
-#pragma unroll
-      for (int i = 0; i < kKch; ++i) {
-        const int ch = c0 + i;
-        if (ch < c1) {
-          const float bv = xs[4 * c4 + q][ch * 16 + r];
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) dacc[i][nb] = mfma_f32_16x16x4(av[nb], bv, dacc[i][nb]);
-        }
-      }
-    }
-    if (tid < NC) {
-      float s = 0.f;
-#pragma unroll
-      for (int row = 0; row < 16; ++row) s += zb[row][tid];
-      dbacc += s;
-    }
+    pend_dw = true;
     ++na;
     return true;
   };
 
   bool ok = true, ended = false;
   for (pc = 0; pc < a.nprog && ok; ++pc) {
-    const int* op = a.prog + 4 * pc;
+    const __attribute__((address_space(4))) int* op = prog + 4 * pc;
     const int code = op[0] & 0xff;
     if (code == kPFwd || code == kPAdj) {
       ok = step(op[1], op[2], op[3], code == kPAdj, code == kPAdj && op[3] != 0);
@@ -481,13 +540,19 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
         if (G == 4) st1<kDev>(d, unsigned(a.c_off) + eoff, ld1<kDev>(s, unsigned(a.c_off) + eoff));
       }
     } else if (code == kPStore) {
-      drain();
+      const bool staged = (op[0] & kPStaged) != 0;
+      if (staged) __syncthreads();  // the step's output slice is in LDS
+      else drain();
       if (wave == kCopyWave) {
         if (pend_store >= 0) {
           if (cl_ok) st4<kSys>(host_rsrc(pend_store), unsigned(lane) * 16u, sv);
         }
-        if (cl_ok) sv = ld4<kDev>(rsrc(buf(op[2]), sbytes), cl_off);
-        dirty = true;  // the slot may be rewritten after the next barrier: land the load first
+        if (staged) {
+          sv = *(const f4*)&stg[4 * lane];
+        } else {
+          if (cl_ok) sv = ld4<kDev>(rsrc(buf(op[2]), sbytes), cl_off);
+          dirty = true;  // the slot may be rewritten after the next barrier: land the load first
+        }
       }
       pend_store = op[3];
     } else if (code == kPPref) {
@@ -497,21 +562,23 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
         ok = false;
         break;
       }
-      if (wave == kCopyWave) {
-        if (pend_store >= 0) {  // the host slot may be the one being stored
-          if (cl_ok) st4<kSys>(host_rsrc(pend_store), unsigned(lane) * 16u, sv);
-          __builtin_amdgcn_s_waitcnt(0);
-        }
-        if (cl_ok) pv = ld4<kSys>(host_rsrc(op[2]), unsigned(lane) * 16u);
+      if (pend_store >= 0) {  // the host slot may be the one being stored
+        if (cl_ok) st4<kSys>(host_rsrc(pend_store), unsigned(lane) * 16u, sv);
+        pcie_st = true;
       }
+      if (early_pc != pc && wave == kCopyWave) host_read(op[2]);  // else it started at the last landing
+      early_pc = -1;
       pend_store = -1;
       pend_pref = op[3];
+      pref_next = op[1] > 0 ? op[1] : -1;
     } else if (code == kPSync) {
       drain();
+      raise();
       ok = enter();
       if (ok) flush();
     } else if (code == kPEnd) {
       drain();
+      raise();
       ok = enter();
       if (ok) flush();
       ended = ok;
@@ -542,9 +609,9 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
     if (G == 4) a.dc0[em * H + ej] = cbs[tid];
   }
 #pragma unroll
-  for (int i = 0; i < kKch; ++i) {
+  for (int i = 0; i < KCH; ++i) {
     const int ch = c0 + i;
-    if (ch < c1) {
+    if (ch < nch) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
@@ -553,7 +620,19 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
     }
   }
   if (tid < NC) a.dbp[(size_t)mt * GH + wrow(tid)] = dbacc;
-  if (tid == 0) a.loss_acc[me] = lacc;
+  {
+    double v = lacc;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+    if (lane == 0) wsum[wave] = v;
+    __syncthreads();
+    if (tid == 0) {
+      double t = 0.0;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) t += wsum[w];
+      a.loss_acc[me] = t;
+    }
+  }
 }
 
 __global__ void resident_reduce(const float* __restrict__ dWp, const float* __restrict__ dbp, int mtiles, int GH,
@@ -576,6 +655,7 @@ __global__ void resident_reduce(const float* __restrict__ dWp, const float* __re
 int resident_units(int G) { return G == 4 ? 8 : 16; }
 int resident_max_k(int) { return kKmax; }
 int resident_max_h(int) { return kHmax; }
+static_assert(kHmax <= 16 * kCopyWave * kNbw, "partial-product blocks");
 
 hipError_t resident_capacity(int G, int* blocks) {
   int dev = 0, per = 0;
@@ -583,8 +663,8 @@ hipError_t resident_capacity(int G, int* blocks) {
   hipError_t e;
   if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
   if ((e = hipGetDeviceProperties(&prop, dev)) != hipSuccess) return e;
-  if (G == 4) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, resident_pass<4>, kThreads, 0);
-  else e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, resident_pass<1>, kThreads, 0);
+  if (G == 4) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, resident_pass<4, kKch>, kThreads, 0);
+  else e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, resident_pass<1, kKch>, kThreads, 0);
   if (e != hipSuccess) return e;
   *blocks = prop.cooperativeLaunch ? per * prop.multiProcessorCount : 0;
   return hipSuccess;
@@ -594,7 +674,12 @@ hipError_t launch_resident(int G, const ResidentArgs& a, hipStream_t s, bool coo
   ResidentArgs arg = a;
   void* args[] = {&arg};
   const dim3 grid(unsigned(a.mtiles * a.ng)), block(kThreads);
-  const void* fn = G == 4 ? (const void*)resident_pass<4> : (const void*)resident_pass<1>;
+  const int nch = (a.D + a.H) / 16, kch = (nch + kWaves - 1) / kWaves;
+  const void* fn;
+  if (kch <= 1) fn = G == 4 ? (const void*)resident_pass<4, 1> : (const void*)resident_pass<1, 1>;
+  else if (kch <= 2) fn = G == 4 ? (const void*)resident_pass<4, 2> : (const void*)resident_pass<1, 2>;
+  else if (kch <= 3) fn = G == 4 ? (const void*)resident_pass<4, 3> : (const void*)resident_pass<1, 3>;
+  else fn = G == 4 ? (const void*)resident_pass<4, kKch> : (const void*)resident_pass<1, kKch>;
   if (cooperative) return hipLaunchCooperativeKernel(fn, grid, block, args, 0, s);
   // plain launch: the caller checked that the grid fits the device at once;
   // if other work keeps some workgroups out, the bounded waits end the pass

@@ -98,7 +98,11 @@ std::vector<int32_t> compile_resident(const Plan& plan, int nslots, bool elide_p
       }
       case Op::Store: {
         if (pend_pref == int(A.a)) sync();
-        emit(kPStore, 0, A.a, A.b);
+        // right after the step that wrote the slot, each workgroup still
+        // holds its slice in LDS and need not read it back from HBM
+        const size_t m = prog.size();
+        const bool staged = m >= 4 && prog[m - 4] == kPFwd && prog[m - 1] == int32_t(A.a);
+        emit(kPStore | (staged ? kPStaged : 0), 0, A.a, A.b);
         c.stores++;
         break;
       }
@@ -123,6 +127,26 @@ std::vector<int32_t> compile_resident(const Plan& plan, int nslots, bool elide_p
   }
   barrier_op(kPEnd, 0, 0, 0);
   c.barriers = bar;
+  // Each prefetch names the entry of the next one (y), whose host read the
+  // kernel may then start when this one lands, as long as every store into
+  // that host slot comes earlier in the program.
+  {
+    const size_t m = prog.size() / 4;
+    std::vector<int64_t> last_store;  // host slot -> last entry storing it
+    std::vector<size_t> prefs;
+    for (size_t i = 0; i < m; ++i) {
+      if ((prog[4 * i] & 0xFF) == kPPref) prefs.push_back(i);
+    }
+    for (size_t j = 0; j + 1 < prefs.size(); ++j) {
+      const size_t i0 = prefs[j], i1 = prefs[j + 1];
+      const int32_t h = prog[4 * i1 + 2];
+      bool later_store = false;
+      for (size_t i = i0; i < i1 && !later_store; ++i)
+        later_store = (prog[4 * i] & 0xFF) == kPStore && prog[4 * i + 3] == h;
+      if (!later_store) prog[4 * i0 + 1] = int32_t(i1);
+    }
+    (void)last_store;
+  }
   if (c.forward_evals != plan.evals) throw std::logic_error("resident program: forward count differs from the schedule");
   if (counts) *counts = c;
   return prog;

@@ -14,7 +14,10 @@ namespace ambptt {
 //   kPAdj   y = t, z = src buffer, w = 1 if first       adjoint step t
 //   kPCopy  y = wait (0: none), z = src, w = dst        copy of a state
 //   kPStore z = slot, w = host slot                     slot -> host tier
-//   kPPref  z = host slot, w = slot                     host tier -> slot
+//           (| kPStaged: taken from the previous step's output in LDS)
+//   kPPref  y = entry of the next kPPref whose host read may start when
+//               this one lands (0: none), z = host slot, w = slot
+//                                                       host tier -> slot
 //   kPSync                                              group barrier only
 //   kPEnd                                               dL/dx_0, dW, loss
 // Buffer ids: 0 .. nslots-1 are the HBM slots, nslots and nslots+1 the two
@@ -30,6 +33,9 @@ namespace ambptt {
 //   - a copy into a buffer that the latest step read waits until every
 //     member has read that step's inputs (y = that barrier's number).
 enum ResidentOp : int32_t { kPEnd = 0, kPFwd = 1, kPAdj = 2, kPCopy = 3, kPStore = 4, kPPref = 5, kPSync = 6 };
+// flag on kPStore (op | kPStaged): the previous entry is the forward step that
+// wrote the slot, whose output slice the workgroup still holds in LDS
+constexpr int32_t kPStaged = 1 << 8;
 
 struct ResidentCounts {
   int64_t forward_evals = 0, adjoints = 0, takeshots = 0, takeshot_copies = 0, restores = 0;

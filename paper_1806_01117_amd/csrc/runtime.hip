@@ -736,16 +736,20 @@ ambptt_status resident_calibrate(ambptt_ctx* C, const void* x, const void* W, co
     std::vector<int32_t> v;
     int cur = L0;
     for (int i = 0; i < steps; ++i) {
-      const int dst = cur == L0 ? L1 : L0;
+      // stores as in the sweep: each step's output lands in a tier slot and
+      // goes to the host right away; prefetches as in the reverse sweep
+      const int dst = kind == 1 ? i % 2 : (cur == L0 ? L1 : L0);
       v.insert(v.end(), {kPFwd, int32_t(i % p.n_steps), cur, dst});
       cur = dst;
-      if (kind == 1) v.insert(v.end(), {kPStore, 0, 0, i % 2});
-      if (kind == 2) v.insert(v.end(), {kPPref, 0, i % 2, 0});
+      if (kind == 1) v.insert(v.end(), {kPStore | kPStaged, 0, dst, i % 2});
+      // each prefetch names the next one (entry 2 i + 3), as compiled programs do
+      if (kind == 2) v.insert(v.end(), {kPPref, i + 1 < steps ? 2 * i + 3 : 0, i % 2, i % 2});
     }
     return v;
   };
   double per[3] = {0, 0, 0};
-  for (int kind = 0; kind < 3; ++kind) {
+  const int kinds = p.fast_slots >= 2 ? 3 : 1;  // the host tier needs two slots
+  for (int kind = 0; kind < kinds; ++kind) {
     float ms[2] = {0.f, 0.f};
     const int steps[2] = {16, 80};
     for (int rep = 0; rep < 2; ++rep) {  // the first round warms up

@@ -12,7 +12,10 @@ step.  Its rules, modelled here:
   * a copy is readable from the next barrier; a copy into a buffer that the
     latest step read must first wait for every workgroup to read it;
   * a store reads the slot at once and writes host memory at the next
-    barrier (or at the next store or prefetch).
+    barrier (or at the next store or prefetch); a store flagged "staged"
+    takes the slice from the output the workgroup just computed, which is
+    only right when the previous entry is the forward step that wrote the
+    slot.
 Under those rules every program must reproduce store-all BPTT bit for bit
 (the schedule decides which states are recomputed, never the arithmetic),
 and its forward count must be the schedule's.
@@ -26,6 +29,7 @@ from oracle.cells import Cell
 amb = pytest.importorskip("paper_1806_01117_amd")
 
 FWD, ADJ, COPY, STORE, PREF, SYNC, END = 1, 2, 3, 4, 5, 6, 0
+STAGED = 1 << 8   # store flag: the slice comes from the previous entry's output in LDS
 
 
 def _cell(kind="lstm", loss="half_sq_last", B=2, D=3, H=4, seed=0):
@@ -62,7 +66,13 @@ def replay_program(prog, cell, n, s, u_of, x0):
             pend_store = None
 
     ended = False
-    for op, y, z, w in prog:
+    prev = None
+    for entry in prog:
+        op, y, z, w = entry
+        flags, op = op >> 8, op & 0xFF
+        if op == STORE and flags & 1:
+            assert prev is not None and prev[0] == FWD and prev[3] == z, "staged store not right after its step"
+        prev = (op, y, z, w)
         assert not ended, "entries after the end"
         if op in (FWD, ADJ):
             bar += 1
@@ -130,6 +140,17 @@ def test_program_reproduces_store_all(n, s, H, I, elide):
         assert np.array_equal(a, b)
 
 
+def test_replayer_catches_a_misplaced_staged_store():
+    cell, x0, rng = _cell()
+    n, s = 30, 4
+    us = [rng.standard_normal((2, 3)) for _ in range(n)]
+    prog = amb.resident_program(n, s, n, 2)
+    i = next(i for i, e in enumerate(prog) if e[0] == STORE | STAGED)
+    broken = prog[:i - 1] + [prog[i], prog[i - 1]] + prog[i + 1:]   # the store before its step
+    with pytest.raises(AssertionError):
+        replay_program(broken, cell, n, s, lambda t: us[t], x0)
+
+
 def test_program_rnn_and_losses():
     for kind in ("rnn", "lstm"):
         for loss in ("half_sq_last", "mean_sq_all", "mean_last"):
@@ -149,11 +170,11 @@ def test_replayer_catches_a_broken_program():
     us = [rng.standard_normal((2, 3)) for _ in range(n)]
     prog = amb.resident_program(n, s, 100, 3, False)
     # drop every barrier-only entry: some step then reads a prefetched slot too early
-    broken = [e for e in prog if e[0] != SYNC]
+    broken = [e for e in prog if e[0] & 0xFF != SYNC]
     if len(broken) == len(prog):  # no extra barrier in this program: move a prefetch right before its reader
-        i = next(i for i, e in enumerate(prog) if e[0] == PREF)
+        i = next(i for i, e in enumerate(prog) if e[0] & 0xFF == PREF)
         k = prog[i][3]
-        j = next(j for j in range(i + 1, len(prog)) if prog[j][0] in (FWD, ADJ) and prog[j][2] == k)
+        j = next(j for j in range(i + 1, len(prog)) if prog[j][0] & 0xFF in (FWD, ADJ) and prog[j][2] == k)
         broken = prog[:i] + prog[i + 1:j] + [prog[i]] + prog[j:]
     with pytest.raises(AssertionError):
         replay_program(broken, cell, n, s, lambda t: us[t], x0)
@@ -161,7 +182,9 @@ def test_replayer_catches_a_broken_program():
 
 def test_program_entry_limits():
     prog = amb.resident_program(1000, 10, 1000, 2)
-    ops = [e[0] for e in prog]
+    ops = [e[0] & 0xFF for e in prog]
+    staged = [e for e in prog if e[0] == STORE | STAGED]
+    assert len(staged) == ops.count(STORE) - 1   # all but the first state's store come from LDS
     assert ops[-1] == END and ops.count(END) == 1
     assert ops.count(ADJ) == 1000
-    assert all(0 <= e[2] < 12 and 0 <= e[3] < 1000 for e in prog if e[0] in (FWD, COPY))
+    assert all(0 <= e[2] < 12 and 0 <= e[3] < 1000 for e in prog if e[0] & 0xFF in (FWD, COPY))
