@@ -88,7 +88,8 @@ struct ResidentArgs {
   size_t c_off;         // byte offset of c within a state (LSTM)
   int nslots;
   char* host;           // host tier (device-visible): [host slot][workgroup][1 KiB]
-  float* P;             // partial h-adjoints [2][mtiles][ng][ng][16 U]
+  float* Z;             // zbar slices for the octets [2][mtiles][ng][16][G U]
+  float* P;             // octet partial h-adjoints [2][mtiles][ng / S][H][16]
   float* dWp;           // per row tile dW partials [mtiles][G*H][D+H]
   float* dbp;           // [mtiles][G*H]
   float* dh0;           // [B][H]
@@ -96,10 +97,12 @@ struct ResidentArgs {
   double* loss_acc;     // [mtiles * ng]
   unsigned* ready;      // [mtiles * ng] syncs entered (zero before launch)
   unsigned* consumed;   // [mtiles * ng] syncs whose inputs are read (zero before launch)
+  unsigned* oflag;      // [mtiles * ng] adjoint steps whose zbar slice is out (zero before launch)
   unsigned* status;     // [0]: abort flag, [1]: op index of the abort + 1
   long long timeout;    // s_memrealtime ticks (100 MHz) a wait may take
   int B, D, H, loss;
   int mtiles, ng;       // row tiles (16 rows); unit groups per row tile
+  int S;                // octet size: min(8, ng), dividing ng, with H / S <= 64
   int xcd_map;          // 1: place each row tile's workgroups on 8 / mtiles XCDs
   float inv_bh;
 };
@@ -109,6 +112,8 @@ int resident_units(int G);
 // largest D + H and H the resident kernel holds in registers
 int resident_max_k(int G);
 int resident_max_h(int G);
+// octet size for ng unit groups of hidden size H (0: the kernel cannot take it)
+int resident_octet(int ng, int H);
 // workgroups of the resident kernel that can be resident at once on device dev
 hipError_t resident_capacity(int G, int* blocks);
 // cooperative: hipLaunchCooperativeKernel (the runtime guarantees that the

@@ -64,8 +64,9 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kCopyWave = kWaves - 1;        // issues the host-tier transfers
 constexpr int kStageThreads = 64 * kCopyWave;  // waves that stage step inputs
 constexpr int kKch = 6;                      // most 16-wide reduction chunks per wave: D + H <= 768
-constexpr int kNbw = 5;                      // 16-column blocks of the partial product per wave
-constexpr int kHmax = 512;                   // H <= 512 (and <= 16 * 7 * kNbw)
+constexpr int kHmax = 512;                   // H <= 512
+constexpr int kSmax = 8;                     // workgroups per octet (the first level of the h-adjoint sum)
+constexpr int kUMmax = 64;                   // hidden units per octet member in that sum: H / S <= 64
 constexpr int kKmax = 16 * kWaves * kKch;
 constexpr int kXld = kKmax + 4;              // LDS row stride of the staged [x | h] rows
 constexpr int kDev = 16;                     // sc1: coherent across the device
@@ -133,29 +134,34 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
   constexpr int NB = NC / 16;          // 16-column MFMA blocks of the gate GEMM
   constexpr int KW = NC / 16;          // 16-wide chunks of the partial product's reduction
   constexpr int NS = 16 * U;           // (row, unit) pairs of the slice (128 | 256)
-  constexpr int NG4 = NS / 4;          // float4s of one partial slab (32 | 64)
-  constexpr int NGRP = kStageThreads / NG4;  // thread groups summing partials (14 | 7)
+  constexpr int NG4 = NS / 4;          // float4s of one slice of partial sums (32 | 64)
   constexpr int PER = U / 4;           // float4s per slice row
-  static_assert(kStageThreads % NG4 == 0, "partial-sum groups");
+  constexpr int OK = kSmax * NC;       // gate columns of an octet (reduction of its partial product)
+  constexpr int OLD = OK + 4;          // LDS row stride of the octet's zbar and of W_h^T
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, q = lane >> 4;
   const int B = a.B, D = a.D, H = a.H, K1 = D + H, GH = G * H;
   const int ng = a.ng, nwg = a.mtiles * a.ng;
   int mt, ug;
-  if (a.xcd_map) {  // ids are dealt to the 8 XCDs round-robin: keep a row tile on 8 / mtiles of them
+  if (a.xcd_map) {
+    // ids are dealt to the 8 XCDs round-robin: a row tile takes 8 / mtiles
+    // XCDs, and consecutive unit groups (so whole octets) share one
     const int per = 8 / a.mtiles, x = int(blockIdx.x % 8);
     mt = x / per;
-    ug = int(blockIdx.x / 8) * per + x % per;
+    ug = (x % per) * (ng / per) + int(blockIdx.x / 8);
   } else {
     mt = int(blockIdx.x) / ng;
     ug = int(blockIdx.x) % ng;
   }
   const int me = mt * ng + ug;
+  // octets: S consecutive unit groups of a row tile (S = min(8, ng))
+  const int S = a.S, nO = ng / S, oc = ug / S, op_ = ug % S;
+  const int UM = H / S;                 // units whose octet partial this workgroup forms
+  const int ub0 = op_ * UM;
   const int m0 = 16 * mt, j0 = U * ug;
   const int nch = K1 / 16;
   const int c0 = KCH * wave;  // chunks c0 .. c0 + KCH - 1; those >= nch are zero
-  const int hb16 = H / 16;
   const unsigned hbytes = unsigned(B) * unsigned(H) * 4u;
   const unsigned sbytes = G == 4 ? unsigned(a.c_off) + hbytes : hbytes;
   auto wrow = [&](int n) { return (n / U) * H + j0 + (n % U); };  // W row of gate column n
@@ -166,9 +172,10 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
   __shared__ __attribute__((aligned(16))) float xs[16][kXld];  // [x_t | h_t] rows of the tile
   __shared__ float zs[kWaves][16][NC + 1];                     // per-wave gate partial sums
   __shared__ __attribute__((aligned(16))) float zb[16][NC + 4];  // zbar_t of the workgroup
-  __shared__ float hp[NGRP][NS];                               // partial h-adjoint sums
+  __shared__ float hp[kSmax][NS];                              // octet partials of the slice's h-adjoint
   __shared__ float cbs[NS];                                    // cbar carried between adjoints
-  __shared__ __attribute__((aligned(16))) float whs[kHmax * (NC + 4)];  // W_h^T of the gate columns
+  __shared__ __attribute__((aligned(16))) float zbo[16][OLD];   // zbar of the octet's gate columns
+  __shared__ __attribute__((aligned(16))) float whs[kUMmax * OLD];  // W_h^T: octet's columns x own units
   __shared__ __attribute__((aligned(16))) float stg[2 * NS];  // the last forward step's output slice (h, c)
   __shared__ double wsum[kWaves];
   __shared__ int stop;
@@ -183,14 +190,18 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
       Wr[i][nb] = ch < nch ? *(const f4*)(a.W + (size_t)wrow(nb * 16 + r) * K1 + ch * 16 + 4 * q)
                            : f4{0.f, 0.f, 0.f, 0.f};
   }
-  // W_h^T for the workgroup's gate columns (the partial product's B
-  // operand): whs[j][n] = W[wrow(n)][D + j], so that a lane's four reduction
-  // indices n = 16 ch + 4 q .. + 3 are one 16-byte read
-  constexpr int WLD = NC + 4;
-  for (int idx = tid; idx < NC * H; idx += kThreads) {
-    const int n = idx / H, j = idx % H;
-    whs[j * WLD + n] = a.W[(size_t)wrow(n) * K1 + D + j];
+  // W_h^T for the octet's partial product (its B operand): whs[u][k] =
+  // W[row of octet column k][D + ub0 + u], k = m NC + n for member m's gate
+  // column n, so that a lane's four reduction indices are one 16-byte read.
+  // Columns of absent members and units beyond UM stay zero, as do the
+  // octet-zbar columns beyond S NC.
+  for (int idx = tid; idx < kUMmax * OK; idx += kThreads) {
+    const int u = idx / OK, k = idx % OK, m = k / NC, n = k % NC;
+    float v = 0.f;
+    if (u < UM && m < S) v = a.W[(size_t)((n / U) * H + U * (oc * S + m) + n % U) * K1 + D + ub0 + u];
+    whs[u * OLD + k] = v;
   }
+  for (int idx = tid; idx < 16 * OLD; idx += kThreads) zbo[idx / OLD][idx % OLD] = 0.f;
   // reduction columns K1 .. 16 * 8 KCH of the staged rows stay zero
   for (int idx = tid; idx < 16 * (16 * kWaves * KCH - K1); idx += kThreads) {
     const int w = 16 * kWaves * KCH - K1;
@@ -269,14 +280,14 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
     }
     if (cl_ok) pv = ld4<kSys>(host_rsrc(h), unsigned(lane) * 16u);
   };
-  // wave 0 waits until every member's flag reaches target
-  auto wait_group = [&](const unsigned* flags, unsigned target) -> bool {
+  // wave 0 waits until flags[0 .. cnt) all reach target
+  auto wait_flags = [&](const unsigned* flags, int cnt, unsigned target) -> bool {
     if (wave == 0) {
       const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
       int st = 0;
       for (unsigned it = 0;; ++it) {
         bool ok = true;
-        for (int j = lane; j < ng; j += 64) ok = ok && ld_flag(flags + mt * ng + j) >= target;
+        for (int j = lane; j < cnt; j += 64) ok = ok && ld_flag(flags + j) >= target;
         if (__all(ok)) break;
         if ((it & 31) == 31) {
           if (ld_flag(a.status) != 0u) {
@@ -301,6 +312,19 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
     __syncthreads();
     return stop == 0;
   };
+  auto wait_group = [&](const unsigned* flags, unsigned target) -> bool {
+    return wait_flags(flags + mt * ng, ng, target);
+  };
+  // the nO octet partials of this workgroup's units from the last adjoint
+  // step, P[octet][unit][row] -> hp[octet][u 16 + row] (staging threads)
+  auto stage_partials = [&]() {
+    const float* pin = a.P + (((size_t)((na + 1) & 1) * a.mtiles + mt) * nO) * H * 16;
+    const __amdgpu_buffer_rsrc_t prs = rsrc(pin, unsigned(nO * H * 16 * 4));
+    for (int idx = tid; idx < nO * NG4; idx += kStageThreads) {
+      const int o2 = idx / NG4, v4 = idx % NG4;
+      *(f4*)&hp[o2][4 * v4] = ld4<kDev>(prs, unsigned(((o2 * H + j0) * 16 + 4 * v4) * 4));
+    }
+  };
   // weight gradient of the workgroup's gate rows for the last adjoint step,
   // dW += zbar^T [x | h], on the wave's own reduction chunks (block (nb,
   // chunk c0 + i) of 16 x 16).  It feeds nothing the other workgroups wait
@@ -308,18 +332,24 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
   // barrier, while the flags of the others are on their way.
   bool pend_dw = false;
   auto deferred_dw = [&]() {
-#pragma unroll 2
+    // operands of batch rows 4 c4 + q, read one group ahead of the MFMAs
+    float av[2][NB], bv[2][KCH];
+    auto load = [&](int c4, int buf_) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) av[buf_][nb] = zb[4 * c4 + q][nb * 16 + r];
+#pragma unroll
+      for (int i = 0; i < KCH; ++i) bv[buf_][i] = xs[4 * c4 + q][(c0 + i) * 16 + r];
+    };
+    load(0, 0);
+#pragma unroll
     for (int c4 = 0; c4 < 4; ++c4) {
-      float av[NB];
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) av[nb] = zb[4 * c4 + q][nb * 16 + r];
-      float bv[KCH];
-#pragma unroll
-      for (int i = 0; i < KCH; ++i) bv[i] = xs[4 * c4 + q][(c0 + i) * 16 + r];
+      if (c4 < 3) load(c4 + 1, (c4 + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the MFMAs that hide them
 #pragma unroll
       for (int i = 0; i < KCH; ++i)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) dacc[i][nb] = mfma_f32_16x16x4(av[nb], bv[i], dacc[i][nb]);
+        for (int nb = 0; nb < NB; ++nb)
+          dacc[i][nb] = mfma_f32_16x16x4(av[c4 & 1][nb], bv[c4 & 1][i], dacc[i][nb]);
     }
     if (tid < NC) {
       float s = 0.f;
@@ -396,14 +426,7 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
         if (m0 + row < B) v = ld4<kDev>(srs, unsigned(((m0 + row) * H + col) * 4));
         *(f4*)&xs[row][D + col] = v;
       }
-      if (adj && !first) {
-        const int v4 = tid % NG4, grp = tid / NG4;
-        const float* slab = a.P + ((((size_t)((na + 1) & 1) * a.mtiles + mt) * ng + ug) * ng) * NS;
-        const __amdgpu_buffer_rsrc_t prs = rsrc(slab, unsigned(ng * NS * 4));
-        f4 s = f4{0.f, 0.f, 0.f, 0.f};
-        for (int srcw = grp; srcw < ng; srcw += NGRP) s += ld4<kDev>(prs, unsigned((srcw * NS + 4 * v4) * 4));
-        *(f4*)&hp[grp][4 * v4] = s;
-      }
+      if (adj && !first) stage_partials();
     }
     __syncthreads();
     if (tid == 0) st_flag(a.consumed + me, sc);
@@ -414,11 +437,14 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
       f4 acc[NB];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) acc[nb] = f4{0.f, 0.f, 0.f, 0.f};
+      f4 av = *(const f4*)&xs[r][c0 * 16 + 4 * q];
 #pragma unroll
       for (int i = 0; i < KCH; ++i) {
-        const f4 av = *(const f4*)&xs[r][(c0 + i) * 16 + 4 * q];
+        const f4 cur = av;
+        if (i + 1 < KCH) av = *(const f4*)&xs[r][(c0 + i + 1) * 16 + 4 * q];  // one chunk ahead
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[nb] = mma4(av, Wr[i][nb], acc[nb]);
+        for (int nb = 0; nb < NB; ++nb) acc[nb] = mma4(cur, Wr[i][nb], acc[nb]);
       }
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
@@ -461,7 +487,8 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
         float hbar = 0.f;
         if (!first) {
 #pragma unroll
-          for (int g = 0; g < NGRP; ++g) hbar += hp[g][u * 16 + ml];
+          for (int g = 0; g < kSmax; ++g)
+            if (g < nO) hbar += hp[g][u * 16 + ml];
         }
         float sd = 0.f;
         if (a.loss == AMBPTT_LOSS_MEAN_SQ_ALL) {
@@ -495,29 +522,59 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
     }
     if (!adj) return true;
     __syncthreads();
-    // partial h-adjoint of the workgroup's gate columns, to the owners of the units
-    if (wave < kCopyWave) {
-      float* pbase = a.P + (((size_t)(na & 1) * a.mtiles + mt) * ng) * ng * NS;
-      const __amdgpu_buffer_rsrc_t prs = rsrc(pbase, unsigned(ng * ng * NS * 4));
-      f4 av[KW];
-#pragma unroll
-      for (int ch = 0; ch < KW; ++ch) av[ch] = *(const f4*)&zb[r][16 * ch + 4 * q];
-#pragma unroll
-      for (int i = 0; i < kNbw; ++i) {
-        const int jb = wave + kCopyWave * i;
-        if (jb < hb16) {
-          f4 bv[KW];
-#pragma unroll
-          for (int ch = 0; ch < KW; ++ch) bv[ch] = *(const f4*)&whs[(jb * 16 + r) * WLD + 16 * ch + 4 * q];
-          f4 acc = f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int ch = 0; ch < KW; ++ch) acc = mma4(av[ch], bv[ch], acc);
-          const int col = jb * 16 + r, dsw = col / U, du = col % U;
-          st4<kDev>(prs, unsigned(((dsw * ng + ug) * NS + du * 16 + 4 * q) * 4), acc);
-        }
+    // h-adjoint, first level: the octet's zbar columns times W_h for this
+    // workgroup's share of units, summed at the owners at the next barrier
+    {
+      float* zout = a.Z + (((size_t)(na & 1) * a.mtiles + mt) * ng + ug) * (16 * NC);
+      if (tid < 4 * NC) {  // 16 rows x NC columns
+        const int row = tid / (NC / 4), c = 4 * (tid % (NC / 4));
+        st4<kDev>(rsrc(zout, 16 * NC * 4), unsigned((row * NC + c) * 4), *(const f4*)&zb[row][c]);
       }
     }
     pend_dw = true;
+    drain();
+    if (tid == 0) st_flag(a.oflag + me, unsigned(na + 1));
+    deferred_dw();  // while the octet's flags travel
+    if (!wait_flags(a.oflag + mt * ng + oc * S, S, unsigned(na + 1))) return false;
+    if (tid < kStageThreads) {
+      const float* zin = a.Z + (((size_t)(na & 1) * a.mtiles + mt) * ng + oc * S) * (16 * NC);
+      const __amdgpu_buffer_rsrc_t zrs = rsrc(zin, unsigned(S * 16 * NC * 4));
+      for (int idx = tid; idx < S * 4 * NC; idx += kStageThreads) {
+        const int m = idx / (4 * NC), w = idx % (4 * NC), row = w / (NC / 4), c = 4 * (w % (NC / 4));
+        *(f4*)&zbo[row][m * NC + c] = ld4<kDev>(zrs, unsigned(idx * 16));
+      }
+    }
+    __syncthreads();
+    if (wave < 4) {  // one 16-unit block of the share per wave (UM <= 64)
+      const int jb = wave;
+      if (jb * 16 < UM) {
+        // two accumulators over even and odd chunks, operands one pair ahead
+        const float* wb = &whs[(jb * 16 + r) * OLD + 4 * q];
+        const float* zr = &zbo[r][4 * q];
+        f4 acc0 = f4{0.f, 0.f, 0.f, 0.f}, acc1 = f4{0.f, 0.f, 0.f, 0.f};
+        f4 a0 = *(const f4*)zr, b0 = *(const f4*)wb, a1 = *(const f4*)(zr + 16), b1 = *(const f4*)(wb + 16);
+#pragma unroll
+        for (int ch = 0; ch < OK / 16; ch += 2) {
+          f4 na0 = a0, nb0 = b0, na1 = a1, nb1 = b1;
+          if (ch + 2 < OK / 16) {
+            na0 = *(const f4*)(zr + 16 * (ch + 2));
+            nb0 = *(const f4*)(wb + 16 * (ch + 2));
+            na1 = *(const f4*)(zr + 16 * (ch + 3));
+            nb1 = *(const f4*)(wb + 16 * (ch + 3));
+          }
+          __builtin_amdgcn_sched_barrier(0);
+          acc0 = mma4(a0, b0, acc0);
+          acc1 = mma4(a1, b1, acc1);
+          a0 = na0, b0 = nb0, a1 = na1, b1 = nb1;
+        }
+        const f4 acc = acc0 + acc1;
+        const int u = jb * 16 + r;
+        if (u < UM) {
+          float* pout = a.P + ((((size_t)(na & 1) * a.mtiles + mt) * nO + oc) * H) * 16;
+          st4<kDev>(rsrc(pout, unsigned(H * 16 * 4)), unsigned(((ub0 + u) * 16 + 4 * q) * 4), acc);
+        }
+      }
+    }
     ++na;
     return true;
   };
@@ -592,19 +649,13 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
 
   // dL/dh_0 = sum of the partials of the adjoint of step 0; dL/dc_0 = cbar_0.
   // (after the loop, so that none of these addresses stays live through it)
-  if (tid < kStageThreads) {
-    const int v4 = tid % NG4, grp = tid / NG4;
-    const float* slab = a.P + ((((size_t)((na + 1) & 1) * a.mtiles + mt) * ng + ug) * ng) * NS;
-    const __amdgpu_buffer_rsrc_t prs = rsrc(slab, unsigned(ng * NS * 4));
-    f4 s = f4{0.f, 0.f, 0.f, 0.f};
-    for (int srcw = grp; srcw < ng; srcw += NGRP) s += ld4<kDev>(prs, unsigned((srcw * NS + 4 * v4) * 4));
-    *(f4*)&hp[grp][4 * v4] = s;
-  }
+  if (tid < kStageThreads) stage_partials();
   __syncthreads();
   if (erow) {
     float hbar = 0.f;
 #pragma unroll
-    for (int g = 0; g < NGRP; ++g) hbar += hp[g][u * 16 + ml];
+    for (int g = 0; g < kSmax; ++g)
+      if (g < nO) hbar += hp[g][u * 16 + ml];
     a.dh0[em * H + ej] = hbar;
     if (G == 4) a.dc0[em * H + ej] = cbs[tid];
   }
@@ -655,7 +706,10 @@ __global__ void resident_reduce(const float* __restrict__ dWp, const float* __re
 int resident_units(int G) { return G == 4 ? 8 : 16; }
 int resident_max_k(int) { return kKmax; }
 int resident_max_h(int) { return kHmax; }
-static_assert(kHmax <= 16 * kCopyWave * kNbw, "partial-product blocks");
+int resident_octet(int ng, int H) {
+  const int S = ng < kSmax ? ng : kSmax;
+  return (ng % S == 0 && H % S == 0 && H / S <= kUMmax) ? S : 0;
+}
 
 hipError_t resident_capacity(int G, int* blocks) {
   int dev = 0, per = 0;

@@ -68,9 +68,10 @@ struct Layout {
   bool mlp = false;      // residual MLP (per-layer weights, one-step dW windows)
   // resident whole-pass kernel (fp32 RNN / LSTM whose weights fit in registers)
   bool res = false;
-  int r_mtiles = 0, r_ng = 0, r_nwg = 0;
+  int r_mtiles = 0, r_ng = 0, r_nwg = 0, r_S = 0;
   size_t r_prog_cap = 0;  // program entries
-  size_t off_prog = 0, off_ready = 0, off_consumed = 0, off_status = 0, off_P = 0, off_dWp = 0, off_dbp = 0;
+  size_t off_prog = 0, off_ready = 0, off_consumed = 0, off_oflag = 0, off_status = 0, off_Z = 0, off_P = 0;
+  size_t off_dWp = 0, off_dbp = 0;
 };
 
 // Largest grid of the resident kernel the layout provisions for; the device's
@@ -139,9 +140,11 @@ Layout make_layout(const ambptt_problem* p, int window) {
     const long nwg = (long)mtiles * ng;
     const double evr = double(revolve_advances(p->n_steps, p->fast_slots)) + 1.0;
     const double cap = 2.0 * (evr + 3.0 * double(p->n_steps)) + 256.0;
-    if (K1 <= resident_max_k(L.G) && p->hidden <= resident_max_h(L.G) && p->hidden % U == 0 &&
+    const int S = p->hidden % U == 0 ? resident_octet(ng, p->hidden) : 0;
+    if (K1 <= resident_max_k(L.G) && p->hidden <= resident_max_h(L.G) && p->hidden % U == 0 && S > 0 &&
         nwg <= kResidentMaxWg && cap < 8.0e6) {
       L.res = true;
+      L.r_S = S;
       L.r_mtiles = mtiles;
       L.r_ng = ng;
       L.r_nwg = int(nwg);
@@ -165,8 +168,10 @@ Layout make_layout(const ambptt_problem* p, int window) {
     L.off_prog = o; o += align_up(L.r_prog_cap * 16);
     L.off_ready = o; o += align_up(nwg * 4);
     L.off_consumed = o; o += align_up(nwg * 4);
+    L.off_oflag = o; o += align_up(nwg * 4);
     L.off_status = o; o += kAlign;
-    L.off_P = o; o += align_up(2 * mt * ng * ng * 16 * U * 4);
+    L.off_Z = o; o += align_up(2 * mt * ng * 16 * GH / ng * 4);
+    L.off_P = o; o += align_up(2 * mt * (ng / size_t(L.r_S)) * size_t(p->hidden) * 16 * 4);
     L.off_dWp = o; o += align_up(mt * GH * K1 * 4);
     L.off_dbp = o; o += align_up(mt * GH * 4);
   }
@@ -656,12 +661,14 @@ ambptt_status resident_args(ambptt_ctx* C, const void* x, const void* W, const f
   a.nslots = p.fast_slots;
   a.host = nullptr;
   if (C->host) HIPCK(hipHostGetDevicePointer((void**)&a.host, C->host, 0));
+  a.Z = (float*)(C->ws + L.off_Z);
   a.P = (float*)(C->ws + L.off_P);
   a.dWp = (float*)(C->ws + L.off_dWp);
   a.dbp = (float*)(C->ws + L.off_dbp);
   a.loss_acc = (double*)(C->ws + L.off_loss);
   a.ready = (unsigned*)(C->ws + L.off_ready);
   a.consumed = (unsigned*)(C->ws + L.off_consumed);
+  a.oflag = (unsigned*)(C->ws + L.off_oflag);
   a.status = (unsigned*)(C->ws + L.off_status);
   a.timeout = (long long)C->res_timeout_ms * 100000LL;  // s_memrealtime runs at 100 MHz
   a.B = p.batch;
@@ -670,6 +677,7 @@ ambptt_status resident_args(ambptt_ctx* C, const void* x, const void* W, const f
   a.loss = p.loss;
   a.mtiles = L.r_mtiles;
   a.ng = L.r_ng;
+  a.S = L.r_S;
   a.xcd_map = (L.r_nwg % 8 == 0 && 8 % L.r_mtiles == 0 && L.r_ng % (8 / L.r_mtiles) == 0) ? 1 : 0;
   a.inv_bh = 1.0f / float((double)p.batch * p.hidden);
   *out = a;
@@ -698,6 +706,7 @@ ambptt_status resident_launch(ambptt_ctx* C, ResidentArgs a, const std::vector<i
   a.nprog = int(n / 4);
   HIPCK(launch_fill32(C->ws + L.off_ready, size_t(L.r_nwg), 0u, C->cs));
   HIPCK(launch_fill32(C->ws + L.off_consumed, size_t(L.r_nwg), 0u, C->cs));
+  HIPCK(launch_fill32(C->ws + L.off_oflag, size_t(L.r_nwg), 0u, C->cs));
   HIPCK(launch_fill32(C->ws + L.off_status, 4, 0u, C->cs));
   if (timed) HIPCK(hipEventRecord(C->ev_r[0], C->cs));
   HIPCK(launch_resident(L.G, a, C->cs, C->res_coop));
