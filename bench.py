@@ -31,6 +31,7 @@ sys.path.insert(0, ROOT)
 METRIC = "BPTT timesteps/sec at fixed HBM slot budget; recompute factor; MFMA % of peak"
 WORKLOAD = "lstm_h512_t1000"
 FP32_MFMA_PEAK_TFLOPS = 157.3
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense
 
 
 def step_flops(spec, window: int) -> dict:
@@ -43,12 +44,13 @@ def step_flops(spec, window: int) -> dict:
     return {"fwd": gate, "adj": gate + hbar, "dw": dw1 * window, "gate": gate, "hbar": hbar, "dw1": dw1}
 
 
-def measured_traffic(kernel: str):
-    """HBM bytes per launch of a kernel from the committed FETCH_SIZE /
-    WRITE_SIZE counter runs (each scaled by a plain copy of known size), or
-    None if the kernel's source has changed since those counters were taken."""
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of a kernel on a workload from the committed
+    FETCH_SIZE / WRITE_SIZE counter runs (each scaled by a plain copy of known
+    size), or None if there are none or the kernel's source has changed since
+    those counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "lstm_h512_t1000_pmc.json")
+    path = os.path.join(ROOT, "profiles", f"{workload}_pmc.json")
     try:
         rec = json.load(open(path))["kernels"][kernel]
         src = open(os.path.join(ROOT, rec["source"]), "rb").read()
@@ -60,6 +62,9 @@ def measured_traffic(kernel: str):
 
 
 def cpu_baseline(wl, budget_s: float = 12.0) -> dict:
+    """The float64 oracle's store-all BPTT on the host cores, on the first
+    steps (layers) of the workload at its full shapes, as many as fit the
+    budget after a probe."""
     import numpy as np
     import synth
     from oracle import bptt
@@ -68,10 +73,20 @@ def cpu_baseline(wl, budget_s: float = 12.0) -> dict:
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = len(os.sched_getaffinity(0))
-    W, b = synth.params(wl)
-    cell = bptt.cell_for(wl, (W.astype(np.float64), b.astype(np.float64)))
     x0 = synth.initial_state(wl)
-    st = (x0["h"].astype(np.float64), x0["c"].astype(np.float64))
+    st = tuple(x0[k].astype(np.float64) for k in ("h", "c") if k in x0)
+    if wl.cell == "resmlp":
+        cache = {}
+
+        def layer(l):
+            if l not in cache:
+                Wl, bl = synth.layer_params(wl, l)
+                cache[l] = (Wl.astype(np.float64), bl.astype(np.float64))
+            return cache[l]
+        cell = bptt.cell_for(wl, layer=layer)
+    else:
+        W, b = synth.params(wl)
+        cell = bptt.cell_for(wl, (W.astype(np.float64), b.astype(np.float64)))
 
     def one(n):
         w = wl.with_(n_steps=n)
@@ -80,13 +95,70 @@ def cpu_baseline(wl, budget_s: float = 12.0) -> dict:
         bptt.store_all(cell, n, lambda i: xs[i], st)
         return time.perf_counter() - t
 
-    probe = 16
+    probe = 2 if wl.batch * wl.hidden >= (1 << 19) else 16
     dt = one(probe)
     n = int(max(probe, min(wl.n_steps, budget_s * probe / max(dt, 1e-6))))
-    dt = one(n)
+    if n > probe:
+        dt = one(n)
     return {"value": n / dt, "unit": "timesteps/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"float64 store-all BPTT (numpy) over the first {n} of {wl.n_steps} steps "
-                      f"at the full shapes, {dt:.1f} s"}
+            "sample": f"float64 store-all BPTT (numpy) over the first {n} of {wl.n_steps} "
+                      f"{'layers' if wl.cell == 'resmlp' else 'steps'} at the full shapes, {dt:.1f} s"}
+
+
+def device_inputs(wl, dev):
+    """Seeded inputs, generated on the host in slices (synth) and moved to HBM
+    in the operand dtype; the residual MLP's layers are drawn in parallel."""
+    import numpy as np
+    import torch
+    from concurrent.futures import ThreadPoolExecutor
+    import synth
+    op = torch.float32 if wl.dtype == "f32" else torch.bfloat16
+    n, B, D, H = wl.n_steps, wl.batch, wl.input, wl.hidden
+    x0 = synth.initial_state(wl)
+    t = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
+    dh = t(x0["h"], op)
+    dc = t(x0["c"], torch.float32) if "c" in x0 else None
+    if wl.cell == "resmlp":
+        dx = None
+        dW = torch.empty((n, H, H), dtype=op, device=dev)
+        db = torch.zeros((n, H), dtype=torch.float32, device=dev)
+        workers = min(16, len(os.sched_getaffinity(0)))
+
+        def put(l):
+            Wl, bl = synth.layer_params(wl, l)
+            return l, torch.from_numpy(Wl).to(op)
+        with ThreadPoolExecutor(workers) as ex:
+            for l0 in range(0, n, 64):
+                for l, Wl in ex.map(put, range(l0, min(n, l0 + 64))):
+                    dW[l].copy_(Wl.to(dev))
+        return dx, dW, db, dh, dc
+    dx = torch.empty((n, B, D), dtype=op, device=dev)
+    chunk = max(1, (256 << 20) // max(1, B * D * 4))
+    for t0 in range(0, n, chunk):
+        t1 = min(n, t0 + chunk)
+        dx[t0:t1].copy_(torch.from_numpy(synth.x_slice(wl, t0, t1)).to(op).to(dev))
+    W, b = synth.params(wl)
+    return dx, t(W, op), t(b, torch.float32), dh, dc
+
+
+def fingerprint(out) -> list:
+    """Exact fingerprints of the gradients (sums of the raw bit patterns in
+    chunks, weighted by chunk), to compare passes bit for bit without keeping
+    two copies of a 134 GB gradient."""
+    import torch
+    fp = []
+    for k in ("dW", "db", "dh0", "dc0"):
+        v = out.get(k)
+        if v is None:
+            continue
+        flat = v.reshape(-1).view(torch.int32)
+        acc = 0
+        step = 1 << 24
+        for i, c0 in enumerate(range(0, flat.numel(), step)):
+            acc += (i + 1) * int(flat[c0:c0 + step].to(torch.int64).sum().item())
+        fp.append(acc)
+    fp.append(float(out["loss"]))
+    return fp
 
 
 def main() -> int:
@@ -98,6 +170,10 @@ def main() -> int:
     ap.add_argument("--timing-sample", type=int, default=8)
     ap.add_argument("--path", choices=["auto", "steps", "resident"], default="auto")
     ap.add_argument("--cooperative", type=int, default=0)
+    ap.add_argument("--workload", default=WORKLOAD, help="a synth workload name (default: the 512-LSTM)")
+    ap.add_argument("--host-slots", type=int, default=-1, help="host-tier slots (default: the workload's)")
+    ap.add_argument("--no-compare", dest="compare", action="store_false",
+                    help="skip the plain-Revolve and other-path passes")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -110,14 +186,12 @@ def main() -> int:
     import paper_1806_01117_amd as amb
     import synth
 
-    wl = synth.get(WORKLOAD)
+    wl = synth.get(args.workload)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    x = synth.x_slice(wl, 0, wl.n_steps)
-    W, b = synth.params(wl)
-    x0 = synth.initial_state(wl)
-    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
-    dx, dW, db, dh, dc = t(x), t(W), t(b), t(x0["h"]), t(x0["c"])
+    dx, dW, db, dh, dc = device_inputs(wl, dev)
+    torch.cuda.synchronize()
+    print(f"inputs of {wl.name} in HBM", file=sys.stderr, flush=True)
 
     # a plain copy of known size (256 MiB read + 256 MiB written): the reference
     # that scales the FETCH_SIZE / WRITE_SIZE counters of a profiling run
@@ -127,55 +201,71 @@ def main() -> int:
     torch.cuda.synchronize()
     del ref_src, ref_dst
 
-    spec = amb.ProblemSpec.from_workload(wl)
+    host_slots = wl.host_slots if args.host_slots < 0 else args.host_slots
+    spec = amb.ProblemSpec.from_workload(wl, slow_slots=host_slots)
+    f32 = dict(dtype=torch.float32, device=dev)
+    outb = {"dW": torch.empty(dW.shape, **f32), "db": torch.empty(db.shape, **f32),
+            "dh0": torch.empty(dh.shape, **f32), "dc0": torch.empty(dh.shape, **f32) if dc is not None else None}
     r = amb.Runner(spec, device=dev)
     if args.path != "auto":
         r.set("path", 1 if args.path == "steps" else 2)
     r.set("resident_cooperative", args.cooperative)
     I_min, t_a, t_t = r.calibrate(dx, dW, db, dh, dc)
+    print(f"calibrated: I_min {I_min}, T_A {t_a:.2f} us, T_T {t_t:.2f} us", file=sys.stderr, flush=True)
     r.set("timing_sample", args.timing_sample)
     for _ in range(args.warmup):
-        r.run(dx, dW, db, dh, dc)
+        r.run(dx, dW, db, dh, dc, out=outb)
     torch.cuda.synchronize()
     stats = []
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        out = r.run(dx, dW, db, dh, dc)
+    for i in range(args.steps):
+        out = r.run(dx, dW, db, dh, dc, out=outb)
         stats.append(out["stats"])
+        print(f"pass {i + 1}/{args.steps} done", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     el = time.perf_counter() - t0
     value = wl.n_steps * args.steps / el
     st = stats[-1]
     resident = st["path"] == 1
+    fp_async = fingerprint(out) if args.compare else None
 
-    def other_run(runner, reps):
-        runner.run(dx, dW, db, dh, dc)
+    def other_run(runner, reps, warm=True):
+        if warm:
+            runner.run(dx, dW, db, dh, dc, out=outb)
         torch.cuda.synchronize()
         tr = time.perf_counter()
         for _ in range(reps):
-            o = runner.run(dx, dW, db, dh, dc)
+            o = runner.run(dx, dW, db, dh, dc, out=outb)
         torch.cuda.synchronize()
-        return wl.n_steps * reps / (time.perf_counter() - tr), o["stats"]
+        return wl.n_steps * reps / (time.perf_counter() - tr), o
 
     reps = max(1, min(3, args.steps))
     # plain Revolve at the same HBM slot budget (no host tier), same path
-    rv = amb.Runner(amb.ProblemSpec.from_workload(wl, slow_slots=0), device=dev)
-    rv.set("path", 2 if resident else 1)
-    rv.set("resident_cooperative", args.cooperative)
-    rv_value, rv_st = other_run(rv, reps)
-    rv.close()
+    rv_value, rv_st, bitwise = None, None, None
+    if args.compare:
+        rv = amb.Runner(amb.ProblemSpec.from_workload(wl, slow_slots=0), device=dev)
+        rv.set("path", 2 if resident else 1)
+        rv.set("resident_cooperative", args.cooperative)
+        rv_value, rvo = other_run(rv, reps if args.steps > 1 else 1, warm=args.steps > 1)
+        rv_st = rvo["stats"]
+        bitwise = fingerprint(rvo) == fp_async
+        print(f"plain Revolve done, bit-identical gradients: {bitwise}", file=sys.stderr, flush=True)
+        rv.close()
     # the same schedule with one kernel launch per step (the other execution path)
     alt = None
-    if resident:
-        ps = amb.Runner(amb.ProblemSpec.from_workload(wl, interval_min=max(1, st["interval"])), device=dev)
+    if resident and args.compare:
+        ps = amb.Runner(amb.ProblemSpec.from_workload(wl, interval_min=max(1, st["interval"]), slow_slots=host_slots),
+                        device=dev)
         ps.set("path", 1)
-        ps_value, ps_st = other_run(ps, reps)
+        ps_value, pso = other_run(ps, reps)
+        ps_st = pso["stats"]
         ps.close()
         alt = {"value": round(ps_value, 2), "unit": "timesteps/s", "interval": ps_st["interval"],
                "recompute_factor": round(ps_st["recompute_factor"], 4)}
 
     # roofline of the dominant kernel (largest device time in one pass)
     from paper_1806_01117_amd._lib import KERNEL_CLASSES
+    peak = FP32_MFMA_PEAK_TFLOPS if wl.dtype == "f32" else BF16_MFMA_PEAK_TFLOPS
     fl = step_flops(spec, st["window"])
     kern = {}
     for i, name in enumerate(KERNEL_CLASSES):
@@ -188,15 +278,20 @@ def main() -> int:
         fwd_ops = st["forward_evals"] - 1          # the first turn's forward step runs inside an adjoint
         flops = {"pass": fwd_ops * fl["gate"] + st["adjoints"] * (fl["gate"] + fl["hbar"] + fl["dw1"])}
         names = {"pass": "resident_pass: whole forward + reverse pass in one launch"}
-        traffic = measured_traffic("resident_pass")
+        traffic = measured_traffic(wl.name, "resident_pass")
     else:
         flops = {"fwd": fl["fwd"], "adj": fl["adj"], "dw": fl["dw"]}
         cand = [k for k in tot if k in flops]
         dom = max(cand, key=tot.get) if cand else "adj"
-        names = {"fwd": "step_small forward: gate GEMM + LSTM update",
-                 "adj": "step_small adjoint: gate recompute + h-adjoint GEMM",
-                 "dw": "dw_lds_f32 weight-gradient window"}
-        traffic = measured_traffic({"fwd": "step_small_fwd", "adj": "step_small_adj"}.get(dom, dom))
+        small = spec.batch * spec.hidden < 1024 * 256 or wl.dtype == "bf16"
+        if wl.cell == "resmlp":
+            names = {"fwd": "resmlp_step forward", "adj": "resmlp_step adjoint (recompute + NN product)",
+                     "dw": "weight gradient of one layer"}
+        else:
+            k = "step_small" if small else "step_f32"
+            names = {"fwd": f"{k} forward: gate GEMM + cell update", "adj": f"{k} adjoint: gate recompute + h-adjoint GEMM",
+                     "dw": ("dw_bf16" if wl.dtype == "bf16" else "dw_lds_f32") + " weight-gradient window"}
+        traffic = measured_traffic(wl.name, {"fwd": "step_small_fwd", "adj": "step_small_adj"}.get(dom, dom))
     dom_us = kern[dom][0] if dom in kern else 0.0
     achieved = flops[dom] / (dom_us * 1e-6) / 1e12 if dom_us > 0 else 0.0
     r.close()
@@ -204,16 +299,17 @@ def main() -> int:
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "timesteps/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(1000 * el / args.steps, 3),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-        "data": "synthetic (seeded normal inputs, uniform weights)",
-        "config": {"workload": WORKLOAD, "cell": "lstm", "batch": wl.batch, "input": wl.input,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+        "data": "synthetic (seeded normal inputs, " + ("normal" if wl.cell == "resmlp" else "uniform") + " weights)",
+        "config": {"workload": wl.name, "cell": wl.cell, "batch": wl.batch, "input": wl.input,
                    "hidden": wl.hidden, "n_steps": wl.n_steps, "fast_slots": wl.fast_slots,
                    "slow_slots": spec.slow_slots, "mode": "async" if st["mode"] else "revolve",
                    "interval": st["interval"], "interval_min": I_min, "t_a_us": round(t_a, 3),
                    "t_t_us": round(t_t, 3), "window": st["window"]},
         "recompute_factor": round(st["recompute_factor"], 4),
-        "plain_revolve": {"value": round(rv_value, 2), "unit": "timesteps/s",
-                          "recompute_factor": round(rv_st["recompute_factor"], 4)},
+        "plain_revolve": None if rv_st is None else {
+            "value": round(rv_value, 2), "unit": "timesteps/s",
+            "recompute_factor": round(rv_st["recompute_factor"], 4), "bit_identical_gradients": bitwise},
         "path": "resident" if resident else "steps",
         "per_step_launches": alt,
         "kernel_us": {k: round(v[0], 3) for k, v in kern.items()},
@@ -225,15 +321,15 @@ def main() -> int:
                       "stores": st["stores"], "prefetches": st["prefetches"],
                       "prefetches_elided": st["prefetches_elided"], "compute_waits": st["compute_waits"]},
         "roofline": {"bound": "mfma", "kernel": names[dom], "achieved": round(achieved, 3),
-                     "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": traffic,
+                     "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": traffic,
                      "avg_launch_us": round(dom_us, 3), "flops_per_launch": flops[dom]},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl)
     print(json.dumps(line), flush=True)
     # release device memory before interpreter teardown
-    del dx, dW, db, dh, dc, r, rv
+    del dx, dW, db, dh, dc, r, outb
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     return 0
