@@ -446,6 +446,7 @@ hipError_t launch_step(int G, int mode, const StepCfg& c, const StepArgs& a, hip
 
 hipError_t launch_dw(const DwArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (a.GH % 16 != 0) return hipErrorInvalidValue;
+  if (dw_f32_big_fits(a)) return launch_dw_f32_big(a, s, e0, e1);
   const int N = a.D + a.H;
   dim3 grid((a.GH + kDwT - 1) / kDwT, (N + kDwT - 1) / kDwT);
   hipExtLaunchKernelGGL(dw_lds_f32, grid, dim3(256), 0, s, e0, e1, 0, a);

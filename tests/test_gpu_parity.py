@@ -125,6 +125,21 @@ def test_resident_abort_path():
     assert_close(got, want, TOL_F32)
 
 
+def test_lstm_wide_ragged_weight_gradient():
+    """Gradient rows 4H = 320 and columns D + H = 288 (the 128 x 128-tile weight-gradient
+    kernel with partial tiles on both edges), windows that do not divide n."""
+    wl = synth.get("lstm_h512_t1000").with_(batch=5, input=208, hidden=80, n_steps=23, name="lstm_wide_ragged")
+    host, dev = _case(wl)
+    want = run_oracle(wl, *host)
+    a = run_gpu(wl, dev, fast_slots=23, slow_slots=0, path=1)
+    assert_close(a, want, TOL_F32)
+    b = run_gpu(wl, dev, fast_slots=3, slow_slots=23, interval_min=2, window=5, path=1)
+    assert b["stats"]["window"] == 5
+    assert_close(b, want, TOL_F32)
+    c = run_gpu(wl, dev, fast_slots=3, slow_slots=23, interval_min=2, window=7, path=1)
+    assert_bitwise(b, c, keys=("loss", "dh0", "dc0"))
+
+
 def test_lstm4096_shapes_short():
     """The offload-stress LSTM at its full per-step shapes (B=512, H=4096, D=1024), 4 steps."""
     wl = synth.get("lstm_h4096_t20000").with_(n_steps=4)
