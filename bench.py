@@ -34,14 +34,17 @@ FP32_MFMA_PEAK_TFLOPS = 157.3
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense
 
 
-def step_flops(spec, window: int) -> dict:
+def step_flops(spec, window: int, wide: bool = False) -> dict:
     """Algorithmic flops of one launch of each per-step kernel, and of the
-    three products of one step (gate GEMM, h-adjoint, weight gradient)."""
+    three products of one step (gate GEMM, h-adjoint, weight gradient).  On
+    the wide-batch bf16 path the h-adjoint product is a launch of its own
+    ("hadj"); otherwise the adjoint launch holds it."""
     B, D, H, G = spec.batch, spec.input, spec.hidden, spec.gates
-    gate = 2.0 * B * G * H * (D + H)            # z = [x|h] W^T
-    hbar = 2.0 * B * H * G * H                  # hbar = zbar W_h
+    gate = 2.0 * B * G * H * (D + H)            # z = [x|h] W^T (the MLP: y W_l^T)
+    hbar = 2.0 * B * H * G * H                  # hbar = zbar W_h (the MLP: zbar W_{l+1})
     dw1 = 2.0 * G * H * (D + H + 1) * B         # dW (+ db) of one step
-    return {"fwd": gate, "adj": gate + hbar, "dw": dw1 * window, "gate": gate, "hbar": hbar, "dw1": dw1}
+    return {"fwd": gate, "adj": gate if wide else gate + hbar, "hadj": hbar, "dw": dw1 * window,
+            "gate": gate, "hbar": hbar, "dw1": dw1}
 
 
 def measured_traffic(workload: str, kernel: str):
@@ -266,7 +269,8 @@ def main() -> int:
     # roofline of the dominant kernel (largest device time in one pass)
     from paper_1806_01117_amd._lib import KERNEL_CLASSES
     peak = FP32_MFMA_PEAK_TFLOPS if wl.dtype == "f32" else BF16_MFMA_PEAK_TFLOPS
-    fl = step_flops(spec, st["window"])
+    wide = st["kernel_calls"][3] > 0
+    fl = step_flops(spec, st["window"], wide)
     kern = {}
     for i, name in enumerate(KERNEL_CLASSES):
         us = [s_["kernel_us"][i] for s_ in stats if s_["kernel_samples"][i] > 0]
@@ -280,11 +284,18 @@ def main() -> int:
         names = {"pass": "resident_pass: whole forward + reverse pass in one launch"}
         traffic = measured_traffic(wl.name, "resident_pass")
     else:
-        flops = {"fwd": fl["fwd"], "adj": fl["adj"], "dw": fl["dw"]}
+        flops = {"fwd": fl["fwd"], "adj": fl["adj"], "hadj": fl["hadj"], "dw": fl["dw"]}
         cand = [k for k in tot if k in flops]
         dom = max(cand, key=tot.get) if cand else "adj"
         small = spec.batch * spec.hidden < 1024 * 256 or wl.dtype == "bf16"
-        if wl.cell == "resmlp":
+        if wide and wl.cell == "resmlp":
+            names = {"fwd": "mlp_wide forward", "adj": "mlp_wide adjoint (recompute + mask)",
+                     "hadj": "prod_wide NN product ybar + zbar W_{l+1}", "dw": "dw_bf16 weight gradient of one layer"}
+        elif wide:
+            names = {"fwd": "cell_wide forward: gate GEMM + cell update",
+                     "adj": "cell_wide adjoint: gate recompute + cell adjoint",
+                     "hadj": "prod_wide h-adjoint product zbar W_h", "dw": "dw_bf16 weight-gradient window"}
+        elif wl.cell == "resmlp":
             names = {"fwd": "resmlp_step forward", "adj": "resmlp_step adjoint (recompute + NN product)",
                      "dw": "weight gradient of one layer"}
         else:

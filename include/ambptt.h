@@ -110,9 +110,11 @@ typedef struct {
 } ambptt_stats;
 
 /* Kernel classes of ambptt_stats.kernel_*: forward step, the resident
- * whole-pass kernel, adjoint step, (unused), weight-gradient window, and
- * everything else. */
-enum { AMBPTT_K_FWD = 0, AMBPTT_K_PASS = 1, AMBPTT_K_ADJ = 2, AMBPTT_K_UNUSED = 3,
+ * whole-pass kernel, adjoint step (gate recomputation and cell adjoint), the
+ * adjoint's own product launch on the wide-batch bf16 path (hbar = zbar W_h,
+ * or the MLP's ybar + zbar W_{l+1}), weight-gradient window, and everything
+ * else. */
+enum { AMBPTT_K_FWD = 0, AMBPTT_K_PASS = 1, AMBPTT_K_ADJ = 2, AMBPTT_K_HADJ = 3,
        AMBPTT_K_DW = 4, AMBPTT_K_OTHER = 5 };
 
 typedef struct ambptt_ctx ambptt_ctx;

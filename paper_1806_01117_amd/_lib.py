@@ -43,7 +43,7 @@ class Stats(C.Structure):
         return d
 
 
-KERNEL_CLASSES = ["fwd", "pass", "adj", "unused", "dw", "other"]
+KERNEL_CLASSES = ["fwd", "pass", "adj", "hadj", "dw", "other"]
 
 
 _lib = None

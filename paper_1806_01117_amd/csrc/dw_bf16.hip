@@ -1,13 +1,25 @@
 // bf16 weight-gradient window and W_h transpose (gfx950).
 //
-// dW[k][c] += sum_r Z[r][k] X[r][c], db[k] += sum_r Z[r][k] over the R rows of
-// one window, Z = zbar and X = [x | h] in bf16, accumulation in fp32 on
-// v_mfma_f32_16x16x32_bf16.  The MFMA wants each lane's 8 consecutive
-// reduction indices r for one k (or c), so rows are staged through LDS
-// transposed: Zt[k][r], Xt[c][r] (row stride padded to 72 elements), filled
-// from coalesced 16-byte global reads of Z and X rows.  Workgroup = 4 waves
-// on a 64 x 64 tile of dW (2 x 2 MFMA blocks per wave), 64 rows per stage,
-// the next stage's global reads in flight while the current stage computes.
+// dW[k][c] (+)= sum_r Z[r][k] X[r][c], db[k] (+)= sum_r Z[r][k] over the R rows
+// of one window, Z = zbar [R][GH] and X = [x | h] [R][D + H] in bf16,
+// accumulation in fp32 on v_mfma_f32_16x16x32_bf16.
+//
+// Both operands have the reduction index r as their row, while the MFMA wants
+// each lane's 8 reduction indices of one k (or c) together.  The rows are
+// staged in LDS as they are stored in memory (coalesced 16-byte reads, one
+// 16-byte LDS write each) and the fragments come out of LDS with gfx950's
+// transposing read ds_read_b64_tr_b16: within a group of 16 lanes, lane i
+// names 4 consecutive 16-bit values (row kb + (i >> 2), columns 4 (i & 3) ..
+// +3 of a 16-column block) and lane j receives value j & 3 of lanes
+// 4 e + (j >> 2), e = 0..3, i.e. rows kb .. kb + 3 of column j.  Two such reads
+// (rows kb and kb + 4) make one bf16x8 fragment.
+//
+// Workgroup: 8 waves on a 256 x 128 tile of dW, each wave 64 x 64 (4 x 4 MFMA
+// blocks); 64 reduction rows per stage, double-buffered, the next stage's
+// global reads in flight while the current one is multiplied.  LDS rows have a
+// pitch of 32 bytes modulo 256 and rows r with (r >> 3) odd have their two
+// 128-byte halves swapped, so the 16 row segments of one transposing read
+// spread over all banks.
 #include <hip/hip_runtime.h>
 
 #include "kernels.hpp"
@@ -16,99 +28,126 @@
 namespace ambptt {
 namespace {
 
-constexpr int kT = 64, kS = 64, kLd = 72;
+constexpr int kTM = 256, kTN = 128;            // dW tile: gate rows x input columns
+constexpr int kS = 64;                         // reduction rows per stage
+constexpr int kPZ = kTM + 16, kPX = kTN + 16;  // LDS row pitch (bf16): 544 and 288 bytes
 
-__global__ __launch_bounds__(256) void dw_bf16(DwArgs a) {
-  __shared__ __attribute__((aligned(16))) __bf16 Zt[2][kT][kLd];
-  __shared__ __attribute__((aligned(16))) __bf16 Xt[2][kT][kLd];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+typedef short s4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u4v __attribute__((ext_vector_type(4)));
+
+// column of element (r, col) of a staged row r (bf16 units): halves swapped for (r >> 3) odd
+__device__ __forceinline__ int swz(int r, int col) { return col ^ (64 * ((r >> 3) & 1)); }
+
+// fragment of the 16 x 32 block (columns c0 .. c0 + 15, rows kb .. kb + 31) of a staged operand
+__device__ __forceinline__ bf16x8 tr_frag(const __bf16* base, int pitch, int kb, int c0) {
+  const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
+  const int r0 = kb + 8 * g + (i >> 2), col = c0 + 4 * (i & 3);
+  typedef __attribute__((address_space(3))) s4 lds_s4;
+  const s4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(base + r0 * pitch + swz(r0, col)));
+  const s4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(base + (r0 + 4) * pitch + swz(r0 + 4, col)));
+  typedef short s8 __attribute__((ext_vector_type(8)));
+  const s8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+__global__ __launch_bounds__(512) void dw_bf16(DwArgs a) {
+  __shared__ __attribute__((aligned(16))) __bf16 Zs[2][kS][kPZ];
+  __shared__ __attribute__((aligned(16))) __bf16 Xs[2][kS][kPX];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
-  const int li = lane & 15, lq = lane >> 4;
-  const int k0 = blockIdx.x * kT, c0 = blockIdx.y * kT;
   const int D = a.D, H = a.H, GH = a.GH, R = a.R, N = D + H;
-  const bool do_bias = blockIdx.y == 0;
+  const int k0 = blockIdx.x * kTM, c0 = blockIdx.y * kTN;
   const __bf16* Z = (const __bf16*)a.zbar;
   const __bf16* X = (const __bf16*)a.x;
   const __bf16* Hw = (const __bf16*)a.hwin;
 
-  // loader: thread t moves rows (t >> 3) + 32 p (p = 0, 1), elements 8 (t & 7) .. +7
-  const int lrow = tid >> 3, lcol = 8 * (tid & 7);
-  const int kc = k0 + lcol, cc = c0 + lcol;
-  const bool kok = kc < GH;  // GH % 32 == 0: a 16-byte group is wholly in or out
-  const bool cok = cc < N;
-  const __bf16* zsrc = Z + min(kc, GH - 8);
-  const __bf16* xsrc = cc < D ? X + cc : Hw + (min(cc, N - 8) - D);
-  const int xld = cc < D ? D : H;
-  bf16x8 zr[2], xr[2];
-  const bf16x8 zero = {};
+  // loader: 16-byte piece p = tid + 512 j; Z: row p >> 5, columns 8 (p & 31) ..;
+  // X: row p >> 4, columns 8 (p & 15) ..  (GH, D, H are multiples of 8: a piece
+  // lies wholly inside or outside each operand)
+  const int zr = tid >> 5, zc = 8 * (tid & 31), xr = tid >> 4, xc = 8 * (tid & 15);
+  const bool zok = k0 + zc < GH;
+  const int xcol = c0 + xc;
+  const bool xok = xcol < N;
+  const __bf16* zsrc = Z + (zok ? k0 + zc : 0);
+  const __bf16* xsrc = xcol < D ? X + xcol : Hw + (xok ? xcol - D : 0);
+  const int xld = xcol < D ? D : H;
+  u4v zv[4], xv[2];
   auto load = [&](int st) {
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
-      const int row = st * kS + lrow + 32 * p;
-      const bool ok = row < R;
-      zr[p] = (ok && kok) ? *(const bf16x8*)(zsrc + (size_t)row * GH) : zero;
-      xr[p] = (ok && cok) ? *(const bf16x8*)(xsrc + (size_t)row * xld) : zero;
+    for (int j = 0; j < 4; ++j) {
+      const int row = st * kS + zr + 16 * j;
+      zv[j] = (zok && row < R) ? *(const u4v*)(zsrc + (size_t)row * GH) : u4v{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int row = st * kS + xr + 32 * j;
+      xv[j] = (xok && row < R) ? *(const u4v*)(xsrc + (size_t)row * xld) : u4v{0u, 0u, 0u, 0u};
     }
   };
-  auto store = [&](int buf) {
+  auto stash = [&](int buf) {
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
-      const int rr = lrow + 32 * p;
+    for (int j = 0; j < 4; ++j) {
+      const int r = zr + 16 * j;
+      *(u4v*)&Zs[buf][r][swz(r, zc)] = zv[j];
+    }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        Zt[buf][lcol + e][rr] = zr[p][e];
-        Xt[buf][lcol + e][rr] = xr[p][e];
-      }
+    for (int j = 0; j < 2; ++j) {
+      const int r = xr + 32 * j;
+      *(u4v*)&Xs[buf][r][swz(r, xc)] = xv[j];
     }
   };
 
-  f4 acc[2][2];
+  f4 acc[4][4];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
   float bsum = 0.f;
+  const bool do_bias = blockIdx.y == 0 && tid < kTM;
 
   const int nst = (R + kS - 1) / kS;
   load(0);
-  store(0);
+  stash(0);
   __syncthreads();
   for (int st = 0; st < nst; ++st) {
     const int buf = st & 1;
     const bool more = st + 1 < nst;
     if (more) load(st + 1);
 #pragma unroll
-    for (int g = 0; g < kS / 32; ++g) {
-      const int r0 = 32 * g + 8 * lq;
-      const bf16x8 a0 = *(const bf16x8*)&Zt[buf][wm * 32 + li][r0];
-      const bf16x8 a1 = *(const bf16x8*)&Zt[buf][wm * 32 + 16 + li][r0];
-      const bf16x8 b0 = *(const bf16x8*)&Xt[buf][wn * 32 + li][r0];
-      const bf16x8 b1 = *(const bf16x8*)&Xt[buf][wn * 32 + 16 + li][r0];
-      acc[0][0] = mfma_bf16_16x16x32(a0, b0, acc[0][0]);
-      acc[0][1] = mfma_bf16_16x16x32(a0, b1, acc[0][1]);
-      acc[1][0] = mfma_bf16_16x16x32(a1, b0, acc[1][0]);
-      acc[1][1] = mfma_bf16_16x16x32(a1, b1, acc[1][1]);
+    for (int kc = 0; kc < kS / 32; ++kc) {
+      bf16x8 af[4], bf[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = tr_frag(&Zs[buf][0][0], kPZ, 32 * kc, 64 * wm + 16 * i);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bf[j] = tr_frag(&Xs[buf][0][0], kPX, 32 * kc, 64 * wn + 16 * j);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma_bf16_16x16x32(af[i], bf[j], acc[i][j]);
     }
-    if (do_bias && wave == 0) {
-      for (int rr = 0; rr < kS; ++rr) bsum += (float)Zt[buf][lane][rr];
+    if (do_bias) {
+#pragma unroll 8
+      for (int rr = 0; rr < kS; ++rr) bsum += (float)Zs[buf][rr][swz(rr, tid)];
     }
-    if (more) store(buf ^ 1);  // buf ^ 1 was last read before the previous barrier
+    if (more) stash(buf ^ 1);  // buf ^ 1 was last read before the previous barrier
     __syncthreads();
   }
+  // lane l holds, for block (i, j) and v = 0..3, row 4 (l >> 4) + v and column l & 15
+  const int q = lane >> 4, cl = lane & 15;
 #pragma unroll
-  for (int ik = 0; ik < 2; ++ik)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int ic = 0; ic < 2; ++ic)
+    for (int v = 0; v < 4; ++v) {
+      const int k = k0 + 64 * wm + 16 * i + 4 * q + v;
+      if (k >= GH) continue;
+      float* drow = a.dW + (size_t)k * N;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int k = k0 + wm * 32 + 16 * ik + 4 * lq + v;
-        const int c = c0 + wn * 32 + 16 * ic + li;
-        if (c < N && k < GH) {
-          float* d = a.dW + (size_t)k * N + c;
-          *d = a.accumulate ? *d + acc[ik][ic][v] : acc[ik][ic][v];
-        }
+      for (int j = 0; j < 4; ++j) {
+        const int c = c0 + 64 * wn + 16 * j + cl;
+        if (c < N) drow[c] = a.accumulate ? drow[c] + acc[i][j][v] : acc[i][j][v];
       }
-  if (do_bias && wave == 0 && k0 + lane < GH) a.db[k0 + lane] = a.accumulate ? a.db[k0 + lane] + bsum : bsum;
+    }
+  if (do_bias && k0 + tid < GH) a.db[k0 + tid] = a.accumulate ? a.db[k0 + tid] + bsum : bsum;
 }
 
 __global__ void transpose_wh_u16(const uint16_t* __restrict__ W, uint16_t* __restrict__ WhT, int GH, int D,
@@ -130,10 +169,10 @@ __global__ void transpose_wh_u16(const uint16_t* __restrict__ W, uint16_t* __res
 }  // namespace
 
 hipError_t launch_dw_bf16(const DwArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  if (a.GH % 32 != 0 || (a.D + a.H) % 32 != 0) return hipErrorInvalidValue;
+  if (a.GH % 8 != 0 || a.D % 8 != 0 || a.H % 8 != 0 || a.R < 1) return hipErrorInvalidValue;
   const int N = a.D + a.H;
-  dim3 grid((a.GH + kT - 1) / kT, (N + kT - 1) / kT);
-  hipExtLaunchKernelGGL(dw_bf16, grid, dim3(256), 0, s, e0, e1, 0, a);
+  dim3 grid((a.GH + kTM - 1) / kTM, (N + kTN - 1) / kTN);
+  hipExtLaunchKernelGGL(dw_bf16, grid, dim3(512), 0, s, e0, e1, 0, a);
   return hipGetLastError();
 }
 

@@ -31,6 +31,7 @@ struct StepArgs {
   void* zbar_out;        // op: adjoint: zbar_t [B][G*H]
   float* cbar_out;       // adjoint: cbar_t [B][H] (LSTM)
   void* hwin_out;        // op: adjoint: copy of h_t for the weight-gradient window
+  const float* hbar_in;  // wide-batch adjoint: hbar_{t+1} = zbar_{t+1} W_h [B][H] (unused when first)
   double* loss_acc;      // adjoint: one accumulator per workgroup
   float* dh0;            // final: dL/dh_0 [B][H]
   float* dc0;            // final: dL/dc_0 [B][H] (LSTM)
@@ -65,10 +66,22 @@ struct MlpArgs {
   void* zbar_out;         // op: zbar_l
   float* ybar_out;        // ybar_{l+1}
   void* ywin_out;         // op: copy of y_l for the weight gradient
+  const float* nn_in;     // wide-batch adjoint: ybar_{l+2} + zbar_{l+1} W_{l+1} [B][w] (unused when first)
   double* loss_acc;
   float* dy0;
   int B, w, loss, first;
   float inv_bw;
+};
+
+// One product of the wide-batch adjoint: out = add (if given) + A Bm, A [M][K]
+// bf16 row-major; Bm(k, n) = B[n][k] ("NT", the cell's W_h^T) or B[k][n]
+// ("NN", the MLP's W_{l+1}); out and add fp32 [M][N].
+struct ProdArgs {
+  const void* A;
+  const void* B;
+  const float* add;
+  float* out;
+  int M, N, K;
 };
 
 enum StepMode { kForward = 0, kAdjoint = 1, kFinal = 2 };
@@ -143,6 +156,17 @@ hipError_t launch_step_small(int G, int bf16, int mode, const StepArgs& a, hipSt
                              hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 void resmlp_grid(int B, int w, dim3* grid, dim3* block);
 hipError_t launch_resmlp(int bf16, int mode, const MlpArgs& a, hipStream_t s);
+// Wide-batch bf16 path (B >= 48): the cell kernel takes 64 rows x 64 gate
+// columns per workgroup; the adjoint's products run as launches of their own.
+bool cell_wide_fits(int D, int H);  // D and H multiples of 64
+int cell_wide_tiles(int G, int B, int H);
+hipError_t launch_cell_wide(int G, int mode, const StepArgs& a, hipStream_t s, hipEvent_t e0 = nullptr,
+                            hipEvent_t e1 = nullptr);
+hipError_t launch_prod_nt(const ProdArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+hipError_t launch_prod_nn(const ProdArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+int mlp_wide_tiles(int B, int w);
+hipError_t launch_mlp_wide(int mode, const MlpArgs& a, hipStream_t s, hipEvent_t e0 = nullptr,
+                           hipEvent_t e1 = nullptr);
 hipError_t launch_dw_bf16(const DwArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_transpose_wh_bf16(const void* W, void* WhT, int GH, int D, int H, hipStream_t s);
 hipError_t launch_transpose_wh(const float* W, float* WhT, int GH, int D, int H, hipStream_t s);

@@ -66,6 +66,10 @@ struct Layout {
   StepCfg cfg{1, 1, 1};  // single-launch path
   bool small = false;    // one-launch small-batch path (step_small)
   bool mlp = false;      // residual MLP (per-layer weights, one-step dW windows)
+  // wide-batch bf16 path (B >= 48): cell / layer kernels over up to 128 rows,
+  // the adjoint's products as launches of their own (wide_bf16.hip)
+  bool wide = false;
+  size_t off_hbar = 0;   // fp32 [B][H]: hbar_{t+1} (cell) or ybar_{l+2} + zbar_{l+1} W_{l+1} (MLP)
   // resident whole-pass kernel (fp32 RNN / LSTM whose weights fit in registers)
   bool res = false;
   int r_mtiles = 0, r_ng = 0, r_nwg = 0, r_S = 0;
@@ -133,6 +137,12 @@ Layout make_layout(const ambptt_problem* p, int window) {
     resmlp_grid(p->batch, p->hidden, &grid, &block);
     L.loss_slots = int(grid.x * grid.y);
   }
+  if (p->dtype == AMBPTT_BF16 && p->batch >= 48 &&
+      (L.mlp ? p->hidden % 64 == 0 : cell_wide_fits(p->input, p->hidden))) {
+    L.wide = true;
+    const int tiles = L.mlp ? mlp_wide_tiles(p->batch, p->hidden) : cell_wide_tiles(L.G, p->batch, p->hidden);
+    L.loss_slots = std::max(L.loss_slots, 8 * ((tiles + 7) / 8));
+  }
   if (!L.mlp && p->dtype == AMBPTT_F32) {
     const int U = resident_units(L.G);
     const int K1 = p->input + p->hidden;
@@ -162,6 +172,9 @@ Layout make_layout(const ambptt_problem* p, int window) {
   L.off_cbar[1] = o; o += align_up(BH * 4);
   L.off_loss = o; o += align_up((size_t)L.loss_slots * 8);
   L.off_lossout = o; o += kAlign;
+  if (L.wide) {
+    L.off_hbar = o; o += align_up(BH * 4);
+  }
   if (L.res) {
     const size_t U = size_t(resident_units(L.G)), K1 = size_t(p->input + p->hidden);
     const size_t mt = size_t(L.r_mtiles), ng = size_t(L.r_ng), nwg = size_t(L.r_nwg);
@@ -204,6 +217,7 @@ struct ambptt_ctx {
   bool elide_prefetch = true;
   int window_opt = 0;
   int path_opt = 0;            // 0: resident kernel when it fits, 1: per-step launches, 2: resident kernel
+  bool wide_opt = true;        // use the wide-batch bf16 kernels where the layout provides them
   int res_cap = -1;            // resident workgroups the device holds at once (-1: not queried)
   int64_t res_timeout_ms = 2000;
   bool res_test_stall = false;
@@ -239,10 +253,14 @@ struct Exec {
   int64_t calls[6] = {0, 0, 0, 0, 0, 0};
   std::vector<Sample> samples;
   bool live_dead = false;  // the live state was consumed by an adjoint step
+  bool wide = false;       // wide-batch bf16 kernels
+  float* hbuf = nullptr;   // their adjoint product (fp32 [B][H])
 
   Exec(ambptt_ctx* c, const void* x_, const void* W_, const float* b_)
       : C(c), L(c->L), p(c->p), x((const char*)x_), W(W_), b(b_), slot_t(size_t(c->p.fast_slots), -1) {
     WhT = C->ws + L.off_wht;
+    wide = L.wide && C->wide_opt;
+    if (wide) hbuf = (float*)(C->ws + L.off_hbar);
   }
   const void* x_at(int64_t t) const { return x + (size_t)t * p.batch * p.input * L.dsize; }
 
@@ -313,6 +331,7 @@ struct Exec {
   }
 
   hipError_t launch(int mode, const StepArgs& a, hipEvent_t e0, hipEvent_t e1) const {
+    if (wide && mode != kFinal) return launch_cell_wide(L.G, mode, a, C->cs, e0, e1);
     return L.small ? launch_step_small(L.G, p.dtype == AMBPTT_BF16, mode, a, C->cs, e0, e1)
                    : launch_step(L.G, mode, L.cfg, a, C->cs, e0, e1);
   }
@@ -339,8 +358,9 @@ struct Exec {
       MlpArgs a = mlp_args(t);
       a.y = src;
       a.y_out = dst;
-      return timed(AMBPTT_K_FWD, [&](hipEvent_t, hipEvent_t) {
-        return launch_resmlp(p.dtype == AMBPTT_BF16, kForward, a, C->cs);
+      return timed(AMBPTT_K_FWD, [&](hipEvent_t e0, hipEvent_t e1) {
+        return wide ? launch_mlp_wide(kForward, a, C->cs, e0, e1)
+                    : launch_resmlp(p.dtype == AMBPTT_BF16, kForward, a, C->cs);
       });
     }
     StepArgs a = base_args();
@@ -394,9 +414,19 @@ struct Exec {
       a.ybar_out = cbar(t);
       a.ywin_out = hwin_at(t);
       a.loss_acc = (double*)(C->ws + L.off_loss);
-      s = timed(AMBPTT_K_ADJ, [&](hipEvent_t, hipEvent_t) {
-        return launch_resmlp(p.dtype == AMBPTT_BF16, kAdjoint, a, C->cs);
-      });
+      if (wide) {
+        if (!first) {  // ybar_{l+2} + zbar_{l+1} W_{l+1}
+          ProdArgs pa{a.zbar_in, a.Wn, a.ybar_in, hbuf, p.batch, p.hidden, p.hidden};
+          s = timed(AMBPTT_K_HADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch_prod_nn(pa, C->cs, e0, e1); });
+          if (s != AMBPTT_OK) return s;
+          a.nn_in = hbuf;
+        }
+        s = timed(AMBPTT_K_ADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch_mlp_wide(kAdjoint, a, C->cs, e0, e1); });
+      } else {
+        s = timed(AMBPTT_K_ADJ, [&](hipEvent_t, hipEvent_t) {
+          return launch_resmlp(p.dtype == AMBPTT_BF16, kAdjoint, a, C->cs);
+        });
+      }
     } else {
       StepArgs a = base_args();
       a.x = x_at(t);
@@ -410,6 +440,12 @@ struct Exec {
       a.cbar_out = cbar(t);
       a.hwin_out = hwin_at(t);
       a.loss_acc = (double*)(C->ws + L.off_loss);
+      if (wide && !first) {  // hbar_{t+1} = zbar_{t+1} W_h
+        ProdArgs pa{a.zbar_in, WhT, nullptr, hbuf, p.batch, p.hidden, L.G * p.hidden};
+        s = timed(AMBPTT_K_HADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch_prod_nt(pa, C->cs, e0, e1); });
+        if (s != AMBPTT_OK) return s;
+        a.hbar_in = hbuf;
+      }
       s = timed(AMBPTT_K_ADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch(kAdjoint, a, e0, e1); });
     }
     if (s != AMBPTT_OK) return s;
@@ -455,6 +491,10 @@ struct Exec {
       a.zbar_in = zbar_at(0);
       a.ybar_in = cbar(0);
       a.dy0 = dh0;
+      if (wide) {  // dL/dy_0 = ybar_1 + zbar_0 W_0
+        ProdArgs pa{a.zbar_in, a.Wn, a.ybar_in, dh0, p.batch, p.hidden, p.hidden};
+        return timed(AMBPTT_K_OTHER, [&](hipEvent_t e0, hipEvent_t e1) { return launch_prod_nn(pa, C->cs, e0, e1); });
+      }
       return timed(AMBPTT_K_OTHER, [&](hipEvent_t, hipEvent_t) {
         return launch_resmlp(p.dtype == AMBPTT_BF16, kFinal, a, C->cs);
       });
@@ -464,6 +504,14 @@ struct Exec {
     a.cbar_in = cbar(0);
     a.dh0 = dh0;
     a.dc0 = dc0;
+    if (wide) {  // dL/dh_0 = zbar_0 W_h, dL/dc_0 = cbar_0
+      ProdArgs pa{a.zbar_in, WhT, nullptr, dh0, p.batch, p.hidden, L.G * p.hidden};
+      ambptt_status s =
+          timed(AMBPTT_K_OTHER, [&](hipEvent_t e0, hipEvent_t e1) { return launch_prod_nt(pa, C->cs, e0, e1); });
+      if (s != AMBPTT_OK) return s;
+      if (L.G == 4) HIPCK(hipMemcpyAsync(dc0, a.cbar_in, (size_t)p.batch * p.hidden * 4, hipMemcpyDeviceToDevice, C->cs));
+      return AMBPTT_OK;
+    }
     return timed(AMBPTT_K_OTHER, [&](hipEvent_t e0, hipEvent_t e1) { return launch(kFinal, a, e0, e1); });
   }
 
@@ -990,6 +1038,8 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
   } else if (k == "path") {
     if (v < 0 || v > 2) return fail(AMBPTT_EINVAL, "path must be 0 (auto), 1 (per-step launches) or 2 (resident)");
     C->path_opt = int(v);
+  } else if (k == "wide_batch") {
+    C->wide_opt = v != 0;
   } else if (k == "resident_cooperative") {
     C->res_coop = v != 0;
   } else if (k == "resident_test_stall") {

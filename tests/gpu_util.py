@@ -42,10 +42,11 @@ def device_inputs(wl, x, W, b, x0):
 
 
 def run_gpu(wl, dev_in, window: int | None = None, timing_sample: int = 0, elide: bool = True,
-            path: int | None = None, **spec_kw):
+            path: int | None = None, wide: bool | None = None, **spec_kw):
     """One forward + reverse pass on the GPU; returns numpy results and stats.
 
-    path: None (library default), 1 (one launch per step), 2 (resident kernel)."""
+    path: None (library default), 1 (one launch per step), 2 (resident kernel).
+    wide: None (library default), False (no wide-batch bf16 kernels)."""
     import paper_1806_01117_amd as amb
     spec = amb.ProblemSpec.from_workload(wl, **spec_kw)
     say(wl.name, spec, "path", path)
@@ -55,6 +56,8 @@ def run_gpu(wl, dev_in, window: int | None = None, timing_sample: int = 0, elide
             r.set("path", path)
         if window is not None:
             r.set("window", window)
+        if wide is not None:
+            r.set("wide_batch", 1 if wide else 0)
         if timing_sample:
             r.set("timing_sample", timing_sample)
         r.set("elide_prefetch", 1 if elide else 0)
