@@ -36,8 +36,7 @@
 namespace ambptt {
 namespace {
 
-constexpr int kWaves = 8;
-constexpr int kThreads = 64 * kWaves;
+constexpr int kWaves = 8;  // waves per workgroup of the launched kernels
 constexpr int kSlot = 2048;  // one 16-row x 128-byte scratch tile
 
 typedef unsigned int u4v __attribute__((ext_vector_type(4)));
@@ -99,15 +98,16 @@ __device__ __forceinline__ Rows rows_of(const void* p, unsigned bytes, int row0,
 }
 
 // Per-lane LDS offsets within one 16 x 128-byte scratch tile.  Row t's
-// 16-byte group k sits at slot k ^ sw(t), sw(t) = (t & 7) ^ ((t >> 3) & 1):
-// the 8 lanes that write one row hit 8 different slots, and the 16 lanes that
-// read one fragment column spread over the banks.
+// 16-byte group k sits at slot k ^ (t & 7): the 8 lanes that write one row hit
+// 8 different slots, and the reads of one fragment column spread over the
+// banks (measured free of bank conflicts on gfx950, where an extra flip for
+// rows 8..15 was not).
 struct Xpose {
   unsigned w0, w1;  // writes of the rows-0..7 and rows-8..15 instructions
   unsigned r0, r1;  // fragment reads: reduction indices 0..31 and 32..63 of the block
   __device__ __forceinline__ void init() {
     const int lane = threadIdx.x & 63;
-    auto sw = [](int t) { return (t & 7) ^ ((t >> 3) & 1); };
+    auto sw = [](int t) { return t & 7; };
     const int t0 = lane >> 3, t1 = 8 + (lane >> 3), k = lane & 7;
     w0 = unsigned(t0 * 128 + 16 * (k ^ sw(t0)));
     w1 = unsigned(t1 * 128 + 16 * (k ^ sw(t1)));
@@ -221,20 +221,20 @@ __device__ __forceinline__ void put_partials(float* ps, int wave, const f4 (&acc
 #pragma unroll
       for (int v = 0; v < 4; ++v) p[(16 * i + 4 * q + v) * LD + nb * 16 + r] = acc[i][nb][v];
 }
-template <int RT, int NB>
+template <int RT, int NB, int NW>
 __device__ __forceinline__ float sum_partials(const float* ps, int row, int col) {
   constexpr int LD = 16 * NB + 1, W = 16 * RT * LD;
   float s = 0.f;
 #pragma unroll
-  for (int wv = 0; wv < kWaves; ++wv) s += ps[wv * W + row * LD + col];
+  for (int wv = 0; wv < NW; ++wv) s += ps[wv * W + row * LD + col];
   return s;
 }
 
 // LDS of a kernel: the partial sums, or the waves' scratch, whichever is larger
-template <int RT, int NB, int SCR>
+template <int RT, int NB, int SCR, int NW>
 constexpr int lds_bytes() {
-  constexpr int ps = kWaves * 16 * RT * (16 * NB + 1) * 4;
-  constexpr int sc = kWaves * SCR;
+  constexpr int ps = NW * 16 * RT * (16 * NB + 1) * 4;
+  constexpr int sc = NW * SCR;
   return ps > sc ? ps : sc;
 }
 
@@ -247,8 +247,8 @@ constexpr int lds_bytes() {
 // step t): with hbar_{t+1} from the product launch before it (absent for the
 // first turn) it forms zbar_t, cbar_t, the loss term and the copy of h_t for
 // the weight-gradient window.
-template <int G, int MODE>
-__global__ __launch_bounds__(kThreads) void cell_wide(StepArgs a) {
+template <int G, int MODE, int NW = kWaves, int S = 2>
+__global__ __launch_bounds__(64 * NW) void cell_wide(StepArgs a) {
   constexpr int RT = 4, NB = 4, TM = 64;
   constexpr int UN = 64 / G;  // hidden units of the tile
   constexpr int SCR = (RT + NB) * kSlot;
@@ -259,7 +259,7 @@ __global__ __launch_bounds__(kThreads) void cell_wide(StepArgs a) {
   if (w >= ntile) return;  // grid padding (the whole workgroup leaves together)
   const int m0 = (w % mg) * TM, j0 = (w / mg) * UN;
 
-  __shared__ __attribute__((aligned(16))) char lds[lds_bytes<RT, NB, SCR>()];
+  __shared__ __attribute__((aligned(16))) char lds[lds_bytes<RT, NB, SCR, NW>()];
   float* ps = (float*)lds;
   {
     f4 acc[RT][NB];
@@ -270,11 +270,11 @@ __global__ __launch_bounds__(kThreads) void cell_wide(StepArgs a) {
     Xpose X;
     X.init();
     const int nbk = K1 / 64, nbx = D / 64;
-    const int c0 = (nbk * wave) / kWaves, c1 = (nbk * (wave + 1)) / kWaves;
+    const int c0 = (nbk * wave) / NW, c1 = (nbk * (wave + 1)) / NW;
     const Rows xs = rows_of(a.x, unsigned(B * D * 2), m0, 2 * D);
     const Rows hs = rows_of(a.h, unsigned(B * H * 2), m0, 2 * H);
     const Rows ws = rows_of(a.W, unsigned(GH * K1 * 2), 0, 2 * K1);
-    nt_rows<RT, NB, 2>(
+    nt_rows<RT, NB, S>(
         c0, c1, lds + wave * SCR, X, acc,
         [&](int g, int h, int blk) -> u4v {  // an x or an h block: the same choice for the whole wave
           return blk < nbx ? xs.load(g, h, blk) : hs.load(g, h, blk - nbx);
@@ -287,14 +287,14 @@ __global__ __launch_bounds__(kThreads) void cell_wide(StepArgs a) {
 
   // epilogue: pair (row ml, unit u), consecutive threads on consecutive units
   float lterm = 0.f;
-  for (int pi = tid; pi < TM * UN; pi += kThreads) {
+  for (int pi = tid; pi < TM * UN; pi += 64 * NW) {
     const int ml = pi / UN, u = pi % UN;
     const int m = m0 + ml, j = j0 + u;
     if (m >= B) continue;
     const int o = m * H + j;
     float z[G];
 #pragma unroll
-    for (int g = 0; g < G; ++g) z[g] = sum_partials<RT, NB>(ps, ml, g * UN + u) + a.bias[g * H + j];
+    for (int g = 0; g < G; ++g) z[g] = sum_partials<RT, NB, NW>(ps, ml, g * UN + u) + a.bias[g * H + j];
     float h1, c1 = 0.f, tc = 0.f, ig = 0.f, fg = 0.f, gg = 0.f, og = 0.f, cold = 0.f;
     if (G == 4) {
       ig = sigm(z[0]);
@@ -347,13 +347,13 @@ __global__ __launch_bounds__(kThreads) void cell_wide(StepArgs a) {
   }
   if (MODE == kAdjoint) {
     const float s = wave_sum(lterm);
-    __shared__ float wsum[kWaves];
+    __shared__ float wsum[NW];
     if (lane == 0) wsum[wave] = s;
     __syncthreads();
     if (tid == 0) {
       float t = 0.f;
 #pragma unroll
-      for (int wv = 0; wv < kWaves; ++wv) t += wsum[wv];
+      for (int wv = 0; wv < NW; ++wv) t += wsum[wv];
       a.loss_acc[w] += (double)t;
     }
   }
@@ -368,12 +368,11 @@ __global__ __launch_bounds__(kThreads) void cell_wide(StepArgs a) {
 //     64): each block's 64 x 64 elements of B go to the wave's scratch as
 //     loaded and are read back by columns, so no transposed copy of the
 //     weights is kept.
-template <int RT, int NB, bool NN>
-__global__ __launch_bounds__(kThreads) void prod_wide(ProdArgs a) {
+template <int RT, int NB, bool NN, int NW = kWaves, int S = NN ? 2 : (RT * NB >= 4 ? 3 : 4)>
+__global__ __launch_bounds__(64 * NW) void prod_wide(ProdArgs a) {
   constexpr int TM = 16 * RT, TN = 16 * NB;
   constexpr int BLD = 66;  // NN: pitch (bf16) of the B block: conflict-free column reads
   constexpr int SCR = NN ? RT * kSlot + 64 * BLD * 2 : (RT + NB) * kSlot;
-  constexpr int S = NN ? 2 : (RT * NB >= 4 ? 3 : 4);
   static_assert(!NN || TN == 64, "the NN product takes 64-column tiles");
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int M = a.M, N = a.N, K = a.K;
@@ -382,14 +381,14 @@ __global__ __launch_bounds__(kThreads) void prod_wide(ProdArgs a) {
   if (w >= ntile) return;
   const int m0 = (w % mg) * TM, n0 = (w / mg) * TN;
 
-  __shared__ __attribute__((aligned(16))) char lds[lds_bytes<RT, NB, SCR>()];
+  __shared__ __attribute__((aligned(16))) char lds[lds_bytes<RT, NB, SCR, NW>()];
   f4 acc[RT][NB];
 #pragma unroll
   for (int i = 0; i < RT; ++i)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[i][nb] = f4{0.f, 0.f, 0.f, 0.f};
   const int nbk = K / 64;
-  const int c0 = (nbk * wave) / kWaves, c1 = (nbk * (wave + 1)) / kWaves;
+  const int c0 = (nbk * wave) / NW, c1 = (nbk * (wave + 1)) / NW;
   Xpose X;
   X.init();
   char* scr = lds + wave * SCR;
@@ -449,11 +448,11 @@ __global__ __launch_bounds__(kThreads) void prod_wide(ProdArgs a) {
   float* ps = (float*)lds;
   put_partials<RT, NB>(ps, wave, acc);
   __syncthreads();
-  for (int pi = tid; pi < TM * TN; pi += kThreads) {
+  for (int pi = tid; pi < TM * TN; pi += 64 * NW) {
     const int ml = pi / TN, nl = pi % TN;
     const int m = m0 + ml;
     if (m >= M) continue;
-    const float s = sum_partials<RT, NB>(ps, ml, nl);
+    const float s = sum_partials<RT, NB, NW>(ps, ml, nl);
     const size_t o = (size_t)m * N + n0 + nl;
     a.out[o] = a.add ? a.add[o] + s : s;
   }
@@ -465,8 +464,8 @@ __global__ __launch_bounds__(kThreads) void prod_wide(ProdArgs a) {
 // Forward: y_{l+1} = y_l + relu(z_l).  Adjoint (recomputation of layer l):
 // ybar_{l+1} = nn_in (= ybar_{l+2} + zbar_{l+1} W_{l+1}, from the product
 // launch before it) plus the loss seed; zbar_l = ybar_{l+1} 1[z_l > 0].
-template <int MODE>
-__global__ __launch_bounds__(kThreads) void mlp_wide(MlpArgs a) {
+template <int MODE, int NW = kWaves, int S = 2>
+__global__ __launch_bounds__(64 * NW) void mlp_wide(MlpArgs a) {
   constexpr int RT = 4, NB = 4, TM = 64, TN = 64;
   constexpr int SCR = (RT + NB) * kSlot;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -476,7 +475,7 @@ __global__ __launch_bounds__(kThreads) void mlp_wide(MlpArgs a) {
   if (tile >= ntile) return;
   const int m0 = (tile % mg) * TM, n0 = (tile / mg) * TN;
 
-  __shared__ __attribute__((aligned(16))) char lds[lds_bytes<RT, NB, SCR>()];
+  __shared__ __attribute__((aligned(16))) char lds[lds_bytes<RT, NB, SCR, NW>()];
   float* ps = (float*)lds;
   {
     f4 acc[RT][NB];
@@ -487,10 +486,10 @@ __global__ __launch_bounds__(kThreads) void mlp_wide(MlpArgs a) {
     Xpose X;
     X.init();
     const int nbk = w / 64;
-    const int c0 = (nbk * wave) / kWaves, c1 = (nbk * (wave + 1)) / kWaves;
+    const int c0 = (nbk * wave) / NW, c1 = (nbk * (wave + 1)) / NW;
     const Rows ys = rows_of(a.y, unsigned(B * w * 2), m0, 2 * w);
     const Rows ws = rows_of(a.W, unsigned(w * w * 2), n0, 2 * w);
-    nt_rows<RT, NB, 2>(
+    nt_rows<RT, NB, S>(
         c0, c1, lds + wave * SCR, X, acc, [&](int g, int h, int blk) -> u4v { return ys.load(g, h, blk); },
         [&](int g, int h, int blk) -> u4v { return ws.load(g, h, blk); });
     __syncthreads();  // every wave has left its scratch
@@ -499,12 +498,12 @@ __global__ __launch_bounds__(kThreads) void mlp_wide(MlpArgs a) {
   __syncthreads();
 
   float lterm = 0.f;
-  for (int pi = tid; pi < TM * TN; pi += kThreads) {
+  for (int pi = tid; pi < TM * TN; pi += 64 * NW) {
     const int ml = pi / TN, nl = pi % TN;
     const int m = m0 + ml, c = n0 + nl;
     if (m >= B) continue;
     const size_t o = (size_t)m * w + c;
-    const float z = sum_partials<RT, NB>(ps, ml, nl) + a.bias[c];
+    const float z = sum_partials<RT, NB, NW>(ps, ml, nl) + a.bias[c];
     const float yv = (float)((const __bf16*)a.y)[o];
     const __bf16 y1s = (__bf16)(yv + fmaxf(z, 0.f));
     if (MODE == kForward) {
@@ -537,13 +536,13 @@ __global__ __launch_bounds__(kThreads) void mlp_wide(MlpArgs a) {
   }
   if (MODE == kAdjoint) {
     const float s = wave_sum(lterm);
-    __shared__ float wsum[kWaves];
+    __shared__ float wsum[NW];
     if (lane == 0) wsum[wave] = s;
     __syncthreads();
     if (tid == 0) {
       float t = 0.f;
 #pragma unroll
-      for (int wv = 0; wv < kWaves; ++wv) t += wsum[wv];
+      for (int wv = 0; wv < NW; ++wv) t += wsum[wv];
       a.loss_acc[tile] += (double)t;
     }
   }
@@ -559,7 +558,7 @@ int cell_wide_tiles(int G, int B, int H) { return ((B + 63) / 64) * (H / (64 / G
 
 hipError_t launch_cell_wide(int G, int mode, const StepArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if ((mode != kForward && mode != kAdjoint) || !cell_wide_fits(a.D, a.H)) return hipErrorInvalidValue;
-  const dim3 grid(grid_for(cell_wide_tiles(G, a.B, a.H))), block(kThreads);
+  const dim3 grid(grid_for(cell_wide_tiles(G, a.B, a.H))), block(64 * kWaves);
   if (G == 4) {
     if (mode == kForward) hipExtLaunchKernelGGL((cell_wide<4, kForward>), grid, block, 0, s, e0, e1, 0, a);
     else hipExtLaunchKernelGGL((cell_wide<4, kAdjoint>), grid, block, 0, s, e0, e1, 0, a);
@@ -574,7 +573,7 @@ bool prod_wide_big(int M, int N) { return N % 32 == 0 && ((M + 31) / 32) * (N / 
 
 hipError_t launch_prod_nt(const ProdArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (a.K % 64 != 0 || a.N % 16 != 0 || a.M < 1) return hipErrorInvalidValue;
-  const dim3 block(kThreads);
+  const dim3 block(64 * kWaves);
   if (prod_wide_big(a.M, a.N)) {
     const dim3 grid(grid_for(((a.M + 31) / 32) * (a.N / 32)));
     hipExtLaunchKernelGGL((prod_wide<2, 2, false>), grid, block, 0, s, e0, e1, 0, a);
@@ -587,7 +586,7 @@ hipError_t launch_prod_nt(const ProdArgs& a, hipStream_t s, hipEvent_t e0, hipEv
 
 hipError_t launch_prod_nn(const ProdArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (a.K % 64 != 0 || a.N % 64 != 0 || a.M < 1) return hipErrorInvalidValue;
-  const dim3 grid(grid_for(((a.M + 63) / 64) * (a.N / 64))), block(kThreads);
+  const dim3 grid(grid_for(((a.M + 63) / 64) * (a.N / 64))), block(64 * kWaves);
   hipExtLaunchKernelGGL((prod_wide<4, 4, true>), grid, block, 0, s, e0, e1, 0, a);
   return hipGetLastError();
 }
@@ -596,7 +595,7 @@ int mlp_wide_tiles(int B, int w) { return ((B + 63) / 64) * (w / 64); }
 
 hipError_t launch_mlp_wide(int mode, const MlpArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (a.w % 64 != 0) return hipErrorInvalidValue;
-  const dim3 grid(grid_for(mlp_wide_tiles(a.B, a.w))), block(kThreads);
+  const dim3 grid(grid_for(mlp_wide_tiles(a.B, a.w))), block(64 * kWaves);
   if (mode == kForward) hipExtLaunchKernelGGL((mlp_wide<kForward>), grid, block, 0, s, e0, e1, 0, a);
   else if (mode == kAdjoint) hipExtLaunchKernelGGL((mlp_wide<kAdjoint>), grid, block, 0, s, e0, e1, 0, a);
   else return hipErrorInvalidValue;
