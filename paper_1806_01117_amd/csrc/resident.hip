@@ -126,7 +126,10 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 // KCH: 16-wide reduction chunks per wave (the reduction is zero-padded to
-// 8 KCH chunks, so no loop over chunks has a bound that varies by wave)
+// 8 KCH chunks, so no loop over chunks has a bound that varies by wave).
+// Wave w holds chunks w, w + 8, w + 16, ...: every wave then has its share of
+// the x columns and of the h columns, and the x part of a step's gate GEMM
+// (which depends on no other workgroup) runs while the h_t rows are loaded.
 template <int G, int KCH>
 __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
   constexpr int U = (G == 4) ? 8 : 16;
@@ -161,7 +164,8 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
   const int ub0 = op_ * UM;
   const int m0 = 16 * mt, j0 = U * ug;
   const int nch = K1 / 16;
-  const int c0 = KCH * wave;  // chunks c0 .. c0 + KCH - 1; those >= nch are zero
+  const int nxc = D / 16;     // chunks of the x columns
+  auto chunk = [&](int i) { return wave + kWaves * i; };  // slot i of this wave; chunks >= nch are zero
   const unsigned hbytes = unsigned(B) * unsigned(H) * 4u;
   const unsigned sbytes = G == 4 ? unsigned(a.c_off) + hbytes : hbytes;
   auto wrow = [&](int n) { return (n / U) * H + j0 + (n % U); };  // W row of gate column n
@@ -184,7 +188,7 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
   f4 Wr[KCH][NB];  // B operands of the gate GEMM: W[col][16 ch + 4 q + e]
 #pragma unroll
   for (int i = 0; i < KCH; ++i) {
-    const int ch = c0 + i;
+    const int ch = chunk(i);
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
       Wr[i][nb] = ch < nch ? *(const f4*)(a.W + (size_t)wrow(nb * 16 + r) * K1 + ch * 16 + 4 * q)
@@ -207,7 +211,7 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
     const int w = 16 * kWaves * KCH - K1;
     xs[idx / w][K1 + idx % w] = 0.f;
   }
-  f4 dacc[KCH][NB];  // dW blocks (gate block nb, reduction chunk c0 + i)
+  f4 dacc[KCH][NB];  // dW blocks (gate block nb, reduction chunk chunk(i))
 #pragma unroll
   for (int i = 0; i < KCH; ++i)
 #pragma unroll
@@ -327,7 +331,7 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
   };
   // weight gradient of the workgroup's gate rows for the last adjoint step,
   // dW += zbar^T [x | h], on the wave's own reduction chunks (block (nb,
-  // chunk c0 + i) of 16 x 16).  It feeds nothing the other workgroups wait
+  // chunk chunk(i)) of 16 x 16).  It feeds nothing the other workgroups wait
   // for, so it runs after this workgroup has raised its flag for the next
   // barrier, while the flags of the others are on their way.
   bool pend_dw = false;
@@ -338,7 +342,7 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) av[buf_][nb] = zb[4 * c4 + q][nb * 16 + r];
 #pragma unroll
-      for (int i = 0; i < KCH; ++i) bv[buf_][i] = xs[4 * c4 + q][(c0 + i) * 16 + r];
+      for (int i = 0; i < KCH; ++i) bv[buf_][i] = xs[4 * c4 + q][chunk(i) * 16 + r];
     };
     load(0, 0);
 #pragma unroll
@@ -416,41 +420,74 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
     }
     float cold = 0.f;
     if (G == 4 && erow) cold = ld1<kDev>(srs, unsigned(a.c_off) + eoff);
-    if (!enter()) return false;
-    // stage [x_t | h_t]; the adjoint also sums the partial h-adjoints of step t + 1
-    if (tid < kStageThreads) {
-      const int nh4 = 4 * H;
-      for (int idx = tid; idx < nh4; idx += kStageThreads) {
-        const int row = idx / (H / 4), col = 4 * (idx % (H / 4));
-        f4 v = f4{0.f, 0.f, 0.f, 0.f};
-        if (m0 + row < B) v = ld4<kDev>(srs, unsigned(((m0 + row) * H + col) * 4));
-        *(f4*)&xs[row][D + col] = v;
+    f4 acc[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[nb] = f4{0.f, 0.f, 0.f, 0.f};
+    auto gemm_part = [&](bool xpart) {
+      f4 av[KCH];
+#pragma unroll
+      for (int i = 0; i < KCH; ++i) {
+        const int ch = chunk(i);
+        if (xpart ? ch < nxc : (ch >= nxc && ch < nch)) av[i] = *(const f4*)&xs[r][ch * 16 + 4 * q];
       }
-      if (adj && !first) stage_partials();
+#pragma unroll
+      for (int i = 0; i < KCH; ++i) {
+        const int ch = chunk(i);
+        if (xpart ? ch < nxc : (ch >= nxc && ch < nch)) {
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) acc[nb] = mma4(av[i], Wr[i][nb], acc[nb]);
+        }
+      }
+    };
+    if (!enter()) return false;
+    // stage h_t next to x_t (and, in an adjoint step, the octet partials of
+    // step t + 1): the loads are issued first, the x part of the gate GEMM
+    // z[16][NC] = [x|h] W^T runs while they travel, then they go to LDS
+    constexpr int NHV = (4 * kHmax + kStageThreads - 1) / kStageThreads;
+    f4 hv[NHV], qv[2];
+    const int nh4 = 4 * H;
+    if (tid < kStageThreads) {
+#pragma unroll
+      for (int j = 0; j < NHV; ++j) {
+        const int idx = tid + j * kStageThreads, row = idx / (H / 4), col = 4 * (idx % (H / 4));
+        hv[j] = f4{0.f, 0.f, 0.f, 0.f};
+        if (idx < nh4 && m0 + row < B) hv[j] = ld4<kDev>(srs, unsigned(((m0 + row) * H + col) * 4));
+      }
+      if (adj && !first) {
+        const float* pin = a.P + (((size_t)((na + 1) & 1) * a.mtiles + mt) * nO) * H * 16;
+        const __amdgpu_buffer_rsrc_t prs = rsrc(pin, unsigned(nO * H * 16 * 4));
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int idx = tid + j * kStageThreads, o2 = idx / NG4, v4 = idx % NG4;
+          if (idx < nO * NG4) qv[j] = ld4<kDev>(prs, unsigned(((o2 * H + j0) * 16 + 4 * v4) * 4));
+        }
+      }
+    }
+    gemm_part(true);
+    if (tid < kStageThreads) {
+#pragma unroll
+      for (int j = 0; j < NHV; ++j) {
+        const int idx = tid + j * kStageThreads, row = idx / (H / 4), col = 4 * (idx % (H / 4));
+        if (idx < nh4) *(f4*)&xs[row][D + col] = hv[j];
+      }
+      if (adj && !first) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int idx = tid + j * kStageThreads, o2 = idx / NG4, v4 = idx % NG4;
+          if (idx < nO * NG4) *(f4*)&hp[o2][4 * v4] = qv[j];
+        }
+      }
     }
     __syncthreads();
     if (tid == 0) st_flag(a.consumed + me, sc);
     flush();
 
-    // gate GEMM: z[16][NC] = [x|h] W^T over this wave's chunks
-    {
-      f4 acc[NB];
+    // the h part of the gate GEMM
+    gemm_part(false);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) acc[nb] = f4{0.f, 0.f, 0.f, 0.f};
-      f4 av = *(const f4*)&xs[r][c0 * 16 + 4 * q];
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int i = 0; i < KCH; ++i) {
-        const f4 cur = av;
-        if (i + 1 < KCH) av = *(const f4*)&xs[r][(c0 + i + 1) * 16 + 4 * q];  // one chunk ahead
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[nb] = mma4(cur, Wr[i][nb], acc[nb]);
-      }
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) zs[wave][4 * q + v][nb * 16 + r] = acc[nb][v];
-    }
+      for (int v = 0; v < 4; ++v) zs[wave][4 * q + v][nb * 16 + r] = acc[nb][v];
     __syncthreads();
 
     float lterm = 0.f;
@@ -661,7 +698,7 @@ __global__ __launch_bounds__(kThreads) void resident_pass(ResidentArgs a) {
   }
 #pragma unroll
   for (int i = 0; i < KCH; ++i) {
-    const int ch = c0 + i;
+    const int ch = chunk(i);
     if (ch < nch) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
