@@ -302,7 +302,15 @@ def main() -> int:
             k = "step_small" if small else "step_f32"
             names = {"fwd": f"{k} forward: gate GEMM + cell update", "adj": f"{k} adjoint: gate recompute + h-adjoint GEMM",
                      "dw": ("dw_bf16" if wl.dtype == "bf16" else "dw_lds_f32") + " weight-gradient window"}
-        traffic = measured_traffic(wl.name, {"fwd": "step_small_fwd", "adj": "step_small_adj"}.get(dom, dom))
+        if wide:
+            fam = {"fwd": "mlp_wide_fwd", "adj": "mlp_wide_adj", "hadj": "prod_wide_nn"} if wl.cell == "resmlp" else \
+                {"fwd": "cell_wide_fwd", "adj": "cell_wide_adj", "hadj": "prod_wide_nt"}
+            key = fam.get(dom, "dw_bf16")
+        elif small:
+            key = {"fwd": "step_small_fwd", "adj": "step_small_adj"}.get(dom, "dw_lds_f32")
+        else:
+            key = {"fwd": "step_f32_fwd", "adj": "step_f32_adj"}.get(dom, "dw_f32_big")
+        traffic = measured_traffic(wl.name, key)
     dom_us = kern[dom][0] if dom in kern else 0.0
     achieved = flops[dom] / (dom_us * 1e-6) / 1e12 if dom_us > 0 else 0.0
     r.close()
