@@ -32,6 +32,7 @@ METRIC = "BPTT timesteps/sec at fixed HBM slot budget; recompute factor; MFMA % 
 WORKLOAD = "lstm_h512_t1000"
 FP32_MFMA_PEAK_TFLOPS = 157.3
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense
+HBM_PEAK_GBS = 8000.0
 
 
 def step_flops(spec, window: int, wide: bool = False) -> dict:
@@ -45,6 +46,37 @@ def step_flops(spec, window: int, wide: bool = False) -> dict:
     dw1 = 2.0 * G * H * (D + H + 1) * B         # dW (+ db) of one step
     return {"fwd": gate, "adj": gate if wide else gate + hbar, "hadj": hbar, "dw": dw1 * window,
             "gate": gate, "hbar": hbar, "dw1": dw1}
+
+
+def step_bytes(wl, spec, window: int, wide: bool) -> dict:
+    """Algorithmic HBM bytes of one launch of each per-step kernel: every
+    operand read once and every result written once, weights included (one
+    step's weights, 50 MB and more on the wide path, are streamed again by each
+    launch).  e is the operand size; c, the adjoints h-bar, c-bar and the MLP's
+    y-bar are fp32."""
+    B, D, H, G = spec.batch, spec.input, spec.hidden, spec.gates
+    e = 2 if wl.dtype == "bf16" else 4
+    K1, GH = D + H, G * H
+    W, b = GH * K1 * e, GH * 4
+    h, f = B * H * e, B * H * 4               # a state row block in the operand type / in fp32
+    c = f if G == 4 else 0
+    zbar = B * GH * e
+    if wl.cell == "resmlp":                  # K1 = H, G = 1, no c
+        fwd = W + b + 2 * h
+        adj = W + b + h + f + zbar + f + h          # y, the N-N product's sum in, zbar, ybar, y window out
+        if not wide:
+            adj += zbar + W + f                     # the next layer's zbar, W_{l+1} and ybar feed the product
+        hadj = zbar + W + 2 * f
+        dw = 2 * B * H * e + W // e * 4 + b         # zbar and y of one layer in, dW_l and db_l written once
+    else:
+        fwd = W + b + B * K1 * e + c + h + c
+        adj = W + b + B * K1 * e + c + f + c + zbar + c + h   # ... hbar in, cbar in, zbar, cbar, h window out
+        if not wide:
+            adj += zbar + GH * H * e - f            # zbar_{t+1} and W_h^T instead of the h-adjoint product
+        hadj = zbar + GH * H * e + f
+        R = window * B
+        dw = R * GH * e + R * K1 * e + 2 * (GH * K1 * 4 + b)   # the window's operands, dW and db read and written
+    return {"fwd": fwd, "adj": adj, "hadj": hadj, "dw": dw}
 
 
 def measured_traffic(workload: str, kernel: str):
@@ -177,7 +209,10 @@ def main() -> int:
     ap.add_argument("--host-slots", type=int, default=-1, help="host-tier slots (default: the workload's)")
     ap.add_argument("--no-compare", dest="compare", action="store_false",
                     help="skip the plain-Revolve and other-path passes")
+    ap.add_argument("--set", action="append", default=[], metavar="KEY=VALUE",
+                    help="an ambptt_set_int knob for the measured passes and the plain-Revolve comparison")
     args = ap.parse_args()
+    knobs = [(k, int(v)) for k, v in (kv.split("=", 1) for kv in args.set)]
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(--gpus must be 1)", file=sys.stderr)
@@ -213,6 +248,8 @@ def main() -> int:
     if args.path != "auto":
         r.set("path", 1 if args.path == "steps" else 2)
     r.set("resident_cooperative", args.cooperative)
+    for k, v in knobs:
+        r.set(k, v)
     I_min, t_a, t_t = r.calibrate(dx, dW, db, dh, dc)
     print(f"calibrated: I_min {I_min}, T_A {t_a:.2f} us, T_T {t_t:.2f} us", file=sys.stderr, flush=True)
     r.set("timing_sample", args.timing_sample)
@@ -249,6 +286,8 @@ def main() -> int:
         rv = amb.Runner(amb.ProblemSpec.from_workload(wl, slow_slots=0), device=dev)
         rv.set("path", 2 if resident else 1)
         rv.set("resident_cooperative", args.cooperative)
+        for k, v in knobs:
+            rv.set(k, v)
         rv_value, rvo = other_run(rv, reps if args.steps > 1 else 1, warm=args.steps > 1)
         rv_st = rvo["stats"]
         bitwise = fingerprint(rvo) == fp_async
@@ -271,6 +310,7 @@ def main() -> int:
     peak = FP32_MFMA_PEAK_TFLOPS if wl.dtype == "f32" else BF16_MFMA_PEAK_TFLOPS
     wide = st["kernel_calls"][3] > 0
     fl = step_flops(spec, st["window"], wide)
+    byts = step_bytes(wl, spec, st["window"], wide)
     kern = {}
     for i, name in enumerate(KERNEL_CLASSES):
         us = [s_["kernel_us"][i] for s_ in stats if s_["kernel_samples"][i] > 0]
@@ -281,6 +321,11 @@ def main() -> int:
         dom = "pass"
         fwd_ops = st["forward_evals"] - 1          # the first turn's forward step runs inside an adjoint
         flops = {"pass": fwd_ops * fl["gate"] + st["adjoints"] * (fl["gate"] + fl["hbar"] + fl["dw1"])}
+        e = 2 if wl.dtype == "bf16" else 4
+        GH, K1 = spec.gates * spec.hidden, spec.input + spec.hidden
+        # x_t of every forward step and adjoint, W in and dW out once, each host-tier transfer through HBM once
+        byts = {"pass": (st["forward_evals"] + st["adjoints"]) * spec.batch * spec.input * e
+                + GH * K1 * (e + 4) + 2 * GH * 4 + st["bytes_d2h"] + st["bytes_h2d"]}
         names = {"pass": "resident_pass: whole forward + reverse pass in one launch"}
         traffic = measured_traffic(wl.name, "resident_pass")
     else:
@@ -312,7 +357,15 @@ def main() -> int:
             key = {"fwd": "step_f32_fwd", "adj": "step_f32_adj"}.get(dom, "dw_f32_big")
         traffic = measured_traffic(wl.name, key)
     dom_us = kern[dom][0] if dom in kern else 0.0
-    achieved = flops[dom] / (dom_us * 1e-6) / 1e12 if dom_us > 0 else 0.0
+    # the roofline that bounds the kernel: HBM if its algorithmic bytes take
+    # longer at 8 TB/s than its flops at the MFMA peak of its operand type
+    hbm = byts[dom] / (HBM_PEAK_GBS * 1e9) > flops[dom] / (peak * 1e12)
+    if hbm:
+        achieved = byts[dom] / (dom_us * 1e-6) / 1e9 if dom_us > 0 else 0.0
+        roof_peak, roof_unit = HBM_PEAK_GBS, "GB/s"
+    else:
+        achieved = flops[dom] / (dom_us * 1e-6) / 1e12 if dom_us > 0 else 0.0
+        roof_peak, roof_unit = peak, "TFLOP/s"
     r.close()
 
     line = {
@@ -324,7 +377,7 @@ def main() -> int:
                    "hidden": wl.hidden, "n_steps": wl.n_steps, "fast_slots": wl.fast_slots,
                    "slow_slots": spec.slow_slots, "mode": "async" if st["mode"] else "revolve",
                    "interval": st["interval"], "interval_min": I_min, "t_a_us": round(t_a, 3),
-                   "t_t_us": round(t_t, 3), "window": st["window"]},
+                   "t_t_us": round(t_t, 3), "window": st["window"], **({"knobs": dict(knobs)} if knobs else {})},
         "recompute_factor": round(st["recompute_factor"], 4),
         "plain_revolve": None if rv_st is None else {
             "value": round(rv_value, 2), "unit": "timesteps/s",
@@ -339,10 +392,12 @@ def main() -> int:
         "host_link": {"bytes_d2h": st["bytes_d2h"], "bytes_h2d": st["bytes_h2d"],
                       "stores": st["stores"], "prefetches": st["prefetches"],
                       "prefetches_elided": st["prefetches_elided"], "compute_waits": st["compute_waits"]},
-        "roofline": {"bound": "mfma", "kernel": names[dom], "achieved": round(achieved, 3),
-                     "peak": peak, "unit": "TFLOP/s",
-                     "frac": round(achieved / peak, 4), "traffic": traffic,
-                     "avg_launch_us": round(dom_us, 3), "flops_per_launch": flops[dom]},
+        "roofline": {"bound": "hbm" if hbm else "mfma", "kernel": names[dom], "achieved": round(achieved, 3),
+                     "peak": roof_peak, "unit": roof_unit,
+                     "frac": round(achieved / roof_peak, 4), "traffic": traffic,
+                     "avg_launch_us": round(dom_us, 3), "flops_per_launch": flops[dom],
+                     "bytes_per_launch": int(byts[dom]),
+                     "flop_per_byte": round(flops[dom] / max(byts[dom], 1), 1)},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl)

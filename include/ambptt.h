@@ -191,7 +191,12 @@ ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
  * the pass ends in the barrier timeout; 1: hipLaunchCooperativeKernel, whose
  * runtime guarantees residency), "resident_test_stall" (1: the resident program starts with a wait
  * that is never satisfied, so the pass ends in that timeout; for tests of the
- * abort path).  EINVAL for unknown keys or values out of range. */
+ * abort path), "wide_batch" (1, default: batches of 48 rows and more in bf16
+ * run the wide-batch kernels; 0: the small-batch kernels), "dw_stream" (1:
+ * weight-gradient windows run on a stream of their own, beside the steps; 0:
+ * on the compute stream, after the window's last adjoint; -1, default: 0 on
+ * the wide-batch bf16 path, whose kernels each fill the device, else 1).  EINVAL
+ * for unknown keys or values out of range. */
 ambptt_status ambptt_set_int(ambptt_ctx* ctx, const char* key, int64_t value);
 
 /* Measures T_A (one forward step) and T_T (one state over the host link,

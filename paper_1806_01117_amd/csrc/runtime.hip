@@ -104,7 +104,12 @@ ambptt_status validate(const ambptt_problem* p) {
 
 int auto_window(const ambptt_problem* p) {
   if (p->cell == AMBPTT_CELL_RESMLP) return 1;  // every layer has its own dW
-  int w = (1024 + p->batch - 1) / p->batch;
+  // rows per window: each window reads and writes dW (fp32) once, so a window
+  // must hold enough rows for its products to outweigh that; the bf16 path's
+  // dW is large against its operands (4 bytes per weight against 2 bytes per
+  // operand element), hence the longer windows
+  const int rows = p->dtype == AMBPTT_BF16 ? 8192 : 1024;
+  int w = (rows + p->batch - 1) / p->batch;
   return std::max(1, std::min(64, w));
 }
 
@@ -220,8 +225,9 @@ struct ambptt_ctx {
   bool wide_opt = true;        // use the wide-batch bf16 kernels where the layout provides them
   int res_cap = -1;            // resident workgroups the device holds at once (-1: not queried)
   int64_t res_timeout_ms = 2000;
-  bool res_test_stall = false;
-  bool res_coop = false;         // cooperative launch of the resident kernel   // tests of the abort path: the first entry waits for a barrier that never comes
+  bool res_test_stall = false;  // tests of the abort path: the first entry waits for a barrier that never comes
+  bool res_coop = false;         // cooperative launch of the resident kernel
+  int dw_stream = -1;            // weight-gradient windows: 1 on their own stream, 0 on the compute stream, -1 by path
   int32_t* prog_host = nullptr;  // pinned staging of the resident program
   size_t prog_host_cap = 0;
   unsigned* status_host = nullptr;  // pinned copy of the resident kernel's status words
@@ -468,16 +474,22 @@ struct Exec {
         d.db = db + (size_t)t * p.hidden;
         d.accumulate = 0;
       }
-      HIPCK(hipEventRecord(C->ev_c2, C->cs));
-      HIPCK(hipStreamWaitEvent(C->ds, C->ev_c2, 0));
+      // the wide-batch kernels each fill the device: beside them a window only
+      // competes for the same units, so it runs in line on the compute stream
+      const bool own = C->dw_stream < 0 ? !wide : C->dw_stream != 0;
+      hipStream_t ws = own ? C->ds : C->cs;
+      if (own) {
+        HIPCK(hipEventRecord(C->ev_c2, C->cs));
+        HIPCK(hipStreamWaitEvent(C->ds, C->ev_c2, 0));
+      }
       s = timed(
           AMBPTT_K_DW,
           [&](hipEvent_t e0, hipEvent_t e1) {
-            return p.dtype == AMBPTT_BF16 ? launch_dw_bf16(d, C->ds, e0, e1) : launch_dw(d, C->ds, e0, e1);
+            return p.dtype == AMBPTT_BF16 ? launch_dw_bf16(d, ws, e0, e1) : launch_dw(d, ws, e0, e1);
           },
-          C->ds);
+          ws);
       if (s != AMBPTT_OK) return s;
-      HIPCK(hipEventRecord(C->ev_dw[hf], C->ds));
+      HIPCK(hipEventRecord(C->ev_dw[hf], ws));
       dw_pending[hf] = true;
     }
     return AMBPTT_OK;
@@ -1040,6 +1052,9 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
     C->path_opt = int(v);
   } else if (k == "wide_batch") {
     C->wide_opt = v != 0;
+  } else if (k == "dw_stream") {
+    if (v < -1 || v > 1) return fail(AMBPTT_EINVAL, "dw_stream must be -1 (by path), 0 or 1");
+    C->dw_stream = int(v);
   } else if (k == "resident_cooperative") {
     C->res_coop = v != 0;
   } else if (k == "resident_test_stall") {

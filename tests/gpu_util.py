@@ -42,11 +42,12 @@ def device_inputs(wl, x, W, b, x0):
 
 
 def run_gpu(wl, dev_in, window: int | None = None, timing_sample: int = 0, elide: bool = True,
-            path: int | None = None, wide: bool | None = None, **spec_kw):
+            path: int | None = None, wide: bool | None = None, opts: dict | None = None, **spec_kw):
     """One forward + reverse pass on the GPU; returns numpy results and stats.
 
     path: None (library default), 1 (one launch per step), 2 (resident kernel).
-    wide: None (library default), False (no wide-batch bf16 kernels)."""
+    wide: None (library default), False (no wide-batch bf16 kernels).
+    opts: further ambptt_set_int keys and values."""
     import paper_1806_01117_amd as amb
     spec = amb.ProblemSpec.from_workload(wl, **spec_kw)
     say(wl.name, spec, "path", path)
@@ -61,6 +62,8 @@ def run_gpu(wl, dev_in, window: int | None = None, timing_sample: int = 0, elide
         if timing_sample:
             r.set("timing_sample", timing_sample)
         r.set("elide_prefetch", 1 if elide else 0)
+        for k, v in (opts or {}).items():
+            r.set(k, v)
         out = r.run(*dev_in)
     finally:
         r.close()

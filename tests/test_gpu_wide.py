@@ -38,6 +38,21 @@ def test_wide_lstm_bf16_ragged():
     assert_close(c, want, TOL_BF16)
 
 
+def test_wide_lstm_bf16_windows():
+    """Weight-gradient windows of 2 steps over 7 (the last one ragged) on the
+    compute stream and on a stream of their own: the same sums in the same
+    order, so the same bits; against the oracle within the bf16 tolerance."""
+    wl = synth.get("lstm_h2048_bf16_t10000").with_(batch=64, input=128, hidden=192, n_steps=7,
+                                                   name="lstm_bf16_wide_windows")
+    host, dev = _case(wl)
+    want = run_oracle(wl, *host)
+    a = run_gpu(wl, dev, fast_slots=3, slow_slots=7, interval_min=2, window=2)
+    assert a["stats"]["window"] == 2 and a["stats"]["kernel_calls"][4] == 4
+    assert_close(a, want, TOL_BF16)
+    b = run_gpu(wl, dev, fast_slots=3, slow_slots=0, window=2, opts={"dw_stream": 1})
+    assert_bitwise(a, b)
+
+
 @pytest.mark.parametrize("loss", ["half_sq_last", "mean_sq_all", "mean_last"])
 def test_wide_rnn_bf16_losses(loss):
     """tanh RNN (G = 1, 64 units per tile), B = 50 on a 64-row tile, every loss."""
