@@ -228,6 +228,12 @@ struct ambptt_ctx {
   bool res_test_stall = false;  // tests of the abort path: the first entry waits for a barrier that never comes
   bool res_coop = false;         // cooperative launch of the resident kernel
   int dw_stream = -1;            // weight-gradient windows: 1 on their own stream, 0 on the compute stream, -1 by path
+  // Executor events order work between the library's streams on one device
+  // and time kernels; none of them publishes device memory to the host, so
+  // by default they carry no system-scope fence (each such fence writes back
+  // and invalidates the caches of every XCD, several microseconds between two
+  // kernels).
+  bool sys_fence = false;
   int32_t* prog_host = nullptr;  // pinned staging of the resident program
   size_t prog_host_cap = 0;
   unsigned* status_host = nullptr;  // pinned copy of the resident kernel's status words
@@ -237,6 +243,30 @@ struct ambptt_ctx {
 namespace {
 
 enum { kNone = 0, kStorePending = 1, kPrefetchPending = 2 };
+
+unsigned event_flags(const ambptt_ctx* C, bool timing) {
+  return (timing ? 0u : unsigned(hipEventDisableTiming)) | (C->sys_fence ? 0u : unsigned(hipEventDisableSystemFence));
+}
+
+// (Re)creates the executor's synchronisation events with the context's fence
+// scope; timing events are recreated on demand.
+hipError_t make_sync_events(ambptt_ctx* C) {
+  auto remake = [&](hipEvent_t& ev) {
+    if (ev) (void)hipEventDestroy(ev);
+    ev = nullptr;
+    return hipEventCreateWithFlags(&ev, event_flags(C, false));
+  };
+  hipError_t e;
+  if ((e = remake(C->ev_c)) != hipSuccess) return e;
+  if ((e = remake(C->ev_c2)) != hipSuccess) return e;
+  for (auto& ev : C->ev_dw)
+    if ((e = remake(ev)) != hipSuccess) return e;
+  for (auto& ev : C->ev_slot)
+    if ((e = remake(ev)) != hipSuccess) return e;
+  for (auto& ev : C->tpool) (void)hipEventDestroy(ev);
+  C->tpool.clear();
+  return hipSuccess;
+}
 
 struct Sample {
   int cls;
@@ -306,7 +336,7 @@ struct Exec {
       const size_t need = 2 * (samples.size() + 1);
       while (C->tpool.size() < need) {
         hipEvent_t e;
-        HIPCK(hipEventCreate(&e));
+        HIPCK(hipEventCreateWithFlags(&e, event_flags(C, true)));
         C->tpool.push_back(e);
       }
       smp.a = C->tpool[need - 2];
@@ -999,15 +1029,10 @@ ambptt_status ambptt_create(const ambptt_problem* p, void* stream, ambptt_ctx** 
   hipError_t e;
   if ((e = hipGetDevice(&C->device)) != hipSuccess) return bail("hipGetDevice", e);
   if ((e = hipStreamCreateWithFlags(&C->xs, hipStreamNonBlocking)) != hipSuccess) return bail("hipStreamCreate", e);
-  if ((e = hipEventCreateWithFlags(&C->ev_c, hipEventDisableTiming)) != hipSuccess) return bail("hipEventCreate", e);
   if ((e = hipStreamCreateWithFlags(&C->ds, hipStreamNonBlocking)) != hipSuccess) return bail("hipStreamCreate", e);
-  if ((e = hipEventCreateWithFlags(&C->ev_c2, hipEventDisableTiming)) != hipSuccess) return bail("hipEventCreate", e);
-  for (auto& ev : C->ev_dw)
-    if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess) return bail("hipEventCreate", e);
   C->ev_slot.resize(size_t(p->fast_slots), nullptr);
   C->pend.assign(size_t(p->fast_slots), kNone);
-  for (auto& ev : C->ev_slot)
-    if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess) return bail("hipEventCreate", e);
+  if ((e = make_sync_events(C)) != hipSuccess) return bail("hipEventCreate", e);
   void* hl = nullptr;
   if ((e = hipHostMalloc(&hl, 64, hipHostMallocDefault)) != hipSuccess) return bail("hipHostMalloc", e);
   C->host_loss = (double*)hl;
@@ -1052,6 +1077,13 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
     C->path_opt = int(v);
   } else if (k == "wide_batch") {
     C->wide_opt = v != 0;
+  } else if (k == "event_system_fence") {
+    if (C->sys_fence != (v != 0)) {
+      C->sys_fence = v != 0;
+      hipError_t e = hipDeviceSynchronize();
+      if (e == hipSuccess) e = make_sync_events(C);
+      if (e != hipSuccess) return fail(AMBPTT_EHIP, std::string("event_system_fence: ") + hipGetErrorString(e));
+    }
   } else if (k == "dw_stream") {
     if (v < -1 || v > 1) return fail(AMBPTT_EINVAL, "dw_stream must be -1 (by path), 0 or 1");
     C->dw_stream = int(v);
@@ -1101,8 +1133,8 @@ ambptt_status ambptt_calibrate(ambptt_ctx* C, const void* x_seq, const void* W, 
   if ((s = prepare_inputs(C, W, h0, c0, E)) != AMBPTT_OK) return s;
   if ((s = ensure_host(C, C->L.stride)) != AMBPTT_OK) return s;
   hipEvent_t e0, e1;
-  HIPCK(hipEventCreate(&e0));
-  HIPCK(hipEventCreate(&e1));
+  HIPCK(hipEventCreateWithFlags(&e0, event_flags(C, true)));
+  HIPCK(hipEventCreateWithFlags(&e1, event_flags(C, true)));
   const int64_t n = C->p.n_steps;
   const int reps = 16;
   float ms = 0.f;
