@@ -252,6 +252,10 @@ def main() -> int:
         r.set(k, v)
     I_min, t_a, t_t = r.calibrate(dx, dW, db, dh, dc)
     print(f"calibrated: I_min {I_min}, T_A {t_a:.2f} us, T_T {t_t:.2f} us", file=sys.stderr, flush=True)
+    for k, v in knobs:  # an interval_min given here replaces the calibrated one
+        if k == "interval_min":
+            r.set(k, v)
+            I_min = v
     r.set("timing_sample", args.timing_sample)
     for _ in range(args.warmup):
         r.run(dx, dW, db, dh, dc, out=outb)

@@ -46,10 +46,10 @@ def test_wide_lstm_bf16_windows():
                                                    name="lstm_bf16_wide_windows")
     host, dev = _case(wl)
     want = run_oracle(wl, *host)
-    a = run_gpu(wl, dev, fast_slots=3, slow_slots=7, interval_min=2, window=2)
-    assert a["stats"]["window"] == 2 and a["stats"]["kernel_calls"][4] == 4
+    a = run_gpu(wl, dev, fast_slots=2, slow_slots=7, interval_min=2, window=2)
+    assert a["stats"]["mode"] == 1 and a["stats"]["window"] == 2 and a["stats"]["kernel_calls"][4] == 4
     assert_close(a, want, TOL_BF16)
-    b = run_gpu(wl, dev, fast_slots=3, slow_slots=0, window=2, opts={"dw_stream": 1})
+    b = run_gpu(wl, dev, fast_slots=2, slow_slots=0, window=2, opts={"dw_stream": 1})
     assert_bitwise(a, b)
 
 
