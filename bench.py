@@ -196,6 +196,38 @@ def fingerprint(out) -> list:
     return fp
 
 
+def gemm_reference(wl, dev, reps: int = 200) -> dict:
+    """The vendor GEMM (torch.matmul, hipBLASLt on ROCm) on the step products
+    of a workload, back to back on the same operands: a reference for the
+    library's fused step kernels, which add the cell or layer epilogue."""
+    import torch
+    e = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    B, D, H = wl.batch, wl.input, wl.hidden
+    G = 4 if wl.cell == "lstm" else 1
+    if wl.cell == "resmlp":
+        shapes = {"layer product y W^T": (B, H, H, True), "adjoint product zbar W": (B, H, H, False)}
+    else:
+        shapes = {"gate product [x|h] W^T": (B, G * H, D + H, True), "h-adjoint product zbar W_h": (B, H, G * H, True)}
+    out = {}
+    for name, (M, N, K, nt) in shapes.items():
+        a = torch.randn(M, K, device=dev).to(e)
+        w = torch.randn(N, K, device=dev).to(e) if nt else torch.randn(K, N, device=dev).to(e)
+        o = torch.empty(M, N, device=dev, dtype=e)
+        f = (lambda: torch.matmul(a, w.t(), out=o)) if nt else (lambda: torch.matmul(a, w, out=o))
+        for _ in range(10):
+            f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1000.0 / reps
+        out[name] = {"shape": [M, N, K], "us": round(us, 2), "tflops": round(2.0 * M * N * K / us / 1e6, 1)}
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -209,6 +241,8 @@ def main() -> int:
     ap.add_argument("--host-slots", type=int, default=-1, help="host-tier slots (default: the workload's)")
     ap.add_argument("--no-compare", dest="compare", action="store_false",
                     help="skip the plain-Revolve and other-path passes")
+    ap.add_argument("--gemm-reference", action="store_true",
+                    help="only time the vendor GEMM on the workload's step products and print them")
     ap.add_argument("--set", action="append", default=[], metavar="KEY=VALUE",
                     help="an ambptt_set_int knob for the measured passes and the plain-Revolve comparison")
     args = ap.parse_args()
@@ -227,6 +261,9 @@ def main() -> int:
     wl = synth.get(args.workload)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.gemm_reference:
+        print(json.dumps({"workload": wl.name, "vendor_gemm": gemm_reference(wl, dev)}), flush=True)
+        return 0
     dx, dW, db, dh, dc = device_inputs(wl, dev)
     torch.cuda.synchronize()
     print(f"inputs of {wl.name} in HBM", file=sys.stderr, flush=True)

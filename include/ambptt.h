@@ -85,8 +85,9 @@ typedef struct {
 /* Counters of one ambptt_run.  recompute_factor = forward_evals / n, where a
  * forward evaluation is one forward step (advances plus the first turn's). */
 typedef struct {
-  int32_t mode;            /* 0 = Revolve, 1 = asynchronous two-level */
-  int32_t interval;        /* I (0 in Revolve mode) */
+  int32_t mode;            /* 0 = Revolve, 1 = asynchronous two-level, 2 = two-level with
+                              stores decided during the sweep ("store_policy" 1) */
+  int32_t interval;        /* I (0 in Revolve mode; in mode 2 the longest interval) */
   int32_t window;          /* steps per dW accumulation window (0: resident kernel) */
   int32_t path;            /* 0 = one launch per step, 1 = resident whole-pass kernel */
   int64_t n_steps;
@@ -146,6 +147,19 @@ int64_t ambptt_schedule_evals(int64_t n, int32_t s, int64_t H, int32_t interval_
 ambptt_status ambptt_schedule_text(int64_t n, int32_t s, int64_t H, int32_t interval_min,
                                    char* buf, size_t cap, size_t* needed);
 
+/* Canonical text of the two-level schedule over interval starts decided
+ * during the forward sweep, the non-uniform policy that the paper's
+ * conclusions (Section 6) propose: the next state is stored whenever the
+ * previous transfer has completed.  starts[0..nstarts) must be 0 = t_0 <
+ * t_1 < ... < t_{K-1} < n with K - 1 <= H, and s >= 2.  Interval k is
+ * [t_k, t_{k+1}) (the last one [t_{K-1}, n)); the sweep stores t_0 .. t_{K-2}
+ * to host slots 0 .. K-2 through fast slots k % 2, and the reverse prefetches
+ * one interval ahead and reverses each interval with Revolve on s - 1 slots,
+ * as in ambptt_schedule_text (header "I=0 mode=dynamic").  Buffer rules as
+ * there; EINVAL on bad starts. */
+ambptt_status ambptt_schedule_text_starts(int64_t n, int32_t s, int64_t H, const int64_t* starts,
+                                          int64_t nstarts, char* buf, size_t cap, size_t* needed);
+
 /* The program the resident whole-pass kernel would run for the schedule of
  * (n, s, H, I_min), 4 int32 per entry {op, y, z, w}:
  *   0 end (dL/dx_0, dW, loss)      1 forward step y, buffer z -> buffer w
@@ -198,8 +212,13 @@ ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
  * the wide-batch bf16 path, whose kernels each fill the device, else 1),
  * "event_system_fence" (0, default: the events that order the library's
  * streams and time its kernels use device-scope fences; 1: system-scope, as
- * HIP's default events do).  EINVAL
- * for unknown keys or values out of range. */
+ * HIP's default events do), "store_policy" (0, default: the sweep stores
+ * every I-th state; 1: it stores the next state once the previous store has
+ * completed, at least ceil(n / (H + 1)) steps apart, the non-uniform policy
+ * of Section 6; where the fixed-interval policy would use the host tier, on
+ * the per-step path only: EUNSUPPORTED with "path" 2; stats mode 2 and
+ * ambptt_last_schedule_text give the schedule that ran).  EINVAL for unknown
+ * keys or values out of range. */
 ambptt_status ambptt_set_int(ambptt_ctx* ctx, const char* key, int64_t value);
 
 /* Measures T_A (one forward step) and T_T (one state over the host link,
@@ -222,6 +241,12 @@ ambptt_status ambptt_calibrate(ambptt_ctx* ctx, const void* x_seq, const void* W
 ambptt_status ambptt_run(ambptt_ctx* ctx, const void* x_seq, const void* W, const float* b,
                          const void* h0, const float* c0, float* dW, float* db,
                          float* dh0, float* dc0, double* loss, ambptt_stats* stats);
+
+/* Canonical text (as ambptt_schedule_text) of the schedule the last
+ * ambptt_run on this context executed; with "store_policy" 1 it holds the
+ * interval starts the sweep chose.  Buffer rules as there; EINVAL before the
+ * first pass.  Host only. */
+ambptt_status ambptt_last_schedule_text(ambptt_ctx* ctx, char* buf, size_t cap, size_t* needed);
 
 /* Frees the host tier, the copy stream and events.  NULL-safe. */
 void ambptt_destroy(ambptt_ctx* ctx);

@@ -48,9 +48,23 @@ Asynchronous two-level policy (Section 2, with the interval of Section 3):
   when not even one store fits, Section 3, generalised), so the policy never
   recomputes more than Revolve at the same fast-slot budget.
 
+Stores when the previous transfer has completed (the non-uniform policy the
+paper's conclusions propose instead of a fixed I): the interval starts
+0 = t_0 < t_1 < ... < t_{K-1} < n are decided during the forward sweep, and
+the same two-level rule applies with interval k = [t_k, t_{k+1}) (the last
+one [t_{K-1}, n)):
+    forward sweep, k = 0 .. K-2:   S (k%2) t_k ; W (k%2) k t_k ; A t_k t_{k+1}
+    reverse, k = K-1 .. 0, a = t_k, l = its length, base = k%2:
+       k = K-1: S base a
+       k >= 1 : P (k-1) ((k-1)%2) t_{k-1}
+       reverse [a, a+l) with s-1 slots
+  Forward evaluations = t_{K-1} + sum_k F(l_k, s-1) + 1.  Fixed intervals are
+  the case t_k = kI.
+
 Canonical text: a header line
-  ambptt-schedule v1 n=<n> s=<s> H=<H> I=<I or 0> mode=<revolve|async>
-then the actions, single spaces, decimal integers, newline-terminated.
+  ambptt-schedule v1 n=<n> s=<s> H=<H> I=<I or 0> mode=<revolve|async|dynamic>
+(I = 0 for revolve and dynamic) then the actions, single spaces, decimal
+integers, newline-terminated.
 """
 from __future__ import annotations
 
@@ -154,6 +168,24 @@ class _Gen:
             l = m
 
 
+def _two_level(g: _Gen, n: int, s: int, starts: list[int]) -> None:
+    """The sweep and the reverse of the two-level policy over the given interval starts."""
+    K = len(starts)
+    ends = starts[1:] + [n]
+    g.live = 0
+    for k in range(K - 1):
+        g.emit("S", k % 2, starts[k])
+        g.emit("W", k % 2, k, starts[k])
+        g.advance(starts[k], starts[k + 1])
+    for k in range(K - 1, -1, -1):
+        a, l, base = starts[k], ends[k] - starts[k], k % 2
+        if k == K - 1:
+            g.emit("S", base, a)
+        if k >= 1:
+            g.emit("P", k - 1, (k - 1) % 2, starts[k - 1])
+        g.reverse(a, l, s - 1, base, list(range(2, s)))
+
+
 def schedule(n: int, s: int, H: int = 0, I_min: int = 0) -> tuple[dict, list[tuple]]:
     """(header dict, action list) for n steps, s fast slots, H slow slots."""
     if n < 1 or s < 1 or H < 0 or I_min < 0:
@@ -165,30 +197,57 @@ def schedule(n: int, s: int, H: int = 0, I_min: int = 0) -> tuple[dict, list[tup
         g.live = 0
         g.reverse(0, n, s, 0, list(range(1, s)))
     else:
-        K = -(-n // I)
-        g.live = 0
-        for k in range(K - 1):
-            g.emit("S", k % 2, k * I)
-            g.emit("W", k % 2, k, k * I)
-            g.advance(k * I, (k + 1) * I)
-        for k in range(K - 1, -1, -1):
-            a = k * I
-            l = n - a if k == K - 1 else I
-            base = k % 2
-            if k == K - 1:
-                g.emit("S", base, a)
-            if k >= 1:
-                g.emit("P", k - 1, (k - 1) % 2, (k - 1) * I)
-            g.reverse(a, l, s - 1, base, list(range(2, s)))
+        _two_level(g, n, s, list(range(0, n, I)))
     head = {"n": n, "s": s, "H": H, "I": I, "mode": mode, "evals": ev}
     return head, g.out
 
 
-def text(n: int, s: int, H: int = 0, I_min: int = 0) -> str:
-    head, acts = schedule(n, s, H, I_min)
-    lines = [f"ambptt-schedule v1 n={n} s={s} H={H} I={head['I']} mode={head['mode']}"]
+def dynamic_evals(n: int, s: int, starts: list[int]) -> int:
+    ends = list(starts[1:]) + [n]
+    return starts[-1] + sum(advances(e - a, s - 1) for a, e in zip(starts, ends)) + 1
+
+
+def schedule_from_starts(n: int, s: int, H: int, starts: list[int]) -> tuple[dict, list[tuple]]:
+    """(header dict, action list) of the two-level policy with interval starts
+    decided during the sweep (stores whenever the previous one completed)."""
+    starts = list(starts)
+    if n < 1 or s < 2 or not starts or starts[0] != 0 or any(b <= a for a, b in zip(starts, starts[1:])) \
+            or starts[-1] >= n or len(starts) - 1 > H:
+        raise ValueError("need s >= 2 and starts 0 = t_0 < t_1 < ... < n with at most H + 1 of them")
+    g = _Gen(n)
+    _two_level(g, n, s, starts)
+    head = {"n": n, "s": s, "H": H, "I": 0, "mode": "dynamic", "evals": dynamic_evals(n, s, starts)}
+    return head, g.out
+
+
+def _render(head: dict, acts: list[tuple]) -> str:
+    lines = [f"ambptt-schedule v1 n={head['n']} s={head['s']} H={head['H']} I={head['I']} mode={head['mode']}"]
     lines += [" ".join(str(v) for v in a) for a in acts]
     return "\n".join(lines) + "\n"
+
+
+def text(n: int, s: int, H: int = 0, I_min: int = 0) -> str:
+    return _render(*schedule(n, s, H, I_min))
+
+
+def text_from_starts(n: int, s: int, H: int, starts: list[int]) -> str:
+    return _render(*schedule_from_starts(n, s, H, starts))
+
+
+def parse(txt: str) -> tuple[dict, list[tuple]]:
+    """Canonical text -> (header dict, action list)."""
+    lines = txt.strip("\n").split("\n")
+    f = lines[0].split()
+    assert f[:2] == ["ambptt-schedule", "v1"], lines[0]
+    head = {}
+    for kv in f[2:]:
+        k, v = kv.split("=")
+        head[k] = v if k == "mode" else int(v)
+    acts = []
+    for ln in lines[1:]:
+        p = ln.split()
+        acts.append((p[0],) + tuple(int(v) for v in p[1:]))
+    return head, acts
 
 
 # ---------------------------------------------------------------------------

@@ -13,8 +13,9 @@ DTYPE = {"f32": 0, "bf16": 1}
 LOSS = {"half_sq_last": 0, "mean_sq_all": 1, "mean_last": 2}
 
 EXPORTS = ["ambptt_version", "ambptt_revolve_advances", "ambptt_schedule_evals", "ambptt_schedule_text",
-           "ambptt_resident_program", "ambptt_query", "ambptt_last_error", "ambptt_create", "ambptt_bind", "ambptt_set_int",
-           "ambptt_calibrate", "ambptt_run", "ambptt_destroy"]
+           "ambptt_schedule_text_starts", "ambptt_resident_program", "ambptt_query", "ambptt_last_error",
+           "ambptt_create", "ambptt_bind", "ambptt_set_int", "ambptt_calibrate", "ambptt_run",
+           "ambptt_last_schedule_text", "ambptt_destroy"]
 
 
 class Problem(C.Structure):
@@ -72,6 +73,10 @@ def load():
     L.ambptt_schedule_evals.restype = i64
     L.ambptt_schedule_text.argtypes = [i64, i32, i64, i32, C.c_char_p, sz, C.POINTER(sz)]
     L.ambptt_schedule_text.restype = C.c_int
+    L.ambptt_schedule_text_starts.argtypes = [i64, i32, i64, C.POINTER(i64), i64, C.c_char_p, sz, C.POINTER(sz)]
+    L.ambptt_schedule_text_starts.restype = C.c_int
+    L.ambptt_last_schedule_text.argtypes = [vp, C.c_char_p, sz, C.POINTER(sz)]
+    L.ambptt_last_schedule_text.restype = C.c_int
     L.ambptt_resident_program.argtypes = [i64, i32, i64, i32, i32, C.POINTER(i32), sz, C.POINTER(sz)]
     L.ambptt_resident_program.restype = C.c_int
     L.ambptt_query.argtypes = [C.POINTER(Problem), C.POINTER(sz), C.POINTER(sz), C.POINTER(sz)]

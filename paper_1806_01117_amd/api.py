@@ -44,6 +44,25 @@ def schedule_text(n: int, s: int, H: int = 0, interval_min: int = 0) -> str:
     return buf.value.decode()
 
 
+def _text(call) -> str:
+    """A canonical-text call: size query, then the text."""
+    need = C.c_size_t(0)
+    call(None, 0, C.byref(need))
+    if need.value == 0:
+        check(call(None, 0, C.byref(need)))
+    buf = C.create_string_buffer(need.value)
+    check(call(buf, need.value, C.byref(need)))
+    return buf.value.decode()
+
+
+def schedule_text_starts(n: int, s: int, H: int, starts) -> str:
+    """Canonical text of the two-level schedule over interval starts chosen
+    during the sweep (ambptt_schedule_text_starts)."""
+    L = load()
+    arr = (C.c_int64 * len(starts))(*[int(t) for t in starts])
+    return _text(lambda buf, cap, need: L.ambptt_schedule_text_starts(n, s, H, arr, len(starts), buf, cap, need))
+
+
 def resident_program(n: int, s: int, H: int = 0, interval_min: int = 0, elide_prefetch: bool = True):
     """The resident whole-pass kernel's program for a schedule, as a list of
     (op, y, z, w) tuples (see ambptt_resident_program in include/ambptt.h)."""
@@ -172,6 +191,10 @@ class Runner:
         res["loss"] = float(loss.value)
         res["stats"] = st.as_dict()
         return res
+
+    def last_schedule_text(self) -> str:
+        """The canonical text of the schedule the last run executed."""
+        return _text(lambda buf, cap, need: self.L.ambptt_last_schedule_text(self.ctx, buf, cap, need))
 
     def close(self) -> None:
         if getattr(self, "ctx", None) is not None and self.ctx.value:

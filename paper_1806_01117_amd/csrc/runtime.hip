@@ -234,6 +234,9 @@ struct ambptt_ctx {
   // and invalidates the caches of every XCD, several microseconds between two
   // kernels).
   bool sys_fence = false;
+  int store_policy = 0;  // 0: every I-th state; 1: the next state once the previous store has completed
+  hipEvent_t ev_sweep[3] = {nullptr, nullptr, nullptr};  // host pacing of the sweep with store_policy 1
+  Plan last_plan;        // the schedule the last ambptt_run executed
   int32_t* prog_host = nullptr;  // pinned staging of the resident program
   size_t prog_host_cap = 0;
   unsigned* status_host = nullptr;  // pinned copy of the resident kernel's status words
@@ -262,6 +265,8 @@ hipError_t make_sync_events(ambptt_ctx* C) {
   for (auto& ev : C->ev_dw)
     if ((e = remake(ev)) != hipSuccess) return e;
   for (auto& ev : C->ev_slot)
+    if ((e = remake(ev)) != hipSuccess) return e;
+  for (auto& ev : C->ev_sweep)
     if ((e = remake(ev)) != hipSuccess) return e;
   for (auto& ev : C->tpool) (void)hipEventDestroy(ev);
   C->tpool.clear();
@@ -577,10 +582,56 @@ struct Exec {
     cur_live = -1;
   }
 
-  ambptt_status run(const Plan& plan, float* dW, float* db) {
-    const auto& acts = plan.acts;
+  ambptt_status run(const Plan& plan, float* dW, float* db) { return run_acts(plan.acts, 0, dW, db); }
+
+  // The two-level policy with the interval starts decided during the sweep
+  // (the non-uniform policy of Section 6): the output of forward step t
+  // becomes the next interval start when the store of the previous start has
+  // completed by the time step t is issued, and at least `spacing` steps have
+  // passed since that start (ceil(n / (H + 1)), so that H host slots span the
+  // sequence).  The host stays at most kAhead steps ahead of the device, so
+  // that "completed" reflects the device's progress.  A start after which at
+  // most as many steps remain as have passed since the previous start is the
+  // last one (kept in HBM only), so the sweep ends within one interval of n;
+  // so is the start that takes the last host slot's successor.  Needs n >= 2,
+  // s >= 2, H >= 1.  Returns the starts; the reverse is built from them.
+  ambptt_status dynamic_sweep(std::vector<int64_t>& starts, float* dW, float* db) {
+    constexpr int kAhead = 3;
+    const int64_t n = p.n_steps, H = p.slow_slots;
+    const int64_t spacing = std::max<int64_t>(1, (n + H) / (H + 1));
     ambptt_status s;
-    for (size_t i = 0; i < acts.size(); ++i) {
+    starts.assign(1, 0);
+    const std::vector<Action> head = {{Op::Snap, 0, 0, 0}, {Op::Store, 0, 0, 0}};
+    if ((s = run_acts(head, 0, dW, db)) != AMBPTT_OK) return s;
+    for (int64_t t = 0;; ++t) {
+      const int64_t k = int64_t(starts.size()) - 1, tk = starts.back(), t1 = t + 1;
+      if (t >= kAhead) HIPCK(hipEventSynchronize(C->ev_sweep[t % kAhead]));
+      const hipError_t q = hipEventQuery(C->ev_slot[size_t(k % 2)]);
+      if (q != hipSuccess && q != hipErrorNotReady) HIPCK(q);
+      const bool near_end = n - t1 <= t1 - tk;  // t1 <= n - 1 holds: n - t1 >= 1 until then
+      const bool start = near_end || (q == hipSuccess && t1 - tk >= spacing);
+      const bool last = start && (near_end || k + 1 >= H);
+      if (start) {  // x_{t1} is start k + 1: step t writes it into its fast slot
+        const int64_t ks = (k + 1) % 2;
+        if ((s = wait_slot(ks, true)) != AMBPTT_OK) return s;
+        if ((s = fwd_step(t, cur, slot(ks))) != AMBPTT_OK) return s;
+        set_cur_slot(ks);
+        starts.push_back(t1);
+        if (last) return AMBPTT_OK;  // the reverse begins by snapshotting it (already there)
+        const std::vector<Action> sw = {{Op::Snap, ks, t1, 0}, {Op::Store, ks, k + 1, t1}};
+        if ((s = run_acts(sw, 0, dW, db)) != AMBPTT_OK) return s;
+      } else {
+        char* dst = other_live();
+        if ((s = fwd_step(t, cur, dst)) != AMBPTT_OK) return s;
+        set_cur_live(dst);
+      }
+      HIPCK(hipEventRecord(C->ev_sweep[t % kAhead], C->cs));
+    }
+  }
+
+  ambptt_status run_acts(const std::vector<Action>& acts, size_t from, float* dW, float* db) {
+    ambptt_status s;
+    for (size_t i = from; i < acts.size(); ++i) {
       const Action& A = acts[i];
       switch (A.op) {
         case Op::Advance: {
@@ -708,7 +759,8 @@ ambptt_status prepare_inputs(ambptt_ctx* C, const void* W, const void* h0, const
 // ---- resident whole-pass kernel ----------------------------------------------
 
 bool resident_possible(ambptt_ctx* C) {
-  if (!C->L.res || C->path_opt == 1) return false;
+  // the resident program is compiled before the launch: it takes no decision at run time
+  if (!C->L.res || C->path_opt == 1 || C->store_policy == 1) return false;
   if (C->res_cap < 0) {
     int cap = 0;
     if (resident_capacity(C->L.G, &cap) != hipSuccess) {
@@ -941,6 +993,7 @@ ambptt_status resident_run(ambptt_ctx* C, const void* x_seq, const void* W, cons
   }
   if (rc.forward_evals != plan.evals)
     return fail(AMBPTT_EINTERNAL, "resident forward count differs from the schedule");
+  C->last_plan = std::move(plan);
   return AMBPTT_OK;
 }
 
@@ -1084,6 +1137,10 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
       if (e == hipSuccess) e = make_sync_events(C);
       if (e != hipSuccess) return fail(AMBPTT_EHIP, std::string("event_system_fence: ") + hipGetErrorString(e));
     }
+  } else if (k == "store_policy") {
+    if (v < 0 || v > 1) return fail(AMBPTT_EINVAL, "store_policy must be 0 (every I-th state) or 1 (when the previous store completed)");
+    if (v == 1 && C->path_opt == 2) return fail(AMBPTT_EUNSUPPORTED, "store_policy 1 runs on the per-step path only");
+    C->store_policy = int(v);
   } else if (k == "dw_stream") {
     if (v < -1 || v > 1) return fail(AMBPTT_EINVAL, "dw_stream must be -1 (by path), 0 or 1");
     C->dw_stream = int(v);
@@ -1187,6 +1244,8 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   if (p.slow_slots > 0 && C->interval_min == 0) {
     if ((s = ambptt_calibrate(C, x_seq, W, b, h0, c0, nullptr, nullptr, nullptr)) != AMBPTT_OK) return s;
   }
+  if (C->path_opt == 2 && C->store_policy == 1)
+    return fail(AMBPTT_EUNSUPPORTED, "store_policy 1 runs on the per-step path only");
   if (C->path_opt == 2 && !resident_possible(C))
     return fail(AMBPTT_EUNSUPPORTED, "the resident kernel does not fit this problem on this device");
   if (resident_possible(C)) return resident_run(C, x_seq, W, b, h0, c0, dW, db, dh0, dc0, loss, stats);
@@ -1198,8 +1257,12 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
     return fail(AMBPTT_EINTERNAL, e.what());
   }
   const double t1 = now_us();
+  // stores decided during the sweep, where the fixed-interval policy would
+  // use the host tier at all
+  const bool dynamic = C->store_policy == 1 && plan.async && p.n_steps >= 2;
   if (plan.async) {
-    if ((s = ensure_host(C, (size_t)plan.host_slots_used * L.stride)) != AMBPTT_OK) return s;
+    const size_t slots = dynamic ? size_t(std::min<int64_t>(p.slow_slots, p.n_steps)) : size_t(plan.host_slots_used);
+    if ((s = ensure_host(C, slots * L.stride)) != AMBPTT_OK) return s;
   }
   Exec E(C, x_seq, W, b);
   std::fill(C->pend.begin(), C->pend.end(), kNone);
@@ -1210,7 +1273,21 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   }
   HIPCK(launch_fill32(C->ws + L.off_loss, (size_t)L.loss_slots * 2, 0u, C->cs));
   if ((s = prepare_inputs(C, W, h0, c0, E)) != AMBPTT_OK) return s;
-  if ((s = E.run(plan, dW, db)) != AMBPTT_OK) return s;
+  if (dynamic) {
+    std::vector<int64_t> starts;
+    if ((s = E.dynamic_sweep(starts, dW, db)) != AMBPTT_OK) return s;
+    try {
+      plan = make_plan_starts(p.n_steps, p.fast_slots, p.slow_slots, starts);
+    } catch (const std::exception& e) {
+      return fail(AMBPTT_EINTERNAL, e.what());
+    }
+    for (size_t k = 1; k <= starts.size(); ++k)  // the longest interval
+      plan.interval = std::max(plan.interval, (k < starts.size() ? starts[k] : p.n_steps) - starts[k - 1]);
+    // the sweep ran the plan's first 3 (K - 1) actions: snapshot, store and advance per stored start
+    if ((s = E.run_acts(plan.acts, 3 * (starts.size() - 1), dW, db)) != AMBPTT_OK) return s;
+  } else if ((s = E.run(plan, dW, db)) != AMBPTT_OK) {
+    return s;
+  }
   if ((s = E.final_step(dh0, dc0)) != AMBPTT_OK) return s;
   const double t_enq = now_us();
   double scale = 1.0;
@@ -1234,7 +1311,7 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
     cnt[smp.cls]++;
   }
   if (stats) {
-    st.mode = plan.async ? 1 : 0;
+    st.mode = plan.dynamic ? 2 : plan.async ? 1 : 0;
     st.interval = int32_t(plan.interval);
     st.window = L.window;
     st.n_steps = p.n_steps;
@@ -1253,7 +1330,34 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   if (st.forward_evals != plan.evals)
     return fail(AMBPTT_EINTERNAL, "executor forward count " + std::to_string(st.forward_evals) +
                                       " != schedule count " + std::to_string(plan.evals));
+  C->last_plan = std::move(plan);
   return AMBPTT_OK;
+}
+
+ambptt_status ambptt_last_schedule_text(ambptt_ctx* C, char* buf, size_t cap, size_t* needed) {
+  if (!C) return fail(AMBPTT_EINVAL, "ctx is NULL");
+  if (C->last_plan.n == 0) return fail(AMBPTT_EINVAL, "no pass has run on this context");
+  const std::string t = plan_text(C->last_plan);
+  if (needed) *needed = t.size() + 1;
+  if (!buf || cap < t.size() + 1) return fail(AMBPTT_EINVAL, "schedule: buffer too small");
+  std::memcpy(buf, t.c_str(), t.size() + 1);
+  return AMBPTT_OK;
+}
+
+ambptt_status ambptt_schedule_text_starts(int64_t n, int32_t s, int64_t H, const int64_t* starts, int64_t nstarts,
+                                          char* buf, size_t cap, size_t* needed) {
+  if (!starts || nstarts < 1) return fail(AMBPTT_EINVAL, "schedule: no interval starts");
+  try {
+    const std::string t = plan_text(make_plan_starts(n, s, H, std::vector<int64_t>(starts, starts + nstarts)));
+    if (needed) *needed = t.size() + 1;
+    if (!buf || cap < t.size() + 1) return fail(AMBPTT_EINVAL, "schedule: buffer too small");
+    std::memcpy(buf, t.c_str(), t.size() + 1);
+    return AMBPTT_OK;
+  } catch (const std::invalid_argument& e) {
+    return fail(AMBPTT_EINVAL, e.what());
+  } catch (const std::exception& e) {
+    return fail(AMBPTT_EINTERNAL, e.what());
+  }
 }
 
 void ambptt_destroy(ambptt_ctx* C) {
@@ -1267,6 +1371,8 @@ void ambptt_destroy(ambptt_ctx* C) {
   for (auto& ev : C->ev_dw)
     if (ev) (void)hipEventDestroy(ev);
   if (C->ev_c2) (void)hipEventDestroy(C->ev_c2);
+  for (auto& ev : C->ev_sweep)
+    if (ev) (void)hipEventDestroy(ev);
   if (C->ds) (void)hipStreamDestroy(C->ds);
   if (C->xs) (void)hipStreamDestroy(C->xs);
   if (C->host) (void)hipHostFree(C->host);

@@ -138,6 +138,30 @@ struct Builder {
   }
 };
 
+// The two-level policy over interval starts t_0 = 0 < t_1 < ... < t_{K-1}
+// (Section 2): the sweep snapshots each start but the last into fast slot
+// k % 2 and stores it to host slot k; the reverse takes the intervals from the
+// last, prefetching the previous start one interval ahead, and reverses each
+// with Revolve on s - 1 slots (fast slots 0 and 1 hold the starts; Revolve
+// works in 2 .. s-1).
+void two_level(Builder& b, int32_t s, const std::vector<int64_t>& starts) {
+  const int64_t K = int64_t(starts.size());
+  b.busy[0] = b.busy[1] = 1;
+  for (int64_t k = 0; k + 1 < K; ++k) {
+    b.push(Op::Snap, k % 2, starts[size_t(k)]);
+    b.push(Op::Store, k % 2, k, starts[size_t(k)]);
+    b.advance(starts[size_t(k)], starts[size_t(k + 1)]);
+  }
+  for (int64_t k = K - 1; k >= 0; --k) {
+    const int64_t a = starts[size_t(k)];
+    const int64_t l = (k == K - 1 ? b.n : starts[size_t(k + 1)]) - a;
+    const int64_t base = k % 2;
+    if (k == K - 1) b.push(Op::Snap, base, a);
+    if (k >= 1) b.push(Op::Prefetch, k - 1, (k - 1) % 2, starts[size_t(k - 1)]);
+    b.reverse(a, l, s - 1, base);
+  }
+}
+
 }  // namespace
 
 Plan make_plan(int64_t n, int32_t s, int64_t H, int64_t interval_min) {
@@ -153,23 +177,33 @@ Plan make_plan(int64_t n, int32_t s, int64_t H, int64_t interval_min) {
     b.reverse(0, n, s, 0);
     return p;
   }
-  const int64_t I = p.interval;
-  const int64_t K = (n + I - 1) / I;
-  p.host_slots_used = K - 1;
-  b.busy[0] = b.busy[1] = 1;  // interval bases; Revolve works in slots 2 .. s-1
-  for (int64_t k = 0; k + 1 < K; ++k) {
-    b.push(Op::Snap, k % 2, k * I);
-    b.push(Op::Store, k % 2, k, k * I);
-    b.advance(k * I, (k + 1) * I);
+  std::vector<int64_t> starts;
+  for (int64_t t = 0; t < n; t += p.interval) starts.push_back(t);
+  two_level(b, s, starts);
+  p.host_slots_used = int64_t(starts.size()) - 1;
+  return p;
+}
+
+Plan make_plan_starts(int64_t n, int32_t s, int64_t H, const std::vector<int64_t>& starts) {
+  if (n < 1 || s < 2 || H < 0 || starts.empty() || starts[0] != 0 || starts.back() >= n ||
+      int64_t(starts.size()) - 1 > H)
+    throw std::invalid_argument("schedule: need s >= 2 and starts 0 = t_0 < ... < t_{K-1} < n, K - 1 <= H");
+  for (size_t k = 1; k < starts.size(); ++k)
+    if (starts[k] <= starts[k - 1]) throw std::invalid_argument("schedule: interval starts must increase");
+  Plan p;
+  p.n = n;
+  p.s = s;
+  p.H = H;
+  p.async = true;
+  p.dynamic = true;
+  p.evals = starts.back() + 1;
+  for (size_t k = 0; k < starts.size(); ++k) {
+    const int64_t end = k + 1 < starts.size() ? starts[k + 1] : n;
+    p.evals += revolve_advances(end - starts[k], s - 1);
   }
-  for (int64_t k = K - 1; k >= 0; --k) {
-    const int64_t a = k * I;
-    const int64_t l = (k == K - 1) ? n - a : I;
-    const int64_t base = k % 2;
-    if (k == K - 1) b.push(Op::Snap, base, a);
-    if (k >= 1) b.push(Op::Prefetch, k - 1, (k - 1) % 2, (k - 1) * I);
-    b.reverse(a, l, s - 1, base);
-  }
+  Builder b{n, &p.acts, 0, std::vector<char>(size_t(s), 0)};
+  two_level(b, s, starts);
+  p.host_slots_used = int64_t(starts.size()) - 1;
   return p;
 }
 
@@ -177,8 +211,8 @@ std::string plan_text(const Plan& p) {
   std::string t;
   t.reserve(p.acts.size() * 12 + 96);
   t += "ambptt-schedule v1 n=" + std::to_string(p.n) + " s=" + std::to_string(p.s) +
-       " H=" + std::to_string(p.H) + " I=" + std::to_string(p.interval) +
-       " mode=" + (p.async ? "async" : "revolve") + "\n";
+       " H=" + std::to_string(p.H) + " I=" + std::to_string(p.dynamic ? 0 : p.interval) +
+       " mode=" + (p.dynamic ? "dynamic" : p.async ? "async" : "revolve") + "\n";
   char line[96];
   for (const Action& x : p.acts) {
     int len = 0;

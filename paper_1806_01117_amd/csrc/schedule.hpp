@@ -26,6 +26,7 @@ struct Plan {
   int64_t H = 0;
   int64_t interval = 0;  // 0 in Revolve mode
   bool async = false;
+  bool dynamic = false;  // interval starts decided during the sweep
   int64_t evals = 0;     // forward-step evaluations
   int64_t host_slots_used = 0;
   std::vector<Action> acts;
@@ -42,6 +43,10 @@ int64_t revolve_split(int64_t l, int64_t s);
 // Chooses the mode and interval and builds the action list.  Throws
 // std::invalid_argument on bad arguments.
 Plan make_plan(int64_t n, int32_t s, int64_t H, int64_t interval_min);
+// The two-level plan over interval starts decided during the sweep (the
+// starts increase from 0, stay below n and number at most H + 1; s >= 2).
+// Throws std::invalid_argument otherwise.
+Plan make_plan_starts(int64_t n, int32_t s, int64_t H, const std::vector<int64_t>& starts);
 // Mode, interval and forward evaluations only (no action list).
 void plan_counts(int64_t n, int32_t s, int64_t H, int64_t interval_min, bool* async,
                  int64_t* interval, int64_t* evals);

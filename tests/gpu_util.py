@@ -65,9 +65,11 @@ def run_gpu(wl, dev_in, window: int | None = None, timing_sample: int = 0, elide
         for k, v in (opts or {}).items():
             r.set(k, v)
         out = r.run(*dev_in)
+        text = r.last_schedule_text()
     finally:
         r.close()
     res = {k: (v.float().cpu().numpy() if hasattr(v, "cpu") else v) for k, v in out.items() if v is not None}
+    res["schedule_text"] = text
     if path is not None:
         assert res["stats"]["path"] == path - 1, "the requested path did not run"
     return res

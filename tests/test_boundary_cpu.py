@@ -113,3 +113,22 @@ def test_stats_struct_layout(amb):
     # int32 x4, int64 x14, double x4, double x6, int64 x12
     assert ctypes.sizeof(_lib.Stats) == 16 + 14 * 8 + 4 * 8 + 6 * 8 + 12 * 8
     assert ctypes.sizeof(_lib.Problem) == 48
+
+
+def test_schedule_text_over_starts_matches_oracle_bytewise(amb):
+    import random
+    rng = random.Random(3)
+    for _ in range(400):
+        n = rng.randint(2, 200)
+        s = rng.randint(2, 9)
+        H = rng.randint(1, 300)
+        k = rng.randint(0, min(H, n - 1))
+        starts = [0] + sorted(rng.sample(range(1, n), k))
+        assert amb.schedule_text_starts(n, s, H, starts) == S.text_from_starts(n, s, H, starts), (n, s, H, starts)
+
+
+def test_schedule_text_over_starts_rejects_bad_starts(amb):
+    for n, s, H, starts in [(10, 3, 5, [1, 4]), (10, 3, 5, [0, 4, 4]), (10, 3, 5, [0, 10]), (10, 3, 1, [0, 3, 6]),
+                            (10, 1, 5, [0, 5]), (10, 3, 5, [])]:
+        with pytest.raises(amb.AmbpttError):
+            amb.schedule_text_starts(n, s, H, starts)

@@ -168,6 +168,25 @@ def test_replay_equals_store_all_bitwise(case):
     assert all(np.array_equal(a, b) for a, b in zip(got["dx0"], ref["dx0"]))
 
 
+@pytest.mark.parametrize("kind,starts", [("lstm", [0, 1, 4, 5, 9, 13]), ("rnn", [0, 6]), ("resmlp", [0, 2, 3, 10])])
+def test_replay_over_chosen_starts_equals_store_all_bitwise(kind, starts):
+    """Intervals of unequal length, as stores decided during the sweep make them."""
+    n, s = 15, 3
+    cell, _ = _tiny(kind, "mean_sq_all", B=3, D=2, H=5, seed=5)
+    rng = np.random.default_rng(8)
+    us = rng.standard_normal((n, 3, 2 if kind != "resmlp" else 0))
+    x0 = tuple(rng.standard_normal((3, 5)) * 0.3 for _ in range(2 if kind == "lstm" else 1))
+    ref = bptt.store_all(cell, n, lambda t: us[t], x0)
+    head, acts = S.schedule_from_starts(n, s, 10, starts)
+    got = S.replay(cell, n, lambda t: us[t], x0, acts)
+    assert got["loss"] == ref["loss"]
+    if kind == "resmlp":
+        assert all(np.array_equal(got["dW"][l], ref["dW"][l]) for l in range(n))
+    else:
+        assert np.array_equal(got["dW"], ref["dW"]) and np.array_equal(got["db"], ref["db"])
+    assert all(np.array_equal(a, b) for a, b in zip(got["dx0"], ref["dx0"]))
+
+
 def test_replay_detects_a_wrong_restore():
     # restoring from the wrong slot must change the result (and fail the checker)
     cell, _ = _tiny("lstm", "mean_sq_all", B=2, D=2, H=3, seed=4)

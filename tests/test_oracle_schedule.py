@@ -175,3 +175,53 @@ def test_workload_schedule_counts():
     for n, s in ((128, 4), (1000, 10), (2000, 16), (1777, 7)):
         assert S.advances(n, s) == F[s, n]
     assert S.revolve_evals(128, 4) == 517
+
+
+def _random_starts(rng, n, H):
+    """Interval starts 0 = t_0 < ... < t_{K-1} < n with K - 1 <= H."""
+    k = rng.randint(0, min(H, n - 1))
+    return [0] + sorted(rng.sample(range(1, n), k))
+
+
+def test_schedules_over_chosen_starts_are_valid_and_counted():
+    """Stores decided during the sweep (Section 6): every interval layout gives
+    a valid schedule whose symbolic forward count is the closed form
+    t_{K-1} + sum_k F(l_k, s-1) + 1, with one store and one prefetch per start
+    but the last."""
+    rng = random.Random(7)
+    for _ in range(1500):
+        n = rng.randint(2, 60)
+        s = rng.randint(2, 7)
+        H = rng.randint(1, 70)
+        st = _random_starts(rng, n, H)
+        head, acts = S.schedule_from_starts(n, s, H, st)
+        c = S.check(n, s, H, acts)
+        assert c["evals"] == head["evals"] == S.dynamic_evals(n, s, st), (n, s, H, st)
+        assert c["stores"] == c["prefetches"] == len(st) - 1
+        assert c["adjoints"] == n
+
+
+def test_uniform_starts_reproduce_the_fixed_interval_schedule():
+    """Starts kI reproduce the fixed-interval two-level schedule action for action."""
+    for n in (5, 9, 12, 31, 100):
+        for s in (2, 3, 5):
+            for I in (1, 2, 3, 7):
+                head, acts = S.schedule(n, s, n, I)
+                if head["mode"] != "async":
+                    continue
+                h2, acts2 = S.schedule_from_starts(n, s, n, list(range(0, n, I)))
+                assert acts2 == acts and h2["evals"] == head["evals"], (n, s, I)
+
+
+def test_chosen_starts_edge_cases():
+    # one interval: no store, Revolve on s - 1 slots from x_0
+    head, acts = S.schedule_from_starts(7, 3, 4, [0])
+    assert head["evals"] == S.advances(7, 2) + 1 and not any(a[0] in "WP" for a in acts)
+    # every state an interval start: no recomputation (R = 1)
+    head, acts = S.schedule_from_starts(6, 2, 5, list(range(6)))
+    assert head["evals"] == 6
+    for bad in ([1, 3], [0, 3, 3], [0, 7], [0, 1, 2, 3]):
+        with pytest.raises(ValueError):
+            S.schedule_from_starts(7, 3, 2, bad)
+    with pytest.raises(ValueError):
+        S.schedule_from_starts(7, 1, 2, [0, 3])
