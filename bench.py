@@ -241,6 +241,9 @@ def main() -> int:
     ap.add_argument("--host-slots", type=int, default=-1, help="host-tier slots (default: the workload's)")
     ap.add_argument("--no-compare", dest="compare", action="store_false",
                     help="skip the plain-Revolve and other-path passes")
+    ap.add_argument("--file-tier", default="", metavar="DIR",
+                    help="a file in DIR below the pinned host tier, as many slots as steps; --host-slots then sizes "
+                         "the pinned ring in front of it")
     ap.add_argument("--gemm-reference", action="store_true",
                     help="only time the vendor GEMM on the workload's step products and print them")
     ap.add_argument("--set", action="append", default=[], metavar="KEY=VALUE",
@@ -287,6 +290,8 @@ def main() -> int:
     r.set("resident_cooperative", args.cooperative)
     for k, v in knobs:
         r.set(k, v)
+    if args.file_tier:
+        r.set_file_tier(args.file_tier, wl.n_steps)
     I_min, t_a, t_t = r.calibrate(dx, dW, db, dh, dc)
     print(f"calibrated: I_min {I_min}, T_A {t_a:.2f} us, T_T {t_t:.2f} us", file=sys.stderr, flush=True)
     for k, v in knobs:  # an interval_min given here replaces the calibrated one
@@ -418,7 +423,10 @@ def main() -> int:
                    "hidden": wl.hidden, "n_steps": wl.n_steps, "fast_slots": wl.fast_slots,
                    "slow_slots": spec.slow_slots, "mode": "async" if st["mode"] else "revolve",
                    "interval": st["interval"], "interval_min": I_min, "t_a_us": round(t_a, 3),
-                   "t_t_us": round(t_t, 3), "window": st["window"], **({"knobs": dict(knobs)} if knobs else {})},
+                   "t_t_us": round(t_t, 3), "window": st["window"], **({"knobs": dict(knobs)} if knobs else {}),
+                   **({"file_tier": {"file_slots": wl.n_steps, "pinned_ring": host_slots,
+                                     "bytes_written": st["bytes_file_w"], "bytes_read": st["bytes_file_r"]}}
+                      if args.file_tier else {})},
         "recompute_factor": round(st["recompute_factor"], 4),
         "plain_revolve": None if rv_st is None else {
             "value": round(rv_value, 2), "unit": "timesteps/s",

@@ -108,6 +108,7 @@ typedef struct {
   double kernel_us[6];
   int64_t kernel_samples[6];
   int64_t kernel_calls[6];
+  int64_t bytes_file_w, bytes_file_r;  /* file tier traffic (ambptt_set_file_tier) */
 } ambptt_stats;
 
 /* Kernel classes of ambptt_stats.kernel_*: forward step, the resident
@@ -220,6 +221,20 @@ ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
  * ambptt_last_schedule_text give the schedule that ran).  EINVAL for unknown
  * keys or values out of range. */
 ambptt_status ambptt_set_int(ambptt_ctx* ctx, const char* key, int64_t value);
+
+/* Puts a file below the pinned host tier: a third storage level for states
+ * that do not fit in pinned host memory (the paper's platforms store to DRAM
+ * or SSD, Section 5).  The schedule then has file_slots slow slots; the
+ * problem's slow_slots pinned buffers (>= 1) become a ring in front of the
+ * file: slot h is stored through buffer h % slow_slots and written behind to
+ * the file by a host I/O thread; in the reverse, which takes the slots in
+ * decreasing order, slot h - slow_slots is read back into the buffer as soon
+ * as slot h has left it.  The file is created in `dir` and removed from it at
+ * once (it lives until the tier is replaced or the context destroyed).
+ * file_slots = 0 removes the tier.  Per-step path only (EUNSUPPORTED with
+ * "path" 2; "path" 0 then runs per step).  ambptt_calibrate takes the file's
+ * write time per state into T_T.  EINVAL if the file cannot be created. */
+ambptt_status ambptt_set_file_tier(ambptt_ctx* ctx, const char* dir, int64_t file_slots);
 
 /* Measures T_A (one forward step) and T_T (one state over the host link,
  * the slower direction) and sets the context's I_min = ceil(T_T / T_A)

@@ -14,7 +14,7 @@ LOSS = {"half_sq_last": 0, "mean_sq_all": 1, "mean_last": 2}
 
 EXPORTS = ["ambptt_version", "ambptt_revolve_advances", "ambptt_schedule_evals", "ambptt_schedule_text",
            "ambptt_schedule_text_starts", "ambptt_resident_program", "ambptt_query", "ambptt_last_error",
-           "ambptt_create", "ambptt_bind", "ambptt_set_int", "ambptt_calibrate", "ambptt_run",
+           "ambptt_create", "ambptt_bind", "ambptt_set_int", "ambptt_set_file_tier", "ambptt_calibrate", "ambptt_run",
            "ambptt_last_schedule_text", "ambptt_destroy"]
 
 
@@ -34,7 +34,7 @@ class Stats(C.Structure):
                 ("compute_waits", C.c_int64), ("kernel_launches", C.c_int64),
                 ("recompute_factor", C.c_double), ("schedule_us", C.c_double), ("run_us", C.c_double), ("enqueue_us", C.c_double),
                 ("kernel_us", C.c_double * 6), ("kernel_samples", C.c_int64 * 6),
-                ("kernel_calls", C.c_int64 * 6)]
+                ("kernel_calls", C.c_int64 * 6), ("bytes_file_w", C.c_int64), ("bytes_file_r", C.c_int64)]
 
     def as_dict(self) -> dict:
         d = {}
@@ -76,6 +76,8 @@ def load():
     L.ambptt_schedule_text_starts.argtypes = [i64, i32, i64, C.POINTER(i64), i64, C.c_char_p, sz, C.POINTER(sz)]
     L.ambptt_schedule_text_starts.restype = C.c_int
     L.ambptt_last_schedule_text.argtypes = [vp, C.c_char_p, sz, C.POINTER(sz)]
+    L.ambptt_set_file_tier.argtypes = [vp, C.c_char_p, i64]
+    L.ambptt_set_file_tier.restype = C.c_int
     L.ambptt_last_schedule_text.restype = C.c_int
     L.ambptt_resident_program.argtypes = [i64, i32, i64, i32, i32, C.POINTER(i32), sz, C.POINTER(sz)]
     L.ambptt_resident_program.restype = C.c_int

@@ -192,6 +192,10 @@ class Runner:
         res["stats"] = st.as_dict()
         return res
 
+    def set_file_tier(self, directory: str, file_slots: int) -> None:
+        """A file below the pinned host tier (ambptt_set_file_tier); 0 slots removes it."""
+        check(self.L.ambptt_set_file_tier(self.ctx, str(directory).encode(), int(file_slots)))
+
     def last_schedule_text(self) -> str:
         """The canonical text of the schedule the last run executed."""
         return _text(lambda buf, cap, need: self.L.ambptt_last_schedule_text(self.ctx, buf, cap, need))

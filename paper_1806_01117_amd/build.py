@@ -22,10 +22,10 @@ ARCH = "gfx950"
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-Wno-unused-command-line-argument", "-I", INCLUDE, "-I", CSRC]
-CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-I", INCLUDE, "-I", CSRC]
+CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-pthread", "-I", INCLUDE, "-I", CSRC]
 
 HIP_SOURCES = ["cell_f32.hip", "step_small.hip", "dw_bf16.hip", "dw_f32.hip", "resmlp.hip", "wide_bf16.hip", "resident.hip", "runtime.hip"]
-CXX_SOURCES = ["schedule.cpp", "resident_prog.cpp"]
+CXX_SOURCES = ["schedule.cpp", "resident_prog.cpp", "tier_file.cpp"]
 
 
 def _hipcc() -> str:
@@ -57,7 +57,7 @@ def build(verbose: bool = False) -> str:
     with ThreadPoolExecutor(max(1, min(8, len(jobs)))) as ex:
         list(ex.map(_run, jobs))
     tmp = LIB + ".tmp"
-    _run([hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp])
+    _run([hipcc, "-shared", "-fPIC", "-pthread", f"--offload-arch={ARCH}", *objs, "-o", tmp])
     os.replace(tmp, LIB)
     if verbose:
         print("built", LIB)

@@ -31,6 +31,7 @@
 #include "kernels.hpp"
 #include "resident_prog.hpp"
 #include "schedule.hpp"
+#include "tier_file.hpp"
 
 using namespace ambptt;
 
@@ -237,6 +238,8 @@ struct ambptt_ctx {
   int store_policy = 0;  // 0: every I-th state; 1: the next state once the previous store has completed
   hipEvent_t ev_sweep[3] = {nullptr, nullptr, nullptr};  // host pacing of the sweep with store_policy 1
   Plan last_plan;        // the schedule the last ambptt_run executed
+  FileTier* ftier = nullptr;        // a file below the pinned host tier (per-step path)
+  std::vector<hipEvent_t> ev_file;  // per pinned buffer: its last device copy (system scope: the host reads the data)
   int32_t* prog_host = nullptr;  // pinned staging of the resident program
   size_t prog_host_cap = 0;
   unsigned* status_host = nullptr;  // pinned copy of the resident kernel's status words
@@ -246,6 +249,9 @@ struct ambptt_ctx {
 namespace {
 
 enum { kNone = 0, kStorePending = 1, kPrefetchPending = 2 };
+
+// Slow slots the schedule may use: the pinned host tier's, or the file's below it.
+int64_t slow_capacity(const ambptt_ctx* C) { return C->ftier ? C->ftier->capacity() : C->p.slow_slots; }
 
 unsigned event_flags(const ambptt_ctx* C, bool timing) {
   return (timing ? 0u : unsigned(hipEventDisableTiming)) | (C->sys_fence ? 0u : unsigned(hipEventDisableSystemFence));
@@ -597,7 +603,7 @@ struct Exec {
   // s >= 2, H >= 1.  Returns the starts; the reverse is built from them.
   ambptt_status dynamic_sweep(std::vector<int64_t>& starts, float* dW, float* db) {
     constexpr int kAhead = 3;
-    const int64_t n = p.n_steps, H = p.slow_slots;
+    const int64_t n = p.n_steps, H = slow_capacity(C);
     const int64_t spacing = std::max<int64_t>(1, (n + H) / (H + 1));
     ambptt_status s;
     starts.assign(1, 0);
@@ -684,10 +690,17 @@ struct Exec {
           break;
         case Op::Store: {
           const int64_t k = A.a, h = A.b;
+          char* dst = C->host + (size_t)h * L.stride;
+          if (C->ftier && !(dst = C->ftier->store_buffer(h))) return fail(AMBPTT_EINTERNAL, C->ftier->error());
           HIPCK(hipEventRecord(C->ev_c, C->cs));
           HIPCK(hipStreamWaitEvent(C->xs, C->ev_c, 0));
-          HIPCK(hipMemcpyAsync(C->host + (size_t)h * L.stride, slot(k), L.state_bytes, hipMemcpyDeviceToHost, C->xs));
+          HIPCK(hipMemcpyAsync(dst, slot(k), L.state_bytes, hipMemcpyDeviceToHost, C->xs));
           HIPCK(hipEventRecord(C->ev_slot[size_t(k)], C->xs));
+          if (C->ftier) {  // written behind to the file once the copy has landed
+            hipEvent_t ev = C->ev_file[size_t(h % int64_t(C->ev_file.size()))];
+            HIPCK(hipEventRecord(ev, C->xs));
+            C->ftier->stored(h, [ev] { return hipEventSynchronize(ev) == hipSuccess; });
+          }
           if (C->pend[size_t(k)] != kPrefetchPending) C->pend[size_t(k)] = kStorePending;
           st.stores++;
           st.bytes_d2h += (int64_t)L.state_bytes;
@@ -698,6 +711,7 @@ struct Exec {
           st.prefetches++;
           if (C->elide_prefetch && slot_t[size_t(k)] == t) {
             st.prefetches_elided++;
+            if (C->ftier) C->ftier->prefetched(h, [] { return true; });  // nothing copied out of the buffer
             break;
           }
           if (cur_slot == k && !live_dead) {  // the live state aliases the target: keep it
@@ -705,10 +719,17 @@ struct Exec {
             if ((s = copy_state(dst, cur)) != AMBPTT_OK) return s;
             set_cur_live(dst);
           }
+          const char* src = C->host + (size_t)h * L.stride;
+          if (C->ftier && !(src = C->ftier->prefetch_buffer(h))) return fail(AMBPTT_EINTERNAL, C->ftier->error());
           HIPCK(hipEventRecord(C->ev_c, C->cs));
           HIPCK(hipStreamWaitEvent(C->xs, C->ev_c, 0));
-          HIPCK(hipMemcpyAsync(slot(k), C->host + (size_t)h * L.stride, L.state_bytes, hipMemcpyHostToDevice, C->xs));
+          HIPCK(hipMemcpyAsync(slot(k), src, L.state_bytes, hipMemcpyHostToDevice, C->xs));
           HIPCK(hipEventRecord(C->ev_slot[size_t(k)], C->xs));
+          if (C->ftier) {  // the buffer takes the slot h - R from the file once this copy is done
+            hipEvent_t ev = C->ev_file[size_t(h % int64_t(C->ev_file.size()))];
+            HIPCK(hipEventRecord(ev, C->xs));
+            C->ftier->prefetched(h, [ev] { return hipEventSynchronize(ev) == hipSuccess; });
+          }
           C->pend[size_t(k)] = kPrefetchPending;
           slot_t[size_t(k)] = t;
           st.bytes_h2d += (int64_t)L.state_bytes;
@@ -760,7 +781,7 @@ ambptt_status prepare_inputs(ambptt_ctx* C, const void* W, const void* h0, const
 
 bool resident_possible(ambptt_ctx* C) {
   // the resident program is compiled before the launch: it takes no decision at run time
-  if (!C->L.res || C->path_opt == 1 || C->store_policy == 1) return false;
+  if (!C->L.res || C->path_opt == 1 || C->store_policy == 1 || C->ftier) return false;
   if (C->res_cap < 0) {
     int cap = 0;
     if (resident_capacity(C->L.G, &cap) != hipSuccess) {
@@ -1223,6 +1244,16 @@ ambptt_status ambptt_calibrate(ambptt_ctx* C, const void* x_seq, const void* W, 
     }
     tt = std::max(tt, best);
   }
+  if (C->ftier) {  // the file takes every stored state too: the slower of the two links sets T_T
+    HIPCK(hipMemcpy(C->host, E.live(0), C->L.state_bytes, hipMemcpyDeviceToHost));
+    double best = 1e30;
+    for (int rep = 0; rep < 3; ++rep) {
+      const double sec = C->ftier->time_write(C->host, C->L.state_bytes);
+      if (sec < 0) return fail(AMBPTT_EINTERNAL, "file tier: calibration write failed");
+      best = std::min(best, 1e6 * sec);
+    }
+    tt = std::max(tt, best);
+  }
   HIPCK(hipEventDestroy(e0));
   HIPCK(hipEventDestroy(e1));
   const int64_t I = std::max<int64_t>(1, (int64_t)std::ceil(tt / std::max(ta, 1e-3)));
@@ -1252,7 +1283,7 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   const double t0 = now_us();
   Plan plan;
   try {
-    plan = make_plan(p.n_steps, p.fast_slots, p.slow_slots, std::max<int64_t>(C->interval_min, 1));
+    plan = make_plan(p.n_steps, p.fast_slots, slow_capacity(C), std::max<int64_t>(C->interval_min, 1));
   } catch (const std::exception& e) {
     return fail(AMBPTT_EINTERNAL, e.what());
   }
@@ -1261,8 +1292,23 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   // use the host tier at all
   const bool dynamic = C->store_policy == 1 && plan.async && p.n_steps >= 2;
   if (plan.async) {
-    const size_t slots = dynamic ? size_t(std::min<int64_t>(p.slow_slots, p.n_steps)) : size_t(plan.host_slots_used);
+    size_t slots = dynamic ? size_t(std::min<int64_t>(slow_capacity(C), p.n_steps)) : size_t(plan.host_slots_used);
+    if (C->ftier) slots = std::min<size_t>(slots, size_t(p.slow_slots));  // the pinned ring in front of the file
     if ((s = ensure_host(C, slots * L.stride)) != AMBPTT_OK) return s;
+    if (C->ftier) {
+      if (!C->ftier->finish()) return fail(AMBPTT_EINTERNAL, C->ftier->error());
+      while (C->ev_file.size() < slots) {
+        hipEvent_t ev;
+        HIPCK(hipEventCreateWithFlags(&ev, hipEventDisableTiming));
+        C->ev_file.push_back(ev);
+      }
+      while (C->ev_file.size() > slots) {
+        HIPCK(hipEventDestroy(C->ev_file.back()));
+        C->ev_file.pop_back();
+      }
+      C->ftier->begin(C->host, int64_t(slots), L.stride, L.state_bytes);
+      C->ftier->bytes_written = C->ftier->bytes_read = 0;
+    }
   }
   Exec E(C, x_seq, W, b);
   std::fill(C->pend.begin(), C->pend.end(), kNone);
@@ -1277,7 +1323,7 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
     std::vector<int64_t> starts;
     if ((s = E.dynamic_sweep(starts, dW, db)) != AMBPTT_OK) return s;
     try {
-      plan = make_plan_starts(p.n_steps, p.fast_slots, p.slow_slots, starts);
+      plan = make_plan_starts(p.n_steps, p.fast_slots, slow_capacity(C), starts);
     } catch (const std::exception& e) {
       return fail(AMBPTT_EINTERNAL, e.what());
     }
@@ -1299,9 +1345,14 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   HIPCK(hipStreamSynchronize(C->cs));
   HIPCK(hipStreamSynchronize(C->ds));
   HIPCK(hipStreamSynchronize(C->xs));
+  if (C->ftier && plan.async && !C->ftier->finish()) return fail(AMBPTT_EINTERNAL, C->ftier->error());
   const double t2 = now_us();
   if (loss) *loss = *C->host_loss;
   ambptt_stats& st = E.st;
+  if (C->ftier && plan.async) {
+    st.bytes_file_w = C->ftier->bytes_written;
+    st.bytes_file_r = C->ftier->bytes_read;
+  }
   double sum[6] = {0, 0, 0, 0, 0, 0};
   int64_t cnt[6] = {0, 0, 0, 0, 0, 0};
   for (auto& smp : E.samples) {
@@ -1331,6 +1382,26 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
     return fail(AMBPTT_EINTERNAL, "executor forward count " + std::to_string(st.forward_evals) +
                                       " != schedule count " + std::to_string(plan.evals));
   C->last_plan = std::move(plan);
+  return AMBPTT_OK;
+}
+
+ambptt_status ambptt_set_file_tier(ambptt_ctx* C, const char* dir, int64_t file_slots) {
+  if (!C) return fail(AMBPTT_EINVAL, "ctx is NULL");
+  if (file_slots < 0) return fail(AMBPTT_EINVAL, "file_slots must be >= 0");
+  if (file_slots > 0 && (!dir || !*dir)) return fail(AMBPTT_EINVAL, "file tier: a directory is required");
+  if (file_slots > 0 && C->p.slow_slots < 1)
+    return fail(AMBPTT_EINVAL, "file tier: the problem needs at least one pinned host slot in front of the file");
+  if (file_slots > 0 && C->path_opt == 2) return fail(AMBPTT_EUNSUPPORTED, "the file tier runs on the per-step path only");
+  if (C->ftier) {
+    (void)hipStreamSynchronize(C->xs);
+    (void)C->ftier->finish();
+    delete C->ftier;
+    C->ftier = nullptr;
+  }
+  if (file_slots == 0) return AMBPTT_OK;
+  std::string err;
+  C->ftier = FileTier::open(dir, file_slots, &err);
+  if (!C->ftier) return fail(AMBPTT_EINVAL, err);
   return AMBPTT_OK;
 }
 
@@ -1373,6 +1444,11 @@ void ambptt_destroy(ambptt_ctx* C) {
   if (C->ev_c2) (void)hipEventDestroy(C->ev_c2);
   for (auto& ev : C->ev_sweep)
     if (ev) (void)hipEventDestroy(ev);
+  if (C->ftier) {
+    (void)C->ftier->finish();
+    delete C->ftier;
+  }
+  for (auto& ev : C->ev_file) (void)hipEventDestroy(ev);
   if (C->ds) (void)hipStreamDestroy(C->ds);
   if (C->xs) (void)hipStreamDestroy(C->xs);
   if (C->host) (void)hipHostFree(C->host);

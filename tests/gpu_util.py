@@ -42,12 +42,14 @@ def device_inputs(wl, x, W, b, x0):
 
 
 def run_gpu(wl, dev_in, window: int | None = None, timing_sample: int = 0, elide: bool = True,
-            path: int | None = None, wide: bool | None = None, opts: dict | None = None, **spec_kw):
+            path: int | None = None, wide: bool | None = None, opts: dict | None = None,
+            file_tier: tuple | None = None, **spec_kw):
     """One forward + reverse pass on the GPU; returns numpy results and stats.
 
     path: None (library default), 1 (one launch per step), 2 (resident kernel).
     wide: None (library default), False (no wide-batch bf16 kernels).
-    opts: further ambptt_set_int keys and values."""
+    opts: further ambptt_set_int keys and values.
+    file_tier: (directory, file slots) for ambptt_set_file_tier."""
     import paper_1806_01117_amd as amb
     spec = amb.ProblemSpec.from_workload(wl, **spec_kw)
     say(wl.name, spec, "path", path)
@@ -64,6 +66,8 @@ def run_gpu(wl, dev_in, window: int | None = None, timing_sample: int = 0, elide
         r.set("elide_prefetch", 1 if elide else 0)
         for k, v in (opts or {}).items():
             r.set(k, v)
+        if file_tier is not None:
+            r.set_file_tier(*file_tier)
         out = r.run(*dev_in)
         text = r.last_schedule_text()
     finally:
