@@ -31,6 +31,8 @@ namespace {
 constexpr int kTM = 256, kTN = 128;            // dW tile: gate rows x input columns
 constexpr int kS = 64;                         // reduction rows per stage
 constexpr int kPZ = kTM + 16, kPX = kTN + 16;  // LDS row pitch (bf16): 544 and 288 bytes
+constexpr int kPT = kTN + 4;                     // pitch (floats) of the staged output rows
+static_assert(128 * kPT * 4 <= 2 * 64 * kPZ * 2, "the staged half tile fits in the Z stages");
 
 typedef short s4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u4v __attribute__((ext_vector_type(4)));
@@ -132,21 +134,44 @@ __global__ __launch_bounds__(512) void dw_bf16(DwArgs a) {
     if (more) stash(buf ^ 1);  // buf ^ 1 was last read before the previous barrier
     __syncthreads();
   }
-  // lane l holds, for block (i, j) and v = 0..3, row 4 (l >> 4) + v and column l & 15
+  // The tile goes out through LDS (free after the main loop), 128 rows at a
+  // time, so that dW is read and written in whole rows with 16-byte accesses
+  // (each 16-lane group of the MFMA layout would touch a 64-byte row segment).
+  // Lane l holds, for block (i, j) and v = 0..3, row 4 (l >> 4) + v and column l & 15.
   const int q = lane >> 4, cl = lane & 15;
+  float* T = (float*)&Zs[0][0][0];  // 128 x kPT floats = 67.6 KB of the 69.6 KB of Zs
+  const bool vec = (N % 4) == 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int half = 0; half < 2; ++half) {
+    if ((wm >> 1) == half) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int k = k0 + 64 * wm + 16 * i + 4 * q + v;
-      if (k >= GH) continue;
-      float* drow = a.dW + (size_t)k * N;
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int c = c0 + 64 * wn + 16 * j + cl;
-        if (c < N) drow[c] = a.accumulate ? drow[c] + acc[i][j][v] : acc[i][j][v];
+        for (int v = 0; v < 4; ++v)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            T[(64 * (wm & 1) + 16 * i + 4 * q + v) * kPT + 64 * wn + 16 * j + cl] = acc[i][j][v];
+    }
+    __syncthreads();
+    // 32 lanes per row, 4 columns each: 16 rows per pass, 8 passes
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+      const int row = 16 * p + (tid >> 5), c4 = 4 * (tid & 31);
+      const int k = k0 + 128 * half + row, c = c0 + c4;
+      if (k >= GH || c >= N) continue;
+      float* d = a.dW + (size_t)k * N + c;
+      f4 t = *(const f4*)&T[row * kPT + c4];
+      if (vec) {  // c + 3 < N: N is a multiple of 4 (of 8, by the launch check)
+        if (a.accumulate) t += *(const f4*)d;
+        *(f4*)d = t;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (c + e < N) d[e] = a.accumulate ? d[e] + t[e] : t[e];
       }
     }
+    __syncthreads();  // the next half overwrites T
+  }
   if (do_bias && k0 + tid < GH) a.db[k0 + tid] = a.accumulate ? a.db[k0 + tid] + bsum : bsum;
 }
 
