@@ -379,7 +379,11 @@ def main() -> int:
         cand = [k for k in tot if k in flops]
         dom = max(cand, key=tot.get) if cand else "adj"
         small = spec.batch * spec.hidden < 1024 * 256 or wl.dtype == "bf16"
-        if wide and wl.cell == "resmlp":
+        if wide and wl.dtype == "f32":
+            names = {"fwd": "step_f32 forward: gate GEMM + cell update",
+                     "adj": "step_f32 adjoint: gate recompute + cell adjoint",
+                     "hadj": "prod_f32 h-adjoint product zbar W_h", "dw": "dw_f32_big weight-gradient window"}
+        elif wide and wl.cell == "resmlp":
             names = {"fwd": "mlp_wide forward", "adj": "mlp_wide adjoint (recompute + mask)",
                      "hadj": "prod_wide NN product ybar + zbar W_{l+1}", "dw": "dw_bf16 weight gradient of one layer"}
         elif wide:
@@ -393,7 +397,9 @@ def main() -> int:
             k = "step_small" if small else "step_f32"
             names = {"fwd": f"{k} forward: gate GEMM + cell update", "adj": f"{k} adjoint: gate recompute + h-adjoint GEMM",
                      "dw": ("dw_bf16" if wl.dtype == "bf16" else "dw_lds_f32") + " weight-gradient window"}
-        if wide:
+        if wide and wl.dtype == "f32":
+            key = {"fwd": "step_f32_fwd", "adj": "step_f32_adj", "hadj": "prod_f32"}.get(dom, "dw_f32_big")
+        elif wide:
             fam = {"fwd": "mlp_wide_fwd", "adj": "mlp_wide_adj", "hadj": "prod_wide_nn"} if wl.cell == "resmlp" else \
                 {"fwd": "cell_wide_fwd", "adj": "cell_wide_adj", "hadj": "prod_wide_nt"}
             key = fam.get(dom, "dw_bf16")

@@ -113,8 +113,9 @@ typedef struct {
 
 /* Kernel classes of ambptt_stats.kernel_*: forward step, the resident
  * whole-pass kernel, adjoint step (gate recomputation and cell adjoint), the
- * adjoint's own product launch on the wide-batch bf16 path (hbar = zbar W_h,
- * or the MLP's ybar + zbar W_{l+1}), weight-gradient window, and everything
+ * adjoint's own product launch on the wide-batch bf16 path and the fp32
+ * large-batch path (hbar = zbar W_h, or the MLP's ybar + zbar W_{l+1}),
+ * weight-gradient window, and everything
  * else. */
 enum { AMBPTT_K_FWD = 0, AMBPTT_K_PASS = 1, AMBPTT_K_ADJ = 2, AMBPTT_K_HADJ = 3,
        AMBPTT_K_DW = 4, AMBPTT_K_OTHER = 5 };
@@ -218,8 +219,11 @@ ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
  * completed, at least ceil(n / (H + 1)) steps apart, the non-uniform policy
  * of Section 6; where the fixed-interval policy would use the host tier, on
  * the per-step path only: EUNSUPPORTED with "path" 2; stats mode 2 and
- * ambptt_last_schedule_text give the schedule that ran).  EINVAL for unknown
- * keys or values out of range. */
+ * ambptt_last_schedule_text give the schedule that ran), "hadj_launch" (1,
+ * default: on the fp32 path for large batches the adjoint's h-adjoint
+ * product zbar_{t+1} W_h runs as a launch of its own, kernel class
+ * AMBPTT_K_HADJ; 0: fused into the adjoint step's launch).  EINVAL for
+ * unknown keys or values out of range. */
 ambptt_status ambptt_set_int(ambptt_ctx* ctx, const char* key, int64_t value);
 
 /* Puts a file below the pinned host tier: a third storage level for states

@@ -146,7 +146,8 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
   }
 
   // ---- h-adjoint GEMM of the following step: hbar_{t+1} = zbar_{t+1} W_h --
-  const bool do_hbar = (MODE == kFinal) || (MODE == kAdjoint && !a.first);
+  // (fused only when the adjoint's product did not run as a launch of its own)
+  const bool do_hbar = (MODE == kFinal) || (MODE == kAdjoint && !a.first && !a.hbar_in);
   if (do_hbar) {
     const int nch = GH / 16;
     const int c0 = (nch * wave) / KS, c1 = (nch * (wave + 1)) / KS;
@@ -242,7 +243,7 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
             lterm += h1;
           }
         }
-        const float hb = (a.first ? 0.f : acch[i][jj][v]) + sd;
+        const float hb = (a.first ? 0.f : (a.hbar_in ? a.hbar_in[o] : acch[i][jj][v])) + sd;
         float* zo = (float*)a.zbar_out + (size_t)m * GH + j;
         if (G == 4) {
           const float cb = a.first ? 0.f : a.cbar_in[o];
@@ -262,6 +263,70 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
     const float s = wave_sum(lterm);
     if (lane == 0) a.loss_acc[blockIdx.y * gridDim.x + blockIdx.x] += (double)s;
   }
+}
+
+// The adjoint's h-adjoint product as a launch of its own (fp32):
+// out[m][n] = sum_k A[m][k] B[n][k] (+ add[m][n]), A = zbar_{t+1} [M][GH],
+// B = W_h^T [H][GH], both rows contiguous in k.  Fused into the step kernel
+// it would take the gate GEMM's tile (RJ units, K = GH), which reads 4 times
+// as many operand bytes per flop as the forward's (4 RJ gate columns over
+// K = D + H); here each workgroup takes RM x NB = 2 x 8 blocks of 16 x 16,
+// the forward's ratio of operand loads to MFMAs.  KS waves split K; their
+// partials meet in LDS in wave order (bit-reproducible).
+template <int RM, int NB, int KS>
+__global__ __launch_bounds__(64 * KS) void prod_f32(ProdArgs a) {
+  constexpr int U = 2;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 15, q = lane >> 4;
+  const int M = a.M, N = a.N, K = a.K;
+  const int m0 = blockIdx.x * (16 * RM), n0 = blockIdx.y * (16 * NB);
+  f4 acc[RM][NB];
+#pragma unroll
+  for (int i = 0; i < RM; ++i)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[i][nb] = f4{0.f, 0.f, 0.f, 0.f};
+  int rows[RM];
+#pragma unroll
+  for (int i = 0; i < RM; ++i) rows[i] = min(m0 + 16 * i + r, M - 1);  // rows >= M: clamped, discarded
+  const float* A = (const float*)a.A;
+  const float* Bm = (const float*)a.B;
+  const int nch = K / 16;
+  const int c0 = (nch * wave) / KS, c1 = (nch * (wave + 1)) / KS;
+  nt_chunks<RM, NB, U>(
+      c0, c1, acc, [&](int ch, int i) -> f4 { return *(const f4*)(A + (size_t)rows[i] * K + ch * 16 + 4 * q); },
+      [&](int ch, int nb) -> f4 { return *(const f4*)(Bm + (size_t)(n0 + 16 * nb + r) * K + ch * 16 + 4 * q); });
+  if constexpr (KS > 1) {
+    __shared__ f4 red[(KS - 1) * RM * NB * 64];
+    if (wave > 0) {
+      f4* dst = red + (size_t)(wave - 1) * RM * NB * 64 + lane;
+#pragma unroll
+      for (int i = 0; i < RM; ++i)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) dst[(i * NB + nb) * 64] = acc[i][nb];
+    }
+    __syncthreads();
+    if (wave != 0) return;
+    for (int w = 1; w < KS; ++w) {
+      const f4* src = red + (size_t)(w - 1) * RM * NB * 64 + lane;
+#pragma unroll
+      for (int i = 0; i < RM; ++i)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[i][nb] += src[(i * NB + nb) * 64];
+    }
+  }
+  // accumulator element v of lane l: row 4 (l >> 4) + v, column l & 15 of its block
+#pragma unroll
+  for (int i = 0; i < RM; ++i)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int m = m0 + 16 * i + 4 * q + v;
+      if (m >= M) continue;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const size_t o = (size_t)m * N + n0 + 16 * nb + r;
+        a.out[o] = a.add ? a.add[o] + acc[i][nb][v] : acc[i][nb][v];
+      }
+    }
 }
 
 // dW[k][c] += sum_r Z[r][k] X[r][c] and db[k] += sum_r Z[r][k] over the R rows
@@ -452,6 +517,18 @@ hipError_t launch_dw(const DwArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e
   hipExtLaunchKernelGGL(dw_lds_f32, grid, dim3(256), 0, s, e0, e1, 0, a);
   return hipGetLastError();
 }
+hipError_t launch_prod_f32(const ProdArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (a.K % 16 != 0 || a.N % 16 != 0 || a.M < 1 || a.K < 16) return hipErrorInvalidValue;
+  if (a.N % 128 == 0) {
+    const dim3 grid((a.M + 31) / 32, a.N / 128);
+    hipExtLaunchKernelGGL((prod_f32<2, 8, 4>), grid, dim3(256), 0, s, e0, e1, 0, a);
+  } else {
+    const dim3 grid((a.M + 15) / 16, a.N / 16);
+    hipExtLaunchKernelGGL((prod_f32<1, 1, 4>), grid, dim3(256), 0, s, e0, e1, 0, a);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_transpose_wh(const float* W, float* WhT, int GH, int D, int H, hipStream_t s) {
   dim3 grid((GH + 31) / 32, (H + 31) / 32);
   hipLaunchKernelGGL(transpose_wh_f32, grid, dim3(32, 8), 0, s, W, WhT, GH, D, H);

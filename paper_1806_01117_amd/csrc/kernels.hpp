@@ -147,6 +147,8 @@ void step_grid(const StepCfg& cfg, int B, int H, dim3* grid, dim3* block);
 hipError_t launch_step(int G, int mode, const StepCfg& cfg, const StepArgs& a, hipStream_t s,
                        hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_dw(const DwArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+// fp32 out = A B^T (+ add): the adjoint's h-adjoint product zbar W_h through W_h^T (K % 16 == 0, N % 16 == 0)
+hipError_t launch_prod_f32(const ProdArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 // 128 x 128-tile fp32 weight gradient for GH, D + H >= 256 (launch_dw picks it when it fits).
 bool dw_f32_big_fits(const DwArgs& a);
 hipError_t launch_dw_f32_big(const DwArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1);

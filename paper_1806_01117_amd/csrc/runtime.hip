@@ -71,6 +71,7 @@ struct Layout {
   // the adjoint's products as launches of their own (wide_bf16.hip)
   bool wide = false;
   size_t off_hbar = 0;   // fp32 [B][H]: hbar_{t+1} (cell) or ybar_{l+2} + zbar_{l+1} W_{l+1} (MLP)
+  bool hsep = false;     // fp32 step kernels of large batches: the h-adjoint product may run as its own launch
   // resident whole-pass kernel (fp32 RNN / LSTM whose weights fit in registers)
   bool res = false;
   int r_mtiles = 0, r_ng = 0, r_nwg = 0, r_S = 0;
@@ -178,7 +179,8 @@ Layout make_layout(const ambptt_problem* p, int window) {
   L.off_cbar[1] = o; o += align_up(BH * 4);
   L.off_loss = o; o += align_up((size_t)L.loss_slots * 8);
   L.off_lossout = o; o += kAlign;
-  if (L.wide) {
+  L.hsep = !L.small && !L.mlp && p->dtype == AMBPTT_F32;
+  if (L.wide || L.hsep) {
     L.off_hbar = o; o += align_up(BH * 4);
   }
   if (L.res) {
@@ -236,6 +238,7 @@ struct ambptt_ctx {
   // kernels).
   bool sys_fence = false;
   int store_policy = 0;  // 0: every I-th state; 1: the next state once the previous store has completed
+  bool hadj_launch = true;  // fp32 large-batch path: the adjoint's h-adjoint product as a launch of its own
   hipEvent_t ev_sweep[3] = {nullptr, nullptr, nullptr};  // host pacing of the sweep with store_policy 1
   Plan last_plan;        // the schedule the last ambptt_run executed
   FileTier* ftier = nullptr;        // a file below the pinned host tier (per-step path)
@@ -301,13 +304,15 @@ struct Exec {
   std::vector<Sample> samples;
   bool live_dead = false;  // the live state was consumed by an adjoint step
   bool wide = false;       // wide-batch bf16 kernels
-  float* hbuf = nullptr;   // their adjoint product (fp32 [B][H])
+  bool sep32 = false;      // fp32 step kernels with the h-adjoint product as a launch of its own
+  float* hbuf = nullptr;   // the adjoint's product (fp32 [B][H]) on those two paths
 
   Exec(ambptt_ctx* c, const void* x_, const void* W_, const float* b_)
       : C(c), L(c->L), p(c->p), x((const char*)x_), W(W_), b(b_), slot_t(size_t(c->p.fast_slots), -1) {
     WhT = C->ws + L.off_wht;
     wide = L.wide && C->wide_opt;
-    if (wide) hbuf = (float*)(C->ws + L.off_hbar);
+    sep32 = L.hsep && C->hadj_launch;
+    if (wide || sep32) hbuf = (float*)(C->ws + L.off_hbar);
   }
   const void* x_at(int64_t t) const { return x + (size_t)t * p.batch * p.input * L.dsize; }
 
@@ -487,9 +492,11 @@ struct Exec {
       a.cbar_out = cbar(t);
       a.hwin_out = hwin_at(t);
       a.loss_acc = (double*)(C->ws + L.off_loss);
-      if (wide && !first) {  // hbar_{t+1} = zbar_{t+1} W_h
+      if ((wide || sep32) && !first) {  // hbar_{t+1} = zbar_{t+1} W_h
         ProdArgs pa{a.zbar_in, WhT, nullptr, hbuf, p.batch, p.hidden, L.G * p.hidden};
-        s = timed(AMBPTT_K_HADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch_prod_nt(pa, C->cs, e0, e1); });
+        s = timed(AMBPTT_K_HADJ, [&](hipEvent_t e0, hipEvent_t e1) {
+          return wide ? launch_prod_nt(pa, C->cs, e0, e1) : launch_prod_f32(pa, C->cs, e0, e1);
+        });
         if (s != AMBPTT_OK) return s;
         a.hbar_in = hbuf;
       }
@@ -557,10 +564,11 @@ struct Exec {
     a.cbar_in = cbar(0);
     a.dh0 = dh0;
     a.dc0 = dc0;
-    if (wide) {  // dL/dh_0 = zbar_0 W_h, dL/dc_0 = cbar_0
+    if (wide || sep32) {  // dL/dh_0 = zbar_0 W_h, dL/dc_0 = cbar_0
       ProdArgs pa{a.zbar_in, WhT, nullptr, dh0, p.batch, p.hidden, L.G * p.hidden};
-      ambptt_status s =
-          timed(AMBPTT_K_OTHER, [&](hipEvent_t e0, hipEvent_t e1) { return launch_prod_nt(pa, C->cs, e0, e1); });
+      ambptt_status s = timed(AMBPTT_K_OTHER, [&](hipEvent_t e0, hipEvent_t e1) {
+        return wide ? launch_prod_nt(pa, C->cs, e0, e1) : launch_prod_f32(pa, C->cs, e0, e1);
+      });
       if (s != AMBPTT_OK) return s;
       if (L.G == 4) HIPCK(hipMemcpyAsync(dc0, a.cbar_in, (size_t)p.batch * p.hidden * 4, hipMemcpyDeviceToDevice, C->cs));
       return AMBPTT_OK;
@@ -1158,6 +1166,8 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
       if (e == hipSuccess) e = make_sync_events(C);
       if (e != hipSuccess) return fail(AMBPTT_EHIP, std::string("event_system_fence: ") + hipGetErrorString(e));
     }
+  } else if (k == "hadj_launch") {
+    C->hadj_launch = v != 0;
   } else if (k == "store_policy") {
     if (v < 0 || v > 1) return fail(AMBPTT_EINVAL, "store_policy must be 0 (every I-th state) or 1 (when the previous store completed)");
     if (v == 1 && C->path_opt == 2) return fail(AMBPTT_EUNSUPPORTED, "store_policy 1 runs on the per-step path only");

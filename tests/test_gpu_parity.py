@@ -152,6 +152,23 @@ def test_lstm4096_shapes_short():
     assert_bitwise(a, b)
 
 
+def test_lstm_f32_large_batch_hadj_launch():
+    """fp32 step kernels for large batches (B = 256, H = 1024: 1024 tiles of
+    16 x 16) with the h-adjoint product as its own launch and fused into the
+    adjoint step: each against the oracle, each bit for bit across schedules."""
+    wl = synth.get("lstm_h4096_t20000").with_(batch=256, input=64, hidden=1024, n_steps=6, name="lstm_f32_big")
+    host, dev = _case(wl)
+    want = run_oracle(wl, *host)
+    a = run_gpu(wl, dev, fast_slots=2, slow_slots=6, interval_min=1)
+    assert a["stats"]["kernel_calls"][3] == 5  # one product launch per adjoint but the first turn's
+    assert_close(a, want, TOL_F32)
+    assert_bitwise(a, run_gpu(wl, dev, fast_slots=3, slow_slots=0))
+    f = run_gpu(wl, dev, fast_slots=2, slow_slots=6, interval_min=1, opts={"hadj_launch": 0})
+    assert f["stats"]["kernel_calls"][3] == 0
+    assert_close(f, want, TOL_F32)
+    assert_bitwise(f, run_gpu(wl, dev, fast_slots=3, slow_slots=0, opts={"hadj_launch": 0}))
+
+
 def test_lstm_bf16_small_schedules():
     """bf16 operands and stored h, fp32 cell state: oracle within 2e-2, schedules bit for bit."""
     wl = synth.get("lstm_h2048_bf16_t10000").with_(batch=20, input=64, hidden=96, n_steps=30,
