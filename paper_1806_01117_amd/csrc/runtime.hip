@@ -522,9 +522,10 @@ struct Exec {
         d.db = db + (size_t)t * p.hidden;
         d.accumulate = 0;
       }
-      // the wide-batch kernels each fill the device: beside them a window only
-      // competes for the same units, so it runs in line on the compute stream
-      const bool own = C->dw_stream < 0 ? !wide : C->dw_stream != 0;
+      // the wide-batch bf16 kernels and the large-batch fp32 kernels each fill
+      // the device: beside them a window only competes for the same units, so
+      // it runs in line on the compute stream
+      const bool own = C->dw_stream < 0 ? !(wide || L.hsep) : C->dw_stream != 0;
       hipStream_t ws = own ? C->ds : C->cs;
       if (own) {
         HIPCK(hipEventRecord(C->ev_c2, C->cs));
