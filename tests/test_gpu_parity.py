@@ -169,6 +169,20 @@ def test_lstm_f32_large_batch_hadj_launch():
     assert_bitwise(f, run_gpu(wl, dev, fast_slots=3, slow_slots=0, opts={"hadj_launch": 0}))
 
 
+def test_lstm_f32_large_batch_ragged_product():
+    """The product's fallback tiles (H = 1040 is no multiple of 128: 16 x 16
+    blocks), a batch that is no multiple of 32 (B = 250) and the RNN cell."""
+    for cell in ("lstm", "rnn"):
+        wl = synth.get("lstm_h4096_t20000").with_(cell=cell, batch=250, input=48, hidden=1040, n_steps=4,
+                                                  w_scale=1.0 / 32, name=f"{cell}_f32_big_ragged")
+        host, dev = _case(wl)
+        want = run_oracle(wl, *host)
+        a = run_gpu(wl, dev, fast_slots=2, slow_slots=4, interval_min=1)
+        assert a["stats"]["kernel_calls"][3] == 3
+        assert_close(a, want, TOL_F32)
+        assert_bitwise(a, run_gpu(wl, dev, fast_slots=4, slow_slots=0))
+
+
 def test_lstm_bf16_small_schedules():
     """bf16 operands and stored h, fp32 cell state: oracle within 2e-2, schedules bit for bit."""
     wl = synth.get("lstm_h2048_bf16_t10000").with_(batch=20, input=64, hidden=96, n_steps=30,
