@@ -234,7 +234,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--timing-sample", type=int, default=8)
+    ap.add_argument("--timing-sample", type=int, default=32)
     ap.add_argument("--path", choices=["auto", "steps", "resident"], default="auto")
     ap.add_argument("--cooperative", type=int, default=0)
     ap.add_argument("--workload", default=WORKLOAD, help="a synth workload name (default: the 512-LSTM)")

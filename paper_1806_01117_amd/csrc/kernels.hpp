@@ -157,7 +157,8 @@ void step_small_grid(int G, int B, int H, dim3* grid, dim3* block);
 hipError_t launch_step_small(int G, int bf16, int mode, const StepArgs& a, hipStream_t s,
                              hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 void resmlp_grid(int B, int w, dim3* grid, dim3* block);
-hipError_t launch_resmlp(int bf16, int mode, const MlpArgs& a, hipStream_t s);
+hipError_t launch_resmlp(int bf16, int mode, const MlpArgs& a, hipStream_t s, hipEvent_t e0 = nullptr,
+                         hipEvent_t e1 = nullptr);
 // Wide-batch bf16 path (B >= 48): the cell kernel takes 64 rows x 64 gate
 // columns per workgroup; the adjoint's products run as launches of their own.
 bool cell_wide_fits(int D, int H);  // D and H multiples of 64

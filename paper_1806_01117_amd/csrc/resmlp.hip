@@ -209,10 +209,10 @@ void resmlp_grid(int B, int w, dim3* grid, dim3* block) {
   *block = dim3(64 * kWaves, 1, 1);
 }
 
-hipError_t launch_resmlp(int bf16, int mode, const MlpArgs& a, hipStream_t s) {
+hipError_t launch_resmlp(int bf16, int mode, const MlpArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   dim3 grid, block;
   resmlp_grid(a.B, a.w, &grid, &block);
-#define AMB_M(T_, M_) hipLaunchKernelGGL((resmlp_step<T_, M_>), grid, block, 0, s, a)
+#define AMB_M(T_, M_) hipExtLaunchKernelGGL((resmlp_step<T_, M_>), grid, block, 0, s, e0, e1, 0, a)
   if (bf16) {
     if (mode == kForward) AMB_M(__bf16, kForward);
     else if (mode == kAdjoint) AMB_M(__bf16, kAdjoint);

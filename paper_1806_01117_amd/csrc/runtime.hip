@@ -240,6 +240,7 @@ struct ambptt_ctx {
   int store_policy = 0;  // 0: every I-th state; 1: the next state once the previous store has completed
   bool hadj_launch = true;  // fp32 large-batch path: the adjoint's h-adjoint product as a launch of its own
   hipEvent_t ev_sweep[3] = {nullptr, nullptr, nullptr};  // host pacing of the sweep with store_policy 1
+  hipEvent_t ev_tail = nullptr;  // end of the compute launch a host-tier copy waits for
   Plan last_plan;        // the schedule the last ambptt_run executed
   FileTier* ftier = nullptr;        // a file below the pinned host tier (per-step path)
   std::vector<hipEvent_t> ev_file;  // per pinned buffer: its last device copy (system scope: the host reads the data)
@@ -277,6 +278,9 @@ hipError_t make_sync_events(ambptt_ctx* C) {
     if ((e = remake(ev)) != hipSuccess) return e;
   for (auto& ev : C->ev_sweep)
     if ((e = remake(ev)) != hipSuccess) return e;
+  if (C->ev_tail) (void)hipEventDestroy(C->ev_tail);
+  C->ev_tail = nullptr;
+  if ((e = hipEventCreateWithFlags(&C->ev_tail, event_flags(C, true))) != hipSuccess) return e;
   for (auto& ev : C->tpool) (void)hipEventDestroy(ev);
   C->tpool.clear();
   return hipSuccess;
@@ -303,6 +307,13 @@ struct Exec {
   int64_t calls[6] = {0, 0, 0, 0, 0, 0};
   std::vector<Sample> samples;
   bool live_dead = false;  // the live state was consumed by an adjoint step
+  // Host-tier copies must follow the compute work before them.  When a store
+  // or prefetch comes next in the action list, the compute launches carry an
+  // end event of their own (recorded by the dispatch), which the copy stream
+  // then waits for: no marker packet is put between two kernels.
+  bool want_tail = false;        // the next compute launches carry tail_ev
+  bool tail_ok = false;          // tail_ev marks the end of the latest compute-stream work
+  hipEvent_t tail_ev = nullptr;
   bool wide = false;       // wide-batch bf16 kernels
   bool sep32 = false;      // fp32 step kernels with the h-adjoint product as a launch of its own
   float* hbuf = nullptr;   // the adjoint's product (fp32 [B][H]) on those two paths
@@ -337,15 +348,13 @@ struct Exec {
     return AMBPTT_OK;
   }
 
-  // Runs one launch; every timing_sample-th launch of a class is bracketed by
-  // events on the compute stream (the stream the kernel runs on).
-  // Runs one launch; every timing_sample-th launch of a class is bracketed by a
-  // pair of events recorded on the stream the kernel runs on.  The interval
-  // includes the kernel's dispatch latency (a few microseconds on top of the
-  // execution time a kernel trace reports).
+  // Runs one launch.  Every timing_sample-th launch of a class carries a pair
+  // of events that the dispatch itself records at the kernel's start and end
+  // (hipExtLaunchKernel): no marker packet joins the stream, and the interval
+  // is the kernel's execution time.
   template <class F>
   ambptt_status timed(int cls, F launch, hipStream_t strm = nullptr) {
-    if (!strm) strm = C->cs;
+    const bool compute = strm == nullptr || strm == C->cs;
     const bool sample = C->timing_sample > 0 && (calls[cls] % C->timing_sample) == 0 && samples.size() < 4096;
     Sample smp{cls, nullptr, nullptr};
     if (sample) {
@@ -357,13 +366,15 @@ struct Exec {
       }
       smp.a = C->tpool[need - 2];
       smp.b = C->tpool[need - 1];
-      HIPCK(hipEventRecord(smp.a, strm));
     }
-    HIPCK(launch(nullptr, nullptr));
-    if (sample) {
-      HIPCK(hipEventRecord(smp.b, strm));
-      samples.push_back(smp);
+    hipEvent_t end = smp.b;
+    if (compute && want_tail && !end) end = C->ev_tail;
+    HIPCK(launch(smp.a, end));
+    if (compute) {
+      tail_ok = want_tail;
+      tail_ev = end;
     }
+    if (sample) samples.push_back(smp);
     calls[cls]++;
     st.kernel_launches++;
     return AMBPTT_OK;
@@ -412,7 +423,7 @@ struct Exec {
       a.y_out = dst;
       return timed(AMBPTT_K_FWD, [&](hipEvent_t e0, hipEvent_t e1) {
         return wide ? launch_mlp_wide(kForward, a, C->cs, e0, e1)
-                    : launch_resmlp(p.dtype == AMBPTT_BF16, kForward, a, C->cs);
+                    : launch_resmlp(p.dtype == AMBPTT_BF16, kForward, a, C->cs, e0, e1);
       });
     }
     StepArgs a = base_args();
@@ -475,8 +486,8 @@ struct Exec {
         }
         s = timed(AMBPTT_K_ADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch_mlp_wide(kAdjoint, a, C->cs, e0, e1); });
       } else {
-        s = timed(AMBPTT_K_ADJ, [&](hipEvent_t, hipEvent_t) {
-          return launch_resmlp(p.dtype == AMBPTT_BF16, kAdjoint, a, C->cs);
+        s = timed(AMBPTT_K_ADJ, [&](hipEvent_t e0, hipEvent_t e1) {
+          return launch_resmlp(p.dtype == AMBPTT_BF16, kAdjoint, a, C->cs, e0, e1);
         });
       }
     } else {
@@ -538,8 +549,10 @@ struct Exec {
           },
           ws);
       if (s != AMBPTT_OK) return s;
-      HIPCK(hipEventRecord(C->ev_dw[hf], ws));
-      dw_pending[hf] = true;
+      if (own) {  // in line, stream order already keeps the ring half until the window is done
+        HIPCK(hipEventRecord(C->ev_dw[hf], ws));
+        dw_pending[hf] = true;
+      }
     }
     return AMBPTT_OK;
   }
@@ -556,8 +569,8 @@ struct Exec {
         ProdArgs pa{a.zbar_in, a.Wn, a.ybar_in, dh0, p.batch, p.hidden, p.hidden};
         return timed(AMBPTT_K_OTHER, [&](hipEvent_t e0, hipEvent_t e1) { return launch_prod_nn(pa, C->cs, e0, e1); });
       }
-      return timed(AMBPTT_K_OTHER, [&](hipEvent_t, hipEvent_t) {
-        return launch_resmlp(p.dtype == AMBPTT_BF16, kFinal, a, C->cs);
+      return timed(AMBPTT_K_OTHER, [&](hipEvent_t e0, hipEvent_t e1) {
+        return launch_resmlp(p.dtype == AMBPTT_BF16, kFinal, a, C->cs, e0, e1);
       });
     }
     StepArgs a = base_args();
@@ -579,7 +592,20 @@ struct Exec {
 
   ambptt_status copy_state(char* dst, char* src) {
     HIPCK(hipMemcpyAsync(dst, src, L.state_bytes, hipMemcpyDeviceToDevice, C->cs));
+    tail_ok = false;
     return AMBPTT_OK;
+  }
+  // the copy stream waits for all compute work enqueued so far
+  ambptt_status copy_after_compute() {
+    hipEvent_t dep = tail_ok ? tail_ev : C->ev_c;
+    if (!tail_ok) HIPCK(hipEventRecord(C->ev_c, C->cs));
+    HIPCK(hipStreamWaitEvent(C->xs, dep, 0));
+    return AMBPTT_OK;
+  }
+  static bool copy_follows(const std::vector<Action>& acts, size_t j) {
+    if (j >= acts.size()) return false;
+    if (acts[j].op == Op::Store || acts[j].op == Op::Prefetch) return true;
+    return acts[j].op == Op::Snap && j + 1 < acts.size() && acts[j + 1].op == Op::Store;
   }
 
   char* other_live() {
@@ -629,6 +655,7 @@ struct Exec {
       if (start) {  // x_{t1} is start k + 1: step t writes it into its fast slot
         const int64_t ks = (k + 1) % 2;
         if ((s = wait_slot(ks, true)) != AMBPTT_OK) return s;
+        want_tail = !last;  // its store follows
         if ((s = fwd_step(t, cur, slot(ks))) != AMBPTT_OK) return s;
         set_cur_slot(ks);
         starts.push_back(t1);
@@ -637,10 +664,12 @@ struct Exec {
         if ((s = run_acts(sw, 0, dW, db)) != AMBPTT_OK) return s;
       } else {
         char* dst = other_live();
+        want_tail = false;
         if ((s = fwd_step(t, cur, dst)) != AMBPTT_OK) return s;
         set_cur_live(dst);
       }
       HIPCK(hipEventRecord(C->ev_sweep[t % kAhead], C->cs));
+      tail_ok = false;
     }
   }
 
@@ -648,6 +677,7 @@ struct Exec {
     ambptt_status s;
     for (size_t i = from; i < acts.size(); ++i) {
       const Action& A = acts[i];
+      want_tail = copy_follows(acts, i + 1);
       switch (A.op) {
         case Op::Advance: {
           int64_t fuse_k = -1;
@@ -701,8 +731,7 @@ struct Exec {
           const int64_t k = A.a, h = A.b;
           char* dst = C->host + (size_t)h * L.stride;
           if (C->ftier && !(dst = C->ftier->store_buffer(h))) return fail(AMBPTT_EINTERNAL, C->ftier->error());
-          HIPCK(hipEventRecord(C->ev_c, C->cs));
-          HIPCK(hipStreamWaitEvent(C->xs, C->ev_c, 0));
+          if ((s = copy_after_compute()) != AMBPTT_OK) return s;
           HIPCK(hipMemcpyAsync(dst, slot(k), L.state_bytes, hipMemcpyDeviceToHost, C->xs));
           HIPCK(hipEventRecord(C->ev_slot[size_t(k)], C->xs));
           if (C->ftier) {  // written behind to the file once the copy has landed
@@ -730,8 +759,7 @@ struct Exec {
           }
           const char* src = C->host + (size_t)h * L.stride;
           if (C->ftier && !(src = C->ftier->prefetch_buffer(h))) return fail(AMBPTT_EINTERNAL, C->ftier->error());
-          HIPCK(hipEventRecord(C->ev_c, C->cs));
-          HIPCK(hipStreamWaitEvent(C->xs, C->ev_c, 0));
+          if ((s = copy_after_compute()) != AMBPTT_OK) return s;
           HIPCK(hipMemcpyAsync(slot(k), src, L.state_bytes, hipMemcpyHostToDevice, C->xs));
           HIPCK(hipEventRecord(C->ev_slot[size_t(k)], C->xs));
           if (C->ftier) {  // the buffer takes the slot h - R from the file once this copy is done
@@ -1455,6 +1483,7 @@ void ambptt_destroy(ambptt_ctx* C) {
   if (C->ev_c2) (void)hipEventDestroy(C->ev_c2);
   for (auto& ev : C->ev_sweep)
     if (ev) (void)hipEventDestroy(ev);
+  if (C->ev_tail) (void)hipEventDestroy(C->ev_tail);
   if (C->ftier) {
     (void)C->ftier->finish();
     delete C->ftier;
