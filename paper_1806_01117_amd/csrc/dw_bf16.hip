@@ -73,29 +73,31 @@ __global__ __launch_bounds__(512) void dw_bf16(DwArgs a) {
   const __bf16* zsrc = Z + (zok ? k0 + zc : 0);
   const __bf16* xsrc = xcol < D ? X + xcol : Hw + (xok ? xcol - D : 0);
   const int xld = xcol < D ? D : H;
-  u4v zv[4], xv[2];
-  auto load = [&](int st) {
+  // two register sets: stage s is loaded into set s & 1 two stages before
+  // its MFMAs, so each load has a whole stage of MFMAs to land behind
+  u4v zv[2][4], xv[2][2];
+  auto load = [&](int st, int set) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int row = st * kS + zr + 16 * j;
-      zv[j] = (zok && row < R) ? *(const u4v*)(zsrc + (size_t)row * GH) : u4v{0u, 0u, 0u, 0u};
+      zv[set][j] = (zok && row < R) ? *(const u4v*)(zsrc + (size_t)row * GH) : u4v{0u, 0u, 0u, 0u};
     }
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int row = st * kS + xr + 32 * j;
-      xv[j] = (xok && row < R) ? *(const u4v*)(xsrc + (size_t)row * xld) : u4v{0u, 0u, 0u, 0u};
+      xv[set][j] = (xok && row < R) ? *(const u4v*)(xsrc + (size_t)row * xld) : u4v{0u, 0u, 0u, 0u};
     }
   };
-  auto stash = [&](int buf) {
+  auto stash = [&](int buf, int set) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = zr + 16 * j;
-      *(u4v*)&Zs[buf][r][swz(r, zc)] = zv[j];
+      *(u4v*)&Zs[buf][r][swz(r, zc)] = zv[set][j];
     }
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int r = xr + 32 * j;
-      *(u4v*)&Xs[buf][r][swz(r, xc)] = xv[j];
+      *(u4v*)&Xs[buf][r][swz(r, xc)] = xv[set][j];
     }
   };
 
@@ -107,14 +109,7 @@ __global__ __launch_bounds__(512) void dw_bf16(DwArgs a) {
   float bsum = 0.f;
   const bool do_bias = blockIdx.y == 0 && tid < kTM;
 
-  const int nst = (R + kS - 1) / kS;
-  load(0);
-  stash(0);
-  __syncthreads();
-  for (int st = 0; st < nst; ++st) {
-    const int buf = st & 1;
-    const bool more = st + 1 < nst;
-    if (more) load(st + 1);
+  auto compute = [&](int buf) {
 #pragma unroll
     for (int kc = 0; kc < kS / 32; ++kc) {
       bf16x8 af[4], bf[4];
@@ -131,9 +126,27 @@ __global__ __launch_bounds__(512) void dw_bf16(DwArgs a) {
 #pragma unroll 8
       for (int rr = 0; rr < kS; ++rr) bsum += (float)Zs[buf][rr][swz(rr, tid)];
     }
-    if (more) stash(buf ^ 1);  // buf ^ 1 was last read before the previous barrier
+  };
+  const int nst = (R + kS - 1) / kS;
+  // stage st: its rows are in LDS buffer st & 1; stage st + 1's rows are in
+  // register set (st + 1) & 1; stage st + 2 is loaded into set st & 1
+  auto stage = [&](int st, int p) {  // p = st & 1, a constant in each unrolled half
+    if (st + 2 < nst) load(st + 2, p);
+    compute(p);
+    if (st + 1 < nst) stash(p ^ 1, p ^ 1);  // buffer p ^ 1 was last read before the previous barrier
     __syncthreads();
+  };
+
+  load(0, 0);
+  if (nst > 1) load(1, 1);
+  stash(0, 0);
+  __syncthreads();
+  int st = 0;
+  for (; st + 1 < nst; st += 2) {
+    stage(st, 0);
+    stage(st + 1, 1);
   }
+  if (st < nst) stage(st, 0);
   // The tile goes out through LDS (free after the main loop), 128 rows at a
   // time, so that dW is read and written in whole rows with 16-byte accesses
   // (each 16-lane group of the MFMA layout would touch a 64-byte row segment).
