@@ -223,8 +223,12 @@ ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
  * ambptt_last_schedule_text give the schedule that ran), "hadj_launch" (1,
  * default: on the fp32 path for large batches the adjoint's h-adjoint
  * product zbar_{t+1} W_h runs as a launch of its own, kernel class
- * AMBPTT_K_HADJ; 0: fused into the adjoint step's launch).  EINVAL for
- * unknown keys or values out of range. */
+ * AMBPTT_K_HADJ; 0: fused into the adjoint step's launch), "host_waits"
+ * (when compute must wait for a host-tier copy still in flight: 1 the host
+ * waits before enqueueing the dependent work, 0 a stream wait on the compute
+ * stream; -1, default: 1 on the wide-batch bf16 and large-batch fp32 paths,
+ * whose queued kernels keep the device busy while the host waits, else 0).
+ * EINVAL for unknown keys or values out of range. */
 ambptt_status ambptt_set_int(ambptt_ctx* ctx, const char* key, int64_t value);
 
 /* Puts a file below the pinned host tier: a third storage level for states

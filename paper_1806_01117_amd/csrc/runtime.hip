@@ -239,6 +239,7 @@ struct ambptt_ctx {
   bool sys_fence = false;
   int store_policy = 0;  // 0: every I-th state; 1: the next state once the previous store has completed
   bool hadj_launch = true;  // fp32 large-batch path: the adjoint's h-adjoint product as a launch of its own
+  int host_waits = -1;      // slot dependencies on host-tier copies: 1 waited for on the host, 0 stream waits, -1 by path
   hipEvent_t ev_sweep[3] = {nullptr, nullptr, nullptr};  // host pacing of the sweep with store_policy 1
   hipEvent_t ev_tail = nullptr;  // end of the compute launch a host-tier copy waits for
   Plan last_plan;        // the schedule the last ambptt_run executed
@@ -332,13 +333,21 @@ struct Exec {
   void* hpart(char* s) const { return s; }
   float* cpart(char* s) const { return (float*)(s + align_up(L.h_bytes)); }
 
+  // Compute reads a prefetched slot, or overwrites a slot being stored, only
+  // after that copy.  A copy still in flight when the host gets here costs a
+  // wait: a stream wait on the compute stream, whose barrier packet costs
+  // several microseconds between two kernels even when the copy has long
+  // finished, or, on the paths whose kernels each take tens of microseconds
+  // or more, a wait on the host: the copy was issued an interval or more
+  // before, so the device still has that much work queued while the host
+  // waits.
   ambptt_status wait_slot(int64_t k, bool for_write) {
     int& pd = C->pend[size_t(k)];
     if (pd == kPrefetchPending || (for_write && pd == kStorePending)) {
-      // only a copy still in flight costs the compute stream a wait
       const hipError_t q = hipEventQuery(C->ev_slot[size_t(k)]);
       if (q == hipErrorNotReady) {
-        HIPCK(hipStreamWaitEvent(C->cs, C->ev_slot[size_t(k)], 0));
+        if (C->host_waits < 0 ? (wide || L.hsep) : C->host_waits != 0) HIPCK(hipEventSynchronize(C->ev_slot[size_t(k)]));
+        else HIPCK(hipStreamWaitEvent(C->cs, C->ev_slot[size_t(k)], 0));
         st.compute_waits++;
       } else if (q != hipSuccess) {
         HIPCK(q);
@@ -1195,6 +1204,9 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
       if (e == hipSuccess) e = make_sync_events(C);
       if (e != hipSuccess) return fail(AMBPTT_EHIP, std::string("event_system_fence: ") + hipGetErrorString(e));
     }
+  } else if (k == "host_waits") {
+    if (v < -1 || v > 1) return fail(AMBPTT_EINVAL, "host_waits must be -1 (by path), 0 or 1");
+    C->host_waits = int(v);
   } else if (k == "hadj_launch") {
     C->hadj_launch = v != 0;
   } else if (k == "store_policy") {

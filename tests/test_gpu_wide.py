@@ -51,6 +51,9 @@ def test_wide_lstm_bf16_windows():
     assert_close(a, want, TOL_BF16)
     b = run_gpu(wl, dev, fast_slots=2, slow_slots=0, window=2, opts={"dw_stream": 1})
     assert_bitwise(a, b)
+    c = run_gpu(wl, dev, fast_slots=2, slow_slots=7, interval_min=2, window=2, opts={"host_waits": 0})
+    assert c["stats"]["stores"] == a["stats"]["stores"] > 0
+    assert_bitwise(a, c)  # host-tier dependencies as stream waits instead of host waits
 
 
 @pytest.mark.parametrize("loss", ["half_sq_last", "mean_sq_all", "mean_last"])
