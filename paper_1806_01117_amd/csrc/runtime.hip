@@ -240,8 +240,7 @@ struct ambptt_ctx {
   int store_policy = 0;  // 0: every I-th state; 1: the next state once the previous store has completed
   bool hadj_launch = true;  // fp32 large-batch path: the adjoint's h-adjoint product as a launch of its own
   int host_waits = -1;      // slot dependencies on host-tier copies: 1 waited for on the host, 0 stream waits, -1 by path
-  hipEvent_t ev_sweep[3] = {nullptr, nullptr, nullptr};  // host pacing of the sweep with store_policy 1
-  hipEvent_t ev_tail = nullptr;  // end of the compute launch a host-tier copy waits for
+  hipEvent_t ev_end[8] = {};  // end events recorded by compute dispatches (host-tier copies and sweep pacing wait on them)
   Plan last_plan;        // the schedule the last ambptt_run executed
   FileTier* ftier = nullptr;        // a file below the pinned host tier (per-step path)
   std::vector<hipEvent_t> ev_file;  // per pinned buffer: its last device copy (system scope: the host reads the data)
@@ -277,11 +276,11 @@ hipError_t make_sync_events(ambptt_ctx* C) {
     if ((e = remake(ev)) != hipSuccess) return e;
   for (auto& ev : C->ev_slot)
     if ((e = remake(ev)) != hipSuccess) return e;
-  for (auto& ev : C->ev_sweep)
-    if ((e = remake(ev)) != hipSuccess) return e;
-  if (C->ev_tail) (void)hipEventDestroy(C->ev_tail);
-  C->ev_tail = nullptr;
-  if ((e = hipEventCreateWithFlags(&C->ev_tail, event_flags(C, true))) != hipSuccess) return e;
+  for (auto& ev : C->ev_end) {
+    if (ev) (void)hipEventDestroy(ev);
+    ev = nullptr;
+    if ((e = hipEventCreateWithFlags(&ev, event_flags(C, true))) != hipSuccess) return e;
+  }
   for (auto& ev : C->tpool) (void)hipEventDestroy(ev);
   C->tpool.clear();
   return hipSuccess;
@@ -312,9 +311,12 @@ struct Exec {
   // or prefetch comes next in the action list, the compute launches carry an
   // end event of their own (recorded by the dispatch), which the copy stream
   // then waits for: no marker packet is put between two kernels.
-  bool want_tail = false;        // the next compute launches carry tail_ev
+  bool want_tail = false;        // the next compute launches carry an end event for a copy after them
+  bool want_end = false;         // ... or for the host's pacing of the sweep
   bool tail_ok = false;          // tail_ev marks the end of the latest compute-stream work
   hipEvent_t tail_ev = nullptr;
+  hipEvent_t last_end = nullptr;  // end event of the latest compute launch that carried one
+  unsigned end_cur = 0;           // next event of the ring (8 deep: reused 8 launches later)
   bool wide = false;       // wide-batch bf16 kernels
   bool sep32 = false;      // fp32 step kernels with the h-adjoint product as a launch of its own
   float* hbuf = nullptr;   // the adjoint's product (fp32 [B][H]) on those two paths
@@ -377,11 +379,12 @@ struct Exec {
       smp.b = C->tpool[need - 1];
     }
     hipEvent_t end = smp.b;
-    if (compute && want_tail && !end) end = C->ev_tail;
+    if (compute && (want_tail || want_end) && !end) end = C->ev_end[end_cur++ & 7];
     HIPCK(launch(smp.a, end));
     if (compute) {
       tail_ok = want_tail;
       tail_ev = end;
+      last_end = end;
     }
     if (sample) samples.push_back(smp);
     calls[cls]++;
@@ -653,9 +656,11 @@ struct Exec {
     starts.assign(1, 0);
     const std::vector<Action> head = {{Op::Snap, 0, 0, 0}, {Op::Store, 0, 0, 0}};
     if ((s = run_acts(head, 0, dW, db)) != AMBPTT_OK) return s;
+    hipEvent_t pace[kAhead] = {};  // end events of the last kAhead steps (recorded by their dispatches)
+    want_end = true;
     for (int64_t t = 0;; ++t) {
       const int64_t k = int64_t(starts.size()) - 1, tk = starts.back(), t1 = t + 1;
-      if (t >= kAhead) HIPCK(hipEventSynchronize(C->ev_sweep[t % kAhead]));
+      if (t >= kAhead) HIPCK(hipEventSynchronize(pace[t % kAhead]));
       const hipError_t q = hipEventQuery(C->ev_slot[size_t(k % 2)]);
       if (q != hipSuccess && q != hipErrorNotReady) HIPCK(q);
       const bool near_end = n - t1 <= t1 - tk;  // t1 <= n - 1 holds: n - t1 >= 1 until then
@@ -668,7 +673,11 @@ struct Exec {
         if ((s = fwd_step(t, cur, slot(ks))) != AMBPTT_OK) return s;
         set_cur_slot(ks);
         starts.push_back(t1);
-        if (last) return AMBPTT_OK;  // the reverse begins by snapshotting it (already there)
+        if (last) {
+          want_end = false;
+          return AMBPTT_OK;  // the reverse begins by snapshotting it (already there)
+        }
+        pace[t % kAhead] = last_end;
         const std::vector<Action> sw = {{Op::Snap, ks, t1, 0}, {Op::Store, ks, k + 1, t1}};
         if ((s = run_acts(sw, 0, dW, db)) != AMBPTT_OK) return s;
       } else {
@@ -676,9 +685,8 @@ struct Exec {
         want_tail = false;
         if ((s = fwd_step(t, cur, dst)) != AMBPTT_OK) return s;
         set_cur_live(dst);
+        pace[t % kAhead] = last_end;
       }
-      HIPCK(hipEventRecord(C->ev_sweep[t % kAhead], C->cs));
-      tail_ok = false;
     }
   }
 
@@ -1493,9 +1501,8 @@ void ambptt_destroy(ambptt_ctx* C) {
   for (auto& ev : C->ev_dw)
     if (ev) (void)hipEventDestroy(ev);
   if (C->ev_c2) (void)hipEventDestroy(C->ev_c2);
-  for (auto& ev : C->ev_sweep)
+  for (auto& ev : C->ev_end)
     if (ev) (void)hipEventDestroy(ev);
-  if (C->ev_tail) (void)hipEventDestroy(C->ev_tail);
   if (C->ftier) {
     (void)C->ftier->finish();
     delete C->ftier;
