@@ -61,13 +61,50 @@ one [t_{K-1}, n)):
   Forward evaluations = t_{K-1} + sum_k F(l_k, s-1) + 1.  Fixed intervals are
   the case t_k = kI.
 
+Online checkpointing (the number of steps unknown during the forward sweep,
+the variant named in Section 1.1 beside Revolve): every decision about x_t is
+taken when x_t is computed, knowing only that step t exists (t <= n-2); the
+end of the sequence shows itself when x_{n-1} is reached.  Placement in m
+fast slots from a sweep start a (our policy; the paper only cites the prior
+work):
+  held = [a], phase r = 1; segment j = [held_j, held_{j+1}) (the last one ends
+  at the live state) may be at most cap_j = beta(m - j, r - 1) long, so that
+  reversing it with the m - j slots it will have advances each step at most
+  r - 1 more times; the phase-end placement P_r puts held_j at
+  a + cap_0 + ... + cap_{j-1}.
+  At x_t: if fewer than m states are held, hold x_t.  Otherwise the options
+  are "drop held_j (j >= 1) and hold x_t", allowed when the merged segment
+  fits cap_{j-1}, and "hold nothing new", allowed when the last segment
+  extended to t+1 fits its cap; only options keeping every point of P_r at or
+  before t are admissible.  None admissible: r += 1 and look again.  Among
+  the admissible, take the least cost of reversing if the sweep ended at step
+  t+1, sum_j F(l_j, m - j), then holding x_t before not, then the smallest j.
+  Pinned: optimal (equal to Revolve) for n <= beta(s, 2), no step advanced
+  more often than under Revolve (the least possible repetition number), and
+  the forward prefix does not depend on n.
+Single level (H = 0):  S 0 0, the sweep A/S of the placement with m = s in
+  slots 0 .. s-1 (lowest free slot), F n-1, then the segments from the last
+  down, segment j reversed with s - j slots by the split rule.
+Two levels (H > 0, s >= 2): interval length I = max(I_min, 1) fixed up front.
+  The sweep snapshots each interval start into fast slot 0 or 1 (alternating)
+  and stores it to the lowest free host slot; inside an interval the
+  placement above runs with m = s - 1 (the start's slot and working slots
+  2 .. s-1).  When a start finds every host slot taken, I doubles and the
+  stored starts that are not multiples of the new I give their host slots
+  back (repeated while the step is still a start and nothing was freed).
+  After the sweep: P of the previous start, F n-1, the last interval's
+  segments, then the earlier intervals from the last down, each reversed by
+  the split rule on s - 1 slots with its predecessor prefetched first (into
+  the other one of slots 0, 1).
+
 Canonical text: a header line
-  ambptt-schedule v1 n=<n> s=<s> H=<H> I=<I or 0> mode=<revolve|async|dynamic>
-(I = 0 for revolve and dynamic) then the actions, single spaces, decimal
-integers, newline-terminated.
+  ambptt-schedule v1 n=<n> s=<s> H=<H> I=<I or 0> mode=<revolve|async|dynamic|online>
+(I = 0 for revolve and dynamic, the initial interval for online, 0 when single
+level) then the actions, single spaces, decimal integers, newline-terminated.
 """
 from __future__ import annotations
 
+import heapq
 from math import comb
 
 import numpy as np
@@ -218,6 +255,150 @@ def schedule_from_starts(n: int, s: int, H: int, starts: list[int]) -> tuple[dic
     _two_level(g, n, s, starts)
     head = {"n": n, "s": s, "H": H, "I": 0, "mode": "dynamic", "evals": dynamic_evals(n, s, starts)}
     return head, g.out
+
+
+class OnlinePlacement:
+    """Fast-slot placement for a sweep from x_a whose end is unknown (rules in
+    the module docstring).  held: the times held, increasing, held[0] = a."""
+
+    def __init__(self, m: int, a: int):
+        if m < 1:
+            raise ValueError("need m >= 1 slots")
+        self.m, self.a, self.r = m, a, 1
+        self.held = [a]
+
+    def cap(self, j: int) -> int:
+        return beta(self.m - j, self.r - 1)
+
+    def phase_end_points(self) -> list[int]:
+        pts, acc = [self.a], self.a
+        for j in range(self.m - 1):
+            acc += self.cap(j)
+            pts.append(acc)
+        return pts
+
+    def reverse_cost(self, held: list[int], end: int) -> int:
+        """Advances needed to reverse [a, end) from this placement (end = the last step's index)."""
+        bounds = held + [end]
+        return sum(advances(bounds[j + 1] - bounds[j], self.m - j) for j in range(len(held)))
+
+    def decide(self, t: int):
+        """x_t has been computed and step t exists.  Returns None (hold
+        nothing new) or ("hold", dropped) with dropped the time given up or None."""
+        if len(self.held) < self.m:
+            self.held.append(t)
+            return ("hold", None)
+        k = len(self.held) - 1
+        while True:
+            must = [p for p in self.phase_end_points() if p <= t]
+            opts = []
+            for j in range(1, k + 1):
+                nxt = self.held[j + 1] if j < k else t
+                if nxt - self.held[j - 1] <= self.cap(j - 1):
+                    opts.append((self.held[:j] + self.held[j + 1:] + [t], 0, j))
+            if t + 1 - self.held[k] <= self.cap(k):
+                opts.append((list(self.held), 1, 0))
+            opts = [o for o in opts if all(p in o[0] for p in must)]
+            if opts:
+                held, skip, j = min(opts, key=lambda o: (self.reverse_cost(o[0], t + 1), o[1], o[2]))
+                if skip:
+                    return None
+                dropped = self.held[j]
+                self.held = held
+                return ("hold", dropped)
+            self.r += 1
+
+
+def schedule_online(n: int, s: int, H: int = 0, I_min: int = 0) -> tuple[dict, list[tuple]]:
+    """(header dict, action list) of online checkpointing over n steps; every
+    action before the sweep reaches x_{n-1} is the same for every longer n."""
+    if n < 1 or s < 1 or H < 0 or I_min < 0:
+        raise ValueError("need n >= 1, s >= 1, H >= 0, I_min >= 0")
+    two = H > 0 and s >= 2
+    I0 = max(I_min, 1) if two else 0
+    g = _Gen(n)
+    g.live = 0
+    g.emit("S", 0, 0)
+    run = [0]  # first step of the advance not yet emitted
+
+    def flush(t):
+        if run[0] < t:
+            g.advance(run[0], t)
+        run[0] = t
+
+    m = s - 1 if two else s
+    work = list(range(2, s)) if two else list(range(1, s))
+    base = 0
+    slot_of = {0: 0}
+    pol = OnlinePlacement(m, 0)
+    starts = []  # (time, host slot) of the interval starts kept on the host
+    I = I0
+    if two:
+        g.emit("W", 0, 0, 0)
+        starts.append((0, 0))
+        released, fresh = [], 1  # host slots given back (a heap), the next never used
+    for t in range(1, n):
+        if t == n - 1:
+            break
+        if two and t % I == 0:
+            while not released and fresh >= H and t % I == 0:
+                I *= 2
+                keep = []
+                for a, h in starts:
+                    if a % I == 0:
+                        keep.append((a, h))
+                    else:
+                        heapq.heappush(released, h)
+                starts = keep
+            if t % I == 0:
+                flush(t)
+                base = 1 - base
+                g.emit("S", base, t)
+                if released:  # the lowest free host slot
+                    h = heapq.heappop(released)
+                else:
+                    h, fresh = fresh, fresh + 1
+                g.emit("W", base, h, t)
+                starts.append((t, h))
+                pol = OnlinePlacement(m, t)
+                slot_of = {t: base}
+                continue
+        d = pol.decide(t)
+        if d is not None:
+            used = set(slot_of.values())
+            if d[1] is not None:
+                used.discard(slot_of.pop(d[1]))
+            k = min(x for x in work if x not in used)
+            flush(t)
+            g.emit("S", k, t)
+            slot_of[t] = k
+    flush(n - 1)
+    if two and len(starts) >= 2:
+        a, h = starts[-2]
+        g.emit("P", h, 1 - base, a)
+    g.leaf(n - 1)
+    held = pol.held
+    bounds = held + [n - 1]
+    for j in range(len(held) - 1, -1, -1):
+        l = bounds[j + 1] - bounds[j]
+        if l > 0:
+            busy = {slot_of[x] for x in held[:j + 1]}
+            g.reverse(held[j], l, m - j, slot_of[held[j]], [x for x in work if x not in busy])
+    if two:
+        for k in range(len(starts) - 2, -1, -1):
+            base = 1 - base
+            if k >= 1:
+                a, h = starts[k - 1]
+                g.emit("P", h, 1 - base, a)
+            a = starts[k][0]
+            g.reverse(a, starts[k + 1][0] - a, s - 1, base, list(work))
+    evals = sum(x[2] - x[1] for x in g.out if x[0] == "A") + 1
+    head = {"n": n, "s": s, "H": H, "I": I0, "mode": "online", "evals": evals}
+    return head, g.out
+
+
+def text_online(n: int, s: int, H: int = 0, I_min: int = 0) -> str:
+    return _render(*schedule_online(n, s, H, I_min))
 
 
 def _render(head: dict, acts: list[tuple]) -> str:
