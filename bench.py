@@ -333,7 +333,8 @@ def main() -> int:
         rv.set("path", 2 if resident else 1)
         rv.set("resident_cooperative", args.cooperative)
         for k, v in knobs:
-            rv.set(k, v)
+            if k != "online":  # plain Revolve knows n up front
+                rv.set(k, v)
         rv_value, rvo = other_run(rv, reps if args.steps > 1 else 1, warm=args.steps > 1)
         rv_st = rvo["stats"]
         bitwise = fingerprint(rvo) == fp_async
@@ -345,6 +346,9 @@ def main() -> int:
         ps = amb.Runner(amb.ProblemSpec.from_workload(wl, interval_min=max(1, st["interval"]), slow_slots=host_slots),
                         device=dev)
         ps.set("path", 1)
+        for k, v in knobs:
+            if k == "online":  # the same schedule
+                ps.set(k, v)
         ps_value, pso = other_run(ps, reps)
         ps_st = pso["stats"]
         ps.close()
@@ -427,7 +431,8 @@ def main() -> int:
         "data": "synthetic (seeded normal inputs, " + ("normal" if wl.cell == "resmlp" else "uniform") + " weights)",
         "config": {"workload": wl.name, "cell": wl.cell, "batch": wl.batch, "input": wl.input,
                    "hidden": wl.hidden, "n_steps": wl.n_steps, "fast_slots": wl.fast_slots,
-                   "slow_slots": spec.slow_slots, "mode": "async" if st["mode"] else "revolve",
+                   "slow_slots": spec.slow_slots,
+                   "mode": ["revolve", "async", "dynamic", "online"][st["mode"]],
                    "interval": st["interval"], "interval_min": I_min, "t_a_us": round(t_a, 3),
                    "t_t_us": round(t_t, 3), "window": st["window"], **({"knobs": dict(knobs)} if knobs else {}),
                    **({"file_tier": {"file_slots": wl.n_steps, "pinned_ring": host_slots,

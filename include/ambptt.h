@@ -86,8 +86,10 @@ typedef struct {
  * forward evaluation is one forward step (advances plus the first turn's). */
 typedef struct {
   int32_t mode;            /* 0 = Revolve, 1 = asynchronous two-level, 2 = two-level with
-                              stores decided during the sweep ("store_policy" 1) */
-  int32_t interval;        /* I (0 in Revolve mode; in mode 2 the longest interval) */
+                              stores decided during the sweep ("store_policy" 1),
+                              3 = online checkpointing ("online" 1) */
+  int32_t interval;        /* I (0 in Revolve mode; in mode 2 the longest interval;
+                              in mode 3 the first interval, 0 in one level) */
   int32_t window;          /* steps per dW accumulation window (0: resident kernel) */
   int32_t path;            /* 0 = one launch per step, 1 = resident whole-pass kernel */
   int64_t n_steps;
@@ -162,8 +164,31 @@ ambptt_status ambptt_schedule_text(int64_t n, int32_t s, int64_t H, int32_t inte
 ambptt_status ambptt_schedule_text_starts(int64_t n, int32_t s, int64_t H, const int64_t* starts,
                                           int64_t nstarts, char* buf, size_t cap, size_t* needed);
 
+/* Canonical text of the online checkpointing schedule for n steps (header
+ * "mode=online", I = the first interval, 0 in one level): the variant that
+ * the paper names beside Revolve (Section 1.1), where the number of steps is
+ * not known while the forward sweep runs.  Every decision about state x_t is
+ * taken when x_t is computed, knowing only that step t exists; n shows
+ * itself when x_{n-1} is reached, so every action before the sweep gets
+ * there is the same for every longer n.
+ *   H = 0 (or s = 1): one level.  States are held in the s fast slots by a
+ *     placement that never advances a step more often than Revolve would
+ *     (the least repetition number) and equals Revolve's count for
+ *     n <= C(s + 2, 2); the held segments are reversed with Revolve.
+ *   H > 0, s >= 2: two levels.  Every I-th state (I = max(I_min, 1)) goes
+ *     to the lowest free host slot through fast slot 0 or 1; when a start
+ *     finds no host slot free, I doubles and the stored starts that are not
+ *     its multiples give theirs back.  Inside each interval the one-level
+ *     placement runs on s - 1 slots; the reverse prefetches one interval
+ *     ahead as in the fixed-interval policy.
+ * Buffer rules as in ambptt_schedule_text; EINVAL on bad arguments. */
+ambptt_status ambptt_schedule_text_online(int64_t n, int32_t s, int64_t H, int32_t interval_min,
+                                          char* buf, size_t cap, size_t* needed);
+
 /* The program the resident whole-pass kernel would run for the schedule of
- * (n, s, H, I_min), 4 int32 per entry {op, y, z, w}:
+ * (n, s, H, I_min) (flags bit 0: skip prefetches into a slot that already
+ * holds their state; bit 1: the online schedule of
+ * ambptt_schedule_text_online), 4 int32 per entry {op, y, z, w}:
  *   0 end (dL/dx_0, dW, loss)      1 forward step y, buffer z -> buffer w
  *   2 adjoint step y from buffer z (w = 1: first turn)
  *   3 copy buffer z -> w, first waiting until every workgroup has read the
@@ -175,7 +200,7 @@ ambptt_status ambptt_schedule_text_starts(int64_t n, int32_t s, int64_t H, const
  * Writes at most cap entries and sets *entries to the full count.  EINVAL if
  * cap is too small (buf untouched) or on bad arguments.  Pure host. */
 ambptt_status ambptt_resident_program(int64_t n, int32_t s, int64_t H, int32_t interval_min,
-                                      int32_t elide_prefetch, int32_t* buf, size_t cap, size_t* entries);
+                                      int32_t flags, int32_t* buf, size_t cap, size_t* entries);
 
 /* Sizes the caller allocates: bytes of one state (padded slot stride), of the
  * slot pool (fast_slots * stride) and of the workspace. */
@@ -220,7 +245,11 @@ ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
  * completed, at least ceil(n / (H + 1)) steps apart, the non-uniform policy
  * of Section 6; where the fixed-interval policy would use the host tier, on
  * the per-step path only: EUNSUPPORTED with "path" 2; stats mode 2 and
- * ambptt_last_schedule_text give the schedule that ran), "hadj_launch" (1,
+ * ambptt_last_schedule_text give the schedule that ran), "online" (0,
+ * default; 1: online checkpointing, the schedule of
+ * ambptt_schedule_text_online with the context's I_min, on either path;
+ * stats mode 3; EINVAL together with "store_policy" 1, EUNSUPPORTED over a
+ * file tier), "hadj_launch" (1,
  * default: on the fp32 path for large batches the adjoint's h-adjoint
  * product zbar_{t+1} W_h runs as a launch of its own, kernel class
  * AMBPTT_K_HADJ; 0: fused into the adjoint step's launch), "host_waits"

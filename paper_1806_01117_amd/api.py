@@ -63,16 +63,26 @@ def schedule_text_starts(n: int, s: int, H: int, starts) -> str:
     return _text(lambda buf, cap, need: L.ambptt_schedule_text_starts(n, s, H, arr, len(starts), buf, cap, need))
 
 
-def resident_program(n: int, s: int, H: int = 0, interval_min: int = 0, elide_prefetch: bool = True):
-    """The resident whole-pass kernel's program for a schedule, as a list of
-    (op, y, z, w) tuples (see ambptt_resident_program in include/ambptt.h)."""
+def schedule_text_online(n: int, s: int, H: int = 0, interval_min: int = 0) -> str:
+    """Canonical text of the online checkpointing schedule for n steps
+    (ambptt_schedule_text_online)."""
     L = load()
+    return _text(lambda buf, cap, need: L.ambptt_schedule_text_online(n, s, H, interval_min, buf, cap, need))
+
+
+def resident_program(n: int, s: int, H: int = 0, interval_min: int = 0, elide_prefetch: bool = True,
+                     online: bool = False):
+    """The resident whole-pass kernel's program for a schedule (the online one
+    when `online`), as a list of (op, y, z, w) tuples (see
+    ambptt_resident_program in include/ambptt.h)."""
+    L = load()
+    flags = int(elide_prefetch) | (2 if online else 0)
     need = C.c_size_t(0)
-    L.ambptt_resident_program(n, s, H, interval_min, int(elide_prefetch), None, 0, C.byref(need))
+    L.ambptt_resident_program(n, s, H, interval_min, flags, None, 0, C.byref(need))
     if need.value == 0:
-        check(L.ambptt_resident_program(n, s, H, interval_min, int(elide_prefetch), None, 0, C.byref(need)))
+        check(L.ambptt_resident_program(n, s, H, interval_min, flags, None, 0, C.byref(need)))
     buf = (C.c_int32 * (4 * need.value))()
-    check(L.ambptt_resident_program(n, s, H, interval_min, int(elide_prefetch), buf, need.value, C.byref(need)))
+    check(L.ambptt_resident_program(n, s, H, interval_min, flags, buf, need.value, C.byref(need)))
     return [tuple(buf[4 * i:4 * i + 4]) for i in range(need.value)]
 
 

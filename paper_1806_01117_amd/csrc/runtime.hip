@@ -238,6 +238,7 @@ struct ambptt_ctx {
   // kernels).
   bool sys_fence = false;
   int store_policy = 0;  // 0: every I-th state; 1: the next state once the previous store has completed
+  bool online = false;   // online checkpointing: placement decided without knowing n
   bool hadj_launch = true;  // fp32 large-batch path: the adjoint's h-adjoint product as a launch of its own
   int host_waits = -1;      // slot dependencies on host-tier copies: 1 waited for on the host, 0 stream waits, -1 by path
   hipEvent_t ev_end[8] = {};  // end events recorded by compute dispatches (host-tier copies and sweep pacing wait on them)
@@ -256,6 +257,14 @@ enum { kNone = 0, kStorePending = 1, kPrefetchPending = 2 };
 
 // Slow slots the schedule may use: the pinned host tier's, or the file's below it.
 int64_t slow_capacity(const ambptt_ctx* C) { return C->ftier ? C->ftier->capacity() : C->p.slow_slots; }
+
+// The schedule a pass runs: the online one when the context asks for it.
+Plan pass_plan(const ambptt_ctx* C) {
+  const ambptt_problem& p = C->p;
+  const int64_t I = std::max<int64_t>(C->interval_min, 1);
+  if (C->online) return make_plan_online(p.n_steps, p.fast_slots, p.slow_slots, I);
+  return make_plan(p.n_steps, p.fast_slots, slow_capacity(C), I);
+}
 
 unsigned event_flags(const ambptt_ctx* C, bool timing) {
   return (timing ? 0u : unsigned(hipEventDisableTiming)) | (C->sys_fence ? 0u : unsigned(hipEventDisableSystemFence));
@@ -1003,7 +1012,7 @@ ambptt_status resident_run(ambptt_ctx* C, const void* x_seq, const void* W, cons
   ResidentCounts rc;
   std::vector<int32_t> prog;
   try {
-    plan = make_plan(p.n_steps, p.fast_slots, p.slow_slots, std::max<int64_t>(C->interval_min, 1));
+    plan = pass_plan(C);
     prog = compile_resident(plan, p.fast_slots, C->elide_prefetch, &rc);
     if (C->res_test_stall) prog.insert(prog.begin(), {kPCopy, INT32_MAX, p.fast_slots, p.fast_slots + 1});
   } catch (const std::exception& e) {
@@ -1034,7 +1043,7 @@ ambptt_status resident_run(ambptt_ctx* C, const void* x_seq, const void* W, cons
   if (loss) *loss = *C->host_loss;
   if (stats) {
     ambptt_stats st{};
-    st.mode = plan.async ? 1 : 0;
+    st.mode = plan.online ? 3 : plan.async ? 1 : 0;
     st.interval = int32_t(plan.interval);
     st.window = 0;
     st.path = 1;
@@ -1112,12 +1121,28 @@ ambptt_status ambptt_schedule_text(int64_t n, int32_t s, int64_t H, int32_t inte
   }
 }
 
-ambptt_status ambptt_resident_program(int64_t n, int32_t s, int64_t H, int32_t interval_min, int32_t elide_prefetch,
-                                      int32_t* buf, size_t cap, size_t* entries) {
-  if (n < 1 || s < 1 || H < 0 || interval_min < 0) return fail(AMBPTT_EINVAL, "resident program: bad arguments");
+ambptt_status ambptt_schedule_text_online(int64_t n, int32_t s, int64_t H, int32_t interval_min, char* buf,
+                                          size_t cap, size_t* needed) {
+  if (n < 1 || s < 1 || H < 0 || interval_min < 0) return fail(AMBPTT_EINVAL, "schedule: bad arguments");
   try {
-    const std::vector<int32_t> prog =
-        compile_resident(make_plan(n, s, H, std::max<int32_t>(interval_min, 1)), s, elide_prefetch != 0, nullptr);
+    const std::string t = plan_text(make_plan_online(n, s, H, interval_min));
+    if (needed) *needed = t.size() + 1;
+    if (!buf || cap < t.size() + 1) return fail(AMBPTT_EINVAL, "schedule: buffer too small");
+    std::memcpy(buf, t.c_str(), t.size() + 1);
+    return AMBPTT_OK;
+  } catch (const std::exception& e) {
+    return fail(AMBPTT_EINTERNAL, e.what());
+  }
+}
+
+ambptt_status ambptt_resident_program(int64_t n, int32_t s, int64_t H, int32_t interval_min, int32_t flags,
+                                      int32_t* buf, size_t cap, size_t* entries) {
+  if (n < 1 || s < 1 || H < 0 || interval_min < 0 || (flags & ~3) != 0)
+    return fail(AMBPTT_EINVAL, "resident program: bad arguments");
+  try {
+    const int64_t I = std::max<int32_t>(interval_min, 1);
+    const Plan plan = (flags & 2) ? make_plan_online(n, s, H, I) : make_plan(n, s, H, I);
+    const std::vector<int32_t> prog = compile_resident(plan, s, (flags & 1) != 0, nullptr);
     const size_t m = prog.size() / 4;
     if (entries) *entries = m;
     if (!buf || cap < m) return fail(AMBPTT_EINVAL, "resident program: buffer too small");
@@ -1220,7 +1245,14 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
   } else if (k == "store_policy") {
     if (v < 0 || v > 1) return fail(AMBPTT_EINVAL, "store_policy must be 0 (every I-th state) or 1 (when the previous store completed)");
     if (v == 1 && C->path_opt == 2) return fail(AMBPTT_EUNSUPPORTED, "store_policy 1 runs on the per-step path only");
+    if (v == 1 && C->online) return fail(AMBPTT_EINVAL, "store_policy 1 and online checkpointing exclude each other");
     C->store_policy = int(v);
+  } else if (k == "online") {
+    if (v < 0 || v > 1) return fail(AMBPTT_EINVAL, "online must be 0 or 1");
+    if (v == 1 && C->store_policy == 1)
+      return fail(AMBPTT_EINVAL, "store_policy 1 and online checkpointing exclude each other");
+    if (v == 1 && C->ftier) return fail(AMBPTT_EUNSUPPORTED, "online checkpointing does not run over a file tier");
+    C->online = v != 0;
   } else if (k == "dw_stream") {
     if (v < -1 || v > 1) return fail(AMBPTT_EINVAL, "dw_stream must be -1 (by path), 0 or 1");
     C->dw_stream = int(v);
@@ -1342,7 +1374,7 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   const double t0 = now_us();
   Plan plan;
   try {
-    plan = make_plan(p.n_steps, p.fast_slots, slow_capacity(C), std::max<int64_t>(C->interval_min, 1));
+    plan = pass_plan(C);
   } catch (const std::exception& e) {
     return fail(AMBPTT_EINTERNAL, e.what());
   }
@@ -1421,7 +1453,7 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
     cnt[smp.cls]++;
   }
   if (stats) {
-    st.mode = plan.dynamic ? 2 : plan.async ? 1 : 0;
+    st.mode = plan.online ? 3 : plan.dynamic ? 2 : plan.async ? 1 : 0;
     st.interval = int32_t(plan.interval);
     st.window = L.window;
     st.n_steps = p.n_steps;
@@ -1450,6 +1482,8 @@ ambptt_status ambptt_set_file_tier(ambptt_ctx* C, const char* dir, int64_t file_
   if (file_slots > 0 && (!dir || !*dir)) return fail(AMBPTT_EINVAL, "file tier: a directory is required");
   if (file_slots > 0 && C->p.slow_slots < 1)
     return fail(AMBPTT_EINVAL, "file tier: the problem needs at least one pinned host slot in front of the file");
+  if (file_slots > 0 && C->online)
+    return fail(AMBPTT_EUNSUPPORTED, "online checkpointing does not run over a file tier");
   if (file_slots > 0 && C->path_opt == 2) return fail(AMBPTT_EUNSUPPORTED, "the file tier runs on the per-step path only");
   if (C->ftier) {
     (void)hipStreamSynchronize(C->xs);

@@ -22,6 +22,8 @@
 
 #include <algorithm>
 #include <cstdio>
+#include <functional>
+#include <queue>
 #include <stdexcept>
 
 namespace ambptt {
@@ -207,12 +209,182 @@ Plan make_plan_starts(int64_t n, int32_t s, int64_t H, const std::vector<int64_t
   return p;
 }
 
+int64_t OnlinePlacement::reverse_cost(const std::vector<int64_t>& h, int64_t end) const {
+  int64_t c = 0;
+  for (size_t j = 0; j < h.size(); ++j) {
+    const int64_t l = (j + 1 < h.size() ? h[j + 1] : end) - h[j];
+    c += revolve_advances(l, m_ - int64_t(j));
+  }
+  return c;
+}
+
+bool OnlinePlacement::decide(int64_t t, int64_t* dropped) {
+  *dropped = -1;
+  if (int64_t(held_.size()) < m_) {
+    held_.push_back(t);
+    return true;
+  }
+  const size_t k = held_.size() - 1;
+  std::vector<int64_t> must, cand;
+  for (;;) {
+    // points of the phase-end placement already passed: they must stay held
+    must.assign(1, a_);
+    int64_t acc = a_;
+    for (int64_t j = 0; j + 1 < m_; ++j) {
+      acc += cap(j);
+      if (acc > t) break;
+      must.push_back(acc);
+    }
+    bool all_held = true, all_but_t = true;  // every passed point held (or equal to t)
+    for (int64_t q : must) {
+      const bool in = std::binary_search(held_.begin(), held_.end(), q);
+      all_held = all_held && in;
+      all_but_t = all_but_t && (in || q == t);
+    }
+    int64_t best = -1, best_j = -1;
+    bool best_skip = false;
+    for (size_t j = 1; j <= k && all_but_t; ++j) {
+      const int64_t nxt = j < k ? held_[j + 1] : t;
+      if (nxt - held_[j - 1] > cap(int64_t(j) - 1)) continue;
+      if (std::binary_search(must.begin(), must.end(), held_[j])) continue;
+      cand.assign(held_.begin(), held_.end());
+      cand.erase(cand.begin() + long(j));
+      cand.push_back(t);
+      const int64_t c = reverse_cost(cand, t + 1);
+      if (best < 0 || c < best) best = c, best_j = int64_t(j);
+    }
+    if (all_held && t + 1 - held_[k] <= cap(int64_t(k))) {
+      const int64_t c = reverse_cost(held_, t + 1);
+      if (best < 0 || c < best) best = c, best_skip = true;
+    }
+    if (best >= 0) {
+      if (best_skip) return false;
+      *dropped = held_[size_t(best_j)];
+      held_.erase(held_.begin() + long(best_j));
+      held_.push_back(t);
+      return true;
+    }
+    ++r_;
+  }
+}
+
+Plan make_plan_online(int64_t n, int32_t s, int64_t H, int64_t interval_min) {
+  if (n < 1 || s < 1 || H < 0 || interval_min < 0)
+    throw std::invalid_argument("schedule: need n >= 1, s >= 1, H >= 0, I_min >= 0");
+  Plan p;
+  p.n = n;
+  p.s = s;
+  p.H = H;
+  p.online = true;
+  const bool two = H > 0 && s >= 2;
+  p.async = two;
+  p.interval = two ? std::max<int64_t>(interval_min, 1) : 0;
+  Builder b{n, &p.acts, 0, std::vector<char>(size_t(s), 0)};
+  const int64_t m = two ? s - 1 : s;
+  const int64_t w0 = two ? 2 : 1;  // first working slot
+  std::vector<int64_t> slot_of_t(size_t(n), -1);  // fast slot of a held state
+  std::vector<char> used(size_t(s), 0);
+  auto lowest_free_work = [&]() {
+    for (int64_t k = w0; k < s; ++k)
+      if (!used[size_t(k)]) return k;
+    throw std::logic_error("schedule: no free working slot");
+  };
+  int64_t run = 0;  // first step of the advance not yet emitted
+  auto flush = [&](int64_t t) {
+    if (run < t) b.advance(run, t);
+    run = t;
+  };
+  b.push(Op::Snap, 0, 0);
+  slot_of_t[0] = 0;
+  int64_t base = 0, I = p.interval;
+  OnlinePlacement pol(m, 0);
+  struct Start {
+    int64_t t, h;
+  };
+  std::vector<Start> starts;
+  std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> released;
+  int64_t fresh = 1;  // next never-used host slot
+  if (two) {
+    b.push(Op::Store, 0, 0, 0);
+    starts.push_back({0, 0});
+  }
+  for (int64_t t = 1; t < n - 1; ++t) {
+    if (two && t % I == 0) {
+      while (released.empty() && fresh >= H && t % I == 0) {  // no host slot: double I
+        I *= 2;
+        std::vector<Start> keep;
+        for (const Start& st : starts) {
+          if (st.t % I == 0) keep.push_back(st);
+          else released.push(st.h);
+        }
+        starts.swap(keep);
+      }
+      if (t % I == 0) {  // x_t starts an interval
+        flush(t);
+        for (int64_t k = w0; k < s; ++k) used[size_t(k)] = 0;
+        base = 1 - base;
+        b.push(Op::Snap, base, t);
+        int64_t h;
+        if (!released.empty()) {
+          h = released.top();
+          released.pop();
+        } else {
+          h = fresh++;
+        }
+        b.push(Op::Store, base, h, t);
+        starts.push_back({t, h});
+        pol = OnlinePlacement(m, t);
+        slot_of_t[size_t(t)] = base;
+        continue;
+      }
+    }
+    int64_t dropped;
+    if (!pol.decide(t, &dropped)) continue;
+    if (dropped >= 0) used[size_t(slot_of_t[size_t(dropped)])] = 0;
+    const int64_t k = lowest_free_work();
+    used[size_t(k)] = 1;
+    flush(t);
+    b.push(Op::Snap, k, t);
+    slot_of_t[size_t(t)] = k;
+  }
+  flush(n - 1);
+  if (two && starts.size() >= 2) {
+    const Start& st = starts[starts.size() - 2];
+    b.push(Op::Prefetch, st.h, 1 - base, st.t);
+  }
+  b.turn(n - 1);
+  // the placement's segments, from the last down; segment j has m - j slots
+  const std::vector<int64_t>& held = pol.held();
+  for (size_t j = held.size(); j-- > 0;) {
+    const int64_t l = (j + 1 < held.size() ? held[j + 1] : n - 1) - held[j];
+    if (l <= 0) continue;
+    std::fill(b.busy.begin(), b.busy.end(), 0);
+    if (two) b.busy[0] = b.busy[1] = 1;
+    for (size_t i = 0; i <= j; ++i) b.busy[size_t(slot_of_t[size_t(held[i])])] = 1;
+    b.reverse(held[j], l, m - int64_t(j), slot_of_t[size_t(held[j])]);
+  }
+  if (two) {
+    std::fill(b.busy.begin(), b.busy.end(), 0);
+    b.busy[0] = b.busy[1] = 1;
+    for (size_t k = starts.size() - 1; k-- > 0;) {
+      base = 1 - base;
+      if (k >= 1) b.push(Op::Prefetch, starts[k - 1].h, 1 - base, starts[k - 1].t);
+      b.reverse(starts[k].t, starts[k + 1].t - starts[k].t, s - 1, base);
+    }
+    p.host_slots_used = fresh;
+  }
+  p.evals = 1;
+  for (const Action& x : p.acts)
+    if (x.op == Op::Advance) p.evals += x.b - x.a;
+  return p;
+}
+
 std::string plan_text(const Plan& p) {
   std::string t;
   t.reserve(p.acts.size() * 12 + 96);
   t += "ambptt-schedule v1 n=" + std::to_string(p.n) + " s=" + std::to_string(p.s) +
        " H=" + std::to_string(p.H) + " I=" + std::to_string(p.dynamic ? 0 : p.interval) +
-       " mode=" + (p.dynamic ? "dynamic" : p.async ? "async" : "revolve") + "\n";
+       " mode=" + (p.online ? "online" : p.dynamic ? "dynamic" : p.async ? "async" : "revolve") + "\n";
   char line[96];
   for (const Action& x : p.acts) {
     int len = 0;

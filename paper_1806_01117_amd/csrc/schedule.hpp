@@ -27,6 +27,7 @@ struct Plan {
   int64_t interval = 0;  // 0 in Revolve mode
   bool async = false;
   bool dynamic = false;  // interval starts decided during the sweep
+  bool online = false;   // placement decided without knowing n (interval = the first I)
   int64_t evals = 0;     // forward-step evaluations
   int64_t host_slots_used = 0;
   std::vector<Action> acts;
@@ -47,6 +48,40 @@ Plan make_plan(int64_t n, int32_t s, int64_t H, int64_t interval_min);
 // starts increase from 0, stay below n and number at most H + 1; s >= 2).
 // Throws std::invalid_argument otherwise.
 Plan make_plan_starts(int64_t n, int32_t s, int64_t H, const std::vector<int64_t>& starts);
+// Online checkpointing: every decision about x_t is taken when x_t is
+// computed, knowing only that step t exists; the actions before the sweep
+// reaches x_{n-1} are the same for every longer n.  H = 0 (or s = 1): one
+// level, placement in s fast slots.  H > 0: interval starts every I =
+// max(I_min, 1) steps go to the host (I doubles and the starts that are not
+// its multiples give their host slots back when a start finds none free),
+// with the placement inside each interval on s - 1 slots.
+Plan make_plan_online(int64_t n, int32_t s, int64_t H, int64_t interval_min);
+
+// Placement of fast-slot checkpoints for a sweep from x_a whose end is not
+// known.  Phase r: segment j (from the j-th held state to the next one, the
+// last one to the live state) is at most beta(m - j, r - 1) steps long, so
+// that reversing it with the m - j slots it then has advances every step at
+// most r - 1 more times; the phase-end placement (every segment at its cap)
+// must stay reachable.  Among the admissible moves (hold x_t in a free slot;
+// give up the j-th held state for x_t; hold nothing new) the one with the
+// least reversal cost if the sweep ended at step t + 1 is taken, holding
+// before not, then the smallest j; with no admissible move the phase grows.
+class OnlinePlacement {
+ public:
+  OnlinePlacement(int64_t m, int64_t a) : m_(m), a_(a), held_(1, a) {}
+  // x_t has been computed and step t exists.  Returns true when x_t is to be
+  // held; *dropped is then the time given up, or -1.
+  bool decide(int64_t t, int64_t* dropped);
+  const std::vector<int64_t>& held() const { return held_; }
+  // Advances needed to reverse [a, end) from the placement h.
+  int64_t reverse_cost(const std::vector<int64_t>& h, int64_t end) const;
+
+ private:
+  int64_t cap(int64_t j) const { return binom_beta(m_ - j, r_ - 1); }
+  int64_t m_, a_, r_ = 1;
+  std::vector<int64_t> held_;
+};
+
 // Mode, interval and forward evaluations only (no action list).
 void plan_counts(int64_t n, int32_t s, int64_t H, int64_t interval_min, bool* async,
                  int64_t* interval, int64_t* evals);

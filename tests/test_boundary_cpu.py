@@ -132,3 +132,15 @@ def test_schedule_text_over_starts_rejects_bad_starts(amb):
                             (10, 1, 5, [0, 5]), (10, 3, 5, [])]:
         with pytest.raises(amb.AmbpttError):
             amb.schedule_text_starts(n, s, H, starts)
+
+
+def test_online_schedule_text_matches_oracle_bytewise(amb):
+    for s in (1, 2, 3, 4, 6, 10):
+        for H, I in ((0, 0), (1, 1), (2, 2), (3, 1), (6, 3), (10 ** 6, 2)):
+            for n in list(range(1, 40)) + [63, 128, 301]:
+                assert amb.schedule_text_online(n, s, H, I) == S.text_online(n, s, H, I), (n, s, H, I)
+
+
+@pytest.mark.parametrize("n,s,H,I", [(128, 4, 0, 0), (1000, 10, 1000, 2), (1000, 10, 0, 0), (2000, 16, 40, 1)])
+def test_online_workload_schedules_match_oracle(amb, n, s, H, I):
+    assert amb.schedule_text_online(n, s, H, I) == S.text_online(n, s, H, I)

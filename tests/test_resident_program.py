@@ -188,3 +188,28 @@ def test_program_entry_limits():
     assert ops[-1] == END and ops.count(END) == 1
     assert ops.count(ADJ) == 1000
     assert all(0 <= e[2] < 12 and 0 <= e[3] < 1000 for e in prog if e[0] & 0xFF in (FWD, COPY))
+
+
+ONLINE_CASES = [  # n, s, H, I_min
+    (1, 2, 0, 1), (9, 2, 0, 1), (40, 3, 0, 1), (53, 4, 0, 1), (23, 3, 2, 2), (37, 3, 4, 3), (53, 4, 3, 2),
+    (30, 2, 30, 1), (41, 5, 41, 2),
+]
+
+
+@pytest.mark.parametrize("elide", [True, False])
+@pytest.mark.parametrize("n,s,H,I", ONLINE_CASES)
+def test_online_program_reproduces_store_all(n, s, H, I, elide):
+    """Programs of online schedules: held states dropped and their slots
+    reused during the sweep, host slots given back and stored again."""
+    from oracle import schedule as S
+    cell, x0, rng = _cell(seed=5)
+    us = [rng.standard_normal((2, 3)) for _ in range(n)]
+    u_of = lambda t: us[t]
+    prog = amb.resident_program(n, s, H, I, elide, online=True)
+    got, fwd, _ = replay_program(prog, cell, n, s, u_of, x0)
+    want = bptt.store_all(cell, n, u_of, x0)
+    assert fwd == S.schedule_online(n, s, H, I if H else 0)[0]["evals"]
+    assert got["loss"] == want["loss"]
+    assert np.array_equal(got["dW"], want["dW"]) and np.array_equal(got["db"], want["db"])
+    for a, b in zip(got["dx0"], want["dx0"]):
+        assert np.array_equal(a, b)
