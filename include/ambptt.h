@@ -164,6 +164,18 @@ ambptt_status ambptt_schedule_text(int64_t n, int32_t s, int64_t H, int32_t inte
 ambptt_status ambptt_schedule_text_starts(int64_t n, int32_t s, int64_t H, const int64_t* starts,
                                           int64_t nstarts, char* buf, size_t cap, size_t* needed);
 
+/* The interval I_min for measured times of one forward step (T_A) and of one
+ * state over the host link (T_T), in microseconds, with s fast slots.
+ *   rule 0: the paper's (Section 3), the smallest I whose forward sweep
+ *     hides one transfer: ceil(T_T / T_A).
+ *   rule 1: among I = 1 .. ceil(T_T / T_A), the one with the least
+ *     modelled time per step, (max(I T_A, T_T) + F(I, s - 1) T_A) / I: an
+ *     interval of the sweep takes as long as its store when the link is the
+ *     bottleneck, and its reverse recomputes F(I, s - 1) steps (ties: the
+ *     smaller I).  With T_T <= T_A both give 1.
+ * Pure host.  Returns -1 on bad arguments (T_A <= 0, T_T < 0, s < 1). */
+int64_t ambptt_interval_from_timings(double t_a_us, double t_t_us, int32_t s, int32_t rule);
+
 /* Canonical text of the online checkpointing schedule for n steps (header
  * "mode=online", I = the first interval, 0 in one level): the variant that
  * the paper names beside Revolve (Section 1.1), where the number of steps is
@@ -249,7 +261,9 @@ ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
  * default; 1: online checkpointing, the schedule of
  * ambptt_schedule_text_online with the context's I_min, on either path;
  * stats mode 3; EINVAL together with "store_policy" 1, EUNSUPPORTED over a
- * file tier), "hadj_launch" (1,
+ * file tier), "interval_rule" (1, default: ambptt_calibrate picks the
+ * interval with the least modelled time per step; 0: ceil(T_T / T_A), see
+ * ambptt_interval_from_timings), "hadj_launch" (1,
  * default: on the fp32 path for large batches the adjoint's h-adjoint
  * product zbar_{t+1} W_h runs as a launch of its own, kernel class
  * AMBPTT_K_HADJ; 0: fused into the adjoint step's launch), "host_waits"
@@ -275,9 +289,11 @@ ambptt_status ambptt_set_int(ambptt_ctx* ctx, const char* key, int64_t value);
 ambptt_status ambptt_set_file_tier(ambptt_ctx* ctx, const char* dir, int64_t file_slots);
 
 /* Measures T_A (one forward step) and T_T (one state over the host link,
- * the slower direction) and sets the context's I_min = ceil(T_T / T_A)
- * (Section 3).  Uses the same inputs as ambptt_run; writes nothing the
- * caller owns.  Any out pointer may be NULL. */
+ * the slower direction) and sets the context's I_min from them with the
+ * context's "interval_rule" (ambptt_interval_from_timings; on the resident
+ * kernel rule 0 lets a transfer lengthen a step by 5 % before counting it).
+ * Uses the same inputs as ambptt_run; writes nothing the caller owns.  Any
+ * out pointer may be NULL. */
 ambptt_status ambptt_calibrate(ambptt_ctx* ctx, const void* x_seq, const void* W,
                                const float* b, const void* h0, const float* c0,
                                int32_t* interval_min_out, double* t_a_us, double* t_t_us);

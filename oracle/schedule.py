@@ -159,6 +159,23 @@ def choose(n: int, s: int, H: int, I_min: int) -> tuple[str, int, int]:
     return "async", I, ev
 
 
+def interval_from_timings(t_a: float, t_t: float, s: int, rule: int = 1, slack: float = 0.0) -> int:
+    """Interval from measured times of one forward step (t_a) and of one
+    state over the host link (t_t).  Rule 0 (Section 3): the smallest I whose
+    sweep hides a transfer, ceil(t_t / t_a - slack).  Rule 1: over I = 1 ..
+    that I, the least modelled time per step (max(I t_a, t_t) + F(I, s-1) t_a)
+    / I, where a sweep interval lasts as long as its store when the link is
+    slower, and the reverse recomputes F(I, s-1) of its steps; ties to the
+    smaller I."""
+    import math
+    t_a = max(t_a, 1e-3)
+    strict = max(1, math.ceil(t_t / t_a - slack))
+    if rule == 0 or s < 2:
+        return strict
+    cost = {I: (max(I * t_a, t_t) + advances(I, s - 1) * t_a) / I for I in range(1, strict + 1)}
+    return min(cost, key=lambda I: (cost[I], I))
+
+
 class _Gen:
     def __init__(self, n: int):
         self.n = n

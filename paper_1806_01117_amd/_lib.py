@@ -13,7 +13,8 @@ DTYPE = {"f32": 0, "bf16": 1}
 LOSS = {"half_sq_last": 0, "mean_sq_all": 1, "mean_last": 2}
 
 EXPORTS = ["ambptt_version", "ambptt_revolve_advances", "ambptt_schedule_evals", "ambptt_schedule_text",
-           "ambptt_schedule_text_starts", "ambptt_schedule_text_online", "ambptt_resident_program", "ambptt_query", "ambptt_last_error",
+           "ambptt_schedule_text_starts", "ambptt_schedule_text_online", "ambptt_interval_from_timings",
+           "ambptt_resident_program", "ambptt_query", "ambptt_last_error",
            "ambptt_create", "ambptt_bind", "ambptt_set_int", "ambptt_set_file_tier", "ambptt_calibrate", "ambptt_run",
            "ambptt_last_schedule_text", "ambptt_destroy"]
 
@@ -77,6 +78,8 @@ def load():
     L.ambptt_schedule_text_starts.restype = C.c_int
     L.ambptt_schedule_text_online.argtypes = [i64, i32, i64, i32, C.c_char_p, sz, C.POINTER(sz)]
     L.ambptt_schedule_text_online.restype = C.c_int
+    L.ambptt_interval_from_timings.argtypes = [C.c_double, C.c_double, i32, i32]
+    L.ambptt_interval_from_timings.restype = i64
     L.ambptt_last_schedule_text.argtypes = [vp, C.c_char_p, sz, C.POINTER(sz)]
     L.ambptt_set_file_tier.argtypes = [vp, C.c_char_p, i64]
     L.ambptt_set_file_tier.restype = C.c_int

@@ -63,6 +63,14 @@ def schedule_text_starts(n: int, s: int, H: int, starts) -> str:
     return _text(lambda buf, cap, need: L.ambptt_schedule_text_starts(n, s, H, arr, len(starts), buf, cap, need))
 
 
+def interval_from_timings(t_a_us: float, t_t_us: float, s: int, rule: int = 1) -> int:
+    """I_min for measured T_A and T_T (ambptt_interval_from_timings)."""
+    v = load().ambptt_interval_from_timings(float(t_a_us), float(t_t_us), s, rule)
+    if v < 0:
+        raise ValueError("bad interval arguments")
+    return int(v)
+
+
 def schedule_text_online(n: int, s: int, H: int = 0, interval_min: int = 0) -> str:
     """Canonical text of the online checkpointing schedule for n steps
     (ambptt_schedule_text_online)."""

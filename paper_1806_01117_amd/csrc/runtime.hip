@@ -239,6 +239,7 @@ struct ambptt_ctx {
   bool sys_fence = false;
   int store_policy = 0;  // 0: every I-th state; 1: the next state once the previous store has completed
   bool online = false;   // online checkpointing: placement decided without knowing n
+  int interval_rule = 1;  // 0: smallest I with T_T <= I T_A; 1: I minimising the modelled time per step
   bool hadj_launch = true;  // fp32 large-batch path: the adjoint's h-adjoint product as a launch of its own
   int host_waits = -1;      // slot dependencies on host-tier copies: 1 waited for on the host, 0 stream waits, -1 by path
   hipEvent_t ev_end[8] = {};  // end events recorded by compute dispatches (host-tier copies and sweep pacing wait on them)
@@ -257,6 +258,27 @@ enum { kNone = 0, kStorePending = 1, kPrefetchPending = 2 };
 
 // Slow slots the schedule may use: the pinned host tier's, or the file's below it.
 int64_t slow_capacity(const ambptt_ctx* C) { return C->ftier ? C->ftier->capacity() : C->p.slow_slots; }
+
+// The interval from measured timings (Section 3).  Rule 0, the paper's: the
+// smallest I whose forward sweep hides one transfer, ceil(T_T / T_A), less a
+// relative slack for transfers that lengthen a step only a little.  Rule 1:
+// among I = 1 .. that I, the one with the least modelled time per step,
+//   (max(I T_A, T_T) + F(I, s - 1) T_A) / I,
+// a sweep interval being as slow as its store when the link is the bottleneck
+// (the next store into the same fast slot must wait for it) and the reverse
+// recomputing F(I, s - 1) steps of it; ties go to the smaller I.
+int64_t interval_from_timings(double ta, double tt, int64_t s, int rule, double slack) {
+  ta = std::max(ta, 1e-3);
+  const int64_t strict = std::max<int64_t>(1, (int64_t)std::ceil(tt / ta - slack));
+  if (rule == 0 || s < 2) return strict;
+  int64_t best = 1;
+  double best_c = 0.0;
+  for (int64_t I = 1; I <= strict; ++I) {
+    const double c = (std::max(double(I) * ta, tt) + double(revolve_advances(I, s - 1)) * ta) / double(I);
+    if (I == 1 || c < best_c) best = I, best_c = c;
+  }
+  return best;
+}
 
 // The schedule a pass runs: the online one when the context asks for it.
 Plan pass_plan(const ambptt_ctx* C) {
@@ -1121,6 +1143,14 @@ ambptt_status ambptt_schedule_text(int64_t n, int32_t s, int64_t H, int32_t inte
   }
 }
 
+int64_t ambptt_interval_from_timings(double t_a_us, double t_t_us, int32_t s, int32_t rule) {
+  if (!(t_a_us > 0.0) || !(t_t_us >= 0.0) || s < 1 || rule < 0 || rule > 1) {
+    fail(AMBPTT_EINVAL, "interval: need T_A > 0, T_T >= 0, s >= 1, rule 0 or 1");
+    return -1;
+  }
+  return interval_from_timings(t_a_us, t_t_us, s, rule, 0.0);
+}
+
 ambptt_status ambptt_schedule_text_online(int64_t n, int32_t s, int64_t H, int32_t interval_min, char* buf,
                                           size_t cap, size_t* needed) {
   if (n < 1 || s < 1 || H < 0 || interval_min < 0) return fail(AMBPTT_EINVAL, "schedule: bad arguments");
@@ -1247,6 +1277,9 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
     if (v == 1 && C->path_opt == 2) return fail(AMBPTT_EUNSUPPORTED, "store_policy 1 runs on the per-step path only");
     if (v == 1 && C->online) return fail(AMBPTT_EINVAL, "store_policy 1 and online checkpointing exclude each other");
     C->store_policy = int(v);
+  } else if (k == "interval_rule") {
+    if (v < 0 || v > 1) return fail(AMBPTT_EINVAL, "interval_rule must be 0 (ceil(T_T / T_A)) or 1 (least modelled time)");
+    C->interval_rule = int(v);
   } else if (k == "online") {
     if (v < 0 || v > 1) return fail(AMBPTT_EINVAL, "online must be 0 or 1");
     if (v == 1 && C->store_policy == 1)
@@ -1291,7 +1324,7 @@ ambptt_status ambptt_calibrate(ambptt_ctx* C, const void* x_seq, const void* W, 
     double ta = 0.0, tt = 0.0;
     if ((s = resident_calibrate(C, x_seq, W, b, h0, c0, &ta, &tt)) != AMBPTT_OK) return s;
     // transfers that lengthen a step by less than 5% count as hidden
-    const int64_t I = std::max<int64_t>(1, (int64_t)std::ceil(tt / ta - 0.05));
+    const int64_t I = interval_from_timings(ta, tt, C->p.fast_slots, C->interval_rule, 0.05);
     C->interval_min = I;
     if (interval_min_out) *interval_min_out = int32_t(std::min<int64_t>(I, INT32_MAX));
     if (t_a_us) *t_a_us = ta;
@@ -1300,7 +1333,7 @@ ambptt_status ambptt_calibrate(ambptt_ctx* C, const void* x_seq, const void* W, 
   }
   Exec E(C, x_seq, W, b);
   if ((s = prepare_inputs(C, W, h0, c0, E)) != AMBPTT_OK) return s;
-  if ((s = ensure_host(C, C->L.stride)) != AMBPTT_OK) return s;
+  if ((s = ensure_host(C, 2 * C->L.stride)) != AMBPTT_OK) return s;
   hipEvent_t e0, e1;
   HIPCK(hipEventCreateWithFlags(&e0, event_flags(C, true)));
   HIPCK(hipEventCreateWithFlags(&e1, event_flags(C, true)));
@@ -1335,6 +1368,40 @@ ambptt_status ambptt_calibrate(ambptt_ctx* C, const void* x_seq, const void* W, 
     }
     tt = std::max(tt, best);
   }
+  // The sweep's view of a transfer: per step of a sweep that stores every
+  // state through the two alternating fast slots (the executor's own store
+  // path, copies running beside the forward steps), as the resident kernel's
+  // calibration measures it.  A transfer hidden behind a step gives T_A.
+  if (!C->ftier && n >= 9 && C->p.fast_slots >= 2) {
+    const int64_t steps = std::min<int64_t>(n - 1, 24);
+    std::vector<Action> acts;
+    for (int64_t i = 0; i < steps; ++i) {
+      acts.push_back({Op::Snap, i % 2, i, 0});
+      acts.push_back({Op::Store, i % 2, i % 2, i});
+      acts.push_back({Op::Advance, i, i + 1, 0});
+    }
+    double per[2] = {1e30, 1e30};  // the best of three rounds after a warm-up round
+    const int64_t lens[2] = {steps / 3, steps};
+    for (int rep = 0; rep < 4; ++rep) {
+      for (int k = 0; k < 2; ++k) {
+        std::fill(C->pend.begin(), C->pend.end(), kNone);
+        HIPCK(hipStreamSynchronize(C->xs));
+        HIPCK(hipStreamSynchronize(C->cs));
+        HIPCK(hipEventRecord(e0, C->cs));
+        const std::vector<Action> part(acts.begin(), acts.begin() + 3 * lens[k]);
+        if ((s = E.run_acts(part, 0, nullptr, nullptr)) != AMBPTT_OK) return s;
+        HIPCK(hipEventRecord(C->ev_c, C->xs));  // the last store
+        HIPCK(hipStreamWaitEvent(C->cs, C->ev_c, 0));
+        HIPCK(hipEventRecord(e1, C->cs));
+        HIPCK(hipEventSynchronize(e1));
+        HIPCK(hipEventElapsedTime(&ms, e0, e1));
+        if (rep > 0) per[k] = std::min(per[k], 1000.0 * ms);
+      }
+    }
+    HIPCK(hipStreamSynchronize(C->xs));
+    std::fill(C->pend.begin(), C->pend.end(), kNone);
+    tt = std::max(tt, (per[1] - per[0]) / double(lens[1] - lens[0]));
+  }
   if (C->ftier) {  // the file takes every stored state too: the slower of the two links sets T_T
     HIPCK(hipMemcpy(C->host, E.live(0), C->L.state_bytes, hipMemcpyDeviceToHost));
     double best = 1e30;
@@ -1347,7 +1414,7 @@ ambptt_status ambptt_calibrate(ambptt_ctx* C, const void* x_seq, const void* W, 
   }
   HIPCK(hipEventDestroy(e0));
   HIPCK(hipEventDestroy(e1));
-  const int64_t I = std::max<int64_t>(1, (int64_t)std::ceil(tt / std::max(ta, 1e-3)));
+  const int64_t I = interval_from_timings(ta, tt, C->p.fast_slots, C->interval_rule, 0.0);
   C->interval_min = I;
   if (interval_min_out) *interval_min_out = int32_t(std::min<int64_t>(I, INT32_MAX));
   if (t_a_us) *t_a_us = ta;
