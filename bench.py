@@ -35,6 +35,28 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense
 HBM_PEAK_GBS = 8000.0
 
 
+def step_costs(spec: str, n: int):
+    """Relative step costs from "every:K:F" (step t costs F when t % K == 0, else 1); None for ""."""
+    if not spec:
+        return None
+    kind, k, f = spec.split(":")
+    if kind != "every" or int(k) < 1 or float(f) <= 0:
+        raise SystemExit("--step-costs: expected every:K:F with K >= 1, F > 0")
+    return [float(f) if t % int(k) == 0 else 1.0 for t in range(n)]
+
+
+def weighted_cost(text: str, costs) -> float:
+    """Cost of the forward evaluations of a canonical schedule text for the given step costs."""
+    import numpy as np
+    pre = np.concatenate([[0.0], np.cumsum(costs)])
+    tot = costs[-1]  # the first turn's forward step
+    for ln in text.splitlines()[1:]:
+        p = ln.split()
+        if p[0] == "A":
+            tot += pre[int(p[2])] - pre[int(p[1])]
+    return float(tot)
+
+
 def step_flops(spec, window: int, wide: bool = False) -> dict:
     """Algorithmic flops of one launch of each per-step kernel, and of the
     three products of one step (gate GEMM, h-adjoint, weight gradient).  On
@@ -246,6 +268,9 @@ def main() -> int:
                          "the pinned ring in front of it")
     ap.add_argument("--gemm-reference", action="store_true",
                     help="only time the vendor GEMM on the workload's step products and print them")
+    ap.add_argument("--step-costs", default="", metavar="every:K:F",
+                    help="relative step costs for the schedule (step t costs F when t % K == 0, else 1): "
+                         "reversals split for unequal costs (ambptt_set_step_costs)")
     ap.add_argument("--set", action="append", default=[], metavar="KEY=VALUE",
                     help="an ambptt_set_int knob for the measured passes and the plain-Revolve comparison")
     args = ap.parse_args()
@@ -292,6 +317,9 @@ def main() -> int:
         r.set(k, v)
     if args.file_tier:
         r.set_file_tier(args.file_tier, wl.n_steps)
+    costs = step_costs(args.step_costs, wl.n_steps)
+    if costs is not None:
+        r.set_step_costs(costs)
     I_min, t_a, t_t = r.calibrate(dx, dW, db, dh, dc)
     print(f"calibrated: I_min {I_min}, T_A {t_a:.2f} us, T_T {t_t:.2f} us", file=sys.stderr, flush=True)
     for k, v in knobs:  # an interval_min given here replaces the calibrated one
@@ -349,6 +377,8 @@ def main() -> int:
         for k, v in knobs:
             if k == "online":  # the same schedule
                 ps.set(k, v)
+        if costs is not None:
+            ps.set_step_costs(costs)
         ps_value, pso = other_run(ps, reps)
         ps_st = pso["stats"]
         ps.close()
@@ -459,6 +489,14 @@ def main() -> int:
                      "bytes_per_launch": int(byts[dom]),
                      "flop_per_byte": round(flops[dom] / max(byts[dom], 1), 1)},
     }
+    if costs is not None:
+        # the same pass with Revolve's own splits, weighed with the same costs
+        plain = amb.schedule_text(wl.n_steps, spec.fast_slots, host_slots, max(I_min, 1))
+        total = float(sum(costs))
+        line["step_costs"] = {"spec": args.step_costs, "forward_cost": st["forward_cost"],
+                              "weighted_recompute_factor": round(st["forward_cost"] / total, 4),
+                              "revolve_splits_weighted_recompute_factor":
+                                  round(weighted_cost(plain, costs) / total, 4)}
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl)
     print(json.dumps(line), flush=True)

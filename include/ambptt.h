@@ -111,6 +111,8 @@ typedef struct {
   int64_t kernel_samples[6];
   int64_t kernel_calls[6];
   int64_t bytes_file_w, bytes_file_r;  /* file tier traffic (ambptt_set_file_tier) */
+  double forward_cost;     /* sum of the step costs of every forward evaluation
+                              (ambptt_set_step_costs; without costs = forward_evals) */
 } ambptt_stats;
 
 /* Kernel classes of ambptt_stats.kernel_*: forward step, the resident
@@ -163,6 +165,14 @@ ambptt_status ambptt_schedule_text(int64_t n, int32_t s, int64_t H, int32_t inte
  * there; EINVAL on bad starts. */
 ambptt_status ambptt_schedule_text_starts(int64_t n, int32_t s, int64_t H, const int64_t* starts,
                                           int64_t nstarts, char* buf, size_t cap, size_t* needed);
+
+/* Canonical text of the schedule of ambptt_schedule_text with every
+ * reversal split for the step costs costs[0..n) (see ambptt_set_step_costs);
+ * the header ends with " split=cost".  Buffer rules as in
+ * ambptt_schedule_text; EINVAL on bad arguments or costs, EUNSUPPORTED when a
+ * reversal's table would exceed 1 Mi entries (see ambptt_set_step_costs). */
+ambptt_status ambptt_schedule_text_costs(int64_t n, int32_t s, int64_t H, int32_t interval_min,
+                                         const double* costs, char* buf, size_t cap, size_t* needed);
 
 /* The interval I_min for measured times of one forward step (T_A) and of one
  * state over the host link (T_T), in microseconds, with s fast slots.
@@ -287,6 +297,22 @@ ambptt_status ambptt_set_int(ambptt_ctx* ctx, const char* key, int64_t value);
  * "path" 2; "path" 0 then runs per step).  ambptt_calibrate takes the file's
  * write time per state into T_T.  EINVAL if the file cannot be created. */
 ambptt_status ambptt_set_file_tier(ambptt_ctx* ctx, const char* dir, int64_t file_slots);
+
+/* Relative forward costs of the n steps (costs[t] > 0 for step t; NULL or
+ * n = 0 removes them): layers or steps of unequal cost, which the paper's
+ * Sections 1.1 and 6 point to.  Every reversal of two or more steps on two
+ * or more fast slots is then split where a dynamic program over Revolve's
+ * recursion finds the least total cost of recomputed forward steps
+ * (ambptt_schedule_text_costs); the mode, interval and slots stay those of
+ * the uniform schedule, and equal costs give it exactly.  The costs are
+ * copied.  EINVAL if n differs from the problem's, a cost is not positive
+ * and finite, or "online" or "store_policy" 1 is set.  The dynamic program
+ * of a reversal of l steps on k slots keeps l (l + 1) (k + 1) entries and
+ * takes about l^3 k / 6 operations; a pass whose schedule holds a reversal
+ * over 1 Mi entries (single-level Revolve over ~300 steps with 10 slots;
+ * in the two-level policy the intervals are the reversals) fails in
+ * ambptt_run with EUNSUPPORTED. */
+ambptt_status ambptt_set_step_costs(ambptt_ctx* ctx, const double* costs, int64_t n);
 
 /* Measures T_A (one forward step) and T_T (one state over the host link,
  * the slower direction) and sets the context's I_min from them with the

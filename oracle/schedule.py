@@ -97,8 +97,14 @@ Two levels (H > 0, s >= 2): interval length I = max(I_min, 1) fixed up front.
   the split rule on s - 1 slots with its predecessor prefetched first (into
   the other one of slots 0, 1).
 
+Unequal step costs (Sections 1.1 and 6 point to non-uniform layers): the
+mode, interval and slots stay those above, and every reversal on two or more
+slots splits where a dynamic program over the same recursion finds the least
+total cost of recomputed forward steps (WeightedSplits); the header then ends
+with " split=cost".
+
 Canonical text: a header line
-  ambptt-schedule v1 n=<n> s=<s> H=<H> I=<I or 0> mode=<revolve|async|dynamic|online>
+  ambptt-schedule v1 n=<n> s=<s> H=<H> I=<I or 0> mode=<revolve|async|dynamic|online> [split=cost]
 (I = 0 for revolve and dynamic, the initial interval for online, 0 when single
 level) then the actions, single spaces, decimal integers, newline-terminated.
 """
@@ -181,6 +187,7 @@ class _Gen:
         self.n = n
         self.out: list[tuple] = []
         self.live = None
+        self.split = lambda a, l, k: split_range(l, k)[1]
 
     def emit(self, *a):
         self.out.append(a)
@@ -211,7 +218,7 @@ class _Gen:
                         self.advance(a, a + i)
                     self.leaf(a + i)
                 return
-            m = split_range(l, s)[1]
+            m = self.split(a, l, s)
             self.restore(base, a)
             self.advance(a, a + m)
             k = min(free)
@@ -414,12 +421,88 @@ def schedule_online(n: int, s: int, H: int = 0, I_min: int = 0) -> tuple[dict, l
     return head, g.out
 
 
+class WeightedSplits:
+    """Optimal splits for reversing steps of unequal forward cost (the
+    non-uniform case the paper's Sections 1.1 and 6 point to), by dynamic
+    programming over Revolve's recursion.  costs[t] is the cost of forward
+    step t.  With s slots (x_a's included) and the live state at x_a,
+    reversing [a, a+l) costs
+        T(a, 1, s) = 0                      (the adjoint of step a alone)
+        T(a, l, 1) = sum_{i=1}^{l-1} C(a, a+i)   (restore x_a, advance i, for i = l-1 .. 1)
+        T(a, l, s) = min_m  C(a, a+m) + T(a+m, l-m, s-1) + T(a, m, s)
+    with C(a, b) the cost of steps a .. b-1; ties go to the largest m, so that
+    equal costs give the Revolve split m = hi."""
+
+    def __init__(self, costs):
+        self.c = [float(x) for x in costs]
+        self.pre = [0.0]
+        for x in self.c:
+            self.pre.append(self.pre[-1] + x)
+        self.memo = {}
+
+    def C(self, a: int, b: int) -> float:
+        return self.pre[b] - self.pre[a]
+
+    def T(self, a: int, l: int, s: int) -> float:
+        return self._solve(a, l, s)[0]
+
+    def split(self, a: int, l: int, s: int) -> int:
+        return self._solve(a, l, s)[1]
+
+    def _solve(self, a, l, s):
+        key = (a, l, s)
+        if key in self.memo:
+            return self.memo[key]
+        if l == 1:
+            out = (0.0, 0)
+        elif s == 1:
+            acc = 0.0
+            for i in range(1, l):
+                acc += self.C(a, a + i)
+            out = (acc, 0)
+        else:
+            best = None
+            for m in range(1, l):
+                v = self.C(a, a + m) + self._solve(a + m, l - m, s - 1)[0] + self._solve(a, m, s)[0]
+                if best is None or v <= best[0]:
+                    best = (v, m)
+            out = best
+        self.memo[key] = out
+        return out
+
+
+def schedule_costs(n: int, s: int, costs, H: int = 0, I_min: int = 0) -> tuple[dict, list[tuple]]:
+    """The schedule of `schedule` (same mode, interval and slots) with every
+    reversal of [a, a+l) on k >= 2 slots split where WeightedSplits puts it
+    for the given step costs.  Equal costs give `schedule` itself."""
+    if len(costs) != n or any(not (c > 0) for c in costs):
+        raise ValueError("need n positive step costs")
+    head, _ = schedule(n, s, H, I_min)
+    ws = WeightedSplits(costs)
+    g = _Gen(n)
+    g.split = lambda a, l, k: ws.split(a, l, k)
+    if head["mode"] == "revolve":
+        g.emit("S", 0, 0)
+        g.live = 0
+        g.reverse(0, n, s, 0, list(range(1, s)))
+    else:
+        _two_level(g, n, s, list(range(0, n, head["I"])))
+    evals = sum(x[2] - x[1] for x in g.out if x[0] == "A") + 1
+    cost = sum(ws.C(x[1], x[2]) for x in g.out if x[0] == "A") + costs[n - 1]
+    return dict(head, evals=evals, cost=cost, split="cost"), g.out
+
+
+def text_costs(n: int, s: int, costs, H: int = 0, I_min: int = 0) -> str:
+    return _render(*schedule_costs(n, s, costs, H, I_min))
+
+
 def text_online(n: int, s: int, H: int = 0, I_min: int = 0) -> str:
     return _render(*schedule_online(n, s, H, I_min))
 
 
 def _render(head: dict, acts: list[tuple]) -> str:
-    lines = [f"ambptt-schedule v1 n={head['n']} s={head['s']} H={head['H']} I={head['I']} mode={head['mode']}"]
+    lines = [f"ambptt-schedule v1 n={head['n']} s={head['s']} H={head['H']} I={head['I']} mode={head['mode']}"
+             + (f" split={head['split']}" if head.get("split") else "")]
     lines += [" ".join(str(v) for v in a) for a in acts]
     return "\n".join(lines) + "\n"
 
@@ -440,7 +523,7 @@ def parse(txt: str) -> tuple[dict, list[tuple]]:
     head = {}
     for kv in f[2:]:
         k, v = kv.split("=")
-        head[k] = v if k == "mode" else int(v)
+        head[k] = v if k in ("mode", "split") else int(v)
     acts = []
     for ln in lines[1:]:
         p = ln.split()

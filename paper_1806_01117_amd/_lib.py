@@ -13,7 +13,8 @@ DTYPE = {"f32": 0, "bf16": 1}
 LOSS = {"half_sq_last": 0, "mean_sq_all": 1, "mean_last": 2}
 
 EXPORTS = ["ambptt_version", "ambptt_revolve_advances", "ambptt_schedule_evals", "ambptt_schedule_text",
-           "ambptt_schedule_text_starts", "ambptt_schedule_text_online", "ambptt_interval_from_timings",
+           "ambptt_schedule_text_starts", "ambptt_schedule_text_online", "ambptt_schedule_text_costs",
+           "ambptt_interval_from_timings", "ambptt_set_step_costs",
            "ambptt_resident_program", "ambptt_query", "ambptt_last_error",
            "ambptt_create", "ambptt_bind", "ambptt_set_int", "ambptt_set_file_tier", "ambptt_calibrate", "ambptt_run",
            "ambptt_last_schedule_text", "ambptt_destroy"]
@@ -35,7 +36,8 @@ class Stats(C.Structure):
                 ("compute_waits", C.c_int64), ("kernel_launches", C.c_int64),
                 ("recompute_factor", C.c_double), ("schedule_us", C.c_double), ("run_us", C.c_double), ("enqueue_us", C.c_double),
                 ("kernel_us", C.c_double * 6), ("kernel_samples", C.c_int64 * 6),
-                ("kernel_calls", C.c_int64 * 6), ("bytes_file_w", C.c_int64), ("bytes_file_r", C.c_int64)]
+                ("kernel_calls", C.c_int64 * 6), ("bytes_file_w", C.c_int64), ("bytes_file_r", C.c_int64),
+                ("forward_cost", C.c_double)]
 
     def as_dict(self) -> dict:
         d = {}
@@ -80,6 +82,10 @@ def load():
     L.ambptt_schedule_text_online.restype = C.c_int
     L.ambptt_interval_from_timings.argtypes = [C.c_double, C.c_double, i32, i32]
     L.ambptt_interval_from_timings.restype = i64
+    L.ambptt_schedule_text_costs.argtypes = [i64, i32, i64, i32, C.POINTER(C.c_double), C.c_char_p, sz, C.POINTER(sz)]
+    L.ambptt_schedule_text_costs.restype = C.c_int
+    L.ambptt_set_step_costs.argtypes = [vp, C.POINTER(C.c_double), i64]
+    L.ambptt_set_step_costs.restype = C.c_int
     L.ambptt_last_schedule_text.argtypes = [vp, C.c_char_p, sz, C.POINTER(sz)]
     L.ambptt_set_file_tier.argtypes = [vp, C.c_char_p, i64]
     L.ambptt_set_file_tier.restype = C.c_int

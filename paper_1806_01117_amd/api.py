@@ -71,6 +71,14 @@ def interval_from_timings(t_a_us: float, t_t_us: float, s: int, rule: int = 1) -
     return int(v)
 
 
+def schedule_text_costs(n: int, s: int, costs, H: int = 0, interval_min: int = 0) -> str:
+    """Canonical text of the schedule split for unequal step costs
+    (ambptt_schedule_text_costs)."""
+    L = load()
+    arr = (C.c_double * len(costs))(*[float(c) for c in costs])
+    return _text(lambda buf, cap, need: L.ambptt_schedule_text_costs(n, s, H, interval_min, arr, buf, cap, need))
+
+
 def schedule_text_online(n: int, s: int, H: int = 0, interval_min: int = 0) -> str:
     """Canonical text of the online checkpointing schedule for n steps
     (ambptt_schedule_text_online)."""
@@ -213,6 +221,14 @@ class Runner:
     def set_file_tier(self, directory: str, file_slots: int) -> None:
         """A file below the pinned host tier (ambptt_set_file_tier); 0 slots removes it."""
         check(self.L.ambptt_set_file_tier(self.ctx, str(directory).encode(), int(file_slots)))
+
+    def set_step_costs(self, costs) -> None:
+        """Relative forward costs of the n steps (ambptt_set_step_costs); None removes them."""
+        if costs is None:
+            check(self.L.ambptt_set_step_costs(self.ctx, None, 0))
+            return
+        arr = (C.c_double * len(costs))(*[float(c) for c in costs])
+        check(self.L.ambptt_set_step_costs(self.ctx, arr, len(costs)))
 
     def last_schedule_text(self) -> str:
         """The canonical text of the schedule the last run executed."""

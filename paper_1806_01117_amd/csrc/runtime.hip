@@ -240,6 +240,11 @@ struct ambptt_ctx {
   int store_policy = 0;  // 0: every I-th state; 1: the next state once the previous store has completed
   bool online = false;   // online checkpointing: placement decided without knowing n
   int interval_rule = 1;  // 0: smallest I with T_T <= I T_A; 1: I minimising the modelled time per step
+  std::vector<double> step_costs;  // relative forward step costs (empty: equal)
+  double plan_cost = 0.0;          // cost of the forward evaluations of the last plan built
+  Plan cost_plan;                  // the plan for step_costs, kept while its inputs stay the same
+  int64_t cost_plan_key[3] = {-1, -1, -1};  // interval_min, slow capacity, costs version
+  int64_t costs_version = 0;
   bool hadj_launch = true;  // fp32 large-batch path: the adjoint's h-adjoint product as a launch of its own
   int host_waits = -1;      // slot dependencies on host-tier copies: 1 waited for on the host, 0 stream waits, -1 by path
   hipEvent_t ev_end[8] = {};  // end events recorded by compute dispatches (host-tier copies and sweep pacing wait on them)
@@ -281,10 +286,18 @@ int64_t interval_from_timings(double ta, double tt, int64_t s, int rule, double 
 }
 
 // The schedule a pass runs: the online one when the context asks for it.
-Plan pass_plan(const ambptt_ctx* C) {
+Plan pass_plan(ambptt_ctx* C) {
   const ambptt_problem& p = C->p;
   const int64_t I = std::max<int64_t>(C->interval_min, 1);
   if (C->online) return make_plan_online(p.n_steps, p.fast_slots, p.slow_slots, I);
+  if (!C->step_costs.empty()) {  // the dynamic program runs once per set of inputs
+    const int64_t key[3] = {I, slow_capacity(C), C->costs_version};
+    if (!std::equal(key, key + 3, C->cost_plan_key)) {
+      C->cost_plan = make_plan_costs(p.n_steps, p.fast_slots, key[1], I, C->step_costs, &C->plan_cost);
+      std::copy(key, key + 3, C->cost_plan_key);
+    }
+    return C->cost_plan;
+  }
   return make_plan(p.n_steps, p.fast_slots, slow_capacity(C), I);
 }
 
@@ -1037,6 +1050,8 @@ ambptt_status resident_run(ambptt_ctx* C, const void* x_seq, const void* W, cons
     plan = pass_plan(C);
     prog = compile_resident(plan, p.fast_slots, C->elide_prefetch, &rc);
     if (C->res_test_stall) prog.insert(prog.begin(), {kPCopy, INT32_MAX, p.fast_slots, p.fast_slots + 1});
+  } catch (const std::length_error& e) {
+    return fail(AMBPTT_EUNSUPPORTED, e.what());
   } catch (const std::exception& e) {
     return fail(AMBPTT_EINTERNAL, e.what());
   }
@@ -1084,6 +1099,7 @@ ambptt_status resident_run(ambptt_ctx* C, const void* x_seq, const void* W, cons
     st.compute_waits = 0;
     st.kernel_launches = 6;
     st.recompute_factor = double(rc.forward_evals) / double(p.n_steps);
+    st.forward_cost = plan.weighted ? C->plan_cost : double(rc.forward_evals);
     st.schedule_us = t1 - t0;
     st.run_us = t2 - t1;
     st.enqueue_us = t_enq - t1;
@@ -1138,6 +1154,46 @@ ambptt_status ambptt_schedule_text(int64_t n, int32_t s, int64_t H, int32_t inte
     if (!buf || cap < t.size() + 1) return fail(AMBPTT_EINVAL, "schedule: buffer too small");
     std::memcpy(buf, t.c_str(), t.size() + 1);
     return AMBPTT_OK;
+  } catch (const std::exception& e) {
+    return fail(AMBPTT_EINTERNAL, e.what());
+  }
+}
+
+static bool costs_ok(const double* costs, int64_t n) {
+  for (int64_t t = 0; t < n; ++t)
+    if (!(costs[t] > 0.0) || !(costs[t] < 1e300)) return false;
+  return true;
+}
+
+ambptt_status ambptt_set_step_costs(ambptt_ctx* C, const double* costs, int64_t n) {
+  if (!C) return fail(AMBPTT_EINVAL, "ctx is NULL");
+  if (!costs || n == 0) {
+    C->step_costs.clear();
+    return AMBPTT_OK;
+  }
+  if (n != C->p.n_steps) return fail(AMBPTT_EINVAL, "step costs: need one cost per step of the problem");
+  if (!costs_ok(costs, n)) return fail(AMBPTT_EINVAL, "step costs must be positive and finite");
+  if (C->online) return fail(AMBPTT_EINVAL, "online checkpointing and step costs exclude each other");
+  if (C->store_policy == 1) return fail(AMBPTT_EINVAL, "store_policy 1 and step costs exclude each other");
+  C->step_costs.assign(costs, costs + n);
+  C->costs_version++;
+  return AMBPTT_OK;
+}
+
+ambptt_status ambptt_schedule_text_costs(int64_t n, int32_t s, int64_t H, int32_t interval_min, const double* costs,
+                                         char* buf, size_t cap, size_t* needed) {
+  if (n < 1 || s < 1 || H < 0 || interval_min < 0 || !costs) return fail(AMBPTT_EINVAL, "schedule: bad arguments");
+  if (!costs_ok(costs, n)) return fail(AMBPTT_EINVAL, "step costs must be positive and finite");
+  try {
+    const std::string t = plan_text(make_plan_costs(n, s, H, interval_min, std::vector<double>(costs, costs + n), nullptr));
+    if (needed) *needed = t.size() + 1;
+    if (!buf || cap < t.size() + 1) return fail(AMBPTT_EINVAL, "schedule: buffer too small");
+    std::memcpy(buf, t.c_str(), t.size() + 1);
+    return AMBPTT_OK;
+  } catch (const std::length_error& e) {
+    return fail(AMBPTT_EUNSUPPORTED, e.what());
+  } catch (const std::invalid_argument& e) {
+    return fail(AMBPTT_EINVAL, e.what());
   } catch (const std::exception& e) {
     return fail(AMBPTT_EINTERNAL, e.what());
   }
@@ -1276,6 +1332,7 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
     if (v < 0 || v > 1) return fail(AMBPTT_EINVAL, "store_policy must be 0 (every I-th state) or 1 (when the previous store completed)");
     if (v == 1 && C->path_opt == 2) return fail(AMBPTT_EUNSUPPORTED, "store_policy 1 runs on the per-step path only");
     if (v == 1 && C->online) return fail(AMBPTT_EINVAL, "store_policy 1 and online checkpointing exclude each other");
+    if (v == 1 && !C->step_costs.empty()) return fail(AMBPTT_EINVAL, "store_policy 1 and step costs exclude each other");
     C->store_policy = int(v);
   } else if (k == "interval_rule") {
     if (v < 0 || v > 1) return fail(AMBPTT_EINVAL, "interval_rule must be 0 (ceil(T_T / T_A)) or 1 (least modelled time)");
@@ -1285,6 +1342,7 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
     if (v == 1 && C->store_policy == 1)
       return fail(AMBPTT_EINVAL, "store_policy 1 and online checkpointing exclude each other");
     if (v == 1 && C->ftier) return fail(AMBPTT_EUNSUPPORTED, "online checkpointing does not run over a file tier");
+    if (v == 1 && !C->step_costs.empty()) return fail(AMBPTT_EINVAL, "online checkpointing and step costs exclude each other");
     C->online = v != 0;
   } else if (k == "dw_stream") {
     if (v < -1 || v > 1) return fail(AMBPTT_EINVAL, "dw_stream must be -1 (by path), 0 or 1");
@@ -1442,6 +1500,8 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   Plan plan;
   try {
     plan = pass_plan(C);
+  } catch (const std::length_error& e) {
+    return fail(AMBPTT_EUNSUPPORTED, e.what());
   } catch (const std::exception& e) {
     return fail(AMBPTT_EINTERNAL, e.what());
   }
@@ -1526,6 +1586,7 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
     st.n_steps = p.n_steps;
     st.actions = (int64_t)plan.acts.size();
     st.recompute_factor = double(st.forward_evals) / double(p.n_steps);
+    st.forward_cost = plan.weighted ? C->plan_cost : double(st.forward_evals);
     st.schedule_us = t1 - t0;
     st.run_us = t2 - t1;
     st.enqueue_us = t_enq - t1;

@@ -25,6 +25,7 @@
 #include <functional>
 #include <queue>
 #include <stdexcept>
+#include <unordered_map>
 
 namespace ambptt {
 
@@ -90,6 +91,8 @@ struct Builder {
   std::vector<Action>* out;
   int64_t live = 0;
   std::vector<char> busy;  // fast slot occupied by an active snapshot
+  // split of a reversal of [a, a + l) with s >= 2 slots (default: Revolve's largest optimal one)
+  std::function<int64_t(int64_t, int64_t, int64_t)> split;
 
   void push(Op op, int64_t a, int64_t b = 0, int64_t c = 0) { out->push_back({op, a, b, c}); }
   void turn(int64_t t) { push(t == n - 1 ? Op::First : Op::Youturn, t); }
@@ -128,7 +131,7 @@ struct Builder {
         }
         return;
       }
-      const int64_t m = revolve_split(l, s);
+      const int64_t m = split ? split(a, l, s) : revolve_split(l, s);
       restore(base, a);
       advance(a, a + m);
       const int64_t k = take_slot();
@@ -379,12 +382,98 @@ Plan make_plan_online(int64_t n, int32_t s, int64_t H, int64_t interval_min) {
   return p;
 }
 
+namespace {
+
+// Least cost of reversing [a, a + l) with k slots for unequal step costs, and
+// the split that reaches it.  Queries come top-down, one reversal at a time:
+// a query outside the current root reversal fills a new table for that root,
+// bottom-up over (k, l, a), dense and indexed by (a - a0, l, k).
+class WeightedSplits {
+ public:
+  WeightedSplits(const std::vector<double>& costs, int64_t max_table) : max_table_(max_table) {
+    pre_.assign(costs.size() + 1, 0.0);
+    for (size_t t = 0; t < costs.size(); ++t) pre_[t + 1] = pre_[t] + costs[t];
+  }
+  double C(int64_t a, int64_t b) const { return pre_[size_t(b)] - pre_[size_t(a)]; }
+  int64_t split(int64_t a, int64_t l, int64_t k) {
+    if (!(a >= a0_ && a + l <= a0_ + L_ && k <= K_)) fill(a, l, k);
+    return m_[idx(a, l, k)];
+  }
+
+ private:
+  size_t idx(int64_t a, int64_t l, int64_t k) const { return size_t(((a - a0_) * (L_ + 1) + l) * (K_ + 1) + k); }
+  void fill(int64_t a0, int64_t L, int64_t K) {
+    if (L * (L + 1) * (K + 1) > max_table_) throw std::length_error("schedule: cost table too large");
+    a0_ = a0, L_ = L, K_ = K;
+    v_.assign(size_t(L * (L + 1) * (K + 1)), 0.0);
+    m_.assign(v_.size(), 0);
+    // one slot: restore x_a and advance i steps for i = l-1 .. 1, summed in increasing i
+    for (int64_t a = a0; a < a0 + L; ++a)
+      for (int64_t l = 2; a + l <= a0 + L; ++l) v_[idx(a, l, 1)] = v_[idx(a, l - 1, 1)] + C(a, a + l - 1);
+    for (int64_t k = 2; k <= K; ++k)
+      for (int64_t l = 2; l <= L; ++l)
+        for (int64_t a = a0; a + l <= a0 + L; ++a) {
+          double best = 0.0;
+          int64_t bm = -1;
+          for (int64_t m = 1; m < l; ++m) {
+            const double v = C(a, a + m) + v_[idx(a + m, l - m, k - 1)] + v_[idx(a, m, k)];
+            if (bm < 0 || v <= best) best = v, bm = m;
+          }
+          v_[idx(a, l, k)] = best;
+          m_[idx(a, l, k)] = int32_t(bm);
+        }
+  }
+  std::vector<double> pre_;
+  std::vector<double> v_;
+  std::vector<int32_t> m_;
+  int64_t a0_ = 0, L_ = 0, K_ = 0, max_table_;
+};
+
+}  // namespace
+
+Plan make_plan_costs(int64_t n, int32_t s, int64_t H, int64_t interval_min, const std::vector<double>& costs,
+                     double* cost_out, int64_t max_table) {
+  if (int64_t(costs.size()) != n) throw std::invalid_argument("schedule: need one cost per step");
+  for (double c : costs)
+    if (!(c > 0.0) || !(c < 1e300)) throw std::invalid_argument("schedule: step costs must be positive and finite");
+  Plan p;
+  p.n = n;
+  p.s = s;
+  p.H = H;
+  plan_counts(n, s, H, interval_min, &p.async, &p.interval, &p.evals);
+  p.weighted = true;
+  WeightedSplits ws(costs, max_table);
+  Builder b{n, &p.acts, 0, std::vector<char>(size_t(s), 0), {}};
+  b.split = [&ws](int64_t a, int64_t l, int64_t k) { return ws.split(a, l, k); };
+  if (!p.async) {
+    b.push(Op::Snap, 0, 0);
+    b.busy[0] = 1;
+    b.reverse(0, n, s, 0);
+  } else {
+    std::vector<int64_t> starts;
+    for (int64_t t = 0; t < n; t += p.interval) starts.push_back(t);
+    two_level(b, s, starts);
+    p.host_slots_used = int64_t(starts.size()) - 1;
+  }
+  p.evals = 1;
+  double cost = 0.0;
+  for (const Action& x : p.acts)
+    if (x.op == Op::Advance) {
+      p.evals += x.b - x.a;
+      cost += ws.C(x.a, x.b);
+    }
+  cost += costs[size_t(n - 1)];
+  if (cost_out) *cost_out = cost;
+  return p;
+}
+
 std::string plan_text(const Plan& p) {
   std::string t;
   t.reserve(p.acts.size() * 12 + 96);
   t += "ambptt-schedule v1 n=" + std::to_string(p.n) + " s=" + std::to_string(p.s) +
        " H=" + std::to_string(p.H) + " I=" + std::to_string(p.dynamic ? 0 : p.interval) +
-       " mode=" + (p.online ? "online" : p.dynamic ? "dynamic" : p.async ? "async" : "revolve") + "\n";
+       " mode=" + (p.online ? "online" : p.dynamic ? "dynamic" : p.async ? "async" : "revolve") +
+       (p.weighted ? " split=cost" : "") + "\n";
   char line[96];
   for (const Action& x : p.acts) {
     int len = 0;

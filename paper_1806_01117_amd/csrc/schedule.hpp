@@ -28,6 +28,7 @@ struct Plan {
   bool async = false;
   bool dynamic = false;  // interval starts decided during the sweep
   bool online = false;   // placement decided without knowing n (interval = the first I)
+  bool weighted = false; // splits chosen for unequal step costs
   int64_t evals = 0;     // forward-step evaluations
   int64_t host_slots_used = 0;
   std::vector<Action> acts;
@@ -81,6 +82,21 @@ class OnlinePlacement {
   int64_t m_, a_, r_ = 1;
   std::vector<int64_t> held_;
 };
+
+// The schedule of make_plan (same mode, interval and slots) with every
+// reversal of l >= 2 steps on k >= 2 slots split where it costs least for
+// forward steps of unequal cost (costs[t] > 0 for step t), by dynamic
+// programming over the same recursion:
+//   T(a, 1, k) = 0,  T(a, l, 1) = sum_{i=1}^{l-1} C(a, a+i),
+//   T(a, l, k) = min_m C(a, a+m) + T(a+m, l-m, k-1) + T(a, m, k),
+// C(a, b) the cost of steps a .. b-1, ties to the largest m (equal costs give
+// make_plan's schedule).  The table of one reversal of l steps on k slots has
+// l (l + 1) (k + 1) entries and takes about l^3 k / 6 operations.
+// *cost_out (nullable) receives the cost of every forward evaluation of the
+// schedule.  Throws std::invalid_argument on bad arguments and
+// std::length_error when a reversal's table would exceed max_table entries.
+Plan make_plan_costs(int64_t n, int32_t s, int64_t H, int64_t interval_min, const std::vector<double>& costs,
+                     double* cost_out, int64_t max_table = int64_t(1) << 20);
 
 // Mode, interval and forward evaluations only (no action list).
 void plan_counts(int64_t n, int32_t s, int64_t H, int64_t interval_min, bool* async,

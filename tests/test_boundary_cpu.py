@@ -110,8 +110,8 @@ def test_stats_struct_layout(amb):
     st.kernel_us[2] = 1.5
     d = st.as_dict()
     assert d["kernel_launches"] == 7 and d["kernel_us"][2] == 1.5 and len(d["kernel_calls"]) == 6
-    # int32 x4, int64 x14, double x4, double x6, int64 x12, int64 x2 (file tier)
-    assert ctypes.sizeof(_lib.Stats) == 16 + 14 * 8 + 4 * 8 + 6 * 8 + 12 * 8 + 2 * 8
+    # int32 x4, int64 x14, double x4, double x6, int64 x12, int64 x2 (file tier), double (forward cost)
+    assert ctypes.sizeof(_lib.Stats) == 16 + 14 * 8 + 4 * 8 + 6 * 8 + 12 * 8 + 2 * 8 + 8
     assert ctypes.sizeof(_lib.Problem) == 48
 
 
