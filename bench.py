@@ -57,6 +57,40 @@ def weighted_cost(text: str, costs) -> float:
     return float(tot)
 
 
+def copy_overlap(spec, st, stats, dev, wall_ms: float) -> dict:
+    """Host-link rate of one state's copy (hipMemcpyAsync between HBM and
+    pinned host memory, timed alone) and a lower bound on the overlap of the
+    pass's copies with compute: the compute stream can be idle while a copy
+    is pending for at most the wall time not covered by kernel execution, so
+    overlap >= 1 - (wall - kernel time) / (copy count x copy time)."""
+    import numpy as np
+    import torch
+    nbytes = (st["bytes_d2h"] // st["stores"]) if st["stores"] else (st["bytes_h2d"] // max(1, st["prefetches"]))
+    d = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    h = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    rates = {}
+    for name, (dst, src) in (("d2h", (h, d)), ("h2d", (d, h))):
+        best = None
+        for _ in range(6):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            dst.copy_(src, non_blocking=True)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1)
+            best = ms if best is None else min(best, ms)
+        rates[name] = best
+    n_st, n_pf = st["stores"], st["prefetches"] - st["prefetches_elided"]
+    copy_ms = n_st * rates["d2h"] + n_pf * rates["h2d"]
+    kernel_ms = float(np.mean([sum(s_["kernel_us"][i] * s_["kernel_calls"][i] for i in range(6)) for s_ in stats])) / 1e3
+    idle_ms = max(0.0, wall_ms - kernel_ms)
+    return {"state_bytes": nbytes, "d2h_us": round(1000 * rates["d2h"], 2), "h2d_us": round(1000 * rates["h2d"], 2),
+            "d2h_gb_s": round(nbytes / rates["d2h"] / 1e6, 2), "h2d_gb_s": round(nbytes / rates["h2d"] / 1e6, 2),
+            "copies": n_st + n_pf, "copy_ms_per_pass": round(copy_ms, 2),
+            "kernel_ms_per_pass": round(kernel_ms, 2), "wall_ms_per_pass": round(wall_ms, 2),
+            "overlap_lower_bound": round(1.0 - idle_ms / copy_ms, 4) if copy_ms > 0 else None}
+
+
 def step_flops(spec, window: int, wide: bool = False) -> dict:
     """Algorithmic flops of one launch of each per-step kernel, and of the
     three products of one step (gate GEMM, h-adjoint, weight gradient).  On
@@ -489,6 +523,8 @@ def main() -> int:
                      "bytes_per_launch": int(byts[dom]),
                      "flop_per_byte": round(flops[dom] / max(byts[dom], 1), 1)},
     }
+    if not resident and (st["stores"] or st["prefetches"]):
+        line["transfer_overlap"] = copy_overlap(spec, st, stats, dev, 1000.0 * el / args.steps)
     if costs is not None:
         # the same pass with Revolve's own splits, weighed with the same costs
         plain = amb.schedule_text(wl.n_steps, spec.fast_slots, host_slots, max(I_min, 1))
