@@ -402,6 +402,23 @@ def main() -> int:
         bitwise = fingerprint(rvo) == fp_async
         print(f"plain Revolve done, bit-identical gradients: {bitwise}", file=sys.stderr, flush=True)
         rv.close()
+    # store-all in HBM (a slot for every state: no recomputation, no host tier),
+    # same path, where the slot pool fits in a quarter of the HBM
+    sa = None
+    n_state = amb.query(spec)[0]
+    if args.compare and wl.n_steps * n_state <= 72 * 2 ** 30:
+        sr = amb.Runner(amb.ProblemSpec.from_workload(wl, fast_slots=wl.n_steps, slow_slots=0), device=dev)
+        sr.set("path", 2 if resident else 1)
+        sr.set("resident_cooperative", args.cooperative)
+        sa_value, sao = other_run(sr, reps if args.steps > 1 else 1, warm=args.steps > 1)
+        sa = {"value": round(sa_value, 2), "unit": "timesteps/s",
+              "recompute_factor": round(sao["stats"]["recompute_factor"], 4),
+              "bit_identical_gradients": fingerprint(sao) == fp_async,
+              "slot_pool_gb": round(wl.n_steps * n_state / 2 ** 30, 2)}
+        print(f"store-all done, bit-identical gradients: {sa['bit_identical_gradients']}", file=sys.stderr, flush=True)
+        sr.close()
+        del sr, sao
+        torch.cuda.empty_cache()
     # the same schedule with one kernel launch per step (the other execution path)
     alt = None
     if resident and args.compare:
@@ -506,6 +523,7 @@ def main() -> int:
         "plain_revolve": None if rv_st is None else {
             "value": round(rv_value, 2), "unit": "timesteps/s",
             "recompute_factor": round(rv_st["recompute_factor"], 4), "bit_identical_gradients": bitwise},
+        "store_all": sa,
         "path": "resident" if resident else "steps",
         "per_step_launches": alt,
         "kernel_us": {k: round(v[0], 3) for k, v in kern.items()},
