@@ -310,7 +310,7 @@ def main() -> int:
     args = ap.parse_args()
     knobs = [(k, int(v)) for k, v in (kv.split("=", 1) for kv in args.set)]
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
+        print("bench.py measures one GPU: the library has no multi-GPU path "
               "(--gpus must be 1)", file=sys.stderr)
         return 2
 
