@@ -111,3 +111,35 @@ def test_online_refuses_other_policies():
             r.set("online", 2)
     finally:
         r.close()
+
+
+def test_online_lstm512_full_workload():
+    """The bench workload (1000 steps, B 64, D 256, H 512, 10 slots, a host
+    slot per step) under online checkpointing on the resident kernel: the
+    oracle within tolerance, plain Revolve at the same 10 slots bit for bit."""
+    wl = synth.get("lstm_h512_t1000")
+    host, dev = _case(wl)
+    want = run_oracle(wl, *host)
+    got = run_gpu(wl, dev, path=2, interval_min=1, opts=ONLINE)
+    _check_online(got, 1000, 10, 1000, 1)
+    assert got["stats"]["recompute_factor"] == 1.0
+    assert_close(got, want, TOL_F32)
+    assert_bitwise(got, run_gpu(wl, dev, path=2, slow_slots=0))
+
+
+@pytest.mark.parametrize("rule", [0, 1])
+def test_calibrated_interval_follows_the_rule(rule):
+    """On the per-step path the calibrated interval is the rule's for the
+    T_A and T_T that the calibration reports."""
+    import paper_1806_01117_amd as amb
+    wl = synth.get("lstm_h2048_bf16_t10000").with_(batch=64, input=64, hidden=128, n_steps=40, name="lstm_calib")
+    host, dev = _case(wl)
+    r = amb.Runner(amb.ProblemSpec.from_workload(wl, fast_slots=4, slow_slots=40, interval_min=0))
+    try:
+        r.set("interval_rule", rule)
+        I, ta, tt = r.calibrate(*dev)
+    finally:
+        r.close()
+    assert ta > 0 and tt > 0
+    assert I == amb.interval_from_timings(ta, tt, 4, rule)
+    assert 1 <= I <= max(1, -(-tt // ta))
