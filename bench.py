@@ -520,6 +520,11 @@ def main() -> int:
                                      "bytes_written": st["bytes_file_w"], "bytes_read": st["bytes_file_r"]}}
                       if args.file_tier else {})},
         "recompute_factor": round(st["recompute_factor"], 4),
+        # Section 3's model: R(n, s) for Revolve, R(I, s) for the two-level
+        # policy (the model leaves out the sweep that the count above includes)
+        "paper_model": {"revolve_R": round((amb.revolve_advances(wl.n_steps, spec.fast_slots) + 1) / wl.n_steps, 4),
+                        "async_R": round((amb.revolve_advances(st["interval"], spec.fast_slots) + 1) / st["interval"], 4)
+                        if st["interval"] > 0 else None},
         "plain_revolve": None if rv_st is None else {
             "value": round(rv_value, 2), "unit": "timesteps/s",
             "recompute_factor": round(rv_st["recompute_factor"], 4), "bit_identical_gradients": bitwise},

@@ -149,6 +149,14 @@ def revolve_evals(n: int, s: int) -> int:
     return advances(n, s) + 1
 
 
+def paper_model_R(n: int, s: int) -> float:
+    """The recompute factor of the paper's performance model (Section 3):
+    R(n, s) for plain Revolve over n steps; the model's asynchronous factor
+    is R(I, s), the same function at the interval length (it leaves out the
+    sweep that produces the stored states, which the schedules here count)."""
+    return revolve_evals(n, s) / n
+
+
 def choose(n: int, s: int, H: int, I_min: int) -> tuple[str, int, int]:
     """(mode, I, forward evaluations) under the policy above."""
     plain = revolve_evals(n, s)

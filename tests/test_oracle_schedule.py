@@ -225,3 +225,27 @@ def test_chosen_starts_edge_cases():
             S.schedule_from_starts(7, 3, 2, bad)
     with pytest.raises(ValueError):
         S.schedule_from_starts(7, 1, 2, [0, 3])
+
+
+def test_paper_model_figure():
+    """Section 3's model and its figure (s = 100; classic Revolve against
+    intervals I = 8, 64, 1024; only the axis, 0 to 5, is printed): intervals
+    of at most s + 1 steps need no recomputation; R(I, s) never exceeds
+    R(n, s) for n >= I; Revolve's factor grows with n and stays inside the
+    figure's axis up to a million steps; the schedules' own count of a
+    two-level pass, which includes the sweep, is never below the model's."""
+    s = 100
+    assert S.paper_model_R(8, s) == 1.0 and S.paper_model_R(64, s) == 1.0
+    r1024 = S.paper_model_R(1024, s)
+    assert 1.0 < r1024 < 2.0
+    prev = 0.0
+    for n in (10 ** 3, 10 ** 4, 10 ** 5, 10 ** 6):
+        r = S.paper_model_R(n, s)
+        assert r >= prev and r <= 5.0
+        assert S.paper_model_R(1024, s) <= r or n < 1024
+        prev = r
+    assert abs(S.paper_model_R(10 ** 6, s) - 3.818) < 5e-4
+    for n in (2000, 10 ** 4):
+        for I in (8, 64, 1024):
+            head, _ = S.schedule(n, s, n, I)
+            assert head["evals"] / n >= S.paper_model_R(I, s) - 1e-12
