@@ -145,3 +145,17 @@ def test_c_abi_matches_oracle_bytewise():
         assert amb.schedule_text_costs(n, s, costs, H, I) == S.text_costs(n, s, costs, H, I), (n, s, H, I)
     with pytest.raises(amb.AmbpttError):
         amb.schedule_text_costs(3, 2, [1.0, 0.0, 1.0])
+
+
+def test_c_abi_cost_errors():
+    import math
+    with pytest.raises(amb.AmbpttError, match="positive"):
+        amb.schedule_text_costs(4, 2, [1.0, math.nan, 1.0, 1.0])
+    with pytest.raises(amb.AmbpttError, match="positive"):
+        amb.schedule_text_costs(4, 2, [1.0, math.inf, 1.0, 1.0])
+    # one reversal of 400 steps on 10 slots: 400 * 401 * 11 entries exceed the table limit
+    with pytest.raises(amb.AmbpttError, match="too large"):
+        amb.schedule_text_costs(400, 10, [1.0] * 400)
+    # the same steps in two levels: the intervals are the reversals
+    txt = amb.schedule_text_costs(400, 10, [1.0] * 400, 400, 4)
+    assert txt.startswith("ambptt-schedule v1 n=400 s=10 H=400 I=4 mode=async split=cost")
