@@ -305,8 +305,9 @@ ambptt_status ambptt_set_file_tier(ambptt_ctx* ctx, const char* dir, int64_t fil
  * recursion finds the least total cost of recomputed forward steps
  * (ambptt_schedule_text_costs); the mode, interval and slots stay those of
  * the uniform schedule, and equal costs give it exactly.  The costs are
- * copied.  EINVAL if n differs from the problem's, a cost is not positive
- * and finite, or "online" or "store_policy" 1 is set.  The dynamic program
+ * copied; with "store_policy" 1 the reversals of the intervals the sweep
+ * chose are split for them too.  EINVAL if n differs from the problem's, a
+ * cost is not positive and finite, or "online" is set.  The dynamic program
  * of a reversal of l steps on k slots keeps l (l + 1) (k + 1) entries and
  * takes about l^3 k / 6 operations; a pass whose schedule holds a reversal
  * over 1 Mi entries (single-level Revolve over ~300 steps with 10 slots;

@@ -276,16 +276,26 @@ def dynamic_evals(n: int, s: int, starts: list[int]) -> int:
     return starts[-1] + sum(advances(e - a, s - 1) for a, e in zip(starts, ends)) + 1
 
 
-def schedule_from_starts(n: int, s: int, H: int, starts: list[int]) -> tuple[dict, list[tuple]]:
+def schedule_from_starts(n: int, s: int, H: int, starts: list[int], costs=None) -> tuple[dict, list[tuple]]:
     """(header dict, action list) of the two-level policy with interval starts
-    decided during the sweep (stores whenever the previous one completed)."""
+    decided during the sweep (stores whenever the previous one completed);
+    with step costs every reversal is split by WeightedSplits."""
     starts = list(starts)
     if n < 1 or s < 2 or not starts or starts[0] != 0 or any(b <= a for a, b in zip(starts, starts[1:])) \
             or starts[-1] >= n or len(starts) - 1 > H:
         raise ValueError("need s >= 2 and starts 0 = t_0 < t_1 < ... < n with at most H + 1 of them")
     g = _Gen(n)
+    if costs is not None:
+        if len(costs) != n or any(not (c > 0) for c in costs):
+            raise ValueError("need n positive step costs")
+        ws = WeightedSplits(costs)
+        g.split = lambda a, l, k: ws.split(a, l, k)
     _two_level(g, n, s, starts)
     head = {"n": n, "s": s, "H": H, "I": 0, "mode": "dynamic", "evals": dynamic_evals(n, s, starts)}
+    if costs is not None:
+        head["evals"] = sum(x[2] - x[1] for x in g.out if x[0] == "A") + 1
+        head["cost"] = sum(ws.C(x[1], x[2]) for x in g.out if x[0] == "A") + costs[n - 1]
+        head["split"] = "cost"
     return head, g.out
 
 
@@ -519,8 +529,8 @@ def text(n: int, s: int, H: int = 0, I_min: int = 0) -> str:
     return _render(*schedule(n, s, H, I_min))
 
 
-def text_from_starts(n: int, s: int, H: int, starts: list[int]) -> str:
-    return _render(*schedule_from_starts(n, s, H, starts))
+def text_from_starts(n: int, s: int, H: int, starts: list[int], costs=None) -> str:
+    return _render(*schedule_from_starts(n, s, H, starts, costs))
 
 
 def parse(txt: str) -> tuple[dict, list[tuple]]:

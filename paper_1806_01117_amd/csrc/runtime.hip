@@ -1174,7 +1174,6 @@ ambptt_status ambptt_set_step_costs(ambptt_ctx* C, const double* costs, int64_t 
   if (n != C->p.n_steps) return fail(AMBPTT_EINVAL, "step costs: need one cost per step of the problem");
   if (!costs_ok(costs, n)) return fail(AMBPTT_EINVAL, "step costs must be positive and finite");
   if (C->online) return fail(AMBPTT_EINVAL, "online checkpointing and step costs exclude each other");
-  if (C->store_policy == 1) return fail(AMBPTT_EINVAL, "store_policy 1 and step costs exclude each other");
   C->step_costs.assign(costs, costs + n);
   C->costs_version++;
   return AMBPTT_OK;
@@ -1332,7 +1331,6 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
     if (v < 0 || v > 1) return fail(AMBPTT_EINVAL, "store_policy must be 0 (every I-th state) or 1 (when the previous store completed)");
     if (v == 1 && C->path_opt == 2) return fail(AMBPTT_EUNSUPPORTED, "store_policy 1 runs on the per-step path only");
     if (v == 1 && C->online) return fail(AMBPTT_EINVAL, "store_policy 1 and online checkpointing exclude each other");
-    if (v == 1 && !C->step_costs.empty()) return fail(AMBPTT_EINVAL, "store_policy 1 and step costs exclude each other");
     C->store_policy = int(v);
   } else if (k == "interval_rule") {
     if (v < 0 || v > 1) return fail(AMBPTT_EINVAL, "interval_rule must be 0 (ceil(T_T / T_A)) or 1 (least modelled time)");
@@ -1541,7 +1539,8 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
     std::vector<int64_t> starts;
     if ((s = E.dynamic_sweep(starts, dW, db)) != AMBPTT_OK) return s;
     try {
-      plan = make_plan_starts(p.n_steps, p.fast_slots, slow_capacity(C), starts);
+      plan = make_plan_starts(p.n_steps, p.fast_slots, slow_capacity(C), starts,
+                              C->step_costs.empty() ? nullptr : &C->step_costs, &C->plan_cost);
     } catch (const std::exception& e) {
       return fail(AMBPTT_EINTERNAL, e.what());
     }

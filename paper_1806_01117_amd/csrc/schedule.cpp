@@ -23,6 +23,7 @@
 #include <algorithm>
 #include <cstdio>
 #include <functional>
+#include <memory>
 #include <queue>
 #include <stdexcept>
 #include <unordered_map>
@@ -169,6 +170,55 @@ void two_level(Builder& b, int32_t s, const std::vector<int64_t>& starts) {
 
 }  // namespace
 
+namespace {
+
+// Least cost of reversing [a, a + l) with k slots for unequal step costs, and
+// the split that reaches it.  Queries come top-down, one reversal at a time:
+// a query outside the current root reversal fills a new table for that root,
+// bottom-up over (k, l, a), dense and indexed by (a - a0, l, k).
+class WeightedSplits {
+ public:
+  WeightedSplits(const std::vector<double>& costs, int64_t max_table) : max_table_(max_table) {
+    pre_.assign(costs.size() + 1, 0.0);
+    for (size_t t = 0; t < costs.size(); ++t) pre_[t + 1] = pre_[t] + costs[t];
+  }
+  double C(int64_t a, int64_t b) const { return pre_[size_t(b)] - pre_[size_t(a)]; }
+  int64_t split(int64_t a, int64_t l, int64_t k) {
+    if (!(a >= a0_ && a + l <= a0_ + L_ && k <= K_)) fill(a, l, k);
+    return m_[idx(a, l, k)];
+  }
+
+ private:
+  size_t idx(int64_t a, int64_t l, int64_t k) const { return size_t(((a - a0_) * (L_ + 1) + l) * (K_ + 1) + k); }
+  void fill(int64_t a0, int64_t L, int64_t K) {
+    if (L * (L + 1) * (K + 1) > max_table_) throw std::length_error("schedule: cost table too large");
+    a0_ = a0, L_ = L, K_ = K;
+    v_.assign(size_t(L * (L + 1) * (K + 1)), 0.0);
+    m_.assign(v_.size(), 0);
+    // one slot: restore x_a and advance i steps for i = l-1 .. 1, summed in increasing i
+    for (int64_t a = a0; a < a0 + L; ++a)
+      for (int64_t l = 2; a + l <= a0 + L; ++l) v_[idx(a, l, 1)] = v_[idx(a, l - 1, 1)] + C(a, a + l - 1);
+    for (int64_t k = 2; k <= K; ++k)
+      for (int64_t l = 2; l <= L; ++l)
+        for (int64_t a = a0; a + l <= a0 + L; ++a) {
+          double best = 0.0;
+          int64_t bm = -1;
+          for (int64_t m = 1; m < l; ++m) {
+            const double v = C(a, a + m) + v_[idx(a + m, l - m, k - 1)] + v_[idx(a, m, k)];
+            if (bm < 0 || v <= best) best = v, bm = m;
+          }
+          v_[idx(a, l, k)] = best;
+          m_[idx(a, l, k)] = int32_t(bm);
+        }
+  }
+  std::vector<double> pre_;
+  std::vector<double> v_;
+  std::vector<int32_t> m_;
+  int64_t a0_ = 0, L_ = 0, K_ = 0, max_table_;
+};
+
+}  // namespace
+
 Plan make_plan(int64_t n, int32_t s, int64_t H, int64_t interval_min) {
   Plan p;
   p.n = n;
@@ -189,26 +239,37 @@ Plan make_plan(int64_t n, int32_t s, int64_t H, int64_t interval_min) {
   return p;
 }
 
-Plan make_plan_starts(int64_t n, int32_t s, int64_t H, const std::vector<int64_t>& starts) {
+Plan make_plan_starts(int64_t n, int32_t s, int64_t H, const std::vector<int64_t>& starts,
+                      const std::vector<double>* costs, double* cost_out) {
   if (n < 1 || s < 2 || H < 0 || starts.empty() || starts[0] != 0 || starts.back() >= n ||
       int64_t(starts.size()) - 1 > H)
     throw std::invalid_argument("schedule: need s >= 2 and starts 0 = t_0 < ... < t_{K-1} < n, K - 1 <= H");
   for (size_t k = 1; k < starts.size(); ++k)
     if (starts[k] <= starts[k - 1]) throw std::invalid_argument("schedule: interval starts must increase");
+  if (costs && int64_t(costs->size()) != n) throw std::invalid_argument("schedule: need one cost per step");
   Plan p;
   p.n = n;
   p.s = s;
   p.H = H;
   p.async = true;
   p.dynamic = true;
-  p.evals = starts.back() + 1;
-  for (size_t k = 0; k < starts.size(); ++k) {
-    const int64_t end = k + 1 < starts.size() ? starts[k + 1] : n;
-    p.evals += revolve_advances(end - starts[k], s - 1);
+  Builder b{n, &p.acts, 0, std::vector<char>(size_t(s), 0), {}};
+  std::unique_ptr<WeightedSplits> ws;
+  if (costs) {
+    ws.reset(new WeightedSplits(*costs, int64_t(1) << 20));
+    b.split = [&ws](int64_t a, int64_t l, int64_t k) { return ws->split(a, l, k); };
+    p.weighted = true;
   }
-  Builder b{n, &p.acts, 0, std::vector<char>(size_t(s), 0)};
   two_level(b, s, starts);
   p.host_slots_used = int64_t(starts.size()) - 1;
+  p.evals = 1;
+  double cost = costs ? (*costs)[size_t(n - 1)] : 0.0;
+  for (const Action& x : p.acts)
+    if (x.op == Op::Advance) {
+      p.evals += x.b - x.a;
+      if (ws) cost += ws->C(x.a, x.b);
+    }
+  if (cost_out) *cost_out = costs ? cost : double(p.evals);
   return p;
 }
 
@@ -381,55 +442,6 @@ Plan make_plan_online(int64_t n, int32_t s, int64_t H, int64_t interval_min) {
     if (x.op == Op::Advance) p.evals += x.b - x.a;
   return p;
 }
-
-namespace {
-
-// Least cost of reversing [a, a + l) with k slots for unequal step costs, and
-// the split that reaches it.  Queries come top-down, one reversal at a time:
-// a query outside the current root reversal fills a new table for that root,
-// bottom-up over (k, l, a), dense and indexed by (a - a0, l, k).
-class WeightedSplits {
- public:
-  WeightedSplits(const std::vector<double>& costs, int64_t max_table) : max_table_(max_table) {
-    pre_.assign(costs.size() + 1, 0.0);
-    for (size_t t = 0; t < costs.size(); ++t) pre_[t + 1] = pre_[t] + costs[t];
-  }
-  double C(int64_t a, int64_t b) const { return pre_[size_t(b)] - pre_[size_t(a)]; }
-  int64_t split(int64_t a, int64_t l, int64_t k) {
-    if (!(a >= a0_ && a + l <= a0_ + L_ && k <= K_)) fill(a, l, k);
-    return m_[idx(a, l, k)];
-  }
-
- private:
-  size_t idx(int64_t a, int64_t l, int64_t k) const { return size_t(((a - a0_) * (L_ + 1) + l) * (K_ + 1) + k); }
-  void fill(int64_t a0, int64_t L, int64_t K) {
-    if (L * (L + 1) * (K + 1) > max_table_) throw std::length_error("schedule: cost table too large");
-    a0_ = a0, L_ = L, K_ = K;
-    v_.assign(size_t(L * (L + 1) * (K + 1)), 0.0);
-    m_.assign(v_.size(), 0);
-    // one slot: restore x_a and advance i steps for i = l-1 .. 1, summed in increasing i
-    for (int64_t a = a0; a < a0 + L; ++a)
-      for (int64_t l = 2; a + l <= a0 + L; ++l) v_[idx(a, l, 1)] = v_[idx(a, l - 1, 1)] + C(a, a + l - 1);
-    for (int64_t k = 2; k <= K; ++k)
-      for (int64_t l = 2; l <= L; ++l)
-        for (int64_t a = a0; a + l <= a0 + L; ++a) {
-          double best = 0.0;
-          int64_t bm = -1;
-          for (int64_t m = 1; m < l; ++m) {
-            const double v = C(a, a + m) + v_[idx(a + m, l - m, k - 1)] + v_[idx(a, m, k)];
-            if (bm < 0 || v <= best) best = v, bm = m;
-          }
-          v_[idx(a, l, k)] = best;
-          m_[idx(a, l, k)] = int32_t(bm);
-        }
-  }
-  std::vector<double> pre_;
-  std::vector<double> v_;
-  std::vector<int32_t> m_;
-  int64_t a0_ = 0, L_ = 0, K_ = 0, max_table_;
-};
-
-}  // namespace
 
 Plan make_plan_costs(int64_t n, int32_t s, int64_t H, int64_t interval_min, const std::vector<double>& costs,
                      double* cost_out, int64_t max_table) {

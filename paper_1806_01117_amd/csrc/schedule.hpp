@@ -48,7 +48,10 @@ Plan make_plan(int64_t n, int32_t s, int64_t H, int64_t interval_min);
 // The two-level plan over interval starts decided during the sweep (the
 // starts increase from 0, stay below n and number at most H + 1; s >= 2).
 // Throws std::invalid_argument otherwise.
-Plan make_plan_starts(int64_t n, int32_t s, int64_t H, const std::vector<int64_t>& starts);
+// With costs (one per step, see make_plan_costs) every reversal is split for
+// them; *cost_out (nullable) then receives the cost of the forward evaluations.
+Plan make_plan_starts(int64_t n, int32_t s, int64_t H, const std::vector<int64_t>& starts,
+                      const std::vector<double>* costs = nullptr, double* cost_out = nullptr);
 // Online checkpointing: every decision about x_t is taken when x_t is
 // computed, knowing only that step t exists; the actions before the sweep
 // reaches x_{n-1} are the same for every longer n.  H = 0 (or s = 1): one

@@ -96,9 +96,41 @@ def test_costs_argument_errors():
         r.set_step_costs([1.0] * 8)
         with pytest.raises(amb.AmbpttError):
             r.set("online", 1)
-        with pytest.raises(amb.AmbpttError):
-            r.set("store_policy", 1)
         r.set_step_costs(None)
         r.set("online", 1)
     finally:
         r.close()
+
+
+def test_costs_under_the_dynamic_store_policy():
+    """Interval starts chosen during the sweep (store when the previous store
+    completed), each interval reversed with splits for the step costs: the
+    executed text is the oracle's over the same starts, the gradients equal a
+    store-all run bit for bit and the oracle within tolerance."""
+    n = 48
+    wl = synth.get("lstm_h512_t1000").with_(batch=20, input=32, hidden=48, n_steps=n, name="lstm_dyn_costs")
+    host, dev = _case(wl)
+    want = run_oracle(wl, *host)
+    costs = _costs(n, 4)
+    import paper_1806_01117_amd as amb
+    r = amb.Runner(amb.ProblemSpec.from_workload(wl, fast_slots=4, slow_slots=n, interval_min=1))
+    try:
+        r.set("path", 1)
+        r.set("store_policy", 1)
+        r.set_step_costs(costs)
+        out = r.run(*dev)
+        text = r.last_schedule_text()
+    finally:
+        r.close()
+    got = {k: (v.float().cpu().numpy() if hasattr(v, "cpu") else v) for k, v in out.items() if v is not None}
+    head, acts = S.parse(text)
+    assert head["mode"] == "dynamic" and head["split"] == "cost"
+    starts = [a[3] for a in acts if a[0] == "W"]
+    opening = acts[3 * len(starts)]
+    starts.append(opening[2])
+    assert text == S.text_from_starts(n, 4, n, starts, costs)
+    ohead, _ = S.schedule_from_starts(n, 4, n, starts, costs)
+    assert got["stats"]["forward_evals"] == ohead["evals"]
+    assert got["stats"]["forward_cost"] == pytest.approx(ohead["cost"], rel=1e-12)
+    assert_close(got, want, TOL_F32)
+    assert_bitwise(got, _run(wl, dev, None, path=1, fast_slots=n, slow_slots=0))

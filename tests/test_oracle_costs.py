@@ -159,3 +159,20 @@ def test_c_abi_cost_errors():
     # the same steps in two levels: the intervals are the reversals
     txt = amb.schedule_text_costs(400, 10, [1.0] * 400, 400, 4)
     assert txt.startswith("ambptt-schedule v1 n=400 s=10 H=400 I=4 mode=async split=cost")
+
+
+def test_costs_over_chosen_starts():
+    rng = random.Random(8)
+    for trial in range(60):
+        n = rng.randint(2, 60)
+        s = rng.randint(2, 6)
+        k = rng.randint(0, min(n - 1, 8))
+        starts = [0] + sorted(rng.sample(range(1, n), k))
+        costs = [rng.choice([0.5, 1.0, 3.0]) for _ in range(n)]
+        head, acts = S.schedule_from_starts(n, s, n, starts, costs)
+        c = S.check(n, s, n, acts)
+        assert c["evals"] == head["evals"] and head["cost"] == _weighted(acts, costs)
+        _, racts = S.schedule_from_starts(n, s, n, starts)
+        assert head["cost"] <= _weighted(racts, costs)
+        eq = S.text_from_starts(n, s, n, starts, [1.0] * n)
+        assert _actions(eq) == _actions(S.text_from_starts(n, s, n, starts))
