@@ -225,7 +225,12 @@ ambptt_status ambptt_resident_program(int64_t n, int32_t s, int64_t H, int32_t i
                                       int32_t flags, int32_t* buf, size_t cap, size_t* entries);
 
 /* Sizes the caller allocates: bytes of one state (padded slot stride), of the
- * slot pool (fast_slots * stride) and of the workspace. */
+ * slot pool (fast_slots * stride) and of the workspace.  The slot pool is
+ * Level 1 of Section 2 at exactly the s checkpoints of the problem statement
+ * of Section 3 (the number of states that fit in fast memory at once); the
+ * state is what one step passes to the next (Section 1.1: the checkpoint is
+ * the state of a layer or timestep).  Pure host: EINVAL / EUNSUPPORTED as for
+ * ambptt_create; out pointers may be NULL. */
 ambptt_status ambptt_query(const ambptt_problem* p, size_t* state_bytes,
                            size_t* slot_pool_bytes, size_t* workspace_bytes);
 
@@ -234,11 +239,20 @@ const char* ambptt_last_error(void);
 /* ---- GPU calls ----------------------------------------------------------- */
 
 /* Validates p, creates the copy stream and events on the current device.
- * stream is the compute stream (hipStream_t; NULL = the null stream). */
+ * stream is the compute stream (hipStream_t; NULL = the null stream).
+ * Section 2: the compute stream runs the forward and adjoint operators while
+ * a second, owned stream moves states between Level 1 and Level 2, so that
+ * transfers run beside the computation.  *out is owned by the caller and
+ * released with ambptt_destroy; on failure *out is untouched and nothing is
+ * leaked.  EINVAL for a bad problem, EHIP if a stream or event cannot be
+ * made, EUNSUPPORTED for shapes the kernels do not take. */
 ambptt_status ambptt_create(const ambptt_problem* p, void* stream, ambptt_ctx** out);
 
 /* Binds caller-owned device memory: the slot pool and the workspace, at
- * least the sizes ambptt_query reports, 256-byte aligned. */
+ * least the sizes ambptt_query reports, 256-byte aligned.  The slot pool is
+ * the fixed fast-memory budget of Section 3 (s checkpoints); the library
+ * keeps the pointers (it does not copy or free them) until the next bind or
+ * ambptt_destroy.  EINVAL if a pointer is NULL, misaligned or too small. */
 ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
                           void* workspace, size_t workspace_bytes);
 
@@ -325,7 +339,15 @@ ambptt_status ambptt_calibrate(ambptt_ctx* ctx, const void* x_seq, const void* W
                                const float* b, const void* h0, const float* c0,
                                int32_t* interval_min_out, double* t_a_us, double* t_t_us);
 
-/* One forward + reverse pass (blocks until the compute stream is done).
+/* One forward + reverse pass (blocks until the compute stream is done):
+ * Section 4's driver, which runs the forward and backward operators as the
+ * schedule directs and returns the parameter and initial-state gradients;
+ * the schedule is the two-level one of Sections 2-3 (or plain Revolve).
+ * Fails with EINVAL before enqueueing anything if a pointer is NULL (other
+ * than those marked optional) or nothing is bound; with EHIP if a HIP call
+ * fails (the context is then unusable); with EINTERNAL if an executor
+ * invariant breaks (a resident-kernel barrier timed out), after which the
+ * context stays usable. */
  *   x_seq  [n][B][D] operand dtype (NULL for RESMLP)
  *   W      TANH_RNN/LSTM: [G*H][D+H]; RESMLP: [L][w][w]; operand dtype
  *   b      fp32 [G*H] (RESMLP: [L][w])

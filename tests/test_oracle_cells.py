@@ -88,7 +88,7 @@ def test_fd_lstm(loss):
     _fd_check("lstm", loss, n=5, B=2, D=2, H=3)
 
 
-@pytest.mark.parametrize("loss", ["half_sq_last", "mean_last"])
+@pytest.mark.parametrize("loss", ["half_sq_last", "mean_sq_all", "mean_last"])
 def test_fd_resmlp(loss):
     _fd_check("resmlp", loss, n=5, B=2, H=4)
 

@@ -249,3 +249,51 @@ def test_paper_model_figure():
         for I in (8, 64, 1024):
             head, _ = S.schedule(n, s, n, I)
             assert head["evals"] / n >= S.paper_model_R(I, s) - 1e-12
+
+
+def _mutate(acts, i, new):
+    out = list(acts)
+    out[i] = new
+    return out
+
+
+def test_check_rejects_planted_store_and_prefetch_mistakes():
+    """The symbolic checker's Level-2 rules, each shown to fail on a planted
+    mistake in a valid two-level schedule (Section 2: a stored state is the
+    one its fast slot holds; a prefetch brings back what was stored)."""
+    n, s, H, I = 12, 3, 100, 3
+    _, acts = S.schedule(n, s, H, I)
+    S.check(n, s, H, acts)  # the unmodified schedule passes
+    iw = next(i for i, a in enumerate(acts) if a[0] == "W" and a[3] > 0)
+    # a prefetch whose fast slot holds another state when it is issued (the
+    # first one of this schedule refills a slot that still holds its state)
+    held, ip = {}, None
+    for i, a in enumerate(acts):
+        if a[0] == "S":
+            held[a[1]] = a[2]
+        elif a[0] == "P":
+            if ip is None and held.get(a[2]) != a[3]:
+                ip = i
+            held[a[2]] = a[3]
+    k, h, t = acts[iw][1:]
+    hp, kp, tp = acts[ip][1:]
+    planted = {
+        # a store from a fast slot that holds another state
+        "store wrong slot": _mutate(acts, iw, ("W", 1 - k, h, t)),
+        # a store that claims a state its slot does not hold
+        "store wrong state": _mutate(acts, iw, ("W", k, h, t + 1)),
+        # a store past the host budget
+        "store beyond H": _mutate(acts, iw, ("W", k, H, t)),
+        # a prefetch of a host slot that holds another state
+        "prefetch wrong host slot": _mutate(acts, ip, ("P", hp + 1, kp, tp)),
+        # a prefetch into a slot beyond the fast budget
+        "prefetch beyond s": _mutate(acts, ip, ("P", hp, s, tp)),
+        # a prefetch issued before the store that fills its host slot
+        "prefetch before store": [a for a in acts if not (a[0] == "W" and a[2] == hp)],
+        # a dropped prefetch: the reverse restores a state no slot holds
+        "dropped prefetch": acts[:ip] + acts[ip + 1:],
+    }
+    for name, bad in planted.items():
+        with pytest.raises(AssertionError):
+            S.check(n, s, H, bad)
+            pytest.fail(f"check() accepted: {name}")
