@@ -347,7 +347,7 @@ ambptt_status ambptt_calibrate(ambptt_ctx* ctx, const void* x_seq, const void* W
  * than those marked optional) or nothing is bound; with EHIP if a HIP call
  * fails (the context is then unusable); with EINTERNAL if an executor
  * invariant breaks (a resident-kernel barrier timed out), after which the
- * context stays usable. */
+ * context stays usable.
  *   x_seq  [n][B][D] operand dtype (NULL for RESMLP)
  *   W      TANH_RNN/LSTM: [G*H][D+H]; RESMLP: [L][w][w]; operand dtype
  *   b      fp32 [G*H] (RESMLP: [L][w])
