@@ -1,21 +1,29 @@
 #!/usr/bin/env python3
 """Throughput of checkpointed BPTT on one MI355X.
 
-A step is one whole forward + reverse pass (ambptt_run) over the 1000-step
-LSTM workload (hidden 512, input 256, batch 64, fp32) with 10 HBM checkpoint
-slots and a pinned host tier, under the asynchronous two-level schedule whose
-interval comes from measured T_A and T_T.  Inputs are seeded, synthetic and
-resident in HBM before the timed region starts.  By default the library runs
-the pass as one resident kernel launch (weights held in registers for the
-whole pass); --path steps selects one kernel launch per step.
+A step is one whole forward + reverse pass (ambptt_run) over a workload's n
+recurrent steps.  The default workload is the largest one that fits one GPU:
+the 20000-step LSTM (hidden 4096, input 1024, batch 512, fp32; 16 MiB of
+state per step, 320 GB of states in all) with 64 HBM checkpoint slots and a
+pinned host tier, under the asynchronous two-level schedule whose interval
+comes from measured T_A and T_T.  Pinned host memory is limited per process,
+so the host tier gets the slots that fit --pinned-gib (the schedule raises the
+interval to ceil(n / (H + 1)) accordingly).  Inputs are seeded, synthetic and
+resident in HBM before the timed region starts.
 
-Prints one JSON line: timesteps/s over the timed steps, the recompute factor,
-the same pass under plain Revolve at the same 10 slots, the other execution
-path on the same schedule, the roofline of the dominant kernel (HIP-event
-durations on the compute stream) and the CPU oracle's rate on a bounded
-sample.
+Passes are whole: a pass is never shortened.  When the requested warm-up and
+timed passes would take longer than --max-timed-s (estimated from the
+calibrated forward step), fewer passes run, and the line reports the numbers
+actually run ("steps", "warmup") beside the requested ones.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--path auto|steps|resident]
+Prints one JSON line: timesteps/s over the timed passes, the recompute factor,
+the same pass under plain Revolve at the same HBM slots (gradients compared
+element by element), store-all in HBM where its slots fit, the roofline of the
+dominant kernel (HIP-event durations on the compute stream) and the CPU
+oracle's rate on a bounded sample.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--path auto|steps|resident]
+    python bench.py --workload lstm_h512_t1000 --sweep-n 100,1000,10000,100000
 """
 from __future__ import annotations
 
@@ -29,7 +37,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "BPTT timesteps/sec at fixed HBM slot budget; recompute factor; MFMA % of peak"
-WORKLOAD = "lstm_h512_t1000"
+WORKLOAD = "lstm_h4096_t20000"
 FP32_MFMA_PEAK_TFLOPS = 157.3
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense
 HBM_PEAK_GBS = 8000.0
@@ -80,6 +88,8 @@ def copy_overlap(spec, st, stats, dev, wall_ms: float) -> dict:
             ms = e0.elapsed_time(e1)
             best = ms if best is None else min(best, ms)
         rates[name] = best
+    del d, h
+    release_pinned()
     n_st, n_pf = st["stores"], st["prefetches"] - st["prefetches_elided"]
     copy_ms = n_st * rates["d2h"] + n_pf * rates["h2d"]
     kernel_ms = float(np.mean([sum(s_["kernel_us"][i] * s_["kernel_calls"][i] for i in range(6)) for s_ in stats])) / 1e3
@@ -89,6 +99,42 @@ def copy_overlap(spec, st, stats, dev, wall_ms: float) -> dict:
             "copies": n_st + n_pf, "copy_ms_per_pass": round(copy_ms, 2),
             "kernel_ms_per_pass": round(kernel_ms, 2), "wall_ms_per_pass": round(wall_ms, 2),
             "overlap_lower_bound": round(1.0 - idle_ms / copy_ms, 4) if copy_ms > 0 else None}
+
+
+def release_pinned() -> None:
+    """Frees the pinned blocks torch's host allocator caches, so that no pinned
+    memory is left for static destructors to release at process exit."""
+    import torch
+    torch.cuda.synchronize()
+    fn = getattr(torch._C, "_host_emptyCache", None)
+    if fn is not None:
+        fn()
+
+
+def same_gradients(a: dict, b: dict) -> bool:
+    """Element-by-element equality of two passes' gradients and losses (bit for
+    bit: NaNs compare by their bit patterns)."""
+    import torch
+    for k in ("dW", "db", "dh0", "dc0"):
+        x, y = a.get(k), b.get(k)
+        if (x is None) != (y is None):
+            return False
+        if x is not None and not torch.equal(x.view(torch.int32), y.view(torch.int32)):
+            return False
+    return a["loss"] == b["loss"]
+
+
+def snapshot(out: dict) -> dict:
+    """A copy of a pass's gradients (device) and loss."""
+    return {k: (v.clone() if hasattr(v, "clone") else v) for k, v in out.items() if k in ("dW", "db", "dh0", "dc0", "loss")}
+
+
+def estimate_pass_s(wl, spec, t_a_us: float, I_min: int) -> float:
+    """Rough seconds per pass from the calibrated forward step: R forward steps
+    and about 2.7 forward steps' worth of adjoint work per timestep."""
+    import paper_1806_01117_amd as amb
+    evals = amb.schedule_evals(wl.n_steps, spec.fast_slots, spec.slow_slots, max(1, I_min))[0]
+    return wl.n_steps * t_a_us * 1e-6 * (evals / wl.n_steps + 2.7)
 
 
 def step_flops(spec, window: int, wide: bool = False) -> dict:
@@ -232,26 +278,6 @@ def device_inputs(wl, dev):
     return dx, t(W, op), t(b, torch.float32), dh, dc
 
 
-def fingerprint(out) -> list:
-    """Exact fingerprints of the gradients (sums of the raw bit patterns in
-    chunks, weighted by chunk), to compare passes bit for bit without keeping
-    two copies of a 134 GB gradient."""
-    import torch
-    fp = []
-    for k in ("dW", "db", "dh0", "dc0"):
-        v = out.get(k)
-        if v is None:
-            continue
-        flat = v.reshape(-1).view(torch.int32)
-        acc = 0
-        step = 1 << 24
-        for i, c0 in enumerate(range(0, flat.numel(), step)):
-            acc += (i + 1) * int(flat[c0:c0 + step].to(torch.int64).sum().item())
-        fp.append(acc)
-    fp.append(float(out["loss"]))
-    return fp
-
-
 def gemm_reference(wl, dev, reps: int = 200) -> dict:
     """The vendor GEMM (torch.matmul, hipBLASLt on ROCm) on the step products
     of a workload, back to back on the same operands: a reference for the
@@ -284,17 +310,79 @@ def gemm_reference(wl, dev, reps: int = 200) -> dict:
     return out
 
 
+def sweep_n(args, knobs) -> int:
+    """R(n) and timesteps/s(n) at a fixed HBM slot budget: the two-level
+    schedule against plain Revolve on the same slots, one JSON line per n
+    (the measured counterpart of the constant-overhead claim, Section 3 and
+    Fig. 3).  Each n runs its own whole passes on the workload's shapes."""
+    import torch
+    import paper_1806_01117_amd as amb
+    import synth
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    base = synth.get(args.workload)
+    for n in [int(v) for v in args.sweep_n.split(",")]:
+        wl = base.with_(n_steps=n)
+        dx, dW, db, dh, dc = device_inputs(wl, dev)
+        torch.cuda.synchronize()
+        res = {"workload": wl.name, "n_steps": n, "fast_slots": wl.fast_slots}
+        outs = {}
+        for name, kw in (("async", dict(slow_slots=min(wl.host_slots, n))), ("revolve", dict(slow_slots=0))):
+            spec = amb.ProblemSpec.from_workload(wl, **kw)
+            r = amb.Runner(spec, device=dev)
+            try:
+                if args.path != "auto":
+                    r.set("path", 1 if args.path == "steps" else 2)
+                for k, v in knobs:
+                    r.set(k, v)
+                I_min = 0
+                if name == "async":
+                    I_min, t_a, t_t = r.calibrate(dx, dW, db, dh, dc)
+                r.run(dx, dW, db, dh, dc)  # warm-up
+                torch.cuda.synchronize()
+                reps = max(1, min(args.steps, int(2e6 // n)))
+                t0 = time.perf_counter()
+                for _ in range(reps):
+                    o = r.run(dx, dW, db, dh, dc)
+                torch.cuda.synchronize()
+                el = (time.perf_counter() - t0) / reps
+                outs[name] = snapshot(o)
+                st = o["stats"]
+                res[name] = {"value": round(n / el, 2), "unit": "timesteps/s", "ms_per_pass": round(1000 * el, 3),
+                             "recompute_factor": round(st["recompute_factor"], 4), "interval": st["interval"],
+                             "mode": ["revolve", "async", "dynamic", "online"][st["mode"]], "passes": reps,
+                             "path": "resident" if st["path"] == 1 else "steps"}
+                if name == "async":
+                    res[name].update({"interval_min": I_min, "t_a_us": round(t_a, 3), "t_t_us": round(t_t, 3)})
+            finally:
+                r.close()
+        res["bit_identical_gradients"] = same_gradients(outs["async"], outs["revolve"])
+        res["paper_model"] = {"revolve_R": round((amb.revolve_advances(n, wl.fast_slots) + 1) / n, 4)}
+        print(json.dumps(res), flush=True)
+        del dx, dW, db, dh, dc, outs
+        torch.cuda.empty_cache()
+    release_pinned()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--max-timed-s", type=float, default=120.0,
+                    help="seconds the warm-up and timed passes may take together (estimated from the calibrated "
+                         "forward step); fewer whole passes run beyond it, at least one timed")
+    ap.add_argument("--pinned-gib", type=float, default=56.0,
+                    help="pinned host memory for the host tier (the process limit is 64 GiB); caps its slots")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--timing-sample", type=int, default=32)
     ap.add_argument("--path", choices=["auto", "steps", "resident"], default="auto")
     ap.add_argument("--cooperative", type=int, default=0)
-    ap.add_argument("--workload", default=WORKLOAD, help="a synth workload name (default: the 512-LSTM)")
-    ap.add_argument("--host-slots", type=int, default=-1, help="host-tier slots (default: the workload's)")
+    ap.add_argument("--workload", default=WORKLOAD, help="a synth workload name (default: the 4096-LSTM)")
+    ap.add_argument("--n-steps", type=int, default=0, help="override the workload's step count (profiling runs)")
+    ap.add_argument("--host-slots", type=int, default=-1, help="host-tier slots (default: the workload's, "
+                    "capped by --pinned-gib)")
     ap.add_argument("--no-compare", dest="compare", action="store_false",
                     help="skip the plain-Revolve and other-path passes")
     ap.add_argument("--file-tier", default="", metavar="DIR",
@@ -302,6 +390,8 @@ def main() -> int:
                          "the pinned ring in front of it")
     ap.add_argument("--gemm-reference", action="store_true",
                     help="only time the vendor GEMM on the workload's step products and print them")
+    ap.add_argument("--sweep-n", default="", metavar="N1,N2,...",
+                    help="only measure the two-level schedule against plain Revolve at each step count")
     ap.add_argument("--step-costs", default="", metavar="every:K:F",
                     help="relative step costs for the schedule (step t costs F when t % K == 0, else 1): "
                          "reversals split for unequal costs (ambptt_set_step_costs)")
@@ -320,7 +410,11 @@ def main() -> int:
     import paper_1806_01117_amd as amb
     import synth
 
+    if args.sweep_n:
+        return sweep_n(args, knobs)
     wl = synth.get(args.workload)
+    if args.n_steps > 0:
+        wl = wl.with_(n_steps=args.n_steps)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     if args.gemm_reference:
@@ -338,12 +432,43 @@ def main() -> int:
     torch.cuda.synchronize()
     del ref_src, ref_dst
 
-    host_slots = wl.host_slots if args.host_slots < 0 else args.host_slots
+    stride = amb.query(amb.ProblemSpec.from_workload(wl))[0]
+    pinned_cap = int(args.pinned_gib * 2 ** 30) // stride
+    if args.host_slots >= 0:
+        host_slots = args.host_slots
+    else:
+        host_slots = min(wl.host_slots, pinned_cap) if not args.file_tier else min(wl.host_slots, 256)
     spec = amb.ProblemSpec.from_workload(wl, slow_slots=host_slots)
     f32 = dict(dtype=torch.float32, device=dev)
     outb = {"dW": torch.empty(dW.shape, **f32), "db": torch.empty(db.shape, **f32),
             "dh0": torch.empty(dh.shape, **f32), "dc0": torch.empty(dh.shape, **f32) if dc is not None else None}
-    r = amb.Runner(spec, device=dev)
+    runners = []
+
+    def runner(sp):
+        rr = amb.Runner(sp, device=dev)
+        runners.append(rr)
+        return rr
+
+    try:
+        return _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh, dc, outb, runner)
+    finally:
+        # every context is closed and every pinned block released before the
+        # interpreter's teardown, which then makes no HIP call of ours
+        for rr in runners:
+            rr.close()
+        del dx, dW, db, dh, dc, outb
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        release_pinned()
+
+
+def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh, dc, outb, runner) -> int:
+    import numpy as np
+    import torch
+
+    import paper_1806_01117_amd as amb
+
+    r = runner(spec)
     if args.path != "auto":
         r.set("path", 1 if args.path == "steps" else 2)
     r.set("resident_cooperative", args.cooperative)
@@ -361,45 +486,53 @@ def main() -> int:
             r.set(k, v)
             I_min = v
     r.set("timing_sample", args.timing_sample)
-    for _ in range(args.warmup):
+    # whole passes only: as many of the requested ones as fit the budget
+    est = estimate_pass_s(wl, spec, t_a, I_min)
+    steps, warmup = args.steps, args.warmup
+    if est * (steps + warmup) > args.max_timed_s:
+        fit = int(args.max_timed_s // max(est, 1e-9))
+        steps = max(1, min(steps, fit))
+        warmup = max(0, min(warmup, fit - steps))
+    print(f"estimated {est:.2f} s per pass: {warmup} warm-up and {steps} timed passes", file=sys.stderr, flush=True)
+    for _ in range(warmup):
         r.run(dx, dW, db, dh, dc, out=outb)
     torch.cuda.synchronize()
     stats = []
     t0 = time.perf_counter()
-    for i in range(args.steps):
+    for i in range(steps):
         out = r.run(dx, dW, db, dh, dc, out=outb)
         stats.append(out["stats"])
-        print(f"pass {i + 1}/{args.steps} done", file=sys.stderr, flush=True)
+        print(f"pass {i + 1}/{steps} done", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     el = time.perf_counter() - t0
-    value = wl.n_steps * args.steps / el
+    value = wl.n_steps * steps / el
     st = stats[-1]
     resident = st["path"] == 1
-    fp_async = fingerprint(out) if args.compare else None
+    ref = snapshot(out) if args.compare else None
 
-    def other_run(runner, reps, warm=True):
+    def other_run(rn, reps, warm=True):
         if warm:
-            runner.run(dx, dW, db, dh, dc, out=outb)
+            rn.run(dx, dW, db, dh, dc, out=outb)
         torch.cuda.synchronize()
         tr = time.perf_counter()
         for _ in range(reps):
-            o = runner.run(dx, dW, db, dh, dc, out=outb)
+            o = rn.run(dx, dW, db, dh, dc, out=outb)
         torch.cuda.synchronize()
         return wl.n_steps * reps / (time.perf_counter() - tr), o
 
-    reps = max(1, min(3, args.steps))
+    reps = max(1, min(3, steps))
     # plain Revolve at the same HBM slot budget (no host tier), same path
     rv_value, rv_st, bitwise = None, None, None
     if args.compare:
-        rv = amb.Runner(amb.ProblemSpec.from_workload(wl, slow_slots=0), device=dev)
+        rv = runner(amb.ProblemSpec.from_workload(wl, slow_slots=0))
         rv.set("path", 2 if resident else 1)
         rv.set("resident_cooperative", args.cooperative)
         for k, v in knobs:
             if k != "online":  # plain Revolve knows n up front
                 rv.set(k, v)
-        rv_value, rvo = other_run(rv, reps if args.steps > 1 else 1, warm=args.steps > 1)
+        rv_value, rvo = other_run(rv, reps, warm=steps > 1)
         rv_st = rvo["stats"]
-        bitwise = fingerprint(rvo) == fp_async
+        bitwise = same_gradients(rvo, ref)
         print(f"plain Revolve done, bit-identical gradients: {bitwise}", file=sys.stderr, flush=True)
         rv.close()
     # store-all in HBM (a slot for every state: no recomputation, no host tier),
@@ -407,23 +540,22 @@ def main() -> int:
     sa = None
     n_state = amb.query(spec)[0]
     if args.compare and wl.n_steps * n_state <= 72 * 2 ** 30:
-        sr = amb.Runner(amb.ProblemSpec.from_workload(wl, fast_slots=wl.n_steps, slow_slots=0), device=dev)
+        sr = runner(amb.ProblemSpec.from_workload(wl, fast_slots=wl.n_steps, slow_slots=0))
         sr.set("path", 2 if resident else 1)
         sr.set("resident_cooperative", args.cooperative)
-        sa_value, sao = other_run(sr, reps if args.steps > 1 else 1, warm=args.steps > 1)
+        sa_value, sao = other_run(sr, reps, warm=steps > 1)
         sa = {"value": round(sa_value, 2), "unit": "timesteps/s",
               "recompute_factor": round(sao["stats"]["recompute_factor"], 4),
-              "bit_identical_gradients": fingerprint(sao) == fp_async,
+              "bit_identical_gradients": same_gradients(sao, ref),
               "slot_pool_gb": round(wl.n_steps * n_state / 2 ** 30, 2)}
         print(f"store-all done, bit-identical gradients: {sa['bit_identical_gradients']}", file=sys.stderr, flush=True)
         sr.close()
-        del sr, sao
+        del sao
         torch.cuda.empty_cache()
     # the same schedule with one kernel launch per step (the other execution path)
     alt = None
     if resident and args.compare:
-        ps = amb.Runner(amb.ProblemSpec.from_workload(wl, interval_min=max(1, st["interval"]), slow_slots=host_slots),
-                        device=dev)
+        ps = runner(amb.ProblemSpec.from_workload(wl, interval_min=max(1, st["interval"]), slow_slots=host_slots))
         ps.set("path", 1)
         for k, v in knobs:
             if k == "online":  # the same schedule
@@ -503,11 +635,9 @@ def main() -> int:
     else:
         achieved = flops[dom] / (dom_us * 1e-6) / 1e12 if dom_us > 0 else 0.0
         roof_peak, roof_unit = peak, "TFLOP/s"
-    r.close()
-
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "timesteps/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(1000 * el / args.steps, 3),
+        "steps": steps, "warmup": warmup, "ms_per_step": round(1000 * el / steps, 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
         "data": "synthetic (seeded normal inputs, " + ("normal" if wl.cell == "resmlp" else "uniform") + " weights)",
         "config": {"workload": wl.name, "cell": wl.cell, "batch": wl.batch, "input": wl.input,
@@ -515,7 +645,11 @@ def main() -> int:
                    "slow_slots": spec.slow_slots,
                    "mode": ["revolve", "async", "dynamic", "online"][st["mode"]],
                    "interval": st["interval"], "interval_min": I_min, "t_a_us": round(t_a, 3),
-                   "t_t_us": round(t_t, 3), "window": st["window"], **({"knobs": dict(knobs)} if knobs else {}),
+                   "t_t_us": round(t_t, 3), "window": st["window"],
+                   "pinned_host_gib": round(host_slots * n_state / 2 ** 30, 2),
+                   **({"host_slots_capped_by_pinned_gib": args.pinned_gib}
+                      if host_slots == pinned_cap and pinned_cap < wl.host_slots and not args.file_tier else {}),
+                   **({"knobs": dict(knobs)} if knobs else {}),
                    **({"file_tier": {"file_slots": wl.n_steps, "pinned_ring": host_slots,
                                      "bytes_written": st["bytes_file_w"], "bytes_read": st["bytes_file_r"]}}
                       if args.file_tier else {})},
@@ -547,7 +681,7 @@ def main() -> int:
                      "flop_per_byte": round(flops[dom] / max(byts[dom], 1), 1)},
     }
     if not resident and (st["stores"] or st["prefetches"]):
-        line["transfer_overlap"] = copy_overlap(spec, st, stats, dev, 1000.0 * el / args.steps)
+        line["transfer_overlap"] = copy_overlap(spec, st, stats, dev, 1000.0 * el / steps)
     if costs is not None:
         # the same pass with Revolve's own splits, weighed with the same costs
         plain = amb.schedule_text(wl.n_steps, spec.fast_slots, host_slots, max(I_min, 1))
@@ -558,11 +692,10 @@ def main() -> int:
                                   round(weighted_cost(plain, costs) / total, 4)}
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl)
+    if (steps, warmup) != (args.steps, args.warmup):
+        line["requested"] = {"steps": args.steps, "warmup": args.warmup, "max_timed_s": args.max_timed_s,
+                             "estimated_s_per_pass": round(est, 2)}
     print(json.dumps(line), flush=True)
-    # release device memory before interpreter teardown
-    del dx, dW, db, dh, dc, r, outb
-    torch.cuda.synchronize()
-    torch.cuda.empty_cache()
     return 0
 
 

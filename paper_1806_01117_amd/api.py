@@ -8,6 +8,7 @@ from __future__ import annotations
 
 import ctypes as C
 import dataclasses
+import sys
 
 from . import _lib
 from ._lib import check, load
@@ -201,6 +202,9 @@ class Runner:
         return int(I.value), float(ta.value), float(tt.value)
 
     def run(self, x, W, b, h0, c0=None, out: dict | None = None) -> dict:
+        return self._run(self.L.ambptt_run, x, W, b, h0, c0, out)
+
+    def _run(self, fn, x, W, b, h0, c0, out) -> dict:
         torch, s = self.torch, self.spec
         x, W, b, h0, c0 = self._inputs(x, W, b, h0, c0)
         if out is None:
@@ -210,7 +214,7 @@ class Runner:
                    "dc0": torch.empty(h0.shape, **f32) if s.cell == "lstm" else None}
         loss = C.c_double()
         st = _lib.Stats()
-        check(self.L.ambptt_run(self.ctx, _ptr(x), _ptr(W), _ptr(b), _ptr(h0), _ptr(c0),
+        check(fn(self.ctx, _ptr(x), _ptr(W), _ptr(b), _ptr(h0), _ptr(c0),
                                 _ptr(out["dW"]), _ptr(out["db"]), _ptr(out["dh0"]), _ptr(out.get("dc0")),
                                 C.byref(loss), C.byref(st)))
         res = dict(out)
@@ -240,6 +244,10 @@ class Runner:
             self.ctx = None
 
     def __del__(self):
+        # at interpreter shutdown the HIP runtime may already be going away:
+        # contexts still open then are left to the process's end
+        if sys.is_finalizing():
+            return
         try:
             self.close()
         except Exception:

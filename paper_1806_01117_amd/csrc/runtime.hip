@@ -214,8 +214,13 @@ struct ambptt_ctx {
   std::vector<hipEvent_t> tpool;  // timing events, reused across runs
   char* pool = nullptr;
   char* ws = nullptr;
+  // Pinned host tier: chunks of host_per_chunk slots of host_slot_bytes each
+  // (one pinned allocation of tens of GiB fails well below the per-process
+  // pinned limit, so a large tier comes in chunks); host is the first chunk,
+  // the whole tier where a caller needs it contiguous.
+  std::vector<std::pair<char*, size_t>> host_chunks;
+  size_t host_slot_bytes = 0, host_per_chunk = 0;
   char* host = nullptr;
-  size_t host_bytes = 0;
   double* host_loss = nullptr;  // pinned scalar
   std::vector<hipEvent_t> ev_slot;
   std::vector<int> pend;  // 0 none, 1 store in flight, 2 prefetch in flight
@@ -328,6 +333,61 @@ hipError_t make_sync_events(ambptt_ctx* C) {
   for (auto& ev : C->tpool) (void)hipEventDestroy(ev);
   C->tpool.clear();
   return hipSuccess;
+}
+
+constexpr size_t kHostChunkBytes = size_t(8) << 30;
+
+void free_host(ambptt_ctx* C) {
+  if (C->host_chunks.empty()) return;
+  if (C->xs) (void)hipStreamSynchronize(C->xs);
+  for (auto& c : C->host_chunks) (void)hipHostFree(c.first);
+  C->host_chunks.clear();
+  C->host = nullptr;
+  C->host_slot_bytes = C->host_per_chunk = 0;
+}
+
+int64_t host_capacity(const ambptt_ctx* C) {
+  if (!C->host_slot_bytes) return 0;
+  int64_t n = 0;
+  for (auto& c : C->host_chunks) n += int64_t(c.second / C->host_slot_bytes);
+  return n;
+}
+
+// Pinned memory for `slots` host slots of slot_bytes: in one allocation when
+// `contiguous` (the resident kernel's and the file ring's), else in chunks
+// that host_slot() addresses.  Keeps what is there when it suffices.
+ambptt_status ensure_host(ambptt_ctx* C, int64_t slots, size_t slot_bytes, bool contiguous) {
+  const size_t need = size_t(slots) * slot_bytes;
+  if (need == 0) return AMBPTT_OK;
+  if (!C->host_chunks.empty() && C->host_chunks[0].second >= need) {
+    if (!contiguous) {  // the first chunk holds the whole tier
+      C->host_slot_bytes = slot_bytes;
+      C->host_per_chunk = C->host_chunks[0].second / slot_bytes;
+    }
+    return AMBPTT_OK;
+  }
+  if (!contiguous && C->host_slot_bytes == slot_bytes && host_capacity(C) >= slots) return AMBPTT_OK;
+  free_host(C);
+  const size_t per = contiguous ? size_t(slots) : std::max<size_t>(1, kHostChunkBytes / slot_bytes);
+  for (int64_t h = 0; h < slots; h += int64_t(per)) {
+    const size_t bytes = std::min<size_t>(per, size_t(slots - h)) * slot_bytes;
+    void* ptr = nullptr;
+    if (hipHostMalloc(&ptr, bytes, hipHostMallocDefault) != hipSuccess || !ptr) {
+      (void)hipGetLastError();
+      free_host(C);
+      return fail(AMBPTT_ENOMEM, "hipHostMalloc of " + std::to_string(bytes) + " bytes for the host tier failed (" +
+                                     std::to_string(need) + " bytes in total)");
+    }
+    C->host_chunks.push_back({(char*)ptr, bytes});
+  }
+  C->host = C->host_chunks[0].first;
+  C->host_slot_bytes = slot_bytes;
+  C->host_per_chunk = per;
+  return AMBPTT_OK;
+}
+
+char* host_slot(const ambptt_ctx* C, int64_t h) {
+  return C->host_chunks[size_t(h) / C->host_per_chunk].first + (size_t(h) % C->host_per_chunk) * C->host_slot_bytes;
 }
 
 struct Sample {
@@ -790,7 +850,7 @@ struct Exec {
           break;
         case Op::Store: {
           const int64_t k = A.a, h = A.b;
-          char* dst = C->host + (size_t)h * L.stride;
+          char* dst = host_slot(C, h);
           if (C->ftier && !(dst = C->ftier->store_buffer(h))) return fail(AMBPTT_EINTERNAL, C->ftier->error());
           if ((s = copy_after_compute()) != AMBPTT_OK) return s;
           HIPCK(hipMemcpyAsync(dst, slot(k), L.state_bytes, hipMemcpyDeviceToHost, C->xs));
@@ -818,7 +878,7 @@ struct Exec {
             if ((s = copy_state(dst, cur)) != AMBPTT_OK) return s;
             set_cur_live(dst);
           }
-          const char* src = C->host + (size_t)h * L.stride;
+          const char* src = host_slot(C, h);
           if (C->ftier && !(src = C->ftier->prefetch_buffer(h))) return fail(AMBPTT_EINTERNAL, C->ftier->error());
           if ((s = copy_after_compute()) != AMBPTT_OK) return s;
           HIPCK(hipMemcpyAsync(slot(k), src, L.state_bytes, hipMemcpyHostToDevice, C->xs));
@@ -838,24 +898,6 @@ struct Exec {
     return AMBPTT_OK;
   }
 };
-
-ambptt_status ensure_host(ambptt_ctx* C, size_t bytes) {
-  if (bytes <= C->host_bytes) return AMBPTT_OK;
-  if (C->host) {
-    HIPCK(hipStreamSynchronize(C->xs));
-    HIPCK(hipHostFree(C->host));
-    C->host = nullptr;
-    C->host_bytes = 0;
-  }
-  void* ptr = nullptr;
-  if (hipHostMalloc(&ptr, bytes, hipHostMallocDefault) != hipSuccess || !ptr) {
-    (void)hipGetLastError();
-    return fail(AMBPTT_ENOMEM, "hipHostMalloc of " + std::to_string(bytes) + " bytes for the host tier failed");
-  }
-  C->host = (char*)ptr;
-  C->host_bytes = bytes;
-  return AMBPTT_OK;
-}
 
 ambptt_status prepare_inputs(ambptt_ctx* C, const void* W, const void* h0, const float* c0, Exec& E) {
   const Layout& L = C->L;
@@ -996,7 +1038,7 @@ ambptt_status resident_calibrate(ambptt_ctx* C, const void* x, const void* W, co
                                  const float* c0, double* ta_us, double* tt_us) {
   const Layout& L = C->L;
   const ambptt_problem& p = C->p;
-  ambptt_status s = ensure_host(C, 2 * size_t(L.r_nwg) * 1024);
+  ambptt_status s = ensure_host(C, 2, size_t(L.r_nwg) * 1024, true);
   if (s != AMBPTT_OK) return s;
   if ((s = resident_inputs(C, h0, c0)) != AMBPTT_OK) return s;
   ResidentArgs a;
@@ -1057,7 +1099,7 @@ ambptt_status resident_run(ambptt_ctx* C, const void* x_seq, const void* W, cons
   }
   const double t1 = now_us();
   ambptt_status s;
-  if (plan.async && (s = ensure_host(C, size_t(plan.host_slots_used) * size_t(L.r_nwg) * 1024)) != AMBPTT_OK)
+  if (plan.async && (s = ensure_host(C, plan.host_slots_used, size_t(L.r_nwg) * 1024, true)) != AMBPTT_OK)
     return s;
   ResidentArgs a;
   if ((s = resident_args(C, x_seq, W, b, &a)) != AMBPTT_OK) return s;
@@ -1389,7 +1431,7 @@ ambptt_status ambptt_calibrate(ambptt_ctx* C, const void* x_seq, const void* W, 
   }
   Exec E(C, x_seq, W, b);
   if ((s = prepare_inputs(C, W, h0, c0, E)) != AMBPTT_OK) return s;
-  if ((s = ensure_host(C, 2 * C->L.stride)) != AMBPTT_OK) return s;
+  if ((s = ensure_host(C, 2, C->L.stride, true)) != AMBPTT_OK) return s;
   hipEvent_t e0, e1;
   HIPCK(hipEventCreateWithFlags(&e0, event_flags(C, true)));
   HIPCK(hipEventCreateWithFlags(&e1, event_flags(C, true)));
@@ -1478,17 +1520,22 @@ ambptt_status ambptt_calibrate(ambptt_ctx* C, const void* x_seq, const void* W, 
   return AMBPTT_OK;
 }
 
-ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const float* b, const void* h0,
-                         const float* c0, float* dW, float* db, float* dh0, float* dc0, double* loss,
-                         ambptt_stats* stats) {
-  ambptt_status s = check_run_args(C, x_seq, W, b, h0, c0);
-  if (s != AMBPTT_OK) return s;
-  if (!dW || !db || !dh0 || (C->L.G == 4 && !dc0)) return fail(AMBPTT_EINVAL, "missing gradient pointer");
+// Host slots the per-step pass of `plan` fills: the plan's, or with stores
+// decided during the sweep as many as it may take; in front of a file tier
+// only the pinned ring.
+static int64_t host_slots_needed(const ambptt_ctx* C, const Plan& plan, bool dynamic) {
+  int64_t slots = dynamic ? std::min<int64_t>(slow_capacity(C), C->p.n_steps) : plan.host_slots_used;
+  if (C->ftier) slots = std::min<int64_t>(slots, C->p.slow_slots);
+  return slots;
+}
+
+// One pass on the context's bound buffers (the workspace is C->ws).
+static ambptt_status run_pass(ambptt_ctx* C, const void* x_seq, const void* W, const float* b, const void* h0,
+                              const float* c0, float* dW, float* db, float* dh0, float* dc0, double* loss,
+                              ambptt_stats* stats) {
+  ambptt_status s;
   const ambptt_problem& p = C->p;
   const Layout& L = C->L;
-  if (p.slow_slots > 0 && C->interval_min == 0) {
-    if ((s = ambptt_calibrate(C, x_seq, W, b, h0, c0, nullptr, nullptr, nullptr)) != AMBPTT_OK) return s;
-  }
   if (C->path_opt == 2 && C->store_policy == 1)
     return fail(AMBPTT_EUNSUPPORTED, "store_policy 1 runs on the per-step path only");
   if (C->path_opt == 2 && !resident_possible(C))
@@ -1508,9 +1555,8 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   // use the host tier at all
   const bool dynamic = C->store_policy == 1 && plan.async && p.n_steps >= 2;
   if (plan.async) {
-    size_t slots = dynamic ? size_t(std::min<int64_t>(slow_capacity(C), p.n_steps)) : size_t(plan.host_slots_used);
-    if (C->ftier) slots = std::min<size_t>(slots, size_t(p.slow_slots));  // the pinned ring in front of the file
-    if ((s = ensure_host(C, slots * L.stride)) != AMBPTT_OK) return s;
+    const size_t slots = size_t(host_slots_needed(C, plan, dynamic));
+    if ((s = ensure_host(C, int64_t(slots), L.stride, C->ftier != nullptr)) != AMBPTT_OK) return s;
     if (C->ftier) {
       if (!C->ftier->finish()) return fail(AMBPTT_EINTERNAL, C->ftier->error());
       while (C->ev_file.size() < slots) {
@@ -1603,6 +1649,18 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
   return AMBPTT_OK;
 }
 
+ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const float* b, const void* h0,
+                         const float* c0, float* dW, float* db, float* dh0, float* dc0, double* loss,
+                         ambptt_stats* stats) {
+  ambptt_status s = check_run_args(C, x_seq, W, b, h0, c0);
+  if (s != AMBPTT_OK) return s;
+  if (!dW || !db || !dh0 || (C->L.G == 4 && !dc0)) return fail(AMBPTT_EINVAL, "missing gradient pointer");
+  if (C->p.slow_slots > 0 && C->interval_min == 0) {
+    if ((s = ambptt_calibrate(C, x_seq, W, b, h0, c0, nullptr, nullptr, nullptr)) != AMBPTT_OK) return s;
+  }
+  return run_pass(C, x_seq, W, b, h0, c0, dW, db, dh0, dc0, loss, stats);
+}
+
 ambptt_status ambptt_set_file_tier(ambptt_ctx* C, const char* dir, int64_t file_slots) {
   if (!C) return fail(AMBPTT_EINVAL, "ctx is NULL");
   if (file_slots < 0) return fail(AMBPTT_EINVAL, "file_slots must be >= 0");
@@ -1671,7 +1729,7 @@ void ambptt_destroy(ambptt_ctx* C) {
   for (auto& ev : C->ev_file) (void)hipEventDestroy(ev);
   if (C->ds) (void)hipStreamDestroy(C->ds);
   if (C->xs) (void)hipStreamDestroy(C->xs);
-  if (C->host) (void)hipHostFree(C->host);
+  free_host(C);
   if (C->host_loss) (void)hipHostFree(C->host_loss);
   if (C->prog_host) {
     (void)hipStreamSynchronize(C->cs);
