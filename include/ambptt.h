@@ -252,7 +252,10 @@ ambptt_status ambptt_create(const ambptt_problem* p, void* stream, ambptt_ctx** 
  * least the sizes ambptt_query reports, 256-byte aligned.  The slot pool is
  * the fixed fast-memory budget of Section 3 (s checkpoints); the library
  * keeps the pointers (it does not copy or free them) until the next bind or
- * ambptt_destroy.  EINVAL if a pointer is NULL, misaligned or too small. */
+ * ambptt_destroy.  The workspace may be NULL (any size): then only
+ * ambptt_run_noalloc runs passes, and ambptt_run and ambptt_calibrate fail
+ * with EINVAL.  EINVAL if the pool is NULL, or a pointer is misaligned or its
+ * buffer too small. */
 ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
                           void* workspace, size_t workspace_bytes);
 
@@ -290,7 +293,10 @@ ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
  * ambptt_interval_from_timings), "hadj_launch" (1,
  * default: on the fp32 path for large batches the adjoint's h-adjoint
  * product zbar_{t+1} W_h runs as a launch of its own, kernel class
- * AMBPTT_K_HADJ; 0: fused into the adjoint step's launch), "host_waits"
+ * AMBPTT_K_HADJ; 0: fused into the adjoint step's launch), "reserve" (1: allocate now the pinned host
+ * tier and resident-program staging that the current schedule needs, with
+ * the interval I_min, or 1 before calibration, which takes the most host
+ * slots; see ambptt_run_noalloc), "host_waits"
  * (when compute must wait for a host-tier copy still in flight: 1 the host
  * waits before enqueueing the dependent work, 0 a stream wait on the compute
  * stream; -1, default: 1 on the wide-batch bf16 and large-batch fp32 paths,
@@ -359,6 +365,32 @@ ambptt_status ambptt_calibrate(ambptt_ctx* ctx, const void* x_seq, const void* W
 ambptt_status ambptt_run(ambptt_ctx* ctx, const void* x_seq, const void* W, const float* b,
                          const void* h0, const float* c0, float* dW, float* db,
                          float* dh0, float* dc0, double* loss, ambptt_stats* stats);
+
+/* ambptt_run without allocation, for callers that cannot allocate memory
+ * while they run: code under HIP graph capture, tight serving loops, hosts
+ * that forbid hipMalloc.  The same pass, kernels and results as ambptt_run on
+ * the same context, but the workspace is the library's own static device
+ * array of 64 MiB (one per GPU, held until the process ends) instead of the
+ * bound one; the bound slot pool, the inputs and the outputs are the
+ * caller's as there.  It calls no hipMalloc, hipHostMalloc, hipFree or other
+ * allocating HIP or torch routine (the schedule is built on the host heap,
+ * as in ambptt_run), takes no timing samples beyond events already created,
+ * and therefore refuses, with EINVAL and nothing enqueued, what would need an
+ * allocation:
+ *   - a workspace (ambptt_query) larger than 64 MiB;
+ *   - a host-tier schedule before its interval is known (ambptt_calibrate,
+ *     or "interval_min" set);
+ *   - a pinned host tier or resident-program staging buffer that the pass
+ *     needs and that is not yet allocated: ambptt_set_int(ctx, "reserve", 1)
+ *     allocates them for the current schedule (an earlier ambptt_run of the
+ *     same schedule leaves them allocated too);
+ *   - a file tier (EUNSUPPORTED).
+ * Every call on one GPU shares the scratch array and leaves its contents
+ * behind; the pass clears what must start at zero.  Calls that overlap on
+ * one GPU (two threads, or two streams in flight) race on it: serialise them. */
+ambptt_status ambptt_run_noalloc(ambptt_ctx* ctx, const void* x_seq, const void* W, const float* b,
+                                 const void* h0, const float* c0, float* dW, float* db,
+                                 float* dh0, float* dc0, double* loss, ambptt_stats* stats);
 
 /* Canonical text (as ambptt_schedule_text) of the schedule the last
  * ambptt_run on this context executed; with "store_policy" 1 it holds the

@@ -16,7 +16,7 @@ EXPORTS = ["ambptt_version", "ambptt_revolve_advances", "ambptt_schedule_evals",
            "ambptt_schedule_text_starts", "ambptt_schedule_text_online", "ambptt_schedule_text_costs",
            "ambptt_interval_from_timings", "ambptt_set_step_costs",
            "ambptt_resident_program", "ambptt_query", "ambptt_last_error",
-           "ambptt_create", "ambptt_bind", "ambptt_set_int", "ambptt_set_file_tier", "ambptt_calibrate", "ambptt_run",
+           "ambptt_create", "ambptt_bind", "ambptt_set_int", "ambptt_set_file_tier", "ambptt_calibrate", "ambptt_run", "ambptt_run_noalloc",
            "ambptt_last_schedule_text", "ambptt_destroy"]
 
 
@@ -105,6 +105,8 @@ def load():
     L.ambptt_calibrate.restype = C.c_int
     L.ambptt_run.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, C.POINTER(C.c_double), C.POINTER(Stats)]
     L.ambptt_run.restype = C.c_int
+    L.ambptt_run_noalloc.argtypes = L.ambptt_run.argtypes
+    L.ambptt_run_noalloc.restype = C.c_int
     L.ambptt_destroy.argtypes = [vp]
     L.ambptt_destroy.restype = None
     _lib = L

@@ -204,6 +204,13 @@ class Runner:
     def run(self, x, W, b, h0, c0=None, out: dict | None = None) -> dict:
         return self._run(self.L.ambptt_run, x, W, b, h0, c0, out)
 
+    def run_noalloc(self, x, W, b, h0, c0=None, out: dict | None = None) -> dict:
+        """ambptt_run_noalloc: the same pass with the library's static scratch
+        as workspace; `out` must be given (this call allocates nothing)."""
+        if out is None:
+            raise ValueError("run_noalloc needs preallocated gradient buffers (out)")
+        return self._run(self.L.ambptt_run_noalloc, x, W, b, h0, c0, out)
+
     def _run(self, fn, x, W, b, h0, c0, out) -> dict:
         torch, s = self.torch, self.spec
         x, W, b, h0, c0 = self._inputs(x, W, b, h0, c0)

@@ -23,6 +23,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <stdexcept>
 #include <string>
 #include <vector>
@@ -79,6 +80,17 @@ struct Layout {
   size_t off_prog = 0, off_ready = 0, off_consumed = 0, off_oflag = 0, off_status = 0, off_Z = 0, off_P = 0;
   size_t off_dWp = 0, off_dbp = 0;
 };
+
+// Device memory for ambptt_run_noalloc: the workspace of a pass, for callers
+// that cannot allocate.  Every GPU that loads the library holds one copy until
+// the process ends; all passes on a GPU share it.  Host code never uses the
+// array's name as an address: ambptt_create looks up each device's copy with
+// hipGetSymbolAddress (with that device current) and keeps it in g_scratch.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch[kMaxDevices] = {};
 
 // Largest grid of the resident kernel the layout provisions for; the device's
 // own limit is checked when a context is created.
@@ -221,6 +233,7 @@ struct ambptt_ctx {
   std::vector<std::pair<char*, size_t>> host_chunks;
   size_t host_slot_bytes = 0, host_per_chunk = 0;
   char* host = nullptr;
+  bool no_alloc = false;  // inside ambptt_run_noalloc: any allocation is an error
   double* host_loss = nullptr;  // pinned scalar
   std::vector<hipEvent_t> ev_slot;
   std::vector<int> pend;  // 0 none, 1 store in flight, 2 prefetch in flight
@@ -367,6 +380,9 @@ ambptt_status ensure_host(ambptt_ctx* C, int64_t slots, size_t slot_bytes, bool 
     return AMBPTT_OK;
   }
   if (!contiguous && C->host_slot_bytes == slot_bytes && host_capacity(C) >= slots) return AMBPTT_OK;
+  if (C->no_alloc)
+    return fail(AMBPTT_EINVAL, "this pass needs " + std::to_string(need) +
+                                   " bytes of pinned host tier that are not reserved (ambptt_set_int \"reserve\")");
   free_host(C);
   const size_t per = contiguous ? size_t(slots) : std::max<size_t>(1, kHostChunkBytes / slot_bytes);
   for (int64_t h = 0; h < slots; h += int64_t(per)) {
@@ -470,7 +486,8 @@ struct Exec {
   template <class F>
   ambptt_status timed(int cls, F launch, hipStream_t strm = nullptr) {
     const bool compute = strm == nullptr || strm == C->cs;
-    const bool sample = C->timing_sample > 0 && (calls[cls] % C->timing_sample) == 0 && samples.size() < 4096;
+    const bool sample = C->timing_sample > 0 && (calls[cls] % C->timing_sample) == 0 && samples.size() < 4096 &&
+                        (!C->no_alloc || C->tpool.size() >= 2 * (samples.size() + 1));
     Sample smp{cls, nullptr, nullptr};
     if (sample) {
       const size_t need = 2 * (samples.size() + 1);
@@ -935,6 +952,8 @@ bool resident_possible(ambptt_ctx* C) {
 
 ambptt_status ensure_prog_host(ambptt_ctx* C, size_t ints) {
   if (ints <= C->prog_host_cap) return AMBPTT_OK;
+  if (C->no_alloc)
+    return fail(AMBPTT_EINVAL, "the resident program's staging buffer is not reserved (ambptt_set_int \"reserve\")");
   if (C->prog_host) {
     HIPCK(hipStreamSynchronize(C->cs));
     HIPCK(hipHostFree(C->prog_host));
@@ -1308,6 +1327,15 @@ ambptt_status ambptt_create(const ambptt_problem* p, void* stream, ambptt_ctx** 
   };
   hipError_t e;
   if ((e = hipGetDevice(&C->device)) != hipSuccess) return bail("hipGetDevice", e);
+  if (C->device >= 0 && C->device < kMaxDevices) {  // the device is current: its copy of the scratch array
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch[C->device]) {
+      void* ptr = nullptr;
+      if ((e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch))) != hipSuccess) return bail("hipGetSymbolAddress", e);
+      if (!ptr) return bail("hipGetSymbolAddress", hipErrorInvalidSymbol);
+      g_scratch[C->device] = (char*)ptr;
+    }
+  }
   if ((e = hipStreamCreateWithFlags(&C->xs, hipStreamNonBlocking)) != hipSuccess) return bail("hipStreamCreate", e);
   if ((e = hipStreamCreateWithFlags(&C->ds, hipStreamNonBlocking)) != hipSuccess) return bail("hipStreamCreate", e);
   C->ev_slot.resize(size_t(p->fast_slots), nullptr);
@@ -1327,15 +1355,17 @@ ambptt_status ambptt_create(const ambptt_problem* p, void* stream, ambptt_ctx** 
 
 ambptt_status ambptt_bind(ambptt_ctx* C, void* slot_pool, size_t pool_bytes, void* workspace, size_t ws_bytes) {
   if (!C) return fail(AMBPTT_EINVAL, "ctx is NULL");
-  if (!slot_pool || !workspace) return fail(AMBPTT_EINVAL, "slot pool and workspace are required");
+  if (!slot_pool) return fail(AMBPTT_EINVAL, "the slot pool is required");
   if (((uintptr_t)slot_pool % kAlign) || ((uintptr_t)workspace % kAlign))
     return fail(AMBPTT_EINVAL, "slot pool and workspace must be 256-byte aligned");
   if (pool_bytes < C->L.stride * (size_t)C->p.fast_slots) return fail(AMBPTT_EINVAL, "slot pool too small");
-  if (ws_bytes < C->L.total) return fail(AMBPTT_EINVAL, "workspace too small");
+  if (workspace && ws_bytes < C->L.total) return fail(AMBPTT_EINVAL, "workspace too small");
   C->pool = (char*)slot_pool;
   C->ws = (char*)workspace;
   return AMBPTT_OK;
 }
+
+static ambptt_status reserve(ambptt_ctx* C);
 
 ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
   if (!C || !key) return fail(AMBPTT_EINVAL, "ctx/key is NULL");
@@ -1394,6 +1424,9 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
   } else if (k == "resident_timeout_ms") {
     if (v < 0 || v > 600000) return fail(AMBPTT_EINVAL, "resident_timeout_ms must be in [0, 600000]");
     C->res_timeout_ms = v;
+  } else if (k == "reserve") {
+    if (v != 1) return fail(AMBPTT_EINVAL, "reserve: 1 allocates what the current schedule needs");
+    return reserve(C);
   } else if (k == "interval_min") {
     if (v < 0) return fail(AMBPTT_EINVAL, "interval_min must be >= 0");
     C->interval_min = v;
@@ -1406,7 +1439,8 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
 static ambptt_status check_run_args(ambptt_ctx* C, const void* x_seq, const void* W, const float* b, const void* h0,
                                     const float* c0) {
   if (!C) return fail(AMBPTT_EINVAL, "ctx is NULL");
-  if (!C->pool || !C->ws) return fail(AMBPTT_EINVAL, "ambptt_bind has not been called");
+  if (!C->pool) return fail(AMBPTT_EINVAL, "ambptt_bind has not been called");
+  if (!C->ws) return fail(AMBPTT_EINVAL, "no workspace is bound (only ambptt_run_noalloc runs without one)");
   if ((!x_seq && C->p.input > 0) || !W || !b || !h0) return fail(AMBPTT_EINVAL, "missing input pointer");
   if (C->L.G == 4 && !c0) return fail(AMBPTT_EINVAL, "LSTM needs c0");
   return AMBPTT_OK;
@@ -1527,6 +1561,37 @@ static int64_t host_slots_needed(const ambptt_ctx* C, const Plan& plan, bool dyn
   int64_t slots = dynamic ? std::min<int64_t>(slow_capacity(C), C->p.n_steps) : plan.host_slots_used;
   if (C->ftier) slots = std::min<int64_t>(slots, C->p.slow_slots);
   return slots;
+}
+
+// Allocates now what a pass of the current schedule would otherwise allocate
+// on first use (the pinned host tier and the resident program's staging), so
+// that ambptt_run_noalloc can run it.  The interval is the context's I_min,
+// or 1 (the most host slots any interval takes) before calibration.
+static ambptt_status reserve(ambptt_ctx* C) {
+  const ambptt_problem& p = C->p;
+  Plan plan;
+  std::vector<int32_t> prog;
+  const bool res = resident_possible(C);
+  try {
+    plan = pass_plan(C);
+    if (res) {
+      ResidentCounts rc;
+      prog = compile_resident(plan, p.fast_slots, C->elide_prefetch, &rc);
+    }
+  } catch (const std::length_error& e) {
+    return fail(AMBPTT_EUNSUPPORTED, e.what());
+  } catch (const std::exception& e) {
+    return fail(AMBPTT_EINTERNAL, e.what());
+  }
+  ambptt_status s;
+  if (res) {
+    if ((s = ensure_prog_host(C, prog.size() + 4)) != AMBPTT_OK) return s;
+    if (plan.async) return ensure_host(C, plan.host_slots_used, size_t(C->L.r_nwg) * 1024, true);
+    return AMBPTT_OK;
+  }
+  const bool dynamic = C->store_policy == 1 && plan.async && p.n_steps >= 2;
+  if (plan.async) return ensure_host(C, host_slots_needed(C, plan, dynamic), C->L.stride, C->ftier != nullptr);
+  return AMBPTT_OK;
 }
 
 // One pass on the context's bound buffers (the workspace is C->ws).
@@ -1659,6 +1724,31 @@ ambptt_status ambptt_run(ambptt_ctx* C, const void* x_seq, const void* W, const 
     if ((s = ambptt_calibrate(C, x_seq, W, b, h0, c0, nullptr, nullptr, nullptr)) != AMBPTT_OK) return s;
   }
   return run_pass(C, x_seq, W, b, h0, c0, dW, db, dh0, dc0, loss, stats);
+}
+
+ambptt_status ambptt_run_noalloc(ambptt_ctx* C, const void* x_seq, const void* W, const float* b, const void* h0,
+                                 const float* c0, float* dW, float* db, float* dh0, float* dc0, double* loss,
+                                 ambptt_stats* stats) {
+  if (!C) return fail(AMBPTT_EINVAL, "ctx is NULL");
+  if (!C->pool) return fail(AMBPTT_EINVAL, "ambptt_bind has not been called");
+  if ((!x_seq && C->p.input > 0) || !W || !b || !h0) return fail(AMBPTT_EINVAL, "missing input pointer");
+  if (C->L.G == 4 && !c0) return fail(AMBPTT_EINVAL, "LSTM needs c0");
+  if (!dW || !db || !dh0 || (C->L.G == 4 && !dc0)) return fail(AMBPTT_EINVAL, "missing gradient pointer");
+  if (C->L.total > kScratchBytes)
+    return fail(AMBPTT_EINVAL, "the workspace of this problem (" + std::to_string(C->L.total) +
+                                   " bytes) exceeds the static scratch of " + std::to_string(kScratchBytes) + " bytes");
+  if (C->p.slow_slots > 0 && C->interval_min == 0)
+    return fail(AMBPTT_EINVAL, "the interval is not set: call ambptt_calibrate or set \"interval_min\" first");
+  if (C->ftier) return fail(AMBPTT_EUNSUPPORTED, "the file tier is not available without allocation");
+  if (C->device < 0 || C->device >= kMaxDevices || !g_scratch[C->device])
+    return fail(AMBPTT_EINTERNAL, "no scratch address for this context's device");
+  char* const bound = C->ws;
+  C->ws = g_scratch[C->device];
+  C->no_alloc = true;
+  const ambptt_status s = run_pass(C, x_seq, W, b, h0, c0, dW, db, dh0, dc0, loss, stats);
+  C->no_alloc = false;
+  C->ws = bound;
+  return s;
 }
 
 ambptt_status ambptt_set_file_tier(ambptt_ctx* C, const char* dir, int64_t file_slots) {
