@@ -290,7 +290,18 @@ ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
  * stats mode 3; EINVAL together with "store_policy" 1, EUNSUPPORTED over a
  * file tier), "interval_rule" (1, default: ambptt_calibrate picks the
  * interval with the least modelled time per step; 0: ceil(T_T / T_A), see
- * ambptt_interval_from_timings), "hadj_launch" (1,
+ * ambptt_interval_from_timings), "test_copy_delay_us" (tests of the stream
+ * ordering, per-step path: a host function that holds the copy stream this
+ * many microseconds, at most 100000, before every store and prefetch, and
+ * the weight-gradient stream before every window on it, so that the waits
+ * of compute on them are taken; 0 by default), "test_poison" (1: a prefetch
+ * first fills its fast slot with NaN bytes on the copy stream, so that
+ * compute reading the slot before the prefetch has landed spoils the
+ * gradients), "lds_gemm" (fp32 path for large batches: 1, default, runs the gate
+ * product with its cell epilogue and the h-adjoint product on LDS-tiled
+ * kernels (128 x 256 and 64 x 128 tiles) where their tiles fill the device
+ * at least half; 2 wherever their shape constraints hold; 0 never: the
+ * direct-load kernels), "hadj_launch" (1,
  * default: on the fp32 path for large batches the adjoint's h-adjoint
  * product zbar_{t+1} W_h runs as a launch of its own, kernel class
  * AMBPTT_K_HADJ; 0: fused into the adjoint step's launch), "reserve" (1: allocate now the pinned host

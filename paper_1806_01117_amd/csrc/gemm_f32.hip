@@ -1,0 +1,357 @@
+// LDS-tiled fp32 kernels for the large-batch recurrent cells on gfx950
+// (v_mfma_f32_16x16x4_f32): the forward step and the adjoint's gate
+// recomputation of a tanh RNN (G = 1) or LSTM (G = 4) with the cell epilogue
+// fused, and the adjoint's h-adjoint product hbar = zbar W_h.
+//
+// Both are "NT" products whose operands are contiguous in the reduction
+// index k:
+//   gate product  z[m][n] = sum_k [x | h][m][k] W[n][k]       (K = D + H)
+//   h-adjoint     hbar[m][j] = sum_k zbar[m][k] WhT[j][k]     (K = G H)
+// A workgroup of 4 waves owns one output tile.  The tile's operands pass
+// through LDS in stages of kKT reduction indices, double-buffered: while the
+// waves multiply stage s, the loads of stage s + 1 are in flight in
+// registers, and they are written to the other LDS buffer before the one
+// barrier of the stage.  LDS rows are padded by 4 floats, so that the 16
+// rows one MFMA operand read touches (16 bytes each, at one column) fall on
+// distinct banks.
+//
+// Fragments: lane l reads 4 consecutive k of row l & 15 at column 4 (l >> 4)
+// of a 16-wide chunk, and its 4 components feed 4 MFMAs; A and B use the
+// same mapping, so the 4 MFMAs together cover the chunk.
+//
+// Tiles are placed XCD-aware: workgroup i runs on XCD i % 8, and the row
+// tiles that read the same weight rows are given consecutive slots of one
+// XCD, so the weights stream from HBM once per launch and are shared through
+// that XCD's L2.
+#include <hip/hip_runtime.h>
+
+#include "ambptt.h"
+#include "kernels.hpp"
+
+namespace ambptt {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float sigm(float z) { return 1.0f / (1.0f + __expf(-z)); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// (row tile, column tile) of workgroup i: the mt row tiles of one column tile
+// share an XCD when the column tiles divide evenly over the 8 XCDs.
+__device__ __forceinline__ void tile_of(int i, int mt, int nt, int* tm, int* tn) {
+  if (nt % 8 == 0) {
+    const int xcd = i & 7, k = i >> 3;
+    *tn = xcd * (nt >> 3) + k / mt;
+    *tm = k % mt;
+  } else {
+    *tm = i % mt;
+    *tn = i / mt;
+  }
+}
+
+// ---- gate product with the cell epilogue ------------------------------------
+// Tile: 128 batch rows x 256 gate columns (LSTM: 64 units x 4 gates; RNN:
+// 256 units).  Wave (wm, wn) computes rows 64 wm .. + 63 and, for the LSTM,
+// units 32 wn .. + 31 of all four gates (8 blocks of 16 x 16: block
+// nb = 4 u + g is gate g of units 16 u .. + 15), so a lane holds the four
+// gates of its (row, unit) pairs in the same accumulator element; for the RNN
+// units 128 wn .. + 127.
+constexpr int kCM = 128, kCN = 256, kKT = 32, kLd = kKT + 4;
+
+template <int G, int MODE>
+__global__ __launch_bounds__(256, 1) void cell_gemm_f32(StepArgs a) {
+  __shared__ float As[2][kCM][kLd];
+  __shared__ float Bs[2][kCN][kLd];
+  __shared__ float red[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int r = lane & 15, q = lane >> 4;
+  const int B = a.B, D = a.D, H = a.H, K1 = D + H;
+  const int mt = (B + kCM - 1) / kCM, nt = G * H / kCN;
+  int tm, tn;
+  tile_of(blockIdx.x, mt, nt, &tm, &tn);
+  const int m0 = tm * kCM;
+  const int j0 = tn * (kCN / G);  // first unit of the tile
+
+  // loader: thread t moves rows t / 8 + 32 p, float4 column t % 8 of a stage
+  const int lr = tid >> 3, lc = 4 * (tid & 7);
+  const float* x = (const float*)a.x;
+  const float* h = (const float*)a.h;
+  const float* W = (const float*)a.W;
+  int arow[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) arow[p] = min(m0 + lr + 32 * p, B - 1);  // rows >= B: clamped, discarded
+  const float* brow[8];
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    const int c = lr + 32 * p;
+    const int n = G == 4 ? (c >> 6) * H + j0 + (c & 63) : j0 + c;
+    brow[p] = W + (size_t)n * K1 + lc;
+  }
+  f4 ra[4], rb[8];
+  auto load = [&](int st) {
+    const int k0 = st * kKT;
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+      ra[p] = k0 < D ? *(const f4*)(x + (size_t)arow[p] * D + k0 + lc)
+                     : *(const f4*)(h + (size_t)arow[p] * H + (k0 - D) + lc);
+#pragma unroll
+    for (int p = 0; p < 8; ++p) rb[p] = *(const f4*)(brow[p] + k0);
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) *(f4*)&As[buf][lr + 32 * p][lc] = ra[p];
+#pragma unroll
+    for (int p = 0; p < 8; ++p) *(f4*)&Bs[buf][lr + 32 * p][lc] = rb[p];
+  };
+
+  f4 acc[4][8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb) acc[i][nb] = f4{0.f, 0.f, 0.f, 0.f};
+  // LDS row of B block nb of this wave
+  int bcol[8];
+#pragma unroll
+  for (int nb = 0; nb < 8; ++nb) bcol[nb] = G == 4 ? (nb & 3) * 64 + wn * 32 + 16 * (nb >> 2) : wn * 128 + 16 * nb;
+
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int kk = 0; kk < kKT / 16; ++kk) {
+      f4 af[4], bf[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = *(const f4*)&As[buf][wm * 64 + 16 * i + r][16 * kk + 4 * q];
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) bf[nb] = *(const f4*)&Bs[buf][bcol[nb] + r][16 * kk + 4 * q];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int nb = 0; nb < 8; ++nb) {
+          acc[i][nb] = mfma4(af[i].x, bf[nb].x, acc[i][nb]);
+          acc[i][nb] = mfma4(af[i].y, bf[nb].y, acc[i][nb]);
+          acc[i][nb] = mfma4(af[i].z, bf[nb].z, acc[i][nb]);
+          acc[i][nb] = mfma4(af[i].w, bf[nb].w, acc[i][nb]);
+        }
+    }
+  };
+  // stages 0 .. nst - 2 load the next stage while they multiply; the last one
+  // only multiplies (no branch inside the loop)
+  const int nst = K1 / kKT;
+  load(0);
+  store(0);
+  __syncthreads();
+  for (int st = 0; st + 1 < nst; ++st) {
+    load(st + 1);
+    compute(st & 1);
+    store((st + 1) & 1);
+    __syncthreads();
+  }
+  compute((nst - 1) & 1);
+
+  // ---- epilogue: accumulator element v of lane l is row 4 (l >> 4) + v,
+  //      column l & 15 of its 16 x 16 block ------------------------------------
+  const int GH = G * H;
+  float lterm = 0.f;
+  constexpr int NU = G == 4 ? 2 : 8;  // unit blocks per wave
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int u = 0; u < NU; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int m = m0 + wm * 64 + 16 * i + 4 * q + v;
+        const int j = G == 4 ? j0 + wn * 32 + 16 * u + r : j0 + wn * 128 + 16 * u + r;
+        if (m >= B) continue;
+        const size_t o = (size_t)m * H + j;
+        float h1, c1 = 0.f, tc = 0.f, ig = 0.f, fg = 0.f, gg = 0.f, og = 0.f, cold = 0.f;
+        if (G == 4) {
+          ig = sigm(acc[i][4 * u][v] + a.bias[j]);
+          fg = sigm(acc[i][4 * u + 1][v] + a.bias[H + j]);
+          gg = tanhf(acc[i][4 * u + 2][v] + a.bias[2 * H + j]);
+          og = sigm(acc[i][4 * u + 3][v] + a.bias[3 * H + j]);
+          cold = a.c[o];
+          c1 = fg * cold + ig * gg;
+          tc = tanhf(c1);
+          h1 = og * tc;
+        } else {
+          h1 = tanhf(acc[i][u][v] + a.bias[j]);
+        }
+        if (MODE == kForward) {
+          ((float*)a.h_out)[o] = h1;
+          if (G == 4) a.c_out[o] = c1;
+          continue;
+        }
+        // adjoint: loss term of h_{t+1} and its seed dL/dh_{t+1}
+        float sd = 0.f;
+        if (a.loss == AMBPTT_LOSS_MEAN_SQ_ALL) {
+          sd = 2.f * h1 * a.inv_bh;
+          lterm += h1 * h1;
+        } else if (a.last) {
+          if (a.loss == AMBPTT_LOSS_HALF_SQ_LAST) {
+            sd = h1;
+            lterm += h1 * h1;
+          } else {
+            sd = a.inv_bh;
+            lterm += h1;
+          }
+        }
+        const float hb = (a.first ? 0.f : a.hbar_in[o]) + sd;
+        float* zo = (float*)a.zbar_out + (size_t)m * GH + j;
+        if (G == 4) {
+          const float cb = a.first ? 0.f : a.cbar_in[o];
+          const float ob = hb * tc;
+          const float ch = cb + hb * og * (1.f - tc * tc);
+          zo[0] = ch * gg * ig * (1.f - ig);
+          zo[H] = ch * cold * fg * (1.f - fg);
+          zo[2 * H] = ch * ig * (1.f - gg * gg);
+          zo[3 * H] = ob * og * (1.f - og);
+          a.cbar_out[o] = ch * fg;
+        } else {
+          zo[0] = hb * (1.f - h1 * h1);
+        }
+        ((float*)a.hwin_out)[o] = ((const float*)a.h)[o];
+      }
+  if (MODE == kAdjoint) {  // the four waves' loss terms, summed in wave order
+    const float s = wave_sum(lterm);
+    if (lane == 0) red[wave] = s;
+    __syncthreads();
+    if (tid == 0) a.loss_acc[blockIdx.x] += (double)red[0] + (double)red[1] + (double)red[2] + (double)red[3];
+  }
+}
+
+// ---- h-adjoint product: out = A B^T (+ add) -----------------------------------
+// Tile: 64 rows x 128 columns; wave (wm, wn) computes rows 32 wm .. + 31 and
+// columns 64 wn .. + 63 (2 x 4 blocks); stages of kPT = 64 reduction indices.
+constexpr int kPM = 64, kPN = 128, kPT = 64, kPLd = kPT + 4;
+
+__global__ __launch_bounds__(256, 1) void prod_gemm_f32(ProdArgs a) {
+  __shared__ float As[2][kPM][kPLd];
+  __shared__ float Bs[2][kPN][kPLd];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int r = lane & 15, q = lane >> 4;
+  const int M = a.M, N = a.N, K = a.K;
+  const int mt = (M + kPM - 1) / kPM, nt = N / kPN;
+  int tm, tn;
+  tile_of(blockIdx.x, mt, nt, &tm, &tn);
+  const int m0 = tm * kPM, n0 = tn * kPN;
+
+  // loader: thread t moves rows t / 16 + 16 p, float4 column t % 16 of a stage
+  const int lr = tid >> 4, lc = 4 * (tid & 15);
+  const float* A = (const float*)a.A;
+  const float* Bm = (const float*)a.B;
+  const float* arow[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) arow[p] = A + (size_t)min(m0 + lr + 16 * p, M - 1) * K + lc;
+  const float* brow[8];
+#pragma unroll
+  for (int p = 0; p < 8; ++p) brow[p] = Bm + (size_t)(n0 + lr + 16 * p) * K + lc;
+  f4 ra[4], rb[8];
+  auto load = [&](int st) {
+    const int k0 = st * kPT;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) ra[p] = *(const f4*)(arow[p] + k0);
+#pragma unroll
+    for (int p = 0; p < 8; ++p) rb[p] = *(const f4*)(brow[p] + k0);
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) *(f4*)&As[buf][lr + 16 * p][lc] = ra[p];
+#pragma unroll
+    for (int p = 0; p < 8; ++p) *(f4*)&Bs[buf][lr + 16 * p][lc] = rb[p];
+  };
+
+  f4 acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) acc[i][nb] = f4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int kk = 0; kk < kPT / 16; ++kk) {
+      f4 af[2], bf[4];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) af[i] = *(const f4*)&As[buf][wm * 32 + 16 * i + r][16 * kk + 4 * q];
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) bf[nb] = *(const f4*)&Bs[buf][wn * 64 + 16 * nb + r][16 * kk + 4 * q];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) {
+          acc[i][nb] = mfma4(af[i].x, bf[nb].x, acc[i][nb]);
+          acc[i][nb] = mfma4(af[i].y, bf[nb].y, acc[i][nb]);
+          acc[i][nb] = mfma4(af[i].z, bf[nb].z, acc[i][nb]);
+          acc[i][nb] = mfma4(af[i].w, bf[nb].w, acc[i][nb]);
+        }
+    }
+  };
+  const int nst = K / kPT;
+  load(0);
+  store(0);
+  __syncthreads();
+  for (int st = 0; st + 1 < nst; ++st) {
+    load(st + 1);
+    compute(st & 1);
+    store((st + 1) & 1);
+    __syncthreads();
+  }
+  compute((nst - 1) & 1);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int m = m0 + wm * 32 + 16 * i + 4 * q + v;
+      if (m >= M) continue;
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        const size_t o = (size_t)m * N + n0 + wn * 64 + 16 * nb + r;
+        a.out[o] = a.add ? a.add[o] + acc[i][nb][v] : acc[i][nb][v];
+      }
+    }
+}
+
+}  // namespace
+
+bool cell_gemm_f32_fits(int G, int B, int D, int H) {
+  return (G == 1 || G == 4) && B >= 1 && D % kKT == 0 && H % kKT == 0 && H >= kKT && (G * H) % kCN == 0;
+}
+
+int cell_gemm_f32_tiles(int G, int B, int H) { return ((B + kCM - 1) / kCM) * (G * H / kCN); }
+
+hipError_t launch_cell_gemm_f32(int G, int mode, const StepArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (!cell_gemm_f32_fits(G, a.B, a.D, a.H) || (mode == kAdjoint && !a.first && !a.hbar_in)) return hipErrorInvalidValue;
+  const dim3 grid(cell_gemm_f32_tiles(G, a.B, a.H)), block(256);
+  if (G == 4) {
+    if (mode == kForward) hipExtLaunchKernelGGL((cell_gemm_f32<4, kForward>), grid, block, 0, s, e0, e1, 0, a);
+    else if (mode == kAdjoint) hipExtLaunchKernelGGL((cell_gemm_f32<4, kAdjoint>), grid, block, 0, s, e0, e1, 0, a);
+    else return hipErrorInvalidValue;
+  } else {
+    if (mode == kForward) hipExtLaunchKernelGGL((cell_gemm_f32<1, kForward>), grid, block, 0, s, e0, e1, 0, a);
+    else if (mode == kAdjoint) hipExtLaunchKernelGGL((cell_gemm_f32<1, kAdjoint>), grid, block, 0, s, e0, e1, 0, a);
+    else return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+bool prod_gemm_f32_fits(int M, int N, int K) { return M >= 1 && K >= kPT && K % kPT == 0 && N % kPN == 0; }
+
+int prod_gemm_f32_tiles(int M, int N) { return ((M + kPM - 1) / kPM) * (N / kPN); }
+
+hipError_t launch_prod_gemm_f32(const ProdArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (!prod_gemm_f32_fits(a.M, a.N, a.K)) return hipErrorInvalidValue;
+  const dim3 grid(prod_gemm_f32_tiles(a.M, a.N)), block(256);
+  hipExtLaunchKernelGGL(prod_gemm_f32, grid, block, 0, s, e0, e1, 0, a);
+  return hipGetLastError();
+}
+
+}  // namespace ambptt

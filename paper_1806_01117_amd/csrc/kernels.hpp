@@ -127,8 +127,9 @@ int resident_max_k(int G);
 int resident_max_h(int G);
 // octet size for ng unit groups of hidden size H (0: the kernel cannot take it)
 int resident_octet(int ng, int H);
-// workgroups of the resident kernel that can be resident at once on device dev
-hipError_t resident_capacity(int G, int* blocks);
+// workgroups of the resident kernel variant that (G, D, H) launches that can
+// be resident at once on the current device
+hipError_t resident_capacity(int G, int D, int H, int* blocks);
 // cooperative: hipLaunchCooperativeKernel (the runtime guarantees that the
 // whole grid is resident); otherwise a plain launch of a grid that fits
 hipError_t launch_resident(int G, const ResidentArgs& a, hipStream_t s, bool cooperative);
@@ -149,6 +150,17 @@ hipError_t launch_step(int G, int mode, const StepCfg& cfg, const StepArgs& a, h
 hipError_t launch_dw(const DwArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 // fp32 out = A B^T (+ add): the adjoint's h-adjoint product zbar W_h through W_h^T (K % 16 == 0, N % 16 == 0)
 hipError_t launch_prod_f32(const ProdArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+// LDS-tiled fp32 kernels for large batches (gemm_f32.hip): the gate product
+// with the cell epilogue on 128 x 256 tiles (forward, and the adjoint when its
+// h-adjoint product runs as a launch of its own), and that product on
+// 64 x 128 tiles.  *_fits: the shape constraints; *_tiles: workgroups.
+bool cell_gemm_f32_fits(int G, int B, int D, int H);
+int cell_gemm_f32_tiles(int G, int B, int H);
+hipError_t launch_cell_gemm_f32(int G, int mode, const StepArgs& a, hipStream_t s, hipEvent_t e0 = nullptr,
+                                hipEvent_t e1 = nullptr);
+bool prod_gemm_f32_fits(int M, int N, int K);
+int prod_gemm_f32_tiles(int M, int N);
+hipError_t launch_prod_gemm_f32(const ProdArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 // 128 x 128-tile fp32 weight gradient for GH, D + H >= 256 (launch_dw picks it when it fits).
 bool dw_f32_big_fits(const DwArgs& a);
 hipError_t launch_dw_f32_big(const DwArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1);

@@ -26,6 +26,7 @@
 #include <mutex>
 #include <stdexcept>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "ambptt.h"
@@ -181,6 +182,8 @@ Layout make_layout(const ambptt_problem* p, int window) {
       L.loss_slots = std::max(L.loss_slots, L.r_nwg);
     }
   }
+  if (!L.small && !L.mlp && p->dtype == AMBPTT_F32 && cell_gemm_f32_fits(L.G, p->batch, p->input, p->hidden))
+    L.loss_slots = std::max(L.loss_slots, cell_gemm_f32_tiles(L.G, p->batch, p->hidden));
   size_t o = 0;
   L.off_live[0] = o; o += L.stride;
   L.off_live[1] = o; o += L.stride;
@@ -264,6 +267,12 @@ struct ambptt_ctx {
   int64_t cost_plan_key[3] = {-1, -1, -1};  // interval_min, slow capacity, costs version
   int64_t costs_version = 0;
   bool hadj_launch = true;  // fp32 large-batch path: the adjoint's h-adjoint product as a launch of its own
+  int lds_gemm = 1;         // fp32 large-batch path: LDS-tiled kernels (0 off, 1 when they fill the device, 2 always)
+  // tests of the stream ordering: a host-side delay before every host-tier
+  // copy and weight-gradient window on their streams, and NaN bytes written
+  // into a fast slot before a prefetch refills it
+  int64_t test_copy_delay_us = 0;
+  bool test_poison = false;
   int host_waits = -1;      // slot dependencies on host-tier copies: 1 waited for on the host, 0 stream waits, -1 by path
   hipEvent_t ev_end[8] = {};  // end events recorded by compute dispatches (host-tier copies and sweep pacing wait on them)
   Plan last_plan;        // the schedule the last ambptt_run executed
@@ -406,6 +415,9 @@ char* host_slot(const ambptt_ctx* C, int64_t h) {
   return C->host_chunks[size_t(h) / C->host_per_chunk].first + (size_t(h) % C->host_per_chunk) * C->host_slot_bytes;
 }
 
+// Stream callback of the copy-delay test knob: holds its stream for a bounded time.
+void delay_cb(void* us) { std::this_thread::sleep_for(std::chrono::microseconds((intptr_t)us)); }
+
 struct Sample {
   int cls;
   hipEvent_t a, b;
@@ -439,6 +451,8 @@ struct Exec {
   unsigned end_cur = 0;           // next event of the ring (8 deep: reused 8 launches later)
   bool wide = false;       // wide-batch bf16 kernels
   bool sep32 = false;      // fp32 step kernels with the h-adjoint product as a launch of its own
+  bool lds_cell = false;   // ... whose gate products run on the LDS-tiled kernel
+  bool lds_prod = false;   // ... whose h-adjoint products run on the LDS-tiled kernel
   float* hbuf = nullptr;   // the adjoint's product (fp32 [B][H]) on those two paths
 
   Exec(ambptt_ctx* c, const void* x_, const void* W_, const float* b_)
@@ -446,6 +460,13 @@ struct Exec {
     WhT = C->ws + L.off_wht;
     wide = L.wide && C->wide_opt;
     sep32 = L.hsep && C->hadj_launch;
+    if (L.hsep) {
+      const int G = L.G, B = p.batch, D = p.input, H = p.hidden;
+      lds_cell = C->lds_gemm > 0 && cell_gemm_f32_fits(G, B, D, H) &&
+                 (C->lds_gemm == 2 || cell_gemm_f32_tiles(G, B, H) >= 128);
+      lds_prod = sep32 && C->lds_gemm > 0 && prod_gemm_f32_fits(B, H, G * H) &&
+                 (C->lds_gemm == 2 || prod_gemm_f32_tiles(B, H) >= 128);
+    }
     if (wide || sep32) hbuf = (float*)(C->ws + L.off_hbar);
   }
   const void* x_at(int64_t t) const { return x + (size_t)t * p.batch * p.input * L.dsize; }
@@ -526,8 +547,15 @@ struct Exec {
     return a;
   }
 
+  // the fp32 h-adjoint product out = zbar W_h
+  hipError_t prod32(const ProdArgs& pa, hipEvent_t e0, hipEvent_t e1) const {
+    return lds_prod ? launch_prod_gemm_f32(pa, C->cs, e0, e1) : launch_prod_f32(pa, C->cs, e0, e1);
+  }
+
   hipError_t launch(int mode, const StepArgs& a, hipEvent_t e0, hipEvent_t e1) const {
     if (wide && mode != kFinal) return launch_cell_wide(L.G, mode, a, C->cs, e0, e1);
+    if (lds_cell && (mode == kForward || (mode == kAdjoint && (a.first || a.hbar_in))))
+      return launch_cell_gemm_f32(L.G, mode, a, C->cs, e0, e1);
     return L.small ? launch_step_small(L.G, p.dtype == AMBPTT_BF16, mode, a, C->cs, e0, e1)
                    : launch_step(L.G, mode, L.cfg, a, C->cs, e0, e1);
   }
@@ -639,7 +667,7 @@ struct Exec {
       if ((wide || sep32) && !first) {  // hbar_{t+1} = zbar_{t+1} W_h
         ProdArgs pa{a.zbar_in, WhT, nullptr, hbuf, p.batch, p.hidden, L.G * p.hidden};
         s = timed(AMBPTT_K_HADJ, [&](hipEvent_t e0, hipEvent_t e1) {
-          return wide ? launch_prod_nt(pa, C->cs, e0, e1) : launch_prod_f32(pa, C->cs, e0, e1);
+          return wide ? launch_prod_nt(pa, C->cs, e0, e1) : prod32(pa, e0, e1);
         });
         if (s != AMBPTT_OK) return s;
         a.hbar_in = hbuf;
@@ -674,6 +702,7 @@ struct Exec {
       if (own) {
         HIPCK(hipEventRecord(C->ev_c2, C->cs));
         HIPCK(hipStreamWaitEvent(C->ds, C->ev_c2, 0));
+        if ((s = test_delay(C->ds)) != AMBPTT_OK) return s;
       }
       s = timed(
           AMBPTT_K_DW,
@@ -714,13 +743,19 @@ struct Exec {
     if (wide || sep32) {  // dL/dh_0 = zbar_0 W_h, dL/dc_0 = cbar_0
       ProdArgs pa{a.zbar_in, WhT, nullptr, dh0, p.batch, p.hidden, L.G * p.hidden};
       ambptt_status s = timed(AMBPTT_K_OTHER, [&](hipEvent_t e0, hipEvent_t e1) {
-        return wide ? launch_prod_nt(pa, C->cs, e0, e1) : launch_prod_f32(pa, C->cs, e0, e1);
+        return wide ? launch_prod_nt(pa, C->cs, e0, e1) : prod32(pa, e0, e1);
       });
       if (s != AMBPTT_OK) return s;
       if (L.G == 4) HIPCK(hipMemcpyAsync(dc0, a.cbar_in, (size_t)p.batch * p.hidden * 4, hipMemcpyDeviceToDevice, C->cs));
       return AMBPTT_OK;
     }
     return timed(AMBPTT_K_OTHER, [&](hipEvent_t e0, hipEvent_t e1) { return launch(kFinal, a, e0, e1); });
+  }
+
+  // the copy-delay test knob: the next work on stream `strm` starts late
+  ambptt_status test_delay(hipStream_t strm) {
+    if (C->test_copy_delay_us > 0) HIPCK(hipLaunchHostFunc(strm, delay_cb, (void*)(intptr_t)C->test_copy_delay_us));
+    return AMBPTT_OK;
   }
 
   ambptt_status copy_state(char* dst, char* src) {
@@ -870,6 +905,7 @@ struct Exec {
           char* dst = host_slot(C, h);
           if (C->ftier && !(dst = C->ftier->store_buffer(h))) return fail(AMBPTT_EINTERNAL, C->ftier->error());
           if ((s = copy_after_compute()) != AMBPTT_OK) return s;
+          if ((s = test_delay(C->xs)) != AMBPTT_OK) return s;
           HIPCK(hipMemcpyAsync(dst, slot(k), L.state_bytes, hipMemcpyDeviceToHost, C->xs));
           HIPCK(hipEventRecord(C->ev_slot[size_t(k)], C->xs));
           if (C->ftier) {  // written behind to the file once the copy has landed
@@ -898,6 +934,10 @@ struct Exec {
           const char* src = host_slot(C, h);
           if (C->ftier && !(src = C->ftier->prefetch_buffer(h))) return fail(AMBPTT_EINTERNAL, C->ftier->error());
           if ((s = copy_after_compute()) != AMBPTT_OK) return s;
+          // the poison test knob: until the prefetch lands the slot holds NaNs,
+          // so compute reading it too early shows in the gradients
+          if (C->test_poison) HIPCK(hipMemsetAsync(slot(k), 0xFF, L.state_bytes, C->xs));
+          if ((s = test_delay(C->xs)) != AMBPTT_OK) return s;
           HIPCK(hipMemcpyAsync(slot(k), src, L.state_bytes, hipMemcpyHostToDevice, C->xs));
           HIPCK(hipEventRecord(C->ev_slot[size_t(k)], C->xs));
           if (C->ftier) {  // the buffer takes the slot h - R from the file once this copy is done
@@ -941,7 +981,7 @@ bool resident_possible(ambptt_ctx* C) {
   if (!C->L.res || C->path_opt == 1 || C->store_policy == 1 || C->ftier) return false;
   if (C->res_cap < 0) {
     int cap = 0;
-    if (resident_capacity(C->L.G, &cap) != hipSuccess) {
+    if (resident_capacity(C->L.G, C->p.input, C->p.hidden, &cap) != hipSuccess) {
       (void)hipGetLastError();
       cap = 0;
     }
@@ -1397,6 +1437,14 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
   } else if (k == "host_waits") {
     if (v < -1 || v > 1) return fail(AMBPTT_EINVAL, "host_waits must be -1 (by path), 0 or 1");
     C->host_waits = int(v);
+  } else if (k == "test_copy_delay_us") {
+    if (v < 0 || v > 100000) return fail(AMBPTT_EINVAL, "test_copy_delay_us must be 0 .. 100000");
+    C->test_copy_delay_us = v;
+  } else if (k == "test_poison") {
+    C->test_poison = v != 0;
+  } else if (k == "lds_gemm") {
+    if (v < 0 || v > 2) return fail(AMBPTT_EINVAL, "lds_gemm must be 0, 1 or 2");
+    C->lds_gemm = int(v);
   } else if (k == "hadj_launch") {
     C->hadj_launch = v != 0;
   } else if (k == "store_policy") {
