@@ -137,6 +137,21 @@ def estimate_pass_s(wl, spec, t_a_us: float, I_min: int) -> float:
     return wl.n_steps * t_a_us * 1e-6 * (evals / wl.n_steps + 2.7)
 
 
+def lds_kernels(spec, knobs) -> tuple[bool, bool]:
+    """Whether the fp32 large-batch path runs its gate products and its
+    h-adjoint products on the LDS-tiled kernels (the library's "lds_gemm"
+    rule: shapes that fit their tiles and, by default, fill the device at
+    least half: 128 tiles of 128 x 256, or of 64 x 128)."""
+    G, B, D, H = spec.gates, spec.batch, spec.input, spec.hidden
+    k = dict(knobs)
+    mode = k.get("lds_gemm", 1)
+    cell_fit = D % 32 == 0 and H % 32 == 0 and (G * H) % 256 == 0
+    prod_fit = (G * H) % 64 == 0 and H % 128 == 0 and k.get("hadj_launch", 1) != 0
+    cell = mode > 0 and cell_fit and (mode == 2 or -(-B // 128) * (G * H // 256) >= 128)
+    prod = mode > 0 and prod_fit and (mode == 2 or -(-B // 64) * (H // 128) >= 128)
+    return cell, prod
+
+
 def step_flops(spec, window: int, wide: bool = False) -> dict:
     """Algorithmic flops of one launch of each per-step kernel, and of the
     three products of one step (gate GEMM, h-adjoint, weight gradient).  On
@@ -596,10 +611,12 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
         cand = [k for k in tot if k in flops]
         dom = max(cand, key=tot.get) if cand else "adj"
         small = spec.batch * spec.hidden < 1024 * 256 or wl.dtype == "bf16"
+        lds_cell, lds_prod = lds_kernels(spec, knobs)
         if wide and wl.dtype == "f32":
-            names = {"fwd": "step_f32 forward: gate GEMM + cell update",
-                     "adj": "step_f32 adjoint: gate recompute + cell adjoint",
-                     "hadj": "prod_f32 h-adjoint product zbar W_h", "dw": "dw_f32_big weight-gradient window"}
+            names = {"fwd": ("cell_gemm_f32" if lds_cell else "step_f32") + " forward: gate GEMM + cell update",
+                     "adj": ("cell_gemm_f32" if lds_cell else "step_f32") + " adjoint: gate recompute + cell adjoint",
+                     "hadj": ("prod_gemm_f32" if lds_prod else "prod_f32") + " h-adjoint product zbar W_h",
+                     "dw": "dw_f32_big weight-gradient window"}
         elif wide and wl.cell == "resmlp":
             names = {"fwd": "mlp_wide forward", "adj": "mlp_wide adjoint (recompute + mask)",
                      "hadj": "prod_wide NN product ybar + zbar W_{l+1}", "dw": "dw_bf16 weight gradient of one layer"}
@@ -615,7 +632,9 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
             names = {"fwd": f"{k} forward: gate GEMM + cell update", "adj": f"{k} adjoint: gate recompute + h-adjoint GEMM",
                      "dw": ("dw_bf16" if wl.dtype == "bf16" else "dw_lds_f32") + " weight-gradient window"}
         if wide and wl.dtype == "f32":
-            key = {"fwd": "step_f32_fwd", "adj": "step_f32_adj", "hadj": "prod_f32"}.get(dom, "dw_f32_big")
+            key = {"fwd": "cell_gemm_f32_fwd" if lds_cell else "step_f32_fwd",
+                   "adj": "cell_gemm_f32_adj" if lds_cell else "step_f32_adj",
+                   "hadj": "prod_gemm_f32" if lds_prod else "prod_f32"}.get(dom, "dw_f32_big")
         elif wide:
             fam = {"fwd": "mlp_wide_fwd", "adj": "mlp_wide_adj", "hadj": "prod_wide_nn"} if wl.cell == "resmlp" else \
                 {"fwd": "cell_wide_fwd", "adj": "cell_wide_adj", "hadj": "prod_wide_nt"}

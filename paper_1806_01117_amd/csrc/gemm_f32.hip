@@ -7,11 +7,11 @@
 // index k:
 //   gate product  z[m][n] = sum_k [x | h][m][k] W[n][k]       (K = D + H)
 //   h-adjoint     hbar[m][j] = sum_k zbar[m][k] WhT[j][k]     (K = G H)
-// A workgroup of 4 waves owns one output tile.  The tile's operands pass
-// through LDS in stages of kKT reduction indices, double-buffered: while the
-// waves multiply stage s, the loads of stage s + 1 are in flight in
-// registers, and they are written to the other LDS buffer before the one
-// barrier of the stage.  LDS rows are padded by 4 floats, so that the 16
+// A workgroup of 8 (gate product) or 4 waves (h-adjoint product) owns one
+// output tile.  The tile's operands pass through LDS in stages of kKT
+// reduction indices, double-buffered: while the waves multiply stage s, the
+// loads of stage s + 1 are in flight in registers, and they are written to
+// the other LDS buffer before the one barrier of the stage.  LDS rows are padded by 4 floats, so that the 16
 // rows one MFMA operand read touches (16 bytes each, at one column) fall on
 // distinct banks.
 //
@@ -60,20 +60,21 @@ __device__ __forceinline__ void tile_of(int i, int mt, int nt, int* tm, int* tn)
 
 // ---- gate product with the cell epilogue ------------------------------------
 // Tile: 128 batch rows x 256 gate columns (LSTM: 64 units x 4 gates; RNN:
-// 256 units).  Wave (wm, wn) computes rows 64 wm .. + 63 and, for the LSTM,
-// units 32 wn .. + 31 of all four gates (8 blocks of 16 x 16: block
-// nb = 4 u + g is gate g of units 16 u .. + 15), so a lane holds the four
-// gates of its (row, unit) pairs in the same accumulator element; for the RNN
-// units 128 wn .. + 127.
-constexpr int kCM = 128, kCN = 256, kKT = 32, kLd = kKT + 4;
+// 256 units), 8 waves.  Wave (wm, wn), wm < 2, wn < 4, computes rows
+// 64 wm .. + 63 and, for the LSTM, units 16 wn .. + 15 of all four gates
+// (block g of its 4 x 4 blocks of 16 x 16 is gate g), so a lane holds the
+// four gates of its (row, unit) pairs in the same accumulator element; for
+// the RNN units 64 wn .. + 63.  Two waves per SIMD: one multiplies while the
+// other waits on LDS.
+constexpr int kCM = 128, kCN = 256, kKT = 32, kLd = kKT + 4, kCW = 8;
 
 template <int G, int MODE>
-__global__ __launch_bounds__(256, 1) void cell_gemm_f32(StepArgs a) {
+__global__ __launch_bounds__(64 * kCW, 1) void cell_gemm_f32(StepArgs a) {
   __shared__ float As[2][kCM][kLd];
   __shared__ float Bs[2][kCN][kLd];
-  __shared__ float red[4];
+  __shared__ float red[kCW];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
   const int r = lane & 15, q = lane >> 4;
   const int B = a.B, D = a.D, H = a.H, K1 = D + H;
   const int mt = (B + kCM - 1) / kCM, nt = G * H / kCN;
@@ -82,60 +83,60 @@ __global__ __launch_bounds__(256, 1) void cell_gemm_f32(StepArgs a) {
   const int m0 = tm * kCM;
   const int j0 = tn * (kCN / G);  // first unit of the tile
 
-  // loader: thread t moves rows t / 8 + 32 p, float4 column t % 8 of a stage
+  // loader: thread t moves rows t / 8 + 64 p, float4 column t % 8 of a stage
   const int lr = tid >> 3, lc = 4 * (tid & 7);
   const float* x = (const float*)a.x;
   const float* h = (const float*)a.h;
   const float* W = (const float*)a.W;
-  int arow[4];
+  int arow[2];
 #pragma unroll
-  for (int p = 0; p < 4; ++p) arow[p] = min(m0 + lr + 32 * p, B - 1);  // rows >= B: clamped, discarded
-  const float* brow[8];
+  for (int p = 0; p < 2; ++p) arow[p] = min(m0 + lr + 64 * p, B - 1);  // rows >= B: clamped, discarded
+  const float* brow[4];
 #pragma unroll
-  for (int p = 0; p < 8; ++p) {
-    const int c = lr + 32 * p;
+  for (int p = 0; p < 4; ++p) {
+    const int c = lr + 64 * p;
     const int n = G == 4 ? (c >> 6) * H + j0 + (c & 63) : j0 + c;
     brow[p] = W + (size_t)n * K1 + lc;
   }
-  f4 ra[4], rb[8];
+  f4 ra[2], rb[4];
   auto load = [&](int st) {
     const int k0 = st * kKT;
 #pragma unroll
-    for (int p = 0; p < 4; ++p)
+    for (int p = 0; p < 2; ++p)
       ra[p] = k0 < D ? *(const f4*)(x + (size_t)arow[p] * D + k0 + lc)
                      : *(const f4*)(h + (size_t)arow[p] * H + (k0 - D) + lc);
 #pragma unroll
-    for (int p = 0; p < 8; ++p) rb[p] = *(const f4*)(brow[p] + k0);
+    for (int p = 0; p < 4; ++p) rb[p] = *(const f4*)(brow[p] + k0);
   };
   auto store = [&](int buf) {
 #pragma unroll
-    for (int p = 0; p < 4; ++p) *(f4*)&As[buf][lr + 32 * p][lc] = ra[p];
+    for (int p = 0; p < 2; ++p) *(f4*)&As[buf][lr + 64 * p][lc] = ra[p];
 #pragma unroll
-    for (int p = 0; p < 8; ++p) *(f4*)&Bs[buf][lr + 32 * p][lc] = rb[p];
+    for (int p = 0; p < 4; ++p) *(f4*)&Bs[buf][lr + 64 * p][lc] = rb[p];
   };
 
-  f4 acc[4][8];
+  f4 acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int nb = 0; nb < 8; ++nb) acc[i][nb] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb < 4; ++nb) acc[i][nb] = f4{0.f, 0.f, 0.f, 0.f};
   // LDS row of B block nb of this wave
-  int bcol[8];
+  int bcol[4];
 #pragma unroll
-  for (int nb = 0; nb < 8; ++nb) bcol[nb] = G == 4 ? (nb & 3) * 64 + wn * 32 + 16 * (nb >> 2) : wn * 128 + 16 * nb;
+  for (int nb = 0; nb < 4; ++nb) bcol[nb] = G == 4 ? nb * 64 + wn * 16 : wn * 64 + 16 * nb;
 
   auto compute = [&](int buf) {
 #pragma unroll
     for (int kk = 0; kk < kKT / 16; ++kk) {
-      f4 af[4], bf[8];
+      f4 af[4], bf[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) af[i] = *(const f4*)&As[buf][wm * 64 + 16 * i + r][16 * kk + 4 * q];
 #pragma unroll
-      for (int nb = 0; nb < 8; ++nb) bf[nb] = *(const f4*)&Bs[buf][bcol[nb] + r][16 * kk + 4 * q];
+      for (int nb = 0; nb < 4; ++nb) bf[nb] = *(const f4*)&Bs[buf][bcol[nb] + r][16 * kk + 4 * q];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int nb = 0; nb < 8; ++nb) {
+        for (int nb = 0; nb < 4; ++nb) {
           acc[i][nb] = mfma4(af[i].x, bf[nb].x, acc[i][nb]);
           acc[i][nb] = mfma4(af[i].y, bf[nb].y, acc[i][nb]);
           acc[i][nb] = mfma4(af[i].z, bf[nb].z, acc[i][nb]);
@@ -143,15 +144,18 @@ __global__ __launch_bounds__(256, 1) void cell_gemm_f32(StepArgs a) {
         }
     }
   };
-  // stages 0 .. nst - 2 load the next stage while they multiply; the last one
-  // only multiplies (no branch inside the loop)
+  // The next stage's global loads are issued before the multiplications
+  // start (the scheduling barrier keeps the compiler from sinking them below
+  // the MFMAs, where their latency would stall the stage's LDS writes).
   const int nst = K1 / kKT;
   load(0);
   store(0);
   __syncthreads();
   for (int st = 0; st + 1 < nst; ++st) {
     load(st + 1);
+    __builtin_amdgcn_sched_barrier(0);
     compute(st & 1);
+    __builtin_amdgcn_sched_barrier(0);
     store((st + 1) & 1);
     __syncthreads();
   }
@@ -161,7 +165,7 @@ __global__ __launch_bounds__(256, 1) void cell_gemm_f32(StepArgs a) {
   //      column l & 15 of its 16 x 16 block ------------------------------------
   const int GH = G * H;
   float lterm = 0.f;
-  constexpr int NU = G == 4 ? 2 : 8;  // unit blocks per wave
+  constexpr int NU = G == 4 ? 1 : 4;  // unit blocks per wave
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -169,15 +173,15 @@ __global__ __launch_bounds__(256, 1) void cell_gemm_f32(StepArgs a) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int m = m0 + wm * 64 + 16 * i + 4 * q + v;
-        const int j = G == 4 ? j0 + wn * 32 + 16 * u + r : j0 + wn * 128 + 16 * u + r;
+        const int j = G == 4 ? j0 + wn * 16 + r : j0 + wn * 64 + 16 * u + r;
         if (m >= B) continue;
         const size_t o = (size_t)m * H + j;
         float h1, c1 = 0.f, tc = 0.f, ig = 0.f, fg = 0.f, gg = 0.f, og = 0.f, cold = 0.f;
         if (G == 4) {
-          ig = sigm(acc[i][4 * u][v] + a.bias[j]);
-          fg = sigm(acc[i][4 * u + 1][v] + a.bias[H + j]);
-          gg = tanhf(acc[i][4 * u + 2][v] + a.bias[2 * H + j]);
-          og = sigm(acc[i][4 * u + 3][v] + a.bias[3 * H + j]);
+          ig = sigm(acc[i][0][v] + a.bias[j]);
+          fg = sigm(acc[i][1][v] + a.bias[H + j]);
+          gg = tanhf(acc[i][2][v] + a.bias[2 * H + j]);
+          og = sigm(acc[i][3][v] + a.bias[3 * H + j]);
           cold = a.c[o];
           c1 = fg * cold + ig * gg;
           tc = tanhf(c1);
@@ -220,11 +224,15 @@ __global__ __launch_bounds__(256, 1) void cell_gemm_f32(StepArgs a) {
         }
         ((float*)a.hwin_out)[o] = ((const float*)a.h)[o];
       }
-  if (MODE == kAdjoint) {  // the four waves' loss terms, summed in wave order
+  if (MODE == kAdjoint) {  // the waves' loss terms, summed in wave order
     const float s = wave_sum(lterm);
     if (lane == 0) red[wave] = s;
     __syncthreads();
-    if (tid == 0) a.loss_acc[blockIdx.x] += (double)red[0] + (double)red[1] + (double)red[2] + (double)red[3];
+    if (tid == 0) {
+      double t = 0.0;
+      for (int w = 0; w < kCW; ++w) t += (double)red[w];
+      a.loss_acc[blockIdx.x] += t;
+    }
   }
 }
 
@@ -301,7 +309,9 @@ __global__ __launch_bounds__(256, 1) void prod_gemm_f32(ProdArgs a) {
   __syncthreads();
   for (int st = 0; st + 1 < nst; ++st) {
     load(st + 1);
+    __builtin_amdgcn_sched_barrier(0);
     compute(st & 1);
+    __builtin_amdgcn_sched_barrier(0);
     store((st + 1) & 1);
     __syncthreads();
   }
@@ -330,7 +340,7 @@ int cell_gemm_f32_tiles(int G, int B, int H) { return ((B + kCM - 1) / kCM) * (G
 
 hipError_t launch_cell_gemm_f32(int G, int mode, const StepArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (!cell_gemm_f32_fits(G, a.B, a.D, a.H) || (mode == kAdjoint && !a.first && !a.hbar_in)) return hipErrorInvalidValue;
-  const dim3 grid(cell_gemm_f32_tiles(G, a.B, a.H)), block(256);
+  const dim3 grid(cell_gemm_f32_tiles(G, a.B, a.H)), block(64 * kCW);
   if (G == 4) {
     if (mode == kForward) hipExtLaunchKernelGGL((cell_gemm_f32<4, kForward>), grid, block, 0, s, e0, e1, 0, a);
     else if (mode == kAdjoint) hipExtLaunchKernelGGL((cell_gemm_f32<4, kAdjoint>), grid, block, 0, s, e0, e1, 0, a);
