@@ -31,7 +31,7 @@ class Reverse:
         self.terms = np.zeros(n + 1)
         self.next_t = n - 1
         self.bar = None
-        if cell.kind == "resmlp":
+        if cell.kind in ("resmlp", "mlp"):
             self.dW, self.db = {}, {}
         else:
             self.dW = np.zeros_like(cell.W)
@@ -50,7 +50,7 @@ class Reverse:
         if s is not None:
             bar[0] = bar[0] + s
         bar_t, dW_t, db_t = cell.adjoint(t, x_t, u, tuple(bar))
-        if cell.kind == "resmlp":
+        if cell.kind in ("resmlp", "mlp"):
             self.dW[t], self.db[t] = dW_t, db_t
         else:
             self.dW += dW_t
@@ -89,7 +89,7 @@ def store_all(cell: Cell, n: int, u_of, x0: tuple) -> dict:
 def cell_for(wl, params=None, layer=None) -> Cell:
     """Build an oracle cell for a ``synth`` workload (parameters as float32 arrays)."""
     bf16 = wl.dtype == "bf16"
-    if wl.cell == "resmlp":
-        return Cell("resmlp", wl.loss, wl.batch, 0, wl.hidden, bf16, layer=layer)
+    if wl.cell in ("resmlp", "mlp"):
+        return Cell(wl.cell, wl.loss, wl.batch, 0, wl.hidden, bf16, layer=layer)
     W, b = params
     return Cell(wl.cell, wl.loss, wl.batch, wl.input, wl.hidden, bf16, W=W, b=b)

@@ -14,7 +14,10 @@ Layouts (batch rows, row-major):
   state h[B][H] (and c[B][H] for the LSTM), u[B][D],
   W[G*H][D+H] acting on [u | h] (input columns first), b[G*H];
   LSTM gate blocks of W in the order i, f, g, o;
-  residual MLP: layer l has W_l[w][w] (output x input), b_l[w].
+  residual MLP: layer l has W_l[w][w] (output x input), b_l[w];
+  MLP of layers of different widths (states of different sizes, the case the
+  paper's Sections 1.1 and 6 set beside Revolve's uniform states): layer l
+  maps y_l[B][w_l] to y_{l+1} = relu(y_l W_l^T + b_l), W_l[w_{l+1}][w_l].
 
 Precision: everything is float64.  For bf16 workloads the stored forward
 state h (or y) is rounded to bfloat16 after every step, as the GPU stores it;
@@ -43,7 +46,7 @@ class Cell:
         self.kind, self.loss, self.bf16 = kind, loss, bf16
         self.B, self.D, self.H = batch, input, hidden
         self.G = 4 if kind == "lstm" else 1
-        if kind == "resmlp":
+        if kind in ("resmlp", "mlp"):
             self._layer = layer          # callable l -> (W_l, b_l)
             self._cache = {}
         else:
@@ -78,6 +81,8 @@ class Cell:
         (y,) = state
         W, b = self.layer(t)
         z = y @ W.T + b
+        if self.kind == "mlp":
+            return (self._store(np.maximum(z, 0.0)),)
         return (self._store(y + np.maximum(z, 0.0)),)
 
     # -- adjoint step (x_t, u_t, xbar_{t+1}) -> (xbar_t, dW_t, db_t) --------
@@ -113,6 +118,8 @@ class Cell:
         W, b = self.layer(t)
         z = y @ W.T + b
         zb = yb1 * (z > 0.0)                               # relu'(0) = 0
+        if self.kind == "mlp":                             # no identity path
+            return (zb @ W,), zb.T @ y, zb.sum(axis=0)
         return (yb1 + zb @ W,), zb.T @ y, zb.sum(axis=0)
 
     # -- loss ------------------------------------------------------------

@@ -103,8 +103,28 @@ slots splits where a dynamic program over the same recursion finds the least
 total cost of recomputed forward steps (WeightedSplits); the header then ends
 with " split=cost".
 
+States of different sizes (the other non-uniform case of Sections 1.1 and 6;
+within an interval the paper proposes the known algorithm for non-uniform
+single-stage checkpointing instead of Revolve): sizes[t] is the size of x_t
+in units of a common granule, and the fast memory is a byte-addressed pool of
+P = s * max(sizes) units (s states of the largest size).  Checkpoints form a
+stack: the snapshot taken at recursion depth k ("slot" k) sits right above
+the ones below it, so its offset is the sum of their sizes (in two levels,
+slots 0 and 1 are the interval starts' regions of max(sizes) units each and
+the stack starts above them).  Reversing [a, a+l) with M units free beyond
+x_a (SizedSplits):
+    T(a, 1, M) = 0
+    T(a, l, M) = min over m with sizes[a+m] <= M of
+                 C(a, a+m) + T(a+m, l-m, M - sizes[a+m]) + T(a, m, M)
+    (ties: the largest m), or the chain when no snapshot fits;
+plain: M = P - sizes[0]; two levels: M = P - 2 max(sizes) in every interval.
+The mode is the one with the smaller weighted forward cost (with unit costs:
+forward evaluations), the two levels taken only when strictly cheaper.  With
+unit sizes this is Revolve's recursion with M + 1 slots, and the schedules
+are the canonical ones.  Header suffix " split=size".
+
 Canonical text: a header line
-  ambptt-schedule v1 n=<n> s=<s> H=<H> I=<I or 0> mode=<revolve|async|dynamic|online> [split=cost]
+  ambptt-schedule v1 n=<n> s=<s> H=<H> I=<I or 0> mode=<revolve|async|dynamic|online> [split=cost|size]
 (I = 0 for revolve and dynamic, the initial interval for online, 0 when single
 level) then the actions, single spaces, decimal integers, newline-terminated.
 """
@@ -237,8 +257,33 @@ class _Gen:
             l = m
 
 
-def _two_level(g: _Gen, n: int, s: int, starts: list[int]) -> None:
-    """The sweep and the reverse of the two-level policy over the given interval starts."""
+def _reverse_sized(g: _Gen, ss: "SizedSplits", a: int, l: int, M: int, base: int, depth: int) -> None:
+    """Reverse [a, a+l) with M units free above x_a (in slot `base`); the next
+    snapshot goes to slot `depth` (the top of the stack)."""
+    while True:
+        if l == 1:
+            g.restore(base, a)
+            g.leaf(a)
+            return
+        m = ss.split(a, l, M)
+        if m == 0:  # no snapshot fits: the chain from x_a
+            for i in range(l - 1, -1, -1):
+                g.restore(base, a)
+                if i > 0:
+                    g.advance(a, a + i)
+                g.leaf(a + i)
+            return
+        g.restore(base, a)
+        g.advance(a, a + m)
+        g.emit("S", depth, a + m)
+        _reverse_sized(g, ss, a + m, l - m, M - ss.z[a + m], depth, depth + 1)
+        l = m
+
+
+def _two_level(g: _Gen, n: int, s: int, starts: list[int], sized=None) -> None:
+    """The sweep and the reverse of the two-level policy over the given
+    interval starts; `sized` = (SizedSplits, M) reverses each interval with
+    the sized recursion on M units above its start."""
     K = len(starts)
     ends = starts[1:] + [n]
     g.live = 0
@@ -252,7 +297,10 @@ def _two_level(g: _Gen, n: int, s: int, starts: list[int]) -> None:
             g.emit("S", base, a)
         if k >= 1:
             g.emit("P", k - 1, (k - 1) % 2, starts[k - 1])
-        g.reverse(a, l, s - 1, base, list(range(2, s)))
+        if sized is not None:
+            _reverse_sized(g, sized[0], a, l, sized[1], base, 2)
+        else:
+            g.reverse(a, l, s - 1, base, list(range(2, s)))
 
 
 def schedule(n: int, s: int, H: int = 0, I_min: int = 0) -> tuple[dict, list[tuple]]:
@@ -508,6 +556,195 @@ def schedule_costs(n: int, s: int, costs, H: int = 0, I_min: int = 0) -> tuple[d
     evals = sum(x[2] - x[1] for x in g.out if x[0] == "A") + 1
     cost = sum(ws.C(x[1], x[2]) for x in g.out if x[0] == "A") + costs[n - 1]
     return dict(head, evals=evals, cost=cost, split="cost"), g.out
+
+
+class SizedSplits:
+    """Optimal splits when states differ in size (non-uniform single-stage
+    checkpointing, the algorithm the paper's Section 6 proposes inside each
+    interval; Section 1.1 cites a dynamic program for it): Revolve's
+    recursion with a memory budget in units instead of a slot count.
+    sizes[t] (t = 0 .. n) is the size of x_t in units, costs[t] the cost of
+    forward step t (default 1).  With the live state at x_a and M units free
+    above x_a's own checkpoint, reversing [a, a+l) costs
+        T(a, 1, M) = 0
+        T(a, l, M) = min over m with sizes[a+m] <= M of
+                     C(a, a+m) + T(a+m, l-m, M - sizes[a+m]) + T(a, m, M)
+    (x_{a+m} stays while [a+m, a+l) is reversed above it, then its units are
+    free again for [a, a+m)); ties go to the largest m; when no snapshot fits
+    the chain (restore x_a and advance i steps, i = l-1 .. 1) costs
+    sum_{i=1}^{l-1} C(a, a+i).  A split that fits never costs more than the
+    chain, so a split is always taken when one fits."""
+
+    def __init__(self, sizes, costs=None):
+        self.z = [int(v) for v in sizes]
+        n = len(self.z) - 1
+        if n < 1 or any(v < 1 for v in self.z):
+            raise ValueError("need n + 1 >= 2 positive sizes")
+        self.c = [1.0] * n if costs is None else [float(x) for x in costs]
+        if len(self.c) != n or any(not (x > 0) for x in self.c):
+            raise ValueError("need n positive step costs")
+        self.pre = [0.0]
+        for x in self.c:
+            self.pre.append(self.pre[-1] + x)
+        self.memo = {}
+
+    def C(self, a: int, b: int) -> float:
+        return self.pre[b] - self.pre[a]
+
+    def T(self, a: int, l: int, M: int) -> float:
+        return self._solve(a, l, M)[0]
+
+    def split(self, a: int, l: int, M: int) -> int:
+        """The split m, or 0 for the chain."""
+        return self._solve(a, l, M)[1]
+
+    def _solve(self, a, l, M):
+        key = (a, l, M)
+        if key in self.memo:
+            return self.memo[key]
+        best = None
+        if l == 1:
+            best = (0.0, 0)
+        else:
+            for m in range(1, l):
+                if self.z[a + m] <= M:
+                    v = self.C(a, a + m) + self._solve(a + m, l - m, M - self.z[a + m])[0] + self._solve(a, m, M)[0]
+                    if best is None or v <= best[0]:
+                        best = (v, m)
+            if best is None:
+                best = (sum(self.C(a, a + i) for i in range(1, l)), 0)
+        self.memo[key] = best
+        return best
+
+
+def _sized_result(g: _Gen, head: dict, ss: SizedSplits, n: int) -> tuple[dict, list[tuple]]:
+    head["evals"] = sum(x[2] - x[1] for x in g.out if x[0] == "A") + 1
+    head["cost"] = sum(ss.C(x[1], x[2]) for x in g.out if x[0] == "A") + ss.c[n - 1]
+    head["split"] = "size"
+    return head, g.out
+
+
+def schedule_sized(n: int, s: int, sizes, H: int = 0, I_min: int = 0, costs=None) -> tuple[dict, list[tuple]]:
+    """(header dict, action list) when the states x_0 .. x_n have the given
+    sizes (units), in a fast pool of s * max(sizes) units and H slow slots
+    (each holding any state).  Plain: the sized recursion over [0, n) with
+    P - sizes[0] units above x_0.  Two levels (H > 0, s >= 2, I < n, strictly
+    cheaper): the fixed-interval policy with every interval reversed by the
+    sized recursion on P - 2 max(sizes) units."""
+    if n < 1 or s < 1 or H < 0 or I_min < 0 or len(sizes) != n + 1:
+        raise ValueError("need n >= 1, s >= 1, H >= 0, I_min >= 0 and n + 1 sizes")
+    ss = SizedSplits(sizes, costs)
+    zmax = max(ss.z)
+    P = s * zmax
+    best = ("revolve", 0, ss.T(0, n, P - ss.z[0]))
+    if H > 0 and s >= 2:
+        I = max(I_min, 1, -(-n // (H + 1)))
+        if I < n:
+            starts = list(range(0, n, I))
+            ends = starts[1:] + [n]
+            M = P - 2 * zmax
+            c = ss.C(0, starts[-1]) + sum(ss.T(a, e - a, M) for a, e in zip(starts, ends))
+            if c < best[2]:
+                best = ("async", I, c)
+    g = _Gen(n)
+    if best[0] == "revolve":
+        g.emit("S", 0, 0)
+        g.live = 0
+        _reverse_sized(g, ss, 0, n, P - ss.z[0], 0, 1)
+    else:
+        _two_level(g, n, s, list(range(0, n, best[1])), sized=(ss, P - 2 * zmax))
+    return _sized_result(g, {"n": n, "s": s, "H": H, "I": best[1], "mode": best[0]}, ss, n)
+
+
+def schedule_sized_from_starts(n: int, s: int, H: int, starts: list[int], sizes, costs=None):
+    """The two-level policy over interval starts chosen during the sweep,
+    each interval reversed by the sized recursion (the pairing Section 6
+    proposes: stores whenever the previous transfer completed, and the
+    non-uniform single-stage algorithm inside each interval)."""
+    starts = list(starts)
+    if n < 1 or s < 2 or not starts or starts[0] != 0 or any(b <= a for a, b in zip(starts, starts[1:])) \
+            or starts[-1] >= n or len(starts) - 1 > H or len(sizes) != n + 1:
+        raise ValueError("need s >= 2, starts 0 = t_0 < t_1 < ... < n with at most H + 1 of them, n + 1 sizes")
+    ss = SizedSplits(sizes, costs)
+    zmax = max(ss.z)
+    g = _Gen(n)
+    _two_level(g, n, s, starts, sized=(ss, s * zmax - 2 * zmax))
+    return _sized_result(g, {"n": n, "s": s, "H": H, "I": 0, "mode": "dynamic"}, ss, n)
+
+
+def text_sized(n: int, s: int, sizes, H: int = 0, I_min: int = 0, costs=None) -> str:
+    return _render(*schedule_sized(n, s, sizes, H, I_min, costs))
+
+
+def text_sized_from_starts(n: int, s: int, H: int, starts, sizes, costs=None) -> str:
+    return _render(*schedule_sized_from_starts(n, s, H, starts, sizes, costs))
+
+
+def slot_offsets(acts: list[tuple], sizes, two_level: bool) -> list[int | None]:
+    """Unit offset of every S / R / W / P action's fast slot in the stack
+    layout of sized schedules (None for other actions): slot k sits above
+    the states most recently snapshotted into slots below it (two levels:
+    slots 0 and 1 at 0 and max(sizes), the stack from 2 max(sizes))."""
+    zmax = max(sizes)
+    content: dict[int, int] = {}
+    out = []
+
+    def off(k):
+        if two_level and k <= 1:
+            return k * zmax
+        lo = 2 if two_level else 0
+        assert all(j in content for j in range(lo, k)), ("a slot below slot", k, "holds no state")
+        return (2 * zmax if two_level else 0) + sum(sizes[content[j]] for j in range(lo, k))
+
+    for a in acts:
+        op = a[0]
+        if op in ("S", "R", "W"):
+            k = a[1]
+            if op == "S":
+                out.append(off(k))
+                content[k] = a[2]
+            else:
+                out.append(off(k))
+        elif op == "P":
+            out.append(off(a[2]))
+            content[a[2]] = a[3]
+        else:
+            out.append(None)
+    return out
+
+
+def check_sized(n: int, s: int, H: int, acts: list[tuple], sizes, two_level: bool) -> dict:
+    """check() plus the byte budget of the sized layout: every snapshot lies
+    inside the pool of s * max(sizes) units, every state read back from a
+    slot is read at the offset it was written to, and the interval starts
+    fit their regions."""
+    c = check(n, s_slots(acts, s), H, acts)
+    zmax = max(sizes)
+    P = s * zmax
+    offs = slot_offsets(acts, sizes, two_level)
+    written: dict[int, int] = {}
+    for a, o in zip(acts, offs):
+        op = a[0]
+        if op == "S":
+            k, t = a[1], a[2]
+            assert o + sizes[t] <= P, (a, o, P)
+            if two_level and k <= 1:
+                assert sizes[t] <= zmax
+            written[k] = o
+        elif op == "P":
+            assert a[2] <= 1 and two_level, a
+            written[a[2]] = o
+        elif op in ("R", "W"):
+            assert written.get(a[1]) == o, ("slot moved under its state", a, o, written.get(a[1]))
+    c["peak_units"] = max([o + sizes[a[2]] for a, o in zip(acts, offs) if a[0] == "S"] + [0])
+    return c
+
+
+def s_slots(acts: list[tuple], s: int) -> int:
+    """Slot ids a sized schedule may use (stack depths can exceed s when the
+    states are small): one more than the largest id it names, at least s."""
+    ks = [a[1] for a in acts if a[0] in ("S", "R", "W")] + [a[2] for a in acts if a[0] == "P"]
+    return max([s] + [k + 1 for k in ks])
 
 
 def text_costs(n: int, s: int, costs, H: int = 0, I_min: int = 0) -> str:

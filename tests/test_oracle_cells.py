@@ -213,3 +213,41 @@ def test_workload_loss_scale_small_rnn():
     out = bptt.store_all(cell, wl.n_steps, lambda t: xs[t], (h0,))
     assert math.isfinite(out["loss"]) and 0 < out["loss"] < 0.5 * wl.batch * wl.hidden
     assert np.all(np.abs(out["states"][-1][0]) < 1)
+
+
+@pytest.mark.parametrize("loss", ["half_sq_last", "mean_sq_all", "mean_last"])
+def test_fd_mlp_of_different_widths(loss):
+    """Central finite differences for the MLP whose layers change width (states
+    of different sizes): every weight, bias and initial-state entry."""
+    widths = [4, 6, 3, 5, 2, 6]
+    n, B = len(widths) - 1, 2
+    rng = np.random.default_rng(11)
+    Ws = {l: [rng.standard_normal((widths[l + 1], widths[l])) * 0.8, rng.standard_normal(widths[l + 1]) * 0.3]
+          for l in range(n)}
+    cell = Cell("mlp", loss, B, 0, max(widths), layer=lambda l: tuple(Ws[l]))
+    y0 = rng.standard_normal((B, widths[0]))
+    zero = np.zeros((B, 0))
+    run = lambda: bptt.store_all(cell, n, lambda t: zero, (y0,))
+    out = run()
+    eps = 1e-6
+
+    def fd(arr):
+        g = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            keep = arr[idx]
+            arr[idx] = keep + eps; cell._cache.clear(); lp = run()["loss"]
+            arr[idx] = keep - eps; cell._cache.clear(); lm = run()["loss"]
+            arr[idx] = keep
+            g[idx] = (lp - lm) / (2 * eps)
+        cell._cache.clear()
+        return g
+
+    def close(a, b):
+        scale = max(np.max(np.abs(b)), 1e-3)
+        assert np.max(np.abs(a - b)) / scale < 1e-6, (np.max(np.abs(a - b)), scale)
+
+    for l in range(n):
+        close(out["dW"][l], fd(Ws[l][0]))
+        close(out["db"][l], fd(Ws[l][1]))
+    close(out["dx0"][0], fd(y0))
+    assert out["dW"][2].shape == (widths[3], widths[2])
