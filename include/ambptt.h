@@ -55,8 +55,15 @@ enum {
   AMBPTT_CELL_TANH_RNN = 1, /* h' = tanh(W [x|h] + b), W[H][D+H] */
   AMBPTT_CELL_LSTM = 2,     /* z = W [x|h] + b, W[4H][D+H], gate blocks i,f,g,o;
                                c' = s(f) c + s(i) tanh(g); h' = s(o) tanh(c') */
-  AMBPTT_CELL_RESMLP = 3    /* depth as sequence: y' = y + relu(W_l y + b_l),
+  AMBPTT_CELL_RESMLP = 3,   /* depth as sequence: y' = y + relu(W_l y + b_l),
                                W[L][w][w] (output x input), b[L][w]; D = 0 */
+  AMBPTT_CELL_MLP = 4       /* depth as sequence with layers of different
+                               widths, states of different sizes (Sections 1.1
+                               and 6): y_{l+1} = relu(W_l y_l + b_l),
+                               W_l [w_{l+1}][w_l] and b_l [w_{l+1}] stored one
+                               layer after the other; widths from
+                               ambptt_set_widths (all = hidden by default,
+                               hidden = the largest); D = 0; fp32 only */
 };
 
 enum { AMBPTT_F32 = 0, AMBPTT_BF16 = 1 };
@@ -173,6 +180,31 @@ ambptt_status ambptt_schedule_text_starts(int64_t n, int32_t s, int64_t H, const
  * reversal's table would exceed 1 Mi entries (see ambptt_set_step_costs). */
 ambptt_status ambptt_schedule_text_costs(int64_t n, int32_t s, int64_t H, int32_t interval_min,
                                          const double* costs, char* buf, size_t cap, size_t* needed);
+
+/* Canonical text of the schedule when the states differ in size (the case
+ * Sections 1.1 and 6 set beside Revolve's uniform states; Section 6 proposes
+ * the algorithm for non-uniform single-stage checkpointing inside each
+ * interval).  sizes[0..n] (>= 1) are the sizes of x_0 .. x_n in units of a
+ * common granule; the fast pool holds s * max(sizes) units and the
+ * snapshots stack in it: the one taken at recursion depth k ("slot" k, which
+ * may exceed s - 1 when states are small) lies above the states in the slots
+ * below it, and in two levels slots 0 and 1 are the interval starts'
+ * regions of max(sizes) units each.  Every reversal of [a, a+l) with M units
+ * free above x_a splits where a dynamic program over Revolve's recursion
+ * with a budget finds the least total cost of recomputed steps,
+ *   T(a, l, M) = min over m with sizes[a+m] <= M of
+ *                C(a, a+m) + T(a+m, l-m, M - sizes[a+m]) + T(a, m, M),
+ * ties to the largest m, the chain when no snapshot fits (C: the step costs,
+ * costs[0..n) > 0, or 1 each when costs is NULL).  Plain: M = s max(sizes) -
+ * sizes[0]; two levels (H > 0, s >= 2, I = max(I_min, 1, ceil(n / (H+1))) <
+ * n), taken when strictly cheaper: M = (s - 2) max(sizes) in every interval.
+ * Unit sizes give ambptt_schedule_text's schedule.  Header suffix
+ * " split=size".  Buffer rules as in ambptt_schedule_text; EINVAL on bad
+ * arguments, EUNSUPPORTED when a reversal's table would exceed 1 Mi entries
+ * (l (l + 1) (M + 1)). */
+ambptt_status ambptt_schedule_text_sized(int64_t n, int32_t s, int64_t H, int32_t interval_min,
+                                         const int64_t* sizes, const double* costs, char* buf, size_t cap,
+                                         size_t* needed);
 
 /* The interval I_min for measured times of one forward step (T_A) and of one
  * state over the host link (T_T), in microseconds, with s fast slots.
@@ -329,6 +361,19 @@ ambptt_status ambptt_set_int(ambptt_ctx* ctx, const char* key, int64_t value);
  * write time per state into T_T.  EINVAL if the file cannot be created. */
 ambptt_status ambptt_set_file_tier(ambptt_ctx* ctx, const char* dir, int64_t file_slots);
 
+/* Layer widths w_0 .. w_n of an AMBPTT_CELL_MLP problem (count = n + 1):
+ * multiples of 16 from 16 up to the problem's hidden size, which one of them
+ * must equal.  State x_t is y_t [B][w_t] (fp32); the slot pool of
+ * fast_slots states of the largest size is then byte-addressed and every
+ * schedule is the sized one of ambptt_schedule_text_sized, with the sizes of
+ * the states (rounded up to 256 bytes) in units of their greatest common
+ * divisor: small states stack more snapshots into the same HBM budget, and
+ * with stores decided during the sweep ("store_policy" 1) every interval is
+ * reversed by the same sized recursion, the pairing Section 6 proposes.
+ * Online checkpointing is not available for it (EUNSUPPORTED at run time).
+ * EINVAL for another cell, a wrong count or width. */
+ambptt_status ambptt_set_widths(ambptt_ctx* ctx, const int32_t* widths, int64_t count);
+
 /* Relative forward costs of the n steps (costs[t] > 0 for step t; NULL or
  * n = 0 removes them): layers or steps of unequal cost, which the paper's
  * Sections 1.1 and 6 point to.  Every reversal of two or more steps on two
@@ -366,11 +411,12 @@ ambptt_status ambptt_calibrate(ambptt_ctx* ctx, const void* x_seq, const void* W
  * invariant breaks (a resident-kernel barrier timed out), after which the
  * context stays usable.
  *   x_seq  [n][B][D] operand dtype (NULL for RESMLP)
- *   W      TANH_RNN/LSTM: [G*H][D+H]; RESMLP: [L][w][w]; operand dtype
- *   b      fp32 [G*H] (RESMLP: [L][w])
- *   h0     [B][H] operand dtype; c0 fp32 [B][H] for LSTM, else NULL
+ *   W      TANH_RNN/LSTM: [G*H][D+H]; RESMLP: [L][w][w]; MLP: the layers'
+ *          [w_{l+1}][w_l] one after the other; operand dtype
+ *   b      fp32 [G*H] (RESMLP: [L][w]; MLP: the layers' [w_{l+1}])
+ *   h0     [B][H] operand dtype (MLP: [B][w_0]); c0 fp32 [B][H] for LSTM, else NULL
  *   dW, db fp32, same layouts as W, b (overwritten)
- *   dh0    fp32 [B][H]; dc0 fp32 [B][H] for LSTM, else NULL
+ *   dh0    fp32 [B][H] (MLP: [B][w_0]); dc0 fp32 [B][H] for LSTM, else NULL
  *   loss   host double (may be NULL); stats host (may be NULL)
  * The inputs must not be written while the call runs. */
 ambptt_status ambptt_run(ambptt_ctx* ctx, const void* x_seq, const void* W, const float* b,

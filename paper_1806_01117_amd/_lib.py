@@ -13,7 +13,7 @@ DTYPE = {"f32": 0, "bf16": 1}
 LOSS = {"half_sq_last": 0, "mean_sq_all": 1, "mean_last": 2}
 
 EXPORTS = ["ambptt_version", "ambptt_revolve_advances", "ambptt_schedule_evals", "ambptt_schedule_text",
-           "ambptt_schedule_text_starts", "ambptt_schedule_text_online", "ambptt_schedule_text_costs",
+           "ambptt_schedule_text_starts", "ambptt_schedule_text_online", "ambptt_schedule_text_costs", "ambptt_schedule_text_sized",
            "ambptt_interval_from_timings", "ambptt_set_step_costs",
            "ambptt_resident_program", "ambptt_query", "ambptt_last_error",
            "ambptt_create", "ambptt_bind", "ambptt_set_int", "ambptt_set_file_tier", "ambptt_calibrate", "ambptt_run", "ambptt_run_noalloc",
@@ -84,6 +84,9 @@ def load():
     L.ambptt_interval_from_timings.restype = i64
     L.ambptt_schedule_text_costs.argtypes = [i64, i32, i64, i32, C.POINTER(C.c_double), C.c_char_p, sz, C.POINTER(sz)]
     L.ambptt_schedule_text_costs.restype = C.c_int
+    L.ambptt_schedule_text_sized.argtypes = [i64, i32, i64, i32, C.POINTER(i64), C.POINTER(C.c_double), C.c_char_p, sz,
+                                             C.POINTER(sz)]
+    L.ambptt_schedule_text_sized.restype = C.c_int
     L.ambptt_set_step_costs.argtypes = [vp, C.POINTER(C.c_double), i64]
     L.ambptt_set_step_costs.restype = C.c_int
     L.ambptt_last_schedule_text.argtypes = [vp, C.c_char_p, sz, C.POINTER(sz)]

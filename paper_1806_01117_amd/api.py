@@ -80,6 +80,15 @@ def schedule_text_costs(n: int, s: int, costs, H: int = 0, interval_min: int = 0
     return _text(lambda buf, cap, need: L.ambptt_schedule_text_costs(n, s, H, interval_min, arr, buf, cap, need))
 
 
+def schedule_text_sized(n: int, s: int, sizes, H: int = 0, interval_min: int = 0, costs=None) -> str:
+    """Canonical text of the schedule for states of different sizes
+    (ambptt_schedule_text_sized): sizes[0..n] in units of a common granule."""
+    L = load()
+    za = (C.c_int64 * len(sizes))(*[int(v) for v in sizes])
+    ca = (C.c_double * len(costs))(*[float(c) for c in costs]) if costs is not None else None
+    return _text(lambda buf, cap, need: L.ambptt_schedule_text_sized(n, s, H, interval_min, za, ca, buf, cap, need))
+
+
 def schedule_text_online(n: int, s: int, H: int = 0, interval_min: int = 0) -> str:
     """Canonical text of the online checkpointing schedule for n steps
     (ambptt_schedule_text_online)."""

@@ -1299,6 +1299,27 @@ ambptt_status ambptt_schedule_text_costs(int64_t n, int32_t s, int64_t H, int32_
   }
 }
 
+ambptt_status ambptt_schedule_text_sized(int64_t n, int32_t s, int64_t H, int32_t interval_min, const int64_t* sizes,
+                                         const double* costs, char* buf, size_t cap, size_t* needed) {
+  if (n < 1 || s < 1 || H < 0 || interval_min < 0 || !sizes) return fail(AMBPTT_EINVAL, "schedule: bad arguments");
+  if (costs && !costs_ok(costs, n)) return fail(AMBPTT_EINVAL, "step costs must be positive and finite");
+  try {
+    const std::vector<double> c = costs ? std::vector<double>(costs, costs + n) : std::vector<double>();
+    const std::string t = plan_text(make_plan_sized(n, s, H, interval_min, std::vector<int64_t>(sizes, sizes + n + 1),
+                                                    costs ? &c : nullptr, nullptr));
+    if (needed) *needed = t.size() + 1;
+    if (!buf || cap < t.size() + 1) return fail(AMBPTT_EINVAL, "schedule: buffer too small");
+    std::memcpy(buf, t.c_str(), t.size() + 1);
+    return AMBPTT_OK;
+  } catch (const std::length_error& e) {
+    return fail(AMBPTT_EUNSUPPORTED, e.what());
+  } catch (const std::invalid_argument& e) {
+    return fail(AMBPTT_EINVAL, e.what());
+  } catch (const std::exception& e) {
+    return fail(AMBPTT_EINTERNAL, e.what());
+  }
+}
+
 int64_t ambptt_interval_from_timings(double t_a_us, double t_t_us, int32_t s, int32_t rule) {
   if (!(t_a_us > 0.0) || !(t_t_us >= 0.0) || s < 1 || rule < 0 || rule > 1) {
     fail(AMBPTT_EINVAL, "interval: need T_A > 0, T_T >= 0, s >= 1, rule 0 or 1");

@@ -485,7 +485,7 @@ std::string plan_text(const Plan& p) {
   t += "ambptt-schedule v1 n=" + std::to_string(p.n) + " s=" + std::to_string(p.s) +
        " H=" + std::to_string(p.H) + " I=" + std::to_string(p.dynamic ? 0 : p.interval) +
        " mode=" + (p.online ? "online" : p.dynamic ? "dynamic" : p.async ? "async" : "revolve") +
-       (p.weighted ? " split=cost" : "") + "\n";
+       (p.sized ? " split=size" : p.weighted ? " split=cost" : "") + "\n";
   char line[96];
   for (const Action& x : p.acts) {
     int len = 0;
@@ -505,6 +505,251 @@ std::string plan_text(const Plan& p) {
     t.append(line, size_t(len));
   }
   return t;
+}
+
+namespace {
+
+// Least cost of reversing [a, a + l) with M units free above x_a when the
+// states differ in size, and the split that reaches it (0: the chain).  One
+// dense table per root reversal [a0, a0 + L) with budget M0, filled
+// bottom-up over (M, l, a) and indexed by (a - a0, l, M).
+class SizedSplits {
+ public:
+  SizedSplits(const std::vector<int64_t>& sizes, const std::vector<double>* costs, int64_t max_table)
+      : z_(sizes), max_table_(max_table) {
+    const size_t n = sizes.size() - 1;
+    pre_.assign(n + 1, 0.0);
+    for (size_t t = 0; t < n; ++t) pre_[t + 1] = pre_[t] + (costs ? (*costs)[t] : 1.0);
+  }
+  double C(int64_t a, int64_t b) const { return pre_[size_t(b)] - pre_[size_t(a)]; }
+  int64_t split(int64_t a, int64_t l, int64_t M) {
+    ensure(a, l, M);
+    return m_[idx(a, l, M)];
+  }
+  double T(int64_t a, int64_t l, int64_t M) {
+    ensure(a, l, M);
+    return v_[idx(a, l, M)];
+  }
+  int64_t z(int64_t t) const { return z_[size_t(t)]; }
+
+ private:
+  void ensure(int64_t a, int64_t l, int64_t M) {
+    if (!(a >= a0_ && a + l <= a0_ + L_ && M <= M0_)) fill(a, l, M);
+  }
+  size_t idx(int64_t a, int64_t l, int64_t M) const { return size_t(((a - a0_) * (L_ + 1) + l) * (M0_ + 1) + M); }
+  void fill(int64_t a0, int64_t L, int64_t M0) {
+    if (M0 < 0) M0 = 0;
+    if (double(L) * double(L + 1) * double(M0 + 1) > double(max_table_))
+      throw std::length_error("schedule: sized table too large");
+    a0_ = a0, L_ = L, M0_ = M0;
+    v_.assign(size_t(L * (L + 1) * (M0 + 1)), 0.0);
+    m_.assign(v_.size(), 0);
+    std::vector<double> chain(size_t(L + 1));
+    for (int64_t M = 0; M <= M0; ++M)
+      for (int64_t a = a0; a < a0 + L; ++a) {
+        // the chain from x_a: restore it and advance i steps, i = l-1 .. 1
+        chain[1] = 0.0;
+        for (int64_t l = 2; a + l <= a0 + L; ++l) chain[size_t(l)] = chain[size_t(l - 1)] + C(a, a + l - 1);
+        for (int64_t l = 2; a + l <= a0 + L; ++l) {
+          double best = 0.0;
+          int64_t bm = 0;
+          for (int64_t m = 1; m < l; ++m) {
+            const int64_t zm = z_[size_t(a + m)];
+            if (zm > M) continue;
+            const double v = C(a, a + m) + v_[idx(a + m, l - m, M - zm)] + v_[idx(a, m, M)];
+            if (bm == 0 || v <= best) best = v, bm = m;
+          }
+          if (bm == 0) best = chain[size_t(l)];
+          v_[idx(a, l, M)] = best;
+          m_[idx(a, l, M)] = int32_t(bm);
+        }
+      }
+  }
+  std::vector<int64_t> z_;
+  std::vector<double> pre_, v_;
+  std::vector<int32_t> m_;
+  int64_t a0_ = 0, L_ = 0, M0_ = -1, max_table_;
+};
+
+struct SizedBuilder {
+  Builder& b;
+  SizedSplits& ss;
+  // Reverse [a, a + l) with M units free above x_a (in slot `base`); the next
+  // snapshot goes to slot `depth`, the top of the stack.
+  void reverse(int64_t a, int64_t l, int64_t M, int64_t base, int64_t depth) {
+    for (;;) {
+      if (l == 1) {
+        b.restore(base, a);
+        b.turn(a);
+        return;
+      }
+      const int64_t m = ss.split(a, l, M);
+      if (m == 0) {
+        for (int64_t i = l - 1; i >= 0; --i) {
+          b.restore(base, a);
+          if (i > 0) b.advance(a, a + i);
+          b.turn(a + i);
+        }
+        return;
+      }
+      b.restore(base, a);
+      b.advance(a, a + m);
+      b.push(Op::Snap, depth, a + m);
+      reverse(a + m, l - m, M - ss.z(a + m), depth, depth + 1);
+      l = m;
+    }
+  }
+};
+
+// The sweep and reverse of the two-level policy with the sized recursion in
+// every interval (M units above each start).
+void two_level_sized(Builder& b, SizedSplits& ss, const std::vector<int64_t>& starts, int64_t M) {
+  const int64_t K = int64_t(starts.size());
+  for (int64_t k = 0; k + 1 < K; ++k) {
+    b.push(Op::Snap, k % 2, starts[size_t(k)]);
+    b.push(Op::Store, k % 2, k, starts[size_t(k)]);
+    b.advance(starts[size_t(k)], starts[size_t(k + 1)]);
+  }
+  SizedBuilder sb{b, ss};
+  for (int64_t k = K - 1; k >= 0; --k) {
+    const int64_t a = starts[size_t(k)];
+    const int64_t l = (k == K - 1 ? b.n : starts[size_t(k + 1)]) - a;
+    if (k == K - 1) b.push(Op::Snap, k % 2, a);
+    if (k >= 1) b.push(Op::Prefetch, k - 1, (k - 1) % 2, starts[size_t(k - 1)]);
+    sb.reverse(a, l, M, k % 2, 2);
+  }
+}
+
+// Unit offsets of every action's fast slot in the stack layout.
+void sized_offsets(Plan& p, const std::vector<int64_t>& z, bool two) {
+  const int64_t zmax = *std::max_element(z.begin(), z.end());
+  std::vector<int64_t> content;
+  auto off = [&](int64_t k) -> int64_t {
+    if (two && k <= 1) return k * zmax;
+    int64_t o = two ? 2 * zmax : 0;
+    for (int64_t j = two ? 2 : 0; j < k; ++j) {
+      if (size_t(j) >= content.size() || content[size_t(j)] < 0) throw std::logic_error("schedule: empty slot below");
+      o += z[size_t(content[size_t(j)])];
+    }
+    return o;
+  };
+  int64_t ids = 0;
+  for (Action& x : p.acts) {
+    int64_t k = -1, t = -1;
+    if (x.op == Op::Snap) k = x.a, t = x.b;
+    else if (x.op == Op::Restore || x.op == Op::Store) k = x.a;
+    else if (x.op == Op::Prefetch) k = x.b, t = x.c;
+    if (k < 0) continue;
+    ids = std::max(ids, k + 1);
+    x.off = off(k);
+    if (t >= 0) {
+      if (content.size() <= size_t(k)) content.resize(size_t(k) + 1, -1);
+      content[size_t(k)] = t;
+    }
+  }
+  p.slot_ids = ids;
+}
+
+void sized_check_args(int64_t n, int32_t s, int64_t H, const std::vector<int64_t>& sizes,
+                      const std::vector<double>* costs) {
+  if (n < 1 || s < 1 || H < 0 || int64_t(sizes.size()) != n + 1)
+    throw std::invalid_argument("schedule: need n >= 1, s >= 1, H >= 0 and n + 1 sizes");
+  for (int64_t z : sizes)
+    if (z < 1 || z > (int64_t(1) << 40)) throw std::invalid_argument("schedule: sizes must be positive");
+  if (costs) {
+    if (int64_t(costs->size()) != n) throw std::invalid_argument("schedule: need one cost per step");
+    for (double c : *costs)
+      if (!(c > 0.0) || !(c < 1e300)) throw std::invalid_argument("schedule: step costs must be positive and finite");
+  }
+}
+
+void sized_finish(Plan& p, SizedSplits& ss, const std::vector<double>* costs, double* cost_out) {
+  p.sized = true;
+  p.weighted = costs != nullptr;
+  p.evals = 1;
+  double cost = 0.0;
+  for (const Action& x : p.acts)
+    if (x.op == Op::Advance) {
+      p.evals += x.b - x.a;
+      cost += ss.C(x.a, x.b);
+    }
+  cost += ss.C(p.n - 1, p.n);
+  if (cost_out) *cost_out = cost;
+}
+
+}  // namespace
+
+Plan make_plan_sized(int64_t n, int32_t s, int64_t H, int64_t interval_min, const std::vector<int64_t>& sizes,
+                     const std::vector<double>* costs, double* cost_out, int64_t max_table) {
+  sized_check_args(n, s, H, sizes, costs);
+  if (interval_min < 0) throw std::invalid_argument("schedule: interval_min must be >= 0");
+  SizedSplits ss(sizes, costs, max_table);
+  const int64_t zmax = *std::max_element(sizes.begin(), sizes.end());
+  const int64_t P = int64_t(s) * zmax;
+  // the plain reversal's cost; a table too large for it leaves only two levels
+  double plain = 0.0;
+  bool plain_ok = true;
+  try {
+    plain = ss.T(0, n, P - sizes[0]);
+  } catch (const std::length_error&) {
+    plain_ok = false;
+  }
+  Plan p;
+  p.n = n;
+  p.s = s;
+  p.H = H;
+  std::vector<int64_t> starts;
+  if (H > 0 && s >= 2) {
+    const int64_t I = std::max<int64_t>({interval_min, 1, (n + H) / (H + 1)});
+    if (I < n) {
+      for (int64_t t = 0; t < n; t += I) starts.push_back(t);
+      double c = ss.C(0, starts.back());
+      for (size_t k = 0; k < starts.size(); ++k) {
+        const int64_t e = k + 1 < starts.size() ? starts[k + 1] : n;
+        c += ss.T(starts[k], e - starts[k], P - 2 * zmax);
+      }
+      if (!plain_ok || c < plain) {
+        p.async = true;
+        p.interval = I;
+      }
+    }
+  }
+  if (!p.async && !plain_ok) throw std::length_error("schedule: sized table too large");
+  Builder b{n, &p.acts, 0, std::vector<char>(size_t(s), 0), {}};
+  if (!p.async) {
+    b.push(Op::Snap, 0, 0);
+    SizedBuilder{b, ss}.reverse(0, n, P - sizes[0], 0, 1);
+  } else {
+    two_level_sized(b, ss, starts, P - 2 * zmax);
+    p.host_slots_used = int64_t(starts.size()) - 1;
+  }
+  sized_offsets(p, sizes, p.async);
+  sized_finish(p, ss, costs, cost_out);
+  return p;
+}
+
+Plan make_plan_sized_starts(int64_t n, int32_t s, int64_t H, const std::vector<int64_t>& starts,
+                            const std::vector<int64_t>& sizes, const std::vector<double>* costs, double* cost_out,
+                            int64_t max_table) {
+  sized_check_args(n, s, H, sizes, costs);
+  if (s < 2 || starts.empty() || starts[0] != 0 || starts.back() >= n || int64_t(starts.size()) - 1 > H)
+    throw std::invalid_argument("schedule: need s >= 2 and starts 0 = t_0 < ... < t_{K-1} < n, K - 1 <= H");
+  for (size_t k = 1; k < starts.size(); ++k)
+    if (starts[k] <= starts[k - 1]) throw std::invalid_argument("schedule: interval starts must increase");
+  SizedSplits ss(sizes, costs, max_table);
+  const int64_t zmax = *std::max_element(sizes.begin(), sizes.end());
+  Plan p;
+  p.n = n;
+  p.s = s;
+  p.H = H;
+  p.async = true;
+  p.dynamic = true;
+  Builder b{n, &p.acts, 0, std::vector<char>(size_t(s), 0), {}};
+  two_level_sized(b, ss, starts, int64_t(s - 2) * zmax);
+  p.host_slots_used = int64_t(starts.size()) - 1;
+  sized_offsets(p, sizes, true);
+  sized_finish(p, ss, costs, cost_out);
+  return p;
 }
 
 }  // namespace ambptt

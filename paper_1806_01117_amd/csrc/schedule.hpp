@@ -18,6 +18,9 @@ enum class Op : uint8_t { Advance, Snap, Restore, First, Youturn, Store, Prefetc
 struct Action {
   Op op;
   int64_t a, b, c;
+  // sized plans: offset of the action's fast slot in units of the pool's
+  // granule (Snap, Restore, Store, Prefetch); -1 elsewhere
+  int64_t off = -1;
 };
 
 struct Plan {
@@ -29,6 +32,8 @@ struct Plan {
   bool dynamic = false;  // interval starts decided during the sweep
   bool online = false;   // placement decided without knowing n (interval = the first I)
   bool weighted = false; // splits chosen for unequal step costs
+  bool sized = false;    // states of different sizes in a byte-addressed pool (Action::off set)
+  int64_t slot_ids = 0;  // fast slot ids used (sized plans may stack more states than s)
   int64_t evals = 0;     // forward-step evaluations
   int64_t host_slots_used = 0;
   std::vector<Action> acts;
@@ -100,6 +105,33 @@ class OnlinePlacement {
 // std::length_error when a reversal's table would exceed max_table entries.
 Plan make_plan_costs(int64_t n, int32_t s, int64_t H, int64_t interval_min, const std::vector<double>& costs,
                      double* cost_out, int64_t max_table = int64_t(1) << 20);
+
+// States of different sizes: sizes[t] (t = 0 .. n, >= 1) is the size of
+// x_t in units of a common granule, and the fast pool holds s * max(sizes)
+// units.  Snapshots stack: the one taken at recursion depth k (slot k) sits
+// above the states in slots below it (in two levels slots 0 and 1 are the
+// interval starts' regions of max(sizes) units each, the stack starting at
+// 2 max(sizes)).  Every reversal of [a, a + l) with M units free above x_a
+// splits by dynamic programming over Revolve's recursion with a budget:
+//   T(a, 1, M) = 0,
+//   T(a, l, M) = min over m with sizes[a+m] <= M of
+//                C(a, a+m) + T(a+m, l-m, M - sizes[a+m]) + T(a, m, M),
+// ties to the largest m, the chain (sum_{i=1}^{l-1} C(a, a+i)) when no
+// snapshot fits; C(a, b) the cost of steps a .. b-1 (costs, or 1 each).
+// Plain: M = s max(sizes) - sizes[0] over [0, n); two levels (H > 0, s >= 2,
+// I = max(I_min, 1, ceil(n / (H + 1))) < n) when strictly cheaper, every
+// interval on M = (s - 2) max(sizes).  Unit sizes give make_plan's
+// schedule.  Sets Action::off and slot_ids; *cost_out (nullable) receives the
+// cost of the forward evaluations.  Throws std::invalid_argument on bad
+// arguments and std::length_error when the table of the reversal the plan
+// runs would exceed max_table entries (l (l + 1) (M + 1) per reversal).
+Plan make_plan_sized(int64_t n, int32_t s, int64_t H, int64_t interval_min, const std::vector<int64_t>& sizes,
+                     const std::vector<double>* costs, double* cost_out, int64_t max_table = int64_t(1) << 20);
+// The two-level plan over interval starts decided during the sweep (as
+// make_plan_starts) with every interval reversed by the sized recursion.
+Plan make_plan_sized_starts(int64_t n, int32_t s, int64_t H, const std::vector<int64_t>& starts,
+                            const std::vector<int64_t>& sizes, const std::vector<double>* costs, double* cost_out,
+                            int64_t max_table = int64_t(1) << 20);
 
 // Mode, interval and forward evaluations only (no action list).
 void plan_counts(int64_t n, int32_t s, int64_t H, int64_t interval_min, bool* async,

@@ -205,3 +205,28 @@ def test_replay_of_sized_schedules_equals_store_all(loss):
         for l in range(n):
             assert np.array_equal(got["dW"][l], want["dW"][l]) and np.array_equal(got["db"][l], want["db"][l])
         assert np.array_equal(got["dx0"][0], want["dx0"][0])
+
+
+amb_lib = pytest.importorskip("paper_1806_01117_amd")
+
+
+def test_c_abi_sized_text_equals_the_oracle():
+    """The library's sized schedule builder against the oracle, byte for byte."""
+    rng = random.Random(37)
+    cases = list(_random_cases(41, 250))
+    cases += [(n, s, [rng.choice([1, 2, 4, 8]) for _ in range(n + 1)], H, I)
+              for n, s, H, I in ((90, 2, 0, 0), (120, 3, 40, 0), (64, 2, 64, 1))]
+    for n, s, sizes, H, I in cases:
+        costs = [rng.choice([1.0, 2.0, 0.5]) for _ in range(n)] if rng.random() < 0.3 else None
+        want = S.text_sized(n, s, sizes, H, I, costs)
+        assert amb_lib.schedule_text_sized(n, s, sizes, H, I, costs) == want, (n, s, sizes, H, I)
+
+
+def test_c_abi_sized_errors():
+    from paper_1806_01117_amd._lib import EINVAL, EUNSUPPORTED, AmbpttError
+    with pytest.raises(AmbpttError) as e:
+        amb_lib.schedule_text_sized(4, 2, [1, 1, 0, 1, 1])
+    assert e.value.status == EINVAL
+    with pytest.raises(AmbpttError) as e:    # one reversal of 400 steps on 1200 units: table too large
+        amb_lib.schedule_text_sized(400, 300, [4] * 401)
+    assert e.value.status == EUNSUPPORTED
