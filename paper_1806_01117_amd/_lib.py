@@ -8,13 +8,13 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libambptt.so")
 
 OK, EINVAL, ENOMEM, EHIP, EUNSUPPORTED, EINTERNAL = 0, -1, -2, -3, -4, -5
-CELL = {"rnn": 1, "lstm": 2, "resmlp": 3}
+CELL = {"rnn": 1, "lstm": 2, "resmlp": 3, "mlp": 4}
 DTYPE = {"f32": 0, "bf16": 1}
 LOSS = {"half_sq_last": 0, "mean_sq_all": 1, "mean_last": 2}
 
 EXPORTS = ["ambptt_version", "ambptt_revolve_advances", "ambptt_schedule_evals", "ambptt_schedule_text",
            "ambptt_schedule_text_starts", "ambptt_schedule_text_online", "ambptt_schedule_text_costs", "ambptt_schedule_text_sized",
-           "ambptt_interval_from_timings", "ambptt_set_step_costs",
+           "ambptt_interval_from_timings", "ambptt_set_step_costs", "ambptt_set_widths",
            "ambptt_resident_program", "ambptt_query", "ambptt_last_error",
            "ambptt_create", "ambptt_bind", "ambptt_set_int", "ambptt_set_file_tier", "ambptt_calibrate", "ambptt_run", "ambptt_run_noalloc",
            "ambptt_last_schedule_text", "ambptt_destroy"]
@@ -87,6 +87,8 @@ def load():
     L.ambptt_schedule_text_sized.argtypes = [i64, i32, i64, i32, C.POINTER(i64), C.POINTER(C.c_double), C.c_char_p, sz,
                                              C.POINTER(sz)]
     L.ambptt_schedule_text_sized.restype = C.c_int
+    L.ambptt_set_widths.argtypes = [vp, C.POINTER(i32), i64]
+    L.ambptt_set_widths.restype = C.c_int
     L.ambptt_set_step_costs.argtypes = [vp, C.POINTER(C.c_double), i64]
     L.ambptt_set_step_costs.restype = C.c_int
     L.ambptt_last_schedule_text.argtypes = [vp, C.c_char_p, sz, C.POINTER(sz)]

@@ -114,7 +114,7 @@ def resident_program(n: int, s: int, H: int = 0, interval_min: int = 0, elide_pr
 
 @dataclasses.dataclass
 class ProblemSpec:
-    cell: str             # "rnn" | "lstm" | "resmlp"
+    cell: str             # "rnn" | "lstm" | "resmlp" | "mlp"
     dtype: str            # "f32" | "bf16"
     loss: str             # "half_sq_last" | "mean_sq_all" | "mean_last"
     batch: int
@@ -124,12 +124,14 @@ class ProblemSpec:
     fast_slots: int
     slow_slots: int = 0
     interval_min: int = 0
+    widths: tuple | None = None  # "mlp": layer widths w_0 .. w_n (None: all = hidden)
 
     @classmethod
     def from_workload(cls, wl, **kw) -> "ProblemSpec":
         d = dict(cell=wl.cell, dtype=wl.dtype, loss=wl.loss, batch=wl.batch, input=wl.input,
                  hidden=wl.hidden, n_steps=wl.n_steps, fast_slots=wl.fast_slots,
-                 slow_slots=wl.host_slots, interval_min=0)
+                 slow_slots=wl.host_slots, interval_min=0,
+                 widths=tuple(getattr(wl, "layer_widths", lambda: None)() or ()) or None)
         d.update(kw)
         return cls(**d)
 
@@ -174,6 +176,9 @@ class Runner:
         check(self.L.ambptt_create(C.byref(self._p), C.c_void_p(self.stream.cuda_stream), C.byref(ctx)))
         self.ctx = ctx
         check(self.L.ambptt_bind(ctx, _ptr(self.pool), self.pool.numel(), _ptr(self.ws), self.ws.numel()))
+        if spec.cell == "mlp" and spec.widths:
+            w = (C.c_int32 * len(spec.widths))(*[int(v) for v in spec.widths])
+            check(self.L.ambptt_set_widths(ctx, w, len(spec.widths)))
 
     # -- checks (shapes, dtypes, device, contiguity) -------------------------
     def _check(self, name, t, shape, dtype):
@@ -191,6 +196,12 @@ class Runner:
         if s.cell == "resmlp":
             self._check("W", W, (n, H, H), op)
             self._check("b", b, (n, H), torch.float32)
+        elif s.cell == "mlp":
+            w = s.widths or (H,) * (n + 1)
+            self._check("W", W, (sum(w[l + 1] * w[l] for l in range(n)),), op)
+            self._check("b", b, (sum(w[1:]),), torch.float32)
+            self._check("h0", h0, (B, w[0]), op)
+            return x, W, b, h0, None
         else:
             self._check("x", x, (n, B, D), op)
             self._check("W", W, (G * H, D + H), op)

@@ -24,7 +24,7 @@ HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
              "-Wno-unused-command-line-argument", "-I", INCLUDE, "-I", CSRC]
 CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-pthread", "-I", INCLUDE, "-I", CSRC]
 
-HIP_SOURCES = ["cell_f32.hip", "gemm_f32.hip", "step_small.hip", "dw_bf16.hip", "dw_f32.hip", "resmlp.hip", "wide_bf16.hip", "resident.hip", "runtime.hip"]
+HIP_SOURCES = ["cell_f32.hip", "gemm_f32.hip", "mlp_f32.hip", "step_small.hip", "dw_bf16.hip", "dw_f32.hip", "resmlp.hip", "wide_bf16.hip", "resident.hip", "runtime.hip"]
 CXX_SOURCES = ["schedule.cpp", "resident_prog.cpp", "tier_file.cpp"]
 
 

@@ -11,8 +11,8 @@
 // for B, so the operands stay in the global row-major layout in LDS (no
 // transpose) and 4 reduction rows cost two 16-byte LDS reads per lane for 16
 // MFMAs.  Stages of 32 rows are double-buffered: the next stage's global
-// reads are in flight while the current one is multiplied, with one barrier
-// per stage.
+// reads are issued before the current one is multiplied and are in flight
+// meanwhile, with one barrier per stage.
 #include <hip/hip_runtime.h>
 
 #include "kernels.hpp"
@@ -71,14 +71,7 @@ __global__ __launch_bounds__(256) void dw_f32_big(DwArgs a) {
   float bsum = 0.f;
   const bool do_bias = blockIdx.y == 0 && tid < kT;
 
-  const int nst = (R + kS - 1) / kS;
-  load(0);
-  stash(0);
-  __syncthreads();
-  for (int st = 0; st < nst; ++st) {
-    const int buf = st & 1;
-    const bool more = st + 1 < nst;
-    if (more) load(st + 1);
+  auto multiply = [&](int buf) {
 #pragma unroll
     for (int kc = 0; kc < kS / 4; ++kc) {
       const f4 av = Zs[buf][4 * kc + q][16 * wm + m];
@@ -93,9 +86,22 @@ __global__ __launch_bounds__(256) void dw_f32_big(DwArgs a) {
 #pragma unroll
       for (int rr = 0; rr < kS; ++rr) bsum += zc[rr * kT];
     }
-    if (more) stash(buf ^ 1);  // buf ^ 1 was last read before the previous barrier
+  };
+  // every stage but the last loads the next one while it multiplies; the
+  // scheduling barriers keep the global loads ahead of the MFMAs
+  const int nst = (R + kS - 1) / kS;
+  load(0);
+  stash(0);
+  __syncthreads();
+  for (int st = 0; st + 1 < nst; ++st) {
+    load(st + 1);
+    __builtin_amdgcn_sched_barrier(0);
+    multiply(st & 1);
+    __builtin_amdgcn_sched_barrier(0);
+    stash((st + 1) & 1);  // that buffer was last read before the previous barrier
     __syncthreads();
   }
+  multiply((nst - 1) & 1);
   // lane (q, m) holds, for accumulator (e, f) and v = 0..3, row i = 4q + v and
   // column j = m of the 16 x 16 product: k = 4i + e, c = 4j + f
   const int c = c0 + 64 * wn + 4 * m;

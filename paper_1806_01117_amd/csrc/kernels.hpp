@@ -84,6 +84,26 @@ struct ProdArgs {
   int M, N, K;
 };
 
+// One launch of the MLP whose layers change width (mlp_f32.hip):
+//   kForward  out = relu(A W^T + bias)                  A [M][K], W [N][K]
+//   kAdjoint  zbar_out = (nn_in + dL/dy') * 1[A W^T + bias > 0], y' = relu(...),
+//             its loss term added to loss_acc[workgroup]
+//   kFinal    out = A W (+ add)                          A [M][K], W [K][N]
+// M >= 1 rows; N and K multiples of 16.  inv = 1 / (M N) of the layer's output.
+struct MlpvArgs {
+  const float* A;
+  const float* W;
+  const float* bias;
+  const float* add;
+  float* out;
+  const float* nn_in;  // adjoint: zbar_{l+1} W_{l+1} [M][N], NULL for the last layer
+  float* zbar_out;
+  double* loss_acc;
+  int M, N, K;
+  int loss, last;
+  float inv;
+};
+
 enum StepMode { kForward = 0, kAdjoint = 1, kFinal = 2 };
 
 // Resident whole-pass kernel (fp32 tanh RNN / LSTM with small states): one
@@ -183,6 +203,10 @@ int mlp_wide_tiles(int B, int w);
 hipError_t launch_mlp_wide(int mode, const MlpArgs& a, hipStream_t s, hipEvent_t e0 = nullptr,
                            hipEvent_t e1 = nullptr);
 hipError_t launch_dw_bf16(const DwArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+// The MLP of layers of different widths: workgroups of one launch on M x N,
+// and the launch (mode kForward, kAdjoint, or kFinal for the NN product).
+int mlpv_tiles(int M, int N);
+hipError_t launch_mlpv(int mode, const MlpvArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_transpose_wh_bf16(const void* W, void* WhT, int GH, int D, int H, hipStream_t s);
 hipError_t launch_transpose_wh(const float* W, float* WhT, int GH, int D, int H, hipStream_t s);
 hipError_t launch_fill32(void* p, size_t words, uint32_t value, hipStream_t s);

@@ -748,15 +748,25 @@ int resident_octet(int ng, int H) {
   return (ng % S == 0 && H % S == 0 && H / S <= kUMmax) ? S : 0;
 }
 
-hipError_t resident_capacity(int G, int* blocks) {
+// The kernel variant a problem runs: its reduction chunks per wave (the
+// register-held weight slice) decide the template instance.
+static const void* resident_fn(int G, int D, int H) {
+  const int nch = (D + H) / 16, kch = (nch + kWaves - 1) / kWaves;
+  if (kch <= 1) return G == 4 ? (const void*)resident_pass<4, 1> : (const void*)resident_pass<1, 1>;
+  if (kch <= 2) return G == 4 ? (const void*)resident_pass<4, 2> : (const void*)resident_pass<1, 2>;
+  if (kch <= 3) return G == 4 ? (const void*)resident_pass<4, 3> : (const void*)resident_pass<1, 3>;
+  return G == 4 ? (const void*)resident_pass<4, kKch> : (const void*)resident_pass<1, kKch>;
+}
+
+hipError_t resident_capacity(int G, int D, int H, int* blocks) {
   int dev = 0, per = 0;
   hipDeviceProp_t prop;
   hipError_t e;
   if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
   if ((e = hipGetDeviceProperties(&prop, dev)) != hipSuccess) return e;
-  if (G == 4) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, resident_pass<4, kKch>, kThreads, 0);
-  else e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, resident_pass<1, kKch>, kThreads, 0);
-  if (e != hipSuccess) return e;
+  // occupancy of the variant that launch_resident will launch for (G, D, H)
+  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, resident_fn(G, D, H), kThreads, 0)) != hipSuccess)
+    return e;
   *blocks = prop.cooperativeLaunch ? per * prop.multiProcessorCount : 0;
   return hipSuccess;
 }
@@ -765,12 +775,7 @@ hipError_t launch_resident(int G, const ResidentArgs& a, hipStream_t s, bool coo
   ResidentArgs arg = a;
   void* args[] = {&arg};
   const dim3 grid(unsigned(a.mtiles * a.ng)), block(kThreads);
-  const int nch = (a.D + a.H) / 16, kch = (nch + kWaves - 1) / kWaves;
-  const void* fn;
-  if (kch <= 1) fn = G == 4 ? (const void*)resident_pass<4, 1> : (const void*)resident_pass<1, 1>;
-  else if (kch <= 2) fn = G == 4 ? (const void*)resident_pass<4, 2> : (const void*)resident_pass<1, 2>;
-  else if (kch <= 3) fn = G == 4 ? (const void*)resident_pass<4, 3> : (const void*)resident_pass<1, 3>;
-  else fn = G == 4 ? (const void*)resident_pass<4, kKch> : (const void*)resident_pass<1, kKch>;
+  const void* fn = resident_fn(G, a.D, a.H);
   if (cooperative) return hipLaunchCooperativeKernel(fn, grid, block, args, 0, s);
   // plain launch: the caller checked that the grid fits the device at once;
   // if other work keeps some workgroups out, the bounded waits end the pass

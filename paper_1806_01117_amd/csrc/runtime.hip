@@ -23,6 +23,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <numeric>
 #include <mutex>
 #include <stdexcept>
 #include <string>
@@ -69,6 +70,7 @@ struct Layout {
   StepCfg cfg{1, 1, 1};  // single-launch path
   bool small = false;    // one-launch small-batch path (step_small)
   bool mlp = false;      // residual MLP (per-layer weights, one-step dW windows)
+  bool mlpv = false;     // MLP of layers of different widths (per-layer weights, states of different sizes)
   // wide-batch bf16 path (B >= 48): cell / layer kernels over up to 128 rows,
   // the adjoint's products as launches of their own (wide_bf16.hip)
   bool wide = false;
@@ -99,7 +101,8 @@ constexpr int kResidentMaxWg = 1024;
 
 ambptt_status validate(const ambptt_problem* p) {
   if (!p) return fail(AMBPTT_EINVAL, "problem is NULL");
-  if (p->cell != AMBPTT_CELL_TANH_RNN && p->cell != AMBPTT_CELL_LSTM && p->cell != AMBPTT_CELL_RESMLP)
+  if (p->cell != AMBPTT_CELL_TANH_RNN && p->cell != AMBPTT_CELL_LSTM && p->cell != AMBPTT_CELL_RESMLP &&
+      p->cell != AMBPTT_CELL_MLP)
     return fail(AMBPTT_EINVAL, "unknown cell");
   if (p->dtype != AMBPTT_F32 && p->dtype != AMBPTT_BF16) return fail(AMBPTT_EINVAL, "unknown dtype");
   if (p->loss < AMBPTT_LOSS_HALF_SQ_LAST || p->loss > AMBPTT_LOSS_MEAN_LAST) return fail(AMBPTT_EINVAL, "unknown loss");
@@ -113,12 +116,15 @@ ambptt_status validate(const ambptt_problem* p) {
   if (p->dtype == AMBPTT_BF16 && (p->hidden % 32 || p->input % 32))
     return fail(AMBPTT_EUNSUPPORTED, "bf16 operands need hidden and input sizes that are multiples of 32");
   if (p->cell == AMBPTT_CELL_RESMLP && p->input != 0) return fail(AMBPTT_EINVAL, "the residual MLP has no step input");
+  if (p->cell == AMBPTT_CELL_MLP && p->input != 0) return fail(AMBPTT_EINVAL, "the MLP has no step input");
+  if (p->cell == AMBPTT_CELL_MLP && p->dtype != AMBPTT_F32)
+    return fail(AMBPTT_EUNSUPPORTED, "the MLP of layers of different widths runs in fp32");
   if ((int64_t)p->batch * p->hidden > (int64_t(1) << 31)) return fail(AMBPTT_EUNSUPPORTED, "state too large");
   return AMBPTT_OK;
 }
 
 int auto_window(const ambptt_problem* p) {
-  if (p->cell == AMBPTT_CELL_RESMLP) return 1;  // every layer has its own dW
+  if (p->cell == AMBPTT_CELL_RESMLP || p->cell == AMBPTT_CELL_MLP) return 1;  // every layer has its own dW
   // rows per window: each window reads and writes dW (fp32) once, so a window
   // must hold enough rows for its products to outweigh that; the bf16 path's
   // dW is large against its operands (4 bytes per weight against 2 bytes per
@@ -134,6 +140,7 @@ Layout make_layout(const ambptt_problem* p, int window) {
   L.dsize = p->dtype == AMBPTT_BF16 ? 2 : 4;
   L.window = window > 0 ? window : auto_window(p);
   L.mlp = p->cell == AMBPTT_CELL_RESMLP;
+  L.mlpv = p->cell == AMBPTT_CELL_MLP;
   const size_t BH = (size_t)p->batch * p->hidden;
   const size_t GH = (size_t)L.G * p->hidden;
   L.h_bytes = BH * L.dsize;
@@ -163,7 +170,7 @@ Layout make_layout(const ambptt_problem* p, int window) {
     const int tiles = L.mlp ? mlp_wide_tiles(p->batch, p->hidden) : cell_wide_tiles(L.G, p->batch, p->hidden);
     L.loss_slots = std::max(L.loss_slots, 8 * ((tiles + 7) / 8));
   }
-  if (!L.mlp && p->dtype == AMBPTT_F32) {
+  if (!L.mlp && !L.mlpv && p->dtype == AMBPTT_F32) {
     const int U = resident_units(L.G);
     const int K1 = p->input + p->hidden;
     const int mtiles = (p->batch + 15) / 16, ng = p->hidden / U;
@@ -182,20 +189,25 @@ Layout make_layout(const ambptt_problem* p, int window) {
       L.loss_slots = std::max(L.loss_slots, L.r_nwg);
     }
   }
-  if (!L.small && !L.mlp && p->dtype == AMBPTT_F32 && cell_gemm_f32_fits(L.G, p->batch, p->input, p->hidden))
+  if (!L.small && !L.mlp && !L.mlpv && p->dtype == AMBPTT_F32 &&
+      cell_gemm_f32_fits(L.G, p->batch, p->input, p->hidden))
     L.loss_slots = std::max(L.loss_slots, cell_gemm_f32_tiles(L.G, p->batch, p->hidden));
   size_t o = 0;
   L.off_live[0] = o; o += L.stride;
   L.off_live[1] = o; o += L.stride;
-  L.off_wht = o; o += L.mlp ? 0 : align_up((size_t)p->hidden * GH * L.dsize);
+  if (L.mlpv) {
+    L.small = false;
+    L.loss_slots = mlpv_tiles(p->batch, p->hidden);
+  }
+  L.off_wht = o; o += (L.mlp || L.mlpv) ? 0 : align_up((size_t)p->hidden * GH * L.dsize);
   L.off_zbar = o; o += align_up(2 * (size_t)L.window * p->batch * GH * L.dsize);
   L.off_hwin = o; o += align_up(2 * (size_t)L.window * BH * L.dsize);
   L.off_cbar[0] = o; o += align_up(BH * 4);
   L.off_cbar[1] = o; o += align_up(BH * 4);
   L.off_loss = o; o += align_up((size_t)L.loss_slots * 8);
   L.off_lossout = o; o += kAlign;
-  L.hsep = !L.small && !L.mlp && p->dtype == AMBPTT_F32;
-  if (L.wide || L.hsep) {
+  L.hsep = !L.small && !L.mlp && !L.mlpv && p->dtype == AMBPTT_F32;
+  if (L.wide || L.hsep || L.mlpv) {
     L.off_hbar = o; o += align_up(BH * 4);
   }
   if (L.res) {
@@ -273,6 +285,12 @@ struct ambptt_ctx {
   // into a fast slot before a prefetch refills it
   int64_t test_copy_delay_us = 0;
   bool test_poison = false;
+  // the MLP of layers of different widths: w_0 .. w_n, the offsets of each
+  // layer's weights and bias, and the state sizes in units of `unit` bytes
+  std::vector<int32_t> widths;
+  std::vector<size_t> woff, boff;
+  std::vector<int64_t> zunits;
+  size_t unit = 0;
   int host_waits = -1;      // slot dependencies on host-tier copies: 1 waited for on the host, 0 stream waits, -1 by path
   hipEvent_t ev_end[8] = {};  // end events recorded by compute dispatches (host-tier copies and sweep pacing wait on them)
   Plan last_plan;        // the schedule the last ambptt_run executed
@@ -316,6 +334,11 @@ int64_t interval_from_timings(double ta, double tt, int64_t s, int rule, double 
 Plan pass_plan(ambptt_ctx* C) {
   const ambptt_problem& p = C->p;
   const int64_t I = std::max<int64_t>(C->interval_min, 1);
+  if (C->L.mlpv) {  // states of different sizes: the sized recursion in every reversal
+    if (C->online) throw std::invalid_argument("online checkpointing is not available for states of different sizes");
+    return make_plan_sized(p.n_steps, p.fast_slots, slow_capacity(C), I, C->zunits,
+                           C->step_costs.empty() ? nullptr : &C->step_costs, &C->plan_cost);
+  }
   if (C->online) return make_plan_online(p.n_steps, p.fast_slots, p.slow_slots, I);
   if (!C->step_costs.empty()) {  // the dynamic program runs once per set of inputs
     const int64_t key[3] = {I, slow_capacity(C), C->costs_version};
@@ -326,6 +349,28 @@ Plan pass_plan(ambptt_ctx* C) {
     return C->cost_plan;
   }
   return make_plan(p.n_steps, p.fast_slots, slow_capacity(C), I);
+}
+
+// Widths of the MLP's layers: weight and bias offsets, state sizes in units
+// of their greatest common divisor (every size is a multiple of 256 bytes).
+void set_layer_widths(ambptt_ctx* C, const std::vector<int32_t>& w) {
+  C->widths = w;
+  const size_t n = w.size() - 1;
+  C->woff.assign(n + 1, 0);
+  C->boff.assign(n + 1, 0);
+  for (size_t l = 0; l < n; ++l) {
+    C->woff[l + 1] = C->woff[l] + size_t(w[l + 1]) * size_t(w[l]);
+    C->boff[l + 1] = C->boff[l] + size_t(w[l + 1]);
+  }
+  std::vector<size_t> bytes(n + 1);
+  size_t g = 0;
+  for (size_t t = 0; t <= n; ++t) {
+    bytes[t] = align_up(size_t(C->p.batch) * size_t(w[t]) * 4);
+    g = std::gcd(g, bytes[t]);
+  }
+  C->unit = g;
+  C->zunits.resize(n + 1);
+  for (size_t t = 0; t <= n; ++t) C->zunits[t] = int64_t(bytes[t] / g);
 }
 
 unsigned event_flags(const ambptt_ctx* C, bool timing) {
@@ -418,6 +463,19 @@ char* host_slot(const ambptt_ctx* C, int64_t h) {
 // Stream callback of the copy-delay test knob: holds its stream for a bounded time.
 void delay_cb(void* us) { std::this_thread::sleep_for(std::chrono::microseconds((intptr_t)us)); }
 
+// Sized plans may stack more snapshots than there are fast slots: slot ids
+// up to `ids` get their synchronisation events.
+ambptt_status grow_slot_events(ambptt_ctx* C, int64_t ids) {
+  if (ids <= int64_t(C->pend.size())) return AMBPTT_OK;
+  if (C->no_alloc) return fail(AMBPTT_EINVAL, "this pass needs slot events that are not reserved (ambptt_set_int \"reserve\")");
+  const size_t k0 = C->ev_slot.size();
+  C->ev_slot.resize(size_t(ids), nullptr);
+  for (size_t k = k0; k < C->ev_slot.size(); ++k)
+    HIPCK(hipEventCreateWithFlags(&C->ev_slot[k], event_flags(C, false)));
+  C->pend.resize(size_t(ids), kNone);
+  return AMBPTT_OK;
+}
+
 struct Sample {
   int cls;
   hipEvent_t a, b;
@@ -456,7 +514,9 @@ struct Exec {
   float* hbuf = nullptr;   // the adjoint's product (fp32 [B][H]) on those two paths
 
   Exec(ambptt_ctx* c, const void* x_, const void* W_, const float* b_)
-      : C(c), L(c->L), p(c->p), x((const char*)x_), W(W_), b(b_), slot_t(size_t(c->p.fast_slots), -1) {
+      : C(c), L(c->L), p(c->p), x((const char*)x_), W(W_), b(b_), slot_t(c->pend.size(), -1) {
+    slot_off.resize(C->pend.size());
+    for (size_t k = 0; k < slot_off.size(); ++k) slot_off[k] = k * L.stride;
     WhT = C->ws + L.off_wht;
     wide = L.wide && C->wide_opt;
     sep32 = L.hsep && C->hadj_launch;
@@ -467,11 +527,36 @@ struct Exec {
       lds_prod = sep32 && C->lds_gemm > 0 && prod_gemm_f32_fits(B, H, G * H) &&
                  (C->lds_gemm == 2 || prod_gemm_f32_tiles(B, H) >= 128);
     }
-    if (wide || sep32) hbuf = (float*)(C->ws + L.off_hbar);
+    if (wide || sep32 || L.mlpv) hbuf = (float*)(C->ws + L.off_hbar);
   }
   const void* x_at(int64_t t) const { return x + (size_t)t * p.batch * p.input * L.dsize; }
 
-  char* slot(int64_t k) const { return C->pool + (size_t)k * L.stride; }
+  // byte offset of every fast slot: k * stride, or in sized plans the stacked
+  // offset the plan's action names (set when the slot is written)
+  std::vector<size_t> slot_off;
+  char* slot(int64_t k) const { return C->pool + slot_off[size_t(k)]; }
+  // bytes of state x_t (the MLP's states differ in size)
+  size_t bytes_of(int64_t t) const {
+    return L.mlpv ? align_up(size_t(p.batch) * size_t(C->widths[size_t(t)]) * 4) : L.state_bytes;
+  }
+  ambptt_status grow_slots(int64_t ids) {
+    const ambptt_status s = grow_slot_events(C, ids);
+    if (s != AMBPTT_OK) return s;
+    for (size_t k = slot_off.size(); k < C->pend.size(); ++k) slot_off.push_back(k * L.stride);
+    slot_t.resize(C->pend.size(), -1);
+    return AMBPTT_OK;
+  }
+  // a sized plan's action places slot k at A.off units; a write moves the
+  // slot there, a read must find it there; the state must lie in the pool
+  ambptt_status place(const Action& A, int64_t k, int64_t t, bool write) {
+    if (A.off < 0) return AMBPTT_OK;
+    const size_t o = size_t(A.off) * C->unit;
+    if (o + bytes_of(t) > size_t(p.fast_slots) * L.stride)
+      return fail(AMBPTT_EINTERNAL, "sized plan: a state past the end of the slot pool");
+    if (write) slot_off[size_t(k)] = o;
+    else if (slot_off[size_t(k)] != o) return fail(AMBPTT_EINTERNAL, "sized plan: a slot read away from where it was written");
+    return AMBPTT_OK;
+  }
   char* live(int i) const { return C->ws + L.off_live[i]; }
   void* hpart(char* s) const { return s; }
   float* cpart(char* s) const { return (float*)(s + align_up(L.h_bytes)); }
@@ -576,8 +661,28 @@ struct Exec {
     return a;
   }
 
+  // layer t of the MLP of different widths: M = B rows, N = w_{t+1}, K = w_t
+  MlpvArgs mlpv_args(int64_t t) const {
+    MlpvArgs a{};
+    a.W = (const float*)W + C->woff[size_t(t)];
+    a.bias = b + C->boff[size_t(t)];
+    a.M = p.batch;
+    a.N = C->widths[size_t(t) + 1];
+    a.K = C->widths[size_t(t)];
+    a.loss = p.loss;
+    a.last = t == p.n_steps - 1;
+    a.inv = 1.0f / float(double(p.batch) * double(a.N));
+    return a;
+  }
+
   ambptt_status fwd_step(int64_t t, char* src, char* dst) {
     st.forward_evals++;
+    if (L.mlpv) {
+      MlpvArgs a = mlpv_args(t);
+      a.A = (const float*)src;
+      a.out = (float*)dst;
+      return timed(AMBPTT_K_FWD, [&](hipEvent_t e0, hipEvent_t e1) { return launch_mlpv(kForward, a, C->cs, e0, e1); });
+    }
     if (L.mlp) {
       MlpArgs a = mlp_args(t);
       a.y = src;
@@ -627,7 +732,27 @@ struct Exec {
       dw_pending[hf] = false;
     }
     ambptt_status s;
-    if (L.mlp) {
+    if (L.mlpv) {
+      MlpvArgs a = mlpv_args(t);
+      a.A = (const float*)cur;
+      a.zbar_out = (float*)zbar_at(t);
+      a.loss_acc = (double*)(C->ws + L.off_loss);
+      if (!first) {  // u = zbar_{t+1} W_{t+1}: N = w_{t+1}, K = w_{t+2}
+        MlpvArgs u = mlpv_args(t + 1);
+        u.A = (const float*)zbar_at(t + 1);
+        u.out = hbuf;
+        u.N = C->widths[size_t(t) + 1];
+        u.K = C->widths[size_t(t) + 2];
+        s = timed(AMBPTT_K_HADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch_mlpv(kFinal, u, C->cs, e0, e1); });
+        if (s != AMBPTT_OK) return s;
+        a.nn_in = hbuf;
+      }
+      s = timed(AMBPTT_K_ADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch_mlpv(kAdjoint, a, C->cs, e0, e1); });
+      if (s != AMBPTT_OK) return s;
+      // y_t beside zbar_t for the layer's weight gradient
+      HIPCK(hipMemcpyAsync(hwin_at(t), cur, size_t(p.batch) * size_t(C->widths[size_t(t)]) * 4,
+                           hipMemcpyDeviceToDevice, C->cs));
+    } else if (L.mlp) {
       MlpArgs a = mlp_args(t);
       a.y = cur;
       a.first = first;
@@ -694,6 +819,13 @@ struct Exec {
         d.db = db + (size_t)t * p.hidden;
         d.accumulate = 0;
       }
+      if (L.mlpv) {  // layer t's own gradient [w_{t+1}][w_t], written once
+        d.dW = dW + C->woff[size_t(t)];
+        d.db = db + C->boff[size_t(t)];
+        d.H = C->widths[size_t(t)];
+        d.GH = C->widths[size_t(t) + 1];
+        d.accumulate = 0;
+      }
       // the wide-batch bf16 kernels and the large-batch fp32 kernels each fill
       // the device: beside them a window only competes for the same units, so
       // it runs in line on the compute stream
@@ -721,6 +853,14 @@ struct Exec {
 
   // dL/dx_0 = (zbar_0 W_h, cbar_0)
   ambptt_status final_step(float* dh0, float* dc0) {
+    if (L.mlpv) {  // dL/dy_0 = zbar_0 W_0: N = w_0, K = w_1
+      MlpvArgs u = mlpv_args(0);
+      u.A = (const float*)zbar_at(0);
+      u.out = dh0;
+      u.N = C->widths[0];
+      u.K = C->widths[1];
+      return timed(AMBPTT_K_OTHER, [&](hipEvent_t e0, hipEvent_t e1) { return launch_mlpv(kFinal, u, C->cs, e0, e1); });
+    }
     if (L.mlp) {
       MlpArgs a = mlp_args(0);
       a.Wn = W_of(0);
@@ -758,8 +898,8 @@ struct Exec {
     return AMBPTT_OK;
   }
 
-  ambptt_status copy_state(char* dst, char* src) {
-    HIPCK(hipMemcpyAsync(dst, src, L.state_bytes, hipMemcpyDeviceToDevice, C->cs));
+  ambptt_status copy_state(char* dst, char* src, size_t bytes) {
+    HIPCK(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, C->cs));
     tail_ok = false;
     return AMBPTT_OK;
   }
@@ -861,6 +1001,7 @@ struct Exec {
             const bool last = (t + 1 == A.b);
             if (last && fuse_k >= 0) {
               if ((s = wait_slot(fuse_k, true)) != AMBPTT_OK) return s;
+              if ((s = place(acts[i + 1], fuse_k, A.b, true)) != AMBPTT_OK) return s;
               if ((s = fwd_step(t, cur, slot(fuse_k))) != AMBPTT_OK) return s;
               set_cur_slot(fuse_k);
             } else {
@@ -880,17 +1021,20 @@ struct Exec {
         case Op::Snap: {
           st.takeshots++;
           if (cur_slot == A.a) {  // already there
+            if ((s = place(A, A.a, A.b, false)) != AMBPTT_OK) return s;
             slot_t[size_t(A.a)] = A.b;
             break;
           }
           if ((s = wait_slot(A.a, true)) != AMBPTT_OK) return s;
-          if ((s = copy_state(slot(A.a), cur)) != AMBPTT_OK) return s;
+          if ((s = place(A, A.a, A.b, true)) != AMBPTT_OK) return s;
+          if ((s = copy_state(slot(A.a), cur, bytes_of(A.b))) != AMBPTT_OK) return s;
           st.takeshot_copies++;
           slot_t[size_t(A.a)] = A.b;
           break;
         }
         case Op::Restore: {
           st.restores++;
+          if ((s = place(A, A.a, A.b, false)) != AMBPTT_OK) return s;
           if ((s = wait_slot(A.a, false)) != AMBPTT_OK) return s;
           set_cur_slot(A.a);
           live_dead = false;
@@ -904,9 +1048,10 @@ struct Exec {
           const int64_t k = A.a, h = A.b;
           char* dst = host_slot(C, h);
           if (C->ftier && !(dst = C->ftier->store_buffer(h))) return fail(AMBPTT_EINTERNAL, C->ftier->error());
+          if ((s = place(A, k, A.c, false)) != AMBPTT_OK) return s;
           if ((s = copy_after_compute()) != AMBPTT_OK) return s;
           if ((s = test_delay(C->xs)) != AMBPTT_OK) return s;
-          HIPCK(hipMemcpyAsync(dst, slot(k), L.state_bytes, hipMemcpyDeviceToHost, C->xs));
+          HIPCK(hipMemcpyAsync(dst, slot(k), bytes_of(A.c), hipMemcpyDeviceToHost, C->xs));
           HIPCK(hipEventRecord(C->ev_slot[size_t(k)], C->xs));
           if (C->ftier) {  // written behind to the file once the copy has landed
             hipEvent_t ev = C->ev_file[size_t(h % int64_t(C->ev_file.size()))];
@@ -915,12 +1060,13 @@ struct Exec {
           }
           if (C->pend[size_t(k)] != kPrefetchPending) C->pend[size_t(k)] = kStorePending;
           st.stores++;
-          st.bytes_d2h += (int64_t)L.state_bytes;
+          st.bytes_d2h += (int64_t)bytes_of(A.c);
           break;
         }
         case Op::Prefetch: {
           const int64_t h = A.a, k = A.b, t = A.c;
           st.prefetches++;
+          if ((s = place(A, k, t, true)) != AMBPTT_OK) return s;
           if (C->elide_prefetch && slot_t[size_t(k)] == t) {
             st.prefetches_elided++;
             if (C->ftier) C->ftier->prefetched(h, [] { return true; });  // nothing copied out of the buffer
@@ -928,7 +1074,7 @@ struct Exec {
           }
           if (cur_slot == k && !live_dead) {  // the live state aliases the target: keep it
             char* dst = live(0);
-            if ((s = copy_state(dst, cur)) != AMBPTT_OK) return s;
+            if ((s = copy_state(dst, cur, bytes_of(slot_t[size_t(k)]))) != AMBPTT_OK) return s;
             set_cur_live(dst);
           }
           const char* src = host_slot(C, h);
@@ -938,7 +1084,7 @@ struct Exec {
           // so compute reading it too early shows in the gradients
           if (C->test_poison) HIPCK(hipMemsetAsync(slot(k), 0xFF, L.state_bytes, C->xs));
           if ((s = test_delay(C->xs)) != AMBPTT_OK) return s;
-          HIPCK(hipMemcpyAsync(slot(k), src, L.state_bytes, hipMemcpyHostToDevice, C->xs));
+          HIPCK(hipMemcpyAsync(slot(k), src, bytes_of(t), hipMemcpyHostToDevice, C->xs));
           HIPCK(hipEventRecord(C->ev_slot[size_t(k)], C->xs));
           if (C->ftier) {  // the buffer takes the slot h - R from the file once this copy is done
             hipEvent_t ev = C->ev_file[size_t(h % int64_t(C->ev_file.size()))];
@@ -947,7 +1093,7 @@ struct Exec {
           }
           C->pend[size_t(k)] = kPrefetchPending;
           slot_t[size_t(k)] = t;
-          st.bytes_h2d += (int64_t)L.state_bytes;
+          st.bytes_h2d += (int64_t)bytes_of(t);
           break;
         }
       }
@@ -959,7 +1105,7 @@ struct Exec {
 ambptt_status prepare_inputs(ambptt_ctx* C, const void* W, const void* h0, const float* c0, Exec& E) {
   const Layout& L = C->L;
   const ambptt_problem& p = C->p;
-  if (L.mlp) {
+  if (L.mlp || L.mlpv) {
     // no transposed weights: the residual MLP kernels transpose W tiles in LDS
   } else if (p.dtype == AMBPTT_BF16) {
     HIPCK(launch_transpose_wh_bf16(W, E.WhT, L.G * p.hidden, p.input, p.hidden, C->cs));
@@ -968,7 +1114,9 @@ ambptt_status prepare_inputs(ambptt_ctx* C, const void* W, const void* h0, const
   }
   // live state <- x_0
   char* l0 = E.live(0);
-  HIPCK(hipMemcpyAsync(l0, h0, L.h_bytes, hipMemcpyDeviceToDevice, C->cs));
+  // the MLP's y_0 is [B][w_0]
+  const size_t hb = L.mlpv ? size_t(p.batch) * size_t(C->widths[0]) * 4 : L.h_bytes;
+  HIPCK(hipMemcpyAsync(l0, h0, hb, hipMemcpyDeviceToDevice, C->cs));
   if (L.G == 4) HIPCK(hipMemcpyAsync(E.cpart(l0), c0, L.c_bytes, hipMemcpyDeviceToDevice, C->cs));
   E.set_cur_live(l0);
   return AMBPTT_OK;
@@ -1266,6 +1414,21 @@ static bool costs_ok(const double* costs, int64_t n) {
   return true;
 }
 
+ambptt_status ambptt_set_widths(ambptt_ctx* C, const int32_t* widths, int64_t count) {
+  if (!C || !widths) return fail(AMBPTT_EINVAL, "ctx/widths is NULL");
+  if (!C->L.mlpv) return fail(AMBPTT_EINVAL, "layer widths belong to the MLP cell");
+  if (count != C->p.n_steps + 1) return fail(AMBPTT_EINVAL, "need n + 1 widths");
+  int32_t top = 0;
+  for (int64_t t = 0; t < count; ++t) {
+    const int32_t w = widths[t];
+    if (w < 16 || w % 16 || w > C->p.hidden) return fail(AMBPTT_EINVAL, "widths must be multiples of 16 up to hidden");
+    top = std::max(top, w);
+  }
+  if (top != C->p.hidden) return fail(AMBPTT_EINVAL, "the largest width must equal the problem's hidden size");
+  set_layer_widths(C, std::vector<int32_t>(widths, widths + count));
+  return AMBPTT_OK;
+}
+
 ambptt_status ambptt_set_step_costs(ambptt_ctx* C, const double* costs, int64_t n) {
   if (!C) return fail(AMBPTT_EINVAL, "ctx is NULL");
   if (!costs || n == 0) {
@@ -1399,6 +1562,7 @@ ambptt_status ambptt_create(const ambptt_problem* p, void* stream, ambptt_ctx** 
   }
   if ((e = hipStreamCreateWithFlags(&C->xs, hipStreamNonBlocking)) != hipSuccess) return bail("hipStreamCreate", e);
   if ((e = hipStreamCreateWithFlags(&C->ds, hipStreamNonBlocking)) != hipSuccess) return bail("hipStreamCreate", e);
+  if (C->L.mlpv) set_layer_widths(C, std::vector<int32_t>(size_t(p->n_steps) + 1, p->hidden));
   C->ev_slot.resize(size_t(p->fast_slots), nullptr);
   C->pend.assign(size_t(p->fast_slots), kNone);
   if ((e = make_sync_events(C)) != hipSuccess) return bail("hipEventCreate", e);
@@ -1653,6 +1817,7 @@ static ambptt_status reserve(ambptt_ctx* C) {
     return fail(AMBPTT_EINTERNAL, e.what());
   }
   ambptt_status s;
+  if ((s = grow_slot_events(C, plan.slot_ids)) != AMBPTT_OK) return s;
   if (res) {
     if ((s = ensure_prog_host(C, prog.size() + 4)) != AMBPTT_OK) return s;
     if (plan.async) return ensure_host(C, plan.host_slots_used, size_t(C->L.r_nwg) * 1024, true);
@@ -1675,6 +1840,8 @@ static ambptt_status run_pass(ambptt_ctx* C, const void* x_seq, const void* W, c
   if (C->path_opt == 2 && !resident_possible(C))
     return fail(AMBPTT_EUNSUPPORTED, "the resident kernel does not fit this problem on this device");
   if (resident_possible(C)) return resident_run(C, x_seq, W, b, h0, c0, dW, db, dh0, dc0, loss, stats);
+  if (L.mlpv && C->online)
+    return fail(AMBPTT_EUNSUPPORTED, "online checkpointing is not available for states of different sizes");
   const double t0 = now_us();
   Plan plan;
   try {
@@ -1707,6 +1874,7 @@ static ambptt_status run_pass(ambptt_ctx* C, const void* x_seq, const void* W, c
     }
   }
   Exec E(C, x_seq, W, b);
+  if ((s = E.grow_slots(plan.slot_ids)) != AMBPTT_OK) return s;
   std::fill(C->pend.begin(), C->pend.end(), kNone);
   const size_t GH = (size_t)L.G * p.hidden;
   if (!L.mlp) {  // windows accumulate into dW; the MLP writes each layer once
@@ -1719,11 +1887,14 @@ static ambptt_status run_pass(ambptt_ctx* C, const void* x_seq, const void* W, c
     std::vector<int64_t> starts;
     if ((s = E.dynamic_sweep(starts, dW, db)) != AMBPTT_OK) return s;
     try {
-      plan = make_plan_starts(p.n_steps, p.fast_slots, slow_capacity(C), starts,
-                              C->step_costs.empty() ? nullptr : &C->step_costs, &C->plan_cost);
+      const std::vector<double>* costs = C->step_costs.empty() ? nullptr : &C->step_costs;
+      plan = L.mlpv ? make_plan_sized_starts(p.n_steps, p.fast_slots, slow_capacity(C), starts, C->zunits, costs,
+                                             &C->plan_cost)
+                    : make_plan_starts(p.n_steps, p.fast_slots, slow_capacity(C), starts, costs, &C->plan_cost);
     } catch (const std::exception& e) {
       return fail(AMBPTT_EINTERNAL, e.what());
     }
+    if ((s = E.grow_slots(plan.slot_ids)) != AMBPTT_OK) return s;
     for (size_t k = 1; k <= starts.size(); ++k)  // the longest interval
       plan.interval = std::max(plan.interval, (k < starts.size() ? starts[k] : p.n_steps) - starts[k - 1]);
     // the sweep ran the plan's first 3 (K - 1) actions: snapshot, store and advance per stored start

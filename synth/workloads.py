@@ -57,6 +57,7 @@ class Workload:
     forget_bias: float = 0.0
     h0_std: float = 0.0       # rnn h0 / resmlp y0 standard deviation
     seed_index: int = 0
+    widths: tuple = ()        # "mlp": layer widths cycled from w_0 (empty: all = hidden)
 
     @property
     def gates(self) -> int:
@@ -69,6 +70,14 @@ class Workload:
     @property
     def host_slots(self) -> int:
         return self.n_steps if self.slow_slots < 0 else self.slow_slots
+
+    def layer_widths(self) -> list[int] | None:
+        """w_0 .. w_n of the MLP of layers of different widths (the pattern
+        repeated), or None for the other cells."""
+        if self.cell != "mlp":
+            return None
+        pat = self.widths or (self.hidden,)
+        return [int(pat[t % len(pat)]) for t in range(self.n_steps + 1)]
 
     def with_(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)
@@ -91,6 +100,11 @@ WORKLOADS: dict[str, Workload] = {w.name: w for w in [
     Workload("resmlp_w4096_l2000_bf16", "resmlp", "bf16", batch=256, input=0, hidden=4096,
              n_steps=2000, fast_slots=16, slow_slots=-1, loss="half_sq_last",
              w_dist="normal", w_scale=0.02 / math.sqrt(2000), h0_std=1.0, seed_index=4),
+    # MLP of layers of different widths (as before and after a pooling layer):
+    # states of 1, 1/2 and 1/4 of the largest size, fp32, He-scaled weights
+    Workload("mlp_widths_l2000", "mlp", "f32", batch=256, input=0, hidden=1024, n_steps=2000,
+             fast_slots=16, slow_slots=-1, loss="half_sq_last",
+             w_dist="he", w_scale=1.0, h0_std=1.0, seed_index=6, widths=(1024, 512, 256, 512)),
     # offload-stress LSTM: 16 MiB of fp32 state per step, 20000 steps
     Workload("lstm_h4096_t20000", "lstm", "f32", batch=512, input=1024, hidden=4096,
              n_steps=20000, fast_slots=64, slow_slots=-1, loss="mean_last",
@@ -157,6 +171,8 @@ def x_slice(wl: Workload, t0: int, t1: int) -> np.ndarray:
 
 
 def _draw_w(wl: Workload, rng: np.random.Generator, shape) -> np.ndarray:
+    if wl.w_dist == "he":  # N(0, 2 / fan_in) times w_scale
+        return (rng.standard_normal(shape) * (wl.w_scale * math.sqrt(2.0 / shape[1]))).astype(np.float32)
     if wl.w_dist == "uniform":
         return (rng.random(shape) * (2.0 * wl.w_scale) - wl.w_scale).astype(np.float32)
     return (rng.standard_normal(shape) * wl.w_scale).astype(np.float32)
@@ -174,11 +190,17 @@ def params(wl: Workload) -> tuple[np.ndarray, np.ndarray]:
 
 
 def layer_params(wl: Workload, layer: int) -> tuple[np.ndarray, np.ndarray]:
-    """(W_l[w][w], b_l[w]) as float32 for one residual-MLP layer, seeded by l."""
-    assert wl.cell == "resmlp"
-    w = wl.hidden
-    W = _as_operand(wl, _draw_w(wl, _rng(wl, _S_LAYER, layer), (w, w)))
-    return W, np.zeros(w, np.float32)
+    """(W_l, b_l) as float32 for one layer, seeded by l: [w][w] and [w] for
+    the residual MLP, [w_{l+1}][w_l] and [w_{l+1}] for the MLP of layers of
+    different widths."""
+    assert wl.cell in ("resmlp", "mlp")
+    if wl.cell == "mlp":
+        ws = wl.layer_widths()
+        shape = (ws[layer + 1], ws[layer])
+    else:
+        shape = (wl.hidden, wl.hidden)
+    W = _as_operand(wl, _draw_w(wl, _rng(wl, _S_LAYER, layer), shape))
+    return W, np.zeros(shape[0], np.float32)
 
 
 def initial_state(wl: Workload) -> dict[str, np.ndarray]:
@@ -188,5 +210,6 @@ def initial_state(wl: Workload) -> dict[str, np.ndarray]:
         return {"h": _as_operand(wl, h0)}
     if wl.cell == "lstm":
         return {"h": np.zeros((B, H), np.float32), "c": np.zeros((B, H), np.float32)}
-    y0 = _rng(wl, _S_X0).standard_normal((B, H)) * wl.h0_std
+    w0 = wl.layer_widths()[0] if wl.cell == "mlp" else H
+    y0 = _rng(wl, _S_X0).standard_normal((B, w0)) * wl.h0_std
     return {"h": _as_operand(wl, y0)}

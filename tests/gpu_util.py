@@ -27,6 +27,9 @@ def inputs(wl):
     if wl.cell == "resmlp":
         Ws, bs = zip(*(synth.layer_params(wl, l) for l in range(wl.n_steps)))
         return None, np.stack(Ws), np.stack(bs), x0
+    if wl.cell == "mlp":  # layers of different widths, one after the other
+        Ws, bs = zip(*(synth.layer_params(wl, l) for l in range(wl.n_steps)))
+        return None, np.concatenate([w.ravel() for w in Ws]), np.concatenate(bs), x0
     x = synth.x_slice(wl, 0, wl.n_steps)
     W, b = synth.params(wl)
     return x, W, b, x0
@@ -79,7 +82,28 @@ def run_gpu(wl, dev_in, window: int | None = None, timing_sample: int = 0, elide
     return res
 
 
+def mlp_layers(wl, W, b):
+    """Per-layer (W_l, b_l) views of the MLP's flat parameters."""
+    ws = wl.layer_widths()
+    out, o, ob = [], 0, 0
+    for l in range(wl.n_steps):
+        m, k = ws[l + 1], ws[l]
+        out.append((W[o:o + m * k].reshape(m, k), b[ob:ob + m]))
+        o += m * k
+        ob += m
+    return out
+
+
 def run_oracle(wl, x, W, b, x0):
+    if wl.cell == "mlp":
+        layers = mlp_layers(wl, W, b)
+        cell = bptt.cell_for(wl, layer=lambda l: (layers[l][0].astype(np.float64), layers[l][1].astype(np.float64)))
+        n, B = wl.n_steps, wl.batch
+        out = bptt.store_all(cell, n, lambda t: np.zeros((B, 0)), (x0["h"].astype(np.float64),))
+        z = [out["states"][l][0] @ layers[l][0].astype(np.float64).T + layers[l][1] for l in range(n)]
+        return {"loss": out["loss"], "dW": np.concatenate([out["dW"][l].ravel() for l in range(n)]),
+                "db": np.concatenate([out["db"][l] for l in range(n)]), "dh0": out["dx0"][0], "z": z,
+                "dW_layers": [out["dW"][l] for l in range(n)], "db_layers": [out["db"][l] for l in range(n)]}
     if wl.cell == "resmlp":
         cell = bptt.cell_for(wl, layer=lambda l: (W[l].astype(np.float64), b[l].astype(np.float64)))
         n, B = wl.n_steps, wl.batch
@@ -88,7 +112,8 @@ def run_oracle(wl, x, W, b, x0):
         db = np.stack([out["db"][l] for l in range(n)])
         z = [out["states"][l][0] @ W[l].astype(np.float64).T + b[l] for l in range(n)]
         return {"loss": out["loss"], "dW": dW, "db": db, "dh0": out["dx0"][0], "z": z,
-                "ybar": _mlp_ybar(cell, n, out), "y": [out["states"][l][0] for l in range(n)]}
+                "ybar": _mlp_ybar(cell, n, out), "y": [out["states"][l][0] for l in range(n)],
+                "wrow": [np.max(np.abs(W[l].astype(np.float64)), axis=1) for l in range(n)]}
     cell = bptt.cell_for(wl, (W.astype(np.float64), b.astype(np.float64)))
     xs = x.astype(np.float64)
     st = (x0["h"].astype(np.float64),) + ((x0["c"].astype(np.float64),) if "c" in x0 else ())
@@ -147,9 +172,26 @@ def assert_close_relu(got: dict, want: dict, tol: float, band: float = 3e-4, max
     by at most the sum of its ambiguous terms (|ybar[m][k]| for db,
     |ybar[m][k]| |y_l[m][c]| for dW) plus the tolerance.
     """
-    assert_close(got, want, tol, keys=("loss", "dh0"))
+    assert_close(got, want, tol, keys=("loss",))
     dW, db = np.asarray(got["dW"], np.float64), np.asarray(got["db"], np.float64)
     n = dW.shape[0]
+    # dL/dy_0: the adjoint never mixes batch rows, so a mask decided the other
+    # way at (l, m, k) moves row m only, by about |ybar_{l+1}[m][k]| times row
+    # k of W_l (allowed 10 times over for its way down through the layers
+    # below); rows without such a decision must meet the tolerance
+    dh = np.asarray(got["dh0"], np.float64)
+    sh = np.max(np.abs(want["dh0"]))
+    bound = np.zeros(dh.shape[0])
+    for l in range(n):
+        z = want["z"][l]
+        amb = np.abs(z) < band * np.sqrt(np.mean(z * z))
+        bound += (np.where(amb, np.abs(want["ybar"][l]), 0.0) * want["wrow"][l][None, :]).sum(axis=1)
+    clean = bound == 0
+    err_rows = np.max(np.abs(dh - want["dh0"]), axis=1)
+    assert np.all(err_rows[clean] <= tol * sh), ("dh0", float(np.max(err_rows[clean]) / sh))
+    assert np.all(err_rows[~clean] <= 10 * bound[~clean] + tol * sh), ("dh0 beyond the flip bound", np.nonzero(~clean))
+    say(f"dh0: rows without an ambiguous mask {int(clean.sum())}/{clean.size} within {tol}; "
+        f"max error {float(np.max(err_rows) / sh):.2e}")
     amb_rows = 0
     sW, sb = np.max(np.abs(want["dW"])), np.max(np.abs(want["db"]))
     worst = 0.0
@@ -173,3 +215,30 @@ def assert_close_relu(got: dict, want: dict, tol: float, band: float = 3e-4, max
     frac = amb_rows / (n * dW.shape[1])
     say(f"relu-unambiguous rows: max error {worst:.2e}; ambiguous rows {amb_rows} ({frac:.2%}) within the flip bound")
     assert frac <= max_frac, frac
+
+
+def assert_close_mlp(got: dict, want: dict, wl, tol: float, band: float = 3e-4):
+    """The MLP of layers of different widths: loss and dL/dy_0 within the
+    tolerance, and per layer the weight- and bias-gradient rows whose unit
+    has no pre-activation within band * rms(z) of zero (the relu mask decided
+    alike on both sides); the other rows are reported and may be few."""
+    assert_close(got, want, tol, keys=("loss", "dh0"))
+    ws = wl.layer_widths()
+    dW, db = np.asarray(got["dW"], np.float64), np.asarray(got["db"], np.float64)
+    o = ob = 0
+    sW = max(np.max(np.abs(x)) for x in want["dW_layers"])
+    sb = max(np.max(np.abs(x)) for x in want["db_layers"])
+    amb_rows = 0
+    for l in range(wl.n_steps):
+        m, k = ws[l + 1], ws[l]
+        gW = dW[o:o + m * k].reshape(m, k)
+        gb = db[ob:ob + m]
+        o += m * k
+        ob += m
+        z = want["z"][l]
+        ok = ~np.any(np.abs(z) < band * np.sqrt(np.mean(z * z)), axis=0)
+        amb_rows += int((~ok).sum())
+        assert np.max(np.abs(gW[ok] - want["dW_layers"][l][ok]), initial=0.0) <= tol * sW, ("dW", l)
+        assert np.max(np.abs(gb[ok] - want["db_layers"][l][ok]), initial=0.0) <= tol * sb, ("db", l)
+    assert amb_rows <= 0.05 * sum(ws[1:]), amb_rows
+    say(f"mlp: every layer's unambiguous rows within {tol}; ambiguous rows {amb_rows}")

@@ -1,0 +1,86 @@
+"""States of different sizes on the GPU: the MLP whose layers change width
+(1, 1/2 and 1/4 of the largest state), its snapshots stacked in the
+byte-addressed HBM pool.  The executed schedules are the oracle's sized
+schedules text for text (one level, two levels with a fixed interval, stores
+decided during the sweep), their gradients equal store-all's bit for bit and
+the oracle's within the fp32 tolerance, and the byte budget buys fewer
+recomputations than slots of the largest size would."""
+import math
+
+import pytest
+
+import synth
+from oracle import schedule as S
+
+from gpu_util import TOL_F32, assert_bitwise, assert_close_mlp, device_inputs, inputs, run_gpu, run_oracle, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _sizes(wl):
+    """State sizes in units of their greatest common divisor, as the library
+    computes them (B w_t fp32 values rounded up to 256 bytes)."""
+    b = [-(-wl.batch * w * 4 // 256) * 256 for w in wl.layer_widths()]
+    g = 0
+    for v in b:
+        g = math.gcd(g, v)
+    return [v // g for v in b]
+
+
+def _case(wl):
+    host = inputs(wl)
+    return host, device_inputs(wl, *host)
+
+
+@pytest.mark.parametrize("shape", [dict(batch=64, hidden=256, widths=(256, 128, 64, 128)),
+                                   dict(batch=50, hidden=64, widths=(64, 16, 48, 32))],
+                         ids=["pooled", "ragged"])
+def test_mlp_of_different_widths(shape):
+    wl = synth.get("mlp_widths_l2000").with_(n_steps=24, **shape)
+    n, sizes = wl.n_steps, _sizes(wl)
+    host, dev = _case(wl)
+    want = run_oracle(wl, *host)
+    ref = run_gpu(wl, dev, fast_slots=n + 1, slow_slots=0)          # every state fits: no recomputation
+    assert ref["stats"]["forward_evals"] == n
+    assert_close_mlp(ref, want, wl, TOL_F32)
+    for kw in (dict(fast_slots=2, slow_slots=0), dict(fast_slots=3, slow_slots=0),
+               dict(fast_slots=3, slow_slots=n, interval_min=3), dict(fast_slots=2, slow_slots=n, interval_min=4)):
+        got = run_gpu(wl, dev, **kw)
+        text = S.text_sized(n, kw["fast_slots"], sizes, kw["slow_slots"], kw.get("interval_min", 0))
+        assert got["schedule_text"] == text, kw
+        head, _ = S.schedule_sized(n, kw["fast_slots"], sizes, kw["slow_slots"], kw.get("interval_min", 0))
+        uni, _ = S.schedule_sized(n, kw["fast_slots"], [max(sizes)] * (n + 1), kw["slow_slots"],
+                                  kw.get("interval_min", 0))
+        assert got["stats"]["forward_evals"] == head["evals"] <= uni["evals"], kw
+        say(kw, "evals", head["evals"], "with slots of the largest size", uni["evals"])
+        assert_bitwise(got, ref)
+    # stores decided during the sweep, every interval reversed by the sized recursion
+    dyn = run_gpu(wl, dev, fast_slots=3, slow_slots=n, interval_min=2, opts={"store_policy": 1})
+    h, acts = S.parse(dyn["schedule_text"])
+    assert h["mode"] == "dynamic" and h.get("split") == "size"
+    starts = [a[3] for a in acts if a[0] == "W"] + [a[2] for a in acts if a[0] == "S" and a[1] <= 1][-1:]
+    starts = sorted(set(starts))
+    assert dyn["schedule_text"] == S.text_sized_from_starts(n, 3, n, starts, sizes)
+    S.check_sized(n, 3, n, acts, sizes, True)
+    assert_bitwise(dyn, ref)
+
+
+def test_mlp_widths_refusals():
+    import paper_1806_01117_amd as amb
+    from paper_1806_01117_amd._lib import EINVAL, EUNSUPPORTED, AmbpttError
+    wl = synth.get("mlp_widths_l2000").with_(n_steps=6, batch=32, hidden=128, widths=(128, 64))
+    host, dev = _case(wl)
+    r = amb.Runner(amb.ProblemSpec.from_workload(wl, fast_slots=2, slow_slots=0))
+    try:
+        import ctypes as C
+        bad = (C.c_int32 * 7)(128, 64, 128, 64, 128, 64, 100)     # not a multiple of 16
+        with pytest.raises(AmbpttError) as e:
+            from paper_1806_01117_amd._lib import check
+            check(r.L.ambptt_set_widths(r.ctx, bad, 7))
+        assert e.value.status == EINVAL
+        r.set("online", 1)
+        with pytest.raises(AmbpttError) as e:
+            r.run(*dev)
+        assert e.value.status == EUNSUPPORTED
+    finally:
+        r.close()
