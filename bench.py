@@ -140,15 +140,15 @@ def estimate_pass_s(wl, spec, t_a_us: float, I_min: int) -> float:
 def lds_kernels(spec, knobs) -> tuple[bool, bool]:
     """Whether the fp32 large-batch path runs its gate products and its
     h-adjoint products on the LDS-tiled kernels (the library's "lds_gemm"
-    rule: shapes that fit their tiles and, by default, fill the device at
-    least half: 128 tiles of 128 x 256, or of 64 x 128)."""
+    rule: shapes that fit their tiles and, by default, give every CU two
+    workgroups: 256 tiles of 128 x 128, or of 64 x 64)."""
     G, B, D, H = spec.gates, spec.batch, spec.input, spec.hidden
     k = dict(knobs)
     mode = k.get("lds_gemm", 1)
-    cell_fit = D % 32 == 0 and H % 32 == 0 and (G * H) % 256 == 0
-    prod_fit = (G * H) % 64 == 0 and H % 128 == 0 and k.get("hadj_launch", 1) != 0
-    cell = mode > 0 and cell_fit and (mode == 2 or -(-B // 128) * (G * H // 256) >= 128)
-    prod = mode > 0 and prod_fit and (mode == 2 or -(-B // 64) * (H // 128) >= 128)
+    cell_fit = D % 4 == 0 and H % 4 == 0 and (G * H) % 128 == 0
+    prod_fit = (G * H) % 4 == 0 and H % 64 == 0 and k.get("hadj_launch", 1) != 0
+    cell = mode > 0 and cell_fit and (mode == 2 or -(-B // 128) * (G * H // 128) >= 256)
+    prod = mode > 0 and prod_fit and (mode == 2 or -(-B // 64) * (H // 64) >= 256)
     return cell, prod
 
 

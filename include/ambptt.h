@@ -331,9 +331,9 @@ ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
  * compute reading the slot before the prefetch has landed spoils the
  * gradients), "lds_gemm" (fp32 path for large batches: 1, default, runs the gate
  * product with its cell epilogue and the h-adjoint product on LDS-tiled
- * kernels (128 x 256 and 64 x 128 tiles) where their tiles fill the device
- * at least half; 2 wherever their shape constraints hold; 0 never: the
- * direct-load kernels), "hadj_launch" (1,
+ * kernels (128 x 128 and 64 x 64 tiles, two workgroups per CU) where they
+ * have at least 256 tiles; 2 wherever their shape constraints hold; 0 never:
+ * the direct-load kernels), "hadj_launch" (1,
  * default: on the fp32 path for large batches the adjoint's h-adjoint
  * product zbar_{t+1} W_h runs as a launch of its own, kernel class
  * AMBPTT_K_HADJ; 0: fused into the adjoint step's launch), "reserve" (1: allocate now the pinned host

@@ -7,13 +7,14 @@
 // index k:
 //   gate product  z[m][n] = sum_k [x | h][m][k] W[n][k]       (K = D + H)
 //   h-adjoint     hbar[m][j] = sum_k zbar[m][k] WhT[j][k]     (K = G H)
-// A workgroup of 8 (gate product) or 4 waves (h-adjoint product) owns one
-// output tile.  The tile's operands pass through LDS in stages of kKT
-// reduction indices, double-buffered: while the waves multiply stage s, the
-// loads of stage s + 1 are in flight in registers, and they are written to
-// the other LDS buffer before the one barrier of the stage.  LDS rows are padded by 4 floats, so that the 16
-// rows one MFMA operand read touches (16 bytes each, at one column) fall on
-// distinct banks.
+// A workgroup of 4 waves owns one output tile, and two workgroups share a
+// CU (each holds one LDS buffer of 64-wide stages, under 80 KB), so that
+// while one workgroup waits at a barrier or on LDS the other keeps the
+// matrix cores busy.  A stage is loaded into registers while the previous
+// one is multiplied, written to LDS between the stage's two barriers, and
+// multiplied from there.  Reduction indices past K read as zero.  LDS rows
+// are padded by 4 floats, so that the 16 rows one MFMA operand read touches
+// (16 bytes each, at one column) fall on distinct banks.
 //
 // Fragments: lane l reads 4 consecutive k of row l & 15 at column 4 (l >> 4)
 // of a 16-wide chunk, and its 4 components feed 4 MFMAs; A and B use the
@@ -59,22 +60,21 @@ __device__ __forceinline__ void tile_of(int i, int mt, int nt, int* tm, int* tn)
 }
 
 // ---- gate product with the cell epilogue ------------------------------------
-// Tile: 128 batch rows x 256 gate columns (LSTM: 64 units x 4 gates; RNN:
-// 256 units), 8 waves.  Wave (wm, wn), wm < 2, wn < 4, computes rows
+// Tile: 128 batch rows x 128 gate columns (LSTM: 32 units x 4 gates; RNN:
+// 128 units), 4 waves.  Wave (wm, wn), wm, wn < 2, computes rows
 // 64 wm .. + 63 and, for the LSTM, units 16 wn .. + 15 of all four gates
 // (block g of its 4 x 4 blocks of 16 x 16 is gate g), so a lane holds the
 // four gates of its (row, unit) pairs in the same accumulator element; for
-// the RNN units 64 wn .. + 63.  Two waves per SIMD: one multiplies while the
-// other waits on LDS.
-constexpr int kCM = 128, kCN = 256, kKT = 32, kLd = kKT + 4, kCW = 8;
+// the RNN units 64 wn .. + 63.
+constexpr int kCM = 128, kCN = 128, kKT = 64, kLd = kKT + 4, kCW = 4;
 
 template <int G, int MODE>
-__global__ __launch_bounds__(64 * kCW, 1) void cell_gemm_f32(StepArgs a) {
-  __shared__ float As[2][kCM][kLd];
-  __shared__ float Bs[2][kCN][kLd];
+__global__ __launch_bounds__(64 * kCW, 2) void cell_gemm_f32(StepArgs a) {
+  __shared__ float As[kCM][kLd];
+  __shared__ float Bs[kCN][kLd];
   __shared__ float red[kCW];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave >> 1, wn = wave & 1;
   const int r = lane & 15, q = lane >> 4;
   const int B = a.B, D = a.D, H = a.H, K1 = D + H;
   const int mt = (B + kCM - 1) / kCM, nt = G * H / kCN;
@@ -83,36 +83,46 @@ __global__ __launch_bounds__(64 * kCW, 1) void cell_gemm_f32(StepArgs a) {
   const int m0 = tm * kCM;
   const int j0 = tn * (kCN / G);  // first unit of the tile
 
-  // loader: thread t moves rows t / 8 + 64 p, float4 column t % 8 of a stage
-  const int lr = tid >> 3, lc = 4 * (tid & 7);
+  // loader: thread t moves rows t / 16 + 16 p, float4 column t % 16 of a
+  // stage; a float4 lies wholly in x or in h (D, H multiples of 4)
+  const int lr = tid >> 4, lc = 4 * (tid & 15);
   const float* x = (const float*)a.x;
   const float* h = (const float*)a.h;
   const float* W = (const float*)a.W;
-  int arow[2];
+  int arow[8];
 #pragma unroll
-  for (int p = 0; p < 2; ++p) arow[p] = min(m0 + lr + 64 * p, B - 1);  // rows >= B: clamped, discarded
-  const float* brow[4];
+  for (int p = 0; p < 8; ++p) arow[p] = min(m0 + lr + 16 * p, B - 1);  // rows >= B: clamped, discarded
+  const float* brow[8];
 #pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const int c = lr + 64 * p;
-    const int n = G == 4 ? (c >> 6) * H + j0 + (c & 63) : j0 + c;
-    brow[p] = W + (size_t)n * K1 + lc;
+  for (int p = 0; p < 8; ++p) {
+    const int c = lr + 16 * p;
+    const int n = G == 4 ? (c >> 5) * H + j0 + (c & 31) : j0 + c;
+    brow[p] = W + (size_t)n * K1;
   }
-  f4 ra[2], rb[4];
+  // Every load is unconditional (a lane past K reads column 0 of its row),
+  // so that no branch splits the stage's loads; past K the values are
+  // replaced by zero when they are written to LDS.
+  f4 ra[8], rb[8];
+  bool kin = true;
   auto load = [&](int st) {
-    const int k0 = st * kKT;
+    const int k = st * kKT + lc;
+    kin = k < K1;
+    const int kc = kin ? k : 0;
+    const bool inx = kc < D;
 #pragma unroll
-    for (int p = 0; p < 2; ++p)
-      ra[p] = k0 < D ? *(const f4*)(x + (size_t)arow[p] * D + k0 + lc)
-                     : *(const f4*)(h + (size_t)arow[p] * H + (k0 - D) + lc);
+    for (int p = 0; p < 8; ++p) {
+      const float* src = inx ? x + (size_t)arow[p] * D + kc : h + (size_t)arow[p] * H + (kc - D);
+      ra[p] = *(const f4*)src;
+    }
 #pragma unroll
-    for (int p = 0; p < 4; ++p) rb[p] = *(const f4*)(brow[p] + k0);
+    for (int p = 0; p < 8; ++p) rb[p] = *(const f4*)(brow[p] + kc);
   };
-  auto store = [&](int buf) {
+  auto store = [&]() {
+    const f4 zero = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int p = 0; p < 2; ++p) *(f4*)&As[buf][lr + 64 * p][lc] = ra[p];
+    for (int p = 0; p < 8; ++p) *(f4*)&As[lr + 16 * p][lc] = kin ? ra[p] : zero;
 #pragma unroll
-    for (int p = 0; p < 4; ++p) *(f4*)&Bs[buf][lr + 64 * p][lc] = rb[p];
+    for (int p = 0; p < 8; ++p) *(f4*)&Bs[lr + 16 * p][lc] = kin ? rb[p] : zero;
   };
 
   f4 acc[4][4];
@@ -123,16 +133,16 @@ __global__ __launch_bounds__(64 * kCW, 1) void cell_gemm_f32(StepArgs a) {
   // LDS row of B block nb of this wave
   int bcol[4];
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb) bcol[nb] = G == 4 ? nb * 64 + wn * 16 : wn * 64 + 16 * nb;
+  for (int nb = 0; nb < 4; ++nb) bcol[nb] = G == 4 ? nb * 32 + wn * 16 : wn * 64 + 16 * nb;
 
-  auto compute = [&](int buf) {
+  auto compute = [&]() {
 #pragma unroll
     for (int kk = 0; kk < kKT / 16; ++kk) {
       f4 af[4], bf[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) af[i] = *(const f4*)&As[buf][wm * 64 + 16 * i + r][16 * kk + 4 * q];
+      for (int i = 0; i < 4; ++i) af[i] = *(const f4*)&As[wm * 64 + 16 * i + r][16 * kk + 4 * q];
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) bf[nb] = *(const f4*)&Bs[buf][bcol[nb] + r][16 * kk + 4 * q];
+      for (int nb = 0; nb < 4; ++nb) bf[nb] = *(const f4*)&Bs[bcol[nb] + r][16 * kk + 4 * q];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -145,21 +155,20 @@ __global__ __launch_bounds__(64 * kCW, 1) void cell_gemm_f32(StepArgs a) {
     }
   };
   // The next stage's global loads are issued before the multiplications
-  // start (the scheduling barrier keeps the compiler from sinking them below
-  // the MFMAs, where their latency would stall the stage's LDS writes).
-  const int nst = K1 / kKT;
+  // start (the scheduling barriers keep the compiler from sinking them below
+  // the MFMAs); the first barrier of a stage waits for every wave to finish
+  // reading the previous one.
+  const int nst = (K1 + kKT - 1) / kKT;
   load(0);
-  store(0);
-  __syncthreads();
-  for (int st = 0; st + 1 < nst; ++st) {
-    load(st + 1);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(st & 1);
-    __builtin_amdgcn_sched_barrier(0);
-    store((st + 1) & 1);
+  for (int st = 0; st < nst; ++st) {
+    if (st) __syncthreads();
+    store();
+    if (st + 1 < nst) load(st + 1);
     __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    compute();
+    __builtin_amdgcn_sched_barrier(0);
   }
-  compute((nst - 1) & 1);
 
   // ---- epilogue: accumulator element v of lane l is row 4 (l >> 4) + v,
   //      column l & 15 of its 16 x 16 block ------------------------------------
@@ -237,13 +246,15 @@ __global__ __launch_bounds__(64 * kCW, 1) void cell_gemm_f32(StepArgs a) {
 }
 
 // ---- h-adjoint product: out = A B^T (+ add) -----------------------------------
-// Tile: 64 rows x 128 columns; wave (wm, wn) computes rows 32 wm .. + 31 and
-// columns 64 wn .. + 63 (2 x 4 blocks); stages of kPT = 64 reduction indices.
-constexpr int kPM = 64, kPN = 128, kPT = 64, kPLd = kPT + 4;
+// Tile: 64 rows x 64 columns; wave (wm, wn) computes rows 32 wm .. + 31 and
+// columns 32 wn .. + 31 (2 x 2 blocks); stages of kPT = 64 reduction indices.
+// The 4 MFMAs of one k-component run over all 4 blocks before the next
+// component, so consecutive MFMAs never share an accumulator.
+constexpr int kPM = 64, kPN = 64, kPT = 64, kPLd = kPT + 4;
 
-__global__ __launch_bounds__(256, 1) void prod_gemm_f32(ProdArgs a) {
-  __shared__ float As[2][kPM][kPLd];
-  __shared__ float Bs[2][kPN][kPLd];
+__global__ __launch_bounds__(256, 2) void prod_gemm_f32(ProdArgs a) {
+  __shared__ float As[kPM][kPLd];
+  __shared__ float Bs[kPN][kPLd];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int r = lane & 15, q = lane >> 4;
@@ -255,67 +266,64 @@ __global__ __launch_bounds__(256, 1) void prod_gemm_f32(ProdArgs a) {
 
   // loader: thread t moves rows t / 16 + 16 p, float4 column t % 16 of a stage
   const int lr = tid >> 4, lc = 4 * (tid & 15);
-  const float* A = (const float*)a.A;
-  const float* Bm = (const float*)a.B;
   const float* arow[4];
+  const float* brow[4];
 #pragma unroll
-  for (int p = 0; p < 4; ++p) arow[p] = A + (size_t)min(m0 + lr + 16 * p, M - 1) * K + lc;
-  const float* brow[8];
+  for (int p = 0; p < 4; ++p) {
+    arow[p] = (const float*)a.A + (size_t)min(m0 + lr + 16 * p, M - 1) * K;  // rows >= M: clamped, discarded
+    brow[p] = (const float*)a.B + (size_t)(n0 + lr + 16 * p) * K;
+  }
+  f4 ra[4], rb[4];
+  bool kin = true;
+  auto load = [&](int st) {  // unconditional loads, as in the gate product
+    const int k = st * kPT + lc;
+    kin = k < K;
+    const int kc = kin ? k : 0;
 #pragma unroll
-  for (int p = 0; p < 8; ++p) brow[p] = Bm + (size_t)(n0 + lr + 16 * p) * K + lc;
-  f4 ra[4], rb[8];
-  auto load = [&](int st) {
-    const int k0 = st * kPT;
+    for (int p = 0; p < 4; ++p) ra[p] = *(const f4*)(arow[p] + kc);
 #pragma unroll
-    for (int p = 0; p < 4; ++p) ra[p] = *(const f4*)(arow[p] + k0);
-#pragma unroll
-    for (int p = 0; p < 8; ++p) rb[p] = *(const f4*)(brow[p] + k0);
+    for (int p = 0; p < 4; ++p) rb[p] = *(const f4*)(brow[p] + kc);
   };
-  auto store = [&](int buf) {
+  auto store = [&]() {
+    const f4 zero = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int p = 0; p < 4; ++p) *(f4*)&As[buf][lr + 16 * p][lc] = ra[p];
+    for (int p = 0; p < 4; ++p) *(f4*)&As[lr + 16 * p][lc] = kin ? ra[p] : zero;
 #pragma unroll
-    for (int p = 0; p < 8; ++p) *(f4*)&Bs[buf][lr + 16 * p][lc] = rb[p];
+    for (int p = 0; p < 4; ++p) *(f4*)&Bs[lr + 16 * p][lc] = kin ? rb[p] : zero;
   };
 
-  f4 acc[2][4];
+  f4 acc[2][2];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb) acc[i][nb] = f4{0.f, 0.f, 0.f, 0.f};
-
-  auto compute = [&](int buf) {
+    for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&]() {
 #pragma unroll
     for (int kk = 0; kk < kPT / 16; ++kk) {
-      f4 af[2], bf[4];
+      f4 af[2], bf[2];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) af[i] = *(const f4*)&As[buf][wm * 32 + 16 * i + r][16 * kk + 4 * q];
+      for (int i = 0; i < 2; ++i) af[i] = *(const f4*)&As[wm * 32 + 16 * i + r][16 * kk + 4 * q];
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) bf[nb] = *(const f4*)&Bs[buf][wn * 64 + 16 * nb + r][16 * kk + 4 * q];
+      for (int j = 0; j < 2; ++j) bf[j] = *(const f4*)&Bs[wn * 32 + 16 * j + r][16 * kk + 4 * q];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int c = 0; c < 4; ++c)
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb) {
-          acc[i][nb] = mfma4(af[i].x, bf[nb].x, acc[i][nb]);
-          acc[i][nb] = mfma4(af[i].y, bf[nb].y, acc[i][nb]);
-          acc[i][nb] = mfma4(af[i].z, bf[nb].z, acc[i][nb]);
-          acc[i][nb] = mfma4(af[i].w, bf[nb].w, acc[i][nb]);
-        }
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) acc[i][j] = mfma4(af[i][c], bf[j][c], acc[i][j]);
     }
   };
-  const int nst = K / kPT;
+  const int nst = (K + kPT - 1) / kPT;
   load(0);
-  store(0);
-  __syncthreads();
-  for (int st = 0; st + 1 < nst; ++st) {
-    load(st + 1);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(st & 1);
-    __builtin_amdgcn_sched_barrier(0);
-    store((st + 1) & 1);
+  for (int st = 0; st < nst; ++st) {
+    if (st) __syncthreads();
+    store();
+    if (st + 1 < nst) load(st + 1);
     __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    compute();
+    __builtin_amdgcn_sched_barrier(0);
   }
-  compute((nst - 1) & 1);
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -323,9 +331,9 @@ __global__ __launch_bounds__(256, 1) void prod_gemm_f32(ProdArgs a) {
       const int m = m0 + wm * 32 + 16 * i + 4 * q + v;
       if (m >= M) continue;
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        const size_t o = (size_t)m * N + n0 + wn * 64 + 16 * nb + r;
-        a.out[o] = a.add ? a.add[o] + acc[i][nb][v] : acc[i][nb][v];
+      for (int j = 0; j < 2; ++j) {
+        const size_t o = (size_t)m * N + n0 + wn * 32 + 16 * j + r;
+        a.out[o] = a.add ? a.add[o] + acc[i][j][v] : acc[i][j][v];
       }
     }
 }
@@ -333,7 +341,7 @@ __global__ __launch_bounds__(256, 1) void prod_gemm_f32(ProdArgs a) {
 }  // namespace
 
 bool cell_gemm_f32_fits(int G, int B, int D, int H) {
-  return (G == 1 || G == 4) && B >= 1 && D % kKT == 0 && H % kKT == 0 && H >= kKT && (G * H) % kCN == 0;
+  return (G == 1 || G == 4) && B >= 1 && D >= 0 && D % 4 == 0 && H >= 1 && H % 4 == 0 && (G * H) % kCN == 0;
 }
 
 int cell_gemm_f32_tiles(int G, int B, int H) { return ((B + kCM - 1) / kCM) * (G * H / kCN); }
@@ -353,7 +361,7 @@ hipError_t launch_cell_gemm_f32(int G, int mode, const StepArgs& a, hipStream_t 
   return hipGetLastError();
 }
 
-bool prod_gemm_f32_fits(int M, int N, int K) { return M >= 1 && K >= kPT && K % kPT == 0 && N % kPN == 0; }
+bool prod_gemm_f32_fits(int M, int N, int K) { return M >= 1 && K >= 4 && K % 4 == 0 && N >= kPN && N % kPN == 0; }
 
 int prod_gemm_f32_tiles(int M, int N) { return ((M + kPM - 1) / kPM) * (N / kPN); }
 

@@ -279,7 +279,7 @@ struct ambptt_ctx {
   int64_t cost_plan_key[3] = {-1, -1, -1};  // interval_min, slow capacity, costs version
   int64_t costs_version = 0;
   bool hadj_launch = true;  // fp32 large-batch path: the adjoint's h-adjoint product as a launch of its own
-  int lds_gemm = 1;         // fp32 large-batch path: LDS-tiled kernels (0 off, 1 when they fill the device, 2 always)
+  int lds_gemm = 1;         // fp32 large-batch path: LDS-tiled kernels (0 off, 1 when they fill the device twice over, 2 always)
   // tests of the stream ordering: a host-side delay before every host-tier
   // copy and weight-gradient window on their streams, and NaN bytes written
   // into a fast slot before a prefetch refills it
@@ -522,10 +522,11 @@ struct Exec {
     sep32 = L.hsep && C->hadj_launch;
     if (L.hsep) {
       const int G = L.G, B = p.batch, D = p.input, H = p.hidden;
+      // by default only shapes that give every CU its two workgroups
       lds_cell = C->lds_gemm > 0 && cell_gemm_f32_fits(G, B, D, H) &&
-                 (C->lds_gemm == 2 || cell_gemm_f32_tiles(G, B, H) >= 128);
+                 (C->lds_gemm == 2 || cell_gemm_f32_tiles(G, B, H) >= 256);
       lds_prod = sep32 && C->lds_gemm > 0 && prod_gemm_f32_fits(B, H, G * H) &&
-                 (C->lds_gemm == 2 || prod_gemm_f32_tiles(B, H) >= 128);
+                 (C->lds_gemm == 2 || prod_gemm_f32_tiles(B, H) >= 256);
     }
     if (wide || sep32 || L.mlpv) hbuf = (float*)(C->ws + L.off_hbar);
   }
