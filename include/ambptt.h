@@ -173,6 +173,17 @@ ambptt_status ambptt_schedule_text(int64_t n, int32_t s, int64_t H, int32_t inte
 ambptt_status ambptt_schedule_text_starts(int64_t n, int32_t s, int64_t H, const int64_t* starts,
                                           int64_t nstarts, char* buf, size_t cap, size_t* needed);
 
+/* The schedule of ambptt_schedule_text_starts with every reversal split for
+ * the step costs costs[0..n) (see ambptt_set_step_costs): what a pass runs
+ * with store_policy 1 and step costs (Section 6's stores decided during the
+ * sweep, with the dynamic program inside each interval).  The header ends
+ * with " split=cost".  Buffer rules as in ambptt_schedule_text; EINVAL on bad
+ * starts or costs, EUNSUPPORTED when a reversal's table would exceed 1 Mi
+ * entries. */
+ambptt_status ambptt_schedule_text_starts_costs(int64_t n, int32_t s, int64_t H, const int64_t* starts,
+                                                int64_t nstarts, const double* costs, char* buf, size_t cap,
+                                                size_t* needed);
+
 /* Canonical text of the schedule of ambptt_schedule_text with every
  * reversal split for the step costs costs[0..n) (see ambptt_set_step_costs);
  * the header ends with " split=cost".  Buffer rules as in

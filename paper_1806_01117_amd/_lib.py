@@ -13,7 +13,7 @@ DTYPE = {"f32": 0, "bf16": 1}
 LOSS = {"half_sq_last": 0, "mean_sq_all": 1, "mean_last": 2}
 
 EXPORTS = ["ambptt_version", "ambptt_revolve_advances", "ambptt_schedule_evals", "ambptt_schedule_text",
-           "ambptt_schedule_text_starts", "ambptt_schedule_text_online", "ambptt_schedule_text_costs", "ambptt_schedule_text_sized",
+           "ambptt_schedule_text_starts", "ambptt_schedule_text_starts_costs", "ambptt_schedule_text_online", "ambptt_schedule_text_costs", "ambptt_schedule_text_sized",
            "ambptt_interval_from_timings", "ambptt_set_step_costs", "ambptt_set_widths",
            "ambptt_resident_program", "ambptt_query", "ambptt_last_error",
            "ambptt_create", "ambptt_bind", "ambptt_set_int", "ambptt_set_file_tier", "ambptt_calibrate", "ambptt_run", "ambptt_run_noalloc",
@@ -78,6 +78,9 @@ def load():
     L.ambptt_schedule_text.restype = C.c_int
     L.ambptt_schedule_text_starts.argtypes = [i64, i32, i64, C.POINTER(i64), i64, C.c_char_p, sz, C.POINTER(sz)]
     L.ambptt_schedule_text_starts.restype = C.c_int
+    L.ambptt_schedule_text_starts_costs.argtypes = [i64, i32, i64, C.POINTER(i64), i64, C.POINTER(C.c_double), C.c_char_p,
+                                                    sz, C.POINTER(sz)]
+    L.ambptt_schedule_text_starts_costs.restype = C.c_int
     L.ambptt_schedule_text_online.argtypes = [i64, i32, i64, i32, C.c_char_p, sz, C.POINTER(sz)]
     L.ambptt_schedule_text_online.restype = C.c_int
     L.ambptt_interval_from_timings.argtypes = [C.c_double, C.c_double, i32, i32]

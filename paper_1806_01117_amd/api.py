@@ -56,12 +56,19 @@ def _text(call) -> str:
     return buf.value.decode()
 
 
-def schedule_text_starts(n: int, s: int, H: int, starts) -> str:
+def schedule_text_starts(n: int, s: int, H: int, starts, costs=None) -> str:
     """Canonical text of the two-level schedule over interval starts chosen
-    during the sweep (ambptt_schedule_text_starts)."""
+    during the sweep (ambptt_schedule_text_starts), with every reversal split
+    for the step costs when they are given (ambptt_schedule_text_starts_costs)."""
     L = load()
     arr = (C.c_int64 * len(starts))(*[int(t) for t in starts])
-    return _text(lambda buf, cap, need: L.ambptt_schedule_text_starts(n, s, H, arr, len(starts), buf, cap, need))
+    if costs is None:
+        return _text(lambda buf, cap, need: L.ambptt_schedule_text_starts(n, s, H, arr, len(starts), buf, cap, need))
+    if len(costs) != n:
+        raise ValueError("need one cost per step")
+    cv = (C.c_double * n)(*[float(c) for c in costs])
+    return _text(lambda buf, cap, need: L.ambptt_schedule_text_starts_costs(n, s, H, arr, len(starts), cv, buf, cap,
+                                                                           need))
 
 
 def interval_from_timings(t_a_us: float, t_t_us: float, s: int, rule: int = 1) -> int:

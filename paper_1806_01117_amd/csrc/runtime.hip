@@ -340,6 +340,14 @@ Plan pass_plan(ambptt_ctx* C) {
                            C->step_costs.empty() ? nullptr : &C->step_costs, &C->plan_cost);
   }
   if (C->online) return make_plan_online(p.n_steps, p.fast_slots, p.slow_slots, I);
+  if (!C->step_costs.empty() && C->store_policy == 1 && C->path_opt != 2) {
+    // stores decided during the sweep: the reverse is built from the chosen
+    // starts, so the fixed intervals' cost splits are not needed; the uniform
+    // plan, whose mode the cost splits keep, decides whether the host tier is
+    // used (if not, plain Revolve with the cost splits runs)
+    Plan u = make_plan(p.n_steps, p.fast_slots, slow_capacity(C), I);
+    if (u.async) return u;
+  }
   if (!C->step_costs.empty()) {  // the dynamic program runs once per set of inputs
     const int64_t key[3] = {I, slow_capacity(C), C->costs_version};
     if (!std::equal(key, key + 3, C->cost_plan_key)) {
@@ -1893,6 +1901,12 @@ static ambptt_status run_pass(ambptt_ctx* C, const void* x_seq, const void* W, c
                                              &C->plan_cost)
                     : make_plan_starts(p.n_steps, p.fast_slots, slow_capacity(C), starts, costs, &C->plan_cost);
     } catch (const std::exception& e) {
+      // the sweep is enqueued: let it and its stores finish before reporting
+      (void)hipStreamSynchronize(C->cs);
+      (void)hipStreamSynchronize(C->xs);
+      (void)hipStreamSynchronize(C->ds);
+      if (C->ftier) (void)C->ftier->finish();
+      if (dynamic_cast<const std::length_error*>(&e)) return fail(AMBPTT_EUNSUPPORTED, e.what());
       return fail(AMBPTT_EINTERNAL, e.what());
     }
     if ((s = E.grow_slots(plan.slot_ids)) != AMBPTT_OK) return s;
@@ -2033,6 +2047,28 @@ ambptt_status ambptt_schedule_text_starts(int64_t n, int32_t s, int64_t H, const
     if (!buf || cap < t.size() + 1) return fail(AMBPTT_EINVAL, "schedule: buffer too small");
     std::memcpy(buf, t.c_str(), t.size() + 1);
     return AMBPTT_OK;
+  } catch (const std::invalid_argument& e) {
+    return fail(AMBPTT_EINVAL, e.what());
+  } catch (const std::exception& e) {
+    return fail(AMBPTT_EINTERNAL, e.what());
+  }
+}
+
+ambptt_status ambptt_schedule_text_starts_costs(int64_t n, int32_t s, int64_t H, const int64_t* starts,
+                                                int64_t nstarts, const double* costs, char* buf, size_t cap,
+                                                size_t* needed) {
+  if (!starts || nstarts < 1) return fail(AMBPTT_EINVAL, "schedule: no interval starts");
+  if (!costs || n < 1) return fail(AMBPTT_EINVAL, "schedule: need one cost per step");
+  try {
+    const std::vector<double> cv(costs, costs + n);
+    const std::string t =
+        plan_text(make_plan_starts(n, s, H, std::vector<int64_t>(starts, starts + nstarts), &cv, nullptr));
+    if (needed) *needed = t.size() + 1;
+    if (!buf || cap < t.size() + 1) return fail(AMBPTT_EINVAL, "schedule: buffer too small");
+    std::memcpy(buf, t.c_str(), t.size() + 1);
+    return AMBPTT_OK;
+  } catch (const std::length_error& e) {
+    return fail(AMBPTT_EUNSUPPORTED, e.what());
   } catch (const std::invalid_argument& e) {
     return fail(AMBPTT_EINVAL, e.what());
   } catch (const std::exception& e) {

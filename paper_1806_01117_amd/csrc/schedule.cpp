@@ -247,6 +247,9 @@ Plan make_plan_starts(int64_t n, int32_t s, int64_t H, const std::vector<int64_t
   for (size_t k = 1; k < starts.size(); ++k)
     if (starts[k] <= starts[k - 1]) throw std::invalid_argument("schedule: interval starts must increase");
   if (costs && int64_t(costs->size()) != n) throw std::invalid_argument("schedule: need one cost per step");
+  if (costs)
+    for (double c : *costs)
+      if (!(c > 0.0) || !(c < 1e300)) throw std::invalid_argument("schedule: step costs must be positive and finite");
   Plan p;
   p.n = n;
   p.s = s;

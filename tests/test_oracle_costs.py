@@ -176,3 +176,29 @@ def test_costs_over_chosen_starts():
         assert head["cost"] <= _weighted(racts, costs)
         eq = S.text_from_starts(n, s, n, starts, [1.0] * n)
         assert _actions(eq) == _actions(S.text_from_starts(n, s, n, starts))
+
+
+def test_c_abi_costs_over_chosen_starts_bytewise():
+    """The library's schedule for stores decided during the sweep with step
+    costs (ambptt_schedule_text_starts_costs) against the oracle, byte for
+    byte, and its error codes."""
+    rng = random.Random(12)
+    for trial in range(150):
+        n = rng.randint(2, 60)
+        s = rng.randint(2, 6)
+        H = rng.choice([n, n + 3, 8])
+        k = rng.randint(0, min(n - 1, H, 8))
+        starts = [0] + sorted(rng.sample(range(1, n), k))
+        costs = [rng.choice([0.5, 1.0, 3.0]) for _ in range(n)]
+        assert amb.schedule_text_starts(n, s, H, starts, costs) == S.text_from_starts(n, s, H, starts, costs), \
+            (n, s, H, starts)
+    from paper_1806_01117_amd._lib import EINVAL, EUNSUPPORTED
+    # an interval of 1499 steps reversed on 2 slots: 1499 * 1500 * 3 entries exceed the table limit
+    with pytest.raises(amb.AmbpttError) as e:
+        amb.schedule_text_starts(1500, 3, 10, [0, 1], [1.0] * 1500)
+    assert e.value.status == EUNSUPPORTED
+    with pytest.raises(amb.AmbpttError) as e:
+        amb.schedule_text_starts(10, 3, 10, [0, 4], [1.0] * 9 + [0.0])
+    assert e.value.status == EINVAL
+    with pytest.raises(ValueError):
+        amb.schedule_text_starts(10, 3, 10, [0, 4], [1.0] * 9)
