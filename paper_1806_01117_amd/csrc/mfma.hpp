@@ -12,15 +12,19 @@ __device__ __forceinline__ f4 mfma_f32_16x16x4(float a, float b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
-// v_mfma_f32_16x16x32_bf16 followed by four explicit wait states.  With the
-// ROCm 7.2 compiler, a vector instruction that overwrote one of this MFMA's
-// A/B source registers right after it was issued corrupted the product (the
-// bf16 step kernels disagreed with the float64 reference by ~25% until the
-// pad was added; the pad after the last MFMA alone did not help, so the
-// hazard is on the sources).  The pad costs ~4 cycles per 16x16x32 MFMA.
+// v_mfma_f32_16x16x32_bf16 followed by an empty asm statement with a memory
+// clobber, which keeps LDS and global accesses from moving across it.  With
+// nothing after the MFMA, the ROCm 7.2 build of the small-batch bf16 step
+// kernel gives wrong results (loss off by 180 %); with this statement, or
+// with an `s_nop 3` without the clobber, every bf16 kernel is bit-exact
+// across schedules and within tolerance of the float64 oracle.  In the ISA of
+// the failing build the only pattern its passing builds lack is a VALU write
+// of the MFMA's B register in the very next cycle, but the weight-gradient
+// kernel holds such writes in every build and is correct, so the mechanism
+// is not established; the GPU tests of every bf16 kernel are the check.
 __device__ __forceinline__ f4 mfma_bf16_16x16x32(const bf16x8& a, const bf16x8& b, f4 c) {
   c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-  asm volatile("s_nop 3" ::: "memory");
+  asm volatile("" ::: "memory");
   return c;
 }
 
