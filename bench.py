@@ -111,6 +111,31 @@ def release_pinned() -> None:
         fn()
 
 
+def mlp_layer_work(ws, B: int) -> tuple[dict, dict]:
+    """Algorithmic flops and HBM bytes of one launch of each kernel class of
+    the MLP of layers of different widths, averaged over its layers (fp32):
+    forward y_{l+1} = relu(y_l W_l^T + b_l); adjoint z-bar_l from the
+    recomputed z_l, the NN product's sum and the seed; the NN product
+    z-bar_{l+1} W_{l+1}; the weight gradient of one layer."""
+    n = len(ws) - 1
+    f = {"fwd": 0.0, "adj": 0.0, "hadj": 0.0, "dw": 0.0}
+    b = dict(f)
+    for l in range(n):
+        a, c = ws[l], ws[l + 1]
+        f["fwd"] += 2.0 * B * a * c
+        b["fwd"] += 4.0 * (c * a + c + B * a + B * c)             # W_l, b_l, y_l in; y_{l+1} out
+        f["adj"] += 2.0 * B * a * c
+        b["adj"] += 4.0 * (c * a + c + B * a + B * c + B * c)     # ... and the NN product's sum in; z-bar_l out
+        f["dw"] += 2.0 * B * c * (a + 1)
+        b["dw"] += 4.0 * (B * c + B * a + c * a + c)              # z-bar_l, y_l in; dW_l, db_l written once
+        if l + 1 < n:
+            d = ws[l + 2]
+            f["hadj"] += 2.0 * B * c * d
+            b["hadj"] += 4.0 * (B * d + d * c + B * c)            # z-bar_{l+1}, W_{l+1} in; the product out
+    cnt = {"fwd": n, "adj": n, "dw": n, "hadj": max(1, n - 1)}
+    return {k: v / cnt[k] for k, v in f.items()}, {k: v / cnt[k] for k, v in b.items()}
+
+
 _HASH_CHUNK = 64 << 20  # 4-byte elements per hashed chunk (256 MiB)
 
 
@@ -278,7 +303,7 @@ def cpu_baseline(wl, budget_s: float = 12.0) -> dict:
         threads = len(os.sched_getaffinity(0))
     x0 = synth.initial_state(wl)
     st = tuple(x0[k].astype(np.float64) for k in ("h", "c") if k in x0)
-    if wl.cell == "resmlp":
+    if wl.cell in ("resmlp", "mlp"):
         cache = {}
 
         def layer(l):
@@ -305,7 +330,7 @@ def cpu_baseline(wl, budget_s: float = 12.0) -> dict:
         dt = one(n)
     return {"value": n / dt, "unit": "timesteps/s", "cores": int(threads), "kind": "oracle",
             "sample": f"float64 store-all BPTT (numpy) over the first {n} of {wl.n_steps} "
-                      f"{'layers' if wl.cell == 'resmlp' else 'steps'} at the full shapes, {dt:.1f} s"}
+                      f"{'layers' if wl.cell in ('resmlp', 'mlp') else 'steps'} at the full shapes, {dt:.1f} s"}
 
 
 def device_inputs(wl, dev):
@@ -321,6 +346,17 @@ def device_inputs(wl, dev):
     t = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
     dh = t(x0["h"], op)
     dc = t(x0["c"], torch.float32) if "c" in x0 else None
+    if wl.cell == "mlp":  # layers of different widths: weights and biases one after the other
+        ws = wl.layer_widths()
+        dW = torch.empty(sum(ws[l + 1] * ws[l] for l in range(n)), dtype=torch.float32, device=dev)
+        db = torch.zeros(sum(ws[1:]), dtype=torch.float32, device=dev)
+        offs = [0]
+        for l in range(n):
+            offs.append(offs[-1] + ws[l + 1] * ws[l])
+        with ThreadPoolExecutor(min(16, len(os.sched_getaffinity(0)))) as ex:
+            for l, Wl in ex.map(lambda l: (l, synth.layer_params(wl, l)[0]), range(n)):
+                dW[offs[l]:offs[l + 1]].copy_(torch.from_numpy(Wl.ravel()).to(dev))
+        return None, dW, db, dh, None
     if wl.cell == "resmlp":
         dx = None
         dW = torch.empty((n, H, H), dtype=op, device=dev)
@@ -601,6 +637,19 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
         bitwise = same_gradients(rvo, ref)
         print(f"plain Revolve done, bit-identical gradients: {bitwise}", file=sys.stderr, flush=True)
         rv.close()
+    # states of different sizes: the same pass planned with slots of the
+    # largest size in the same byte budget
+    uni = None
+    if args.compare and wl.cell == "mlp":
+        r.set("uniform_sizes", 1)
+        u_value, uo = other_run(r, reps, warm=steps > 1)
+        r.set("uniform_sizes", 0)
+        uni = {"value": round(u_value, 2), "unit": "timesteps/s",
+               "recompute_factor": round(uo["stats"]["recompute_factor"], 4),
+               "bit_identical_gradients": same_gradients(uo, ref)}
+        print(f"slots of the largest size done, bit-identical gradients: {uni['bit_identical_gradients']}",
+              file=sys.stderr, flush=True)
+        del uo
     # store-all in HBM (a slot for every state: no recomputation, no host tier),
     # same path, where the slot pool fits in a quarter of the HBM
     sa = None
@@ -638,8 +687,11 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
     from paper_1806_01117_amd._lib import KERNEL_CLASSES
     peak = FP32_MFMA_PEAK_TFLOPS if wl.dtype == "f32" else BF16_MFMA_PEAK_TFLOPS
     wide = st["kernel_calls"][3] > 0
-    fl = step_flops(spec, st["window"], wide)
-    byts = step_bytes(wl, spec, st["window"], wide)
+    if wl.cell == "mlp":
+        fl, byts = mlp_layer_work(wl.layer_widths(), wl.batch)
+    else:
+        fl = step_flops(spec, st["window"], wide)
+        byts = step_bytes(wl, spec, st["window"], wide)
     kern = {}
     for i, name in enumerate(KERNEL_CLASSES):
         us = [s_["kernel_us"][i] for s_ in stats if s_["kernel_samples"][i] > 0]
@@ -663,7 +715,12 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
         dom = max(cand, key=tot.get) if cand else "adj"
         small = spec.batch * spec.hidden < 1024 * 256 or wl.dtype == "bf16"
         lds_cell, lds_prod = lds_kernels(spec, knobs)
-        if wide and wl.dtype == "f32":
+        if wl.cell == "mlp":
+            names = {"fwd": "mlpv_gemm forward: layer product + relu (mean over layers)",
+                     "adj": "mlpv_gemm adjoint: recompute, mask, seed (mean over layers)",
+                     "hadj": "mlpv_gemm NN product zbar W_{l+1} (mean over layers)",
+                     "dw": "weight gradient of one layer (mean over layers)"}
+        elif wide and wl.dtype == "f32":
             names = {"fwd": ("cell_gemm_f32" if lds_cell else "step_f32") + " forward: gate GEMM + cell update",
                      "adj": ("cell_gemm_f32" if lds_cell else "step_f32") + " adjoint: gate recompute + cell adjoint",
                      "hadj": ("prod_gemm_f32" if lds_prod else "prod_f32") + " h-adjoint product zbar W_h",
@@ -682,7 +739,9 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
             k = "step_small" if small else "step_f32"
             names = {"fwd": f"{k} forward: gate GEMM + cell update", "adj": f"{k} adjoint: gate recompute + h-adjoint GEMM",
                      "dw": ("dw_bf16" if wl.dtype == "bf16" else "dw_lds_f32") + " weight-gradient window"}
-        if wide and wl.dtype == "f32":
+        if wl.cell == "mlp":
+            key = "mlpv_" + dom
+        elif wide and wl.dtype == "f32":
             key = {"fwd": "cell_gemm_f32_fwd" if lds_cell else "step_f32_fwd",
                    "adj": "cell_gemm_f32_adj" if lds_cell else "step_f32_adj",
                    "hadj": "prod_gemm_f32" if lds_prod else "prod_f32"}.get(dom, "dw_f32_big")
@@ -709,7 +768,8 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
         "metric": METRIC, "value": round(value, 2), "unit": "timesteps/s", "n_gpus": 1,
         "steps": steps, "warmup": warmup, "ms_per_step": round(1000 * el / steps, 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
-        "data": "synthetic (seeded normal inputs, " + ("normal" if wl.cell == "resmlp" else "uniform") + " weights)",
+        "data": "synthetic (seeded normal inputs, " + ("normal" if wl.cell in ("resmlp", "mlp") else "uniform")
+                + " weights)",
         "config": {"workload": wl.name, "cell": wl.cell, "batch": wl.batch, "input": wl.input,
                    "hidden": wl.hidden, "n_steps": wl.n_steps, "fast_slots": wl.fast_slots,
                    "slow_slots": spec.slow_slots,
@@ -734,6 +794,7 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
             "recompute_factor": round(rv_st["recompute_factor"], 4), "bit_identical_gradients": bitwise,
             "compared": comparison_kind(ref)},
         "store_all": sa,
+        **({"slots_of_the_largest_size": uni} if uni is not None else {}),
         "path": "resident" if resident else "steps",
         "per_step_launches": alt,
         "kernel_us": {k: round(v[0], 3) for k, v in kern.items()},

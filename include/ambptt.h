@@ -193,9 +193,8 @@ ambptt_status ambptt_schedule_text_costs(int64_t n, int32_t s, int64_t H, int32_
                                          const double* costs, char* buf, size_t cap, size_t* needed);
 
 /* Canonical text of the schedule when the states differ in size (the case
- * Sections 1.1 and 6 set beside Revolve's uniform states; Section 6 proposes
- * the algorithm for non-uniform single-stage checkpointing inside each
- * interval).  sizes[0..n] (>= 1) are the sizes of x_0 .. x_n in units of a
+ * Sections 1.1 and 6 set beside Revolve's uniform states; Section 6 would
+ * run a one-level method for unequal checkpoints inside each interval).  sizes[0..n] (>= 1) are the sizes of x_0 .. x_n in units of a
  * common granule; the fast pool holds s * max(sizes) units and the
  * snapshots stack in it: the one taken at recursion depth k ("slot" k, which
  * may exceed s - 1 when states are small) lies above the states in the slots
@@ -340,7 +339,10 @@ ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
  * of compute on them are taken; 0 by default), "test_poison" (1: a prefetch
  * first fills its fast slot with NaN bytes on the copy stream, so that
  * compute reading the slot before the prefetch has landed spoils the
- * gradients), "lds_gemm" (fp32 path for large batches: 1, default, runs the gate
+ * gradients), "uniform_sizes" (states of different sizes: 1 plans the
+ * schedule as if every state had the size of the largest, i.e. slots of the
+ * largest size in the same byte budget, for comparison with the sized
+ * schedule; 0 by default), "lds_gemm" (fp32 path for large batches: 1, default, runs the gate
  * product with its cell epilogue and the h-adjoint product on LDS-tiled
  * kernels (128 x 128 and 64 x 64 tiles, two workgroups per CU) where they
  * have at least 256 tiles; 2 wherever their shape constraints hold; 0 never:

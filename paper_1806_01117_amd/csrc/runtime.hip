@@ -291,6 +291,7 @@ struct ambptt_ctx {
   std::vector<size_t> woff, boff;
   std::vector<int64_t> zunits;
   size_t unit = 0;
+  bool uniform_sizes = false;  // plan as if every state had the largest size (for comparison)
   int host_waits = -1;      // slot dependencies on host-tier copies: 1 waited for on the host, 0 stream waits, -1 by path
   hipEvent_t ev_end[8] = {};  // end events recorded by compute dispatches (host-tier copies and sweep pacing wait on them)
   Plan last_plan;        // the schedule the last ambptt_run executed
@@ -331,12 +332,14 @@ int64_t interval_from_timings(double ta, double tt, int64_t s, int rule, double 
 }
 
 // The schedule a pass runs: the online one when the context asks for it.
+std::vector<int64_t> plan_units(const ambptt_ctx* C);
+
 Plan pass_plan(ambptt_ctx* C) {
   const ambptt_problem& p = C->p;
   const int64_t I = std::max<int64_t>(C->interval_min, 1);
   if (C->L.mlpv) {  // states of different sizes: the sized recursion in every reversal
     if (C->online) throw std::invalid_argument("online checkpointing is not available for states of different sizes");
-    return make_plan_sized(p.n_steps, p.fast_slots, slow_capacity(C), I, C->zunits,
+    return make_plan_sized(p.n_steps, p.fast_slots, slow_capacity(C), I, plan_units(C),
                            C->step_costs.empty() ? nullptr : &C->step_costs, &C->plan_cost);
   }
   if (C->online) return make_plan_online(p.n_steps, p.fast_slots, p.slow_slots, I);
@@ -379,6 +382,14 @@ void set_layer_widths(ambptt_ctx* C, const std::vector<int32_t>& w) {
   C->unit = g;
   C->zunits.resize(n + 1);
   for (size_t t = 0; t <= n; ++t) C->zunits[t] = int64_t(bytes[t] / g);
+}
+
+// The state sizes the sized schedules plan with: the states' own, or the
+// largest for every state (knob "uniform_sizes": slots of the largest size).
+std::vector<int64_t> plan_units(const ambptt_ctx* C) {
+  if (!C->uniform_sizes) return C->zunits;
+  const int64_t m = *std::max_element(C->zunits.begin(), C->zunits.end());
+  return std::vector<int64_t>(C->zunits.size(), m);
 }
 
 unsigned event_flags(const ambptt_ctx* C, bool timing) {
@@ -1641,6 +1652,9 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
     C->lds_gemm = int(v);
   } else if (k == "hadj_launch") {
     C->hadj_launch = v != 0;
+  } else if (k == "uniform_sizes") {
+    if (v < 0 || v > 1) return fail(AMBPTT_EINVAL, "uniform_sizes must be 0 or 1");
+    C->uniform_sizes = v == 1;
   } else if (k == "store_policy") {
     if (v < 0 || v > 1) return fail(AMBPTT_EINVAL, "store_policy must be 0 (every I-th state) or 1 (when the previous store completed)");
     if (v == 1 && C->path_opt == 2) return fail(AMBPTT_EUNSUPPORTED, "store_policy 1 runs on the per-step path only");
@@ -1897,7 +1911,7 @@ static ambptt_status run_pass(ambptt_ctx* C, const void* x_seq, const void* W, c
     if ((s = E.dynamic_sweep(starts, dW, db)) != AMBPTT_OK) return s;
     try {
       const std::vector<double>* costs = C->step_costs.empty() ? nullptr : &C->step_costs;
-      plan = L.mlpv ? make_plan_sized_starts(p.n_steps, p.fast_slots, slow_capacity(C), starts, C->zunits, costs,
+      plan = L.mlpv ? make_plan_sized_starts(p.n_steps, p.fast_slots, slow_capacity(C), starts, plan_units(C), costs,
                                              &C->plan_cost)
                     : make_plan_starts(p.n_steps, p.fast_slots, slow_capacity(C), starts, costs, &C->plan_cost);
     } catch (const std::exception& e) {

@@ -58,3 +58,14 @@ def test_lds_rule_of_the_4096_lstm():
     assert bench.lds_kernels(spec, [("lds_gemm", 0)]) == (False, False)
     small = amb.ProblemSpec.from_workload(synth.get("lstm_h512_t1000"))
     assert bench.lds_kernels(small, []) == (False, False)
+
+
+def test_mlp_layer_work_reduces_to_one_width():
+    B, w, n = 8, 32, 5
+    f, b = bench.mlp_layer_work([w] * (n + 1), B)
+    assert f["fwd"] == f["adj"] == f["hadj"] == 2.0 * B * w * w
+    assert f["dw"] == 2.0 * B * w * (w + 1)
+    assert b["fwd"] == 4.0 * (w * w + w + 2 * B * w)
+    # widths that alternate: the mean over layers of each class
+    f2, _ = bench.mlp_layer_work([16, 32, 16], 4)
+    assert f2["fwd"] == (2 * 4 * 16 * 32 + 2 * 4 * 32 * 16) / 2 and f2["hadj"] == 2 * 4 * 32 * 16
