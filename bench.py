@@ -624,7 +624,7 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
 
     reps = max(1, min(3, steps))
     # plain Revolve at the same HBM slot budget (no host tier), same path
-    rv_value, rv_st, bitwise = None, None, None
+    rv_value, rv_st, bitwise, rv_refused = None, None, None, None
     if args.compare:
         rv = runner(amb.ProblemSpec.from_workload(wl, slow_slots=0))
         rv.set("path", 2 if resident else 1)
@@ -632,10 +632,16 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
         for k, v in knobs:
             if k != "online":  # plain Revolve knows n up front
                 rv.set(k, v)
-        rv_value, rvo = other_run(rv, reps, warm=steps > 1)
-        rv_st = rvo["stats"]
-        bitwise = same_gradients(rvo, ref)
-        print(f"plain Revolve done, bit-identical gradients: {bitwise}", file=sys.stderr, flush=True)
+        try:
+            rv_value, rvo = other_run(rv, reps, warm=steps > 1)
+            rv_st = rvo["stats"]
+            bitwise = same_gradients(rvo, ref)
+            print(f"plain Revolve done, bit-identical gradients: {bitwise}", file=sys.stderr, flush=True)
+        except amb.AmbpttError as e:
+            if e.status != amb._lib.EUNSUPPORTED:
+                raise
+            rv_refused = str(e)  # e.g. one sized reversal of all n steps needs a table past the limit
+            print(f"plain Revolve refused: {e}", file=sys.stderr, flush=True)
         rv.close()
     # states of different sizes: the same pass planned with slots of the
     # largest size in the same byte budget
@@ -789,7 +795,7 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
         "paper_model": {"revolve_R": round((amb.revolve_advances(wl.n_steps, spec.fast_slots) + 1) / wl.n_steps, 4),
                         "async_R": round((amb.revolve_advances(st["interval"], spec.fast_slots) + 1) / st["interval"], 4)
                         if st["interval"] > 0 else None},
-        "plain_revolve": None if rv_st is None else {
+        "plain_revolve": ({"refused": rv_refused} if rv_refused else None) if rv_st is None else {
             "value": round(rv_value, 2), "unit": "timesteps/s",
             "recompute_factor": round(rv_st["recompute_factor"], 4), "bit_identical_gradients": bitwise,
             "compared": comparison_kind(ref)},
