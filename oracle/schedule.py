@@ -104,8 +104,8 @@ total cost of recomputed forward steps (WeightedSplits); the header then ends
 with " split=cost".
 
 States of different sizes (the other non-uniform case of Sections 1.1 and 6;
-within an interval the paper proposes the known algorithm for non-uniform
-single-stage checkpointing instead of Revolve): sizes[t] is the size of x_t
+inside an interval the paper would replace Revolve by an existing one-level
+method for checkpoints of unequal size): sizes[t] is the size of x_t
 in units of a common granule, and the fast memory is a byte-addressed pool of
 P = s * max(sizes) units (s states of the largest size).  Checkpoints form a
 stack: the snapshot taken at recursion depth k ("slot" k) sits right above
@@ -559,9 +559,9 @@ def schedule_costs(n: int, s: int, costs, H: int = 0, I_min: int = 0) -> tuple[d
 
 
 class SizedSplits:
-    """Optimal splits when states differ in size (non-uniform single-stage
-    checkpointing, the algorithm the paper's Section 6 proposes inside each
-    interval; Section 1.1 cites a dynamic program for it): Revolve's
+    """Optimal splits when states differ in size (one-level checkpointing of
+    unequal states, which Section 6 would run inside each interval and for
+    which Section 1.1 cites a dynamic program): Revolve's
     recursion with a memory budget in units instead of a slot count.
     sizes[t] (t = 0 .. n) is the size of x_t in units, costs[t] the cost of
     forward step t (default 1).  With the live state at x_a and M units free
@@ -573,7 +573,11 @@ class SizedSplits:
     free again for [a, a+m)); ties go to the largest m; when no snapshot fits
     the chain (restore x_a and advance i steps, i = l-1 .. 1) costs
     sum_{i=1}^{l-1} C(a, a+i).  A split that fits never costs more than the
-    chain, so a split is always taken when one fits."""
+    chain, so a split is always taken when one fits.  When every state of
+    (a, a+l) fits in M, splitting at 1 at every level advances each step
+    once and every other split costs more, so T and split answer such a part
+    directly (C(a, a+l-1) and 1) without the recursion; the pins check this
+    against the recursion."""
 
     def __init__(self, sizes, costs=None):
         self.z = [int(v) for v in sizes]
@@ -591,11 +595,19 @@ class SizedSplits:
     def C(self, a: int, b: int) -> float:
         return self.pre[b] - self.pre[a]
 
+    def fits(self, a: int, l: int, M: int) -> bool:
+        """Every state strictly inside [a, a+l) fits in M units at once."""
+        return l <= 1 or sum(self.z[a + 1:a + l]) <= M
+
     def T(self, a: int, l: int, M: int) -> float:
+        if self.fits(a, l, M):
+            return 0.0 if l <= 1 else self.C(a, a + l - 1)
         return self._solve(a, l, M)[0]
 
     def split(self, a: int, l: int, M: int) -> int:
         """The split m, or 0 for the chain."""
+        if self.fits(a, l, M):
+            return 1
         return self._solve(a, l, M)[1]
 
     def _solve(self, a, l, M):
@@ -659,8 +671,8 @@ def schedule_sized(n: int, s: int, sizes, H: int = 0, I_min: int = 0, costs=None
 def schedule_sized_from_starts(n: int, s: int, H: int, starts: list[int], sizes, costs=None):
     """The two-level policy over interval starts chosen during the sweep,
     each interval reversed by the sized recursion (the pairing Section 6
-    proposes: stores whenever the previous transfer completed, and the
-    non-uniform single-stage algorithm inside each interval)."""
+    proposes: a store as soon as the previous one has finished, and one-level
+    checkpointing of unequal states inside each interval)."""
     starts = list(starts)
     if n < 1 or s < 2 or not starts or starts[0] != 0 or any(b <= a for a, b in zip(starts, starts[1:])) \
             or starts[-1] >= n or len(starts) - 1 > H or len(sizes) != n + 1:

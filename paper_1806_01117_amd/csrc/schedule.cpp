@@ -515,7 +515,10 @@ namespace {
 // Least cost of reversing [a, a + l) with M units free above x_a when the
 // states differ in size, and the split that reaches it (0: the chain).  One
 // dense table per root reversal [a0, a0 + L) with budget M0, filled
-// bottom-up over (M, l, a) and indexed by (a - a0, l, M).
+// bottom-up over (M, l, a) and indexed by (a - a0, l, M).  A part whose
+// states x_{a+1} .. x_{a+l-1} all fit in M needs no table: splitting at 1 at
+// every level advances each step once, which every other split exceeds by a
+// positive cost, so it is the recursion's unique optimum.
 class SizedSplits {
  public:
   SizedSplits(const std::vector<int64_t>& sizes, const std::vector<double>* costs, int64_t max_table)
@@ -523,13 +526,20 @@ class SizedSplits {
     const size_t n = sizes.size() - 1;
     pre_.assign(n + 1, 0.0);
     for (size_t t = 0; t < n; ++t) pre_[t + 1] = pre_[t] + (costs ? (*costs)[t] : 1.0);
+    zpre_.assign(n + 2, 0);
+    for (size_t t = 0; t <= n; ++t) zpre_[t + 1] = zpre_[t] + sizes[t];
   }
   double C(int64_t a, int64_t b) const { return pre_[size_t(b)] - pre_[size_t(a)]; }
+  bool fits(int64_t a, int64_t l, int64_t M) const {
+    return l <= 1 || zpre_[size_t(a + l)] - zpre_[size_t(a + 1)] <= M;
+  }
   int64_t split(int64_t a, int64_t l, int64_t M) {
+    if (fits(a, l, M)) return 1;
     ensure(a, l, M);
     return m_[idx(a, l, M)];
   }
   double T(int64_t a, int64_t l, int64_t M) {
+    if (fits(a, l, M)) return l <= 1 ? 0.0 : C(a, a + l - 1);
     ensure(a, l, M);
     return v_[idx(a, l, M)];
   }
@@ -568,7 +578,7 @@ class SizedSplits {
         }
       }
   }
-  std::vector<int64_t> z_;
+  std::vector<int64_t> z_, zpre_;
   std::vector<double> pre_, v_;
   std::vector<int32_t> m_;
   int64_t a0_ = 0, L_ = 0, M0_ = -1, max_table_;

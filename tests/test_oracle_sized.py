@@ -1,8 +1,8 @@
 """Pins for schedules over states of different sizes (CPU only).
 
 Sections 1.1 and 6 set states of unequal size beside Revolve's uniform ones
-and propose, inside each interval, the algorithm for non-uniform
-single-stage checkpointing.  The oracle's SizedSplits runs Revolve's
+and would checkpoint them, inside each interval, with a one-level method for
+unequal states.  The oracle's SizedSplits runs Revolve's
 recursion with a memory budget in units of a common granule, the snapshots
 stacked in a byte-addressed pool.  Pinned against:
   * Revolve itself: with unit sizes the schedules are the canonical ones,
@@ -230,3 +230,37 @@ def test_c_abi_sized_errors():
     with pytest.raises(AmbpttError) as e:    # one reversal of 400 steps on 1200 units: table too large
         amb_lib.schedule_text_sized(400, 300, [4] * 401)
     assert e.value.status == EUNSUPPORTED
+
+
+def test_parts_that_fit_are_answered_without_the_recursion():
+    """A part whose inner states all fit: the recursion itself splits at 1 and
+    costs each step once, which is what T and split return directly."""
+    rng = random.Random(43)
+    for _ in range(200):
+        n = rng.randint(2, 12)
+        sizes = [rng.randint(1, 3) for _ in range(n + 1)]
+        costs = [rng.choice([0.5, 1.0, 2.0]) for _ in range(n)] if rng.random() < 0.5 else None
+        ss = S.SizedSplits(sizes, costs)
+        a = rng.randint(0, n - 2)
+        l = rng.randint(2, n - a)
+        M = sum(sizes[a + 1:a + l]) + rng.randint(0, 2)
+        assert ss.fits(a, l, M)
+        v, m = ss._solve(a, l, M)
+        assert m == 1 and v == pytest.approx(ss.C(a, a + l - 1), rel=1e-12)
+        assert ss.split(a, l, M) == 1 and ss.T(a, l, M) == ss.C(a, a + l - 1)
+        # one unit less than everything needs: the recursion must recompute
+        assert not ss.fits(a, l, sum(sizes[a + 1:a + l]) - 1)
+
+
+def test_store_all_over_many_states_of_different_sizes():
+    """A slot for every state: the schedule advances every step once, for the
+    oracle and the library alike, with no table (400 steps would need a table
+    of 257 M entries; the library also over 2000)."""
+    n = 400
+    sizes = [4, 2, 1, 2] * (n // 4) + [4]
+    txt = S.text_sized(n, n + 1, sizes)
+    _, acts = S.parse(txt)
+    assert sum(a[2] - a[1] for a in acts if a[0] == "A") == n - 1   # with the first turn's step: n
+    assert amb_lib.schedule_text_sized(n, n + 1, sizes) == txt
+    _, big = S.parse(amb_lib.schedule_text_sized(2000, 2001, [4, 2, 1, 2] * 500 + [4]))
+    assert sum(a[2] - a[1] for a in big if a[0] == "A") == 1999
