@@ -277,7 +277,12 @@ struct ambptt_ctx {
   double plan_cost = 0.0;          // cost of the forward evaluations of the last plan built
   Plan cost_plan;                  // the plan for step_costs, kept while its inputs stay the same
   int64_t cost_plan_key[3] = {-1, -1, -1};  // interval_min, slow capacity, costs version
+  double cost_plan_cost = 0.0;
   int64_t costs_version = 0;
+  Plan sized_plan;                 // the plan of states of different sizes, kept likewise
+  int64_t sized_plan_key[6] = {-1, -1, -1, -1, -1, -1};
+  double sized_plan_cost = 0.0;
+  int64_t widths_version = 0;
   bool hadj_launch = true;  // fp32 large-batch path: the adjoint's h-adjoint product as a launch of its own
   int lds_gemm = 1;         // fp32 large-batch path: LDS-tiled kernels (0 off, 1 when they fill the device twice over, 2 always)
   // tests of the stream ordering: a host-side delay before every host-tier
@@ -339,8 +344,16 @@ Plan pass_plan(ambptt_ctx* C) {
   const int64_t I = std::max<int64_t>(C->interval_min, 1);
   if (C->L.mlpv) {  // states of different sizes: the sized recursion in every reversal
     if (C->online) throw std::invalid_argument("online checkpointing is not available for states of different sizes");
-    return make_plan_sized(p.n_steps, p.fast_slots, slow_capacity(C), I, plan_units(C),
-                           C->step_costs.empty() ? nullptr : &C->step_costs, &C->plan_cost);
+    // built once per set of inputs: its tables take a visible time on the host
+    const int64_t key[6] = {I, slow_capacity(C), C->costs_version, int64_t(C->step_costs.empty()),
+                            C->widths_version, int64_t(C->uniform_sizes)};
+    if (!std::equal(key, key + 6, C->sized_plan_key)) {
+      C->sized_plan = make_plan_sized(p.n_steps, p.fast_slots, slow_capacity(C), I, plan_units(C),
+                                      C->step_costs.empty() ? nullptr : &C->step_costs, &C->sized_plan_cost);
+      std::copy(key, key + 6, C->sized_plan_key);
+    }
+    C->plan_cost = C->sized_plan_cost;
+    return C->sized_plan;
   }
   if (C->online) return make_plan_online(p.n_steps, p.fast_slots, p.slow_slots, I);
   if (!C->step_costs.empty() && C->store_policy == 1 && C->path_opt != 2) {
@@ -354,9 +367,10 @@ Plan pass_plan(ambptt_ctx* C) {
   if (!C->step_costs.empty()) {  // the dynamic program runs once per set of inputs
     const int64_t key[3] = {I, slow_capacity(C), C->costs_version};
     if (!std::equal(key, key + 3, C->cost_plan_key)) {
-      C->cost_plan = make_plan_costs(p.n_steps, p.fast_slots, key[1], I, C->step_costs, &C->plan_cost);
+      C->cost_plan = make_plan_costs(p.n_steps, p.fast_slots, key[1], I, C->step_costs, &C->cost_plan_cost);
       std::copy(key, key + 3, C->cost_plan_key);
     }
+    C->plan_cost = C->cost_plan_cost;
     return C->cost_plan;
   }
   return make_plan(p.n_steps, p.fast_slots, slow_capacity(C), I);
@@ -366,6 +380,7 @@ Plan pass_plan(ambptt_ctx* C) {
 // of their greatest common divisor (every size is a multiple of 256 bytes).
 void set_layer_widths(ambptt_ctx* C, const std::vector<int32_t>& w) {
   C->widths = w;
+  C->widths_version++;
   const size_t n = w.size() - 1;
   C->woff.assign(n + 1, 0);
   C->boff.assign(n + 1, 0);
@@ -1453,6 +1468,7 @@ ambptt_status ambptt_set_step_costs(ambptt_ctx* C, const double* costs, int64_t 
   if (!C) return fail(AMBPTT_EINVAL, "ctx is NULL");
   if (!costs || n == 0) {
     C->step_costs.clear();
+    C->costs_version++;
     return AMBPTT_OK;
   }
   if (n != C->p.n_steps) return fail(AMBPTT_EINVAL, "step costs: need one cost per step of the problem");
