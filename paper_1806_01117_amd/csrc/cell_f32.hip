@@ -153,9 +153,10 @@ __global__ __launch_bounds__(64 * KS) void step_f32(StepArgs a) {
     const int c0 = (nch * wave) / KS, c1 = (nch * (wave + 1)) / KS;
     const float* zb = (const float*)a.zbar_in;
     const float* wt = (const float*)a.WhT;
+    const size_t ldw = a.ld_wht ? a.ld_wht : GH;
     auto la = [&](int ch, int i) -> f4 { return *(const f4*)(zb + (size_t)rows[i] * GH + ch * 16 + 4 * q); };
     auto lb = [&](int ch, int jj) -> f4 {
-      return *(const f4*)(wt + (size_t)(j0 + 16 * jj + r) * GH + ch * 16 + 4 * q);
+      return *(const f4*)(wt + (size_t)(j0 + 16 * jj + r) * ldw + ch * 16 + 4 * q);
     };
     nt_chunks<RM, RJ, U>(c0, c1, acch, la, lb);
   }
@@ -290,11 +291,12 @@ __global__ __launch_bounds__(64 * KS) void prod_f32(ProdArgs a) {
   for (int i = 0; i < RM; ++i) rows[i] = min(m0 + 16 * i + r, M - 1);  // rows >= M: clamped, discarded
   const float* A = (const float*)a.A;
   const float* Bm = (const float*)a.B;
+  const size_t ldb = a.ldb ? a.ldb : K;
   const int nch = K / 16;
   const int c0 = (nch * wave) / KS, c1 = (nch * (wave + 1)) / KS;
   nt_chunks<RM, NB, U>(
       c0, c1, acc, [&](int ch, int i) -> f4 { return *(const f4*)(A + (size_t)rows[i] * K + ch * 16 + 4 * q); },
-      [&](int ch, int nb) -> f4 { return *(const f4*)(Bm + (size_t)(n0 + 16 * nb + r) * K + ch * 16 + 4 * q); });
+      [&](int ch, int nb) -> f4 { return *(const f4*)(Bm + (size_t)(n0 + 16 * nb + r) * ldb + ch * 16 + 4 * q); });
   if constexpr (KS > 1) {
     __shared__ f4 red[(KS - 1) * RM * NB * 64];
     if (wave > 0) {
@@ -425,7 +427,7 @@ __global__ __launch_bounds__(256) void dw_lds_f32(DwArgs a) {
   if (do_bias && wave == 0 && k0 + lane < GH) a.db[k0 + lane] = a.accumulate ? a.db[k0 + lane] + bsum : bsum;
 }
 
-__global__ void transpose_wh_f32(const float* __restrict__ W, float* __restrict__ WhT, int GH, int D, int H) {
+__global__ void transpose_wh_f32(const float* __restrict__ W, float* __restrict__ WhT, int GH, int D, int H, int ld) {
   __shared__ float tile[32][33];
   const int kb = blockIdx.x * 32, jb = blockIdx.y * 32;
   const int tx = threadIdx.x, ty = threadIdx.y;
@@ -436,7 +438,7 @@ __global__ void transpose_wh_f32(const float* __restrict__ W, float* __restrict_
   __syncthreads();
   for (int y = ty; y < 32; y += 8) {
     const int j = jb + y, k = kb + tx;
-    if (j < H && k < GH) WhT[(size_t)j * GH + k] = tile[tx][y];
+    if (j < H && k < GH) WhT[(size_t)j * ld + k] = tile[tx][y];
   }
 }
 
@@ -529,9 +531,10 @@ hipError_t launch_prod_f32(const ProdArgs& a, hipStream_t s, hipEvent_t e0, hipE
   return hipGetLastError();
 }
 
-hipError_t launch_transpose_wh(const float* W, float* WhT, int GH, int D, int H, hipStream_t s) {
+hipError_t launch_transpose_wh(const float* W, float* WhT, int GH, int D, int H, int ld, hipStream_t s) {
+  if (ld < GH) return hipErrorInvalidValue;
   dim3 grid((GH + 31) / 32, (H + 31) / 32);
-  hipLaunchKernelGGL(transpose_wh_f32, grid, dim3(32, 8), 0, s, W, WhT, GH, D, H);
+  hipLaunchKernelGGL(transpose_wh_f32, grid, dim3(32, 8), 0, s, W, WhT, GH, D, H, ld);
   return hipGetLastError();
 }
 

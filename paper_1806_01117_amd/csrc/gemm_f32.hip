@@ -271,7 +271,7 @@ __global__ __launch_bounds__(256, 2) void prod_gemm_f32(ProdArgs a) {
 #pragma unroll
   for (int p = 0; p < 4; ++p) {
     arow[p] = (const float*)a.A + (size_t)min(m0 + lr + 16 * p, M - 1) * K;  // rows >= M: clamped, discarded
-    brow[p] = (const float*)a.B + (size_t)(n0 + lr + 16 * p) * K;
+    brow[p] = (const float*)a.B + (size_t)(n0 + lr + 16 * p) * (a.ldb ? a.ldb : K);
   }
   f4 ra[4], rb[4];
   bool kin = true;

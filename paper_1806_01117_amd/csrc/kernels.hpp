@@ -40,6 +40,7 @@ struct StepArgs {
   int first;             // adjoint of step n-1: no incoming adjoint
   int last;              // the step's output is x_n
   float inv_bh;          // 1 / (B H)
+  int ld_wht = 0;        // row stride of WhT in elements (0: G*H)
 };
 
 // Weight-gradient window: dW[k][c] += sum_r Z[r][k] X[r][c], db[k] += sum_r Z[r][k],
@@ -82,6 +83,7 @@ struct ProdArgs {
   const float* add;
   float* out;
   int M, N, K;
+  int ldb = 0;  // row stride of B in elements (0: K)
 };
 
 // One launch of the MLP whose layers change width (mlp_f32.hip):
@@ -208,7 +210,8 @@ hipError_t launch_dw_bf16(const DwArgs& a, hipStream_t s, hipEvent_t e0 = nullpt
 int mlpv_tiles(int M, int N);
 hipError_t launch_mlpv(int mode, const MlpvArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_transpose_wh_bf16(const void* W, void* WhT, int GH, int D, int H, hipStream_t s);
-hipError_t launch_transpose_wh(const float* W, float* WhT, int GH, int D, int H, hipStream_t s);
+// WhT[j][k] = W[k][D + j] with rows of ld >= GH floats
+hipError_t launch_transpose_wh(const float* W, float* WhT, int GH, int D, int H, int ld, hipStream_t s);
 hipError_t launch_fill32(void* p, size_t words, uint32_t value, hipStream_t s);
 hipError_t launch_loss_sum(const double* acc, int n, double scale, double* out, hipStream_t s);
 

@@ -65,6 +65,7 @@ struct Layout {
   int G = 1, dsize = 4, window = 1;
   size_t h_bytes = 0, c_bytes = 0, state_bytes = 0, stride = 0;
   size_t off_live[2] = {0, 0}, off_wht = 0, off_zbar = 0, off_hwin = 0, off_cbar[2] = {0, 0};
+  int ld_wht = 0;        // row stride of WhT in elements
   size_t off_loss = 0, off_lossout = 0, total = 0;
   int loss_slots = 0;
   StepCfg cfg{1, 1, 1};  // single-launch path
@@ -199,7 +200,12 @@ Layout make_layout(const ambptt_problem* p, int window) {
     L.small = false;
     L.loss_slots = mlpv_tiles(p->batch, p->hidden);
   }
-  L.off_wht = o; o += (L.mlp || L.mlpv) ? 0 : align_up((size_t)p->hidden * GH * L.dsize);
+  // the large-batch fp32 kernels read WhT rows in 64-wide stages; rows padded
+  // by 32 floats keep a power-of-two row length from mapping every row's
+  // stage onto the same L2 sets
+  const bool pad_wht = !L.small && !L.mlp && !L.mlpv && p->dtype == AMBPTT_F32;
+  L.ld_wht = int(GH) + (pad_wht ? 32 : 0);
+  L.off_wht = o; o += (L.mlp || L.mlpv) ? 0 : align_up((size_t)p->hidden * L.ld_wht * L.dsize);
   L.off_zbar = o; o += align_up(2 * (size_t)L.window * p->batch * GH * L.dsize);
   L.off_hwin = o; o += align_up(2 * (size_t)L.window * BH * L.dsize);
   L.off_cbar[0] = o; o += align_up(BH * 4);
@@ -662,6 +668,7 @@ struct Exec {
     a.W = W;
     a.bias = b;
     a.WhT = WhT;
+    a.ld_wht = L.ld_wht;
     a.loss = p.loss;
     a.inv_bh = 1.0f / float((double)p.batch * p.hidden);
     return a;
@@ -825,7 +832,7 @@ struct Exec {
       a.hwin_out = hwin_at(t);
       a.loss_acc = (double*)(C->ws + L.off_loss);
       if ((wide || sep32) && !first) {  // hbar_{t+1} = zbar_{t+1} W_h
-        ProdArgs pa{a.zbar_in, WhT, nullptr, hbuf, p.batch, p.hidden, L.G * p.hidden};
+        ProdArgs pa{a.zbar_in, WhT, nullptr, hbuf, p.batch, p.hidden, L.G * p.hidden, L.ld_wht};
         s = timed(AMBPTT_K_HADJ, [&](hipEvent_t e0, hipEvent_t e1) {
           return wide ? launch_prod_nt(pa, C->cs, e0, e1) : prod32(pa, e0, e1);
         });
@@ -916,7 +923,7 @@ struct Exec {
     a.dh0 = dh0;
     a.dc0 = dc0;
     if (wide || sep32) {  // dL/dh_0 = zbar_0 W_h, dL/dc_0 = cbar_0
-      ProdArgs pa{a.zbar_in, WhT, nullptr, dh0, p.batch, p.hidden, L.G * p.hidden};
+      ProdArgs pa{a.zbar_in, WhT, nullptr, dh0, p.batch, p.hidden, L.G * p.hidden, L.ld_wht};
       ambptt_status s = timed(AMBPTT_K_OTHER, [&](hipEvent_t e0, hipEvent_t e1) {
         return wide ? launch_prod_nt(pa, C->cs, e0, e1) : prod32(pa, e0, e1);
       });
@@ -1145,7 +1152,7 @@ ambptt_status prepare_inputs(ambptt_ctx* C, const void* W, const void* h0, const
   } else if (p.dtype == AMBPTT_BF16) {
     HIPCK(launch_transpose_wh_bf16(W, E.WhT, L.G * p.hidden, p.input, p.hidden, C->cs));
   } else {
-    HIPCK(launch_transpose_wh((const float*)W, (float*)E.WhT, L.G * p.hidden, p.input, p.hidden, C->cs));
+    HIPCK(launch_transpose_wh((const float*)W, (float*)E.WhT, L.G * p.hidden, p.input, p.hidden, L.ld_wht, C->cs));
   }
   // live state <- x_0
   char* l0 = E.live(0);
