@@ -9,13 +9,16 @@
 //   product   u = zbar W  (an "NN" product: W[k][c] is contiguous in c)
 // dW_l = zbar_l^T y_l and db_l run on the weight-gradient kernels.
 //
-// One launch per step.  A workgroup owns 32 rows x 32 columns, each of its
-// 4 waves one 16 x 16 block; the reduction runs in chunks of 16 straight from
-// global memory: lane l reads 4 consecutive k of row l & 15 at 4 (l >> 4) and
-// its components feed 4 MFMAs (A and the "NT" B the same way; the "NN" B as
-// 4 reads of one column each, coalesced across the 16 lanes).  Widths are
-// multiples of 16; a tile's second column block may fall past N and then
-// idles.  The loss terms of a workgroup are summed in wave order.
+// One launch per step.  A workgroup owns 32 rows x 32 columns; each of its 4
+// waves computes the whole tile (2 x 2 blocks of 16 x 16) over a quarter of
+// the reduction, in chunks of 16 read straight from global memory with the
+// next chunk's operands loaded before the current chunk's 16 MFMAs, and the
+// four partial tiles are summed in wave order through LDS by wave 0, which
+// then runs the epilogue.  Lane l reads 4 consecutive k of row l & 15 at 4
+// (l >> 4) and its components feed 4 MFMAs (A and the "NT" B the same way;
+// the "NN" B as 4 reads of one column each, coalesced across the 16 lanes).
+// Widths are multiples of 16; a tile's second column block may fall past N
+// and then idles.  The loss terms of a workgroup are summed by wave 0.
 #include <hip/hip_runtime.h>
 
 #include "ambptt.h"
@@ -40,75 +43,115 @@ enum { kMlpvFwd = 0, kMlpvAdj = 1, kMlpvNN = 2 };
 
 template <int MODE>
 __global__ __launch_bounds__(256) void mlpv_gemm(MlpvArgs a) {
-  __shared__ float red[4];
+  __shared__ f4 part[3][4][64];  // waves 1..3: their four accumulators, lane by lane
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, q = lane >> 4;
   const int M = a.M, N = a.N, K = a.K;
-  const int m0 = blockIdx.x * 32 + (wave >> 1) * 16;
-  const int n0 = blockIdx.y * 32 + (wave & 1) * 16;
-  const bool active = n0 < N;
-  f4 acc = {0.f, 0.f, 0.f, 0.f};
-  if (active) {
-    const float* arow = a.A + (size_t)min(m0 + r, M - 1) * K + 4 * q;  // rows >= M: clamped, discarded
-    for (int k0 = 0; k0 < K; k0 += 16) {
-      const f4 av = *(const f4*)(arow + k0);
-      f4 bv;
-      if (MODE == kMlpvNN) {
-        const float* w = a.W + (size_t)(k0 + 4 * q) * N + n0 + r;
-        bv = f4{w[0], w[N], w[2 * (size_t)N], w[3 * (size_t)N]};
-      } else {
-        bv = *(const f4*)(a.W + (size_t)(n0 + r) * K + k0 + 4 * q);
-      }
-      acc = mfma4(av.x, bv.x, acc);
-      acc = mfma4(av.y, bv.y, acc);
-      acc = mfma4(av.z, bv.z, acc);
-      acc = mfma4(av.w, bv.w, acc);
-    }
-  }
-  // accumulator element v of lane l: row 4 (l >> 4) + v, column l & 15 of the block
-  float lterm = 0.f;
-  if (active) {
+  const int m0 = blockIdx.x * 32, n0 = blockIdx.y * 32;
+  const bool two = n0 + 16 < N;  // the second column block lies inside N
+  const int nch = K / 16, c0 = nch * wave / 4, c1 = nch * (wave + 1) / 4;
+  const float* arow[2];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int m = m0 + 4 * q + v, n = n0 + r;
-      if (m >= M) continue;
-      const size_t o = (size_t)m * N + n;
-      if (MODE == kMlpvNN) {
-        a.out[o] = a.add ? a.add[o] + acc[v] : acc[v];
-        continue;
-      }
-      const float z = acc[v] + a.bias[n];
-      const float y1 = fmaxf(z, 0.f);
-      if (MODE == kMlpvFwd) {
-        a.out[o] = y1;
-        continue;
-      }
-      // the loss term of y_{l+1} (already scaled by its own 1 / (B w_{l+1}))
-      // and its seed dL/dy_{l+1}
-      float sd = 0.f;
-      if (a.loss == AMBPTT_LOSS_MEAN_SQ_ALL) {
-        sd = 2.f * y1 * a.inv;
-        lterm += y1 * y1 * a.inv;
-      } else if (a.last) {
-        if (a.loss == AMBPTT_LOSS_HALF_SQ_LAST) {
-          sd = y1;
-          lterm += y1 * y1;
-        } else {
-          sd = a.inv;
-          lterm += y1 * a.inv;
-        }
-      }
-      const float yb = (a.nn_in ? a.nn_in[o] : 0.f) + sd;
-      a.zbar_out[o] = z > 0.f ? yb : 0.f;
+  for (int i = 0; i < 2; ++i) arow[i] = a.A + (size_t)min(m0 + 16 * i + r, M - 1) * K + 4 * q;  // rows >= M: clamped, discarded
+  int col[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) col[j] = min(n0 + 16 * j + r, N - 1);  // past N: clamped, discarded
+  auto ldb = [&](int k0, int j) -> f4 {
+    if (MODE == kMlpvNN) {
+      const float* w = a.W + (size_t)(k0 + 4 * q) * N + col[j];
+      return f4{w[0], w[N], w[2 * (size_t)N], w[3 * (size_t)N]};
     }
+    return *(const f4*)(a.W + (size_t)col[j] * K + k0 + 4 * q);
+  };
+  f4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+  f4 xa[2], xb[2], ya[2], yb[2];
+  if (c0 < c1) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) xa[i] = *(const f4*)(arow[i] + 16 * c0);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) xb[j] = ldb(16 * c0, j);
   }
+  for (int c = c0; c < c1; ++c) {
+    if (c + 1 < c1) {  // the next chunk's operands, in flight during this chunk's MFMAs
+#pragma unroll
+      for (int i = 0; i < 2; ++i) ya[i] = *(const f4*)(arow[i] + 16 * (c + 1));
+#pragma unroll
+      for (int j = 0; j < 2; ++j) yb[j] = ldb(16 * (c + 1), j);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma4(xa[i][k], xb[j][k], acc[i][j]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) xa[i] = ya[i];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) xb[j] = yb[j];
+  }
+  if (wave > 0) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) part[wave - 1][2 * i + j][lane] = acc[i][j];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int w = 0; w < 3; ++w)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] += part[w][2 * i + j][lane];
+
+  // accumulator element v of lane l: row 4 (l >> 4) + v, column l & 15 of its block
+  float lterm = 0.f;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      if (j == 1 && !two) continue;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int m = m0 + 16 * i + 4 * q + v, n = n0 + 16 * j + r;
+        if (m >= M) continue;
+        const size_t o = (size_t)m * N + n;
+        if (MODE == kMlpvNN) {
+          a.out[o] = a.add ? a.add[o] + acc[i][j][v] : acc[i][j][v];
+          continue;
+        }
+        const float z = acc[i][j][v] + a.bias[n];
+        const float y1 = fmaxf(z, 0.f);
+        if (MODE == kMlpvFwd) {
+          a.out[o] = y1;
+          continue;
+        }
+        // the loss term of y_{l+1} (already scaled by its own 1 / (B w_{l+1}))
+        // and its seed dL/dy_{l+1}
+        float sd = 0.f;
+        if (a.loss == AMBPTT_LOSS_MEAN_SQ_ALL) {
+          sd = 2.f * y1 * a.inv;
+          lterm += y1 * y1 * a.inv;
+        } else if (a.last) {
+          if (a.loss == AMBPTT_LOSS_HALF_SQ_LAST) {
+            sd = y1;
+            lterm += y1 * y1;
+          } else {
+            sd = a.inv;
+            lterm += y1 * a.inv;
+          }
+        }
+        const float yb1 = (a.nn_in ? a.nn_in[o] : 0.f) + sd;
+        a.zbar_out[o] = z > 0.f ? yb1 : 0.f;
+      }
+    }
   if (MODE == kMlpvAdj) {
     const float s = wave_sum(lterm);
-    if (lane == 0) red[wave] = s;
-    __syncthreads();
-    if (tid == 0)
-      a.loss_acc[blockIdx.y * gridDim.x + blockIdx.x] +=
-          (double)red[0] + (double)red[1] + (double)red[2] + (double)red[3];
+    if (lane == 0) a.loss_acc[blockIdx.y * gridDim.x + blockIdx.x] += (double)s;
   }
 }
 
