@@ -9,16 +9,19 @@
 //   product   u = zbar W  (an "NN" product: W[k][c] is contiguous in c)
 // dW_l = zbar_l^T y_l and db_l run on the weight-gradient kernels.
 //
-// One launch per step.  A workgroup owns 32 rows x 32 columns; each of its 4
-// waves computes the whole tile (2 x 2 blocks of 16 x 16) over a quarter of
-// the reduction, in chunks of 16 read straight from global memory with the
-// next chunk's operands loaded before the current chunk's 16 MFMAs, and the
-// four partial tiles are summed in wave order through LDS by wave 0, which
-// then runs the epilogue.  Lane l reads 4 consecutive k of row l & 15 at 4
-// (l >> 4) and its components feed 4 MFMAs (A and the "NT" B the same way;
-// the "NN" B as 4 reads of one column each, coalesced across the 16 lanes).
-// Widths are multiples of 16; a tile's second column block may fall past N
-// and then idles.  The loss terms of a workgroup are summed by wave 0.
+// One launch per step.  A workgroup of 16 waves owns 32 rows x 32 columns.
+// The reduction runs in chunks of 16; wave w takes chunks w, w + 16, ... in
+// groups of up to four whose loads all issue before the group's first MFMA,
+// so that a launch of a few hundred workgroups waits about one memory latency
+// per group (one in all for K <= 1024) instead of one per chunk.  Each wave computes the whole tile (2 x 2 blocks of
+// 16 x 16) over its chunks; the 16 partial tiles go to LDS and every thread
+// then sums one output over the waves in wave order (deterministic) and runs
+// the epilogue for it, 32 consecutive columns per half wave.  Lane l reads 4
+// consecutive k of row l & 15 at 4 (l >> 4) and its components feed 4 MFMAs
+// (A and the "NT" B the same way; the "NN" B as 4 reads of one column each,
+// coalesced across the 16 lanes).  Widths are multiples of 16; a tile's
+// second column block may fall past N and then idles.  The loss terms of a
+// workgroup are summed in a fixed order by its first thread.
 #include <hip/hip_runtime.h>
 
 #include "ambptt.h"
@@ -41,117 +44,122 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 enum { kMlpvFwd = 0, kMlpvAdj = 1, kMlpvNN = 2 };
 
-template <int MODE>
-__global__ __launch_bounds__(256) void mlpv_gemm(MlpvArgs a) {
-  __shared__ f4 part[3][4][64];  // waves 1..3: their four accumulators, lane by lane
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+constexpr int kVW = 16;  // waves per workgroup
+
+// ND: chunks per wave and group, all in flight at once (ceil(K / 256) up to 4).
+template <int MODE, int ND>
+__global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
+  __shared__ float part[kVW][32][36];  // partial tiles; rows of 36: the stores of a wave spread over the banks
+  __shared__ float lpart[kVW];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 15, q = lane >> 4;
   const int M = a.M, N = a.N, K = a.K;
   const int m0 = blockIdx.x * 32, n0 = blockIdx.y * 32;
-  const bool two = n0 + 16 < N;  // the second column block lies inside N
-  const int nch = K / 16, c0 = nch * wave / 4, c1 = nch * (wave + 1) / 4;
+  const int nch = K / 16;
+  const int ngrp = (nch + kVW * ND - 1) / (kVW * ND);  // groups of ND chunks per wave
   const float* arow[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) arow[i] = a.A + (size_t)min(m0 + 16 * i + r, M - 1) * K + 4 * q;  // rows >= M: clamped, discarded
   int col[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) col[j] = min(n0 + 16 * j + r, N - 1);  // past N: clamped, discarded
-  auto ldb = [&](int k0, int j) -> f4 {
-    if (MODE == kMlpvNN) {
-      const float* w = a.W + (size_t)(k0 + 4 * q) * N + col[j];
-      return f4{w[0], w[N], w[2 * (size_t)N], w[3 * (size_t)N]};
+  // chunk c of the reduction; past the last chunk the operands read the last
+  // one (and are zeroed before use), so that every wave issues the same loads
+  // in straight line
+  auto load = [&](int c, f4 (&xa)[2], f4 (&xb)[2]) {
+    const int k0 = 16 * min(c, nch - 1);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) xa[i] = *(const f4*)(arow[i] + k0);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      if (MODE == kMlpvNN) {
+        const float* w = a.W + (size_t)(k0 + 4 * q) * N + col[j];
+        xb[j] = f4{w[0], w[N], w[2 * (size_t)N], w[3 * (size_t)N]};
+      } else {
+        xb[j] = *(const f4*)(a.W + (size_t)col[j] * K + k0 + 4 * q);
+      }
     }
-    return *(const f4*)(a.W + (size_t)col[j] * K + k0 + 4 * q);
   };
   f4 acc[2][2];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
-  f4 xa[2], xb[2], ya[2], yb[2];
-  if (c0 < c1) {
+  for (int g = 0; g < ngrp; ++g) {
+    f4 xa[ND][2], xb[ND][2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) xa[i] = *(const f4*)(arow[i] + 16 * c0);
+    for (int u = 0; u < ND; ++u) load(wave + kVW * (ND * g + u), xa[u], xb[u]);
+    __builtin_amdgcn_sched_barrier(0);  // every load of the group issues before its first MFMA
 #pragma unroll
-    for (int j = 0; j < 2; ++j) xb[j] = ldb(16 * c0, j);
-  }
-  for (int c = c0; c < c1; ++c) {
-    if (c + 1 < c1) {  // the next chunk's operands, in flight during this chunk's MFMAs
+    for (int u = 0; u < ND; ++u) {
+      if (wave + kVW * (ND * g + u) >= nch) {  // uniform: a chunk past the reduction adds nothing
 #pragma unroll
-      for (int i = 0; i < 2; ++i) ya[i] = *(const f4*)(arow[i] + 16 * (c + 1));
+        for (int i = 0; i < 2; ++i) xa[u][i] = xb[u][i] = f4{0.f, 0.f, 0.f, 0.f};
+      }
 #pragma unroll
-      for (int j = 0; j < 2; ++j) yb[j] = ldb(16 * (c + 1), j);
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) acc[i][j] = mfma4(xa[u][i][k], xb[u][j][k], acc[i][j]);
     }
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma4(xa[i][k], xb[j][k], acc[i][j]);
-#pragma unroll
-    for (int i = 0; i < 2; ++i) xa[i] = ya[i];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) xb[j] = yb[j];
   }
-  if (wave > 0) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) part[wave - 1][2 * i + j][lane] = acc[i][j];
-  }
-  __syncthreads();
-  if (wave != 0) return;
-#pragma unroll
-  for (int w = 0; w < 3; ++w)
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] += part[w][2 * i + j][lane];
-
   // accumulator element v of lane l: row 4 (l >> 4) + v, column l & 15 of its block
-  float lterm = 0.f;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      if (j == 1 && !two) continue;
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int m = m0 + 16 * i + 4 * q + v, n = n0 + 16 * j + r;
-        if (m >= M) continue;
-        const size_t o = (size_t)m * N + n;
-        if (MODE == kMlpvNN) {
-          a.out[o] = a.add ? a.add[o] + acc[i][j][v] : acc[i][j][v];
-          continue;
-        }
-        const float z = acc[i][j][v] + a.bias[n];
-        const float y1 = fmaxf(z, 0.f);
-        if (MODE == kMlpvFwd) {
-          a.out[o] = y1;
-          continue;
-        }
+      for (int v = 0; v < 4; ++v) part[wave][16 * i + 4 * q + v][16 * j + r] = acc[i][j][v];
+  __syncthreads();
+
+  const int ml = tid >> 5, nl = tid & 31;
+  const int m = m0 + ml, n = n0 + nl;
+  float sum = 0.f;
+#pragma unroll
+  for (int w = 0; w < kVW; ++w) sum += part[w][ml][nl];
+  float lterm = 0.f;
+  if (m < M && n < N) {
+    const size_t o = (size_t)m * N + n;
+    if (MODE == kMlpvNN) {
+      a.out[o] = a.add ? a.add[o] + sum : sum;
+    } else {
+      const float z = sum + a.bias[n];
+      const float y1 = fmaxf(z, 0.f);
+      if (MODE == kMlpvFwd) {
+        a.out[o] = y1;
+      } else {
         // the loss term of y_{l+1} (already scaled by its own 1 / (B w_{l+1}))
         // and its seed dL/dy_{l+1}
         float sd = 0.f;
         if (a.loss == AMBPTT_LOSS_MEAN_SQ_ALL) {
           sd = 2.f * y1 * a.inv;
-          lterm += y1 * y1 * a.inv;
+          lterm = y1 * y1 * a.inv;
         } else if (a.last) {
           if (a.loss == AMBPTT_LOSS_HALF_SQ_LAST) {
             sd = y1;
-            lterm += y1 * y1;
+            lterm = y1 * y1;
           } else {
             sd = a.inv;
-            lterm += y1 * a.inv;
+            lterm = y1 * a.inv;
           }
         }
         const float yb1 = (a.nn_in ? a.nn_in[o] : 0.f) + sd;
         a.zbar_out[o] = z > 0.f ? yb1 : 0.f;
       }
     }
+  }
   if (MODE == kMlpvAdj) {
     const float s = wave_sum(lterm);
-    if (lane == 0) a.loss_acc[blockIdx.y * gridDim.x + blockIdx.x] += (double)s;
+    if (lane == 0) lpart[wave] = s;
+    __syncthreads();
+    if (tid == 0) {
+      float t = 0.f;
+#pragma unroll
+      for (int w = 0; w < kVW; ++w) t += lpart[w];
+      a.loss_acc[blockIdx.y * gridDim.x + blockIdx.x] += (double)t;
+    }
   }
 }
 
@@ -159,13 +167,22 @@ __global__ __launch_bounds__(256) void mlpv_gemm(MlpvArgs a) {
 
 int mlpv_tiles(int M, int N) { return ((M + 31) / 32) * ((N + 31) / 32); }
 
+template <int MODE>
+hipError_t launch_mlpv_nd(const MlpvArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  const dim3 grid((a.M + 31) / 32, (a.N + 31) / 32), block(64 * kVW);
+  const int per_wave = (a.K / 16 + kVW - 1) / kVW;
+  if (per_wave <= 1) hipExtLaunchKernelGGL((mlpv_gemm<MODE, 1>), grid, block, 0, s, e0, e1, 0, a);
+  else if (per_wave == 2) hipExtLaunchKernelGGL((mlpv_gemm<MODE, 2>), grid, block, 0, s, e0, e1, 0, a);
+  else if (per_wave == 3) hipExtLaunchKernelGGL((mlpv_gemm<MODE, 3>), grid, block, 0, s, e0, e1, 0, a);
+  else hipExtLaunchKernelGGL((mlpv_gemm<MODE, 4>), grid, block, 0, s, e0, e1, 0, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_mlpv(int mode, const MlpvArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (a.M < 1 || a.N < 16 || a.K < 16 || a.N % 16 || a.K % 16) return hipErrorInvalidValue;
-  const dim3 grid((a.M + 31) / 32, (a.N + 31) / 32), block(256);
-  if (mode == kForward) hipExtLaunchKernelGGL(mlpv_gemm<kMlpvFwd>, grid, block, 0, s, e0, e1, 0, a);
-  else if (mode == kAdjoint) hipExtLaunchKernelGGL(mlpv_gemm<kMlpvAdj>, grid, block, 0, s, e0, e1, 0, a);
-  else hipExtLaunchKernelGGL(mlpv_gemm<kMlpvNN>, grid, block, 0, s, e0, e1, 0, a);
-  return hipGetLastError();
+  if (mode == kForward) return launch_mlpv_nd<kMlpvFwd>(a, s, e0, e1);
+  if (mode == kAdjoint) return launch_mlpv_nd<kMlpvAdj>(a, s, e0, e1);
+  return launch_mlpv_nd<kMlpvNN>(a, s, e0, e1);
 }
 
 }  // namespace ambptt

@@ -33,8 +33,11 @@ def _case(wl):
 
 
 @pytest.mark.parametrize("shape", [dict(batch=64, hidden=256, widths=(256, 128, 64, 128)),
-                                   dict(batch=50, hidden=64, widths=(64, 16, 48, 32))],
-                         ids=["pooled", "ragged"])
+                                   dict(batch=50, hidden=64, widths=(64, 16, 48, 32)),
+                                   # reductions of 32 to 80 chunks of 16: one to five per wave,
+                                   # in one group or two, the last ones padded
+                                   dict(batch=40, hidden=1280, widths=(1280, 512, 1040, 720))],
+                         ids=["pooled", "ragged", "deep"])
 def test_mlp_of_different_widths(shape):
     wl = synth.get("mlp_widths_l2000").with_(n_steps=24, **shape)
     n, sizes = wl.n_steps, _sizes(wl)
