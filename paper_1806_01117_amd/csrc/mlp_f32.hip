@@ -18,8 +18,8 @@
 // then sums one output over the waves in wave order (deterministic) and runs
 // the epilogue for it, 32 consecutive columns per half wave.  Lane l reads 4
 // consecutive k of row l & 15 at 4 (l >> 4) and its components feed 4 MFMAs
-// (A and the "NT" B the same way; the "NN" B as 4 reads of one column each,
-// coalesced across the 16 lanes).  Widths are multiples of 16; a tile's
+// (A and the "NT" B the same way; the "NN" B is read as whole rows and turned
+// into fragments through a per-wave tile in LDS).  Widths are multiples of 16; a tile's
 // second column block may fall past N and then idles.  The loss terms of a
 // workgroup are summed in a fixed order by its first thread.
 #include <hip/hip_runtime.h>
@@ -64,6 +64,14 @@ __global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
   int col[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) col[j] = min(n0 + 16 * j + r, N - 1);  // past N: clamped, discarded
+  // NN: the B chunk (16 reduction rows x 32 columns, contiguous along the
+  // columns) is read as whole 128-byte rows, 8 lanes a row, and passes through
+  // the wave's own tile in LDS (rows of 36 floats: the column reads of a
+  // fragment fall in 64 distinct banks); xb then holds the raw rows brow and
+  // brow + 8.  The other modes read B's rows directly.
+  __shared__ __attribute__((aligned(16))) float bt[MODE == kMlpvNN ? kVW : 1][16][36];
+  const int brow = lane >> 3, bcol = 4 * (lane & 7);
+  const float* wnn = a.W + min(n0 + bcol, N - 4);  // a float4 past N: clamped, discarded
   // chunk c of the reduction; past the last chunk the operands read the last
   // one (and are zeroed before use), so that every wave issues the same loads
   // in straight line
@@ -73,13 +81,18 @@ __global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
     for (int i = 0; i < 2; ++i) xa[i] = *(const f4*)(arow[i] + k0);
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      if (MODE == kMlpvNN) {
-        const float* w = a.W + (size_t)(k0 + 4 * q) * N + col[j];
-        xb[j] = f4{w[0], w[N], w[2 * (size_t)N], w[3 * (size_t)N]};
-      } else {
-        xb[j] = *(const f4*)(a.W + (size_t)col[j] * K + k0 + 4 * q);
-      }
+      if (MODE == kMlpvNN) xb[j] = *(const f4*)(wnn + (size_t)(k0 + brow + 8 * j) * N);
+      else xb[j] = *(const f4*)(a.W + (size_t)col[j] * K + k0 + 4 * q);
     }
+  };
+  // NN: the raw rows to the B fragments (column n0 + 16 j + r, rows 4 q .. 4 q + 3)
+  auto nn_frag = [&](f4 (&xb)[2]) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) *(f4*)&bt[wave][brow + 8 * h][bcol] = xb[h];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      xb[j] = f4{bt[wave][4 * q][16 * j + r], bt[wave][4 * q + 1][16 * j + r], bt[wave][4 * q + 2][16 * j + r],
+                 bt[wave][4 * q + 3][16 * j + r]};
   };
   f4 acc[2][2];
 #pragma unroll
@@ -93,6 +106,7 @@ __global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
     __builtin_amdgcn_sched_barrier(0);  // every load of the group issues before its first MFMA
 #pragma unroll
     for (int u = 0; u < ND; ++u) {
+      if (MODE == kMlpvNN) nn_frag(xb[u]);
       if (wave + kVW * (ND * g + u) >= nch) {  // uniform: a chunk past the reduction adds nothing
 #pragma unroll
         for (int i = 0; i < 2; ++i) xa[u][i] = xb[u][i] = f4{0.f, 0.f, 0.f, 0.f};
@@ -103,6 +117,12 @@ __global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
         for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int j = 0; j < 2; ++j) acc[i][j] = mfma4(xa[u][i][k], xb[u][j][k], acc[i][j]);
+      if (MODE == kMlpvAdj && blockIdx.y == 0 && a.ywin_out) {  // y_l beside zbar_l for dW_l
+        const int c = wave + kVW * (ND * g + u);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          if (c < nch && m0 + 16 * i + r < M) *(f4*)(a.ywin_out + (size_t)(m0 + 16 * i + r) * K + 16 * c + 4 * q) = xa[u][i];
+      }
     }
   }
   // accumulator element v of lane l: row 4 (l >> 4) + v, column l & 15 of its block
@@ -163,7 +183,116 @@ __global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
   }
 }
 
+// dW_l[n][c] = sum_m zbar_l[m][n] y_l[m][c] and db_l[n] = sum_m zbar_l[m][n]
+// over the R = B rows of the layer.  The same 16-wave layout: a 32 x 32 tile
+// of dW_l, the rows m in chunks of 16 spread over the waves (up to ND in
+// flight), partial tiles summed in wave order through LDS.  Both operands are
+// read along m, so a lane reads its 4 rows of one column as 4 words,
+// coalesced across the 16 lanes of a quarter wave; rows past R read row R - 1
+// and are zeroed.  The first column of workgroups also sums db.
+template <int ND>
+__global__ __launch_bounds__(64 * kVW) void mlpv_dw(DwArgs a) {
+  __shared__ float part[kVW][32][33];
+  __shared__ float bpart[kVW][4][32];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 15, q = lane >> 4;
+  const int NW = a.GH, CW = a.H, R = a.R;
+  const float* Z = (const float*)a.zbar;
+  const float* Y = (const float*)a.hwin;
+  const int n0 = blockIdx.x * 32, c0 = blockIdx.y * 32;
+  const int nch = (R + 15) / 16;
+  const int ngrp = (nch + kVW * ND - 1) / (kVW * ND);
+  int zc[2], yc[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    zc[i] = min(n0 + 16 * i + r, NW - 1);  // past the tile's edge: clamped, discarded
+    yc[i] = min(c0 + 16 * i + r, CW - 1);
+  }
+  f4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+  float bs[2] = {0.f, 0.f};
+  for (int g = 0; g < ngrp; ++g) {
+    f4 xa[ND][2], xb[ND][2];
+#pragma unroll
+    for (int u = 0; u < ND; ++u) {
+      const int mb = 16 * min(wave + kVW * (ND * g + u), nch - 1) + 4 * q;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const size_t m = (size_t)min(mb + k, R - 1);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          xa[u][i][k] = Z[m * NW + zc[i]];
+          xb[u][i][k] = Y[m * CW + yc[i]];
+        }
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);  // every load of the group issues before its first MFMA
+#pragma unroll
+    for (int u = 0; u < ND; ++u) {
+      const int c = wave + kVW * (ND * g + u);
+      const int mb = 16 * c + 4 * q;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const bool ok = c < nch && mb + k < R;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          xa[u][i][k] = ok ? xa[u][i][k] : 0.f;
+          xb[u][i][k] = ok ? xb[u][i][k] : 0.f;
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          bs[i] += xa[u][i][k];
+#pragma unroll
+          for (int j = 0; j < 2; ++j) acc[i][j] = mfma4(xa[u][i][k], xb[u][j][k], acc[i][j]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    bpart[wave][q][16 * i + r] = bs[i];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) part[wave][16 * i + 4 * q + v][16 * j + r] = acc[i][j][v];
+  }
+  __syncthreads();
+  const int nl = tid >> 5, cl = tid & 31;
+  const int n = n0 + nl, c = c0 + cl;
+  float sum = 0.f;
+#pragma unroll
+  for (int w = 0; w < kVW; ++w) sum += part[w][nl][cl];
+  if (n < NW && c < CW) {
+    float* o = a.dW + (size_t)n * CW + c;
+    *o = a.accumulate ? *o + sum : sum;
+  }
+  if (blockIdx.y == 0 && tid < 32 && n0 + tid < NW) {
+    float b = 0.f;
+#pragma unroll
+    for (int w = 0; w < kVW; ++w)
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq) b += bpart[w][qq][tid];
+    float* o = a.db + n0 + tid;
+    *o = a.accumulate ? *o + b : b;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_mlpv_dw(const DwArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (a.R < 1 || a.H < 1 || a.GH < 1 || a.D != 0) return hipErrorInvalidValue;
+  const dim3 grid((a.GH + 31) / 32, (a.H + 31) / 32), block(64 * kVW);
+  if ((a.R + 15) / 16 <= kVW) hipExtLaunchKernelGGL(mlpv_dw<1>, grid, block, 0, s, e0, e1, 0, a);
+  else hipExtLaunchKernelGGL(mlpv_dw<2>, grid, block, 0, s, e0, e1, 0, a);
+  return hipGetLastError();
+}
 
 int mlpv_tiles(int M, int N) { return ((M + 31) / 32) * ((N + 31) / 32); }
 

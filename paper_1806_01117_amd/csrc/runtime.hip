@@ -778,6 +778,7 @@ struct Exec {
       MlpvArgs a = mlpv_args(t);
       a.A = (const float*)cur;
       a.zbar_out = (float*)zbar_at(t);
+      a.ywin_out = (float*)hwin_at(t);  // y_t beside zbar_t for the layer's weight gradient
       a.loss_acc = (double*)(C->ws + L.off_loss);
       if (!first) {  // u = zbar_{t+1} W_{t+1}: N = w_{t+1}, K = w_{t+2}
         MlpvArgs u = mlpv_args(t + 1);
@@ -791,9 +792,6 @@ struct Exec {
       }
       s = timed(AMBPTT_K_ADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch_mlpv(kAdjoint, a, C->cs, e0, e1); });
       if (s != AMBPTT_OK) return s;
-      // y_t beside zbar_t for the layer's weight gradient
-      HIPCK(hipMemcpyAsync(hwin_at(t), cur, size_t(p.batch) * size_t(C->widths[size_t(t)]) * 4,
-                           hipMemcpyDeviceToDevice, C->cs));
     } else if (L.mlp) {
       MlpArgs a = mlp_args(t);
       a.y = cur;
@@ -881,7 +879,8 @@ struct Exec {
       s = timed(
           AMBPTT_K_DW,
           [&](hipEvent_t e0, hipEvent_t e1) {
-            return p.dtype == AMBPTT_BF16 ? launch_dw_bf16(d, ws, e0, e1) : launch_dw(d, ws, e0, e1);
+            return L.mlpv ? launch_mlpv_dw(d, ws, e0, e1)
+                          : p.dtype == AMBPTT_BF16 ? launch_dw_bf16(d, ws, e0, e1) : launch_dw(d, ws, e0, e1);
           },
           ws);
       if (s != AMBPTT_OK) return s;
