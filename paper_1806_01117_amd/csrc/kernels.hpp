@@ -101,8 +101,10 @@ struct MlpvArgs {
   const float* nn_in;  // adjoint: zbar_{l+1} W_{l+1} [M][N], NULL for the last layer
   float* zbar_out;
   float* ywin_out;     // adjoint: a copy of A (y_l) for the weight gradient, NULL for none
+  const float* A2;     // adjoint in one launch: zbar_{l+1} [M][K2], NULL: nn_in (or nothing) instead
+  const float* W2;     // W_{l+1} [K2][N]
   double* loss_acc;
-  int M, N, K;
+  int M, N, K, K2;
   int loss, last;
   float inv;
 };

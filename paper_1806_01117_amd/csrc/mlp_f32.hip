@@ -9,20 +9,15 @@
 //   product   u = zbar W  (an "NN" product: W[k][c] is contiguous in c)
 // dW_l = zbar_l^T y_l and db_l run on the weight-gradient kernels.
 //
-// One launch per step.  A workgroup of 16 waves owns 32 rows x 32 columns.
-// The reduction runs in chunks of 16; wave w takes chunks w, w + 16, ... in
-// groups of up to four whose loads all issue before the group's first MFMA,
-// so that a launch of a few hundred workgroups waits about one memory latency
-// per group (one in all for K <= 1024) instead of one per chunk.  Each wave computes the whole tile (2 x 2 blocks of
-// 16 x 16) over its chunks; the 16 partial tiles go to LDS and every thread
-// then sums one output over the waves in wave order (deterministic) and runs
-// the epilogue for it, 32 consecutive columns per half wave.  Lane l reads 4
-// consecutive k of row l & 15 at 4 (l >> 4) and its components feed 4 MFMAs
-// (A and the "NT" B the same way; the "NN" B is read as whole rows and turned
-// into fragments through a per-wave tile in LDS).  Widths are multiples of 16; a tile's
+// One launch per step: the forward, the NN product alone (dL/dy_0), and the
+// adjoint, which also forms u for its own tile.  A workgroup of 16 waves owns
+// 32 x 32 outputs, its waves split the reduction, and the partial tiles meet
+// in LDS in wave order (deterministic).  Widths are multiples of 16; a tile's
 // second column block may fall past N and then idles.  The loss terms of a
 // workgroup are summed in a fixed order by its first thread.
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 
 #include "ambptt.h"
 #include "kernels.hpp"
@@ -42,59 +37,41 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-enum { kMlpvFwd = 0, kMlpvAdj = 1, kMlpvNN = 2 };
+enum { kMlpvFwd = 0, kMlpvAdj = 1, kMlpvNN = 2, kMlpvAdjU = 3 };
 
 constexpr int kVW = 16;  // waves per workgroup
 
-// ND: chunks per wave and group, all in flight at once (ceil(K / 256) up to 4).
-template <int MODE, int ND>
-__global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
-  __shared__ float part[kVW][32][36];  // partial tiles; rows of 36: the stores of a wave spread over the banks
-  __shared__ float lpart[kVW];
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int r = lane & 15, q = lane >> 4;
-  const int M = a.M, N = a.N, K = a.K;
-  const int m0 = blockIdx.x * 32, n0 = blockIdx.y * 32;
+struct MlpvTile {
+  int tid, lane, wave, r, q, m0, n0;
+};
+
+// acc[i][j] += the wave's share of A[m0 + 16 i ..][:] . B[:][n0 + 16 j ..] for
+// A [M][K] row-major and B = W^T (NT: W [N][K]) or B = W (NN: W [K][N]).
+// Wave w takes chunks w, w + 16, ... of 16 reduction indices in groups of ND
+// whose loads all issue before the group's first MFMA; past the last chunk
+// the operands read the last one and are zeroed before use, so every wave
+// issues the same loads in straight line.  Lane l reads 4 consecutive k of
+// row l & 15 at 4 (l >> 4) and its components feed 4 MFMAs (A and the NT B
+// the same way).  The NN B chunk (16 reduction rows x 32 columns) is read as
+// whole 128-byte rows, 8 lanes a row, and turned into fragments through the
+// wave's own tile bt in LDS (rows of 36 floats: the column reads of a
+// fragment fall in 64 distinct banks).  With ywin, the first column of
+// workgroups also writes a copy of its A rows there.
+template <bool NN, int ND>
+__device__ __forceinline__ void tile_product(const MlpvTile& t, const float* __restrict__ A,
+                                             const float* __restrict__ W, int M, int N, int K, float (&bt)[16][36],
+                                             float* ywin, f4 (&acc)[2][2]) {
+  const int r = t.r, q = t.q, wave = t.wave;
   const int nch = K / 16;
   const int ngrp = (nch + kVW * ND - 1) / (kVW * ND);  // groups of ND chunks per wave
   const float* arow[2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) arow[i] = a.A + (size_t)min(m0 + 16 * i + r, M - 1) * K + 4 * q;  // rows >= M: clamped, discarded
-  int col[2];
+  for (int i = 0; i < 2; ++i) arow[i] = A + (size_t)min(t.m0 + 16 * i + r, M - 1) * K + 4 * q;  // rows >= M: clamped, discarded
+  const float* brow[2];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) col[j] = min(n0 + 16 * j + r, N - 1);  // past N: clamped, discarded
-  // NN: the B chunk (16 reduction rows x 32 columns, contiguous along the
-  // columns) is read as whole 128-byte rows, 8 lanes a row, and passes through
-  // the wave's own tile in LDS (rows of 36 floats: the column reads of a
-  // fragment fall in 64 distinct banks); xb then holds the raw rows brow and
-  // brow + 8.  The other modes read B's rows directly.
-  __shared__ __attribute__((aligned(16))) float bt[MODE == kMlpvNN ? kVW : 1][16][36];
-  const int brow = lane >> 3, bcol = 4 * (lane & 7);
-  const float* wnn = a.W + min(n0 + bcol, N - 4);  // a float4 past N: clamped, discarded
-  // chunk c of the reduction; past the last chunk the operands read the last
-  // one (and are zeroed before use), so that every wave issues the same loads
-  // in straight line
-  auto load = [&](int c, f4 (&xa)[2], f4 (&xb)[2]) {
-    const int k0 = 16 * min(c, nch - 1);
-#pragma unroll
-    for (int i = 0; i < 2; ++i) xa[i] = *(const f4*)(arow[i] + k0);
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      if (MODE == kMlpvNN) xb[j] = *(const f4*)(wnn + (size_t)(k0 + brow + 8 * j) * N);
-      else xb[j] = *(const f4*)(a.W + (size_t)col[j] * K + k0 + 4 * q);
-    }
-  };
-  // NN: the raw rows to the B fragments (column n0 + 16 j + r, rows 4 q .. 4 q + 3)
-  auto nn_frag = [&](f4 (&xb)[2]) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) *(f4*)&bt[wave][brow + 8 * h][bcol] = xb[h];
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-      xb[j] = f4{bt[wave][4 * q][16 * j + r], bt[wave][4 * q + 1][16 * j + r], bt[wave][4 * q + 2][16 * j + r],
-                 bt[wave][4 * q + 3][16 * j + r]};
-  };
-  f4 acc[2][2];
+  for (int j = 0; j < 2; ++j) brow[j] = W + (size_t)min(t.n0 + 16 * j + r, N - 1) * K + 4 * q;  // NT; past N: clamped, discarded
+  const int nrow = t.lane >> 3, ncol = 4 * (t.lane & 7);
+  const float* wnn = W + min(t.n0 + ncol, N - 4);  // NN: a float4 past N: clamped, discarded
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -102,12 +79,26 @@ __global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
   for (int g = 0; g < ngrp; ++g) {
     f4 xa[ND][2], xb[ND][2];
 #pragma unroll
-    for (int u = 0; u < ND; ++u) load(wave + kVW * (ND * g + u), xa[u], xb[u]);
+    for (int u = 0; u < ND; ++u) {
+      const int k0 = 16 * min(wave + kVW * (ND * g + u), nch - 1);
+#pragma unroll
+      for (int i = 0; i < 2; ++i) xa[u][i] = *(const f4*)(arow[i] + k0);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        xb[u][j] = NN ? *(const f4*)(wnn + (size_t)(k0 + nrow + 8 * j) * N) : *(const f4*)(brow[j] + k0);
+    }
     __builtin_amdgcn_sched_barrier(0);  // every load of the group issues before its first MFMA
 #pragma unroll
     for (int u = 0; u < ND; ++u) {
-      if (MODE == kMlpvNN) nn_frag(xb[u]);
-      if (wave + kVW * (ND * g + u) >= nch) {  // uniform: a chunk past the reduction adds nothing
+      const int c = wave + kVW * (ND * g + u);
+      if (NN) {  // raw rows nrow, nrow + 8 -> fragments of columns n0 + 16 j + r, rows 4 q .. 4 q + 3
+#pragma unroll
+        for (int h = 0; h < 2; ++h) *(f4*)&bt[nrow + 8 * h][ncol] = xb[u][h];
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          xb[u][j] = f4{bt[4 * q][16 * j + r], bt[4 * q + 1][16 * j + r], bt[4 * q + 2][16 * j + r], bt[4 * q + 3][16 * j + r]};
+      }
+      if (c >= nch) {  // uniform: a chunk past the reduction adds nothing
 #pragma unroll
         for (int i = 0; i < 2; ++i) xa[u][i] = xb[u][i] = f4{0.f, 0.f, 0.f, 0.f};
       }
@@ -117,28 +108,66 @@ __global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
         for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int j = 0; j < 2; ++j) acc[i][j] = mfma4(xa[u][i][k], xb[u][j][k], acc[i][j]);
-      if (MODE == kMlpvAdj && blockIdx.y == 0 && a.ywin_out) {  // y_l beside zbar_l for dW_l
-        const int c = wave + kVW * (ND * g + u);
+      if (ywin && blockIdx.y == 0) {
 #pragma unroll
         for (int i = 0; i < 2; ++i)
-          if (c < nch && m0 + 16 * i + r < M) *(f4*)(a.ywin_out + (size_t)(m0 + 16 * i + r) * K + 16 * c + 4 * q) = xa[u][i];
+          if (c < nch && t.m0 + 16 * i + r < M) *(f4*)(ywin + (size_t)(t.m0 + 16 * i + r) * K + 16 * c + 4 * q) = xa[u][i];
       }
     }
   }
-  // accumulator element v of lane l: row 4 (l >> 4) + v, column l & 15 of its block
+}
+
+// The 16 waves' partial tiles summed in wave order: thread tid gets element
+// (tid >> 5, tid & 31) of the 32 x 32 tile.  Accumulator element v of lane l
+// is row 4 (l >> 4) + v, column l & 15 of its 16 x 16 block.
+__device__ __forceinline__ float tile_sum(const MlpvTile& t, float (&part)[kVW][32][36], const f4 (&acc)[2][2]) {
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) part[wave][16 * i + 4 * q + v][16 * j + r] = acc[i][j][v];
+      for (int v = 0; v < 4; ++v) part[t.wave][16 * i + 4 * t.q + v][16 * j + t.r] = acc[i][j][v];
   __syncthreads();
-
-  const int ml = tid >> 5, nl = tid & 31;
-  const int m = m0 + ml, n = n0 + nl;
   float sum = 0.f;
 #pragma unroll
-  for (int w = 0; w < kVW; ++w) sum += part[w][ml][nl];
+  for (int w = 0; w < kVW; ++w) sum += part[w][t.tid >> 5][t.tid & 31];
+  return sum;
+}
+
+// One launch per step.  A workgroup of 16 waves owns 32 rows x 32 columns of
+// the step's output; all threads run the epilogue, 32 consecutive columns
+// per half wave.  kMlpvAdjU runs the adjoint's two products in one launch:
+// first u = zbar_{l+1} W_{l+1} (NN, reduction over w_{l+2}, with ND2), then
+// z_l (NT, with ND), the LDS tiles reused in between.  Its u is summed in
+// the same order as the NN launch's.
+template <int MODE, int ND, int ND2>
+__global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
+  __shared__ float part[kVW][32][36];  // partial tiles; rows of 36: the stores of a wave spread over the banks
+  __shared__ __attribute__((aligned(16))) float bt[(MODE == kMlpvNN || MODE == kMlpvAdjU) ? kVW : 1][16][36];
+  __shared__ float lpart[kVW];
+  MlpvTile t;
+  t.tid = threadIdx.x;
+  t.lane = t.tid & 63;
+  t.wave = __builtin_amdgcn_readfirstlane(t.tid >> 6);
+  t.r = t.lane & 15;
+  t.q = t.lane >> 4;
+  t.m0 = blockIdx.x * 32;
+  t.n0 = blockIdx.y * 32;
+  const int M = a.M, N = a.N;
+  const bool adj = MODE == kMlpvAdj || MODE == kMlpvAdjU;
+  float u = 0.f;
+  if (MODE == kMlpvAdjU) {
+    f4 acc2[2][2];
+    tile_product<true, ND2>(t, a.A2, a.W2, M, N, a.K2, bt[t.wave], nullptr, acc2);
+    u = tile_sum(t, part, acc2);
+    __syncthreads();  // part is written again below
+  }
+  f4 acc[2][2];
+  tile_product<MODE == kMlpvNN, ND>(t, a.A, a.W, M, N, a.K, bt[MODE == kMlpvNN ? t.wave : 0], adj ? a.ywin_out : nullptr,
+                                    acc);
+  const float sum = tile_sum(t, part, acc);
+
+  const int m = t.m0 + (t.tid >> 5), n = t.n0 + (t.tid & 31);
   float lterm = 0.f;
   if (m < M && n < N) {
     const size_t o = (size_t)m * N + n;
@@ -165,20 +194,20 @@ __global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
             lterm = y1 * a.inv;
           }
         }
-        const float yb1 = (a.nn_in ? a.nn_in[o] : 0.f) + sd;
+        const float yb1 = (MODE == kMlpvAdjU ? u : a.nn_in ? a.nn_in[o] : 0.f) + sd;
         a.zbar_out[o] = z > 0.f ? yb1 : 0.f;
       }
     }
   }
-  if (MODE == kMlpvAdj) {
+  if (adj) {
     const float s = wave_sum(lterm);
-    if (lane == 0) lpart[wave] = s;
+    if (t.lane == 0) lpart[t.wave] = s;
     __syncthreads();
-    if (tid == 0) {
-      float t = 0.f;
+    if (t.tid == 0) {
+      float tot = 0.f;
 #pragma unroll
-      for (int w = 0; w < kVW; ++w) t += lpart[w];
-      a.loss_acc[blockIdx.y * gridDim.x + blockIdx.x] += (double)t;
+      for (int w = 0; w < kVW; ++w) tot += lpart[w];
+      a.loss_acc[blockIdx.y * gridDim.x + blockIdx.x] += (double)tot;
     }
   }
 }
@@ -296,22 +325,33 @@ hipError_t launch_mlpv_dw(const DwArgs& a, hipStream_t s, hipEvent_t e0, hipEven
 
 int mlpv_tiles(int M, int N) { return ((M + 31) / 32) * ((N + 31) / 32); }
 
-template <int MODE>
-hipError_t launch_mlpv_nd(const MlpvArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+// chunks of 16 per wave in flight: ceil(K / 256), up to 4 (longer reductions loop)
+static int mlpv_nd(int K) { return std::min(4, std::max(1, (K / 16 + kVW - 1) / kVW)); }
+
+template <int MODE, int ND2>
+static hipError_t launch_mlpv_nd(const MlpvArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const dim3 grid((a.M + 31) / 32, (a.N + 31) / 32), block(64 * kVW);
-  const int per_wave = (a.K / 16 + kVW - 1) / kVW;
-  if (per_wave <= 1) hipExtLaunchKernelGGL((mlpv_gemm<MODE, 1>), grid, block, 0, s, e0, e1, 0, a);
-  else if (per_wave == 2) hipExtLaunchKernelGGL((mlpv_gemm<MODE, 2>), grid, block, 0, s, e0, e1, 0, a);
-  else if (per_wave == 3) hipExtLaunchKernelGGL((mlpv_gemm<MODE, 3>), grid, block, 0, s, e0, e1, 0, a);
-  else hipExtLaunchKernelGGL((mlpv_gemm<MODE, 4>), grid, block, 0, s, e0, e1, 0, a);
+  switch (mlpv_nd(a.K)) {
+    case 1: hipExtLaunchKernelGGL((mlpv_gemm<MODE, 1, ND2>), grid, block, 0, s, e0, e1, 0, a); break;
+    case 2: hipExtLaunchKernelGGL((mlpv_gemm<MODE, 2, ND2>), grid, block, 0, s, e0, e1, 0, a); break;
+    case 3: hipExtLaunchKernelGGL((mlpv_gemm<MODE, 3, ND2>), grid, block, 0, s, e0, e1, 0, a); break;
+    default: hipExtLaunchKernelGGL((mlpv_gemm<MODE, 4, ND2>), grid, block, 0, s, e0, e1, 0, a); break;
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_mlpv(int mode, const MlpvArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (a.M < 1 || a.N < 16 || a.K < 16 || a.N % 16 || a.K % 16) return hipErrorInvalidValue;
-  if (mode == kForward) return launch_mlpv_nd<kMlpvFwd>(a, s, e0, e1);
-  if (mode == kAdjoint) return launch_mlpv_nd<kMlpvAdj>(a, s, e0, e1);
-  return launch_mlpv_nd<kMlpvNN>(a, s, e0, e1);
+  if (mode == kForward) return launch_mlpv_nd<kMlpvFwd, 1>(a, s, e0, e1);
+  if (mode == kFinal) return launch_mlpv_nd<kMlpvNN, 1>(a, s, e0, e1);
+  if (!a.A2) return launch_mlpv_nd<kMlpvAdj, 1>(a, s, e0, e1);
+  if (a.K2 < 16 || a.K2 % 16 || !a.W2 || a.nn_in) return hipErrorInvalidValue;
+  switch (mlpv_nd(a.K2)) {
+    case 1: return launch_mlpv_nd<kMlpvAdjU, 1>(a, s, e0, e1);
+    case 2: return launch_mlpv_nd<kMlpvAdjU, 2>(a, s, e0, e1);
+    case 3: return launch_mlpv_nd<kMlpvAdjU, 3>(a, s, e0, e1);
+    default: return launch_mlpv_nd<kMlpvAdjU, 4>(a, s, e0, e1);
+  }
 }
 
 }  // namespace ambptt

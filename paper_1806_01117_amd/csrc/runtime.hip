@@ -780,15 +780,10 @@ struct Exec {
       a.zbar_out = (float*)zbar_at(t);
       a.ywin_out = (float*)hwin_at(t);  // y_t beside zbar_t for the layer's weight gradient
       a.loss_acc = (double*)(C->ws + L.off_loss);
-      if (!first) {  // u = zbar_{t+1} W_{t+1}: N = w_{t+1}, K = w_{t+2}
-        MlpvArgs u = mlpv_args(t + 1);
-        u.A = (const float*)zbar_at(t + 1);
-        u.out = hbuf;
-        u.N = C->widths[size_t(t) + 1];
-        u.K = C->widths[size_t(t) + 2];
-        s = timed(AMBPTT_K_HADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch_mlpv(kFinal, u, C->cs, e0, e1); });
-        if (s != AMBPTT_OK) return s;
-        a.nn_in = hbuf;
+      if (!first) {  // u = zbar_{t+1} W_{t+1} in the same launch: N = w_{t+1}, K2 = w_{t+2}
+        a.A2 = (const float*)zbar_at(t + 1);
+        a.W2 = (const float*)W + C->woff[size_t(t) + 1];
+        a.K2 = C->widths[size_t(t) + 2];
       }
       s = timed(AMBPTT_K_ADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch_mlpv(kAdjoint, a, C->cs, e0, e1); });
       if (s != AMBPTT_OK) return s;
