@@ -212,9 +212,11 @@ hipError_t launch_dw_bf16(const DwArgs& a, hipStream_t s, hipEvent_t e0 = nullpt
 // and the launch (mode kForward, kAdjoint, or kFinal for the NN product).
 int mlpv_tiles(int M, int N);
 hipError_t launch_mlpv(int mode, const MlpvArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
-// dW_l = zbar_l^T y_l [w_{l+1}][w_l] and db_l, written (accumulate 0) or added:
+// The weight gradients of up to kMlpvDwGroup layers in one launch: member i
+// is dW = zbar^T y [GH][H] and db, written (accumulate 0) or added, with
 // zbar = DwArgs::zbar [R][GH], y = DwArgs::hwin [R][H].
-hipError_t launch_mlpv_dw(const DwArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+constexpr int kMlpvDwGroup = 8;
+hipError_t launch_mlpv_dw(const DwArgs* a, int count, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_transpose_wh_bf16(const void* W, void* WhT, int GH, int D, int H, hipStream_t s);
 // WhT[j][k] = W[k][D + j] with rows of ld >= GH floats
 hipError_t launch_transpose_wh(const float* W, float* WhT, int GH, int D, int H, int ld, hipStream_t s);

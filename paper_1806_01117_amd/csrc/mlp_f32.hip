@@ -212,17 +212,25 @@ __global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
   }
 }
 
+struct MlpvDwGroup {
+  DwArgs g[kMlpvDwGroup];
+};
+
 // dW_l[n][c] = sum_m zbar_l[m][n] y_l[m][c] and db_l[n] = sum_m zbar_l[m][n]
-// over the R = B rows of the layer.  The same 16-wave layout: a 32 x 32 tile
-// of dW_l, the rows m in chunks of 16 spread over the waves (up to ND in
-// flight), partial tiles summed in wave order through LDS.  Both operands are
-// read along m, so a lane reads its 4 rows of one column as 4 words,
-// coalesced across the 16 lanes of a quarter wave; rows past R read row R - 1
-// and are zeroed.  The first column of workgroups also sums db.
+// over the R = B rows of the layer, for the layers of a window in one launch
+// (blockIdx.z: the member; tiles past its own dW return at once).  The same
+// 16-wave layout: a 32 x 32 tile of dW_l, the rows m in chunks of 16 spread
+// over the waves (up to ND in flight), partial tiles summed in wave order
+// through LDS.  Both operands are read along m, so a lane reads its 4 rows of
+// one column as 4 words, coalesced across the 16 lanes of a quarter wave;
+// rows past R read row R - 1 and are zeroed.  The first column of workgroups
+// also sums db.
 template <int ND>
-__global__ __launch_bounds__(64 * kVW) void mlpv_dw(DwArgs a) {
+__global__ __launch_bounds__(64 * kVW) void mlpv_dw(MlpvDwGroup grp) {
   __shared__ float part[kVW][32][33];
   __shared__ float bpart[kVW][4][32];
+  const DwArgs& a = grp.g[blockIdx.z];
+  if (int(blockIdx.x) * 32 >= a.GH || int(blockIdx.y) * 32 >= a.H) return;  // the whole workgroup, before any barrier
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 15, q = lane >> 4;
@@ -315,11 +323,20 @@ __global__ __launch_bounds__(64 * kVW) void mlpv_dw(DwArgs a) {
 
 }  // namespace
 
-hipError_t launch_mlpv_dw(const DwArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  if (a.R < 1 || a.H < 1 || a.GH < 1 || a.D != 0) return hipErrorInvalidValue;
-  const dim3 grid((a.GH + 31) / 32, (a.H + 31) / 32), block(64 * kVW);
-  if ((a.R + 15) / 16 <= kVW) hipExtLaunchKernelGGL(mlpv_dw<1>, grid, block, 0, s, e0, e1, 0, a);
-  else hipExtLaunchKernelGGL(mlpv_dw<2>, grid, block, 0, s, e0, e1, 0, a);
+hipError_t launch_mlpv_dw(const DwArgs* a, int count, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (count < 1 || count > kMlpvDwGroup) return hipErrorInvalidValue;
+  MlpvDwGroup grp{};
+  int tx = 0, ty = 0;
+  for (int i = 0; i < count; ++i) {
+    const DwArgs& d = a[i];
+    if (d.R < 1 || d.H < 1 || d.GH < 1 || d.D != 0 || d.R != a[0].R) return hipErrorInvalidValue;
+    grp.g[i] = d;
+    tx = std::max(tx, (d.GH + 31) / 32);
+    ty = std::max(ty, (d.H + 31) / 32);
+  }
+  const dim3 grid(tx, ty, count), block(64 * kVW);
+  if ((a[0].R + 15) / 16 <= kVW) hipExtLaunchKernelGGL(mlpv_dw<1>, grid, block, 0, s, e0, e1, 0, grp);
+  else hipExtLaunchKernelGGL(mlpv_dw<2>, grid, block, 0, s, e0, e1, 0, grp);
   return hipGetLastError();
 }
 

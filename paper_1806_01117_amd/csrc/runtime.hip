@@ -125,7 +125,10 @@ ambptt_status validate(const ambptt_problem* p) {
 }
 
 int auto_window(const ambptt_problem* p) {
-  if (p->cell == AMBPTT_CELL_RESMLP || p->cell == AMBPTT_CELL_MLP) return 1;  // every layer has its own dW
+  if (p->cell == AMBPTT_CELL_RESMLP) return 1;  // every layer has its own dW
+  // every layer has its own dW; a window's layers go in one grouped launch,
+  // which saves the host the cost of a stream handoff per layer
+  if (p->cell == AMBPTT_CELL_MLP) return kMlpvDwGroup;
   // rows per window: each window reads and writes dW (fp32) once, so a window
   // must hold enough rows for its products to outweigh that; the bf16 path's
   // dW is large against its operands (4 bytes per weight against 2 bytes per
@@ -854,12 +857,20 @@ struct Exec {
         d.db = db + (size_t)t * p.hidden;
         d.accumulate = 0;
       }
-      if (L.mlpv) {  // layer t's own gradient [w_{t+1}][w_t], written once
-        d.dW = dW + C->woff[size_t(t)];
-        d.db = db + C->boff[size_t(t)];
-        d.H = C->widths[size_t(t)];
-        d.GH = C->widths[size_t(t) + 1];
-        d.accumulate = 0;
+      DwArgs grp[kMlpvDwGroup];
+      if (L.mlpv) {  // each layer's own gradient [w_{t+i+1}][w_{t+i}], written once
+        for (int64_t i = 0; i < cnt; ++i) {
+          DwArgs& g = grp[i];
+          g = DwArgs{};
+          g.zbar = zbar_at(t + i);
+          g.hwin = hwin_at(t + i);
+          g.dW = dW + C->woff[size_t(t + i)];
+          g.db = db + C->boff[size_t(t + i)];
+          g.R = p.batch;
+          g.H = C->widths[size_t(t + i)];
+          g.GH = C->widths[size_t(t + i) + 1];
+          g.accumulate = 0;
+        }
       }
       // the wide-batch bf16 kernels and the large-batch fp32 kernels each fill
       // the device: beside them a window only competes for the same units, so
@@ -874,7 +885,7 @@ struct Exec {
       s = timed(
           AMBPTT_K_DW,
           [&](hipEvent_t e0, hipEvent_t e1) {
-            return L.mlpv ? launch_mlpv_dw(d, ws, e0, e1)
+            return L.mlpv ? launch_mlpv_dw(grp, int(cnt), ws, e0, e1)
                           : p.dtype == AMBPTT_BF16 ? launch_dw_bf16(d, ws, e0, e1) : launch_dw(d, ws, e0, e1);
           },
           ws);
