@@ -115,25 +115,25 @@ def mlp_layer_work(ws, B: int) -> tuple[dict, dict]:
     """Algorithmic flops and HBM bytes of one launch of each kernel class of
     the MLP of layers of different widths, averaged over its layers (fp32):
     forward y_{l+1} = relu(y_l W_l^T + b_l); adjoint z-bar_l from the
-    recomputed z_l, the NN product's sum and the seed; the NN product
-    z-bar_{l+1} W_{l+1}; the weight gradient of one layer."""
+    recomputed z_l, the seed and u = z-bar_{l+1} W_{l+1}, formed in the same
+    launch (no u for the last layer), with the copy of y_l kept for the
+    weight gradient; the weight gradient of one layer."""
     n = len(ws) - 1
-    f = {"fwd": 0.0, "adj": 0.0, "hadj": 0.0, "dw": 0.0}
+    f = {"fwd": 0.0, "adj": 0.0, "dw": 0.0}
     b = dict(f)
     for l in range(n):
         a, c = ws[l], ws[l + 1]
         f["fwd"] += 2.0 * B * a * c
         b["fwd"] += 4.0 * (c * a + c + B * a + B * c)             # W_l, b_l, y_l in; y_{l+1} out
         f["adj"] += 2.0 * B * a * c
-        b["adj"] += 4.0 * (c * a + c + B * a + B * c + B * c)     # ... and the NN product's sum in; z-bar_l out
-        f["dw"] += 2.0 * B * c * (a + 1)
-        b["dw"] += 4.0 * (B * c + B * a + c * a + c)              # z-bar_l, y_l in; dW_l, db_l written once
+        b["adj"] += 4.0 * (c * a + c + B * a + B * c + B * a)     # W_l, b_l, y_l in; z-bar_l and the copy of y_l out
         if l + 1 < n:
             d = ws[l + 2]
-            f["hadj"] += 2.0 * B * c * d
-            b["hadj"] += 4.0 * (B * d + d * c + B * c)            # z-bar_{l+1}, W_{l+1} in; the product out
-    cnt = {"fwd": n, "adj": n, "dw": n, "hadj": max(1, n - 1)}
-    return {k: v / cnt[k] for k, v in f.items()}, {k: v / cnt[k] for k, v in b.items()}
+            f["adj"] += 2.0 * B * c * d
+            b["adj"] += 4.0 * (B * d + d * c)                      # z-bar_{l+1}, W_{l+1} in
+        f["dw"] += 2.0 * B * c * (a + 1)
+        b["dw"] += 4.0 * (B * c + B * a + c * a + c)              # z-bar_l, y_l in; dW_l, db_l written once
+    return {k: v / n for k, v in f.items()}, {k: v / n for k, v in b.items()}
 
 
 _HASH_CHUNK = 64 << 20  # 4-byte elements per hashed chunk (256 MiB)
@@ -716,16 +716,15 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
         names = {"pass": "resident_pass: whole forward + reverse pass in one launch"}
         traffic = measured_traffic(wl.name, "resident_pass")
     else:
-        flops = {"fwd": fl["fwd"], "adj": fl["adj"], "hadj": fl["hadj"], "dw": fl["dw"]}
+        flops = {k: fl[k] for k in ("fwd", "adj", "hadj", "dw") if k in fl}
         cand = [k for k in tot if k in flops]
         dom = max(cand, key=tot.get) if cand else "adj"
         small = spec.batch * spec.hidden < 1024 * 256 or wl.dtype == "bf16"
         lds_cell, lds_prod = lds_kernels(spec, knobs)
         if wl.cell == "mlp":
             names = {"fwd": "mlpv_gemm forward: layer product + relu (mean over layers)",
-                     "adj": "mlpv_gemm adjoint: recompute, mask, seed (mean over layers)",
-                     "hadj": "mlpv_gemm NN product zbar W_{l+1} (mean over layers)",
-                     "dw": "weight gradient of one layer (mean over layers)"}
+                     "adj": "mlpv_gemm adjoint: zbar_{l+1} W_{l+1}, recompute, mask, seed (mean over layers)",
+                     "dw": "mlpv_dw weight gradient of one layer (mean over layers)"}
         elif wide and wl.dtype == "f32":
             names = {"fwd": ("cell_gemm_f32" if lds_cell else "step_f32") + " forward: gate GEMM + cell update",
                      "adj": ("cell_gemm_f32" if lds_cell else "step_f32") + " adjoint: gate recompute + cell adjoint",

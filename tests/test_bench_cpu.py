@@ -63,9 +63,13 @@ def test_lds_rule_of_the_4096_lstm():
 def test_mlp_layer_work_reduces_to_one_width():
     B, w, n = 8, 32, 5
     f, b = bench.mlp_layer_work([w] * (n + 1), B)
-    assert f["fwd"] == f["adj"] == f["hadj"] == 2.0 * B * w * w
+    assert set(f) == {"fwd", "adj", "dw"}
+    assert f["fwd"] == 2.0 * B * w * w
+    # the adjoint also forms zbar_{l+1} W_{l+1}, for every layer but the last
+    assert f["adj"] == 2.0 * B * w * w * (1 + (n - 1) / n)
     assert f["dw"] == 2.0 * B * w * (w + 1)
     assert b["fwd"] == 4.0 * (w * w + w + 2 * B * w)
     # widths that alternate: the mean over layers of each class
     f2, _ = bench.mlp_layer_work([16, 32, 16], 4)
-    assert f2["fwd"] == (2 * 4 * 16 * 32 + 2 * 4 * 32 * 16) / 2 and f2["hadj"] == 2 * 4 * 32 * 16
+    assert f2["fwd"] == (2 * 4 * 16 * 32 + 2 * 4 * 32 * 16) / 2
+    assert f2["adj"] == (2 * 4 * 16 * 32 + 2 * 4 * 32 * 16 + 2 * 4 * 32 * 16) / 2
