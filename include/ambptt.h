@@ -349,7 +349,11 @@ ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
  * the direct-load kernels), "hadj_launch" (1,
  * default: on the fp32 path for large batches the adjoint's h-adjoint
  * product zbar_{t+1} W_h runs as a launch of its own, kernel class
- * AMBPTT_K_HADJ; 0: fused into the adjoint step's launch), "reserve" (1: allocate now the pinned host
+ * AMBPTT_K_HADJ; 0: fused into the adjoint step's launch), "prod_split" (1,
+ * default: where both LDS-tiled kernels run and the 64 x 64 tiles would move
+ * twice the operand rows per MFMA, that launch uses 128 x 128 tiles with the
+ * reduction split in up to 4 parts, which the adjoint adds in order; 0: the
+ * 64 x 64 tiles), "reserve" (1: allocate now the pinned host
  * tier and resident-program staging that the current schedule needs, with
  * the interval I_min, or 1 before calibration, which takes the most host
  * slots; see ambptt_run_noalloc), "host_waits"

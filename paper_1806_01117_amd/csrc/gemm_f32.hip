@@ -217,7 +217,12 @@ __global__ __launch_bounds__(64 * kCW, 2) void cell_gemm_f32(StepArgs a) {
             lterm += h1;
           }
         }
-        const float hb = (a.first ? 0.f : a.hbar_in[o]) + sd;
+        float hin = 0.f;
+        if (!a.first) {  // the product's partial sums, in order
+          hin = a.hbar_in[o];
+          for (int ps = 1; ps < a.hbar_parts; ++ps) hin += a.hbar_in[o + (size_t)ps * B * H];
+        }
+        const float hb = hin + sd;
         float* zo = (float*)a.zbar_out + (size_t)m * GH + j;
         if (G == 4) {
           const float cb = a.first ? 0.f : a.cbar_in[o];
@@ -338,6 +343,102 @@ __global__ __launch_bounds__(256, 2) void prod_gemm_f32(ProdArgs a) {
     }
 }
 
+// ---- h-adjoint product on the gate product's tiles, the reduction split ---------
+// The 64 x 64 tiles above give the 4096-LSTM's product (512 x 4096 outputs)
+// 512 workgroups, but move twice the operand rows per MFMA of the 128 x 128
+// tiles.  Here each of the 128 x 128 tiles takes `parts` workgroups, one per
+// contiguous run of stages, so the grid keeps two workgroups per CU; part s
+// is written whole to out + s M N and the adjoint adds the parts in order.
+// Loader, LDS layout, fragments and stage loop are the gate product's (wave
+// (wm, wn): rows 64 wm .., columns 64 wn ..).  The row tiles of one
+// (column tile, part) share an XCD, as the gate product's do.
+__global__ __launch_bounds__(64 * kCW, 2) void prod_split_f32(ProdArgs a, int parts) {
+  __shared__ float As[kCM][kLd];
+  __shared__ float Bs[kCN][kLd];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int r = lane & 15, q = lane >> 4;
+  const int M = a.M, N = a.N, K = a.K;
+  const int mt = (M + kCM - 1) / kCM, nt = N / kCN;
+  int tm, tc;
+  tile_of(blockIdx.x, mt, nt * parts, &tm, &tc);
+  const int tn = tc / parts, part = tc % parts;
+  const int m0 = tm * kCM, n0 = tn * kCN;
+  const int nall = (K + kKT - 1) / kKT;
+  const int st0 = part * nall / parts, st1 = (part + 1) * nall / parts;
+
+  const int lr = tid >> 4, lc = 4 * (tid & 15);
+  const float* arow[8];
+  const float* brow[8];
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    arow[p] = (const float*)a.A + (size_t)min(m0 + lr + 16 * p, M - 1) * K;  // rows >= M: clamped, discarded
+    brow[p] = (const float*)a.B + (size_t)(n0 + lr + 16 * p) * (a.ldb ? a.ldb : K);
+  }
+  f4 ra[8], rb[8];
+  bool kin = true;
+  auto load = [&](int st) {  // unconditional loads, as in the gate product
+    const int k = st * kKT + lc;
+    kin = k < K;
+    const int kc = kin ? k : 0;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) ra[p] = *(const f4*)(arow[p] + kc);
+#pragma unroll
+    for (int p = 0; p < 8; ++p) rb[p] = *(const f4*)(brow[p] + kc);
+  };
+  auto store = [&]() {
+    const f4 zero = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int p = 0; p < 8; ++p) *(f4*)&As[lr + 16 * p][lc] = kin ? ra[p] : zero;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) *(f4*)&Bs[lr + 16 * p][lc] = kin ? rb[p] : zero;
+  };
+  f4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) acc[i][nb] = f4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&]() {
+#pragma unroll
+    for (int kk = 0; kk < kKT / 16; ++kk) {
+      f4 af[4], bf[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = *(const f4*)&As[wm * 64 + 16 * i + r][16 * kk + 4 * q];
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) bf[nb] = *(const f4*)&Bs[wn * 64 + 16 * nb + r][16 * kk + 4 * q];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) {
+          acc[i][nb] = mfma4(af[i].x, bf[nb].x, acc[i][nb]);
+          acc[i][nb] = mfma4(af[i].y, bf[nb].y, acc[i][nb]);
+          acc[i][nb] = mfma4(af[i].z, bf[nb].z, acc[i][nb]);
+          acc[i][nb] = mfma4(af[i].w, bf[nb].w, acc[i][nb]);
+        }
+    }
+  };
+  if (st0 < st1) load(st0);
+  for (int st = st0; st < st1; ++st) {
+    if (st > st0) __syncthreads();
+    store();
+    if (st + 1 < st1) load(st + 1);
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    compute();
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  float* out = a.out + (size_t)part * M * N;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int m = m0 + wm * 64 + 16 * i + 4 * q + v;
+      if (m >= M) continue;
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) out[(size_t)m * N + n0 + wn * 64 + 16 * nb + r] = acc[i][nb][v];
+    }
+}
+
 }  // namespace
 
 bool cell_gemm_f32_fits(int G, int B, int D, int H) {
@@ -369,6 +470,22 @@ hipError_t launch_prod_gemm_f32(const ProdArgs& a, hipStream_t s, hipEvent_t e0,
   if (!prod_gemm_f32_fits(a.M, a.N, a.K)) return hipErrorInvalidValue;
   const dim3 grid(prod_gemm_f32_tiles(a.M, a.N)), block(256);
   hipExtLaunchKernelGGL(prod_gemm_f32, grid, block, 0, s, e0, e1, 0, a);
+  return hipGetLastError();
+}
+
+int prod_split_f32_parts(int M, int N, int K) {
+  if (M < 1 || K < 4 || K % 4 || N < kCN || N % kCN) return 1;
+  const int tiles = ((M + kCM - 1) / kCM) * (N / kCN);
+  int parts = 1;  // two workgroups per CU, each with at least 16 stages
+  while (parts < kProdSplitMax && tiles * parts < 512 && (K / kKT) / (2 * parts) >= 16) parts *= 2;
+  return parts;
+}
+
+hipError_t launch_prod_split_f32(const ProdArgs& a, int parts, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (parts < 1 || parts > kProdSplitMax || a.add || a.M < 1 || a.K < 4 || a.K % 4 || a.N < kCN || a.N % kCN)
+    return hipErrorInvalidValue;
+  const dim3 grid(((a.M + kCM - 1) / kCM) * (a.N / kCN) * parts), block(64 * kCW);
+  hipExtLaunchKernelGGL(prod_split_f32, grid, block, 0, s, e0, e1, 0, a, parts);
   return hipGetLastError();
 }
 

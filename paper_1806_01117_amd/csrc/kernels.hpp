@@ -41,6 +41,7 @@ struct StepArgs {
   int last;              // the step's output is x_n
   float inv_bh;          // 1 / (B H)
   int ld_wht = 0;        // row stride of WhT in elements (0: G*H)
+  int hbar_parts = 1;    // hbar_in holds this many [B][H] partial sums, added in order
 };
 
 // Weight-gradient window: dW[k][c] += sum_r Z[r][k] X[r][c], db[k] += sum_r Z[r][k],
@@ -186,6 +187,12 @@ hipError_t launch_cell_gemm_f32(int G, int mode, const StepArgs& a, hipStream_t 
 bool prod_gemm_f32_fits(int M, int N, int K);
 int prod_gemm_f32_tiles(int M, int N);
 hipError_t launch_prod_gemm_f32(const ProdArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+// The same product on 128 x 128 tiles with the reduction split `parts` ways:
+// part s goes to out + s M N (no add).  kProdSplitMax parts at most.
+constexpr int kProdSplitMax = 4;
+int prod_split_f32_parts(int M, int N, int K);  // 1: the split does not fit or does not pay
+hipError_t launch_prod_split_f32(const ProdArgs& a, int parts, hipStream_t s, hipEvent_t e0 = nullptr,
+                                 hipEvent_t e1 = nullptr);
 // 128 x 128-tile fp32 weight gradient for GH, D + H >= 256 (launch_dw picks it when it fits).
 bool dw_f32_big_fits(const DwArgs& a);
 hipError_t launch_dw_f32_big(const DwArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1);

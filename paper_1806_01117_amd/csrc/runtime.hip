@@ -216,8 +216,8 @@ Layout make_layout(const ambptt_problem* p, int window) {
   L.off_loss = o; o += align_up((size_t)L.loss_slots * 8);
   L.off_lossout = o; o += kAlign;
   L.hsep = !L.small && !L.mlp && !L.mlpv && p->dtype == AMBPTT_F32;
-  if (L.wide || L.hsep || L.mlpv) {
-    L.off_hbar = o; o += align_up(BH * 4);
+  if (L.wide || L.hsep || L.mlpv) {  // the fp32 large-batch path may hold the product in split parts
+    L.off_hbar = o; o += align_up(BH * 4 * (L.hsep ? kProdSplitMax : 1));
   }
   if (L.res) {
     const size_t U = size_t(resident_units(L.G)), K1 = size_t(p->input + p->hidden);
@@ -293,6 +293,7 @@ struct ambptt_ctx {
   double sized_plan_cost = 0.0;
   int64_t widths_version = 0;
   bool hadj_launch = true;  // fp32 large-batch path: the adjoint's h-adjoint product as a launch of its own
+  bool prod_split = true;   // ... on 128 x 128 tiles with the reduction split, when that fills the device
   int lds_gemm = 1;         // fp32 large-batch path: LDS-tiled kernels (0 off, 1 when they fill the device twice over, 2 always)
   // tests of the stream ordering: a host-side delay before every host-tier
   // copy and weight-gradient window on their streams, and NaN bytes written
@@ -555,6 +556,7 @@ struct Exec {
   bool lds_cell = false;   // ... whose gate products run on the LDS-tiled kernel
   bool lds_prod = false;   // ... whose h-adjoint products run on the LDS-tiled kernel
   float* hbuf = nullptr;   // the adjoint's product (fp32 [B][H]) on those two paths
+  int hparts = 1;          // split parts of the fp32 LDS-tiled product (summed by the adjoint)
 
   Exec(ambptt_ctx* c, const void* x_, const void* W_, const float* b_)
       : C(c), L(c->L), p(c->p), x((const char*)x_), W(W_), b(b_), slot_t(c->pend.size(), -1) {
@@ -570,6 +572,8 @@ struct Exec {
                  (C->lds_gemm == 2 || cell_gemm_f32_tiles(G, B, H) >= 256);
       lds_prod = sep32 && C->lds_gemm > 0 && prod_gemm_f32_fits(B, H, G * H) &&
                  (C->lds_gemm == 2 || prod_gemm_f32_tiles(B, H) >= 256);
+      // the split parts are summed by the LDS-tiled adjoint only
+      if (lds_prod && lds_cell && C->prod_split) hparts = prod_split_f32_parts(B, H, G * H);
     }
     if (wide || sep32 || L.mlpv) hbuf = (float*)(C->ws + L.off_hbar);
   }
@@ -830,10 +834,12 @@ struct Exec {
       if ((wide || sep32) && !first) {  // hbar_{t+1} = zbar_{t+1} W_h
         ProdArgs pa{a.zbar_in, WhT, nullptr, hbuf, p.batch, p.hidden, L.G * p.hidden, L.ld_wht};
         s = timed(AMBPTT_K_HADJ, [&](hipEvent_t e0, hipEvent_t e1) {
+          if (hparts > 1) return launch_prod_split_f32(pa, hparts, C->cs, e0, e1);
           return wide ? launch_prod_nt(pa, C->cs, e0, e1) : prod32(pa, e0, e1);
         });
         if (s != AMBPTT_OK) return s;
         a.hbar_in = hbuf;
+        a.hbar_parts = hparts;
       }
       s = timed(AMBPTT_K_ADJ, [&](hipEvent_t e0, hipEvent_t e1) { return launch(kAdjoint, a, e0, e1); });
     }
@@ -1680,6 +1686,8 @@ ambptt_status ambptt_set_int(ambptt_ctx* C, const char* key, int64_t v) {
     C->lds_gemm = int(v);
   } else if (k == "hadj_launch") {
     C->hadj_launch = v != 0;
+  } else if (k == "prod_split") {
+    C->prod_split = v != 0;
   } else if (k == "uniform_sizes") {
     if (v < 0 || v > 1) return fail(AMBPTT_EINVAL, "uniform_sizes must be 0 or 1");
     C->uniform_sizes = v == 1;

@@ -1,9 +1,10 @@
 """The LDS-tiled fp32 kernels of the large-batch path (gate product with the
-cell epilogue on 128 x 256 tiles, h-adjoint product on 64 x 128 tiles),
-forced onto shapes that are ragged against their tiles: batches that leave a
-partial row tile, for the LSTM and the tanh RNN, every loss.  Each run is
-compared with the oracle and, bit for bit, across schedules; the direct-load
-kernels on the same inputs meet the same tolerance."""
+cell epilogue on 128 x 128 tiles; h-adjoint product on 128 x 128 tiles with
+the reduction split in parts, or on 64 x 64 tiles), forced onto shapes that
+are ragged against their tiles: batches that leave a partial row tile, for
+the LSTM and the tanh RNN, every loss.  Each run is compared with the oracle
+and, bit for bit, across schedules; the direct-load kernels on the same
+inputs meet the same tolerance."""
 import pytest
 
 import synth
@@ -34,6 +35,10 @@ def test_lds_lstm_ragged_batch_schedules():
     assert_bitwise(a, run_gpu(wl, dev, fast_slots=3, slow_slots=0, opts=LDS))   # plain Revolve
     old = run_gpu(wl, dev, fast_slots=3, slow_slots=9, interval_min=2, opts={"lds_gemm": 0})
     assert_close(old, want, TOL_F32)
+    # the product on 64 x 64 tiles, unsplit (K = 4096 splits in 4 parts of 16 stages by default)
+    whole = run_gpu(wl, dev, fast_slots=3, slow_slots=9, interval_min=2, opts=dict(LDS, prod_split=0))
+    assert_close(whole, want, TOL_F32)
+    assert_bitwise(whole, run_gpu(wl, dev, fast_slots=9, slow_slots=0, opts=dict(LDS, prod_split=0)))
     # the h-adjoint product fused into the direct-load adjoint beside the LDS-tiled forward
     f = run_gpu(wl, dev, fast_slots=3, slow_slots=9, interval_min=2, opts={"lds_gemm": 2, "hadj_launch": 0})
     assert f["stats"]["kernel_calls"][3] == 0
