@@ -228,6 +228,23 @@ def lds_kernels(spec, knobs) -> tuple[bool, bool]:
     return cell, prod
 
 
+def prod_split_parts(spec, knobs) -> int:
+    """Parts of the fp32 h-adjoint product's split reduction (the library's
+    "prod_split" rule: both LDS-tiled kernels in use, 128 x 128 tiles, parts
+    doubled up to 4 while the grid has fewer than 512 workgroups and every
+    part keeps at least 16 stages of 64); 1 where it is not split."""
+    cell, prod = lds_kernels(spec, knobs)
+    if not (cell and prod and dict(knobs).get("prod_split", 1) != 0):
+        return 1
+    M, N, K = spec.batch, spec.hidden, spec.gates * spec.hidden
+    if N % 128 or K % 4:
+        return 1
+    tiles, parts = -(-M // 128) * (N // 128), 1
+    while parts < 4 and tiles * parts < 512 and (K // 64) // (2 * parts) >= 16:
+        parts *= 2
+    return parts
+
+
 def step_flops(spec, window: int, wide: bool = False) -> dict:
     """Algorithmic flops of one launch of each per-step kernel, and of the
     three products of one step (gate GEMM, h-adjoint, weight gradient).  On
@@ -726,9 +743,12 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
                      "adj": "mlpv_gemm adjoint: zbar_{l+1} W_{l+1}, recompute, mask, seed (mean over layers)",
                      "dw": "mlpv_dw weight gradient of one layer (mean over layers)"}
         elif wide and wl.dtype == "f32":
+            parts = prod_split_parts(spec, knobs)
+            hadj_kernel = (f"prod_split_f32 ({parts} parts)" if parts > 1 else
+                           "prod_gemm_f32" if lds_prod else "prod_f32")
             names = {"fwd": ("cell_gemm_f32" if lds_cell else "step_f32") + " forward: gate GEMM + cell update",
                      "adj": ("cell_gemm_f32" if lds_cell else "step_f32") + " adjoint: gate recompute + cell adjoint",
-                     "hadj": ("prod_gemm_f32" if lds_prod else "prod_f32") + " h-adjoint product zbar W_h",
+                     "hadj": hadj_kernel + " h-adjoint product zbar W_h",
                      "dw": "dw_f32_big weight-gradient window"}
         elif wide and wl.cell == "resmlp":
             names = {"fwd": "mlp_wide forward", "adj": "mlp_wide adjoint (recompute + mask)",
@@ -749,7 +769,8 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
         elif wide and wl.dtype == "f32":
             key = {"fwd": "cell_gemm_f32_fwd" if lds_cell else "step_f32_fwd",
                    "adj": "cell_gemm_f32_adj" if lds_cell else "step_f32_adj",
-                   "hadj": "prod_gemm_f32" if lds_prod else "prod_f32"}.get(dom, "dw_f32_big")
+                   "hadj": "prod_split_f32" if prod_split_parts(spec, knobs) > 1 else
+                   "prod_gemm_f32" if lds_prod else "prod_f32"}.get(dom, "dw_f32_big")
         elif wide:
             fam = {"fwd": "mlp_wide_fwd", "adj": "mlp_wide_adj", "hadj": "prod_wide_nn"} if wl.cell == "resmlp" else \
                 {"fwd": "cell_wide_fwd", "adj": "cell_wide_adj", "hadj": "prod_wide_nt"}

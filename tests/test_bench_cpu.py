@@ -60,6 +60,20 @@ def test_lds_rule_of_the_4096_lstm():
     assert bench.lds_kernels(small, []) == (False, False)
 
 
+def test_prod_split_rule():
+    import synth
+    import paper_1806_01117_amd as amb
+    big = amb.ProblemSpec.from_workload(synth.get("lstm_h4096_t20000"))
+    assert bench.prod_split_parts(big, []) == 4                     # 128 tiles of 128 x 128, 256 stages
+    assert bench.prod_split_parts(big, [("prod_split", 0)]) == 1
+    assert bench.prod_split_parts(big, [("lds_gemm", 0)]) == 1
+    ragged = amb.ProblemSpec.from_workload(synth.get("lstm_h4096_t20000").with_(batch=300, input=96, hidden=1024))
+    assert bench.prod_split_parts(ragged, [("lds_gemm", 2)]) == 4   # 24 tiles, 64 stages: 4 parts of 16
+    rnn = amb.ProblemSpec.from_workload(synth.get("lstm_h4096_t20000").with_(cell="rnn", batch=300, input=64,
+                                                                            hidden=1024))
+    assert bench.prod_split_parts(rnn, [("lds_gemm", 2)]) == 1      # 16 stages: a part would hold 8
+
+
 def test_mlp_layer_work_reduces_to_one_width():
     B, w, n = 8, 32, 5
     f, b = bench.mlp_layer_work([w] * (n + 1), B)
