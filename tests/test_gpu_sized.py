@@ -39,13 +39,17 @@ def _case(wl):
                                    dict(batch=40, hidden=1280, widths=(1280, 512, 1040, 720))],
                          ids=["pooled", "ragged", "deep"])
 def test_mlp_of_different_widths(shape):
-    wl = synth.get("mlp_widths_l2000").with_(n_steps=24, **shape)
+    # 27 layers: the weight gradients go in groups of 8 layers, the last of 3
+    wl = synth.get("mlp_widths_l2000").with_(n_steps=27, **shape)
     n, sizes = wl.n_steps, _sizes(wl)
     host, dev = _case(wl)
     want = run_oracle(wl, *host)
     ref = run_gpu(wl, dev, fast_slots=n + 1, slow_slots=0)          # every state fits: no recomputation
     assert ref["stats"]["forward_evals"] == n
     assert_close_mlp(ref, want, wl, TOL_F32)
+    # weight-gradient groups of 3 and of 1 layer: each layer's gradient is its own launch member
+    for win in (3, 1):
+        assert_bitwise(run_gpu(wl, dev, fast_slots=n + 1, slow_slots=0, window=win), ref)
     for kw in (dict(fast_slots=2, slow_slots=0), dict(fast_slots=3, slow_slots=0),
                dict(fast_slots=3, slow_slots=n, interval_min=3), dict(fast_slots=2, slow_slots=n, interval_min=4)):
         got = run_gpu(wl, dev, **kw)
