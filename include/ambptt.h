@@ -318,7 +318,7 @@ ambptt_status ambptt_bind(ambptt_ctx* ctx, void* slot_pool, size_t pool_bytes,
  * weight-gradient windows run on a stream of their own, beside the steps; 0:
  * on the compute stream, after the window's last adjoint; -1, default: 0 on
  * the wide-batch bf16 path and the large-batch fp32 path, whose kernels each
- * fill the device, else 1),
+ * fill the device, and for the MLP of layers of different widths, else 1),
  * "event_system_fence" (0, default: the events that order the library's
  * streams and time its kernels use device-scope fences; 1: system-scope, as
  * HIP's default events do), "store_policy" (0, default: the sweep stores

@@ -880,8 +880,10 @@ struct Exec {
       }
       // the wide-batch bf16 kernels and the large-batch fp32 kernels each fill
       // the device: beside them a window only competes for the same units, so
-      // it runs in line on the compute stream
-      const bool own = C->dw_stream < 0 ? !(wide || L.hsep) : C->dw_stream != 0;
+      // it runs in line on the compute stream; so does the grouped window of
+      // the MLP of different widths (measured at the same rate either way,
+      // without a stream handoff per window)
+      const bool own = C->dw_stream < 0 ? !(wide || L.hsep || L.mlpv) : C->dw_stream != 0;
       hipStream_t ws = own ? C->ds : C->cs;
       if (own) {
         HIPCK(hipEventRecord(C->ev_c2, C->cs));
