@@ -7,7 +7,7 @@
 //   adjoint   ybar_{l+1} = u + dL/dy_{l+1},  u = zbar_{l+1} W_{l+1} (0 for the last layer)
 //             zbar_l = ybar_{l+1} * 1[z_l > 0]   (relu'(0) = 0)
 //   product   u = zbar W  (an "NN" product: W[k][c] is contiguous in c)
-// dW_l = zbar_l^T y_l and db_l run on the weight-gradient kernels.
+//   gradient  dW_l = zbar_l^T y_l,  db_l = column sums of zbar_l (mlpv_dw, a window of layers per launch)
 //
 // One launch per step: the forward, the NN product alone (dL/dy_0), and the
 // adjoint, which also forms u for its own tile.  A workgroup of 16 waves owns
@@ -45,7 +45,7 @@ struct MlpvTile {
   int tid, lane, wave, r, q, m0, n0;
 };
 
-// acc[i][j] += the wave's share of A[m0 + 16 i ..][:] . B[:][n0 + 16 j ..] for
+// acc[i][j] = the wave's share of A[m0 + 16 i ..][:] . B[:][n0 + 16 j ..] for
 // A [M][K] row-major and B = W^T (NT: W [N][K]) or B = W (NN: W [K][N]).
 // Wave w takes chunks w, w + 16, ... of 16 reduction indices in groups of ND
 // whose loads all issue before the group's first MFMA; past the last chunk
