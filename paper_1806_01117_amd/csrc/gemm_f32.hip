@@ -59,6 +59,82 @@ __device__ __forceinline__ void tile_of(int i, int mt, int nt, int* tm, int* tn)
   }
 }
 
+// ---- epilogue of the gate product: one wave's 64 x 64 accumulators ----------
+// Accumulator element v of lane l is row 4 (l >> 4) + v, column l & 15 of its
+// 16 x 16 block.  Forward: the cell update; adjoint: loss term (returned),
+// seed, cell adjoint, zbar_t, cbar_t and the copy of h_t.
+template <int G, int MODE>
+__device__ __forceinline__ float cell_epilogue(const StepArgs& a, const f4 (&acc)[4][4], int m0, int j0, int wm,
+                                               int wn, int r, int q) {
+  const int B = a.B, H = a.H, GH = G * H;
+  float lterm = 0.f;
+  constexpr int NU = G == 4 ? 1 : 4;  // unit blocks per wave
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int u = 0; u < NU; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int m = m0 + wm * 64 + 16 * i + 4 * q + v;
+        const int j = G == 4 ? j0 + wn * 16 + r : j0 + wn * 64 + 16 * u + r;
+        if (m >= B) continue;
+        const size_t o = (size_t)m * H + j;
+        float h1, c1 = 0.f, tc = 0.f, ig = 0.f, fg = 0.f, gg = 0.f, og = 0.f, cold = 0.f;
+        if (G == 4) {
+          ig = sigm(acc[i][0][v] + a.bias[j]);
+          fg = sigm(acc[i][1][v] + a.bias[H + j]);
+          gg = tanhf(acc[i][2][v] + a.bias[2 * H + j]);
+          og = sigm(acc[i][3][v] + a.bias[3 * H + j]);
+          cold = a.c[o];
+          c1 = fg * cold + ig * gg;
+          tc = tanhf(c1);
+          h1 = og * tc;
+        } else {
+          h1 = tanhf(acc[i][u][v] + a.bias[j]);
+        }
+        if (MODE == kForward) {
+          ((float*)a.h_out)[o] = h1;
+          if (G == 4) a.c_out[o] = c1;
+          continue;
+        }
+        // adjoint: loss term of h_{t+1} and its seed dL/dh_{t+1}
+        float sd = 0.f;
+        if (a.loss == AMBPTT_LOSS_MEAN_SQ_ALL) {
+          sd = 2.f * h1 * a.inv_bh;
+          lterm += h1 * h1;
+        } else if (a.last) {
+          if (a.loss == AMBPTT_LOSS_HALF_SQ_LAST) {
+            sd = h1;
+            lterm += h1 * h1;
+          } else {
+            sd = a.inv_bh;
+            lterm += h1;
+          }
+        }
+        float hin = 0.f;
+        if (!a.first) {  // the product's partial sums, in order
+          hin = a.hbar_in[o];
+          for (int ps = 1; ps < a.hbar_parts; ++ps) hin += a.hbar_in[o + (size_t)ps * B * H];
+        }
+        const float hb = hin + sd;
+        float* zo = (float*)a.zbar_out + (size_t)m * GH + j;
+        if (G == 4) {
+          const float cb = a.first ? 0.f : a.cbar_in[o];
+          const float ob = hb * tc;
+          const float ch = cb + hb * og * (1.f - tc * tc);
+          zo[0] = ch * gg * ig * (1.f - ig);
+          zo[H] = ch * cold * fg * (1.f - fg);
+          zo[2 * H] = ch * ig * (1.f - gg * gg);
+          zo[3 * H] = ob * og * (1.f - og);
+          a.cbar_out[o] = ch * fg;
+        } else {
+          zo[0] = hb * (1.f - h1 * h1);
+        }
+        ((float*)a.hwin_out)[o] = ((const float*)a.h)[o];
+      }
+  return lterm;
+}
+
 // ---- gate product with the cell epilogue ------------------------------------
 // Tile: 128 batch rows x 128 gate columns (LSTM: 32 units x 4 gates; RNN:
 // 128 units), 4 waves.  Wave (wm, wn), wm, wn < 2, computes rows
@@ -170,74 +246,7 @@ __global__ __launch_bounds__(64 * kCW, 2) void cell_gemm_f32(StepArgs a) {
     __builtin_amdgcn_sched_barrier(0);
   }
 
-  // ---- epilogue: accumulator element v of lane l is row 4 (l >> 4) + v,
-  //      column l & 15 of its 16 x 16 block ------------------------------------
-  const int GH = G * H;
-  float lterm = 0.f;
-  constexpr int NU = G == 4 ? 1 : 4;  // unit blocks per wave
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int u = 0; u < NU; ++u)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int m = m0 + wm * 64 + 16 * i + 4 * q + v;
-        const int j = G == 4 ? j0 + wn * 16 + r : j0 + wn * 64 + 16 * u + r;
-        if (m >= B) continue;
-        const size_t o = (size_t)m * H + j;
-        float h1, c1 = 0.f, tc = 0.f, ig = 0.f, fg = 0.f, gg = 0.f, og = 0.f, cold = 0.f;
-        if (G == 4) {
-          ig = sigm(acc[i][0][v] + a.bias[j]);
-          fg = sigm(acc[i][1][v] + a.bias[H + j]);
-          gg = tanhf(acc[i][2][v] + a.bias[2 * H + j]);
-          og = sigm(acc[i][3][v] + a.bias[3 * H + j]);
-          cold = a.c[o];
-          c1 = fg * cold + ig * gg;
-          tc = tanhf(c1);
-          h1 = og * tc;
-        } else {
-          h1 = tanhf(acc[i][u][v] + a.bias[j]);
-        }
-        if (MODE == kForward) {
-          ((float*)a.h_out)[o] = h1;
-          if (G == 4) a.c_out[o] = c1;
-          continue;
-        }
-        // adjoint: loss term of h_{t+1} and its seed dL/dh_{t+1}
-        float sd = 0.f;
-        if (a.loss == AMBPTT_LOSS_MEAN_SQ_ALL) {
-          sd = 2.f * h1 * a.inv_bh;
-          lterm += h1 * h1;
-        } else if (a.last) {
-          if (a.loss == AMBPTT_LOSS_HALF_SQ_LAST) {
-            sd = h1;
-            lterm += h1 * h1;
-          } else {
-            sd = a.inv_bh;
-            lterm += h1;
-          }
-        }
-        float hin = 0.f;
-        if (!a.first) {  // the product's partial sums, in order
-          hin = a.hbar_in[o];
-          for (int ps = 1; ps < a.hbar_parts; ++ps) hin += a.hbar_in[o + (size_t)ps * B * H];
-        }
-        const float hb = hin + sd;
-        float* zo = (float*)a.zbar_out + (size_t)m * GH + j;
-        if (G == 4) {
-          const float cb = a.first ? 0.f : a.cbar_in[o];
-          const float ob = hb * tc;
-          const float ch = cb + hb * og * (1.f - tc * tc);
-          zo[0] = ch * gg * ig * (1.f - ig);
-          zo[H] = ch * cold * fg * (1.f - fg);
-          zo[2 * H] = ch * ig * (1.f - gg * gg);
-          zo[3 * H] = ob * og * (1.f - og);
-          a.cbar_out[o] = ch * fg;
-        } else {
-          zo[0] = hb * (1.f - h1 * h1);
-        }
-        ((float*)a.hwin_out)[o] = ((const float*)a.h)[o];
-      }
+  const float lterm = cell_epilogue<G, MODE>(a, acc, m0, j0, wm, wn, r, q);
   if (MODE == kAdjoint) {  // the waves' loss terms, summed in wave order
     const float s = wave_sum(lterm);
     if (lane == 0) red[wave] = s;
