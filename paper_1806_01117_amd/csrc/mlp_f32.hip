@@ -43,24 +43,7 @@ constexpr int kVW = 16;  // waves per workgroup
 
 struct MlpvTile {
   int tid, lane, wave, r, q, m0, n0;
-  bool first_col;  // the tile of the first 32 columns: it copies its A rows (adjoint)
 };
-
-// Workgroup id -> (row tile, column tile), XCD-aware: ids are dealt to the 8
-// XCDs round-robin, and each XCD takes whole column tiles (all their row
-// tiles), so the weight rows of a column tile are fetched into one L2 and
-// the row tiles there hit it.  The rows of A, 4 to 32 times smaller than W
-// in these layers, reach every XCD.
-__device__ __forceinline__ void mlpv_tile_of(int i, int mt, int nt, int* tm, int* tn) {
-  if (nt % 8 == 0) {
-    const int xcd = i & 7, k = i >> 3;
-    *tn = xcd * (nt >> 3) + k / mt;
-    *tm = k % mt;
-  } else {
-    *tm = i % mt;
-    *tn = i / mt;
-  }
-}
 
 // acc[i][j] = the wave's share of A[m0 + 16 i ..][:] . B[:][n0 + 16 j ..] for
 // A [M][K] row-major and B = W^T (NT: W [N][K]) or B = W (NN: W [K][N]).
@@ -125,7 +108,7 @@ __device__ __forceinline__ void tile_product(const MlpvTile& t, const float* __r
         for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int j = 0; j < 2; ++j) acc[i][j] = mfma4(xa[u][i][k], xb[u][j][k], acc[i][j]);
-      if (ywin && t.first_col) {
+      if (ywin && blockIdx.y == 0) {
 #pragma unroll
         for (int i = 0; i < 2; ++i)
           if (c < nch && t.m0 + 16 * i + r < M) *(f4*)(ywin + (size_t)(t.m0 + 16 * i + r) * K + 16 * c + 4 * q) = xa[u][i];
@@ -168,13 +151,9 @@ __global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
   t.wave = __builtin_amdgcn_readfirstlane(t.tid >> 6);
   t.r = t.lane & 15;
   t.q = t.lane >> 4;
+  t.m0 = blockIdx.x * 32;
+  t.n0 = blockIdx.y * 32;
   const int M = a.M, N = a.N;
-  const int mt = (M + 31) / 32, nt = (N + 31) / 32;
-  int tm, tn;
-  mlpv_tile_of(blockIdx.x, mt, nt, &tm, &tn);
-  t.m0 = tm * 32;
-  t.n0 = tn * 32;
-  t.first_col = tn == 0;
   const bool adj = MODE == kMlpvAdj || MODE == kMlpvAdjU;
   float u = 0.f;
   if (MODE == kMlpvAdjU) {
@@ -228,7 +207,7 @@ __global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
       float tot = 0.f;
 #pragma unroll
       for (int w = 0; w < kVW; ++w) tot += lpart[w];
-      a.loss_acc[tn * mt + tm] += (double)tot;
+      a.loss_acc[blockIdx.y * gridDim.x + blockIdx.x] += (double)tot;
     }
   }
 }
@@ -368,7 +347,7 @@ static int mlpv_nd(int K) { return std::min(4, std::max(1, (K / 16 + kVW - 1) / 
 
 template <int MODE, int ND2>
 static hipError_t launch_mlpv_nd(const MlpvArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  const dim3 grid(((a.M + 31) / 32) * ((a.N + 31) / 32)), block(64 * kVW);
+  const dim3 grid((a.M + 31) / 32, (a.N + 31) / 32), block(64 * kVW);
   switch (mlpv_nd(a.K)) {
     case 1: hipExtLaunchKernelGGL((mlpv_gemm<MODE, 1, ND2>), grid, block, 0, s, e0, e1, 0, a); break;
     case 2: hipExtLaunchKernelGGL((mlpv_gemm<MODE, 2, ND2>), grid, block, 0, s, e0, e1, 0, a); break;
