@@ -87,3 +87,12 @@ def test_mlp_layer_work_reduces_to_one_width():
     f2, _ = bench.mlp_layer_work([16, 32, 16], 4)
     assert f2["fwd"] == (2 * 4 * 16 * 32 + 2 * 4 * 32 * 16) / 2
     assert f2["adj"] == (2 * 4 * 16 * 32 + 2 * 4 * 32 * 16 + 2 * 4 * 32 * 16) / 2
+
+
+def test_pmc_table_names_kernel_instances():
+    from paper_1806_01117_amd.pmc_summary import _instance
+    assert _instance("void ambptt::(anonymous namespace)::mlpv_gemm<3, 1, 4>(ambptt::MlpvArgs)") == "mlpv_gemm<3, 1, 4>"
+    assert _instance("ambptt::(anonymous namespace)::dw_f32_big(ambptt::DwArgs)") == "dw_f32_big"
+    assert _instance("void ambptt::(anonymous namespace)::mlpv_dw<1>(ambptt::(anonymous namespace)::MlpvDwGroup)") \
+        == "mlpv_dw<1>"
+    assert _instance("__amd_rocclr_copyBuffer") == "__amd_rocclr_copyBuffer"
