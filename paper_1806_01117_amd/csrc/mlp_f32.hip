@@ -45,7 +45,7 @@ struct MlpvTile {
   int tid, lane, wave, r, q, m0, n0;
 };
 
-// acc[i][j] = the wave's share of A[m0 + 16 i ..][:] . B[:][n0 + 16 j ..] for
+// acc[i][j] = the wave's share of A[m0 + 16 i ..][:] . B[:][n0 + 16 j ..], i < RT, for
 // A [M][K] row-major and B = W^T (NT: W [N][K]) or B = W (NN: W [K][N]).
 // Wave w takes chunks w, w + 16, ... of 16 reduction indices in groups of ND
 // whose loads all issue before the group's first MFMA; past the last chunk
@@ -57,32 +57,32 @@ struct MlpvTile {
 // wave's own tile bt in LDS (rows of 36 floats: the column reads of a
 // fragment fall in 64 distinct banks).  With ywin, the first column of
 // workgroups also writes a copy of its A rows there.
-template <bool NN, int ND>
+template <bool NN, int ND, int RT>
 __device__ __forceinline__ void tile_product(const MlpvTile& t, const float* __restrict__ A,
                                              const float* __restrict__ W, int M, int N, int K, float (&bt)[16][36],
-                                             float* ywin, f4 (&acc)[2][2]) {
+                                             float* ywin, f4 (&acc)[RT][2]) {
   const int r = t.r, q = t.q, wave = t.wave;
   const int nch = K / 16;
   const int ngrp = (nch + kVW * ND - 1) / (kVW * ND);  // groups of ND chunks per wave
-  const float* arow[2];
+  const float* arow[RT];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) arow[i] = A + (size_t)min(t.m0 + 16 * i + r, M - 1) * K + 4 * q;  // rows >= M: clamped, discarded
+  for (int i = 0; i < RT; ++i) arow[i] = A + (size_t)min(t.m0 + 16 * i + r, M - 1) * K + 4 * q;  // rows >= M: clamped, discarded
   const float* brow[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) brow[j] = W + (size_t)min(t.n0 + 16 * j + r, N - 1) * K + 4 * q;  // NT; past N: clamped, discarded
   const int nrow = t.lane >> 3, ncol = 4 * (t.lane & 7);
   const float* wnn = W + min(t.n0 + ncol, N - 4);  // NN: a float4 past N: clamped, discarded
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < RT; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
   for (int g = 0; g < ngrp; ++g) {
-    f4 xa[ND][2], xb[ND][2];
+    f4 xa[ND][RT], xb[ND][2];
 #pragma unroll
     for (int u = 0; u < ND; ++u) {
       const int k0 = 16 * min(wave + kVW * (ND * g + u), nch - 1);
 #pragma unroll
-      for (int i = 0; i < 2; ++i) xa[u][i] = *(const f4*)(arow[i] + k0);
+      for (int i = 0; i < RT; ++i) xa[u][i] = *(const f4*)(arow[i] + k0);
 #pragma unroll
       for (int j = 0; j < 2; ++j)
         xb[u][j] = NN ? *(const f4*)(wnn + (size_t)(k0 + nrow + 8 * j) * N) : *(const f4*)(brow[j] + k0);
@@ -100,47 +100,54 @@ __device__ __forceinline__ void tile_product(const MlpvTile& t, const float* __r
       }
       if (c >= nch) {  // uniform: a chunk past the reduction adds nothing
 #pragma unroll
-        for (int i = 0; i < 2; ++i) xa[u][i] = xb[u][i] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < RT; ++i) xa[u][i] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < 2; ++j) xb[u][j] = f4{0.f, 0.f, 0.f, 0.f};
       }
 #pragma unroll
       for (int k = 0; k < 4; ++k)
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < RT; ++i)
 #pragma unroll
           for (int j = 0; j < 2; ++j) acc[i][j] = mfma4(xa[u][i][k], xb[u][j][k], acc[i][j]);
       if (ywin && blockIdx.y == 0) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < RT; ++i)
           if (c < nch && t.m0 + 16 * i + r < M) *(f4*)(ywin + (size_t)(t.m0 + 16 * i + r) * K + 16 * c + 4 * q) = xa[u][i];
       }
     }
   }
 }
 
-// The 16 waves' partial tiles summed in wave order: thread tid gets element
-// (tid >> 5, tid & 31) of the 32 x 32 tile.  Accumulator element v of lane l
-// is row 4 (l >> 4) + v, column l & 15 of its 16 x 16 block.
-__device__ __forceinline__ float tile_sum(const MlpvTile& t, float (&part)[kVW][32][36], const f4 (&acc)[2][2]) {
+// The 16 waves' partial tiles summed in wave order: thread tid < 512 RT gets
+// element (tid >> 5, tid & 31) of the 16 RT x 32 tile (the others get 0).
+// Accumulator element v of lane l is row 4 (l >> 4) + v, column l & 15 of its
+// 16 x 16 block.
+template <int RT>
+__device__ __forceinline__ float tile_sum(const MlpvTile& t, float (&part)[kVW][32][36], const f4 (&acc)[RT][2]) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < RT; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int v = 0; v < 4; ++v) part[t.wave][16 * i + 4 * t.q + v][16 * j + t.r] = acc[i][j][v];
   __syncthreads();
   float sum = 0.f;
+  if (t.tid < 512 * RT) {
 #pragma unroll
-  for (int w = 0; w < kVW; ++w) sum += part[w][t.tid >> 5][t.tid & 31];
+    for (int w = 0; w < kVW; ++w) sum += part[w][t.tid >> 5][t.tid & 31];
+  }
   return sum;
 }
 
-// One launch per step.  A workgroup of 16 waves owns 32 rows x 32 columns of
-// the step's output; all threads run the epilogue, 32 consecutive columns
-// per half wave.  kMlpvAdjU runs the adjoint's two products in one launch:
+// One launch per step.  A workgroup of 16 waves owns 16 RT rows x 32 columns
+// of the step's output (RT = 1 where 32-row tiles would leave the device
+// short of workgroups); its first 512 RT threads run the epilogue, 32
+// consecutive columns per half wave.  kMlpvAdjU runs the adjoint's two products in one launch:
 // first u = zbar_{l+1} W_{l+1} (NN, reduction over w_{l+2}, with ND2), then
 // z_l (NT, with ND), the LDS tiles reused in between.  Its u is summed in
 // the same order as the NN launch's.
-template <int MODE, int ND, int ND2>
+template <int MODE, int ND, int ND2, int RT>
 __global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
   __shared__ float part[kVW][32][36];  // partial tiles; rows of 36: the stores of a wave spread over the banks
   __shared__ __attribute__((aligned(16))) float bt[(MODE == kMlpvNN || MODE == kMlpvAdjU) ? kVW : 1][16][36];
@@ -151,25 +158,25 @@ __global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
   t.wave = __builtin_amdgcn_readfirstlane(t.tid >> 6);
   t.r = t.lane & 15;
   t.q = t.lane >> 4;
-  t.m0 = blockIdx.x * 32;
+  t.m0 = blockIdx.x * 16 * RT;
   t.n0 = blockIdx.y * 32;
   const int M = a.M, N = a.N;
   const bool adj = MODE == kMlpvAdj || MODE == kMlpvAdjU;
   float u = 0.f;
   if (MODE == kMlpvAdjU) {
-    f4 acc2[2][2];
-    tile_product<true, ND2>(t, a.A2, a.W2, M, N, a.K2, bt[t.wave], nullptr, acc2);
+    f4 acc2[RT][2];
+    tile_product<true, ND2, RT>(t, a.A2, a.W2, M, N, a.K2, bt[t.wave], nullptr, acc2);
     u = tile_sum(t, part, acc2);
     __syncthreads();  // part is written again below
   }
-  f4 acc[2][2];
-  tile_product<MODE == kMlpvNN, ND>(t, a.A, a.W, M, N, a.K, bt[MODE == kMlpvNN ? t.wave : 0], adj ? a.ywin_out : nullptr,
-                                    acc);
+  f4 acc[RT][2];
+  tile_product<MODE == kMlpvNN, ND, RT>(t, a.A, a.W, M, N, a.K, bt[MODE == kMlpvNN ? t.wave : 0],
+                                        adj ? a.ywin_out : nullptr, acc);
   const float sum = tile_sum(t, part, acc);
 
   const int m = t.m0 + (t.tid >> 5), n = t.n0 + (t.tid & 31);
   float lterm = 0.f;
-  if (m < M && n < N) {
+  if (t.tid < 512 * RT && m < M && n < N) {
     const size_t o = (size_t)m * N + n;
     if (MODE == kMlpvNN) {
       a.out[o] = a.add ? a.add[o] + sum : sum;
@@ -340,21 +347,29 @@ hipError_t launch_mlpv_dw(const DwArgs* a, int count, hipStream_t s, hipEvent_t 
   return hipGetLastError();
 }
 
-int mlpv_tiles(int M, int N) { return ((M + 31) / 32) * ((N + 31) / 32); }
+int mlpv_tiles(int M, int N) { return ((M + 15) / 16) * ((N + 31) / 32); }  // the most tiles any launch has
 
 // chunks of 16 per wave in flight: ceil(K / 256), up to 4 (longer reductions loop)
 static int mlpv_nd(int K) { return std::min(4, std::max(1, (K / 16 + kVW - 1) / kVW)); }
 
-template <int MODE, int ND2>
-static hipError_t launch_mlpv_nd(const MlpvArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  const dim3 grid((a.M + 31) / 32, (a.N + 31) / 32), block(64 * kVW);
+// rows per tile: 32, or 16 where 32-row tiles give fewer workgroups than CUs
+static int mlpv_rows(int M, int N) { return ((M + 31) / 32) * ((N + 31) / 32) < 256 ? 16 : 32; }
+
+template <int MODE, int ND2, int RT>
+static hipError_t launch_mlpv_rt(const MlpvArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  const dim3 grid((a.M + 16 * RT - 1) / (16 * RT), (a.N + 31) / 32), block(64 * kVW);
   switch (mlpv_nd(a.K)) {
-    case 1: hipExtLaunchKernelGGL((mlpv_gemm<MODE, 1, ND2>), grid, block, 0, s, e0, e1, 0, a); break;
-    case 2: hipExtLaunchKernelGGL((mlpv_gemm<MODE, 2, ND2>), grid, block, 0, s, e0, e1, 0, a); break;
-    case 3: hipExtLaunchKernelGGL((mlpv_gemm<MODE, 3, ND2>), grid, block, 0, s, e0, e1, 0, a); break;
-    default: hipExtLaunchKernelGGL((mlpv_gemm<MODE, 4, ND2>), grid, block, 0, s, e0, e1, 0, a); break;
+    case 1: hipExtLaunchKernelGGL((mlpv_gemm<MODE, 1, ND2, RT>), grid, block, 0, s, e0, e1, 0, a); break;
+    case 2: hipExtLaunchKernelGGL((mlpv_gemm<MODE, 2, ND2, RT>), grid, block, 0, s, e0, e1, 0, a); break;
+    case 3: hipExtLaunchKernelGGL((mlpv_gemm<MODE, 3, ND2, RT>), grid, block, 0, s, e0, e1, 0, a); break;
+    default: hipExtLaunchKernelGGL((mlpv_gemm<MODE, 4, ND2, RT>), grid, block, 0, s, e0, e1, 0, a); break;
   }
   return hipGetLastError();
+}
+
+template <int MODE, int ND2>
+static hipError_t launch_mlpv_nd(const MlpvArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  return mlpv_rows(a.M, a.N) == 16 ? launch_mlpv_rt<MODE, ND2, 1>(a, s, e0, e1) : launch_mlpv_rt<MODE, ND2, 2>(a, s, e0, e1);
 }
 
 hipError_t launch_mlpv(int mode, const MlpvArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {

@@ -36,8 +36,11 @@ def _case(wl):
                                    dict(batch=50, hidden=64, widths=(64, 16, 48, 32)),
                                    # reductions of 32 to 80 chunks of 16: one to five per wave,
                                    # in one group or two, the last ones padded
-                                   dict(batch=40, hidden=1280, widths=(1280, 512, 1040, 720))],
-                         ids=["pooled", "ragged", "deep"])
+                                   dict(batch=40, hidden=1280, widths=(1280, 512, 1040, 720)),
+                                   # the bench's batch: the 512 -> 1024 layers fill 256 workgroups of
+                                   # 32-row tiles, the others run on 16-row tiles
+                                   dict(batch=256, hidden=1024, widths=(1024, 512, 1024, 256))],
+                         ids=["pooled", "ragged", "deep", "batch256"])
 def test_mlp_of_different_widths(shape):
     # 27 layers: the weight gradients go in groups of 8 layers, the last of 3
     wl = synth.get("mlp_widths_l2000").with_(n_steps=27, **shape)
@@ -46,7 +49,10 @@ def test_mlp_of_different_widths(shape):
     want = run_oracle(wl, *host)
     ref = run_gpu(wl, dev, fast_slots=n + 1, slow_slots=0)          # every state fits: no recomputation
     assert ref["stats"]["forward_evals"] == n
-    assert_close_mlp(ref, want, wl, TOL_F32)
+    # a weight-gradient row sums over the batch: at 256 rows many more of them
+    # meet a pre-activation near zero, so the mask band narrows to 3e-5 rms(z),
+    # still some 30 times what fp32 against float64 moves z by over 1024 terms
+    assert_close_mlp(ref, want, wl, TOL_F32, band=3e-4 if wl.batch <= 64 else 3e-5)
     # weight-gradient groups of 3 and of 1 layer: each layer's gradient is its own launch member
     for win in (3, 1):
         assert_bitwise(run_gpu(wl, dev, fast_slots=n + 1, slow_slots=0, window=win), ref)
