@@ -45,7 +45,7 @@ struct MlpvTile {
   int tid, lane, wave, r, q, m0, n0;
 };
 
-// acc[i][j] = the wave's share of A[m0 + 16 i ..][:] . B[:][n0 + 16 j ..], i < RT, for
+// TileProduct: acc[i][j] = the wave's share of A[m0 + 16 i ..][:] . B[:][n0 + 16 j ..], i < RT, for
 // A [M][K] row-major and B = W^T (NT: W [N][K]) or B = W (NN: W [K][N]).
 // Wave w takes chunks w, w + 16, ... of 16 reduction indices in groups of ND
 // whose loads all issue before the group's first MFMA; past the last chunk
@@ -58,39 +58,43 @@ struct MlpvTile {
 // fragment fall in 64 distinct banks).  With ywin, the first column of
 // workgroups also writes a copy of its A rows there.
 template <bool NN, int ND, int RT>
-__device__ __forceinline__ void tile_product(const MlpvTile& t, const float* __restrict__ A,
-                                             const float* __restrict__ W, int M, int N, int K, float (&bt)[16][36],
-                                             float* ywin, f4 (&acc)[RT][2]) {
-  const int r = t.r, q = t.q, wave = t.wave;
-  const int nch = K / 16;
-  const int ngrp = (nch + kVW * ND - 1) / (kVW * ND);  // groups of ND chunks per wave
+struct TileProduct {
   const float* arow[RT];
-#pragma unroll
-  for (int i = 0; i < RT; ++i) arow[i] = A + (size_t)min(t.m0 + 16 * i + r, M - 1) * K + 4 * q;  // rows >= M: clamped, discarded
   const float* brow[2];
+  const float* wnn;
+  int M, N, K, nch, ngrp, nrow, ncol;
+  __device__ __forceinline__ TileProduct(const MlpvTile& t, const float* __restrict__ A, const float* __restrict__ W,
+                                         int M_, int N_, int K_)
+      : M(M_), N(N_), K(K_) {
+    nch = K / 16;
+    ngrp = (nch + kVW * ND - 1) / (kVW * ND);  // groups of ND chunks per wave
 #pragma unroll
-  for (int j = 0; j < 2; ++j) brow[j] = W + (size_t)min(t.n0 + 16 * j + r, N - 1) * K + 4 * q;  // NT; past N: clamped, discarded
-  const int nrow = t.lane >> 3, ncol = 4 * (t.lane & 7);
-  const float* wnn = W + min(t.n0 + ncol, N - 4);  // NN: a float4 past N: clamped, discarded
+    for (int i = 0; i < RT; ++i) arow[i] = A + (size_t)min(t.m0 + 16 * i + t.r, M - 1) * K + 4 * t.q;  // rows >= M: clamped, discarded
 #pragma unroll
-  for (int i = 0; i < RT; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
-  for (int g = 0; g < ngrp; ++g) {
-    f4 xa[ND][RT], xb[ND][2];
+    for (int j = 0; j < 2; ++j) brow[j] = W + (size_t)min(t.n0 + 16 * j + t.r, N - 1) * K + 4 * t.q;  // NT; past N: clamped, discarded
+    nrow = t.lane >> 3;
+    ncol = 4 * (t.lane & 7);
+    wnn = W + min(t.n0 + ncol, N - 4);  // NN: a float4 past N: clamped, discarded
+  }
+  // the loads of group g of the wave's chunks
+  __device__ __forceinline__ void load(const MlpvTile& t, int g, f4 (&xa)[ND][RT], f4 (&xb)[ND][2]) const {
 #pragma unroll
     for (int u = 0; u < ND; ++u) {
-      const int k0 = 16 * min(wave + kVW * (ND * g + u), nch - 1);
+      const int k0 = 16 * min(t.wave + kVW * (ND * g + u), nch - 1);
 #pragma unroll
       for (int i = 0; i < RT; ++i) xa[u][i] = *(const f4*)(arow[i] + k0);
 #pragma unroll
       for (int j = 0; j < 2; ++j)
         xb[u][j] = NN ? *(const f4*)(wnn + (size_t)(k0 + nrow + 8 * j) * N) : *(const f4*)(brow[j] + k0);
     }
-    __builtin_amdgcn_sched_barrier(0);  // every load of the group issues before its first MFMA
+  }
+  // group g's MFMAs into acc (and the copy of A's rows into ywin)
+  __device__ __forceinline__ void mma(const MlpvTile& t, int g, f4 (&xa)[ND][RT], f4 (&xb)[ND][2],
+                                      float (&bt)[16][36], float* ywin, f4 (&acc)[RT][2]) const {
+    const int r = t.r, q = t.q;
 #pragma unroll
     for (int u = 0; u < ND; ++u) {
-      const int c = wave + kVW * (ND * g + u);
+      const int c = t.wave + kVW * (ND * g + u);
       if (NN) {  // raw rows nrow, nrow + 8 -> fragments of columns n0 + 16 j + r, rows 4 q .. 4 q + 3
 #pragma unroll
         for (int h = 0; h < 2; ++h) *(f4*)&bt[nrow + 8 * h][ncol] = xb[u][h];
@@ -117,7 +121,31 @@ __device__ __forceinline__ void tile_product(const MlpvTile& t, const float* __r
       }
     }
   }
-}
+  // the whole product; with pre, group 0's loads were issued already into xa0, xb0
+  __device__ __forceinline__ void run(const MlpvTile& t, float (&bt)[16][36], float* ywin, f4 (&acc)[RT][2],
+                                      f4 (*xa0)[RT] = nullptr, f4 (*xb0)[2] = nullptr) const {
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int g = 0; g < ngrp; ++g) {
+      f4 xa[ND][RT], xb[ND][2];
+      if (g == 0 && xa0) {
+#pragma unroll
+        for (int u = 0; u < ND; ++u) {
+#pragma unroll
+          for (int i = 0; i < RT; ++i) xa[u][i] = xa0[u][i];
+#pragma unroll
+          for (int j = 0; j < 2; ++j) xb[u][j] = xb0[u][j];
+        }
+      } else {
+        load(t, g, xa, xb);
+      }
+      __builtin_amdgcn_sched_barrier(0);  // every load of the group issues before its first MFMA
+      mma(t, g, xa, xb, bt, ywin, acc);
+    }
+  }
+};
 
 // The 16 waves' partial tiles summed in wave order: thread tid < 512 RT gets
 // element (tid >> 5, tid & 31) of the 16 RT x 32 tile (the others get 0).
@@ -163,15 +191,20 @@ __global__ __launch_bounds__(64 * kVW) void mlpv_gemm(MlpvArgs a) {
   const int M = a.M, N = a.N;
   const bool adj = MODE == kMlpvAdj || MODE == kMlpvAdjU;
   float u = 0.f;
+  const TileProduct<MODE == kMlpvNN, ND, RT> main(t, a.A, a.W, M, N, a.K);
+  f4 acc[RT][2];
   if (MODE == kMlpvAdjU) {
     f4 acc2[RT][2];
-    tile_product<true, ND2, RT>(t, a.A2, a.W2, M, N, a.K2, bt[t.wave], nullptr, acc2);
+    TileProduct<true, ND2, RT>(t, a.A2, a.W2, M, N, a.K2).run(t, bt[t.wave], nullptr, acc2);
+    // the main product's first loads go out before the reduction of u
+    f4 xa0[ND][RT], xb0[ND][2];
+    main.load(t, 0, xa0, xb0);
     u = tile_sum(t, part, acc2);
     __syncthreads();  // part is written again below
+    main.run(t, bt[0], a.ywin_out, acc, xa0, xb0);
+  } else {
+    main.run(t, bt[MODE == kMlpvNN ? t.wave : 0], adj ? a.ywin_out : nullptr, acc);
   }
-  f4 acc[RT][2];
-  tile_product<MODE == kMlpvNN, ND, RT>(t, a.A, a.W, M, N, a.K, bt[MODE == kMlpvNN ? t.wave : 0],
-                                        adj ? a.ywin_out : nullptr, acc);
   const float sum = tile_sum(t, part, acc);
 
   const int m = t.m0 + (t.tid >> 5), n = t.n0 + (t.tid & 31);
