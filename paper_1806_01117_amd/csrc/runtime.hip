@@ -845,7 +845,7 @@ struct Exec {
     }
     if (s != AMBPTT_OK) return s;
     live_dead = true;
-    if (t % w == 0) {  // window [t, min(t + w, n)) complete: accumulate it on the dW stream
+    if (t % w == 0) {  // window [t, min(t + w, n)) complete: its weight gradient, here or on the dW stream
       const int64_t cnt = std::min(w, n - t);
       DwArgs d{};
       d.zbar = zbar_at(t);
@@ -898,7 +898,7 @@ struct Exec {
           },
           ws);
       if (s != AMBPTT_OK) return s;
-      if (own) {  // in line, stream order already keeps the ring half until the window is done
+      if (own) {  // the ring half stays taken until this event (in line, stream order keeps it)
         HIPCK(hipEventRecord(C->ev_dw[hf], ws));
         dw_pending[hf] = true;
       }
