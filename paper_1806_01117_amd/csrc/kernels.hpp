@@ -205,11 +205,15 @@ hipError_t launch_resmlp(int bf16, int mode, const MlpArgs& a, hipStream_t s, hi
                          hipEvent_t e1 = nullptr);
 // Wide-batch bf16 path (B >= 48): the cell kernel takes 64 rows x 64 gate
 // columns per workgroup; the adjoint's products run as launches of their own.
+// The cell's a.W and the NT product's B are fragment-order copies made by
+// launch_pack_nt_bf16 (of W [G H][D + H] and of W_h^T [H][G H]).
 bool cell_wide_fits(int D, int H);  // D and H multiples of 64
 int cell_wide_tiles(int G, int B, int H);
 hipError_t launch_cell_wide(int G, int mode, const StepArgs& a, hipStream_t s, hipEvent_t e0 = nullptr,
                             hipEvent_t e1 = nullptr);
 hipError_t launch_prod_nt(const ProdArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+// dst (N K bf16, fragment order) <- the [N][K] bf16 rows of src with row stride ld
+hipError_t launch_pack_nt_bf16(const void* src, int N, int K, int ld, void* dst, hipStream_t s);
 hipError_t launch_prod_nn(const ProdArgs& a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 int mlp_wide_tiles(int B, int w);
 hipError_t launch_mlp_wide(int mode, const MlpArgs& a, hipStream_t s, hipEvent_t e0 = nullptr,

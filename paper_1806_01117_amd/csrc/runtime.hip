@@ -65,6 +65,7 @@ struct Layout {
   int G = 1, dsize = 4, window = 1;
   size_t h_bytes = 0, c_bytes = 0, state_bytes = 0, stride = 0;
   size_t off_live[2] = {0, 0}, off_wht = 0, off_zbar = 0, off_hwin = 0, off_cbar[2] = {0, 0};
+  size_t off_wpk = 0, off_whpk = 0;  // wide bf16 cell: W and W_h^T in fragment order
   int ld_wht = 0;        // row stride of WhT in elements
   size_t off_loss = 0, off_lossout = 0, total = 0;
   int loss_slots = 0;
@@ -209,6 +210,10 @@ Layout make_layout(const ambptt_problem* p, int window) {
   const bool pad_wht = !L.small && !L.mlp && !L.mlpv && p->dtype == AMBPTT_F32;
   L.ld_wht = int(GH) + (pad_wht ? 32 : 0);
   L.off_wht = o; o += (L.mlp || L.mlpv) ? 0 : align_up((size_t)p->hidden * L.ld_wht * L.dsize);
+  if (L.wide && !L.mlp) {
+    L.off_wpk = o; o += align_up(GH * size_t(p->input + p->hidden) * 2);
+    L.off_whpk = o; o += align_up(size_t(p->hidden) * GH * 2);
+  }
   L.off_zbar = o; o += align_up(2 * (size_t)L.window * p->batch * GH * L.dsize);
   L.off_hwin = o; o += align_up(2 * (size_t)L.window * BH * L.dsize);
   L.off_cbar[0] = o; o += align_up(BH * 4);
@@ -533,6 +538,8 @@ struct Exec {
   const void* W;
   const float* b;
   void* WhT;
+  void* Wpk = nullptr;   // wide bf16 cell: W in fragment order (the gate products)
+  void* WhPk = nullptr;  // ... and W_h^T (the h-adjoint products)
   ambptt_stats st{};
   char* cur = nullptr;
   int cur_slot = -1;  // slot index the live state aliases, or -1
@@ -576,6 +583,10 @@ struct Exec {
       if (lds_prod && lds_cell && C->prod_split) hparts = prod_split_f32_parts(B, H, G * H);
     }
     if (wide || sep32 || L.mlpv) hbuf = (float*)(C->ws + L.off_hbar);
+    if (wide && !L.mlp) {
+      Wpk = C->ws + L.off_wpk;
+      WhPk = C->ws + L.off_whpk;
+    }
   }
   const void* x_at(int64_t t) const { return x + (size_t)t * p.batch * p.input * L.dsize; }
 
@@ -687,7 +698,11 @@ struct Exec {
   }
 
   hipError_t launch(int mode, const StepArgs& a, hipEvent_t e0, hipEvent_t e1) const {
-    if (wide && mode != kFinal) return launch_cell_wide(L.G, mode, a, C->cs, e0, e1);
+    if (wide && mode != kFinal) {
+      StepArgs w = a;
+      w.W = Wpk;
+      return launch_cell_wide(L.G, mode, w, C->cs, e0, e1);
+    }
     if (lds_cell && (mode == kForward || (mode == kAdjoint && (a.first || a.hbar_in))))
       return launch_cell_gemm_f32(L.G, mode, a, C->cs, e0, e1);
     return L.small ? launch_step_small(L.G, p.dtype == AMBPTT_BF16, mode, a, C->cs, e0, e1)
@@ -832,7 +847,7 @@ struct Exec {
       a.hwin_out = hwin_at(t);
       a.loss_acc = (double*)(C->ws + L.off_loss);
       if ((wide || sep32) && !first) {  // hbar_{t+1} = zbar_{t+1} W_h
-        ProdArgs pa{a.zbar_in, WhT, nullptr, hbuf, p.batch, p.hidden, L.G * p.hidden, L.ld_wht};
+        ProdArgs pa{a.zbar_in, wide ? WhPk : WhT, nullptr, hbuf, p.batch, p.hidden, L.G * p.hidden, L.ld_wht};
         s = timed(AMBPTT_K_HADJ, [&](hipEvent_t e0, hipEvent_t e1) {
           if (hparts > 1) return launch_prod_split_f32(pa, hparts, C->cs, e0, e1);
           return wide ? launch_prod_nt(pa, C->cs, e0, e1) : prod32(pa, e0, e1);
@@ -936,7 +951,7 @@ struct Exec {
     a.dh0 = dh0;
     a.dc0 = dc0;
     if (wide || sep32) {  // dL/dh_0 = zbar_0 W_h, dL/dc_0 = cbar_0
-      ProdArgs pa{a.zbar_in, WhT, nullptr, dh0, p.batch, p.hidden, L.G * p.hidden, L.ld_wht};
+      ProdArgs pa{a.zbar_in, wide ? WhPk : WhT, nullptr, dh0, p.batch, p.hidden, L.G * p.hidden, L.ld_wht};
       ambptt_status s = timed(AMBPTT_K_OTHER, [&](hipEvent_t e0, hipEvent_t e1) {
         return wide ? launch_prod_nt(pa, C->cs, e0, e1) : prod32(pa, e0, e1);
       });
@@ -1164,6 +1179,11 @@ ambptt_status prepare_inputs(ambptt_ctx* C, const void* W, const void* h0, const
     // no transposed weights: the residual MLP kernels transpose W tiles in LDS
   } else if (p.dtype == AMBPTT_BF16) {
     HIPCK(launch_transpose_wh_bf16(W, E.WhT, L.G * p.hidden, p.input, p.hidden, C->cs));
+    if (E.Wpk) {  // the wide kernels' fragment-order copies
+      const int GH = L.G * p.hidden, K1 = p.input + p.hidden;
+      HIPCK(launch_pack_nt_bf16(W, GH, K1, K1, E.Wpk, C->cs));
+      HIPCK(launch_pack_nt_bf16(E.WhT, p.hidden, GH, L.ld_wht, E.WhPk, C->cs));
+    }
   } else {
     HIPCK(launch_transpose_wh((const float*)W, (float*)E.WhT, L.G * p.hidden, p.input, p.hidden, L.ld_wht, C->cs));
   }

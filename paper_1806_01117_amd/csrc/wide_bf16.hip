@@ -11,12 +11,16 @@
 //     The adjoint's products hbar = zbar W_h (cell) and zbar W_{l+1} (MLP)
 //     are launches of their own: each reads the whole zbar of its rows, and
 //     fused into the cell kernel's tile they would move twice the bytes.
-//   * Loads use whole 128-byte rows: one load instruction covers 8 rows x 128
-//     bytes (lane l: row l >> 3, bytes 16 (l & 7) ..), which pulls about
-//     twice the bandwidth of the MFMA operand layout (16 rows x 64 bytes per
-//     instruction).  Each wave turns its rows into MFMA fragments through
-//     LDS scratch tiles of its own (swizzled 16 x 128-byte tiles), so no
-//     workgroup barrier sits in the main loop.
+//   * Loads cover whole 128-byte lines.  The activation operand is read as
+//     rows, one load instruction covering 8 rows x 128 bytes (lane l: row
+//     l >> 3, bytes 16 (l & 7) ..), which pulls about twice the bandwidth of
+//     the MFMA operand layout (16 rows x 64 bytes per instruction); each wave
+//     turns its rows into MFMA fragments through LDS scratch tiles of its own
+//     (swizzled 16 x 128-byte tiles), so no workgroup barrier sits in the
+//     main loop.  The recurrent cell's weights, fixed for a pass, are read
+//     from a copy in fragment order (pack_nt below): one load instruction
+//     reads a fragment's 1 KiB contiguously into the lanes that multiply it,
+//     with no trip through LDS.
 // Inside a workgroup the 8 waves split the reduction in 64-wide blocks, so no
 // byte is loaded twice; the loads of the next block(s) are in flight while
 // the current one is multiplied.  The partial products meet in LDS and are
@@ -97,6 +101,27 @@ __device__ __forceinline__ Rows rows_of(const void* p, unsigned bytes, int row0,
   return s;
 }
 
+// An NT operand Bm(k, n) = B[n][k] in fragment order: the fragment of n tile
+// jt (columns 16 jt ..) and 32-wide reduction step ks is 1 KiB, lane l's 16
+// bytes being B[16 jt + (l & 15)][32 ks + 8 (l >> 4) .. +7], the operand
+// layout of v_mfma_f32_16x16x32_bf16; the K / 32 fragments of an n tile are
+// consecutive (n tile major).
+struct Frags {
+  __amdgpu_buffer_rsrc_t r;
+  unsigned voff;  // 16 lane
+  unsigned tile;  // bytes of one n tile: K / 32 fragments
+  __device__ __forceinline__ u4v load(int jt, int ks) const {
+    return bload(r, voff, unsigned(jt) * tile + unsigned(ks) * 1024u);
+  }
+};
+__device__ __forceinline__ Frags frags_of(const void* p, int N, int K) {
+  Frags f;
+  f.r = rsrc(p, unsigned(N) * unsigned(K) * 2u);
+  f.voff = unsigned(threadIdx.x & 63) * 16u;
+  f.tile = unsigned(K / 32) * 1024u;
+  return f;
+}
+
 // Per-lane LDS offsets within one 16 x 128-byte scratch tile.  Row t's
 // 16-byte group k sits at slot k ^ (t & 7): the 8 lanes that write one row hit
 // 8 different slots, and the reads of one fragment column spread over the
@@ -169,8 +194,10 @@ __device__ __forceinline__ void pipeline(int c0, int c1, LD ld, USE use) {
 
 // acc[i][nb] += A_i . B_nb over the wave's blocks [c0, c1); la(g, h, blk) and
 // lb(g, h, blk) load instruction h of 16-row group g of block blk.  The wave's
-// scratch `scr` holds NB + RT tiles.
-template <int RT, int NB, int S, class LA, class LB>
+// scratch `scr` holds NB + RT tiles.  With PB, lb(g, c, blk) loads the
+// fragment of B's group g for the block's 32-wide chunk c (Frags), which the
+// MFMAs take as loaded.
+template <int RT, int NB, int S, bool PB = false, class LA, class LB>
 __device__ __forceinline__ void nt_rows(int c0, int c1, char* scr, const Xpose& X, f4 (&acc)[RT][NB], LA la, LB lb) {
   u4v va[S][RT][2], vb[S][NB][2];
   pipeline<S>(
@@ -186,8 +213,10 @@ __device__ __forceinline__ void nt_rows(int c0, int c1, char* scr, const Xpose& 
           for (int h = 0; h < 2; ++h) vb[s][g][h] = lb(g, h, blk);
       },
       [&](int s) {
+        if constexpr (!PB) {
 #pragma unroll
-        for (int g = 0; g < NB; ++g) X.put(scr + g * kSlot, vb[s][g][0], vb[s][g][1]);
+          for (int g = 0; g < NB; ++g) X.put(scr + g * kSlot, vb[s][g][0], vb[s][g][1]);
+        }
 #pragma unroll
         for (int i = 0; i < RT; ++i) X.put(scr + (NB + i) * kSlot, va[s][i][0], va[s][i][1]);
         __builtin_amdgcn_wave_barrier();
@@ -195,7 +224,7 @@ __device__ __forceinline__ void nt_rows(int c0, int c1, char* scr, const Xpose& 
         for (int c = 0; c < 2; ++c) {
           bf16x8 fb[NB];
 #pragma unroll
-          for (int g = 0; g < NB; ++g) fb[g] = X.get(scr + g * kSlot, c);
+          for (int g = 0; g < NB; ++g) fb[g] = PB ? __builtin_bit_cast(bf16x8, vb[s][g][c]) : X.get(scr + g * kSlot, c);
 #pragma unroll
           for (int i = 0; i < RT; ++i) {
             const bf16x8 fa = X.get(scr + (NB + i) * kSlot, c);
@@ -243,7 +272,8 @@ constexpr int lds_bytes() {
 // Workgroup tile: 64 batch rows x UN hidden units, all G gates (64 gate
 // columns: UN = 16 for the LSTM, 64 for the tanh RNN).  Gate column n =
 // g UN + u is weight row g H + j0 + u; a 16-column group is 16 consecutive
-// weight rows.  Forward: h_{t+1}, c_{t+1}.  Adjoint (gate recomputation of
+// weight rows, one n tile of the fragment-order copy of W (a.W: pack_nt of
+// the [G H][D + H] weights).  Forward: h_{t+1}, c_{t+1}.  Adjoint (gate recomputation of
 // step t): with hbar_{t+1} from the product launch before it (absent for the
 // first turn) it forms zbar_t, cbar_t, the loss term and the copy of h_t for
 // the weight-gradient window.
@@ -273,13 +303,13 @@ __global__ __launch_bounds__(64 * NW) void cell_wide(StepArgs a) {
     const int c0 = (nbk * wave) / NW, c1 = (nbk * (wave + 1)) / NW;
     const Rows xs = rows_of(a.x, unsigned(B * D * 2), m0, 2 * D);
     const Rows hs = rows_of(a.h, unsigned(B * H * 2), m0, 2 * H);
-    const Rows ws = rows_of(a.W, unsigned(GH * K1 * 2), 0, 2 * K1);
-    nt_rows<RT, NB, S>(
+    const Frags wf = frags_of(a.W, GH, K1);
+    nt_rows<RT, NB, S, true>(
         c0, c1, lds + wave * SCR, X, acc,
         [&](int g, int h, int blk) -> u4v {  // an x or an h block: the same choice for the whole wave
           return blk < nbx ? xs.load(g, h, blk) : hs.load(g, h, blk - nbx);
         },
-        [&](int g, int h, int blk) -> u4v { return ws.load_at((16 * g / UN) * H + j0 + (16 * g) % UN, h, blk); });
+        [&](int g, int c, int blk) -> u4v { return wf.load(((16 * g / UN) * H + j0 + (16 * g) % UN) / 16, 2 * blk + c); });
     __syncthreads();  // every wave has left its scratch
     put_partials<RT, NB>(ps, wave, acc);
   }
@@ -363,7 +393,8 @@ __global__ __launch_bounds__(64 * NW) void cell_wide(StepArgs a) {
 //
 // out[m][n] = add[m][n] (if given) + sum_k A[m][k] Bm(k, n), A [M][K] bf16,
 // over a TM x TN tile (TM = 16 RT, TN = 16 NB) per workgroup.
-//   NN = false: Bm(k, n) = B[n][k] (the cell's W_h^T: rows contiguous in k);
+//   NN = false: Bm(k, n) = B[n][k] (the cell's W_h^T), B in fragment order
+//     (pack_nt of the [N][K] rows);
 //   NN = true:  Bm(k, n) = B[k][n] (the MLP's W_{l+1}, contiguous in n; TN =
 //     64): each block's 64 x 64 elements of B go to the wave's scratch as
 //     loaded and are read back by columns, so no transposed copy of the
@@ -394,10 +425,10 @@ __global__ __launch_bounds__(64 * NW) void prod_wide(ProdArgs a) {
   char* scr = lds + wave * SCR;
   const Rows as = rows_of(a.A, unsigned(M * K * 2), m0, 2 * K);
   if constexpr (!NN) {
-    const Rows bs = rows_of(a.B, unsigned(N * K * 2), n0, 2 * K);
-    nt_rows<RT, NB, S>(
+    const Frags bf = frags_of(a.B, N, K);
+    nt_rows<RT, NB, S, true>(
         c0, c1, scr, X, acc, [&](int g, int h, int blk) -> u4v { return as.load(g, h, blk); },
-        [&](int g, int h, int blk) -> u4v { return bs.load(g, h, blk); });
+        [&](int g, int c, int blk) -> u4v { return bf.load(n0 / 16 + g, 2 * blk + c); });
   } else {
     // B block: instruction p covers k rows 8 p + (lane >> 3) of the block, columns n0 + 8 (lane & 7) .. +7
     const int lane = tid & 63, r = lane & 15, q = lane >> 4;
@@ -550,7 +581,30 @@ __global__ __launch_bounds__(64 * NW) void mlp_wide(MlpArgs a) {
 
 unsigned grid_for(int ntile) { return unsigned(8 * ((ntile + 7) / 8)); }
 
+// dst (fragment order, Frags) <- the [N][K] rows of src (row stride ld): one
+// thread per 16-byte lane chunk, written in order.
+__global__ __launch_bounds__(256) void pack_nt(const char* __restrict__ src, int K, int ld, size_t chunks,
+                                               char* __restrict__ dst) {
+  const size_t t = size_t(blockIdx.x) * 256 + threadIdx.x;
+  if (t >= chunks) return;
+  const int l = int(t & 63);
+  const size_t f = t >> 6, kf = size_t(K / 32);
+  const size_t jt = f / kf, ks = f % kf;
+  const size_t row = 16 * jt + size_t(l & 15), col = 32 * ks + 8 * size_t(l >> 4);
+  *(u4v*)(dst + 16 * t) = *(const u4v*)(src + 2 * (row * size_t(ld) + col));
+}
+
 }  // namespace
+
+hipError_t launch_pack_nt_bf16(const void* src, int N, int K, int ld, void* dst, hipStream_t s) {
+  if (N < 16 || N % 16 != 0 || K < 32 || K % 32 != 0 || ld < K || ld % 8 != 0 ||
+      size_t(N) * size_t(K) * 2 > 0xFFFFFFFFull)  // Frags addresses the copy with 32-bit offsets
+    return hipErrorInvalidValue;
+  const size_t chunks = size_t(N) * size_t(K) / 8;
+  hipLaunchKernelGGL(pack_nt, dim3(unsigned((chunks + 255) / 256)), dim3(256), 0, s, (const char*)src, K, ld, chunks,
+                     (char*)dst);
+  return hipGetLastError();
+}
 
 bool cell_wide_fits(int D, int H) { return D % 64 == 0 && H % 64 == 0 && H > 0; }
 
