@@ -56,7 +56,8 @@ def _per_dispatch(rows: list[dict], counter: str) -> list[tuple[str, float]]:
 
 def _scale(disp: list[tuple[str, float]]) -> float:
     """bytes the reference copy moved divided by what the counter read for it:
-    the first copy-named dispatch whose counter is within a factor 4 of 256 MiB"""
+    the first copy-named dispatch whose counter is within a factor 4 of 256 MiB
+    (bench.py makes the reference copy before any other copy)"""
     for name, v in disp:
         if "copy" in name.lower() and COPY_BYTES / 4 <= v <= COPY_BYTES * 4:
             return COPY_BYTES / v
