@@ -207,7 +207,8 @@ hipError_t launch_resmlp(int bf16, int mode, const MlpArgs& a, hipStream_t s, hi
 // columns per workgroup; the adjoint's products run as launches of their own.
 // The cell's a.W and the NT product's B are fragment-order copies made by
 // launch_pack_nt_bf16 (of W [G H][D + H] and of W_h^T [H][G H]).
-bool cell_wide_fits(int D, int H);  // D and H multiples of 64
+bool cell_wide_fits(int G, int B, int D, int H);  // D and H multiples of 64, operands under 4 GiB
+bool mlp_wide_fits(int B, int w);                  // w a multiple of 64, operands under 4 GiB
 int cell_wide_tiles(int G, int B, int H);
 hipError_t launch_cell_wide(int G, int mode, const StepArgs& a, hipStream_t s, hipEvent_t e0 = nullptr,
                             hipEvent_t e1 = nullptr);

@@ -170,7 +170,7 @@ Layout make_layout(const ambptt_problem* p, int window) {
     L.loss_slots = int(grid.x * grid.y);
   }
   if (p->dtype == AMBPTT_BF16 && p->batch >= 48 &&
-      (L.mlp ? p->hidden % 64 == 0 : cell_wide_fits(p->input, p->hidden))) {
+      (L.mlp ? mlp_wide_fits(p->batch, p->hidden) : cell_wide_fits(L.G, p->batch, p->input, p->hidden))) {
     L.wide = true;
     const int tiles = L.mlp ? mlp_wide_tiles(p->batch, p->hidden) : cell_wide_tiles(L.G, p->batch, p->hidden);
     L.loss_slots = std::max(L.loss_slots, 8 * ((tiles + 7) / 8));

@@ -301,8 +301,8 @@ __global__ __launch_bounds__(64 * NW) void cell_wide(StepArgs a) {
     X.init();
     const int nbk = K1 / 64, nbx = D / 64;
     const int c0 = (nbk * wave) / NW, c1 = (nbk * (wave + 1)) / NW;
-    const Rows xs = rows_of(a.x, unsigned(B * D * 2), m0, 2 * D);
-    const Rows hs = rows_of(a.h, unsigned(B * H * 2), m0, 2 * H);
+    const Rows xs = rows_of(a.x, unsigned(size_t(B) * D * 2), m0, 2 * D);  // < 4 GiB: cell_wide_fits
+    const Rows hs = rows_of(a.h, unsigned(size_t(B) * H * 2), m0, 2 * H);
     const Frags wf = frags_of(a.W, GH, K1);
     nt_rows<RT, NB, S, true>(
         c0, c1, lds + wave * SCR, X, acc,
@@ -423,7 +423,7 @@ __global__ __launch_bounds__(64 * NW) void prod_wide(ProdArgs a) {
   Xpose X;
   X.init();
   char* scr = lds + wave * SCR;
-  const Rows as = rows_of(a.A, unsigned(M * K * 2), m0, 2 * K);
+  const Rows as = rows_of(a.A, unsigned(size_t(M) * K * 2), m0, 2 * K);  // < 4 GiB: the fits checks
   if constexpr (!NN) {
     const Frags bf = frags_of(a.B, N, K);
     nt_rows<RT, NB, S, true>(
@@ -432,7 +432,7 @@ __global__ __launch_bounds__(64 * NW) void prod_wide(ProdArgs a) {
   } else {
     // B block: instruction p covers k rows 8 p + (lane >> 3) of the block, columns n0 + 8 (lane & 7) .. +7
     const int lane = tid & 63, r = lane & 15, q = lane >> 4;
-    const Rows bs = rows_of(a.B, unsigned(K * N * 2), 0, 2 * N);
+    const Rows bs = rows_of(a.B, unsigned(size_t(K) * N * 2), 0, 2 * N);
     const unsigned bcol = unsigned(n0) * 2u;
     __bf16* bt = (__bf16*)(scr + RT * kSlot);
     const int lr = lane >> 3, lc = 8 * (lane & 7);
@@ -518,8 +518,8 @@ __global__ __launch_bounds__(64 * NW) void mlp_wide(MlpArgs a) {
     X.init();
     const int nbk = w / 64;
     const int c0 = (nbk * wave) / NW, c1 = (nbk * (wave + 1)) / NW;
-    const Rows ys = rows_of(a.y, unsigned(B * w * 2), m0, 2 * w);
-    const Rows ws = rows_of(a.W, unsigned(w * w * 2), n0, 2 * w);
+    const Rows ys = rows_of(a.y, unsigned(size_t(B) * w * 2), m0, 2 * w);  // < 4 GiB: mlp_wide_fits
+    const Rows ws = rows_of(a.W, unsigned(size_t(w) * w * 2), n0, 2 * w);
     nt_rows<RT, NB, S>(
         c0, c1, lds + wave * SCR, X, acc, [&](int g, int h, int blk) -> u4v { return ys.load(g, h, blk); },
         [&](int g, int h, int blk) -> u4v { return ws.load(g, h, blk); });
@@ -606,12 +606,20 @@ hipError_t launch_pack_nt_bf16(const void* src, int N, int K, int ld, void* dst,
   return hipGetLastError();
 }
 
-bool cell_wide_fits(int D, int H) { return D % 64 == 0 && H % 64 == 0 && H > 0; }
+// Every operand is addressed with 32-bit buffer offsets: each must stay under 4 GiB.
+static bool under_4g(size_t rows, size_t cols) { return rows * cols * 2 <= 0xFFFFFFFFull; }
+
+bool cell_wide_fits(int G, int B, int D, int H) {
+  return D % 64 == 0 && H % 64 == 0 && H > 0 && B > 0 && under_4g(size_t(B), size_t(D) + size_t(H)) &&
+         under_4g(size_t(G) * H, size_t(D) + size_t(H)) && under_4g(size_t(B), size_t(G) * H);
+}
+
+bool mlp_wide_fits(int B, int w) { return w % 64 == 0 && w > 0 && B > 0 && under_4g(size_t(w), size_t(w)) && under_4g(size_t(B), size_t(w)); }
 
 int cell_wide_tiles(int G, int B, int H) { return ((B + 63) / 64) * (H / (64 / G)); }
 
 hipError_t launch_cell_wide(int G, int mode, const StepArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  if ((mode != kForward && mode != kAdjoint) || !cell_wide_fits(a.D, a.H)) return hipErrorInvalidValue;
+  if ((mode != kForward && mode != kAdjoint) || !cell_wide_fits(G, a.B, a.D, a.H)) return hipErrorInvalidValue;
   const dim3 grid(grid_for(cell_wide_tiles(G, a.B, a.H))), block(64 * kWaves);
   if (G == 4) {
     if (mode == kForward) hipExtLaunchKernelGGL((cell_wide<4, kForward>), grid, block, 0, s, e0, e1, 0, a);
@@ -648,7 +656,7 @@ hipError_t launch_prod_nn(const ProdArgs& a, hipStream_t s, hipEvent_t e0, hipEv
 int mlp_wide_tiles(int B, int w) { return ((B + 63) / 64) * (w / 64); }
 
 hipError_t launch_mlp_wide(int mode, const MlpArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  if (a.w % 64 != 0) return hipErrorInvalidValue;
+  if (!mlp_wide_fits(a.B, a.w)) return hipErrorInvalidValue;
   const dim3 grid(grid_for(mlp_wide_tiles(a.B, a.w))), block(64 * kWaves);
   if (mode == kForward) hipExtLaunchKernelGGL((mlp_wide<kForward>), grid, block, 0, s, e0, e1, 0, a);
   else if (mode == kAdjoint) hipExtLaunchKernelGGL((mlp_wide<kAdjoint>), grid, block, 0, s, e0, e1, 0, a);
