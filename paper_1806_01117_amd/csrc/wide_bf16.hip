@@ -389,6 +389,28 @@ __global__ __launch_bounds__(64 * NW) void cell_wide(StepArgs a) {
   }
 }
 
+// The NN product's B block in LDS: row t (one k, 64 columns n) is 128 bytes,
+// its 32-byte segments (16 columns each) permuted by nn_swz(t) so that the
+// 16 rows one transposing read touches (rows kb + 8 g + 0..3, g = 0..3) fall
+// on distinct banks within each half wave.
+__device__ __forceinline__ int nn_swz(int t) { return ((t >> 1) & 1) | (((t >> 3) & 1) << 1); }
+
+// Fragment of the block's 16 x 32 piece (columns 16 nb .., rows kb .. kb + 31):
+// lane l receives rows kb + 8 (l >> 4) .. +7 of column l & 15.  Each
+// ds_read_b64_tr_b16 gives lane j of a 16-lane group rows r .. r + 3 of
+// column j, the group's lane i naming 4 consecutive values (row r + (i >> 2),
+// columns 4 (i & 3) ..) of that 16-column segment.
+__device__ __forceinline__ bf16x8 nn_frag(const char* bt, int kb, int nb) {
+  const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
+  const int r0 = kb + 8 * g + (i >> 2), r1 = r0 + 4;
+  typedef short s4 __attribute__((ext_vector_type(4)));
+  typedef short s8 __attribute__((ext_vector_type(8)));
+  typedef __attribute__((address_space(3))) s4 lds_s4;
+  const s4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(bt + r0 * 128 + 32 * (nb ^ nn_swz(r0)) + 8 * (i & 3)));
+  const s4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(bt + r1 * 128 + 32 * (nb ^ nn_swz(r1)) + 8 * (i & 3)));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
 // ---- products of the adjoint ------------------------------------------------
 //
 // out[m][n] = add[m][n] (if given) + sum_k A[m][k] Bm(k, n), A [M][K] bf16,
@@ -397,13 +419,13 @@ __global__ __launch_bounds__(64 * NW) void cell_wide(StepArgs a) {
 //     (pack_nt of the [N][K] rows);
 //   NN = true:  Bm(k, n) = B[k][n] (the MLP's W_{l+1}, contiguous in n; TN =
 //     64): each block's 64 x 64 elements of B go to the wave's scratch as
-//     loaded and are read back by columns, so no transposed copy of the
-//     weights is kept.
+//     loaded (rows k of 128 bytes) and come back as fragments through
+//     gfx950's transposing LDS read, so no transposed copy of the weights
+//     is kept.
 template <int RT, int NB, bool NN, int NW = kWaves, int S = NN ? 2 : (RT * NB >= 4 ? 3 : 4)>
 __global__ __launch_bounds__(64 * NW) void prod_wide(ProdArgs a) {
   constexpr int TM = 16 * RT, TN = 16 * NB;
-  constexpr int BLD = 66;  // NN: pitch (bf16) of the B block: conflict-free column reads
-  constexpr int SCR = NN ? RT * kSlot + 64 * BLD * 2 : (RT + NB) * kSlot;
+  constexpr int SCR = NN ? RT * kSlot + 64 * 128 : (RT + NB) * kSlot;
   static_assert(!NN || TN == 64, "the NN product takes 64-column tiles");
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int M = a.M, N = a.N, K = a.K;
@@ -430,12 +452,15 @@ __global__ __launch_bounds__(64 * NW) void prod_wide(ProdArgs a) {
         c0, c1, scr, X, acc, [&](int g, int h, int blk) -> u4v { return as.load(g, h, blk); },
         [&](int g, int c, int blk) -> u4v { return bf.load(n0 / 16 + g, 2 * blk + c); });
   } else {
-    // B block: instruction p covers k rows 8 p + (lane >> 3) of the block, columns n0 + 8 (lane & 7) .. +7
-    const int lane = tid & 63, r = lane & 15, q = lane >> 4;
+    // B block: instruction p covers k rows 8 p + (lane >> 3) of the block, columns n0 + 8 (lane & 7) .. +7.
+    // Row t of the block is stored as 128 bytes, its four 32-byte segments (16 columns each) permuted by
+    // nn_swz(t), and a fragment (column l & 15 of a 16-column segment, 8 consecutive k) comes back with two
+    // transposing reads (nn_frag).
+    const int lane = tid & 63;
     const Rows bs = rows_of(a.B, unsigned(size_t(K) * N * 2), 0, 2 * N);
     const unsigned bcol = unsigned(n0) * 2u;
-    __bf16* bt = (__bf16*)(scr + RT * kSlot);
-    const int lr = lane >> 3, lc = 8 * (lane & 7);
+    char* bt = scr + RT * kSlot;
+    const int lr = lane >> 3, lp = lane & 7;  // row within the instruction, 16-byte piece of the row
     u4v va[S][RT][2], vb[S][8];
     pipeline<S>(
         c0, c1,
@@ -452,19 +477,15 @@ __global__ __launch_bounds__(64 * NW) void prod_wide(ProdArgs a) {
           for (int i = 0; i < RT; ++i) X.put(scr + i * kSlot, va[s][i][0], va[s][i][1]);
 #pragma unroll
           for (int p = 0; p < 8; ++p) {
-            // k row 8 p + lr, 8 columns: four 4-byte stores (the pitch keeps rows 4-byte aligned)
-            unsigned* dst = (unsigned*)(bt + (8 * p + lr) * BLD + lc);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) dst[e] = vb[s][p][e];
+            const int t = 8 * p + lr;
+            *(u4v*)(bt + t * 128 + 32 * ((lp >> 1) ^ nn_swz(t)) + 16 * (lp & 1)) = vb[s][p];
           }
           __builtin_amdgcn_wave_barrier();
 #pragma unroll
           for (int c = 0; c < 2; ++c) {
             bf16x8 fb[NB];
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-              for (int e = 0; e < 8; ++e) fb[nb][e] = bt[(32 * c + 8 * q + e) * BLD + nb * 16 + r];  // column n, 8 consecutive k
+            for (int nb = 0; nb < NB; ++nb) fb[nb] = nn_frag(bt, 32 * c, nb);
 #pragma unroll
             for (int i = 0; i < RT; ++i) {
               const bf16x8 fa = X.get(scr + i * kSlot, c);
