@@ -187,7 +187,7 @@ __global__ __launch_bounds__(2 * TM, TM == 128 ? 2 : 1) void dw_bf16(DwArgs a) {
       f4 t = *(const f4*)&T[row * kPT + c4];
       if (vec) {  // c + 3 < N: N is a multiple of 4 (of 8, by the launch check)
         if (a.accumulate) t += *(const f4*)d;
-        *(f4*)d = t;
+        __builtin_nontemporal_store(t, (f4*)d);  // streamed: dW is not read again by this launch
       } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
