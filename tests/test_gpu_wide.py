@@ -56,6 +56,25 @@ def test_wide_lstm_bf16_windows():
     assert_bitwise(a, c)  # host-tier dependencies as stream waits instead of host waits
 
 
+def test_wide_lstm_bf16_long_window_ragged_columns():
+    """Weight-gradient windows longer than 512 rows (the 256 x 192 tiles): B = 64 over
+    20 steps in one window of 1280 rows, N = D + H = 448 columns (two full 192-column
+    tiles and one of 64), against the oracle and, with 4-step windows of 256 rows
+    (the 128 x 128 tiles), within rounding of the same sums."""
+    wl = synth.get("lstm_h2048_bf16_t10000").with_(batch=64, input=128, hidden=320, n_steps=20,
+                                                   name="lstm_bf16_wide_long_window")
+    host, dev = _case(wl)
+    want = run_oracle(wl, *host)
+    a = run_gpu(wl, dev, fast_slots=3, slow_slots=20, interval_min=2, window=20)
+    assert a["stats"]["mode"] == 1 and a["stats"]["window"] == 20 and a["stats"]["kernel_calls"][4] == 1
+    assert_close(a, want, TOL_BF16)
+    b = run_gpu(wl, dev, fast_slots=3, slow_slots=20, interval_min=2, window=4)
+    assert b["stats"]["window"] == 4 and b["stats"]["kernel_calls"][4] == 5
+    assert_close(b, want, TOL_BF16)
+    for k in ("loss", "dh0", "dc0"):  # the windows change only the weight-gradient sums
+        assert (a[k] == b[k]).all() if k != "loss" else a[k] == b[k], k
+
+
 @pytest.mark.parametrize("loss", ["half_sq_last", "mean_sq_all", "mean_last"])
 def test_wide_rnn_bf16_losses(loss):
     """tanh RNN (G = 1, 64 units per tile), B = 50 on a 64-row tile, every loss."""
