@@ -1826,27 +1826,36 @@ ambptt_status ambptt_calibrate(ambptt_ctx* C, const void* x_seq, const void* W, 
       acts.push_back({Op::Store, i % 2, i % 2, i});
       acts.push_back({Op::Advance, i, i + 1, 0});
     }
-    double per[2] = {1e30, 1e30};  // the best of three rounds after a warm-up round
     const int64_t lens[2] = {steps / 3, steps};
-    for (int rep = 0; rep < 4; ++rep) {
-      for (int k = 0; k < 2; ++k) {
-        std::fill(C->pend.begin(), C->pend.end(), kNone);
-        HIPCK(hipStreamSynchronize(C->xs));
-        HIPCK(hipStreamSynchronize(C->cs));
-        HIPCK(hipEventRecord(e0, C->cs));
-        const std::vector<Action> part(acts.begin(), acts.begin() + 3 * lens[k]);
-        if ((s = E.run_acts(part, 0, nullptr, nullptr)) != AMBPTT_OK) return s;
-        HIPCK(hipEventRecord(C->ev_c, C->xs));  // the last store
-        HIPCK(hipStreamWaitEvent(C->cs, C->ev_c, 0));
-        HIPCK(hipEventRecord(e1, C->cs));
-        HIPCK(hipEventSynchronize(e1));
-        HIPCK(hipEventElapsedTime(&ms, e0, e1));
-        if (rep > 0) per[k] = std::min(per[k], 1000.0 * ms);
+    // The host link can be slow for a few milliseconds at a time (seen
+    // right after other processes pinned and released large blocks): an
+    // attempt whose sweep cost exceeds 1.5 times the plain copy is measured
+    // again after a pause, up to three attempts, and the least cost counts.
+    double sweep = 1e30;
+    for (int attempt = 0; attempt < 3 && sweep > 1.5 * tt; ++attempt) {
+      if (attempt) std::this_thread::sleep_for(std::chrono::milliseconds(50));
+      double per[2] = {1e30, 1e30};  // the best of three rounds after a warm-up round
+      for (int rep = 0; rep < 4; ++rep) {
+        for (int k = 0; k < 2; ++k) {
+          std::fill(C->pend.begin(), C->pend.end(), kNone);
+          HIPCK(hipStreamSynchronize(C->xs));
+          HIPCK(hipStreamSynchronize(C->cs));
+          HIPCK(hipEventRecord(e0, C->cs));
+          const std::vector<Action> part(acts.begin(), acts.begin() + 3 * lens[k]);
+          if ((s = E.run_acts(part, 0, nullptr, nullptr)) != AMBPTT_OK) return s;
+          HIPCK(hipEventRecord(C->ev_c, C->xs));  // the last store
+          HIPCK(hipStreamWaitEvent(C->cs, C->ev_c, 0));
+          HIPCK(hipEventRecord(e1, C->cs));
+          HIPCK(hipEventSynchronize(e1));
+          HIPCK(hipEventElapsedTime(&ms, e0, e1));
+          if (rep > 0) per[k] = std::min(per[k], 1000.0 * ms);
+        }
       }
+      sweep = std::min(sweep, (per[1] - per[0]) / double(lens[1] - lens[0]));
     }
     HIPCK(hipStreamSynchronize(C->xs));
     std::fill(C->pend.begin(), C->pend.end(), kNone);
-    tt = std::max(tt, (per[1] - per[0]) / double(lens[1] - lens[0]));
+    tt = std::max(tt, sweep);
   }
   if (C->ftier) {  // the file takes every stored state too: the slower of the two links sets T_T
     HIPCK(hipMemcpy(C->host, E.live(0), C->L.state_bytes, hipMemcpyDeviceToHost));
