@@ -607,6 +607,15 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
             r.set(k, v)
             I_min = v
     r.set("timing_sample", args.timing_sample)
+    # the pinned host tier and the slot events are allocated now, as a context
+    # that runs pass after pass holds them, so that a timed pass without a
+    # warm-up pass before it does not include pinning tens of GB
+    try:
+        r.set("reserve", 1)
+        reserved = True
+    except amb.AmbpttError as e:  # a schedule the library plans only inside the pass
+        print(f"host tier not reserved ahead: {e}", file=sys.stderr, flush=True)
+        reserved = False
     # whole passes only: as many of the requested ones as fit the budget
     est = estimate_pass_s(wl, spec, t_a, I_min)
     steps, warmup = args.steps, args.warmup
@@ -804,7 +813,7 @@ def _measure(args, knobs, wl, spec, host_slots, pinned_cap, dev, dx, dW, db, dh,
                    "mode": ["revolve", "async", "dynamic", "online"][st["mode"]],
                    "interval": st["interval"], "interval_min": I_min, "t_a_us": round(t_a, 3),
                    "t_t_us": round(t_t, 3), "window": st["window"],
-                   "pinned_host_gib": round(host_slots * n_state / 2 ** 30, 2),
+                   "pinned_host_gib": round(host_slots * n_state / 2 ** 30, 2), "host_tier_reserved": reserved,
                    **({"host_slots_capped_by_pinned_gib": args.pinned_gib}
                       if host_slots == pinned_cap and pinned_cap < wl.host_slots and not args.file_tier else {}),
                    **({"knobs": dict(knobs)} if knobs else {}),

@@ -1829,10 +1829,11 @@ ambptt_status ambptt_calibrate(ambptt_ctx* C, const void* x_seq, const void* W, 
     const int64_t lens[2] = {steps / 3, steps};
     // The host link can be slow for a few milliseconds at a time (seen
     // right after other processes pinned and released large blocks): an
-    // attempt whose sweep cost exceeds 1.5 times the plain copy is measured
-    // again after a pause, up to three attempts, and the least cost counts.
+    // attempt whose sweep cost per step exceeds 1.5 times the larger of the
+    // plain copy and the step is measured again after a pause, up to three
+    // attempts, and the least cost counts.
     double sweep = 1e30;
-    for (int attempt = 0; attempt < 3 && sweep > 1.5 * tt; ++attempt) {
+    for (int attempt = 0; attempt < 3 && sweep > 1.5 * std::max(tt, ta); ++attempt) {
       if (attempt) std::this_thread::sleep_for(std::chrono::milliseconds(50));
       double per[2] = {1e30, 1e30};  // the best of three rounds after a warm-up round
       for (int rep = 0; rep < 4; ++rep) {
