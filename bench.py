@@ -497,7 +497,7 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--timing-sample", type=int, default=32)
     ap.add_argument("--path", choices=["auto", "steps", "resident"], default="auto")
-    ap.add_argument("--cooperative", type=int, default=0)
+    ap.add_argument("--cooperative", type=int, default=1, help="resident kernel: 1 cooperative launch (default), 0 plain")
     ap.add_argument("--workload", default=WORKLOAD, help="a synth workload name (default: the 4096-LSTM)")
     ap.add_argument("--n-steps", type=int, default=0, help="override the workload's step count (profiling runs)")
     ap.add_argument("--host-slots", type=int, default=-1, help="host-tier slots (default: the workload's, "

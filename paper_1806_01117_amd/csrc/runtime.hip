@@ -278,7 +278,7 @@ struct ambptt_ctx {
   int res_cap = -1;            // resident workgroups the device holds at once (-1: not queried)
   int64_t res_timeout_ms = 2000;
   bool res_test_stall = false;  // tests of the abort path: the first entry waits for a barrier that never comes
-  bool res_coop = false;         // cooperative launch of the resident kernel
+  bool res_coop = true;          // cooperative launch of the resident kernel (residency guaranteed)
   int dw_stream = -1;            // weight-gradient windows: 1 on their own stream, 0 on the compute stream, -1 by path
   // Executor events order work between the library's streams on one device
   // and time kernels; none of them publishes device memory to the host, so

@@ -59,8 +59,8 @@ def test_late_copies_wide_bf16():
 def test_resident_cooperative_launch():
     wl = synth.get("lstm_h512_t1000").with_(n_steps=64)
     host, dev = _case(wl)
-    plain = run_gpu(wl, dev, fast_slots=3, slow_slots=64, interval_min=2, path=2)
-    coop = run_gpu(wl, dev, fast_slots=3, slow_slots=64, interval_min=2, path=2, opts={"resident_cooperative": 1})
+    plain = run_gpu(wl, dev, fast_slots=3, slow_slots=64, interval_min=2, path=2, opts={"resident_cooperative": 0})
+    coop = run_gpu(wl, dev, fast_slots=3, slow_slots=64, interval_min=2, path=2)  # the default launch
     assert coop["stats"]["mode"] == 1
     assert_bitwise(coop, plain)
     assert_close(coop, run_oracle(wl, *host), TOL_F32)
